@@ -1,0 +1,294 @@
+"""Pins for the CPU oracle (no GPU).
+
+Each test checks the oracle against something other than itself: hand-worked
+values (tests/golden), closed forms, an independent PyTorch restatement of the
+model, brute-force recomputation, or an invariant the paper states.
+"""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+
+import synth
+from oracle import tlf_oracle as O
+from tests import textbook
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _model(cfg, w, **kw):
+    return O.Model(w, cfg.n_heads, cfg.head_dim, rms_eps=cfg.rms_eps, **kw)
+
+
+# ---------------------------------------------------------------------------
+# Router rules (Eq. 2-5)
+# ---------------------------------------------------------------------------
+
+def test_router_golden_cases():
+    cases = json.load(open(os.path.join(GOLDEN, "router_cases.json")))["cases"]
+    for c in cases:
+        z = np.array(c["z"] if "z" in c else np.log(c["pi"]), dtype=np.float64)[None, :]
+        m, margin = O.depth_rule(z, c["rule"], c.get("theta", 0.5), c.get("depth"))
+        assert int(m[0]) == c["m"], c
+        if c["margin"] is None:
+            assert not np.isfinite(margin[0]) or z.shape[1] == 1
+        else:
+            assert margin[0] == pytest.approx(c["margin"], abs=1e-9), c
+
+
+def test_cumprob_half_is_lower_median():
+    """m = max{i : P(depth >= i) > 1/2} equals min{i : P(depth <= i) >= 1/2}."""
+    rng = np.random.default_rng(0)
+    z = rng.normal(size=(5000, 8)) * 2.0
+    m, _ = O.depth_rule(z, O.CUMPROB, 0.5)
+    pi = np.exp(z - z.max(1, keepdims=True))
+    pi /= pi.sum(1, keepdims=True)
+    cdf = np.cumsum(pi, axis=1)
+    med = np.argmax(cdf >= 0.5, axis=1) + 1
+    assert np.array_equal(m, med)
+
+
+def test_cumprob_active_sets_nested_and_threshold_monotone():
+    rng = np.random.default_rng(1)
+    z = rng.normal(size=(2000, 6))
+    prev = None
+    for th in (0.2, 0.35, 0.5, 0.65, 0.8):
+        m, margin = O.depth_rule(z, O.CUMPROB, th)
+        assert m.min() >= 1 and m.max() <= 6
+        assert np.all(margin >= 0)
+        if prev is not None:
+            assert np.all(m <= prev)  # higher threshold never deepens a token
+        prev = m
+
+
+def test_argmax_rule_matches_textbook_argmax_on_model():
+    cfg = synth.tiny_config(max_loops=4, prompt_len=40)
+    w = synth.make_weights(cfg)
+    toks = synth.make_prompts(cfg)[0]
+    M = _model(cfg, w)
+    _, _, m, _ = O.prefill(M, toks)
+    assert np.array_equal(m, textbook.routed_argmax_depths(w, toks))
+
+
+# ---------------------------------------------------------------------------
+# Closed forms of the elementary pieces
+# ---------------------------------------------------------------------------
+
+def test_rms_norm_closed_form():
+    x = np.array([[3.0, 4.0]])
+    y = O.rms_norm(x, 0.0)
+    assert np.allclose(y, [[3.0 / math.sqrt(12.5), 4.0 / math.sqrt(12.5)]])
+    assert np.allclose(O.rms_norm(np.array([[2.0, 2.0, 2.0, 2.0]]), 0.0), 1.0)
+
+
+def test_attention_closed_forms():
+    q = np.array([[[1.0, 0.0]]])                  # [n=1][H=1][D=2]
+    k = np.array([[[0.3, 0.7]]])
+    v = np.array([[[5.0, -2.0]]])
+    # one key: the output is that value
+    assert np.allclose(O.attend(q, k, v, np.ones((1, 1), bool)), v)
+    # two keys with equal scores: the mean of the values
+    k2 = np.array([[[0.0, 1.0]], [[0.0, -1.0]]])
+    v2 = np.array([[[1.0, 2.0]], [[3.0, 6.0]]])
+    assert np.allclose(O.attend(q, k2, v2, np.ones((1, 2), bool)), [[[2.0, 4.0]]])
+    # scores 0 and sqrt(2)*ln 3 / sqrt(2): weights 1/4, 3/4
+    k3 = np.array([[[0.0, 0.0]], [[math.sqrt(2) * math.log(3.0), 0.0]]])
+    assert np.allclose(O.attend(q, k3, v2, np.ones((1, 2), bool)), [[[2.5, 5.0]]])
+    # a masked key gets no weight
+    assert np.allclose(O.attend(q, k3, v2, np.array([[True, False]])), [[[1.0, 2.0]]])
+
+
+def test_silu_closed_form():
+    assert O.silu(np.array([0.0]))[0] == 0.0
+    assert O.silu(np.array([1.0]))[0] == pytest.approx(1.0 / (1.0 + math.exp(-1.0)))
+
+
+# ---------------------------------------------------------------------------
+# Block math against an independent dense PyTorch model
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("loops", [1, 3])
+def test_fixed_depth_equals_tied_weight_gpt(loops):
+    """FIXED(k): the looped model is a pre-norm GPT with k*J weight-tied layers."""
+    cfg = synth.tiny_config(max_loops=4, prompt_len=14)
+    w = synth.make_weights(cfg)
+    toks = synth.make_prompts(cfg)[1]
+    M = _model(cfg, w, route_rule=O.FIXED, fixed_depth=loops)
+    _, logits, m, _ = O.prefill(M, toks, all_logits=True)
+    assert np.all(m == loops)
+    ref = textbook.tied_gpt_logits(w, toks, cfg.n_heads, cfg.head_dim, loops, cfg.rms_eps)
+    assert np.max(np.abs(logits - ref)) < 1e-12
+
+
+def test_fixed_depth_decode_equals_tied_weight_gpt():
+    cfg = synth.tiny_config(max_loops=3, prompt_len=9, steps=5)
+    w = synth.make_weights(cfg)
+    toks = synth.make_prompts(cfg, prompt_len=cfg.prompt_len + cfg.steps)[0]
+    M = _model(cfg, w, route_rule=O.FIXED, fixed_depth=3)
+    st, _, _, _ = O.prefill(M, toks[: cfg.prompt_len])
+    ref = textbook.tied_gpt_logits(w, toks, cfg.n_heads, cfg.head_dim, 3, cfg.rms_eps)
+    for s in range(cfg.steps):
+        t = cfg.prompt_len + s
+        lg, _, _ = O.decode(M, [st], [toks[t]])
+        assert np.max(np.abs(lg[0] - ref[t])) < 1e-12
+
+
+def test_single_loop_model_is_plain_gpt():
+    """R = 1: every token takes exactly one pass of the J-layer block."""
+    cfg = synth.tiny_config(max_loops=1, n_layers=3, prompt_len=10)
+    w = synth.make_weights(cfg)
+    toks = synth.make_prompts(cfg)[0]
+    _, logits, m, _ = O.prefill(_model(cfg, w), toks, all_logits=True)
+    assert np.all(m == 1)
+    ref = textbook.tied_gpt_logits(w, toks, cfg.n_heads, cfg.head_dim, 1, cfg.rms_eps)
+    assert np.max(np.abs(logits - ref)) < 1e-12
+
+
+@pytest.mark.parametrize("seed", [3, 4])
+def test_routed_prefill_equals_dense_masked_model(seed):
+    """Gather-scatter (Eq. 6-7) with compact caches equals the dense formulation
+    where each loop sees every row, masks keys by depth (mu, Eq. 10) and only
+    updates rows whose depth reaches the loop."""
+    cfg = synth.tiny_config(max_loops=4, prompt_len=24)
+    w = synth.make_weights(cfg, seed=seed)
+    toks = synth.make_prompts(cfg, seed=seed)[0]
+    _, logits, m, _ = O.prefill(_model(cfg, w), toks, all_logits=True)
+    assert len(set(m.tolist())) >= 3  # several depths present
+    ref = textbook.routed_dense_logits(w, toks, m, cfg.n_heads, cfg.head_dim, cfg.rms_eps)
+    assert np.max(np.abs(logits - ref)) < 1e-12
+
+
+# ---------------------------------------------------------------------------
+# Recursion-wise cache
+# ---------------------------------------------------------------------------
+
+def _run(cfg, w, mode="compact", use_mask=True, steps=None, model_kw=None, seed=synth.SEED):
+    steps = cfg.steps if steps is None else steps
+    M = _model(cfg, w, **(model_kw or {}))
+    toks = synth.make_prompts(cfg, seed=seed, prompt_len=cfg.prompt_len + steps)
+    states, logits, _, _ = O.prefill_batch(M, toks[:, : cfg.prompt_len], mode=mode,
+                                           capacity=cfg.prompt_len + steps, use_mask=use_mask)
+    outs = [logits]
+    for s in range(steps):
+        lg, _, _ = O.decode(M, states, toks[:, cfg.prompt_len + s])
+        outs.append(lg)
+    return M, states, np.stack(outs, 1), toks
+
+
+def test_literal_masked_cache_equals_compact_cache():
+    cfg = synth.tiny_config(batch=2, prompt_len=10, steps=6)
+    w = synth.make_weights(cfg)
+    _, _, a, _ = _run(cfg, w, "compact")
+    _, _, b, _ = _run(cfg, w, "literal")
+    assert np.max(np.abs(a - b)) < 1e-12
+
+
+def test_dropping_validity_mask_changes_results():
+    """Appendix B: without mu the softmax gives weight to exited tokens' zero slots."""
+    cfg = synth.tiny_config(batch=2, prompt_len=10, steps=4)
+    w = synth.make_weights(cfg)
+    _, _, a, _ = _run(cfg, w, "compact")
+    _, _, b, _ = _run(cfg, w, "literal", use_mask=False)
+    assert np.max(np.abs(a - b)) > 1e-3
+
+
+def test_cached_decode_equals_full_recompute():
+    """Every cached decode step equals the last row of a from-scratch prefill of
+    the extended sequence, and of the independent dense masked model."""
+    cfg = synth.tiny_config(batch=1, prompt_len=8, steps=7, max_loops=4)
+    w = synth.make_weights(cfg, seed=11)
+    M, states, logits, toks = _run(cfg, w, seed=11)
+    for s in range(cfg.steps + 1):
+        T = cfg.prompt_len + s
+        _, lg_full, m_full, _ = O.prefill(M, toks[0, :T])
+        assert np.max(np.abs(logits[0, s] - lg_full)) < 1e-12
+        dense = textbook.routed_dense_logits(w, toks[0, :T], m_full, cfg.n_heads,
+                                             cfg.head_dim, cfg.rms_eps)
+        assert np.max(np.abs(logits[0, s] - dense[-1])) < 1e-12
+
+
+def test_cache_holds_exactly_positions_with_depth_at_least_loop():
+    cfg = synth.tiny_config(batch=3, prompt_len=20, steps=10, max_loops=4)
+    w = synth.make_weights(cfg)
+    M, states, _, _ = _run(cfg, w)
+    for st in states:
+        depths = np.array(st.depths)
+        assert len(depths) == st.length == cfg.prompt_len + cfg.steps
+        idx = O.cache_index(st, M.R)
+        for i in range(M.R):
+            assert np.array_equal(idx[i], np.flatnonzero(depths >= i + 1))
+        n = np.array([len(x) for x in idx])
+        assert n[0] == st.length                      # A_1 holds every token
+        assert np.all(np.diff(n) <= 0)                # nested active sets
+        assert n.sum() == depths.sum()                # each token stored once per loop run
+
+
+def test_batch_composition_does_not_change_a_sequence():
+    cfg = synth.tiny_config(batch=3, prompt_len=9, steps=4)
+    w = synth.make_weights(cfg)
+    _, _, full, toks = _run(cfg, w)
+    M = _model(cfg, w)
+    for b in (2, 0):
+        st, lg, _, _ = O.prefill(M, toks[b, : cfg.prompt_len])
+        outs = [lg]
+        for s in range(cfg.steps):
+            l2, _, _ = O.decode(M, [st], [toks[b, cfg.prompt_len + s]])
+            outs.append(l2[0])
+        assert np.max(np.abs(np.stack(outs) - full[b])) < 1e-12
+
+
+def test_single_token_prompt_and_all_deepest():
+    cfg = synth.tiny_config(batch=1, prompt_len=1, steps=3, max_loops=3)
+    w = synth.make_weights(cfg)
+    # bias that routes everything to the deepest loop
+    w = dict(w, router_b=np.array([0.0, 0.0, 10.0], dtype=np.float32))
+    M, states, logits, toks = _run(cfg, w)
+    assert all(d == 3 for d in states[0].depths)
+    ref = textbook.tied_gpt_logits(w, toks[0], cfg.n_heads, cfg.head_dim, 3, cfg.rms_eps)
+    assert np.max(np.abs(logits[0] - ref[:, :])) < 1e-12
+
+
+def test_cumprob_rule_end_to_end_with_dense_model():
+    cfg = synth.tiny_config(batch=1, prompt_len=16, max_loops=4)
+    w = synth.make_weights(cfg)
+    w = dict(w, router_w=(w["router_w"] * 200.0).astype(np.float32))  # spread the depths
+    M = _model(cfg, w, route_rule=O.CUMPROB, threshold=0.5)
+    toks = synth.make_prompts(cfg)[0]
+    _, logits, m, _ = O.prefill(M, toks, all_logits=True)
+    assert len(set(m.tolist())) >= 2
+    ref = textbook.routed_dense_logits(w, toks, m, cfg.n_heads, cfg.head_dim, cfg.rms_eps)
+    assert np.max(np.abs(logits - ref)) < 1e-12
+
+
+def test_bf16_rounding_mode_stays_close():
+    cfg = synth.tiny_config(batch=1, prompt_len=12, steps=3)
+    w = synth.make_weights(cfg)
+    _, _, a, _ = _run(cfg, w)
+    _, _, b, _ = _run(cfg, w, model_kw=dict(round_bf16=True))
+    err = np.max(np.abs(a - b))
+    assert 0 < err < 3e-2
+
+
+# ---------------------------------------------------------------------------
+# Synthetic inputs
+# ---------------------------------------------------------------------------
+
+def test_splitmix64_reference_vector():
+    """Sequential SplitMix64 from state 1234567 (Vigna's reference output)."""
+    x0 = np.uint64(1234567)
+    with np.errstate(over="ignore"):
+        states = x0 + np.arange(1, 6, dtype=np.uint64) * np.uint64(0x9E3779B97F4A7C15)
+    out = synth._mix64(states.copy())
+    assert [int(v) for v in out[:3]] == [6457827717110365317, 3203168211198807973,
+                                         9817491932198370423]
+
+
+def test_generators_are_prefix_stable_and_normal():
+    a = synth.normal(7, 3, 10000)
+    b = synth.normal(7, 3, 2 * (1 << 22) + 5)[:10000]
+    assert np.array_equal(a, b)
+    assert abs(b.mean()) < 0.05 and abs(b.std() - 1.0) < 0.05
+    assert np.all(synth.round_to_bf16(np.array([1.0 + 2 ** -8], np.float32)) == 1.0)
+    assert np.all(synth.round_to_bf16(np.array([1.0 + 3 * 2 ** -8], np.float32)) == 1.0 + 2 ** -6)
