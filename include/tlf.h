@@ -1,0 +1,205 @@
+/*
+ * tlf.h - C ABI of libtlf: routed prefill and decode of a looped, weight-shared
+ * transformer with token-level depth and a recursion-wise KV cache
+ * (T-LoopFormer, Section 3.2 and Section 3.3), for AMD Instinct MI355X (gfx950).
+ *
+ * Model
+ *   h0 = E[x] + P[pos] (token plus learned absolute position, added once;
+ *   Section 3 and Section 3.2).  A router maps h0 to R logits (Eq. 2) and a
+ *   depth rule turns them into the token's loop count m in [1, R] (Eq. 3-5, or
+ *   argmax, or a fixed depth).  Loop i (1..R) applies the shared block of J
+ *   pre-norm layers (RMSNorm without affine, multi-head attention, SwiGLU FFN,
+ *   residuals inside each layer; Appendix A) to the tokens with m >= i only
+ *   (gather, Eq. 6; scatter, Eq. 7).  Exited tokens keep h^(m).  Logits are
+ *   RMSNorm(h^(m)) times the LM head (tied to E unless a head is given).
+ *
+ * Recursion-wise KV cache (Eq. 8-11)
+ *   Every (sequence b, loop i) owns its own cache, shared by the J layers'
+ *   K/V planes.  A token that executes loop i writes its k, v there (Eq. 11);
+ *   a query at loop i attends only to the entries of that cache (Eq. 10): the
+ *   earlier tokens of the sequence whose depth is >= i, and itself.  Entries
+ *   are stored compactly in position order in 16-token pages, with the
+ *   original position of every entry recorded; tokens that never reached loop
+ *   i occupy no slot, so the validity mask of Eq. 10 is implicit.
+ *
+ * Conventions
+ *   - Every function returns an int status (TLF_OK or a negative TLF_E_*
+ *     code); no C++ exception crosses this boundary.
+ *   - Device pointers ("d_") are HIP device memory on the device that is
+ *     current when tlf_init is called.  Host pointers ("h_") are host memory.
+ *   - Weights and the workspace are borrowed: the caller keeps them alive and
+ *     unchanged until tlf_destroy.  Outputs are caller-allocated.  The context
+ *     owns only host-side state.
+ *   - Work is enqueued asynchronously on the stream given to tlf_init; only
+ *     tlf_cache_stats waits for the stream.  A context is not thread-safe.
+ *   - Arguments are validated on the host before any device work; an argument
+ *     error (TLF_E_INVALID_ARG, TLF_E_STATE) leaves the context unchanged.
+ *   - A HIP error (TLF_E_HIP) poisons the context: later calls return
+ *     TLF_E_STATE.  Errors found on the device (a token id out of range, the
+ *     page pool exhausted) are sticky and are returned by tlf_cache_stats and
+ *     by every call after it.
+ */
+#ifndef TLF_H
+#define TLF_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define TLF_ABI_VERSION 1
+#define TLF_MAX_LOOPS 16
+#define TLF_MAX_LAYERS 8
+#define TLF_MAX_BATCH 4096
+#define TLF_PAGE_TOKENS 16
+
+/* Status codes. */
+#define TLF_OK 0
+#define TLF_E_INVALID_ARG (-1)    /* bad argument or unsupported shape */
+#define TLF_E_NEED_WORKSPACE (-2) /* tlf_init size query: *ws_needed is set */
+#define TLF_E_OUT_OF_PAGES (-3)   /* the KV page pool (max_pages) is exhausted */
+#define TLF_E_STATE (-4)          /* call not valid in this state (e.g. decode before prefill) */
+#define TLF_E_HIP (-5)            /* a HIP runtime call failed; the context is poisoned */
+#define TLF_E_DEVICE (-6)         /* the device found a bad input (token id out of range) */
+
+/* Storage dtype of embeddings, block weights, activations between kernels and
+ * the KV cache.  The residual stream, router, softmax, accumulators and logits
+ * are float32 in both cases. */
+#define TLF_DTYPE_F32 0
+#define TLF_DTYPE_BF16 1
+
+/* Depth rules (Section 3.2). */
+#define TLF_ROUTE_ARGMAX 0  /* m = 1 + index of the largest router logit (lowest on ties) */
+#define TLF_ROUTE_CUMPROB 1 /* m = max{i : sum_{l>=i} softmax(z)_l > threshold} (Eq. 2-5) */
+#define TLF_ROUTE_FIXED 2   /* m = fixed_depth for every token (fixed-depth looped model) */
+
+/* tlf_prefill flags. */
+#define TLF_PREFILL_ALL_LOGITS 1u /* logits for every position ([B][T][V]) instead of the last */
+
+typedef struct tlf_config {
+  int32_t abi_version;   /* must be TLF_ABI_VERSION */
+  int32_t dtype;         /* TLF_DTYPE_F32 or TLF_DTYPE_BF16 */
+  int32_t vocab;         /* V >= 1 */
+  int32_t d_model;       /* d, multiple of 64 */
+  int32_t n_heads;       /* H, n_heads * head_dim == d_model */
+  int32_t head_dim;      /* D: 64 or 128 (16 for float32 models only) */
+  int32_t d_ff;          /* F, SwiGLU hidden width, multiple of 64 */
+  int32_t n_layers;      /* J in [1, TLF_MAX_LAYERS], layers of the shared block */
+  int32_t max_loops;     /* R = M in [1, TLF_MAX_LOOPS], router width and loop cap */
+  int32_t max_pos;       /* rows of the position table; prompt + decode steps <= max_pos */
+  int32_t max_batch;     /* sequences per call, in [1, TLF_MAX_BATCH] */
+  int32_t page_tokens;   /* tokens per KV page, must be TLF_PAGE_TOKENS */
+  int32_t max_pages;     /* KV pages in the pool (all sequences and loops) */
+  int32_t max_prefill_tokens; /* activation rows for prefill; larger prefills run in sequence groups */
+  int32_t route_rule;    /* TLF_ROUTE_* */
+  float route_threshold; /* CUMPROB threshold in (0, 1); the paper uses 0.5 */
+  int32_t fixed_depth;   /* FIXED depth in [1, R] */
+  float rms_eps;         /* RMSNorm epsilon (> 0) */
+} tlf_config;
+
+/* Weights of layer j of the shared block, row-major [out][in] (y = x W^T),
+ * in the storage dtype. */
+typedef struct tlf_layer_weights {
+  const void* w_qkv;     /* [3d][d]: rows q | k | v, each head-major (head h = rows h*D..h*D+D-1) */
+  const void* w_o;       /* [d][d] */
+  const void* w_gate_up; /* [2F][d]: rows gate | up; FFN(y) = W_down (silu(W_gate y) * (W_up y)) */
+  const void* w_down;    /* [d][F] */
+} tlf_layer_weights;
+
+typedef struct tlf_weights {
+  const void* tok_emb;      /* [V][d] storage dtype; also the LM head when lm_head is NULL */
+  const void* pos_emb;      /* [max_pos][d] storage dtype */
+  const float* router_w;    /* [R][d] float32 */
+  const float* router_b;    /* [R] float32 */
+  const void* lm_head;      /* [V][d] storage dtype, or NULL for a head tied to tok_emb */
+  int32_t n_layers;         /* must equal config.n_layers */
+  const tlf_layer_weights* layers; /* host array of n_layers entries (copied by tlf_init) */
+} tlf_weights;
+
+typedef struct tlf_cache_stats_t {
+  int64_t slots_per_loop[TLF_MAX_LOOPS];  /* sum over sequences of cache entries of loop i */
+  int64_t pages_per_loop[TLF_MAX_LOOPS];  /* pages held by loop i's caches */
+  int64_t depth_hist[TLF_MAX_LOOPS];      /* routed depth counts of every token seen (index m-1) */
+  int64_t pages_used;
+  int64_t pages_total;
+  int64_t kv_bytes_resident;              /* pages_used * bytes per page */
+  int64_t batch;                          /* sequences in the current batch */
+  int64_t seq_len;                        /* tokens per sequence so far */
+  /* Algorithmic bytes of the last decode step (exact, from the step's depths):
+   * kv_read counts only valid entries (cache entries plus the step's own);
+   * kv_write the appended k, v; weight bytes count the shared block once per
+   * executed loop plus the LM head and router. */
+  int64_t last_step_kv_read_bytes;
+  int64_t last_step_kv_write_bytes;
+  int64_t last_step_weight_bytes;
+  int64_t last_step_loops_executed;       /* #{i : some token of the step has m >= i} */
+  int64_t last_step_active_rows[TLF_MAX_LOOPS]; /* n_i = #{b : m_b >= i} in the last step */
+  int32_t device_error;                   /* sticky device-side status (TLF_OK if none) */
+  int32_t reserved;
+} tlf_cache_stats_t;
+
+typedef struct tlf_ctx tlf_ctx;
+
+/* Create a context (Section 3.3 inference state).
+ *   cfg, w:       model description; w's device pointers are borrowed.
+ *   d_workspace:  device memory for the KV page pool, page tables, positions,
+ *                 activations and split-K partials; NULL to query the size.
+ *   ws_bytes:     size of d_workspace.
+ *   ws_needed:    out (may be NULL unless d_workspace is NULL): bytes needed.
+ *   hip_stream:   hipStream_t on which all work is enqueued (NULL = default).
+ *   out:          receives the context.
+ * Returns TLF_E_NEED_WORKSPACE (with *ws_needed set) when d_workspace is NULL
+ * or ws_bytes is too small, TLF_E_INVALID_ARG on a bad config or weight set. */
+int tlf_init(const tlf_config* cfg, const tlf_weights* w, void* d_workspace, size_t ws_bytes,
+             size_t* ws_needed, void* hip_stream, tlf_ctx** out);
+
+/* Batched prefill (Section 3.3; gather-scatter of Eq. 6-7 with K/V written at
+ * the gathered original positions, Eq. 11, and causal attention among the
+ * gathered tokens of each loop).  Resets every cache and starts a new batch of
+ * `batch` sequences of `seq_len` tokens each.
+ *   d_tokens: [batch][seq_len] int32 token ids in [0, V).
+ *   d_logits: [batch][V] float32 logits of the last position, or
+ *             [batch][seq_len][V] with TLF_PREFILL_ALL_LOGITS.
+ *   d_depths: [batch][seq_len] int32 routed depths, or NULL.
+ * Requires 1 <= batch <= max_batch, 1 <= seq_len <= max_pos. */
+int tlf_prefill(tlf_ctx* ctx, int32_t batch, int32_t seq_len, const int32_t* d_tokens,
+                float* d_logits, int32_t* d_depths, uint32_t flags);
+
+/* One decode step for every sequence of the current batch (Section 3.3,
+ * Eq. 9-11): token b sits at position seq_len, is routed, runs its m_b loops
+ * (appending k, v to each loop's cache and attending over it) and exits.
+ *   d_tokens: [batch] int32 token ids (the caller picks them, e.g. d_next of
+ *             the previous step for greedy decoding).
+ *   d_logits: [batch][V] float32.
+ *   d_next:   [batch] int32 greedy token (lowest id among maxima), or NULL.
+ *   d_depths: [batch] int32 routed depth, or NULL.
+ *   d_margin: [batch] float32 depth-decision margin (argmax: top1 - top2
+ *             logit; cumprob: min(p^(m) - threshold, threshold - p^(m+1));
+ *             fixed: +inf), or NULL.
+ * Returns TLF_E_STATE before a prefill or once seq_len == max_pos. */
+int tlf_decode_step(tlf_ctx* ctx, const int32_t* d_tokens, float* d_logits, int32_t* d_next,
+                    int32_t* d_depths, float* d_margin);
+
+/* Waits for the stream, then fills *out and, optionally, the logical cache index.
+ *   h_len: [batch][R] int32 host array of cache lengths n_{b,i}, or NULL.
+ *   h_pos: host array receiving, for b = 0..batch-1 and i = 1..R in that order,
+ *          the ascending original positions held by cache (b, i), or NULL.
+ *   pos_cap: capacity of h_pos in int32 elements (TLF_E_INVALID_ARG if short).
+ * Physical page ids are implementation-defined and are not reported.
+ * Returns the sticky device error, if any, after filling *out. */
+int tlf_cache_stats(tlf_ctx* ctx, tlf_cache_stats_t* out, int32_t* h_len, int32_t* h_pos,
+                    size_t pos_cap);
+
+/* Releases the host context (waits for the stream first).  NULL is ignored. */
+void tlf_destroy(tlf_ctx* ctx);
+
+/* Static text for a status code. */
+const char* tlf_status_str(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TLF_H */

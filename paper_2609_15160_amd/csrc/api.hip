@@ -1,0 +1,513 @@
+// Host side of libtlf: argument validation, workspace layout, the inference
+// state machine, and the launch sequences of prefill and decode.
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "../../include/tlf.h"
+#include "kernels.h"
+
+using namespace tlf;
+
+namespace {
+
+size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// Workspace buffers, in carve order.
+enum Buf {
+  B_POOL, B_POS, B_PAGE_TABLE, B_CACHE_LEN, B_SEQ_LEN, B_SCALARS, B_DEPTH_HIST, B_STEP_STATS,
+  B_X_DEC, B_DEPTH_DEC, B_PERM, B_NACT, B_Q_DEC, B_O_DEC, B_ACT_DEC, B_KEYS, B_UNITS,
+  B_UNIT_COUNT, B_CHUNK_TOKENS, B_NCHUNKS, B_PARTIAL, B_COUNTERS,
+  B_X_PRE, B_DEPTH_PRE, B_TOK_IDX, B_Q_PRE, B_O_PRE, B_ACT_PRE,
+  B_COUNT
+};
+
+struct Layout {
+  size_t off[B_COUNT];
+  size_t size[B_COUNT];
+  size_t total = 0;
+  int64_t page_elems = 0;
+  int pages_per_seq = 0, max_chunks = 0, units_cap = 0, pre_rows = 0, s = 0;
+};
+
+bool make_layout(const tlf_config& c, Layout* L) {
+  const int64_t s = c.dtype == TLF_DTYPE_BF16 ? 2 : 4;
+  const int64_t R = c.max_loops, B = c.max_batch, d = c.d_model, F = c.d_ff, H = c.n_heads, D = c.head_dim;
+  L->s = (int)s;
+  L->page_elems = (int64_t)c.n_layers * 2 * H * kPage * D;
+  L->pages_per_seq = (int)ceil_div(c.max_pos, kPage);
+  L->max_chunks = (int)ceil_div(L->pages_per_seq, kMinChunkPages);
+  L->units_cap = (int)(B * L->max_chunks);
+  L->pre_rows = std::max(c.max_prefill_tokens, c.max_pos);
+  const int64_t P = L->pre_rows;
+  int64_t sz[B_COUNT];
+  sz[B_POOL] = (int64_t)c.max_pages * L->page_elems * s;
+  sz[B_POS] = (int64_t)c.max_pages * kPage * 4;
+  sz[B_PAGE_TABLE] = B * R * L->pages_per_seq * 4;
+  sz[B_CACHE_LEN] = B * R * 4;
+  sz[B_SEQ_LEN] = B * 4;
+  sz[B_SCALARS] = 2 * 4;  // page_next, err
+  sz[B_DEPTH_HIST] = R * 8;
+  sz[B_STEP_STATS] = kStatCount * 8;
+  sz[B_X_DEC] = B * d * 4;
+  sz[B_DEPTH_DEC] = B * 4;
+  sz[B_PERM] = B * 4;
+  sz[B_NACT] = R * 4;
+  sz[B_Q_DEC] = B * d * s;
+  sz[B_O_DEC] = B * d * s;
+  sz[B_ACT_DEC] = B * F * s;
+  sz[B_KEYS] = B * 8;
+  sz[B_UNITS] = R * (int64_t)L->units_cap * 4;
+  sz[B_UNIT_COUNT] = R * 4;
+  sz[B_CHUNK_TOKENS] = R * 4;
+  sz[B_NCHUNKS] = R * B * 4;
+  sz[B_PARTIAL] = B * H * L->max_chunks * (D + 2) * 4;
+  sz[B_COUNTERS] = B * H * 4;
+  sz[B_X_PRE] = P * d * 4;
+  sz[B_DEPTH_PRE] = P * 4;
+  sz[B_TOK_IDX] = R * P * 4;
+  sz[B_Q_PRE] = P * d * s;
+  sz[B_O_PRE] = P * d * s;
+  sz[B_ACT_PRE] = P * F * s;
+  size_t off = 0;
+  for (int i = 0; i < B_COUNT; ++i) {
+    if (sz[i] < 0) return false;
+    L->off[i] = off;
+    L->size[i] = (size_t)sz[i];
+    off = align_up(off + (size_t)sz[i], 256);
+  }
+  L->total = off;
+  return true;
+}
+
+int validate_config(const tlf_config* c) {
+  if (!c) return TLF_E_INVALID_ARG;
+  if (c->abi_version != TLF_ABI_VERSION) return TLF_E_INVALID_ARG;
+  if (c->dtype != TLF_DTYPE_F32 && c->dtype != TLF_DTYPE_BF16) return TLF_E_INVALID_ARG;
+  if (c->vocab < 1 || c->d_model < 64 || c->d_model % 64 != 0) return TLF_E_INVALID_ARG;
+  if (c->head_dim != 16 && c->head_dim != 64 && c->head_dim != 128) return TLF_E_INVALID_ARG;
+  if (c->dtype == TLF_DTYPE_BF16 && c->head_dim == 16) return TLF_E_INVALID_ARG;
+  if (c->n_heads < 1 || (int64_t)c->n_heads * c->head_dim != c->d_model) return TLF_E_INVALID_ARG;
+  if (c->d_ff < 64 || c->d_ff % 64 != 0) return TLF_E_INVALID_ARG;
+  if (c->n_layers < 1 || c->n_layers > TLF_MAX_LAYERS) return TLF_E_INVALID_ARG;
+  if (c->max_loops < 1 || c->max_loops > TLF_MAX_LOOPS) return TLF_E_INVALID_ARG;
+  if (c->max_pos < 1 || c->max_batch < 1 || c->max_batch > TLF_MAX_BATCH) return TLF_E_INVALID_ARG;
+  if (c->page_tokens != TLF_PAGE_TOKENS || c->max_pages < 1) return TLF_E_INVALID_ARG;
+  if (c->max_prefill_tokens < 1) return TLF_E_INVALID_ARG;
+  if (c->route_rule == TLF_ROUTE_CUMPROB) {
+    if (!(c->route_threshold > 0.f && c->route_threshold < 1.f)) return TLF_E_INVALID_ARG;
+  } else if (c->route_rule == TLF_ROUTE_FIXED) {
+    if (c->fixed_depth < 1 || c->fixed_depth > c->max_loops) return TLF_E_INVALID_ARG;
+  } else if (c->route_rule != TLF_ROUTE_ARGMAX) {
+    return TLF_E_INVALID_ARG;
+  }
+  if (!(c->rms_eps > 0.f) || !std::isfinite(c->rms_eps)) return TLF_E_INVALID_ARG;
+  // compact row index and chunk index share one int32 in the attention work list
+  if (c->max_batch > 0xFFFF) return TLF_E_INVALID_ARG;
+  // positions, row indices and work-list offsets are int32
+  if ((int64_t)std::max(c->max_prefill_tokens, c->max_pos) * std::max(c->d_ff, 3 * c->d_model) > INT32_MAX)
+    return TLF_E_INVALID_ARG;
+  return TLF_OK;
+}
+
+int validate_weights(const tlf_config* c, const tlf_weights* w) {
+  if (!w || !w->tok_emb || !w->pos_emb || !w->router_w || !w->router_b) return TLF_E_INVALID_ARG;
+  if (w->n_layers != c->n_layers || !w->layers) return TLF_E_INVALID_ARG;
+  for (int j = 0; j < w->n_layers; ++j) {
+    const tlf_layer_weights& l = w->layers[j];
+    if (!l.w_qkv || !l.w_o || !l.w_gate_up || !l.w_down) return TLF_E_INVALID_ARG;
+  }
+  return TLF_OK;
+}
+
+}  // namespace
+
+struct tlf_ctx {
+  tlf_config cfg;
+  tlf_weights w;
+  std::vector<tlf_layer_weights> layers;
+  Layout L;
+  hipStream_t stream = nullptr;
+  char* ws = nullptr;
+  CacheView cv;
+  int batch = 0, seq_len = 0;
+  bool prefilled = false, poisoned = false;
+  int sticky = TLF_OK;
+  int attn_grid = 0;
+
+  template <typename P> P* buf(Buf b) const { return reinterpret_cast<P*>(ws + L.off[b]); }
+};
+
+#define TLF_HIP(expr)                  \
+  do {                                 \
+    hipError_t e_ = (expr);            \
+    if (e_ != hipSuccess) {            \
+      ctx->poisoned = true;            \
+      return TLF_E_HIP;                \
+    }                                  \
+  } while (0)
+
+namespace {
+
+int precheck(tlf_ctx* ctx) {
+  if (!ctx) return TLF_E_INVALID_ARG;
+  if (ctx->poisoned) return TLF_E_STATE;
+  if (ctx->sticky != TLF_OK) return ctx->sticky;
+  return TLF_OK;
+}
+
+const void* head_weights(const tlf_ctx* ctx) { return ctx->w.lm_head ? ctx->w.lm_head : ctx->w.tok_emb; }
+
+template <typename T>
+int run_prefill(tlf_ctx* ctx, int B, int T_, const int32_t* tokens, float* logits, int32_t* depths,
+                uint32_t flags) {
+  const tlf_config& c = ctx->cfg;
+  hipStream_t s = ctx->stream;
+  const int d = c.d_model, F = c.d_ff, R = c.max_loops;
+  TLF_HIP(launch_fill_i32(ctx->cv.page_next, 0, 1, s));
+  TLF_HIP(launch_fill_u64(ctx->cv.depth_hist, 0ull, R, s));
+  const int G = std::max(1, ctx->L.pre_rows / T_);
+  float* x = ctx->buf<float>(B_X_PRE);
+  for (int b0 = 0; b0 < B; b0 += G) {
+    const int Gc = std::min(G, B - b0);
+    const int rows = Gc * T_;
+    EmbedArgs ea;
+    ea.tok_emb = ctx->w.tok_emb; ea.pos_emb = ctx->w.pos_emb; ea.Wr = ctx->w.router_w; ea.br = ctx->w.router_b;
+    ea.tokens = tokens + (int64_t)b0 * T_;
+    ea.rows = rows; ea.V = c.vocab; ea.d = d; ea.R = R; ea.prefill_T = T_;
+    ea.x = x; ea.depth = ctx->buf<int32_t>(B_DEPTH_PRE);
+    ea.out_depth = depths ? depths + (int64_t)b0 * T_ : nullptr;
+    ea.rule = c.route_rule; ea.threshold = c.route_threshold; ea.fixed = c.fixed_depth;
+    ea.err = ctx->cv.err;
+    TLF_HIP(launch_embed_route<T>(ea, s));
+
+    PrefillPlanArgs pa;
+    pa.c = ctx->cv; pa.b0 = b0; pa.G = Gc; pa.T = T_;
+    pa.depth = ctx->buf<int32_t>(B_DEPTH_PRE);
+    pa.tok_idx = ctx->buf<int32_t>(B_TOK_IDX);
+    TLF_HIP(launch_plan_prefill(pa, s));
+
+    for (int i = 0; i < R; ++i) {
+      RowMap rm;
+      rm.src = ctx->buf<int32_t>(B_TOK_IDX) + (int64_t)i * rows;
+      rm.seg_cnt = ctx->cv.cache_len + (int64_t)b0 * R + i;
+      rm.seg = T_; rm.seg_cnt_stride = R; rm.rows = rows;
+      for (int j = 0; j < c.n_layers; ++j) {
+        const tlf_layer_weights& lw = ctx->layers[j];
+        GemmArgs q;
+        q.A = x; q.lda = d; q.W = lw.w_qkv; q.N = 3 * d; q.K = d; q.w_rows = 3 * d; q.rm = rm; q.eps = c.rms_eps;
+        q.out = ctx->buf<void>(B_Q_PRE); q.ldo = d; q.d = d;
+        q.kv.c = ctx->cv; q.kv.loop = i; q.kv.layer = j; q.kv.prefill = 1; q.kv.b0 = b0; q.kv.seg = T_;
+        TLF_HIP(launch_gemm<T>(q, A_NORM, E_QKV, true, s));
+
+        AttnPrefillArgs at;
+        at.c = ctx->cv; at.loop = i; at.layer = j; at.d = d; at.b0 = b0; at.G = Gc; at.T = T_;
+        at.q = ctx->buf<void>(B_Q_PRE); at.o = ctx->buf<void>(B_O_PRE);
+        at.scale_log2 = 1.4426950408889634f / std::sqrt((float)c.head_dim);
+        TLF_HIP(launch_attn_prefill<T>(at, s));
+
+        GemmArgs o;
+        o.A = ctx->buf<void>(B_O_PRE); o.lda = d; o.W = lw.w_o; o.N = d; o.K = d; o.w_rows = d; o.rm = rm;
+        o.out = x; o.ldo = d;
+        TLF_HIP(launch_gemm<T>(o, A_BUF, E_RESID, true, s));
+
+        GemmArgs gu;
+        gu.A = x; gu.lda = d; gu.W = lw.w_gate_up; gu.N = 2 * F; gu.K = d; gu.w_rows = 2 * F; gu.rm = rm;
+        gu.eps = c.rms_eps; gu.out = ctx->buf<void>(B_ACT_PRE); gu.ldo = F; gu.F = F;
+        TLF_HIP(launch_gemm<T>(gu, A_NORM, E_SWIGLU, true, s));
+
+        GemmArgs dn;
+        dn.A = ctx->buf<void>(B_ACT_PRE); dn.lda = F; dn.W = lw.w_down; dn.N = d; dn.K = F; dn.w_rows = d;
+        dn.rm = rm; dn.out = x; dn.ldo = d;
+        TLF_HIP(launch_gemm<T>(dn, A_BUF, E_RESID, true, s));
+      }
+    }
+    GemmArgs hd;
+    hd.A = x; hd.lda = d; hd.W = head_weights(ctx); hd.N = c.vocab; hd.K = d; hd.w_rows = c.vocab;
+    hd.eps = c.rms_eps; hd.out = logits; hd.ldo = c.vocab;
+    if (flags & TLF_PREFILL_ALL_LOGITS) {
+      hd.rm.rows = rows; hd.rm.src_stride = 1; hd.rm.src_off = 0;
+      hd.out_row_off = b0 * T_;
+    } else {
+      hd.rm.rows = Gc; hd.rm.src_stride = T_; hd.rm.src_off = T_ - 1;
+      hd.out_row_off = b0;
+    }
+    TLF_HIP(launch_gemm<T>(hd, A_NORM, E_LOGITS, flags & TLF_PREFILL_ALL_LOGITS, s));
+  }
+  return TLF_OK;
+}
+
+template <typename T>
+int run_decode(tlf_ctx* ctx, const int32_t* tokens, float* logits, int32_t* next, int32_t* depths,
+               float* margin) {
+  const tlf_config& c = ctx->cfg;
+  hipStream_t s = ctx->stream;
+  const int d = c.d_model, F = c.d_ff, R = c.max_loops, B = ctx->batch;
+  float* x = ctx->buf<float>(B_X_DEC);
+  int32_t* perm = ctx->buf<int32_t>(B_PERM);
+  int32_t* nact = ctx->buf<int32_t>(B_NACT);
+
+  EmbedArgs ea;
+  ea.tok_emb = ctx->w.tok_emb; ea.pos_emb = ctx->w.pos_emb; ea.Wr = ctx->w.router_w; ea.br = ctx->w.router_b;
+  ea.tokens = tokens; ea.rows = B; ea.V = c.vocab; ea.d = d; ea.R = R; ea.prefill_T = 0;
+  ea.seq_len = ctx->cv.seq_len; ea.x = x; ea.depth = ctx->buf<int32_t>(B_DEPTH_DEC);
+  ea.out_depth = depths; ea.out_margin = margin;
+  ea.rule = c.route_rule; ea.threshold = c.route_threshold; ea.fixed = c.fixed_depth; ea.err = ctx->cv.err;
+  TLF_HIP(launch_embed_route<T>(ea, s));
+
+  DecodePlanArgs pa;
+  pa.c = ctx->cv; pa.B = B; pa.depth = ctx->buf<int32_t>(B_DEPTH_DEC); pa.perm = perm; pa.nact = nact;
+  pa.units = ctx->buf<int32_t>(B_UNITS); pa.units_cap = ctx->L.units_cap;
+  pa.unit_count = ctx->buf<int32_t>(B_UNIT_COUNT); pa.chunk_tokens = ctx->buf<int32_t>(B_CHUNK_TOKENS);
+  pa.nchunks = ctx->buf<int32_t>(B_NCHUNKS); pa.max_batch = c.max_batch; pa.max_chunks = ctx->L.max_chunks;
+  pa.argmax_keys = ctx->buf<unsigned long long>(B_KEYS);
+  pa.kv_entry_bytes = (int64_t)c.n_layers * 2 * c.d_model * ctx->L.s;
+  TLF_HIP(launch_plan_decode(pa, s));
+
+  for (int i = 0; i < R; ++i) {
+    RowMap rm;
+    rm.src = perm; rm.nact = nact + i; rm.rows = B;
+    RowMap rc = rm;  // compact buffers are indexed by the row itself
+    for (int j = 0; j < c.n_layers; ++j) {
+      const tlf_layer_weights& lw = ctx->layers[j];
+      GemmArgs q;
+      q.A = x; q.lda = d; q.W = lw.w_qkv; q.N = 3 * d; q.K = d; q.w_rows = 3 * d; q.rm = rm; q.eps = c.rms_eps;
+      q.out = ctx->buf<void>(B_Q_DEC); q.ldo = d; q.d = d;
+      q.kv.c = ctx->cv; q.kv.loop = i; q.kv.layer = j; q.kv.prefill = 0;
+      TLF_HIP(launch_gemm<T>(q, A_NORM, E_QKV, false, s));
+
+      AttnDecodeArgs at;
+      at.c = ctx->cv; at.loop = i; at.layer = j; at.d = d; at.perm = perm;
+      at.q = ctx->buf<void>(B_Q_DEC); at.o = ctx->buf<void>(B_O_DEC);
+      at.units = ctx->buf<int32_t>(B_UNITS) + (int64_t)i * ctx->L.units_cap;
+      at.unit_count = ctx->buf<int32_t>(B_UNIT_COUNT) + i;
+      at.chunk_tokens = ctx->buf<int32_t>(B_CHUNK_TOKENS) + i;
+      at.nchunks = ctx->buf<int32_t>(B_NCHUNKS) + (int64_t)i * c.max_batch;
+      at.partial = ctx->buf<float>(B_PARTIAL); at.counters = ctx->buf<int32_t>(B_COUNTERS);
+      at.max_chunks = ctx->L.max_chunks;
+      at.scale_log2 = 1.4426950408889634f / std::sqrt((float)c.head_dim);
+      at.grid = ctx->attn_grid;
+      TLF_HIP(launch_attn_decode<T>(at, s));
+
+      GemmArgs o;
+      o.A = ctx->buf<void>(B_O_DEC); o.lda = d; o.W = lw.w_o; o.N = d; o.K = d; o.w_rows = d; o.rm = rc;
+      o.out = x; o.ldo = d;
+      TLF_HIP(launch_gemm<T>(o, A_BUF, E_RESID, false, s));
+
+      GemmArgs gu;
+      gu.A = x; gu.lda = d; gu.W = lw.w_gate_up; gu.N = 2 * F; gu.K = d; gu.w_rows = 2 * F; gu.rm = rm;
+      gu.eps = c.rms_eps; gu.out = ctx->buf<void>(B_ACT_DEC); gu.ldo = F; gu.F = F;
+      TLF_HIP(launch_gemm<T>(gu, A_NORM, E_SWIGLU, false, s));
+
+      GemmArgs dn;
+      dn.A = ctx->buf<void>(B_ACT_DEC); dn.lda = F; dn.W = lw.w_down; dn.N = d; dn.K = F; dn.w_rows = d;
+      dn.rm = rc; dn.out = x; dn.ldo = d;
+      TLF_HIP(launch_gemm<T>(dn, A_BUF, E_RESID, false, s));
+    }
+  }
+  GemmArgs hd;
+  hd.A = x; hd.lda = d; hd.W = head_weights(ctx); hd.N = c.vocab; hd.K = d; hd.w_rows = c.vocab;
+  hd.rm.rows = B; hd.eps = c.rms_eps; hd.out = logits; hd.ldo = c.vocab;
+  hd.argmax_keys = ctx->buf<unsigned long long>(B_KEYS);
+  TLF_HIP(launch_gemm<T>(hd, A_NORM, E_LOGITS, false, s));
+  if (next) TLF_HIP(launch_argmax_finalize(ctx->buf<unsigned long long>(B_KEYS), next, B, s));
+  return TLF_OK;
+}
+
+int device_status(int err_bits) {
+  if (err_bits & kErrOutOfPages) return TLF_E_OUT_OF_PAGES;
+  if (err_bits & kErrBadToken) return TLF_E_DEVICE;
+  return TLF_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int tlf_init(const tlf_config* cfg, const tlf_weights* w, void* d_workspace, size_t ws_bytes,
+             size_t* ws_needed, void* hip_stream, tlf_ctx** out) {
+  int st = validate_config(cfg);
+  if (st != TLF_OK) return st;
+  Layout L;
+  if (!make_layout(*cfg, &L)) return TLF_E_INVALID_ARG;
+  if (ws_needed) *ws_needed = L.total;
+  if (!d_workspace || ws_bytes < L.total) return TLF_E_NEED_WORKSPACE;
+  if (reinterpret_cast<uintptr_t>(d_workspace) % 256 != 0) return TLF_E_INVALID_ARG;
+  st = validate_weights(cfg, w);
+  if (st != TLF_OK) return st;
+  if (!out) return TLF_E_INVALID_ARG;
+
+  tlf_ctx* ctx = new (std::nothrow) tlf_ctx();
+  if (!ctx) return TLF_E_INVALID_ARG;
+  ctx->cfg = *cfg;
+  ctx->w = *w;
+  ctx->layers.assign(w->layers, w->layers + w->n_layers);
+  ctx->w.layers = ctx->layers.data();
+  ctx->L = L;
+  ctx->stream = reinterpret_cast<hipStream_t>(hip_stream);
+  ctx->ws = reinterpret_cast<char*>(d_workspace);
+
+  CacheView& cv = ctx->cv;
+  cv.pool = ctx->buf<void>(B_POOL);
+  cv.pos = ctx->buf<int32_t>(B_POS);
+  cv.page_table = ctx->buf<int32_t>(B_PAGE_TABLE);
+  cv.cache_len = ctx->buf<int32_t>(B_CACHE_LEN);
+  cv.seq_len = ctx->buf<int32_t>(B_SEQ_LEN);
+  cv.page_next = ctx->buf<int32_t>(B_SCALARS);
+  cv.err = ctx->buf<int32_t>(B_SCALARS) + 1;
+  cv.depth_hist = ctx->buf<unsigned long long>(B_DEPTH_HIST);
+  cv.step_stats = ctx->buf<long long>(B_STEP_STATS);
+  cv.page_elems = L.page_elems;
+  cv.max_pages = cfg->max_pages;
+  cv.pages_per_seq = L.pages_per_seq;
+  cv.R = cfg->max_loops;
+  cv.J = cfg->n_layers;
+  cv.H = cfg->n_heads;
+  cv.D = cfg->head_dim;
+
+  int dev = 0, cus = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess) { delete ctx; return TLF_E_HIP; }
+  ctx->attn_grid = std::max(1, cus) * 8;
+
+  // Free pages are NaN-poisoned: a read of a slot that was never written
+  // turns the logits into NaN instead of silently using stale values.
+  hipStream_t s = ctx->stream;
+  const int64_t pool_words = (int64_t)(L.size[B_POOL] / 4);
+  e = launch_fill_i32(reinterpret_cast<int32_t*>(cv.pool), -1, pool_words, s);
+  if (e == hipSuccess) e = launch_fill_i32(cv.pos, -1, (int64_t)cfg->max_pages * kPage, s);
+  if (e == hipSuccess) e = launch_fill_i32(cv.page_table, -1, (int64_t)(L.size[B_PAGE_TABLE] / 4), s);
+  if (e == hipSuccess) e = launch_fill_i32(cv.cache_len, 0, (int64_t)cfg->max_batch * cfg->max_loops, s);
+  if (e == hipSuccess) e = launch_fill_i32(cv.seq_len, 0, cfg->max_batch, s);
+  if (e == hipSuccess) e = launch_fill_i32(cv.page_next, 0, 2, s);
+  if (e == hipSuccess) e = launch_fill_u64(cv.depth_hist, 0ull, cfg->max_loops, s);
+  if (e == hipSuccess) e = launch_fill_u64(reinterpret_cast<unsigned long long*>(cv.step_stats), 0ull, kStatCount, s);
+  if (e == hipSuccess)
+    e = launch_fill_i32(ctx->buf<int32_t>(B_COUNTERS), 0, (int64_t)cfg->max_batch * cfg->n_heads, s);
+  if (e != hipSuccess) { delete ctx; return TLF_E_HIP; }
+  *out = ctx;
+  return TLF_OK;
+}
+
+int tlf_prefill(tlf_ctx* ctx, int32_t batch, int32_t seq_len, const int32_t* d_tokens, float* d_logits,
+                int32_t* d_depths, uint32_t flags) {
+  int st = precheck(ctx);
+  if (st != TLF_OK) return st;
+  const tlf_config& c = ctx->cfg;
+  if (batch < 1 || batch > c.max_batch || seq_len < 1 || seq_len > c.max_pos) return TLF_E_INVALID_ARG;
+  if (!d_tokens || !d_logits || (flags & ~TLF_PREFILL_ALL_LOGITS)) return TLF_E_INVALID_ARG;
+  // loop 1 alone needs one page per 16 tokens of every sequence
+  if ((int64_t)batch * ceil_div(seq_len, kPage) > c.max_pages) return TLF_E_OUT_OF_PAGES;
+  ctx->prefilled = false;
+  st = c.dtype == TLF_DTYPE_BF16 ? run_prefill<bf16>(ctx, batch, seq_len, d_tokens, d_logits, d_depths, flags)
+                                 : run_prefill<float>(ctx, batch, seq_len, d_tokens, d_logits, d_depths, flags);
+  if (st != TLF_OK) return st;
+  ctx->batch = batch;
+  ctx->seq_len = seq_len;
+  ctx->prefilled = true;
+  return TLF_OK;
+}
+
+int tlf_decode_step(tlf_ctx* ctx, const int32_t* d_tokens, float* d_logits, int32_t* d_next,
+                    int32_t* d_depths, float* d_margin) {
+  int st = precheck(ctx);
+  if (st != TLF_OK) return st;
+  if (!ctx->prefilled || ctx->seq_len >= ctx->cfg.max_pos) return TLF_E_STATE;
+  if (!d_tokens || !d_logits) return TLF_E_INVALID_ARG;
+  st = ctx->cfg.dtype == TLF_DTYPE_BF16 ? run_decode<bf16>(ctx, d_tokens, d_logits, d_next, d_depths, d_margin)
+                                        : run_decode<float>(ctx, d_tokens, d_logits, d_next, d_depths, d_margin);
+  if (st != TLF_OK) return st;
+  ctx->seq_len += 1;
+  return TLF_OK;
+}
+
+int tlf_cache_stats(tlf_ctx* ctx, tlf_cache_stats_t* out, int32_t* h_len, int32_t* h_pos, size_t pos_cap) {
+  if (!ctx || !out) return TLF_E_INVALID_ARG;
+  if (ctx->poisoned) return TLF_E_STATE;
+  const tlf_config& c = ctx->cfg;
+  const int B = ctx->batch, R = c.max_loops;
+  if (h_pos && !ctx->prefilled) return TLF_E_STATE;
+  std::memset(out, 0, sizeof(*out));
+  hipError_t e = hipStreamSynchronize(ctx->stream);
+  if (e != hipSuccess) { ctx->poisoned = true; return TLF_E_HIP; }
+  std::vector<int32_t> len((size_t)std::max(B, 1) * R, 0);
+  int32_t scal[2] = {0, 0};
+  unsigned long long hist[TLF_MAX_LOOPS] = {0};
+  long long stats[kStatCount] = {0};
+  if (B > 0) e = hipMemcpy(len.data(), ctx->cv.cache_len, sizeof(int32_t) * B * R, hipMemcpyDeviceToHost);
+  if (e == hipSuccess) e = hipMemcpy(scal, ctx->cv.page_next, sizeof(scal), hipMemcpyDeviceToHost);
+  if (e == hipSuccess) e = hipMemcpy(hist, ctx->cv.depth_hist, sizeof(unsigned long long) * R, hipMemcpyDeviceToHost);
+  if (e == hipSuccess) e = hipMemcpy(stats, ctx->cv.step_stats, sizeof(stats), hipMemcpyDeviceToHost);
+  if (e != hipSuccess) { ctx->poisoned = true; return TLF_E_HIP; }
+
+  const int64_t page_bytes = ctx->L.page_elems * ctx->L.s;
+  for (int i = 0; i < R; ++i) {
+    for (int b = 0; b < B; ++b) {
+      out->slots_per_loop[i] += len[(size_t)b * R + i];
+      out->pages_per_loop[i] += ceil_div(len[(size_t)b * R + i], kPage);
+    }
+    out->depth_hist[i] = (int64_t)hist[i];
+    out->last_step_active_rows[i] = stats[kStatRows + i];
+  }
+  out->pages_used = std::min<int64_t>(scal[0], c.max_pages);
+  out->pages_total = c.max_pages;
+  out->kv_bytes_resident = out->pages_used * page_bytes;
+  out->batch = B;
+  out->seq_len = ctx->seq_len;
+  out->last_step_kv_read_bytes = stats[kStatKvRead];
+  out->last_step_kv_write_bytes = stats[kStatKvWrite];
+  out->last_step_loops_executed = stats[kStatLoops];
+  const int64_t block_params = 4LL * c.d_model * c.d_model + 3LL * c.d_model * c.d_ff;
+  out->last_step_weight_bytes = stats[kStatLoops] * c.n_layers * block_params * ctx->L.s +
+                                (int64_t)c.vocab * c.d_model * ctx->L.s + (int64_t)R * c.d_model * 4;
+  out->device_error = device_status(scal[1]);
+  if (out->device_error != TLF_OK) ctx->sticky = out->device_error;
+
+  if (h_len && B > 0) std::memcpy(h_len, len.data(), sizeof(int32_t) * B * R);
+  if (h_pos && B > 0) {
+    size_t need = 0;
+    for (size_t k = 0; k < (size_t)B * R; ++k) need += (size_t)len[k];
+    if (pos_cap < need) return TLF_E_INVALID_ARG;
+    const int pps = ctx->L.pages_per_seq;
+    std::vector<int32_t> pt((size_t)B * R * pps);
+    std::vector<int32_t> pos((size_t)c.max_pages * kPage);
+    e = hipMemcpy(pt.data(), ctx->cv.page_table, sizeof(int32_t) * pt.size(), hipMemcpyDeviceToHost);
+    if (e == hipSuccess) e = hipMemcpy(pos.data(), ctx->cv.pos, sizeof(int32_t) * pos.size(), hipMemcpyDeviceToHost);
+    if (e != hipSuccess) { ctx->poisoned = true; return TLF_E_HIP; }
+    size_t o = 0;
+    for (int b = 0; b < B; ++b)
+      for (int i = 0; i < R; ++i) {
+        const int n = len[(size_t)b * R + i];
+        for (int t = 0; t < n; ++t) {
+          const int page = pt[((size_t)b * R + i) * pps + t / kPage];
+          h_pos[o++] = (page >= 0 && page < c.max_pages) ? pos[(size_t)page * kPage + t % kPage] : -1;
+        }
+      }
+  }
+  return out->device_error;
+}
+
+void tlf_destroy(tlf_ctx* ctx) {
+  if (!ctx) return;
+  if (!ctx->poisoned) (void)hipStreamSynchronize(ctx->stream);
+  delete ctx;
+}
+
+const char* tlf_status_str(int status) {
+  switch (status) {
+    case TLF_OK: return "ok";
+    case TLF_E_INVALID_ARG: return "invalid argument";
+    case TLF_E_NEED_WORKSPACE: return "workspace needed";
+    case TLF_E_OUT_OF_PAGES: return "KV page pool exhausted";
+    case TLF_E_STATE: return "invalid state";
+    case TLF_E_HIP: return "HIP runtime error";
+    case TLF_E_DEVICE: return "device-detected input error";
+    default: return "unknown status";
+  }
+}
+
+}  // extern "C"

@@ -1,0 +1,133 @@
+// Internal definitions shared by libtlf's kernels and host code (gfx950 only).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+typedef __bf16 bf16;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+namespace tlf {
+
+constexpr int kPage = 16;          // tokens per KV page
+constexpr int kWave = 64;          // CDNA wavefront width
+constexpr int kMaxLoops = 16;
+constexpr int kPlanThreads = 1024; // single-workgroup planners
+constexpr int kMinChunkPages = 4;  // smallest split-K chunk of the decode attention
+constexpr int kAttnWaveTarget = 4096; // wave-units the decode attention aims to expose per launch
+
+// Sticky device error bits (reported through tlf_cache_stats).
+constexpr int kErrBadToken = 1;
+constexpr int kErrOutOfPages = 2;
+
+// Per-step statistics written by the decode planner (int64 slots).
+enum StepStat {
+  kStatKvRead = 0,
+  kStatKvWrite = 1,
+  kStatLoops = 2,
+  kStatRows = 3,   // kStatRows + i: n_i of the step, i < kMaxLoops
+  kStatCount = kStatRows + kMaxLoops
+};
+
+// Device view of the recursion-wise cache and the bookkeeping around it.
+struct CacheView {
+  void* pool;             // max_pages pages of page_elems storage elements
+  int32_t* pos;           // [max_pages][kPage] original position of every slot (-1 if empty)
+  int32_t* page_table;    // [max_batch][R][pages_per_seq] physical page of (b, i, p)
+  int32_t* cache_len;     // [max_batch][R] entries n_{b,i}
+  int32_t* seq_len;       // [max_batch] tokens of sequence b so far
+  int32_t* page_next;     // [1] bump allocator: pages in use
+  int32_t* err;           // [1] sticky error bits
+  unsigned long long* depth_hist; // [R]
+  long long* step_stats;  // [kStatCount]
+  int64_t page_elems;     // J * 2 * H * kPage * D
+  int max_pages, pages_per_seq, R, J, H, D;
+};
+
+// Element offset of (layer j, k-or-v, head h, slot) inside a page.
+__device__ __forceinline__ int64_t page_off(const CacheView& c, int j, int kv, int h, int slot) {
+  return ((int64_t)((j * 2 + kv) * c.H + h) * kPage + slot) * c.D;
+}
+
+template <typename T> __device__ __forceinline__ float to_f(T v);
+template <> __device__ __forceinline__ float to_f<float>(float v) { return v; }
+template <> __device__ __forceinline__ float to_f<bf16>(bf16 v) { return (float)v; }
+template <typename T> __device__ __forceinline__ T from_f(float v);
+template <> __device__ __forceinline__ float from_f<float>(float v) { return v; }
+template <> __device__ __forceinline__ bf16 from_f<bf16>(float v) { return (bf16)v; }
+
+// 16-byte vector of storage elements.
+template <typename T> struct V16 {
+  static constexpr int N = 16 / sizeof(T);
+  union { uint4 u; T e[16 / sizeof(T)]; };
+};
+
+template <typename T> __device__ __forceinline__ V16<T> ld16(const T* p) {
+  V16<T> v;
+  v.u = *reinterpret_cast<const uint4*>(p);
+  return v;
+}
+template <typename T> __device__ __forceinline__ void st16(T* p, const V16<T>& v) {
+  *reinterpret_cast<uint4*>(p) = v.u;
+}
+
+// MFMA traits: one 16x16 output tile per instruction; KS = k per instruction,
+// EPL = consecutive k elements held by each lane (lane l holds row/col l%16,
+// k = (l/16)*EPL .. +EPL-1 of the step).  Output: lane l holds rows
+// 4*(l/16)+r (r = 0..3) of column l%16.
+template <typename T> struct Mfma;
+template <> struct Mfma<bf16> {
+  static constexpr int KS = 32;
+  static constexpr int EPL = 8;
+  typedef bf16x8 frag;
+  static __device__ __forceinline__ frag load(const bf16* p) {
+    return *reinterpret_cast<const bf16x8*>(p);
+  }
+  static __device__ __forceinline__ f32x4 mma(frag a, frag b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+  }
+};
+template <> struct Mfma<float> {
+  static constexpr int KS = 4;
+  static constexpr int EPL = 1;
+  typedef float frag;
+  static __device__ __forceinline__ frag load(const float* p) { return *p; }
+  static __device__ __forceinline__ f32x4 mma(frag a, frag b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+  }
+};
+
+__device__ __forceinline__ int lane_id() { return threadIdx.x & (kWave - 1); }
+
+template <typename V> __device__ __forceinline__ V shfl_xor(V v, int m) { return __shfl_xor(v, m, kWave); }
+
+__device__ __forceinline__ void set_err(int32_t* err, int bits) { atomicOr(err, bits); }
+
+// Block-wide exclusive prefix sum over blockDim.x (multiple of 64, <= 1024)
+// threads.  `tmp` needs blockDim.x / 64 + 1 ints of shared memory.  Returns
+// this thread's exclusive prefix; *total receives the block total.  All
+// threads must call it.
+__device__ __forceinline__ int block_exclusive_scan(int v, int* tmp, int* total) {
+  const int lane = lane_id(), wid = threadIdx.x / kWave, nw = blockDim.x / kWave;
+  int x = v;
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    int y = __shfl_up(x, o, kWave);
+    if (lane >= o) x += y;
+  }
+  if (lane == kWave - 1) tmp[wid] = x;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int s = 0;
+    for (int w = 0; w < nw; ++w) { int t = tmp[w]; tmp[w] = s; s += t; }
+    tmp[nw] = s;
+  }
+  __syncthreads();
+  int r = tmp[wid] + x - v;
+  *total = tmp[nw];
+  __syncthreads();
+  return r;
+}
+
+}  // namespace tlf

@@ -1,0 +1,163 @@
+// Launch interface between libtlf's host orchestrator and its HIP kernels.
+#pragma once
+
+#include "common.h"
+
+namespace tlf {
+
+// ---------------------------------------------------------------------------
+// Row maps: which GEMM rows are active and where their residual row lives.
+//   decode : row k < n_i is the k-th deepest token of the step, residual row
+//            perm[k]; rows >= n_i have exited (Section 3.3 early exit).
+//   prefill: rows are G segments of T compact slots; slot a of segment g is
+//            active while a < n_{g,i}, and its residual row is tok_idx[r]
+//            (the gathered original position, Eq. 6).
+//   plain  : rows [0, rows) active, residual row r * src_stride + src_off.
+// ---------------------------------------------------------------------------
+struct RowMap {
+  const int32_t* src = nullptr;   // residual row of row r (nullptr: strided)
+  int src_stride = 1, src_off = 0;
+  const int32_t* nact = nullptr;  // decode: rows [0, *nact) are active
+  const int32_t* seg_cnt = nullptr; // prefill: segment s has seg_cnt[s * seg_cnt_stride] active slots
+  int seg = 0, seg_cnt_stride = 0;
+  int rows = 0;                   // rows covered by the grid
+};
+
+__device__ __forceinline__ bool row_active(const RowMap& m, int r) {
+  if (r >= m.rows) return false;
+  if (m.nact) return r < *m.nact;
+  if (m.seg_cnt) return (r % m.seg) < m.seg_cnt[(r / m.seg) * m.seg_cnt_stride];
+  return true;
+}
+__device__ __forceinline__ int row_src(const RowMap& m, int r) {
+  return m.src ? m.src[r] : r * m.src_stride + m.src_off;
+}
+
+// Where the QKV epilogue appends k and v (Eq. 11).
+struct KvDst {
+  CacheView c;
+  int loop = 0, layer = 0;
+  int prefill = 0;  // 0: decode, slot = cache_len[b][i] - 1 with b = residual row;
+                    // 1: prefill, b = b0 + r / seg, slot = r % seg
+  int b0 = 0, seg = 0;
+};
+
+enum AKind { A_NORM = 0, A_BUF = 1 };
+enum EKind { E_QKV = 0, E_RESID = 1, E_SWIGLU = 2, E_LOGITS = 3 };
+
+struct GemmArgs {
+  const void* A = nullptr;  // A_NORM: float residual rows (row = residual index); A_BUF: storage rows (row = r)
+  int lda = 0;
+  const void* W = nullptr;  // [W rows][K] storage dtype
+  int N = 0;                // output columns (E_SWIGLU: 2F in the interleaved gate/up space)
+  int K = 0;
+  int w_rows = 0;           // rows of W (loads are clamped below it)
+  RowMap rm;
+  float eps = 1e-5f;
+  void* out = nullptr;      // E_QKV: q rows; E_RESID: float residual; E_SWIGLU: act rows; E_LOGITS: float logits
+  int ldo = 0;
+  int out_row_off = 0;      // E_LOGITS: output row = out_row_off + r
+  unsigned long long* argmax_keys = nullptr;  // E_LOGITS, may be nullptr
+  KvDst kv;                 // E_QKV
+  int d = 0;                // E_QKV: width of each of q, k, v
+  int F = 0;                // E_SWIGLU: hidden width
+};
+
+template <typename T>
+hipError_t launch_gemm(const GemmArgs& a, AKind ak, EKind ek, bool big_tiles, hipStream_t s);
+
+// ---------------------------------------------------------------------------
+// Embedding + router (Section 3.2): h0 = E[x] + P[pos], z = W_r h0 + b_r,
+// depth rule, margin.
+// ---------------------------------------------------------------------------
+struct EmbedArgs {
+  const void* tok_emb = nullptr;
+  const void* pos_emb = nullptr;
+  const float* Wr = nullptr;
+  const float* br = nullptr;
+  const int32_t* tokens = nullptr;
+  int rows = 0, V = 0, d = 0, R = 0;
+  int prefill_T = 0;              // > 0: pos = row % T; 0: pos = seq_len[row]
+  const int32_t* seq_len = nullptr;
+  float* x = nullptr;             // [rows][d]
+  int32_t* depth = nullptr;       // [rows]
+  int32_t* out_depth = nullptr;   // optional [rows]
+  float* out_margin = nullptr;    // optional [rows]
+  int rule = 0, fixed = 1;
+  float threshold = 0.5f;
+  int32_t* err = nullptr;
+};
+template <typename T> hipError_t launch_embed_route(const EmbedArgs& a, hipStream_t s);
+
+// ---------------------------------------------------------------------------
+// Decode planner (one workgroup): depth-sorted row order, active counts n_i,
+// page allocation and slot bookkeeping for every executed (b, i), statistics,
+// and the split-K work list of the decode attention.
+// ---------------------------------------------------------------------------
+struct DecodePlanArgs {
+  CacheView c;
+  int B = 0;
+  const int32_t* depth = nullptr;
+  int32_t* perm = nullptr;         // [B]
+  int32_t* nact = nullptr;         // [R]
+  int32_t* units = nullptr;        // [R][units_cap] (row k | chunk << 16)
+  int units_cap = 0;
+  int32_t* unit_count = nullptr;   // [R]
+  int32_t* chunk_tokens = nullptr; // [R]
+  int32_t* nchunks = nullptr;      // [R][max_batch]
+  int max_batch = 0, max_chunks = 0;
+  unsigned long long* argmax_keys = nullptr; // [B] cleared for the LM head
+  int64_t kv_entry_bytes = 0;      // bytes of one (token, loop) cache entry over all layers
+};
+hipError_t launch_plan_decode(const DecodePlanArgs& a, hipStream_t s);
+
+// Prefill planner (one workgroup per sequence of the group): per loop i the
+// gathered positions rho^(i) (Eq. 6), n_{b,i}, pages and their positions.
+struct PrefillPlanArgs {
+  CacheView c;
+  int b0 = 0, G = 0, T = 0;
+  const int32_t* depth = nullptr;  // [G][T]
+  int32_t* tok_idx = nullptr;      // [R][G*T]
+};
+hipError_t launch_plan_prefill(const PrefillPlanArgs& a, hipStream_t s);
+
+// ---------------------------------------------------------------------------
+// Attention over the recursion-wise cache (Eq. 10).
+// ---------------------------------------------------------------------------
+struct AttnDecodeArgs {
+  CacheView c;
+  int loop = 0, layer = 0, d = 0;
+  const int32_t* perm = nullptr;
+  const void* q = nullptr;         // [rows][d] compact rows
+  void* o = nullptr;               // [rows][d]
+  const int32_t* units = nullptr;  // this loop's work list
+  const int32_t* unit_count = nullptr;
+  const int32_t* chunk_tokens = nullptr;
+  const int32_t* nchunks = nullptr; // this loop's per-row chunk counts
+  float* partial = nullptr;        // [max_batch][H][max_chunks][D + 2]
+  int32_t* counters = nullptr;     // [max_batch][H], zero between launches
+  int max_chunks = 0;
+  float scale_log2 = 0.f;          // log2(e) / sqrt(D)
+  int grid = 0;
+};
+template <typename T> hipError_t launch_attn_decode(const AttnDecodeArgs& a, hipStream_t s);
+
+struct AttnPrefillArgs {
+  CacheView c;
+  int loop = 0, layer = 0, d = 0;
+  int b0 = 0, G = 0, T = 0;
+  const void* q = nullptr;  // [G*T][d], row g*T + a
+  void* o = nullptr;        // [G*T][d]
+  float scale_log2 = 0.f;
+};
+template <typename T> hipError_t launch_attn_prefill(const AttnPrefillArgs& a, hipStream_t s);
+
+// ---------------------------------------------------------------------------
+// Small utility kernels (no hipMemset inside the step, so a step can be
+// captured in a graph).
+// ---------------------------------------------------------------------------
+hipError_t launch_fill_i32(int32_t* p, int32_t v, int64_t n, hipStream_t s);
+hipError_t launch_fill_u64(unsigned long long* p, unsigned long long v, int64_t n, hipStream_t s);
+hipError_t launch_argmax_finalize(const unsigned long long* keys, int32_t* next, int B, hipStream_t s);
+
+}  // namespace tlf

@@ -1,0 +1,346 @@
+// Embedding + router, the decode and prefill planners, and utility kernels.
+#include "kernels.h"
+
+namespace tlf {
+
+namespace {
+
+// ---------------------------------------------------------------------------
+// h0 = E[x] + P[pos] (learned absolute position added once, Section 3.2),
+// z = W_r h0 + b_r (Eq. 2's router as a linear map), then the depth rule.
+// One wave per row; the residual row is written in float32.
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(256) void k_embed_route(EmbedArgs a) {
+  const int lane = lane_id();
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= a.rows) return;
+  int tok = a.tokens[row];
+  if (tok < 0 || tok >= a.V) {
+    if (lane == 0) set_err(a.err, kErrBadToken);
+    tok = 0;
+  }
+  const int pos = a.prefill_T > 0 ? row % a.prefill_T : a.seq_len[row];
+  const T* e = reinterpret_cast<const T*>(a.tok_emb) + (int64_t)tok * a.d;
+  const T* p = reinterpret_cast<const T*>(a.pos_emb) + (int64_t)pos * a.d;
+  float* x = a.x + (int64_t)row * a.d;
+  float z[kMaxLoops];
+#pragma unroll
+  for (int i = 0; i < kMaxLoops; ++i) z[i] = 0.f;
+  for (int k = lane; k < a.d; k += kWave) {
+    const float h = to_f<T>(e[k]) + to_f<T>(p[k]);
+    x[k] = h;
+#pragma unroll
+    for (int i = 0; i < kMaxLoops; ++i)
+      if (i < a.R) z[i] += a.Wr[(int64_t)i * a.d + k] * h;
+  }
+#pragma unroll
+  for (int i = 0; i < kMaxLoops; ++i) {
+    if (i < a.R) {
+      float v = z[i];
+#pragma unroll
+      for (int o = 1; o < kWave; o <<= 1) v += shfl_xor(v, o);
+      z[i] = v + a.br[i];
+    }
+  }
+  if (lane != 0) return;
+  const int R = a.R;
+  int m = 1;
+  float margin = __builtin_inff();
+  if (a.rule == 0) {  // argmax, lowest index on ties
+    int best = 0;
+    for (int i = 1; i < R; ++i)
+      if (z[i] > z[best]) best = i;
+    float second = -__builtin_inff();
+    for (int i = 0; i < R; ++i)
+      if (i != best && z[i] > second) second = z[i];
+    m = best + 1;
+    if (R > 1) margin = z[best] - second;
+  } else if (a.rule == 1) {  // cumulative probability (Eq. 2-5)
+    float mx = z[0];
+    for (int i = 1; i < R; ++i) mx = fmaxf(mx, z[i]);
+    float ex[kMaxLoops];
+    float tot = 0.f;
+    for (int i = 0; i < R; ++i) { ex[i] = __expf(z[i] - mx); tot += ex[i]; }
+    float p_sfx[kMaxLoops + 1];
+    p_sfx[R] = 0.f;
+    float run = 0.f;
+    for (int i = R - 1; i >= 0; --i) { run += ex[i]; p_sfx[i] = run / tot; }
+    p_sfx[0] = 1.f;  // p^(1) = 1: every token runs loop 1
+    m = 1;
+    for (int i = 1; i < R; ++i)
+      if (p_sfx[i] > a.threshold) m = i + 1;
+    margin = fminf(p_sfx[m - 1] - a.threshold, a.threshold - p_sfx[m]);
+  } else {
+    m = a.fixed;
+  }
+  a.depth[row] = m;
+  if (a.out_depth) a.out_depth[row] = m;
+  if (a.out_margin) a.out_margin[row] = margin;
+}
+
+// ---------------------------------------------------------------------------
+// Decode planner: one workgroup of kPlanThreads threads.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kPlanThreads) void k_plan_decode(DecodePlanArgs a) {
+  const CacheView& c = a.c;
+  const int tid = threadIdx.x, B = a.B, R = c.R;
+  __shared__ int cnt[kMaxLoops + 1];
+  __shared__ int start[kMaxLoops + 1];
+  __shared__ int fill[kMaxLoops + 1];
+  __shared__ int scan_tmp[kPlanThreads / kWave + 1];
+  __shared__ int s_carry, s_total, s_oom, s_chunk;
+  __shared__ unsigned long long hist[kMaxLoops];
+  __shared__ unsigned long long s_kvread, s_kvwrite, s_pages_i;
+  __shared__ int s_maxm;
+
+  if (tid <= kMaxLoops) { cnt[tid] = 0; fill[tid] = 0; }
+  if (tid < kMaxLoops) hist[tid] = 0ull;
+  if (tid == 0) { s_kvread = 0ull; s_kvwrite = 0ull; s_maxm = 0; s_oom = 0; }
+  __syncthreads();
+  for (int b = tid; b < B; b += kPlanThreads) atomicAdd(&cnt[a.depth[b]], 1);
+  __syncthreads();
+  if (tid == 0) {
+    int s = 0;
+    for (int m = R; m >= 1; --m) { start[m] = s; s += cnt[m]; }
+    for (int i = 1; i <= R; ++i) a.nact[i - 1] = start[i] + cnt[i];  // n_i = #{m >= i}
+  }
+  __syncthreads();
+
+  // 1. depth-sorted order (deepest first, stable in b): A_i = rows [0, n_i)
+  for (int b0 = 0; b0 < B; b0 += kPlanThreads) {
+    const int b = b0 + tid;
+    const int m = b < B ? a.depth[b] : 0;
+    for (int dv = R; dv >= 1; --dv) {
+      int tot;
+      const int ex = block_exclusive_scan(m == dv ? 1 : 0, scan_tmp, &tot);
+      if (m == dv) a.perm[start[dv] + fill[dv] + ex] = b;
+      __syncthreads();
+      if (tid == 0) fill[dv] += tot;
+      __syncthreads();
+    }
+  }
+
+  // 2. page allocation: (b, i) needs a new page when its next slot starts one
+  if (tid == 0) s_carry = 0;
+  __syncthreads();
+  for (int b0 = 0; b0 < B; b0 += kPlanThreads) {
+    const int b = b0 + tid;
+    int need = 0;
+    if (b < B) {
+      const int m = a.depth[b];
+      for (int i = 0; i < m; ++i) need += (c.cache_len[b * R + i] % kPage) == 0;
+    }
+    int tot;
+    block_exclusive_scan(need, scan_tmp, &tot);
+    if (tid == 0) s_carry += tot;
+    __syncthreads();
+  }
+  if (tid == 0) {
+    s_total = s_carry;
+    const int base = *c.page_next;
+    if ((int64_t)base + s_total > c.max_pages) {
+      s_oom = 1;
+      set_err(c.err, kErrOutOfPages);
+    }
+    s_carry = base;
+  }
+  __syncthreads();
+  for (int b0 = 0; b0 < B; b0 += kPlanThreads) {
+    const int b = b0 + tid;
+    int need = 0, m = 0;
+    if (b < B) {
+      m = a.depth[b];
+      for (int i = 0; i < m; ++i) need += (c.cache_len[b * R + i] % kPage) == 0;
+    }
+    int tot;
+    const int ex = block_exclusive_scan(need, scan_tmp, &tot);
+    if (b < B && !s_oom) {
+      int next = s_carry + ex;
+      const int t = c.seq_len[b];
+      for (int i = 0; i < m; ++i) {
+        const int slot = c.cache_len[b * R + i];
+        int32_t* pt = c.page_table + ((int64_t)b * R + i) * c.pages_per_seq;
+        if (slot % kPage == 0) pt[slot / kPage] = next++;
+        const int page = pt[slot / kPage];
+        c.pos[(int64_t)page * kPage + slot % kPage] = t;
+        c.cache_len[b * R + i] = slot + 1;
+        atomicAdd(&s_kvread, (unsigned long long)(slot + 1));
+      }
+      atomicAdd(&s_kvwrite, (unsigned long long)m);
+    }
+    if (b < B) {
+      c.seq_len[b] += 1;
+      atomicAdd(&hist[m - 1], 1ull);
+      atomicMax(&s_maxm, m);
+    }
+    __syncthreads();
+    if (tid == 0) s_carry += tot;
+    __syncthreads();
+  }
+  if (tid == 0 && !s_oom) *c.page_next += s_total;
+  if (tid < R) atomicAdd(&c.depth_hist[tid], hist[tid]);
+  if (tid == 0) {
+    c.step_stats[kStatKvRead] = (long long)(s_kvread * (unsigned long long)a.kv_entry_bytes);
+    c.step_stats[kStatKvWrite] = (long long)(s_kvwrite * (unsigned long long)a.kv_entry_bytes);
+    c.step_stats[kStatLoops] = s_maxm;
+  }
+  if (s_oom) {  // the step becomes a no-op for the block: no rows, no attention work
+    if (tid < R) { a.nact[tid] = 0; a.unit_count[tid] = 0; }
+  }
+  __syncthreads();
+  if (tid < R) c.step_stats[kStatRows + tid] = a.nact[tid];
+
+  // 3. split-K work list of the decode attention, per loop
+  for (int i = 0; i < R; ++i) {
+    const int n = a.nact[i];
+    if (tid == 0) s_pages_i = 0ull;
+    __syncthreads();
+    for (int k = tid; k < n; k += kPlanThreads) {
+      const int L = c.cache_len[a.perm[k] * R + i];
+      atomicAdd(&s_pages_i, (unsigned long long)((L + kPage - 1) / kPage));
+    }
+    __syncthreads();
+    if (tid == 0) {
+      const unsigned long long want = (s_pages_i * (unsigned long long)c.H + kAttnWaveTarget - 1) / kAttnWaveTarget;
+      int cp = (int)want;
+      if (cp < kMinChunkPages) cp = kMinChunkPages;
+      s_chunk = cp * kPage;
+      a.chunk_tokens[i] = s_chunk;
+      s_carry = 0;
+    }
+    __syncthreads();
+    const int ct = s_chunk;
+    for (int k0 = 0; k0 < n; k0 += kPlanThreads) {
+      const int k = k0 + tid;
+      int nc = 0;
+      if (k < n) nc = (c.cache_len[a.perm[k] * R + i] + ct - 1) / ct;
+      int tot;
+      const int ex = block_exclusive_scan(nc, scan_tmp, &tot);
+      if (k < n) {
+        a.nchunks[(int64_t)i * a.max_batch + k] = nc;
+        int32_t* u = a.units + (int64_t)i * a.units_cap + s_carry + ex;
+        for (int ch = 0; ch < nc; ++ch) u[ch] = k | (ch << 16);
+      }
+      __syncthreads();
+      if (tid == 0) s_carry += tot;
+      __syncthreads();
+    }
+    if (tid == 0) a.unit_count[i] = s_carry;
+    __syncthreads();
+  }
+  for (int b = tid; b < B; b += kPlanThreads) a.argmax_keys[b] = 0ull;
+}
+
+// ---------------------------------------------------------------------------
+// Prefill planner: workgroup g handles sequence b0 + g.  For each loop i it
+// gathers rho^(i) = sort(A_i) (Eq. 6) by a block prefix sum over the flags
+// m_t >= i, allocates ceil(n / 16) pages, and records every slot's original
+// position (Section 3.3 address translation).
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kPlanThreads) void k_plan_prefill(PrefillPlanArgs a) {
+  const CacheView& c = a.c;
+  const int tid = threadIdx.x, g = blockIdx.x, T = a.T, R = c.R;
+  const int b = a.b0 + g;
+  const int64_t GT = (int64_t)a.G * T;
+  __shared__ int scan_tmp[kPlanThreads / kWave + 1];
+  __shared__ int s_carry, s_base;
+  __shared__ unsigned long long hist[kMaxLoops];
+  if (tid < kMaxLoops) hist[tid] = 0ull;
+  __syncthreads();
+  for (int t = tid; t < T; t += kPlanThreads) atomicAdd(&hist[a.depth[(int64_t)g * T + t] - 1], 1ull);
+  for (int i = 0; i < R; ++i) {
+    int32_t* idx = a.tok_idx + (int64_t)i * GT + (int64_t)g * T;
+    if (tid == 0) s_carry = 0;
+    __syncthreads();
+    for (int t0 = 0; t0 < T; t0 += kPlanThreads) {
+      const int t = t0 + tid;
+      const int f = (t < T && a.depth[(int64_t)g * T + t] >= i + 1) ? 1 : 0;
+      int tot;
+      const int ex = block_exclusive_scan(f, scan_tmp, &tot);
+      if (f) idx[s_carry + ex] = g * T + t;
+      __syncthreads();
+      if (tid == 0) s_carry += tot;
+      __syncthreads();
+    }
+    const int n = s_carry;
+    const int np = (n + kPage - 1) / kPage;
+    if (tid == 0) {
+      int base = np > 0 ? atomicAdd(c.page_next, np) : 0;
+      if ((int64_t)base + np > c.max_pages) {
+        set_err(c.err, kErrOutOfPages);
+        base = -1;
+      }
+      s_base = base;
+    }
+    __syncthreads();
+    const int base = s_base;
+    const int nn = base < 0 ? 0 : n;
+    int32_t* pt = c.page_table + ((int64_t)b * R + i) * c.pages_per_seq;
+    if (base >= 0) {
+      for (int p = tid; p < np; p += kPlanThreads) pt[p] = base + p;
+      for (int s = tid; s < np * kPage; s += kPlanThreads)
+        c.pos[(int64_t)base * kPage + s] = s < n ? idx[s] - g * T : -1;
+    }
+    if (tid == 0) c.cache_len[b * R + i] = nn;
+    __syncthreads();
+  }
+  if (tid == 0) c.seq_len[b] = T;
+  if (tid < R) atomicAdd(&c.depth_hist[tid], hist[tid]);
+}
+
+__global__ void k_fill_i32(int32_t* p, int32_t v, int64_t n) {
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) p[i] = v;
+}
+__global__ void k_fill_u64(unsigned long long* p, unsigned long long v, int64_t n) {
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) p[i] = v;
+}
+__global__ void k_argmax_finalize(const unsigned long long* keys, int32_t* next, int B) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b < B) next[b] = (int32_t)(0xFFFFFFFFu - (unsigned)(keys[b] & 0xFFFFFFFFull));
+}
+
+int fill_grid(int64_t n) {
+  int64_t g = (n + 255) / 256;
+  if (g > 4096) g = 4096;
+  return g < 1 ? 1 : (int)g;
+}
+
+}  // namespace
+
+template <typename T> hipError_t launch_embed_route(const EmbedArgs& a, hipStream_t s) {
+  if (a.rows <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_embed_route<T>, dim3((a.rows + 3) / 4), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+template hipError_t launch_embed_route<float>(const EmbedArgs&, hipStream_t);
+template hipError_t launch_embed_route<bf16>(const EmbedArgs&, hipStream_t);
+
+hipError_t launch_plan_decode(const DecodePlanArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(k_plan_decode, dim3(1), dim3(kPlanThreads), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_plan_prefill(const PrefillPlanArgs& a, hipStream_t s) {
+  if (a.G <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_plan_prefill, dim3(a.G), dim3(kPlanThreads), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_fill_i32(int32_t* p, int32_t v, int64_t n, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_fill_i32, dim3(fill_grid(n)), dim3(256), 0, s, p, v, n);
+  return hipGetLastError();
+}
+hipError_t launch_fill_u64(unsigned long long* p, unsigned long long v, int64_t n, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_fill_u64, dim3(fill_grid(n)), dim3(256), 0, s, p, v, n);
+  return hipGetLastError();
+}
+hipError_t launch_argmax_finalize(const unsigned long long* keys, int32_t* next, int B, hipStream_t s) {
+  if (B <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_argmax_finalize, dim3((B + 255) / 256), dim3(256), 0, s, keys, next, B);
+  return hipGetLastError();
+}
+
+}  // namespace tlf

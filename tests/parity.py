@@ -1,0 +1,112 @@
+"""Runs the HIP path (through the C ABI) and the oracle on the same seeded
+inputs and compares them.  The oracle is teacher-forced on the tokens the GPU
+emits, so a legitimately different greedy pick in bf16 cannot make the two
+sequences diverge."""
+from __future__ import annotations
+
+import dataclasses
+import time
+from typing import Dict, List, Optional, Sequence
+
+import numpy as np
+
+import synth
+from oracle import tlf_oracle as O
+
+
+@dataclasses.dataclass
+class GpuRun:
+    prefill_logits: np.ndarray          # [B][V] or [B][T][V]
+    prefill_depths: np.ndarray          # [B][T]
+    step_tokens: List[np.ndarray]       # token fed at each decode step [B]
+    step_logits: List[np.ndarray]       # [B][V]
+    step_next: List[np.ndarray]
+    step_depths: List[np.ndarray]
+    step_margin: List[np.ndarray]
+    stats: Dict
+
+
+def run_gpu(model: synth.ModelConfig, weights: Dict, prompts: np.ndarray, steps: int,
+            route_rule: str = "argmax", threshold: float = 0.5, fixed_depth: int = 1,
+            all_logits: bool = False, max_pos: Optional[int] = None, max_pages: Optional[int] = None,
+            max_prefill_tokens: int = 65536, keep_logits_rows: Optional[Sequence[int]] = None) -> GpuRun:
+    import torch
+    from paper_2609_15160_amd import tlf
+    B, T = prompts.shape
+    sess = tlf.Session(model, weights, max_batch=B, max_pos=max_pos or (T + steps), max_pages=max_pages,
+                       route_rule=route_rule, threshold=threshold, fixed_depth=fixed_depth,
+                       max_prefill_tokens=max_prefill_tokens)
+    rows = slice(None) if keep_logits_rows is None else list(keep_logits_rows)
+    try:
+        toks = torch.from_numpy(prompts.astype(np.int32)).cuda()
+        lg, dep = sess.prefill(toks, all_logits=all_logits)
+        run = GpuRun(lg.cpu().numpy()[rows], dep.cpu().numpy(), [], [], [], [], [], {})
+        # the first decode token is the greedy pick of the prefill logits
+        last = lg[:, -1, :] if all_logits else lg
+        cur = torch.argmax(last, dim=-1).to(torch.int32)
+        for _ in range(steps):
+            logits, nxt, d, mg = sess.decode(cur)
+            run.step_tokens.append(cur.cpu().numpy())
+            run.step_logits.append(logits.cpu().numpy()[rows])
+            run.step_next.append(nxt.cpu().numpy())
+            run.step_depths.append(d.cpu().numpy())
+            run.step_margin.append(mg.cpu().numpy())
+            cur = nxt
+        run.stats = sess.stats(with_index=True)
+        torch.cuda.synchronize()
+        return run
+    finally:
+        sess.close()
+
+
+@dataclasses.dataclass
+class OracleRun:
+    prefill_logits: np.ndarray
+    prefill_depths: np.ndarray
+    prefill_margin: np.ndarray
+    step_logits: List[np.ndarray]
+    step_depths: List[np.ndarray]
+    step_margin: List[np.ndarray]
+    index: List[List[np.ndarray]]       # [b][i] ascending positions
+    seconds_prefill: float = 0.0
+    seconds_decode: float = 0.0
+
+
+def run_oracle(model: synth.ModelConfig, weights: Dict, prompts: np.ndarray,
+               step_tokens: Sequence[np.ndarray], route_rule: str = "argmax", threshold: float = 0.5,
+               fixed_depth: Optional[int] = None, all_logits: bool = False) -> OracleRun:
+    M = O.Model(weights, model.n_heads, model.head_dim, route_rule=route_rule, threshold=threshold,
+                fixed_depth=fixed_depth, rms_eps=model.rms_eps)
+    t0 = time.perf_counter()
+    states, lg, dep, mg = O.prefill_batch(M, prompts, all_logits=all_logits)
+    t1 = time.perf_counter()
+    run = OracleRun(lg, dep, mg, [], [], [], [])
+    for tok in step_tokens:
+        l, d, m = O.decode(M, states, tok)
+        run.step_logits.append(l)
+        run.step_depths.append(d)
+        run.step_margin.append(m)
+    run.seconds_prefill = t1 - t0
+    run.seconds_decode = time.perf_counter() - t1
+    run.index = [O.cache_index(s, M.R) for s in states]
+    return run
+
+
+def router_decisions(model: synth.ModelConfig, weights: Dict, tokens: np.ndarray, positions: np.ndarray,
+                     route_rule: str = "argmax", threshold: float = 0.5, fixed_depth: Optional[int] = None):
+    """Oracle depth and margin for arbitrary (token, position) pairs (router only)."""
+    M = O.Model(weights, model.n_heads, model.head_dim, route_rule=route_rule, threshold=threshold,
+                fixed_depth=fixed_depth, rms_eps=model.rms_eps)
+    h0 = M.E[tokens] + M.P[positions]
+    m, margin, _ = O.route(M, h0)
+    return m, margin
+
+
+def depth_agreement(gpu_depths: np.ndarray, oracle_depths: np.ndarray, oracle_margin: np.ndarray,
+                    min_margin: float):
+    """(mismatches among decisions with margin > min_margin, overall flip rate)."""
+    g = np.asarray(gpu_depths).ravel()
+    o = np.asarray(oracle_depths).ravel()
+    mg = np.asarray(oracle_margin).ravel()
+    strong = mg > min_margin
+    return int(np.sum((g != o) & strong)), float(np.mean(g != o)) if g.size else 0.0

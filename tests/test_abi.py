@@ -1,0 +1,126 @@
+"""CPU checks of the C ABI: the library loads, exports what include/tlf.h
+declares, its structs match the binding, and host-side validation rejects bad
+arguments before any device work."""
+import ctypes
+import os
+import subprocess
+import tempfile
+
+import pytest
+
+import synth
+from paper_2609_15160_amd import tlf
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return tlf.load()
+
+
+def test_library_exports_every_declared_symbol(lib):
+    declared = tlf.header_exports()
+    assert sorted(declared) == sorted(tlf.EXPORTS)
+    for name in declared:
+        assert hasattr(lib, name), name
+
+
+def test_struct_layouts_match_the_header():
+    src = r"""
+#include <stdio.h>
+#include <stddef.h>
+#include "tlf.h"
+int main(void) {
+  printf("%zu %zu %zu %zu\n", sizeof(tlf_config), sizeof(tlf_layer_weights), sizeof(tlf_weights),
+         sizeof(tlf_cache_stats_t));
+  printf("%zu %zu %zu %zu\n", offsetof(tlf_config, rms_eps), offsetof(tlf_weights, layers),
+         offsetof(tlf_cache_stats_t, last_step_active_rows), offsetof(tlf_cache_stats_t, device_error));
+  return 0;
+}
+"""
+    with tempfile.TemporaryDirectory() as d:
+        c = os.path.join(d, "t.c")
+        exe = os.path.join(d, "t")
+        open(c, "w").write(src)
+        subprocess.check_call(["gcc", "-std=c99", "-I", os.path.join(ROOT, "include"), c, "-o", exe])
+        out = subprocess.check_output([exe]).decode().split()
+    sizes = [int(v) for v in out]
+    assert sizes[:4] == [ctypes.sizeof(tlf.Config), ctypes.sizeof(tlf.LayerWeights),
+                         ctypes.sizeof(tlf.Weights), ctypes.sizeof(tlf.CacheStats)]
+    assert sizes[4:] == [tlf.Config.rms_eps.offset, tlf.Weights.layers.offset,
+                         tlf.CacheStats.last_step_active_rows.offset, tlf.CacheStats.device_error.offset]
+
+
+def _cfg(**kw):
+    m = synth.CONFIGS["c3"]
+    c = tlf.make_config(m, max_batch=256, max_pos=m.max_pos,
+                        max_pages=tlf.worst_case_pages(256, m.max_pos, m.max_loops))
+    for k, v in kw.items():
+        setattr(c, k, v)
+    return c
+
+
+def test_size_query_needs_no_device(lib):
+    need = tlf.workspace_bytes(_cfg())
+    m = synth.CONFIGS["c3"]
+    page_bytes = m.n_layers * 2 * m.d_model * 16 * 2
+    pool = tlf.worst_case_pages(256, m.max_pos, m.max_loops) * page_bytes
+    assert pool < need < pool * 1.2
+
+
+@pytest.mark.parametrize("field,value", [
+    ("abi_version", 2), ("dtype", 7), ("vocab", 0), ("d_model", 100), ("head_dim", 32),
+    ("n_heads", 5), ("d_ff", 1000), ("n_layers", 0), ("n_layers", 9), ("max_loops", 0),
+    ("max_loops", 17), ("max_pos", 0), ("max_batch", 0), ("max_batch", 5000), ("page_tokens", 32),
+    ("max_pages", 0), ("max_prefill_tokens", 0), ("route_rule", 5), ("rms_eps", 0.0),
+])
+def test_invalid_config_rejected(lib, field, value):
+    c = _cfg(**{field: value})
+    need = ctypes.c_size_t(0)
+    st = lib.tlf_init(ctypes.byref(c), None, None, 0, ctypes.byref(need), None, None)
+    assert st == tlf.E_INVALID_ARG
+
+
+def test_route_parameters_validated(lib):
+    need = ctypes.c_size_t(0)
+    for kw in (dict(route_rule=1, route_threshold=0.0), dict(route_rule=1, route_threshold=1.0),
+               dict(route_rule=2, fixed_depth=0), dict(route_rule=2, fixed_depth=9)):
+        c = _cfg(**kw)
+        assert lib.tlf_init(ctypes.byref(c), None, None, 0, ctypes.byref(need), None, None) == tlf.E_INVALID_ARG
+    for kw in (dict(route_rule=1, route_threshold=0.5), dict(route_rule=2, fixed_depth=8)):
+        c = _cfg(**kw)
+        assert lib.tlf_init(ctypes.byref(c), None, None, 0, ctypes.byref(need), None, None) == tlf.E_NEED_WORKSPACE
+
+
+def test_bf16_head_dim_16_rejected_f32_accepted(lib):
+    need = ctypes.c_size_t(0)
+    c = tlf.make_config(synth.CONFIGS["c1"], 1, 64, 64)
+    assert lib.tlf_init(ctypes.byref(c), None, None, 0, ctypes.byref(need), None, None) == tlf.E_NEED_WORKSPACE
+    c.dtype = tlf.DTYPE_BF16
+    assert lib.tlf_init(ctypes.byref(c), None, None, 0, ctypes.byref(need), None, None) == tlf.E_INVALID_ARG
+
+
+def test_missing_weights_rejected_before_device_work(lib):
+    c = _cfg()
+    need = ctypes.c_size_t(0)
+    w = tlf.Weights()  # all NULL
+    fake_ws = ctypes.c_void_p(1 << 20)  # never dereferenced: validation fails first
+    ctx = ctypes.c_void_p()
+    st = lib.tlf_init(ctypes.byref(c), ctypes.byref(w), fake_ws, 1 << 62, ctypes.byref(need), None,
+                      ctypes.byref(ctx))
+    assert st == tlf.E_INVALID_ARG and not ctx.value
+
+
+def test_null_context_calls(lib):
+    out = tlf.CacheStats()
+    assert lib.tlf_prefill(None, 1, 1, None, None, None, 0) == tlf.E_INVALID_ARG
+    assert lib.tlf_decode_step(None, None, None, None, None, None) == tlf.E_INVALID_ARG
+    assert lib.tlf_cache_stats(None, ctypes.byref(out), None, None, 0) == tlf.E_INVALID_ARG
+    lib.tlf_destroy(None)
+
+
+def test_status_strings(lib):
+    assert lib.tlf_status_str(tlf.OK) == b"ok"
+    assert b"page" in lib.tlf_status_str(tlf.E_OUT_OF_PAGES)
+    assert lib.tlf_status_str(12345) == b"unknown status"

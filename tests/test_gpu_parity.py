@@ -1,0 +1,299 @@
+"""GPU parity: the HIP path through the C ABI against the oracle.
+
+Bars: fp32 models - depth decisions and cache indices bit-exact, logits
+max-abs <= 1e-4.  bf16 models - depth decisions whose router margin exceeds
+1e-2 match (flip rate reported), logits max-abs <= 3e-2, cache indices equal
+{t : m_t >= i} for the depths the GPU took.
+"""
+import numpy as np
+import pytest
+
+import synth
+from tests import parity
+
+pytestmark = pytest.mark.gpu
+
+F32_TOL = 1e-4
+BF16_TOL = 3e-2
+BF16_MARGIN = 1e-2
+
+
+def _report(tag, **kv):
+    print(f"[parity] {tag} " + " ".join(f"{k}={v}" for k, v in kv.items()), flush=True)
+
+
+def _max_err(g, o):
+    return float(np.max(np.abs(np.asarray(g, np.float64) - np.asarray(o, np.float64))))
+
+
+def _all_depths(g: parity.GpuRun):
+    """Depth of every token of every sequence, prompt then decode steps: [B][T+S]."""
+    cols = [g.prefill_depths] + [d[:, None] for d in g.step_depths]
+    return np.concatenate(cols, axis=1)
+
+
+def _check_index_matches_depths(g: parity.GpuRun, R: int):
+    dep = _all_depths(g)
+    for b in range(dep.shape[0]):
+        for i in range(R):
+            want = np.flatnonzero(dep[b] >= i + 1)
+            assert np.array_equal(g.stats["index"][b][i], want), (b, i)
+
+
+def _f32_small(**kw):
+    base = dict(name="f32-small", dtype="f32", vocab=300, d_model=64, n_heads=4, head_dim=16, d_ff=128,
+                n_layers=2, max_loops=4, batch=3, prompt_len=37, steps=19, router_bias="zero")
+    base.update(kw)
+    return synth.ModelConfig(**base)
+
+
+def _check_f32(m, w, prompts, g, o, tag):
+    assert np.array_equal(g.prefill_depths, o.prefill_depths)
+    for s in range(len(g.step_depths)):
+        assert np.array_equal(g.step_depths[s], o.step_depths[s]), s
+    err = _max_err(g.prefill_logits, o.prefill_logits)
+    for s in range(len(g.step_logits)):
+        err = max(err, _max_err(g.step_logits[s], o.step_logits[s]))
+    for b in range(prompts.shape[0]):
+        for i in range(m.max_loops):
+            assert np.array_equal(g.stats["index"][b][i], o.index[b][i]), (b, i)
+    for s in range(len(g.step_next)):
+        assert np.array_equal(g.step_next[s], np.argmax(g.step_logits[s], axis=-1))
+    _report(tag, max_abs_logit_err=f"{err:.3g}", steps=len(g.step_logits),
+            depth_hist=g.stats["depth_hist"])
+    assert err <= F32_TOL
+    assert np.all(np.isfinite(g.prefill_logits))
+
+
+def test_c1_fp32_decode_parity():
+    m = synth.CONFIGS["c1"]
+    w = synth.make_weights(m)
+    prompts = synth.make_prompts(m)
+    g = parity.run_gpu(m, w, prompts, m.steps)
+    o = parity.run_oracle(m, w, prompts, g.step_tokens)
+    _check_f32(m, w, prompts, g, o, "c1")
+    # the oracle's own greedy choice agrees wherever its top-2 gap exceeds the tolerance
+    for s in range(m.steps):
+        lo = o.step_logits[s]
+        srt = np.sort(lo, axis=-1)
+        clear = (srt[:, -1] - srt[:, -2]) > 2 * F32_TOL
+        assert np.all(g.step_next[s][clear] == np.argmax(lo, axis=-1)[clear])
+
+
+def test_c1_prefill_all_positions():
+    m = synth.CONFIGS["c1"]
+    w = synth.make_weights(m)
+    prompts = synth.make_prompts(m)
+    g = parity.run_gpu(m, w, prompts, 0, all_logits=True, max_pos=m.max_pos)
+    o = parity.run_oracle(m, w, prompts, [], all_logits=True)
+    err = _max_err(g.prefill_logits, o.prefill_logits)
+    _report("c1-all-logits", max_abs_logit_err=f"{err:.3g}")
+    assert err <= F32_TOL
+
+
+def test_f32_two_layers_ragged_batch():
+    m = _f32_small()
+    w = synth.make_weights(m)
+    prompts = synth.make_prompts(m)
+    g = parity.run_gpu(m, w, prompts, m.steps)
+    o = parity.run_oracle(m, w, prompts, g.step_tokens)
+    _check_f32(m, w, prompts, g, o, "f32-small")
+
+
+def test_f32_single_token_prompt_and_deep_tail():
+    m = _f32_small(batch=2, prompt_len=1, steps=40)
+    w = synth.make_weights(m)
+    prompts = synth.make_prompts(m)
+    g = parity.run_gpu(m, w, prompts, m.steps)
+    o = parity.run_oracle(m, w, prompts, g.step_tokens)
+    _check_f32(m, w, prompts, g, o, "f32-T1")
+
+
+def test_f32_cumprob_rule():
+    m = _f32_small(steps=10)
+    w = dict(synth.make_weights(m))
+    w["router_w"] = (w["router_w"] * 150.0).astype(np.float32)  # spread the routing distribution
+    prompts = synth.make_prompts(m)
+    g = parity.run_gpu(m, w, prompts, m.steps, route_rule="cumprob", threshold=0.5)
+    o = parity.run_oracle(m, w, prompts, g.step_tokens, route_rule="cumprob", threshold=0.5)
+    bad, flips = parity.depth_agreement(g.prefill_depths, o.prefill_depths, o.prefill_margin, 1e-5)
+    _report("cumprob", flips=flips, hist=g.stats["depth_hist"])
+    assert bad == 0
+    assert len(set(g.prefill_depths.ravel().tolist())) >= 3
+    if flips == 0:
+        _check_f32(m, w, prompts, g, o, "cumprob")
+
+
+@pytest.mark.parametrize("depth", [1, 4])
+def test_f32_fixed_depth(depth):
+    m = _f32_small(steps=8)
+    w = synth.make_weights(m)
+    prompts = synth.make_prompts(m)
+    g = parity.run_gpu(m, w, prompts, m.steps, route_rule="fixed", fixed_depth=depth)
+    o = parity.run_oracle(m, w, prompts, g.step_tokens, route_rule="fixed", fixed_depth=depth)
+    assert np.all(g.prefill_depths == depth)
+    _check_f32(m, w, prompts, g, o, f"fixed{depth}")
+
+
+def test_prefill_in_sequence_groups_is_identical():
+    m = _f32_small(batch=5, prompt_len=40, steps=3)
+    w = synth.make_weights(m)
+    prompts = synth.make_prompts(m)
+    a = parity.run_gpu(m, w, prompts, m.steps)
+    b = parity.run_gpu(m, w, prompts, m.steps, max_prefill_tokens=2 * m.prompt_len)
+    assert np.array_equal(a.prefill_logits, b.prefill_logits)
+    for s in range(m.steps):
+        assert np.array_equal(a.step_logits[s], b.step_logits[s])
+
+
+def test_fp32_runs_are_bitwise_deterministic():
+    m = synth.CONFIGS["c1"]
+    w = synth.make_weights(m)
+    prompts = synth.make_prompts(m)
+    a = parity.run_gpu(m, w, prompts, 8)
+    b = parity.run_gpu(m, w, prompts, 8)
+    for s in range(8):
+        assert np.array_equal(a.step_logits[s], b.step_logits[s])
+
+
+def _check_bf16(m, w, prompts, g, o, sample, tag, route_rule="argmax", fixed_depth=None):
+    B, T = prompts.shape
+    # router decisions of every token against the oracle router
+    pos = np.broadcast_to(np.arange(T), (B, T))
+    od, om = parity.router_decisions(m, w, prompts.ravel(), pos.ravel(), route_rule, fixed_depth=fixed_depth)
+    bad, flips = parity.depth_agreement(g.prefill_depths.ravel(), od, om, BF16_MARGIN)
+    nbad, nflips = 0, []
+    for s, tok in enumerate(g.step_tokens):
+        sd, sm = parity.router_decisions(m, w, tok, np.full(B, T + s), route_rule, fixed_depth=fixed_depth)
+        b2, f2 = parity.depth_agreement(g.step_depths[s], sd, sm, BF16_MARGIN)
+        nbad += b2
+        nflips.append(f2)
+    assert bad == 0 and nbad == 0
+    _check_index_matches_depths(g, m.max_loops)
+    err = _max_err(g.prefill_logits, o.prefill_logits)
+    for s in range(len(g.step_logits)):
+        err = max(err, _max_err(g.step_logits[s], o.step_logits[s]))
+    agree = np.mean([np.mean(g.step_next[s][sample] == np.argmax(o.step_logits[s], -1))
+                     for s in range(len(g.step_next))]) if g.step_next else 1.0
+    _report(tag, max_abs_logit_err=f"{err:.3g}", prefill_flip_rate=flips,
+            decode_flip_rate=float(np.mean(nflips)) if nflips else 0.0, greedy_agreement=f"{agree:.3f}",
+            depth_hist=g.stats["depth_hist"])
+    for j, b in enumerate(sample):
+        for i in range(m.max_loops):
+            if np.array_equal(_all_depths(g)[b], np.concatenate([o.prefill_depths[j],
+                                                                  [d[j] for d in o.step_depths]])):
+                assert np.array_equal(g.stats["index"][b][i], o.index[j][i])
+    assert err <= BF16_TOL
+    assert np.all(np.isfinite(g.prefill_logits))
+
+
+def test_c2_bf16_parity_sampled_sequences():
+    m = synth.CONFIGS["c2"]
+    w = synth.make_weights(m)
+    prompts = synth.make_prompts(m)
+    steps = 12
+    sample = [0, 13, 31]
+    g = parity.run_gpu(m, w, prompts, steps, max_pos=m.max_pos, keep_logits_rows=sample)
+    o = parity.run_oracle(m, w, prompts[sample], [t[sample] for t in g.step_tokens])
+    _check_bf16(m, w, prompts, g, o, sample, "c2")
+
+
+def test_bf16_fixed_depth_ragged_prompt():
+    m = synth.CONFIGS["c2"].replace(batch=4, prompt_len=77, steps=6)
+    w = synth.make_weights(synth.CONFIGS["c2"])
+    prompts = synth.make_prompts(m)
+    sample = [1, 3]
+    g = parity.run_gpu(m, w, prompts, m.steps, route_rule="fixed", fixed_depth=8, max_pos=m.max_pos,
+                       keep_logits_rows=sample)
+    o = parity.run_oracle(m, w, prompts[sample], [t[sample] for t in g.step_tokens], route_rule="fixed",
+                          fixed_depth=8)
+    assert np.all(g.prefill_depths == 8)
+    _check_bf16(m, w, prompts, g, o, sample, "bf16-fixed8", route_rule="fixed", fixed_depth=8)
+
+
+@pytest.mark.slow
+def test_c3_full_size_sampled_sequences():
+    """The benchmark's workload (batch 256 x 2048 prompt) with the oracle on two sequences."""
+    m = synth.CONFIGS["c3"]
+    w = synth.make_weights(m)
+    prompts = synth.make_prompts(m)
+    steps = 3
+    sample = [0, 255]
+    g = parity.run_gpu(m, w, prompts, steps, max_pos=m.max_pos, keep_logits_rows=sample)
+    o = parity.run_oracle(m, w, prompts[sample], [t[sample] for t in g.step_tokens])
+    _check_bf16(m, w, prompts, g, o, sample, "c3")
+
+
+# ---------------------------------------------------------------------------
+# Error handling through the C ABI
+# ---------------------------------------------------------------------------
+
+def _session(m, w, **kw):
+    from paper_2609_15160_amd import tlf
+    return tlf.Session(m, w, **kw)
+
+
+def test_state_errors():
+    import torch
+    from paper_2609_15160_amd import tlf
+    m = _f32_small(batch=2, prompt_len=5, steps=2)
+    w = synth.make_weights(m)
+    s = _session(m, w, max_batch=2, max_pos=7)
+    try:
+        tok = torch.zeros(2, dtype=torch.int32, device="cuda")
+        with pytest.raises(tlf.TlfError) as e:
+            s.decode(tok)
+        assert e.value.status == tlf.E_STATE
+        with pytest.raises(tlf.TlfError) as e:
+            s.prefill(torch.zeros((3, 5), dtype=torch.int32, device="cuda"))  # batch > max_batch
+        assert e.value.status == tlf.E_INVALID_ARG
+        s.prefill(torch.zeros((2, 5), dtype=torch.int32, device="cuda"))
+        s.decode(tok)
+        s.decode(tok)
+        with pytest.raises(tlf.TlfError) as e:  # position 7 == max_pos
+            s.decode(tok)
+        assert e.value.status == tlf.E_STATE
+        assert s.stats()["status"] == tlf.OK
+    finally:
+        s.close()
+
+
+def test_out_of_pages_detected():
+    import torch
+    from paper_2609_15160_amd import tlf
+    m = _f32_small(batch=1, prompt_len=32, steps=8, max_loops=2)
+    w = synth.make_weights(m)
+    s = _session(m, w, max_batch=1, max_pos=40, max_pages=1, route_rule="fixed", fixed_depth=2)
+    try:
+        with pytest.raises(tlf.TlfError) as e:  # 32 tokens fill two pages in loop 1 alone
+            s.prefill(torch.zeros((1, 32), dtype=torch.int32, device="cuda"))
+        assert e.value.status == tlf.E_OUT_OF_PAGES
+    finally:
+        s.close()
+    # exactly enough pages for the prefill (2 loops x 1 page); the first decode step needs two more
+    s = _session(m, w, max_batch=1, max_pos=18, max_pages=2, route_rule="fixed", fixed_depth=2)
+    try:
+        s.prefill(torch.zeros((1, 16), dtype=torch.int32, device="cuda"))
+        assert s.stats()["status"] == tlf.OK
+        s.decode(torch.zeros(1, dtype=torch.int32, device="cuda"))
+        st = s.stats()
+        assert st["status"] == tlf.E_OUT_OF_PAGES
+        with pytest.raises(tlf.TlfError) as e:
+            s.decode(torch.zeros(1, dtype=torch.int32, device="cuda"))
+        assert e.value.status == tlf.E_OUT_OF_PAGES
+    finally:
+        s.close()
+
+
+def test_bad_token_reported():
+    import torch
+    from paper_2609_15160_amd import tlf
+    m = _f32_small(batch=1, prompt_len=4, steps=1)
+    w = synth.make_weights(m)
+    s = _session(m, w, max_batch=1, max_pos=5)
+    try:
+        s.prefill(torch.zeros((1, 4), dtype=torch.int32, device="cuda"))
+        s.decode(torch.full((1,), m.vocab, dtype=torch.int32, device="cuda"))
+        assert s.stats()["status"] == tlf.E_DEVICE
+    finally:
+        s.close()
