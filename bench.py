@@ -1,0 +1,251 @@
+#!/usr/bin/env python3
+"""Decode-step benchmark of the routed looped transformer on one MI355X.
+
+Workload (default): the 2-layer d=768 looped block (12 heads x 64, SwiGLU
+2048, vocab 32000, R = 8 loops, bf16 storage) decoding a batch of 256
+sequences after a 2048-token prompt, KV cache paged in 16-token pages, router
+bias calibrated to a long-tailed depth mix with mean ~3.7.  A step is one
+decode step of every sequence: embedding + routing, the depth-sorted plan,
+every executed loop and layer (QKV + cache append, recursion-wise attention,
+O projection, SwiGLU FFN), the LM head and the greedy pick.
+
+Prints one JSON line: decoded tokens/s, the decode attention's achieved HBM
+bandwidth against 8 TB/s (HIP events around every attention launch on the
+library's stream), the same kernels forced to fixed depth R, a prefill
+measurement, and the CPU oracle on a bounded sample.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0      # MI355X HBM3E
+BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
+METRIC = "decoded tokens/s at batch B; recursion-wise KV attn HBM GB/s (% of peak)"
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def decode_run(sess, torch, B, V, warmup, steps, first_tokens):
+    """Warmup, then `steps` timed decode steps with greedy feedback (no allocation)."""
+    dev = sess.device
+    tok = [first_tokens.to(torch.int32).contiguous(), torch.empty(B, dtype=torch.int32, device=dev)]
+    logits = torch.empty((B, V), dtype=torch.float32, device=dev)
+    k = 0
+    for _ in range(warmup):
+        sess.decode_into(tok[k % 2], logits, next_tok=tok[(k + 1) % 2])
+        k += 1
+    torch.cuda.synchronize()
+    sess.set_profiling(True)
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(steps):
+        sess.decode_into(tok[k % 2], logits, next_tok=tok[(k + 1) % 2])
+        k += 1
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1)
+    st = sess.stats()
+    sess.set_profiling(False)
+    if st["status"] != 0:
+        raise RuntimeError(f"device error {st['status']}")
+    if not bool(torch.isfinite(logits).all()):
+        raise RuntimeError("non-finite logits")
+    return ms, st
+
+
+def hot_path_bytes(st, model, steps, B):
+    """Algorithmic HBM bytes of the timed steps' loop-and-layer region."""
+    s = 2 if model.dtype == "bf16" else 4
+    d, F, J = model.d_model, model.d_ff, model.n_layers
+    block_weights = (4 * d * d + 3 * d * F) * s
+    weights = st["loops_executed_total"] * J * block_weights
+    return st["attn_algo_bytes"] + st["kv_write_bytes_total"] + weights
+
+
+def run_config(torch, tlf, model, w, prompts, warmup, steps, route_rule="argmax", fixed_depth=1):
+    B, T = prompts.shape
+    max_pos = T + warmup + steps
+    sess = tlf.Session(model, w, max_batch=B, max_pos=max_pos, route_rule=route_rule,
+                       fixed_depth=fixed_depth, max_prefill_tokens=65536)
+    try:
+        toks = torch.from_numpy(prompts).cuda()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        logits, _ = sess.prefill(toks, want_depths=False)
+        torch.cuda.synchronize()
+        prefill_s = time.perf_counter() - t0
+        first = torch.argmax(logits, dim=-1)
+        del logits
+        ms, st = decode_run(sess, torch, B, model.vocab, warmup, steps, first)
+        hist = sess.stats()["depth_hist"]
+        return ms, st, prefill_s, hist
+    finally:
+        sess.close()
+        torch.cuda.empty_cache()
+
+
+def cpu_baseline(model, w, prompts, budget_s):
+    """The oracle (untuned) decoding one sequence of the same workload on the host."""
+    import numpy as np
+    from oracle import tlf_oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:
+        cores = os.cpu_count() or 1
+    M = O.Model(w, model.n_heads, model.head_dim, rms_eps=model.rms_eps)
+    st, lg, _, _ = O.prefill(M, prompts[0])
+    tok = int(O.greedy(lg))
+    n = 0
+    t0 = time.perf_counter()
+    while n < 2 or (time.perf_counter() - t0 < budget_s and n < model.steps):
+        lg2, _, _ = O.decode(M, [st], [tok])
+        tok = int(O.greedy(lg2[0]))
+        n += 1
+    dt = time.perf_counter() - t0
+    return {"value": n / dt, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"1 of {prompts.shape[0]} sequences: oracle prefill of its {prompts.shape[1]}-token "
+                      f"prompt (untimed), then {n} greedy decode steps timed ({dt:.1f} s)"}
+
+
+def prefill_measure(torch, tlf, synth, name):
+    """Prefill-only workload: time tlf_prefill and count the algorithmic FLOPs."""
+    import numpy as np
+    m = synth.CONFIGS[name]
+    w = synth.make_weights(m)
+    prompts = synth.make_prompts(m)
+    B, T = prompts.shape
+    sess = tlf.Session(m, w, max_batch=B, max_pos=T, max_prefill_tokens=B * T)
+    try:
+        toks = torch.from_numpy(prompts).cuda()
+        sess.prefill(toks)  # warm
+        torch.cuda.synchronize()
+        reps = 3
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            _, depths = sess.prefill(toks)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / reps
+        dep = depths.cpu().numpy()
+    finally:
+        sess.close()
+        torch.cuda.empty_cache()
+    d, F, J, R = m.d_model, m.d_ff, m.n_layers, m.max_loops
+    n = np.stack([(dep >= i).sum(axis=1) for i in range(1, R + 1)], axis=1)  # n_{b,i}
+    gemm = float(n.sum()) * J * 2 * (4 * d * d + 3 * d * F)
+    attn = float((n.astype(np.float64) * (n + 1) / 2).sum()) * J * 4 * d
+    head = 2.0 * B * d * m.vocab
+    flops = gemm + attn + head
+    return {"workload": f"{name} prefill: batch {B} x {T}, d={d}, {m.n_heads}x{m.head_dim} heads, SwiGLU {F}, "
+                        f"R={R}, J={J}", "ms": ms, "tokens_per_s": B * T / ms * 1e3,
+            "algorithmic_tflop": flops / 1e12, "tflops": flops / ms / 1e9,
+            "mfma_frac": flops / ms / 1e9 / BF16_PEAK_TFLOPS}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=8)
+    ap.add_argument("--config", default="c3")
+    ap.add_argument("--no-fixed", action="store_true", help="skip the fixed-depth comparison")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--no-prefill", action="store_true", help="skip the prefill measurement")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path (decode shards by sequence "
+              "with no exchange; run one process per GPU on its own share of the batch)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    import synth
+    from paper_2609_15160_amd import tlf
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    torch.cuda.set_device(0)
+    base = synth.CONFIGS[args.config]
+    if args.warmup + args.steps > base.steps:
+        print(f"warmup + steps must be <= {base.steps} for {args.config}", file=sys.stderr)
+        sys.exit(2)
+    model = base
+    t0 = time.perf_counter()
+    w = synth.make_weights(model)
+    prompts = synth.make_prompts(model)
+    B, T = prompts.shape
+    log(f"inputs ready in {time.perf_counter() - t0:.1f}s: batch {B} x prompt {T}")
+
+    ms, st, prefill_s, hist = run_config(torch, tlf, model, w, prompts, args.warmup, args.steps)
+    log(f"routed: {ms / args.steps:.3f} ms/step, prefill {prefill_s:.2f}s, depth hist {hist}")
+    value = B * args.steps / (ms / 1e3)
+    attn_gbs = st["attn_algo_bytes"] / (st["attn_ms"] / 1e3) / 1e9
+    per_launch = st["attn_algo_bytes"] / max(st["attn_launches"], 1)
+    hot_bytes = hot_path_bytes(st, model, args.steps, B)
+    hot_gbs = hot_bytes / (st["block_ms"] / 1e3) / 1e9
+    tot_hist = np.asarray(hist, dtype=np.float64)
+    mean_depth = float((tot_hist * np.arange(1, len(hist) + 1)).sum() / max(tot_hist.sum(), 1))
+
+    out = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms / args.steps,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": model.dtype,
+        "data": "synthetic (seeded N(0,0.02) weights, uniform-random prompts, greedy decode)",
+        "config": {"workload": f"{args.config} decode: batch {B} x prompt {T}, {model.n_layers}-layer "
+                               f"d={model.d_model} looped block ({model.n_heads}x{model.head_dim} heads, "
+                               f"SwiGLU {model.d_ff}, vocab {model.vocab}), R={model.max_loops}, "
+                               f"argmax router, 16-token KV pages",
+                   "batch": B, "prompt": T, "max_loops": model.max_loops, "layers": model.n_layers,
+                   "mean_depth": mean_depth},
+        "roofline": {"bound": "hbm", "kernel": "k_attn_decode", "achieved": attn_gbs, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": attn_gbs / HBM_PEAK_GBS, "traffic": None,
+                     "launches": st["attn_launches"], "avg_launch_us": st["attn_ms"] * 1e3 / st["attn_launches"],
+                     "algo_bytes_per_launch": per_launch},
+        "hot_path": {"what": "loop-and-layer region per step (attention + QKV/O/SwiGLU GEMMs, gaps included)",
+                     "achieved_gbs": hot_gbs, "frac": hot_gbs / HBM_PEAK_GBS,
+                     "ms_per_step": st["block_ms"] / args.steps, "algo_bytes_per_step": hot_bytes / args.steps},
+        "prefill_s": prefill_s,
+    }
+    if not args.no_fixed:
+        fms, fst, fpre, _ = run_config(torch, tlf, model, w, prompts, args.warmup, args.steps,
+                                       route_rule="fixed", fixed_depth=model.max_loops)
+        fgbs = fst["attn_algo_bytes"] / (fst["attn_ms"] / 1e3) / 1e9
+        out["fixed_depth"] = {"depth": model.max_loops, "value": B * args.steps / (fms / 1e3),
+                              "ms_per_step": fms / args.steps, "attn_achieved_gbs": fgbs,
+                              "attn_frac": fgbs / HBM_PEAK_GBS, "prefill_s": fpre,
+                              "routed_speedup": fms / ms}
+        log(f"fixed depth {model.max_loops}: {fms / args.steps:.3f} ms/step")
+    if not args.no_prefill:
+        out["prefill_c5"] = prefill_measure(torch, tlf, synth, "c5")
+        log(f"prefill c5: {out['prefill_c5']['ms']:.2f} ms")
+    if not args.no_cpu:
+        out["cpu_baseline"] = cpu_baseline(model, w, prompts, args.cpu_seconds)
+        log(f"cpu baseline: {out['cpu_baseline']['value']:.3f} tokens/s")
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -88,7 +88,7 @@ typedef struct tlf_config {
   int32_t d_ff;          /* F, SwiGLU hidden width, multiple of 64 */
   int32_t n_layers;      /* J in [1, TLF_MAX_LAYERS], layers of the shared block */
   int32_t max_loops;     /* R = M in [1, TLF_MAX_LOOPS], router width and loop cap */
-  int32_t max_pos;       /* rows of the position table; prompt + decode steps <= max_pos */
+  int32_t max_pos;       /* rows of the position table, <= 65536; prompt + decode steps <= max_pos */
   int32_t max_batch;     /* sequences per call, in [1, TLF_MAX_BATCH] */
   int32_t page_tokens;   /* tokens per KV page, must be TLF_PAGE_TOKENS */
   int32_t max_pages;     /* KV pages in the pool (all sequences and loops) */
@@ -136,6 +136,14 @@ typedef struct tlf_cache_stats_t {
   int64_t last_step_weight_bytes;
   int64_t last_step_loops_executed;       /* #{i : some token of the step has m >= i} */
   int64_t last_step_active_rows[TLF_MAX_LOOPS]; /* n_i = #{b : m_b >= i} in the last step */
+  /* Totals since profiling was last enabled (tlf_set_profiling): */
+  int64_t decode_steps;                   /* decode steps enqueued */
+  int64_t attn_launches;                  /* decode-attention launches timed */
+  int64_t attn_algo_bytes;                /* their algorithmic bytes: valid K/V entries read, q read, o written */
+  double attn_ms;                         /* their summed duration (HIP events on the context's stream) */
+  int64_t kv_write_bytes_total;           /* bytes of appended k, v */
+  int64_t loops_executed_total;           /* shared-block applications (each streams the block weights once) */
+  double block_ms;                        /* summed duration of the loop-and-layer region of each step */
   int32_t device_error;                   /* sticky device-side status (TLF_OK if none) */
   int32_t reserved;
 } tlf_cache_stats_t;
@@ -191,6 +199,13 @@ int tlf_decode_step(tlf_ctx* ctx, const int32_t* d_tokens, float* d_logits, int3
  * Returns the sticky device error, if any, after filling *out. */
 int tlf_cache_stats(tlf_ctx* ctx, tlf_cache_stats_t* out, int32_t* h_len, int32_t* h_pos,
                     size_t pos_cap);
+
+/* Measurement switch.  enable != 0 resets the totals reported by
+ * tlf_cache_stats (decode_steps, attn_*) and brackets every later
+ * decode-attention launch with a pair of HIP events on the context's stream;
+ * enable == 0 stops the event recording.  It launches one small kernel and
+ * does not wait for the stream. */
+int tlf_set_profiling(tlf_ctx* ctx, int enable);
 
 /* Releases the host context (waits for the stream first).  NULL is ignored. */
 void tlf_destroy(tlf_ctx* ctx);

@@ -19,8 +19,7 @@ int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 // Workspace buffers, in carve order.
 enum Buf {
   B_POOL, B_POS, B_PAGE_TABLE, B_CACHE_LEN, B_SEQ_LEN, B_SCALARS, B_DEPTH_HIST, B_STEP_STATS,
-  B_X_DEC, B_DEPTH_DEC, B_PERM, B_NACT, B_Q_DEC, B_O_DEC, B_ACT_DEC, B_KEYS, B_UNITS,
-  B_UNIT_COUNT, B_CHUNK_TOKENS, B_NCHUNKS, B_PARTIAL, B_COUNTERS,
+  B_X_DEC, B_DEPTH_DEC, B_PERM, B_NACT, B_Q_DEC, B_O_DEC, B_ACT_DEC, B_KEYS,
   B_X_PRE, B_DEPTH_PRE, B_TOK_IDX, B_Q_PRE, B_O_PRE, B_ACT_PRE,
   B_COUNT
 };
@@ -30,7 +29,7 @@ struct Layout {
   size_t size[B_COUNT];
   size_t total = 0;
   int64_t page_elems = 0;
-  int pages_per_seq = 0, max_chunks = 0, units_cap = 0, pre_rows = 0, s = 0;
+  int pages_per_seq = 0, pre_rows = 0, s = 0;
 };
 
 bool make_layout(const tlf_config& c, Layout* L) {
@@ -39,8 +38,6 @@ bool make_layout(const tlf_config& c, Layout* L) {
   L->s = (int)s;
   L->page_elems = (int64_t)c.n_layers * 2 * H * kPage * D;
   L->pages_per_seq = (int)ceil_div(c.max_pos, kPage);
-  L->max_chunks = (int)ceil_div(L->pages_per_seq, kMinChunkPages);
-  L->units_cap = (int)(B * L->max_chunks);
   L->pre_rows = std::max(c.max_prefill_tokens, c.max_pos);
   const int64_t P = L->pre_rows;
   int64_t sz[B_COUNT];
@@ -60,12 +57,6 @@ bool make_layout(const tlf_config& c, Layout* L) {
   sz[B_O_DEC] = B * d * s;
   sz[B_ACT_DEC] = B * F * s;
   sz[B_KEYS] = B * 8;
-  sz[B_UNITS] = R * (int64_t)L->units_cap * 4;
-  sz[B_UNIT_COUNT] = R * 4;
-  sz[B_CHUNK_TOKENS] = R * 4;
-  sz[B_NCHUNKS] = R * B * 4;
-  sz[B_PARTIAL] = B * H * L->max_chunks * (D + 2) * 4;
-  sz[B_COUNTERS] = B * H * 4;
   sz[B_X_PRE] = P * d * 4;
   sz[B_DEPTH_PRE] = P * 4;
   sz[B_TOK_IDX] = R * P * 4;
@@ -105,8 +96,8 @@ int validate_config(const tlf_config* c) {
     return TLF_E_INVALID_ARG;
   }
   if (!(c->rms_eps > 0.f) || !std::isfinite(c->rms_eps)) return TLF_E_INVALID_ARG;
-  // compact row index and chunk index share one int32 in the attention work list
-  if (c->max_batch > 0xFFFF) return TLF_E_INVALID_ARG;
+  // the decode attention stages one sequence's page list in LDS
+  if (ceil_div(c->max_pos, kPage) > kAttnMaxPages) return TLF_E_INVALID_ARG;
   // positions, row indices and work-list offsets are int32
   if ((int64_t)std::max(c->max_prefill_tokens, c->max_pos) * std::max(c->d_ff, 3 * c->d_model) > INT32_MAX)
     return TLF_E_INVALID_ARG;
@@ -136,7 +127,38 @@ struct tlf_ctx {
   int batch = 0, seq_len = 0;
   bool prefilled = false, poisoned = false;
   int sticky = TLF_OK;
-  int attn_grid = 0;
+  int cus = 0;  // compute units of the device
+  int attn_blocks[2] = {1, 1};  // resident decode-attention workgroups per CU (4 and 8 waves)
+  // measurement: event pairs around decode-attention launches, resolved by tlf_cache_stats
+  bool profiling = false;
+  std::vector<hipEvent_t> event_pool;
+  struct Timed { hipEvent_t start, stop; bool attn; };
+  std::vector<Timed> event_pending;
+  int64_t attn_launches = 0;
+  double attn_ms = 0.0, block_ms = 0.0;
+
+  ~tlf_ctx() {
+    recycle_events();
+    for (hipEvent_t e : event_pool) (void)hipEventDestroy(e);
+  }
+  void recycle_events() {
+    for (auto& t : event_pending) { event_pool.push_back(t.start); event_pool.push_back(t.stop); }
+    event_pending.clear();
+  }
+  // records the first event of a timed region; the caller records .stop after the work
+  hipError_t begin_timed(hipStream_t s, bool attn) {
+    Timed t{nullptr, nullptr, attn};
+    hipError_t e = take_event(&t.start);
+    if (e == hipSuccess) e = take_event(&t.stop);
+    if (e == hipSuccess) e = hipEventRecord(t.start, s);
+    if (e == hipSuccess) event_pending.push_back(t);
+    return e;
+  }
+  hipError_t end_timed(hipStream_t s) { return hipEventRecord(event_pending.back().stop, s); }
+  hipError_t take_event(hipEvent_t* e) {
+    if (!event_pool.empty()) { *e = event_pool.back(); event_pool.pop_back(); return hipSuccess; }
+    return hipEventCreate(e);
+  }
 
   template <typename P> P* buf(Buf b) const { return reinterpret_cast<P*>(ws + L.off[b]); }
 };
@@ -157,6 +179,14 @@ int precheck(tlf_ctx* ctx) {
   if (ctx->poisoned) return TLF_E_STATE;
   if (ctx->sticky != TLF_OK) return ctx->sticky;
   return TLF_OK;
+}
+
+// Waves sharing one (row, head) in the decode attention: enough waves in
+// flight to cover the device even when batch x heads is small.
+int attn_waves(const tlf_ctx* ctx) {
+  const int64_t units = (int64_t)ctx->batch * ctx->cfg.n_heads;
+  const int64_t slots = (int64_t)ctx->cus * ctx->attn_blocks[0] * 4;  // resident waves with 4-wave groups
+  return units * 4 >= slots ? 4 : 8;
 }
 
 const void* head_weights(const tlf_ctx* ctx) { return ctx->w.lm_head ? ctx->w.lm_head : ctx->w.tok_emb; }
@@ -260,13 +290,18 @@ int run_decode(tlf_ctx* ctx, const int32_t* tokens, float* logits, int32_t* next
 
   DecodePlanArgs pa;
   pa.c = ctx->cv; pa.B = B; pa.depth = ctx->buf<int32_t>(B_DEPTH_DEC); pa.perm = perm; pa.nact = nact;
-  pa.units = ctx->buf<int32_t>(B_UNITS); pa.units_cap = ctx->L.units_cap;
-  pa.unit_count = ctx->buf<int32_t>(B_UNIT_COUNT); pa.chunk_tokens = ctx->buf<int32_t>(B_CHUNK_TOKENS);
-  pa.nchunks = ctx->buf<int32_t>(B_NCHUNKS); pa.max_batch = c.max_batch; pa.max_chunks = ctx->L.max_chunks;
   pa.argmax_keys = ctx->buf<unsigned long long>(B_KEYS);
   pa.kv_entry_bytes = (int64_t)c.n_layers * 2 * c.d_model * ctx->L.s;
   TLF_HIP(launch_plan_decode(pa, s));
 
+  // the block region (every loop and layer) is timed as a whole when profiling;
+  // the attention launches inside it get their own event pairs
+  hipEvent_t block_start = nullptr, block_stop = nullptr;
+  if (ctx->profiling) {
+    TLF_HIP(ctx->take_event(&block_start));
+    TLF_HIP(ctx->take_event(&block_stop));
+    TLF_HIP(hipEventRecord(block_start, s));
+  }
   for (int i = 0; i < R; ++i) {
     RowMap rm;
     rm.src = perm; rm.nact = nact + i; rm.rows = B;
@@ -280,17 +315,18 @@ int run_decode(tlf_ctx* ctx, const int32_t* tokens, float* logits, int32_t* next
       TLF_HIP(launch_gemm<T>(q, A_NORM, E_QKV, false, s));
 
       AttnDecodeArgs at;
-      at.c = ctx->cv; at.loop = i; at.layer = j; at.d = d; at.perm = perm;
+      at.c = ctx->cv; at.loop = i; at.layer = j; at.d = d; at.perm = perm; at.nact = nact + i;
       at.q = ctx->buf<void>(B_Q_DEC); at.o = ctx->buf<void>(B_O_DEC);
-      at.units = ctx->buf<int32_t>(B_UNITS) + (int64_t)i * ctx->L.units_cap;
-      at.unit_count = ctx->buf<int32_t>(B_UNIT_COUNT) + i;
-      at.chunk_tokens = ctx->buf<int32_t>(B_CHUNK_TOKENS) + i;
-      at.nchunks = ctx->buf<int32_t>(B_NCHUNKS) + (int64_t)i * c.max_batch;
-      at.partial = ctx->buf<float>(B_PARTIAL); at.counters = ctx->buf<int32_t>(B_COUNTERS);
-      at.max_chunks = ctx->L.max_chunks;
       at.scale_log2 = 1.4426950408889634f / std::sqrt((float)c.head_dim);
-      at.grid = ctx->attn_grid;
-      TLF_HIP(launch_attn_decode<T>(at, s));
+      at.waves = attn_waves(ctx);
+      at.grid = ctx->cus * ctx->attn_blocks[at.waves == 4 ? 0 : 1];
+      if (ctx->profiling) {
+        TLF_HIP(ctx->begin_timed(s, true));
+        TLF_HIP(launch_attn_decode<T>(at, s));
+        TLF_HIP(ctx->end_timed(s));
+      } else {
+        TLF_HIP(launch_attn_decode<T>(at, s));
+      }
 
       GemmArgs o;
       o.A = ctx->buf<void>(B_O_DEC); o.lda = d; o.W = lw.w_o; o.N = d; o.K = d; o.w_rows = d; o.rm = rc;
@@ -307,6 +343,10 @@ int run_decode(tlf_ctx* ctx, const int32_t* tokens, float* logits, int32_t* next
       dn.rm = rc; dn.out = x; dn.ldo = d;
       TLF_HIP(launch_gemm<T>(dn, A_BUF, E_RESID, false, s));
     }
+  }
+  if (ctx->profiling) {
+    TLF_HIP(hipEventRecord(block_stop, s));
+    ctx->event_pending.push_back(tlf_ctx::Timed{block_start, block_stop, false});
   }
   GemmArgs hd;
   hd.A = x; hd.lda = d; hd.W = head_weights(ctx); hd.N = c.vocab; hd.K = d; hd.w_rows = c.vocab;
@@ -372,7 +412,14 @@ int tlf_init(const tlf_config* cfg, const tlf_weights* w, void* d_workspace, siz
   hipError_t e = hipGetDevice(&dev);
   if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
   if (e != hipSuccess) { delete ctx; return TLF_E_HIP; }
-  ctx->attn_grid = std::max(1, cus) * 8;
+  ctx->cus = std::max(1, cus);
+  for (int k = 0; k < 2 && e == hipSuccess; ++k) {
+    int blocks = 0;
+    e = cfg->dtype == TLF_DTYPE_BF16 ? attn_decode_blocks_per_cu<bf16>(cfg->head_dim, 4 << k, &blocks)
+                                     : attn_decode_blocks_per_cu<float>(cfg->head_dim, 4 << k, &blocks);
+    ctx->attn_blocks[k] = std::max(1, blocks);
+  }
+  if (e != hipSuccess) { delete ctx; return TLF_E_HIP; }
 
   // Free pages are NaN-poisoned: a read of a slot that was never written
   // turns the logits into NaN instead of silently using stale values.
@@ -386,8 +433,6 @@ int tlf_init(const tlf_config* cfg, const tlf_weights* w, void* d_workspace, siz
   if (e == hipSuccess) e = launch_fill_i32(cv.page_next, 0, 2, s);
   if (e == hipSuccess) e = launch_fill_u64(cv.depth_hist, 0ull, cfg->max_loops, s);
   if (e == hipSuccess) e = launch_fill_u64(reinterpret_cast<unsigned long long*>(cv.step_stats), 0ull, kStatCount, s);
-  if (e == hipSuccess)
-    e = launch_fill_i32(ctx->buf<int32_t>(B_COUNTERS), 0, (int64_t)cfg->max_batch * cfg->n_heads, s);
   if (e != hipSuccess) { delete ctx; return TLF_E_HIP; }
   *out = ctx;
   return TLF_OK;
@@ -464,6 +509,25 @@ int tlf_cache_stats(tlf_ctx* ctx, tlf_cache_stats_t* out, int32_t* h_len, int32_
   const int64_t block_params = 4LL * c.d_model * c.d_model + 3LL * c.d_model * c.d_ff;
   out->last_step_weight_bytes = stats[kStatLoops] * c.n_layers * block_params * ctx->L.s +
                                 (int64_t)c.vocab * c.d_model * ctx->L.s + (int64_t)R * c.d_model * 4;
+  for (auto& t : ctx->event_pending) {
+    float ms = 0.f;
+    e = hipEventElapsedTime(&ms, t.start, t.stop);
+    if (e != hipSuccess) { ctx->poisoned = true; return TLF_E_HIP; }
+    if (t.attn) {
+      ctx->attn_ms += ms;
+      ctx->attn_launches += 1;
+    } else {
+      ctx->block_ms += ms;
+    }
+  }
+  ctx->recycle_events();
+  out->decode_steps = stats[kStatStepsTotal];
+  out->attn_launches = ctx->attn_launches;
+  out->attn_algo_bytes = stats[kStatAttnBytesTotal];
+  out->attn_ms = ctx->attn_ms;
+  out->kv_write_bytes_total = stats[kStatKvWriteTotal];
+  out->loops_executed_total = stats[kStatLoopsTotal];
+  out->block_ms = ctx->block_ms;
   out->device_error = device_status(scal[1]);
   if (out->device_error != TLF_OK) ctx->sticky = out->device_error;
 
@@ -489,6 +553,23 @@ int tlf_cache_stats(tlf_ctx* ctx, tlf_cache_stats_t* out, int32_t* h_len, int32_
       }
   }
   return out->device_error;
+}
+
+int tlf_set_profiling(tlf_ctx* ctx, int enable) {
+  if (!ctx) return TLF_E_INVALID_ARG;
+  if (ctx->poisoned) return TLF_E_STATE;
+  if (enable) {
+    // reset the totals: cumulative device counters and the host-side sums
+    static_assert(kStatLoopsTotal == kStatAttnBytesTotal + 3, "cumulative counters are contiguous");
+    TLF_HIP(launch_fill_u64(reinterpret_cast<unsigned long long*>(ctx->cv.step_stats) + kStatAttnBytesTotal, 0ull,
+                            4, ctx->stream));
+    ctx->attn_launches = 0;
+    ctx->attn_ms = 0.0;
+    ctx->block_ms = 0.0;
+    ctx->recycle_events();
+  }
+  ctx->profiling = enable != 0;
+  return TLF_OK;
 }
 
 void tlf_destroy(tlf_ctx* ctx) {

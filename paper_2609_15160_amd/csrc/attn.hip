@@ -2,12 +2,13 @@
 //
 // Decode: a query at loop i reads only cache (b, i), i.e. the earlier tokens
 // of its sequence whose depth is >= i plus itself; exited tokens have no
-// slot, so the validity mask is implicit.  Each (row, head, chunk of pages)
-// is one wave-unit of a persistent grid; K and V stream from HBM in 16-byte
-// loads (G lanes per token, 64/G tokens per instruction, U tokens per lane in
-// flight), every lane keeps its own online-softmax state, lanes merge with
-// shuffles, and chunks of one (row, head) merge through a log-sum-exp
-// combine done by the last-arriving wave.
+// slot, so the validity mask is implicit.  One workgroup of W waves owns a
+// (row, head) of a persistent grid; its page list is staged in LDS, each wave
+// streams a contiguous share of the entries in 16-byte K/V loads (G lanes per
+// token, 64/G tokens per instruction) with two register batches in flight,
+// every lane keeps its own online-softmax state, lanes merge with DPP moves
+// and shuffles, and the W waves merge through LDS with a log-sum-exp combine.
+// No state crosses workgroups, so no device-scope fence is needed.
 //
 // Prefill: causal attention among the gathered tokens of each loop (Section
 // 3.3), which in compact order is a plain causal mask on the (b, i) slot
@@ -26,35 +27,56 @@ __device__ __forceinline__ float merge_scale(float m, float mn) {
   return m == kNegInf ? 0.f : exp2f(m - mn);
 }
 
-template <typename T, int D>
-__global__ __launch_bounds__(256) void k_attn_decode(AttnDecodeArgs a) {
+// Sum over aligned groups of G lanes (G = 2, 4, 8, 16, 32) with DPP moves
+// inside rows of 16 lanes and a shuffle beyond them.
+template <int CTRL>
+__device__ __forceinline__ float dpp_mov(float x) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, 0xF, 0xF, false));
+}
+
+template <int G>
+__device__ __forceinline__ float group_sum(float v) {
+  if constexpr (G >= 2) v += dpp_mov<0xB1>(v);   // quad_perm [1,0,3,2]: partner lane ^ 1
+  if constexpr (G >= 4) v += dpp_mov<0x4E>(v);   // quad_perm [2,3,0,1]: partner lane ^ 2
+  if constexpr (G >= 8) v += dpp_mov<0x141>(v);  // row_half_mirror: the other quad of the 8
+  if constexpr (G >= 16) v += dpp_mov<0x140>(v); // row_mirror: the other half of the 16
+  if constexpr (G >= 32) v += shfl_xor(v, 16);
+  return v;
+}
+
+template <typename T, int D, int W>
+__global__ __launch_bounds__(W * 64) void k_attn_decode(AttnDecodeArgs a) {
   constexpr int EPL = 16 / (int)sizeof(T);  // elements per 16-byte load
   constexpr int G = D / EPL;                // lanes per token
   constexpr int TPI = kWave / G;            // tokens per wave instruction
-  constexpr int U = 8;                      // tokens per lane per iteration
-  static_assert(G >= 1 && G <= kWave && kWave % G == 0, "head_dim split");
+  constexpr int U = 4;                      // tokens per lane per load batch
+  constexpr int STEP = U * TPI;             // tokens per wave per batch
+  static_assert(G >= 1 && G <= 32 && kWave % G == 0, "head_dim split");
+  __shared__ int s_pages[kAttnMaxPages];
+  __shared__ float s_red[W][D + 2];
 
   const CacheView& c = a.c;
-  const int lane = lane_id();
+  const int lane = lane_id(), w = threadIdx.x >> 6;
   const int tr = lane / G, gl = lane % G;
   const int H = c.H, R = c.R, i = a.loop;
-  const int nunits = *a.unit_count * H;
-  const int CT = *a.chunk_tokens;
-  const int nwaves = gridDim.x * 4;
+  const int nunits = *a.nact * H;
   const T* pool = reinterpret_cast<const T*>(c.pool);
 
-  for (int u = blockIdx.x * 4 + (threadIdx.x >> 6); u < nunits; u += nwaves) {
-    const int ent = a.units[u / H];
-    const int h = u % H;
-    const int k = ent & 0xFFFF, ch = ent >> 16;
+  for (int u = blockIdx.x; u < nunits; u += gridDim.x) {
+    const int k = u / H, h = u % H;
     const int b = a.perm[k];
     const int L = c.cache_len[b * R + i];
-    const int t0 = ch * CT;
-    const int t1 = min(L, t0 + CT);
+    const int np = (L + kPage - 1) / kPage;
     const int32_t* pt = c.page_table + ((int64_t)b * R + i) * c.pages_per_seq;
+    __syncthreads();  // the previous unit is done with s_pages and s_red
+    for (int p = threadIdx.x; p < np; p += W * kWave) s_pages[p] = pt[p];
+    __syncthreads();
+
+    // this wave's contiguous share of the L entries
+    const int per = ((L + W - 1) / W + TPI - 1) / TPI * TPI;
+    const int t0 = w * per, t1 = min(L, t0 + per);
     const int64_t koff = page_off(c, a.layer, 0, h, 0) + gl * EPL;
     const int64_t voff = page_off(c, a.layer, 1, h, 0) + gl * EPL;
-
     const V16<T> qv = ld16(reinterpret_cast<const T*>(a.q) + (int64_t)k * a.d + h * D + gl * EPL);
     float qf[EPL];
 #pragma unroll
@@ -64,44 +86,54 @@ __global__ __launch_bounds__(256) void k_attn_decode(AttnDecodeArgs a) {
 #pragma unroll
     for (int e = 0; e < EPL; ++e) acc[e] = 0.f;
 
-    for (int tb = t0; tb < t1; tb += U * TPI) {
-      V16<T> kr[U], vr[U];
-      bool ok[U];
+    auto load = [&](V16<T>* kr, V16<T>* vr, int tb) {
 #pragma unroll
       for (int uu = 0; uu < U; ++uu) {
         const int t = tb + uu * TPI + tr;
-        ok[uu] = t < t1;
-        const int tt = ok[uu] ? t : t0;  // masked lanes read a valid slot
-        const int64_t base = (int64_t)pt[tt / kPage] * c.page_elems + (tt % kPage) * D;
+        const int tt = t < t1 ? t : t0;  // lanes past the end read a valid slot
+        const int64_t base = (int64_t)s_pages[tt >> 4] * c.page_elems + (tt & (kPage - 1)) * D;
         kr[uu] = ld16(pool + base + koff);
         vr[uu] = ld16(pool + base + voff);
       }
+    };
+    auto consume = [&](const V16<T>* kr, const V16<T>* vr, int tb) {
       float s[U];
+      float mx = m;
 #pragma unroll
       for (int uu = 0; uu < U; ++uu) {
         float d = 0.f;
 #pragma unroll
-        for (int e = 0; e < EPL; ++e) d += qf[e] * to_f<T>(kr[uu].e[e]);
-#pragma unroll
-        for (int o = 1; o < G; o <<= 1) d += shfl_xor(d, o);
-        s[uu] = ok[uu] ? d : kNegInf;
+        for (int e = 0; e < EPL; ++e) d = fmaf(qf[e], to_f<T>(kr[uu].e[e]), d);
+        d = group_sum<G>(d);
+        s[uu] = (tb + uu * TPI + tr < t1) ? d : kNegInf;
+        mx = fmaxf(mx, s[uu]);
       }
-      float mx = m;
+      if (mx != kNegInf) {
+        const float alpha = merge_scale(m, mx);
+        l *= alpha;
 #pragma unroll
-      for (int uu = 0; uu < U; ++uu) mx = fmaxf(mx, s[uu]);
-      if (mx == kNegInf) continue;  // nothing valid for this lane yet
-      const float alpha = merge_scale(m, mx);
-      l *= alpha;
+        for (int e = 0; e < EPL; ++e) acc[e] *= alpha;
 #pragma unroll
-      for (int e = 0; e < EPL; ++e) acc[e] *= alpha;
+        for (int uu = 0; uu < U; ++uu) {
+          const float p = exp2f(s[uu] - mx);  // exp2(-inf) = 0 for masked slots
+          l += p;
 #pragma unroll
-      for (int uu = 0; uu < U; ++uu) {
-        const float p = ok[uu] ? exp2f(s[uu] - mx) : 0.f;
-        l += p;
-#pragma unroll
-        for (int e = 0; e < EPL; ++e) acc[e] += p * to_f<T>(vr[uu].e[e]);
+          for (int e = 0; e < EPL; ++e) acc[e] = fmaf(p, to_f<T>(vr[uu].e[e]), acc[e]);
+        }
+        m = mx;
       }
-      m = mx;
+    };
+    if (t0 < t1) {
+      // two register batches in flight: the next batch loads while this one is consumed
+      V16<T> ka[U], va[U], kb[U], vb[U];
+      load(ka, va, t0);
+      for (int tb = t0; tb < t1; tb += 2 * STEP) {
+        if (tb + STEP < t1) load(kb, vb, tb + STEP);
+        consume(ka, va, tb);
+        if (tb + STEP >= t1) break;
+        if (tb + 2 * STEP < t1) load(ka, va, tb + 2 * STEP);
+        consume(kb, vb, tb + STEP);
+      }
     }
     // merge the TPI token slots that share this lane's dimension slice
 #pragma unroll
@@ -114,54 +146,33 @@ __global__ __launch_bounds__(256) void k_attn_decode(AttnDecodeArgs a) {
       for (int e = 0; e < EPL; ++e) acc[e] = acc[e] * a1 + shfl_xor(acc[e], o) * a2;
       m = mn;
     }
-    const int nc = a.nchunks[k];
-    T* orow = reinterpret_cast<T*>(a.o) + (int64_t)k * a.d + h * D + gl * EPL;
-    if (nc == 1) {
-      if (tr == 0) {
-        V16<T> ov;
-        const float inv = 1.f / l;
-#pragma unroll
-        for (int e = 0; e < EPL; ++e) ov.e[e] = from_f<T>(acc[e] * inv);
-        st16(orow, ov);
-      }
-      continue;
-    }
-    const int64_t pstride = D + 2;
-    float* part = a.partial + (((int64_t)k * H + h) * a.max_chunks + ch) * pstride;
     if (tr == 0) {
 #pragma unroll
-      for (int e = 0; e < EPL; ++e) part[2 + gl * EPL + e] = acc[e];
-      if (gl == 0) { part[0] = m; part[1] = l; }
+      for (int e = 0; e < EPL; ++e) s_red[w][2 + gl * EPL + e] = acc[e];
+      if (gl == 0) { s_red[w][0] = m; s_red[w][1] = l; }
     }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-    int old = 0;
-    if (lane == 0)
-      old = __hip_atomic_fetch_add(&a.counters[k * H + h], 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
-    old = __shfl(old, 0, kWave);
-    if (old != nc - 1) continue;
-    // last chunk of this (row, head) to finish: merge all partials
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-    if (tr == 0) {
+    __syncthreads();
+    // merge the W waves' partial softmax states (log-sum-exp) and write o
+    if (w == 0 && tr == 0) {
       float M = kNegInf, Ls = 0.f, O[EPL];
 #pragma unroll
       for (int e = 0; e < EPL; ++e) O[e] = 0.f;
-      const float* pp = a.partial + ((int64_t)k * H + h) * a.max_chunks * pstride;
-      for (int cc = 0; cc < nc; ++cc, pp += pstride) {
-        const float mc = pp[0], lc = pp[1];
+#pragma unroll
+      for (int ww = 0; ww < W; ++ww) {
+        const float mc = s_red[ww][0], lc = s_red[ww][1];
         const float mn = fmaxf(M, mc);
         const float a1 = merge_scale(M, mn), a2 = merge_scale(mc, mn);
         Ls = Ls * a1 + lc * a2;
 #pragma unroll
-        for (int e = 0; e < EPL; ++e) O[e] = O[e] * a1 + pp[2 + gl * EPL + e] * a2;
+        for (int e = 0; e < EPL; ++e) O[e] = O[e] * a1 + s_red[ww][2 + gl * EPL + e] * a2;
         M = mn;
       }
       V16<T> ov;
       const float inv = 1.f / Ls;
 #pragma unroll
       for (int e = 0; e < EPL; ++e) ov.e[e] = from_f<T>(O[e] * inv);
-      st16(orow, ov);
+      st16(reinterpret_cast<T*>(a.o) + (int64_t)k * a.d + h * D + gl * EPL, ov);
     }
-    if (lane == 0) __hip_atomic_store(&a.counters[k * H + h], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
 }
 
@@ -298,22 +309,48 @@ __global__ __launch_bounds__(256) void k_attn_prefill(AttnPrefillArgs a) {
 
 }  // namespace
 
-template <typename T>
-hipError_t launch_attn_decode(const AttnDecodeArgs& a, hipStream_t s) {
-  const dim3 grid(a.grid > 0 ? a.grid : 1), block(256);
-  switch (a.c.D) {
-    case 16:
-      if constexpr (sizeof(T) == 4) {
-        hipLaunchKernelGGL((k_attn_decode<T, 16>), grid, block, 0, s, a);
-        break;
-      } else {
-        return hipErrorInvalidValue;
-      }
-    case 64: hipLaunchKernelGGL((k_attn_decode<T, 64>), grid, block, 0, s, a); break;
-    case 128: hipLaunchKernelGGL((k_attn_decode<T, 128>), grid, block, 0, s, a); break;
+template <typename T, int D>
+hipError_t launch_decode_d(const AttnDecodeArgs& a, hipStream_t s) {
+  const dim3 grid(a.grid > 0 ? a.grid : 1);
+  switch (a.waves) {
+    case 4: hipLaunchKernelGGL((k_attn_decode<T, D, 4>), grid, dim3(256), 0, s, a); break;
+    case 8: hipLaunchKernelGGL((k_attn_decode<T, D, 8>), grid, dim3(512), 0, s, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
+}
+
+template <typename T, int D>
+hipError_t occupancy_d(int waves, int* blocks) {
+  switch (waves) {
+    case 4: return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, k_attn_decode<T, D, 4>, 256, 0);
+    case 8: return hipOccupancyMaxActiveBlocksPerMultiprocessor(blocks, k_attn_decode<T, D, 8>, 512, 0);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+template <typename T>
+hipError_t launch_attn_decode(const AttnDecodeArgs& a, hipStream_t s) {
+  switch (a.c.D) {
+    case 16:
+      if constexpr (sizeof(T) == 4) return launch_decode_d<T, 16>(a, s);
+      return hipErrorInvalidValue;
+    case 64: return launch_decode_d<T, 64>(a, s);
+    case 128: return launch_decode_d<T, 128>(a, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+template <typename T>
+hipError_t attn_decode_blocks_per_cu(int D, int waves, int* blocks) {
+  switch (D) {
+    case 16:
+      if constexpr (sizeof(T) == 4) return occupancy_d<T, 16>(waves, blocks);
+      return hipErrorInvalidValue;
+    case 64: return occupancy_d<T, 64>(waves, blocks);
+    case 128: return occupancy_d<T, 128>(waves, blocks);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 template <typename T>
@@ -337,6 +374,8 @@ hipError_t launch_attn_prefill(const AttnPrefillArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
+template hipError_t attn_decode_blocks_per_cu<float>(int, int, int*);
+template hipError_t attn_decode_blocks_per_cu<bf16>(int, int, int*);
 template hipError_t launch_attn_decode<float>(const AttnDecodeArgs&, hipStream_t);
 template hipError_t launch_attn_decode<bf16>(const AttnDecodeArgs&, hipStream_t);
 template hipError_t launch_attn_prefill<float>(const AttnPrefillArgs&, hipStream_t);

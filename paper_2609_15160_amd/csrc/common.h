@@ -14,8 +14,7 @@ constexpr int kPage = 16;          // tokens per KV page
 constexpr int kWave = 64;          // CDNA wavefront width
 constexpr int kMaxLoops = 16;
 constexpr int kPlanThreads = 1024; // single-workgroup planners
-constexpr int kMinChunkPages = 4;  // smallest split-K chunk of the decode attention
-constexpr int kAttnWaveTarget = 4096; // wave-units the decode attention aims to expose per launch
+constexpr int kAttnMaxPages = 4096; // page list staged in LDS by the decode attention (max_pos <= 65536)
 
 // Sticky device error bits (reported through tlf_cache_stats).
 constexpr int kErrBadToken = 1;
@@ -26,7 +25,11 @@ enum StepStat {
   kStatKvRead = 0,
   kStatKvWrite = 1,
   kStatLoops = 2,
-  kStatRows = 3,   // kStatRows + i: n_i of the step, i < kMaxLoops
+  kStatAttnBytesTotal = 3,  // cumulative algorithmic bytes of the decode attention
+  kStatStepsTotal = 4,      // cumulative decode steps
+  kStatKvWriteTotal = 5,    // cumulative bytes of appended k, v
+  kStatLoopsTotal = 6,      // cumulative executed loops (shared block applications)
+  kStatRows = 7,            // kStatRows + i: n_i of the step, i < kMaxLoops
   kStatCount = kStatRows + kMaxLoops
 };
 

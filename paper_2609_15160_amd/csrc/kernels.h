@@ -91,8 +91,7 @@ template <typename T> hipError_t launch_embed_route(const EmbedArgs& a, hipStrea
 
 // ---------------------------------------------------------------------------
 // Decode planner (one workgroup): depth-sorted row order, active counts n_i,
-// page allocation and slot bookkeeping for every executed (b, i), statistics,
-// and the split-K work list of the decode attention.
+// page allocation and slot bookkeeping for every executed (b, i), statistics.
 // ---------------------------------------------------------------------------
 struct DecodePlanArgs {
   CacheView c;
@@ -100,12 +99,6 @@ struct DecodePlanArgs {
   const int32_t* depth = nullptr;
   int32_t* perm = nullptr;         // [B]
   int32_t* nact = nullptr;         // [R]
-  int32_t* units = nullptr;        // [R][units_cap] (row k | chunk << 16)
-  int units_cap = 0;
-  int32_t* unit_count = nullptr;   // [R]
-  int32_t* chunk_tokens = nullptr; // [R]
-  int32_t* nchunks = nullptr;      // [R][max_batch]
-  int max_batch = 0, max_chunks = 0;
   unsigned long long* argmax_keys = nullptr; // [B] cleared for the LM head
   int64_t kv_entry_bytes = 0;      // bytes of one (token, loop) cache entry over all layers
 };
@@ -127,20 +120,17 @@ hipError_t launch_plan_prefill(const PrefillPlanArgs& a, hipStream_t s);
 struct AttnDecodeArgs {
   CacheView c;
   int loop = 0, layer = 0, d = 0;
-  const int32_t* perm = nullptr;
+  const int32_t* perm = nullptr;   // depth-sorted row order
+  const int32_t* nact = nullptr;   // n_i of this loop: rows [0, n_i) are active
   const void* q = nullptr;         // [rows][d] compact rows
   void* o = nullptr;               // [rows][d]
-  const int32_t* units = nullptr;  // this loop's work list
-  const int32_t* unit_count = nullptr;
-  const int32_t* chunk_tokens = nullptr;
-  const int32_t* nchunks = nullptr; // this loop's per-row chunk counts
-  float* partial = nullptr;        // [max_batch][H][max_chunks][D + 2]
-  int32_t* counters = nullptr;     // [max_batch][H], zero between launches
-  int max_chunks = 0;
   float scale_log2 = 0.f;          // log2(e) / sqrt(D)
-  int grid = 0;
+  int grid = 0;                    // persistent workgroups
+  int waves = 4;                   // waves per workgroup sharing one (row, head): 4 or 8
 };
 template <typename T> hipError_t launch_attn_decode(const AttnDecodeArgs& a, hipStream_t s);
+// Resident workgroups per compute unit of the decode attention (4 or 8 waves each).
+template <typename T> hipError_t attn_decode_blocks_per_cu(int D, int waves, int* blocks);
 
 struct AttnPrefillArgs {
   CacheView c;

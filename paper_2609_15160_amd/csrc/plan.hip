@@ -89,9 +89,9 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan_decode(DecodePlanArgs a) 
   __shared__ int start[kMaxLoops + 1];
   __shared__ int fill[kMaxLoops + 1];
   __shared__ int scan_tmp[kPlanThreads / kWave + 1];
-  __shared__ int s_carry, s_total, s_oom, s_chunk;
+  __shared__ int s_carry, s_total, s_oom;
   __shared__ unsigned long long hist[kMaxLoops];
-  __shared__ unsigned long long s_kvread, s_kvwrite, s_pages_i;
+  __shared__ unsigned long long s_kvread, s_kvwrite;
   __shared__ int s_maxm;
 
   if (tid <= kMaxLoops) { cnt[tid] = 0; fill[tid] = 0; }
@@ -184,51 +184,24 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan_decode(DecodePlanArgs a) 
     c.step_stats[kStatKvRead] = (long long)(s_kvread * (unsigned long long)a.kv_entry_bytes);
     c.step_stats[kStatKvWrite] = (long long)(s_kvwrite * (unsigned long long)a.kv_entry_bytes);
     c.step_stats[kStatLoops] = s_maxm;
+    c.step_stats[kStatStepsTotal] += 1;
+    c.step_stats[kStatKvWriteTotal] += (long long)(s_kvwrite * (unsigned long long)a.kv_entry_bytes);
+    c.step_stats[kStatLoopsTotal] += s_maxm;
+    if (!s_oom) {
+      // each executed (loop, layer) attention reads every valid entry of its
+      // cache plus one q row and writes one o row per active token; summed
+      // over layers: entry bytes times (entries read + active rows)
+      unsigned long long rows = 0;
+      for (int i = 0; i < R; ++i) rows += (unsigned long long)(start[i + 1] + cnt[i + 1]);
+      c.step_stats[kStatAttnBytesTotal] += (long long)((s_kvread + rows) * (unsigned long long)a.kv_entry_bytes);
+    }
   }
-  if (s_oom) {  // the step becomes a no-op for the block: no rows, no attention work
-    if (tid < R) { a.nact[tid] = 0; a.unit_count[tid] = 0; }
+  if (s_oom) {  // the step becomes a no-op for the block: no active rows
+    if (tid < R) a.nact[tid] = 0;
   }
   __syncthreads();
   if (tid < R) c.step_stats[kStatRows + tid] = a.nact[tid];
 
-  // 3. split-K work list of the decode attention, per loop
-  for (int i = 0; i < R; ++i) {
-    const int n = a.nact[i];
-    if (tid == 0) s_pages_i = 0ull;
-    __syncthreads();
-    for (int k = tid; k < n; k += kPlanThreads) {
-      const int L = c.cache_len[a.perm[k] * R + i];
-      atomicAdd(&s_pages_i, (unsigned long long)((L + kPage - 1) / kPage));
-    }
-    __syncthreads();
-    if (tid == 0) {
-      const unsigned long long want = (s_pages_i * (unsigned long long)c.H + kAttnWaveTarget - 1) / kAttnWaveTarget;
-      int cp = (int)want;
-      if (cp < kMinChunkPages) cp = kMinChunkPages;
-      s_chunk = cp * kPage;
-      a.chunk_tokens[i] = s_chunk;
-      s_carry = 0;
-    }
-    __syncthreads();
-    const int ct = s_chunk;
-    for (int k0 = 0; k0 < n; k0 += kPlanThreads) {
-      const int k = k0 + tid;
-      int nc = 0;
-      if (k < n) nc = (c.cache_len[a.perm[k] * R + i] + ct - 1) / ct;
-      int tot;
-      const int ex = block_exclusive_scan(nc, scan_tmp, &tot);
-      if (k < n) {
-        a.nchunks[(int64_t)i * a.max_batch + k] = nc;
-        int32_t* u = a.units + (int64_t)i * a.units_cap + s_carry + ex;
-        for (int ch = 0; ch < nc; ++ch) u[ch] = k | (ch << 16);
-      }
-      __syncthreads();
-      if (tid == 0) s_carry += tot;
-      __syncthreads();
-    }
-    if (tid == 0) a.unit_count[i] = s_carry;
-    __syncthreads();
-  }
   for (int b = tid; b < B; b += kPlanThreads) a.argmax_keys[b] = 0ull;
 }
 

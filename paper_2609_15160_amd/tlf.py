@@ -67,11 +67,15 @@ class CacheStats(ctypes.Structure):
         ("seq_len", ctypes.c_int64), ("last_step_kv_read_bytes", ctypes.c_int64),
         ("last_step_kv_write_bytes", ctypes.c_int64), ("last_step_weight_bytes", ctypes.c_int64),
         ("last_step_loops_executed", ctypes.c_int64), ("last_step_active_rows", ctypes.c_int64 * MAX_LOOPS),
+        ("decode_steps", ctypes.c_int64), ("attn_launches", ctypes.c_int64), ("attn_algo_bytes", ctypes.c_int64),
+        ("attn_ms", ctypes.c_double), ("kv_write_bytes_total", ctypes.c_int64),
+        ("loops_executed_total", ctypes.c_int64), ("block_ms", ctypes.c_double),
         ("device_error", ctypes.c_int32), ("reserved", ctypes.c_int32),
     ]
 
 
-EXPORTS = ("tlf_init", "tlf_prefill", "tlf_decode_step", "tlf_cache_stats", "tlf_destroy", "tlf_status_str")
+EXPORTS = ("tlf_init", "tlf_prefill", "tlf_decode_step", "tlf_cache_stats", "tlf_set_profiling", "tlf_destroy",
+           "tlf_status_str")
 
 
 def header_exports(path: str = HEADER):
@@ -107,6 +111,8 @@ def load(path: str = LIB_PATH):
     lib.tlf_decode_step.restype = ctypes.c_int
     lib.tlf_cache_stats.argtypes = [vp, ctypes.POINTER(CacheStats), vp, vp, ctypes.c_size_t]
     lib.tlf_cache_stats.restype = ctypes.c_int
+    lib.tlf_set_profiling.argtypes = [vp, ctypes.c_int]
+    lib.tlf_set_profiling.restype = ctypes.c_int
     lib.tlf_destroy.argtypes = [vp]
     lib.tlf_destroy.restype = None
     lib.tlf_status_str.argtypes = [ctypes.c_int]
@@ -270,6 +276,9 @@ class Session:
             res["lens"] = lens[: self.batch]
             res["index"] = index
         return res
+
+    def set_profiling(self, enable: bool) -> None:
+        self._check(self.lib.tlf_set_profiling(self.ctx, 1 if enable else 0), "tlf_set_profiling")
 
     def close(self) -> None:
         if getattr(self, "ctx", None):

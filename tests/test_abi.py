@@ -34,8 +34,9 @@ def test_struct_layouts_match_the_header():
 int main(void) {
   printf("%zu %zu %zu %zu\n", sizeof(tlf_config), sizeof(tlf_layer_weights), sizeof(tlf_weights),
          sizeof(tlf_cache_stats_t));
-  printf("%zu %zu %zu %zu\n", offsetof(tlf_config, rms_eps), offsetof(tlf_weights, layers),
-         offsetof(tlf_cache_stats_t, last_step_active_rows), offsetof(tlf_cache_stats_t, device_error));
+  printf("%zu %zu %zu %zu %zu\n", offsetof(tlf_config, rms_eps), offsetof(tlf_weights, layers),
+         offsetof(tlf_cache_stats_t, last_step_active_rows), offsetof(tlf_cache_stats_t, device_error),
+         offsetof(tlf_cache_stats_t, attn_ms));
   return 0;
 }
 """
@@ -49,7 +50,8 @@ int main(void) {
     assert sizes[:4] == [ctypes.sizeof(tlf.Config), ctypes.sizeof(tlf.LayerWeights),
                          ctypes.sizeof(tlf.Weights), ctypes.sizeof(tlf.CacheStats)]
     assert sizes[4:] == [tlf.Config.rms_eps.offset, tlf.Weights.layers.offset,
-                         tlf.CacheStats.last_step_active_rows.offset, tlf.CacheStats.device_error.offset]
+                         tlf.CacheStats.last_step_active_rows.offset, tlf.CacheStats.device_error.offset,
+                         tlf.CacheStats.attn_ms.offset]
 
 
 def _cfg(**kw):
@@ -117,6 +119,7 @@ def test_null_context_calls(lib):
     assert lib.tlf_prefill(None, 1, 1, None, None, None, 0) == tlf.E_INVALID_ARG
     assert lib.tlf_decode_step(None, None, None, None, None, None) == tlf.E_INVALID_ARG
     assert lib.tlf_cache_stats(None, ctypes.byref(out), None, None, 0) == tlf.E_INVALID_ARG
+    assert lib.tlf_set_profiling(None, 1) == tlf.E_INVALID_ARG
     lib.tlf_destroy(None)
 
 
