@@ -33,8 +33,10 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def decode_run(sess, torch, B, V, warmup, steps, first_tokens):
-    """Warmup, then `steps` timed decode steps with greedy feedback (no allocation)."""
+def decode_run(sess, torch, B, V, warmup, steps, profiled, first_tokens):
+    """Warmup, `steps` timed decode steps (HIP-graph replays), then `profiled`
+    steps launched kernel by kernel with HIP events around every attention
+    launch; greedy feedback throughout, no allocation inside either region."""
     dev = sess.device
     tok = [first_tokens.to(torch.int32).contiguous(), torch.empty(B, dtype=torch.int32, device=dev)]
     logits = torch.empty((B, V), dtype=torch.float32, device=dev)
@@ -42,8 +44,6 @@ def decode_run(sess, torch, B, V, warmup, steps, first_tokens):
     for _ in range(warmup):
         sess.decode_into(tok[k % 2], logits, next_tok=tok[(k + 1) % 2])
         k += 1
-    torch.cuda.synchronize()
-    sess.set_profiling(True)
     stream = torch.cuda.current_stream()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -54,6 +54,11 @@ def decode_run(sess, torch, B, V, warmup, steps, first_tokens):
     e1.record(stream)
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1)
+    sess.set_profiling(True)
+    for _ in range(profiled):
+        sess.decode_into(tok[k % 2], logits, next_tok=tok[(k + 1) % 2])
+        k += 1
+    torch.cuda.synchronize()
     st = sess.stats()
     sess.set_profiling(False)
     if st["status"] != 0:
@@ -72,9 +77,9 @@ def hot_path_bytes(st, model, steps, B):
     return st["attn_algo_bytes"] + st["kv_write_bytes_total"] + weights
 
 
-def run_config(torch, tlf, model, w, prompts, warmup, steps, route_rule="argmax", fixed_depth=1):
+def run_config(torch, tlf, model, w, prompts, warmup, steps, profiled, route_rule="argmax", fixed_depth=1):
     B, T = prompts.shape
-    max_pos = T + warmup + steps
+    max_pos = T + warmup + steps + profiled
     sess = tlf.Session(model, w, max_batch=B, max_pos=max_pos, route_rule=route_rule,
                        fixed_depth=fixed_depth, max_prefill_tokens=65536)
     try:
@@ -86,7 +91,7 @@ def run_config(torch, tlf, model, w, prompts, warmup, steps, route_rule="argmax"
         prefill_s = time.perf_counter() - t0
         first = torch.argmax(logits, dim=-1)
         del logits
-        ms, st = decode_run(sess, torch, B, model.vocab, warmup, steps, first)
+        ms, st = decode_run(sess, torch, B, model.vocab, warmup, steps, profiled, first)
         hist = sess.stats()["depth_hist"]
         return ms, st, prefill_s, hist
     finally:
@@ -94,8 +99,8 @@ def run_config(torch, tlf, model, w, prompts, warmup, steps, route_rule="argmax"
         torch.cuda.empty_cache()
 
 
-def cpu_baseline(model, w, prompts, budget_s):
-    """The oracle (untuned) decoding one sequence of the same workload on the host."""
+def cpu_baseline(model, w, prompts, budget_s, seqs=8):
+    """The oracle (untuned) decoding `seqs` sequences of the same workload on the host."""
     import numpy as np
     from oracle import tlf_oracle as O
     try:
@@ -104,18 +109,18 @@ def cpu_baseline(model, w, prompts, budget_s):
     except Exception:
         cores = os.cpu_count() or 1
     M = O.Model(w, model.n_heads, model.head_dim, rms_eps=model.rms_eps)
-    st, lg, _, _ = O.prefill(M, prompts[0])
-    tok = int(O.greedy(lg))
+    states, lg, _, _ = O.prefill_batch(M, prompts[:seqs])
+    tok = O.greedy(lg)
     n = 0
     t0 = time.perf_counter()
     while n < 2 or (time.perf_counter() - t0 < budget_s and n < model.steps):
-        lg2, _, _ = O.decode(M, [st], [tok])
-        tok = int(O.greedy(lg2[0]))
+        lg2, _, _ = O.decode(M, states, tok)
+        tok = O.greedy(lg2)
         n += 1
     dt = time.perf_counter() - t0
-    return {"value": n / dt, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
-            "sample": f"1 of {prompts.shape[0]} sequences: oracle prefill of its {prompts.shape[1]}-token "
-                      f"prompt (untimed), then {n} greedy decode steps timed ({dt:.1f} s)"}
+    return {"value": seqs * n / dt, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"{seqs} of {prompts.shape[0]} sequences: oracle prefill of their {prompts.shape[1]}-token "
+                      f"prompts (untimed), then {n} batched greedy decode steps timed ({dt:.1f} s)"}
 
 
 def prefill_measure(torch, tlf, synth, name):
@@ -159,6 +164,8 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=8)
+    ap.add_argument("--profiled-steps", type=int, default=20,
+                    help="steps after the timed region launched eagerly with HIP events around each attention launch")
     ap.add_argument("--config", default="c3")
     ap.add_argument("--no-fixed", action="store_true", help="skip the fixed-depth comparison")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
@@ -181,8 +188,9 @@ def main():
         sys.exit(1)
     torch.cuda.set_device(0)
     base = synth.CONFIGS[args.config]
-    if args.warmup + args.steps > base.steps:
-        print(f"warmup + steps must be <= {base.steps} for {args.config}", file=sys.stderr)
+    if args.warmup + args.steps + args.profiled_steps > base.steps or args.profiled_steps < 1:
+        print(f"warmup + steps + profiled-steps must be <= {base.steps} for {args.config} "
+              f"(profiled-steps >= 1)", file=sys.stderr)
         sys.exit(2)
     model = base
     t0 = time.perf_counter()
@@ -191,12 +199,13 @@ def main():
     B, T = prompts.shape
     log(f"inputs ready in {time.perf_counter() - t0:.1f}s: batch {B} x prompt {T}")
 
-    ms, st, prefill_s, hist = run_config(torch, tlf, model, w, prompts, args.warmup, args.steps)
+    ms, st, prefill_s, hist = run_config(torch, tlf, model, w, prompts, args.warmup, args.steps,
+                                         args.profiled_steps)
     log(f"routed: {ms / args.steps:.3f} ms/step, prefill {prefill_s:.2f}s, depth hist {hist}")
     value = B * args.steps / (ms / 1e3)
     attn_gbs = st["attn_algo_bytes"] / (st["attn_ms"] / 1e3) / 1e9
     per_launch = st["attn_algo_bytes"] / max(st["attn_launches"], 1)
-    hot_bytes = hot_path_bytes(st, model, args.steps, B)
+    hot_bytes = hot_path_bytes(st, model, args.profiled_steps, B)
     hot_gbs = hot_bytes / (st["block_ms"] / 1e3) / 1e9
     tot_hist = np.asarray(hist, dtype=np.float64)
     mean_depth = float((tot_hist * np.arange(1, len(hist) + 1)).sum() / max(tot_hist.sum(), 1))
@@ -223,15 +232,19 @@ def main():
         "roofline": {"bound": "hbm", "kernel": "k_attn_decode", "achieved": attn_gbs, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": attn_gbs / HBM_PEAK_GBS, "traffic": None,
                      "launches": st["attn_launches"], "avg_launch_us": st["attn_ms"] * 1e3 / st["attn_launches"],
-                     "algo_bytes_per_launch": per_launch},
-        "hot_path": {"what": "loop-and-layer region per step (attention + QKV/O/SwiGLU GEMMs, gaps included)",
+                     "algo_bytes_per_launch": per_launch,
+                     "measured": f"HIP events around each attention launch over {args.profiled_steps} decode "
+                                 f"steps right after the timed region"},
+        "hot_path": {"what": "loop-and-layer region per step (attention + QKV/O/SwiGLU GEMMs + norms, "
+                             "launch gaps of eager launches included)",
                      "achieved_gbs": hot_gbs, "frac": hot_gbs / HBM_PEAK_GBS,
-                     "ms_per_step": st["block_ms"] / args.steps, "algo_bytes_per_step": hot_bytes / args.steps},
+                     "ms_per_step": st["block_ms"] / args.profiled_steps,
+                     "algo_bytes_per_step": hot_bytes / args.profiled_steps},
         "prefill_s": prefill_s,
     }
     if not args.no_fixed:
         fms, fst, fpre, _ = run_config(torch, tlf, model, w, prompts, args.warmup, args.steps,
-                                       route_rule="fixed", fixed_depth=model.max_loops)
+                                       args.profiled_steps, route_rule="fixed", fixed_depth=model.max_loops)
         fgbs = fst["attn_algo_bytes"] / (fst["attn_ms"] / 1e3) / 1e9
         out["fixed_depth"] = {"depth": model.max_loops, "value": B * args.steps / (fms / 1e3),
                               "ms_per_step": fms / args.steps, "attn_achieved_gbs": fgbs,

@@ -82,10 +82,10 @@ typedef struct tlf_config {
   int32_t abi_version;   /* must be TLF_ABI_VERSION */
   int32_t dtype;         /* TLF_DTYPE_F32 or TLF_DTYPE_BF16 */
   int32_t vocab;         /* V >= 1 */
-  int32_t d_model;       /* d, multiple of 64 */
+  int32_t d_model;       /* d <= 4096, multiple of 128 (bf16) or 64 (float32) */
   int32_t n_heads;       /* H, n_heads * head_dim == d_model */
   int32_t head_dim;      /* D: 64 or 128 (16 for float32 models only) */
-  int32_t d_ff;          /* F, SwiGLU hidden width, multiple of 64 */
+  int32_t d_ff;          /* F, SwiGLU hidden width, multiple of 128 (bf16) or 64 (float32) */
   int32_t n_layers;      /* J in [1, TLF_MAX_LAYERS], layers of the shared block */
   int32_t max_loops;     /* R = M in [1, TLF_MAX_LOOPS], router width and loop cap */
   int32_t max_pos;       /* rows of the position table, <= 65536; prompt + decode steps <= max_pos */
@@ -97,6 +97,9 @@ typedef struct tlf_config {
   float route_threshold; /* CUMPROB threshold in (0, 1); the paper uses 0.5 */
   int32_t fixed_depth;   /* FIXED depth in [1, R] */
   float rms_eps;         /* RMSNorm epsilon (> 0) */
+  int32_t decode_graph;  /* 1: each decode step replays a captured HIP graph (captured on the first
+                            step and again whenever the batch or an output pointer changes);
+                            0: kernels are launched one by one */
 } tlf_config;
 
 /* Weights of layer j of the shared block, row-major [out][in] (y = x W^T),

@@ -19,8 +19,8 @@ int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 // Workspace buffers, in carve order.
 enum Buf {
   B_POOL, B_POS, B_PAGE_TABLE, B_CACHE_LEN, B_SEQ_LEN, B_SCALARS, B_DEPTH_HIST, B_STEP_STATS,
-  B_X_DEC, B_DEPTH_DEC, B_PERM, B_NACT, B_Q_DEC, B_O_DEC, B_ACT_DEC, B_KEYS,
-  B_X_PRE, B_DEPTH_PRE, B_TOK_IDX, B_Q_PRE, B_O_PRE, B_ACT_PRE,
+  B_X_DEC, B_Y_DEC, B_DEPTH_DEC, B_PERM, B_NACT, B_Q_DEC, B_O_DEC, B_ACT_DEC, B_KEYS, B_PARTIAL,
+  B_X_PRE, B_Y_PRE, B_DEPTH_PRE, B_TOK_IDX, B_Q_PRE, B_O_PRE, B_ACT_PRE,
   B_COUNT
 };
 
@@ -50,6 +50,7 @@ bool make_layout(const tlf_config& c, Layout* L) {
   sz[B_DEPTH_HIST] = R * 8;
   sz[B_STEP_STATS] = kStatCount * 8;
   sz[B_X_DEC] = B * d * 4;
+  sz[B_Y_DEC] = B * d * s;
   sz[B_DEPTH_DEC] = B * 4;
   sz[B_PERM] = B * 4;
   sz[B_NACT] = R * 4;
@@ -57,7 +58,9 @@ bool make_layout(const tlf_config& c, Layout* L) {
   sz[B_O_DEC] = B * d * s;
   sz[B_ACT_DEC] = B * F * s;
   sz[B_KEYS] = B * 8;
+  sz[B_PARTIAL] = (int64_t)kMaxSplits * B * d * 4;
   sz[B_X_PRE] = P * d * 4;
+  sz[B_Y_PRE] = P * d * s;
   sz[B_DEPTH_PRE] = P * 4;
   sz[B_TOK_IDX] = R * P * 4;
   sz[B_Q_PRE] = P * d * s;
@@ -78,11 +81,13 @@ int validate_config(const tlf_config* c) {
   if (!c) return TLF_E_INVALID_ARG;
   if (c->abi_version != TLF_ABI_VERSION) return TLF_E_INVALID_ARG;
   if (c->dtype != TLF_DTYPE_F32 && c->dtype != TLF_DTYPE_BF16) return TLF_E_INVALID_ARG;
-  if (c->vocab < 1 || c->d_model < 64 || c->d_model % 64 != 0) return TLF_E_INVALID_ARG;
+  // GEMM K tiles are 256 bytes: 128 bf16 or 64 float32 elements; rows up to 4096 wide
+  const int kq = c->dtype == TLF_DTYPE_BF16 ? 128 : 64;
+  if (c->vocab < 1 || c->d_model < kq || c->d_model % kq != 0 || c->d_model > 4096) return TLF_E_INVALID_ARG;
   if (c->head_dim != 16 && c->head_dim != 64 && c->head_dim != 128) return TLF_E_INVALID_ARG;
   if (c->dtype == TLF_DTYPE_BF16 && c->head_dim == 16) return TLF_E_INVALID_ARG;
   if (c->n_heads < 1 || (int64_t)c->n_heads * c->head_dim != c->d_model) return TLF_E_INVALID_ARG;
-  if (c->d_ff < 64 || c->d_ff % 64 != 0) return TLF_E_INVALID_ARG;
+  if (c->d_ff < kq || c->d_ff % kq != 0) return TLF_E_INVALID_ARG;
   if (c->n_layers < 1 || c->n_layers > TLF_MAX_LAYERS) return TLF_E_INVALID_ARG;
   if (c->max_loops < 1 || c->max_loops > TLF_MAX_LOOPS) return TLF_E_INVALID_ARG;
   if (c->max_pos < 1 || c->max_batch < 1 || c->max_batch > TLF_MAX_BATCH) return TLF_E_INVALID_ARG;
@@ -96,6 +101,7 @@ int validate_config(const tlf_config* c) {
     return TLF_E_INVALID_ARG;
   }
   if (!(c->rms_eps > 0.f) || !std::isfinite(c->rms_eps)) return TLF_E_INVALID_ARG;
+  if (c->decode_graph != 0 && c->decode_graph != 1) return TLF_E_INVALID_ARG;
   // the decode attention stages one sequence's page list in LDS
   if (ceil_div(c->max_pos, kPage) > kAttnMaxPages) return TLF_E_INVALID_ARG;
   // positions, row indices and work-list offsets are int32
@@ -137,9 +143,23 @@ struct tlf_ctx {
   int64_t attn_launches = 0;
   double attn_ms = 0.0, block_ms = 0.0;
 
+  // decode-step graph: captured on cap_stream, replayed on stream
+  hipStream_t cap_stream = nullptr;
+  hipGraphExec_t graph_exec = nullptr;
+  struct GraphKey {
+    int batch = -1;
+    const void *tokens = nullptr, *logits = nullptr, *next = nullptr, *depths = nullptr, *margin = nullptr;
+    bool operator==(const GraphKey& o) const {
+      return batch == o.batch && tokens == o.tokens && logits == o.logits && next == o.next &&
+             depths == o.depths && margin == o.margin;
+    }
+  } graph_key;
+
   ~tlf_ctx() {
     recycle_events();
     for (hipEvent_t e : event_pool) (void)hipEventDestroy(e);
+    if (graph_exec) (void)hipGraphExecDestroy(graph_exec);
+    if (cap_stream) (void)hipStreamDestroy(cap_stream);
   }
   void recycle_events() {
     for (auto& t : event_pending) { event_pool.push_back(t.start); event_pool.push_back(t.stop); }
@@ -181,6 +201,16 @@ int precheck(tlf_ctx* ctx) {
   return TLF_OK;
 }
 
+// Split-K factor of a decode residual projection: at least two K tiles per
+// split, at most kMaxSplits splits, dividing the K tiles evenly.
+template <typename T>
+int decode_splits(int K) {
+  const int kt = K / gemm_k_tile<T>();
+  for (int sp = kMaxSplits; sp > 1; --sp)
+    if (kt % sp == 0 && kt / sp >= 2) return sp;
+  return 1;
+}
+
 // Waves sharing one (row, head) in the decode attention: enough waves in
 // flight to cover the device even when batch x heads is small.
 int attn_waves(const tlf_ctx* ctx) {
@@ -201,6 +231,7 @@ int run_prefill(tlf_ctx* ctx, int B, int T_, const int32_t* tokens, float* logit
   TLF_HIP(launch_fill_u64(ctx->cv.depth_hist, 0ull, R, s));
   const int G = std::max(1, ctx->L.pre_rows / T_);
   float* x = ctx->buf<float>(B_X_PRE);
+  void* y = ctx->buf<void>(B_Y_PRE);
   for (int b0 = 0; b0 < B; b0 += G) {
     const int Gc = std::min(G, B - b0);
     const int rows = Gc * T_;
@@ -208,7 +239,7 @@ int run_prefill(tlf_ctx* ctx, int B, int T_, const int32_t* tokens, float* logit
     ea.tok_emb = ctx->w.tok_emb; ea.pos_emb = ctx->w.pos_emb; ea.Wr = ctx->w.router_w; ea.br = ctx->w.router_b;
     ea.tokens = tokens + (int64_t)b0 * T_;
     ea.rows = rows; ea.V = c.vocab; ea.d = d; ea.R = R; ea.prefill_T = T_;
-    ea.x = x; ea.depth = ctx->buf<int32_t>(B_DEPTH_PRE);
+    ea.x = x; ea.y = y; ea.eps = c.rms_eps; ea.depth = ctx->buf<int32_t>(B_DEPTH_PRE);
     ea.out_depth = depths ? depths + (int64_t)b0 * T_ : nullptr;
     ea.rule = c.route_rule; ea.threshold = c.route_threshold; ea.fixed = c.fixed_depth;
     ea.err = ctx->cv.err;
@@ -221,17 +252,21 @@ int run_prefill(tlf_ctx* ctx, int B, int T_, const int32_t* tokens, float* logit
     TLF_HIP(launch_plan_prefill(pa, s));
 
     for (int i = 0; i < R; ++i) {
+      // rows: G segments of T compact slots; slot a of segment g is the a-th
+      // token of sequence b0 + g with depth >= i + 1, residual row tok_idx[r]
       RowMap rm;
       rm.src = ctx->buf<int32_t>(B_TOK_IDX) + (int64_t)i * rows;
       rm.seg_cnt = ctx->cv.cache_len + (int64_t)b0 * R + i;
       rm.seg = T_; rm.seg_cnt_stride = R; rm.rows = rows;
+      ResidNormArgs rn;
+      rn.rm = rm; rn.x = x; rn.y = y; rn.splits = 0; rn.d = d; rn.eps = c.rms_eps;
       for (int j = 0; j < c.n_layers; ++j) {
         const tlf_layer_weights& lw = ctx->layers[j];
         GemmArgs q;
-        q.A = x; q.lda = d; q.W = lw.w_qkv; q.N = 3 * d; q.K = d; q.w_rows = 3 * d; q.rm = rm; q.eps = c.rms_eps;
+        q.A = y; q.lda = d; q.W = lw.w_qkv; q.N = 3 * d; q.K = d; q.w_rows = 3 * d; q.rm = rm;
         q.out = ctx->buf<void>(B_Q_PRE); q.ldo = d; q.d = d;
         q.kv.c = ctx->cv; q.kv.loop = i; q.kv.layer = j; q.kv.prefill = 1; q.kv.b0 = b0; q.kv.seg = T_;
-        TLF_HIP(launch_gemm<T>(q, A_NORM, E_QKV, true, s));
+        TLF_HIP(launch_gemm<T>(q, A_SRC, E_QKV, true, s));
 
         AttnPrefillArgs at;
         at.c = ctx->cv; at.loop = i; at.layer = j; at.d = d; at.b0 = b0; at.G = Gc; at.T = T_;
@@ -242,22 +277,24 @@ int run_prefill(tlf_ctx* ctx, int B, int T_, const int32_t* tokens, float* logit
         GemmArgs o;
         o.A = ctx->buf<void>(B_O_PRE); o.lda = d; o.W = lw.w_o; o.N = d; o.K = d; o.w_rows = d; o.rm = rm;
         o.out = x; o.ldo = d;
-        TLF_HIP(launch_gemm<T>(o, A_BUF, E_RESID, true, s));
+        TLF_HIP(launch_gemm<T>(o, A_CMP, E_RESID, true, s));
+        TLF_HIP(launch_resid_norm<T>(rn, s));
 
         GemmArgs gu;
-        gu.A = x; gu.lda = d; gu.W = lw.w_gate_up; gu.N = 2 * F; gu.K = d; gu.w_rows = 2 * F; gu.rm = rm;
-        gu.eps = c.rms_eps; gu.out = ctx->buf<void>(B_ACT_PRE); gu.ldo = F; gu.F = F;
-        TLF_HIP(launch_gemm<T>(gu, A_NORM, E_SWIGLU, true, s));
+        gu.A = y; gu.lda = d; gu.W = lw.w_gate_up; gu.N = 2 * F; gu.K = d; gu.w_rows = 2 * F; gu.rm = rm;
+        gu.out = ctx->buf<void>(B_ACT_PRE); gu.ldo = F; gu.F = F;
+        TLF_HIP(launch_gemm<T>(gu, A_SRC, E_SWIGLU, true, s));
 
         GemmArgs dn;
         dn.A = ctx->buf<void>(B_ACT_PRE); dn.lda = F; dn.W = lw.w_down; dn.N = d; dn.K = F; dn.w_rows = d;
         dn.rm = rm; dn.out = x; dn.ldo = d;
-        TLF_HIP(launch_gemm<T>(dn, A_BUF, E_RESID, true, s));
+        TLF_HIP(launch_gemm<T>(dn, A_CMP, E_RESID, true, s));
+        TLF_HIP(launch_resid_norm<T>(rn, s));
       }
     }
     GemmArgs hd;
-    hd.A = x; hd.lda = d; hd.W = head_weights(ctx); hd.N = c.vocab; hd.K = d; hd.w_rows = c.vocab;
-    hd.eps = c.rms_eps; hd.out = logits; hd.ldo = c.vocab;
+    hd.A = y; hd.lda = d; hd.W = head_weights(ctx); hd.N = c.vocab; hd.K = d; hd.w_rows = c.vocab;
+    hd.out = logits; hd.ldo = c.vocab;
     if (flags & TLF_PREFILL_ALL_LOGITS) {
       hd.rm.rows = rows; hd.rm.src_stride = 1; hd.rm.src_off = 0;
       hd.out_row_off = b0 * T_;
@@ -265,25 +302,27 @@ int run_prefill(tlf_ctx* ctx, int B, int T_, const int32_t* tokens, float* logit
       hd.rm.rows = Gc; hd.rm.src_stride = T_; hd.rm.src_off = T_ - 1;
       hd.out_row_off = b0;
     }
-    TLF_HIP(launch_gemm<T>(hd, A_NORM, E_LOGITS, flags & TLF_PREFILL_ALL_LOGITS, s));
+    TLF_HIP(launch_gemm<T>(hd, A_SRC, E_LOGITS, true, s));
   }
   return TLF_OK;
 }
 
 template <typename T>
-int run_decode(tlf_ctx* ctx, const int32_t* tokens, float* logits, int32_t* next, int32_t* depths,
-               float* margin) {
+int run_decode(tlf_ctx* ctx, hipStream_t s, const int32_t* tokens, float* logits, int32_t* next,
+               int32_t* depths, float* margin) {
   const tlf_config& c = ctx->cfg;
-  hipStream_t s = ctx->stream;
   const int d = c.d_model, F = c.d_ff, R = c.max_loops, B = ctx->batch;
   float* x = ctx->buf<float>(B_X_DEC);
+  void* y = ctx->buf<void>(B_Y_DEC);
   int32_t* perm = ctx->buf<int32_t>(B_PERM);
   int32_t* nact = ctx->buf<int32_t>(B_NACT);
+  float* part = ctx->buf<float>(B_PARTIAL);
+  const int split_o = decode_splits<T>(d), split_d = decode_splits<T>(F);
 
   EmbedArgs ea;
   ea.tok_emb = ctx->w.tok_emb; ea.pos_emb = ctx->w.pos_emb; ea.Wr = ctx->w.router_w; ea.br = ctx->w.router_b;
   ea.tokens = tokens; ea.rows = B; ea.V = c.vocab; ea.d = d; ea.R = R; ea.prefill_T = 0;
-  ea.seq_len = ctx->cv.seq_len; ea.x = x; ea.depth = ctx->buf<int32_t>(B_DEPTH_DEC);
+  ea.seq_len = ctx->cv.seq_len; ea.x = x; ea.y = y; ea.eps = c.rms_eps; ea.depth = ctx->buf<int32_t>(B_DEPTH_DEC);
   ea.out_depth = depths; ea.out_margin = margin;
   ea.rule = c.route_rule; ea.threshold = c.route_threshold; ea.fixed = c.fixed_depth; ea.err = ctx->cv.err;
   TLF_HIP(launch_embed_route<T>(ea, s));
@@ -303,16 +342,16 @@ int run_decode(tlf_ctx* ctx, const int32_t* tokens, float* logits, int32_t* next
     TLF_HIP(hipEventRecord(block_start, s));
   }
   for (int i = 0; i < R; ++i) {
+    // rows [0, n_i) of the depth-sorted order are the tokens still active at loop i
     RowMap rm;
     rm.src = perm; rm.nact = nact + i; rm.rows = B;
-    RowMap rc = rm;  // compact buffers are indexed by the row itself
     for (int j = 0; j < c.n_layers; ++j) {
       const tlf_layer_weights& lw = ctx->layers[j];
       GemmArgs q;
-      q.A = x; q.lda = d; q.W = lw.w_qkv; q.N = 3 * d; q.K = d; q.w_rows = 3 * d; q.rm = rm; q.eps = c.rms_eps;
+      q.A = y; q.lda = d; q.W = lw.w_qkv; q.N = 3 * d; q.K = d; q.w_rows = 3 * d; q.rm = rm;
       q.out = ctx->buf<void>(B_Q_DEC); q.ldo = d; q.d = d;
       q.kv.c = ctx->cv; q.kv.loop = i; q.kv.layer = j; q.kv.prefill = 0;
-      TLF_HIP(launch_gemm<T>(q, A_NORM, E_QKV, false, s));
+      TLF_HIP(launch_gemm<T>(q, A_SRC, E_QKV, false, s));
 
       AttnDecodeArgs at;
       at.c = ctx->cv; at.loop = i; at.layer = j; at.d = d; at.perm = perm; at.nact = nact + i;
@@ -329,30 +368,37 @@ int run_decode(tlf_ctx* ctx, const int32_t* tokens, float* logits, int32_t* next
       }
 
       GemmArgs o;
-      o.A = ctx->buf<void>(B_O_DEC); o.lda = d; o.W = lw.w_o; o.N = d; o.K = d; o.w_rows = d; o.rm = rc;
-      o.out = x; o.ldo = d;
-      TLF_HIP(launch_gemm<T>(o, A_BUF, E_RESID, false, s));
+      o.A = ctx->buf<void>(B_O_DEC); o.lda = d; o.W = lw.w_o; o.N = d; o.K = d; o.w_rows = d; o.rm = rm;
+      o.splits = split_o; o.out = part; o.ldo = d; o.part_rows = c.max_batch;
+      TLF_HIP(launch_gemm<T>(o, A_CMP, E_PARTIAL, false, s));
+      ResidNormArgs rn;
+      rn.rm = rm; rn.x = x; rn.y = y; rn.partial = part; rn.splits = split_o; rn.part_rows = c.max_batch;
+      rn.d = d; rn.eps = c.rms_eps;
+      TLF_HIP(launch_resid_norm<T>(rn, s));
 
       GemmArgs gu;
-      gu.A = x; gu.lda = d; gu.W = lw.w_gate_up; gu.N = 2 * F; gu.K = d; gu.w_rows = 2 * F; gu.rm = rm;
-      gu.eps = c.rms_eps; gu.out = ctx->buf<void>(B_ACT_DEC); gu.ldo = F; gu.F = F;
-      TLF_HIP(launch_gemm<T>(gu, A_NORM, E_SWIGLU, false, s));
+      gu.A = y; gu.lda = d; gu.W = lw.w_gate_up; gu.N = 2 * F; gu.K = d; gu.w_rows = 2 * F; gu.rm = rm;
+      gu.out = ctx->buf<void>(B_ACT_DEC); gu.ldo = F; gu.F = F;
+      TLF_HIP(launch_gemm<T>(gu, A_SRC, E_SWIGLU, false, s));
 
       GemmArgs dn;
       dn.A = ctx->buf<void>(B_ACT_DEC); dn.lda = F; dn.W = lw.w_down; dn.N = d; dn.K = F; dn.w_rows = d;
-      dn.rm = rc; dn.out = x; dn.ldo = d;
-      TLF_HIP(launch_gemm<T>(dn, A_BUF, E_RESID, false, s));
+      dn.rm = rm; dn.splits = split_d; dn.out = part; dn.ldo = d; dn.part_rows = c.max_batch;
+      TLF_HIP(launch_gemm<T>(dn, A_CMP, E_PARTIAL, false, s));
+      rn.splits = split_d;
+      TLF_HIP(launch_resid_norm<T>(rn, s));
     }
   }
   if (ctx->profiling) {
     TLF_HIP(hipEventRecord(block_stop, s));
     ctx->event_pending.push_back(tlf_ctx::Timed{block_start, block_stop, false});
   }
+  // every row's y now holds RMSNorm of its last state h^(m_b)
   GemmArgs hd;
-  hd.A = x; hd.lda = d; hd.W = head_weights(ctx); hd.N = c.vocab; hd.K = d; hd.w_rows = c.vocab;
-  hd.rm.rows = B; hd.eps = c.rms_eps; hd.out = logits; hd.ldo = c.vocab;
+  hd.A = y; hd.lda = d; hd.W = head_weights(ctx); hd.N = c.vocab; hd.K = d; hd.w_rows = c.vocab;
+  hd.rm.rows = B; hd.out = logits; hd.ldo = c.vocab;
   hd.argmax_keys = ctx->buf<unsigned long long>(B_KEYS);
-  TLF_HIP(launch_gemm<T>(hd, A_NORM, E_LOGITS, false, s));
+  TLF_HIP(launch_gemm<T>(hd, A_SRC, E_LOGITS, true, s));
   if (next) TLF_HIP(launch_argmax_finalize(ctx->buf<unsigned long long>(B_KEYS), next, B, s));
   return TLF_OK;
 }
@@ -419,13 +465,15 @@ int tlf_init(const tlf_config* cfg, const tlf_weights* w, void* d_workspace, siz
                                      : attn_decode_blocks_per_cu<float>(cfg->head_dim, 4 << k, &blocks);
     ctx->attn_blocks[k] = std::max(1, blocks);
   }
+  if (e == hipSuccess) e = hipStreamCreateWithFlags(&ctx->cap_stream, hipStreamNonBlocking);
   if (e != hipSuccess) { delete ctx; return TLF_E_HIP; }
 
-  // Free pages are NaN-poisoned: a read of a slot that was never written
-  // turns the logits into NaN instead of silently using stale values.
+  // The pool starts zeroed: attention kernels read whole 16-slot pages and
+  // give zero weight to slots past a cache's length, which must hold finite
+  // values (zeros here, or stale entries of an earlier batch).
   hipStream_t s = ctx->stream;
   const int64_t pool_words = (int64_t)(L.size[B_POOL] / 4);
-  e = launch_fill_i32(reinterpret_cast<int32_t*>(cv.pool), -1, pool_words, s);
+  e = launch_fill_i32(reinterpret_cast<int32_t*>(cv.pool), 0, pool_words, s);
   if (e == hipSuccess) e = launch_fill_i32(cv.pos, -1, (int64_t)cfg->max_pages * kPage, s);
   if (e == hipSuccess) e = launch_fill_i32(cv.page_table, -1, (int64_t)(L.size[B_PAGE_TABLE] / 4), s);
   if (e == hipSuccess) e = launch_fill_i32(cv.cache_len, 0, (int64_t)cfg->max_batch * cfg->max_loops, s);
@@ -463,9 +511,48 @@ int tlf_decode_step(tlf_ctx* ctx, const int32_t* d_tokens, float* d_logits, int3
   if (st != TLF_OK) return st;
   if (!ctx->prefilled || ctx->seq_len >= ctx->cfg.max_pos) return TLF_E_STATE;
   if (!d_tokens || !d_logits) return TLF_E_INVALID_ARG;
-  st = ctx->cfg.dtype == TLF_DTYPE_BF16 ? run_decode<bf16>(ctx, d_tokens, d_logits, d_next, d_depths, d_margin)
-                                        : run_decode<float>(ctx, d_tokens, d_logits, d_next, d_depths, d_margin);
-  if (st != TLF_OK) return st;
+  auto enqueue = [&](hipStream_t s) {
+    return ctx->cfg.dtype == TLF_DTYPE_BF16
+               ? run_decode<bf16>(ctx, s, d_tokens, d_logits, d_next, d_depths, d_margin)
+               : run_decode<float>(ctx, s, d_tokens, d_logits, d_next, d_depths, d_margin);
+  };
+  if (ctx->cfg.decode_graph && !ctx->profiling) {
+    const tlf_ctx::GraphKey key{ctx->batch, d_tokens, d_logits, d_next, d_depths, d_margin};
+    if (!ctx->graph_exec || !(key == ctx->graph_key)) {
+      if (ctx->graph_exec) {
+        (void)hipGraphExecDestroy(ctx->graph_exec);
+        ctx->graph_exec = nullptr;
+      }
+      // nothing runs while capturing; the graph is replayed on the context's stream
+      if (hipStreamBeginCapture(ctx->cap_stream, hipStreamCaptureModeThreadLocal) != hipSuccess) {
+        ctx->poisoned = true;
+        return TLF_E_HIP;
+      }
+      st = enqueue(ctx->cap_stream);
+      hipGraph_t graph = nullptr;
+      const hipError_t ec = hipStreamEndCapture(ctx->cap_stream, &graph);
+      if (st != TLF_OK || ec != hipSuccess || !graph) {
+        if (graph) (void)hipGraphDestroy(graph);
+        ctx->poisoned = true;
+        return st != TLF_OK ? st : TLF_E_HIP;
+      }
+      const hipError_t ei = hipGraphInstantiate(&ctx->graph_exec, graph, nullptr, nullptr, 0);
+      (void)hipGraphDestroy(graph);
+      if (ei != hipSuccess) {
+        ctx->graph_exec = nullptr;
+        ctx->poisoned = true;
+        return TLF_E_HIP;
+      }
+      ctx->graph_key = key;
+    }
+    if (hipGraphLaunch(ctx->graph_exec, ctx->stream) != hipSuccess) {
+      ctx->poisoned = true;
+      return TLF_E_HIP;
+    }
+  } else {
+    st = enqueue(ctx->stream);
+    if (st != TLF_OK) return st;
+  }
   ctx->seq_len += 1;
   return TLF_OK;
 }

@@ -23,41 +23,39 @@ namespace {
 
 constexpr float kNegInf = -__builtin_inff();
 
+// Two floats rounded to bf16 (nearest even) in one 32-bit word, low half first.
+__device__ __forceinline__ unsigned int pack_bf16x2(float lo, float hi) {
+  const bf16 a = (bf16)lo, b = (bf16)hi;
+  return (unsigned int)__builtin_bit_cast(unsigned short, a) |
+         ((unsigned int)__builtin_bit_cast(unsigned short, b) << 16);
+}
+
 __device__ __forceinline__ float merge_scale(float m, float mn) {
   return m == kNegInf ? 0.f : exp2f(m - mn);
 }
 
 // Sum over aligned groups of G lanes (G = 2, 4, 8, 16, 32) with DPP moves
 // inside rows of 16 lanes and a shuffle beyond them.
-template <int CTRL>
-__device__ __forceinline__ float dpp_mov(float x) {
-  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, 0xF, 0xF, false));
-}
-
-template <int G>
-__device__ __forceinline__ float group_sum(float v) {
-  if constexpr (G >= 2) v += dpp_mov<0xB1>(v);   // quad_perm [1,0,3,2]: partner lane ^ 1
-  if constexpr (G >= 4) v += dpp_mov<0x4E>(v);   // quad_perm [2,3,0,1]: partner lane ^ 2
-  if constexpr (G >= 8) v += dpp_mov<0x141>(v);  // row_half_mirror: the other quad of the 8
-  if constexpr (G >= 16) v += dpp_mov<0x140>(v); // row_mirror: the other half of the 16
-  if constexpr (G >= 32) v += shfl_xor(v, 16);
-  return v;
-}
-
 template <typename T, int D, int W>
 __global__ __launch_bounds__(W * 64) void k_attn_decode(AttnDecodeArgs a) {
-  constexpr int EPL = 16 / (int)sizeof(T);  // elements per 16-byte load
-  constexpr int G = D / EPL;                // lanes per token
-  constexpr int TPI = kWave / G;            // tokens per wave instruction
-  constexpr int U = 4;                      // tokens per lane per load batch
-  constexpr int STEP = U * TPI;             // tokens per wave per batch
-  static_assert(G >= 1 && G <= 32 && kWave % G == 0, "head_dim split");
+  using M = Mfma<T>;
+  constexpr int KS = M::KS, EPL = M::EPL;
+  constexpr int PPI = EPL == 8 ? 2 : 1;                    // pages per iteration (4 * PPI slots per lane)
+  constexpr int KSTEPS = D / KS;                            // S MFMAs per page
+  constexpr int DT = D / 16;                                // output dimension tiles
+  constexpr int PVM = 4 * PPI / EPL;                        // P.V MFMAs per iteration
+  constexpr int NBUF = D * (int)sizeof(T) <= 128 ? 2 : 1;   // batches in flight
+  static_assert(KSTEPS >= 1 && D % 16 == 0, "head_dim");
+  static_assert(4 * PPI % EPL == 0, "P.V k-slots");
+  // V^T fragment per dimension tile: 4 consecutive slots of one dimension from
+  // each of the PPI pages (bf16: 2 x 8 bytes; f32: 16 bytes)
+  typedef typename M::frag KFrag;
   __shared__ int s_pages[kAttnMaxPages];
   __shared__ float s_red[W][D + 2];
 
   const CacheView& c = a.c;
   const int lane = lane_id(), w = threadIdx.x >> 6;
-  const int tr = lane / G, gl = lane % G;
+  const int quad = lane >> 4, c16 = lane & 15;
   const int H = c.H, R = c.R, i = a.loop;
   const int nunits = *a.nact * H;
   const T* pool = reinterpret_cast<const T*>(c.pool);
@@ -72,106 +70,151 @@ __global__ __launch_bounds__(W * 64) void k_attn_decode(AttnDecodeArgs a) {
     for (int p = threadIdx.x; p < np; p += W * kWave) s_pages[p] = pt[p];
     __syncthreads();
 
-    // this wave's contiguous share of the L entries
-    const int per = ((L + W - 1) / W + TPI - 1) / TPI * TPI;
-    const int t0 = w * per, t1 = min(L, t0 + per);
-    const int64_t koff = page_off(c, a.layer, 0, h, 0) + gl * EPL;
-    const int64_t voff = page_off(c, a.layer, 1, h, 0) + gl * EPL;
-    const V16<T> qv = ld16(reinterpret_cast<const T*>(a.q) + (int64_t)k * a.d + h * D + gl * EPL);
-    float qf[EPL];
-#pragma unroll
-    for (int e = 0; e < EPL; ++e) qf[e] = to_f<T>(qv.e[e]) * a.scale_log2;
+    // this wave's pages [p0, p1), a multiple of PPI pages each
+    const int per = ((np + W - 1) / W + PPI - 1) / PPI * PPI;
+    const int p0 = w * per, p1 = min(np, p0 + per);
+    const int64_t koff = k_block(c, a.layer, h) + (int64_t)c16 * D + quad * EPL;
+    const int64_t voff = v_block(c, a.layer, h) + (int64_t)c16 * kPage + quad * 4;
 
-    float m = kNegInf, l = 0.f, acc[EPL];
+    // q as the B operand of S = K q^T, the same in all 16 columns
+    KFrag qf[KSTEPS];
+    {
+      const T* qp = reinterpret_cast<const T*>(a.q) + (int64_t)k * a.d + h * D + quad * EPL;
 #pragma unroll
-    for (int e = 0; e < EPL; ++e) acc[e] = 0.f;
+      for (int ks = 0; ks < KSTEPS; ++ks) qf[ks] = M::load(qp + ks * KS);
+    }
+    f32x4 o[DT];
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    float m = kNegInf, lsum = 0.f;
 
-    auto load = [&](V16<T>* kr, V16<T>* vr, int tb) {
+    auto load = [&](KFrag (&bk)[PPI][KSTEPS], uint4 (&bv)[DT], int pg) __attribute__((always_inline)) {
+      const T* base[PPI];
 #pragma unroll
-      for (int uu = 0; uu < U; ++uu) {
-        const int t = tb + uu * TPI + tr;
-        const int tt = t < t1 ? t : t0;  // lanes past the end read a valid slot
-        const int64_t base = (int64_t)s_pages[tt >> 4] * c.page_elems + (tt & (kPage - 1)) * D;
-        kr[uu] = ld16(pool + base + koff);
-        vr[uu] = ld16(pool + base + voff);
+      for (int p = 0; p < PPI; ++p) {
+        // past the range: reread the last page (its scores are masked); loads
+        // are never skipped so the compiler can count the batch in flight
+        const int pp = min(pg + p, p1 - 1);
+        base[p] = pool + (int64_t)s_pages[pp] * c.page_elems;
+#pragma unroll
+        for (int ks = 0; ks < KSTEPS; ++ks) bk[p][ks] = M::load(base[p] + koff + ks * KS);
+      }
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+        const int64_t off = voff + (int64_t)dt * 16 * kPage;
+        if constexpr (EPL == 8) {
+          const uint2 lo = *reinterpret_cast<const uint2*>(base[0] + off);
+          const uint2 hi = *reinterpret_cast<const uint2*>(base[PPI - 1] + off);
+          bv[dt] = make_uint4(lo.x, lo.y, hi.x, hi.y);
+        } else {
+          bv[dt] = *reinterpret_cast<const uint4*>(base[0] + off);
+        }
       }
     };
-    auto consume = [&](const V16<T>* kr, const V16<T>* vr, int tb) {
-      float s[U];
+    auto consume = [&](const KFrag (&bk)[PPI][KSTEPS], const uint4 (&bv)[DT], int pg)
+                       __attribute__((always_inline)) {
+      // scores of this lane's tokens: page p, slot 4 * quad + r
+      float sc[PPI][4];
       float mx = m;
 #pragma unroll
-      for (int uu = 0; uu < U; ++uu) {
-        float d = 0.f;
+      for (int p = 0; p < PPI; ++p) {
+        f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int e = 0; e < EPL; ++e) d = fmaf(qf[e], to_f<T>(kr[uu].e[e]), d);
-        d = group_sum<G>(d);
-        s[uu] = (tb + uu * TPI + tr < t1) ? d : kNegInf;
-        mx = fmaxf(mx, s[uu]);
-      }
-      if (mx != kNegInf) {
-        const float alpha = merge_scale(m, mx);
-        l *= alpha;
+        for (int ks = 0; ks < KSTEPS; ++ks) acc = M::mma(bk[p][ks], qf[ks], acc);
 #pragma unroll
-        for (int e = 0; e < EPL; ++e) acc[e] *= alpha;
-#pragma unroll
-        for (int uu = 0; uu < U; ++uu) {
-          const float p = exp2f(s[uu] - mx);  // exp2(-inf) = 0 for masked slots
-          l += p;
-#pragma unroll
-          for (int e = 0; e < EPL; ++e) acc[e] = fmaf(p, to_f<T>(vr[uu].e[e]), acc[e]);
+        for (int r = 0; r < 4; ++r) {
+          const int t = (pg + p) * kPage + 4 * quad + r;
+          const bool ok = (pg + p) < p1 && t < L;
+          sc[p][r] = ok ? acc[r] * a.scale_log2 : kNegInf;
+          mx = fmaxf(mx, sc[p][r]);
         }
-        m = mx;
       }
+      mx = fmaxf(mx, shfl_xor(mx, 16));
+      mx = fmaxf(mx, shfl_xor(mx, 32));
+      if (mx == kNegInf) return;  // wave-uniform: nothing valid yet
+      const float alpha = merge_scale(m, mx);
+      lsum *= alpha;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) o[dt] *= alpha;
+      float pr[PPI][4];
+#pragma unroll
+      for (int p = 0; p < PPI; ++p)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          pr[p][r] = exp2f(sc[p][r] - mx);  // 0 for masked slots
+          lsum += pr[p][r];
+        }
+      // P.V: MFMA mm takes k-slots (page, r) = mm * EPL .. mm * EPL + EPL - 1 of
+      // this lane's tokens, in the same order on both operands
+#pragma unroll
+      for (int mm = 0; mm < PVM; ++mm) {
+        KFrag pa;
+        if constexpr (EPL == 8) {
+          const uint4 u = make_uint4(pack_bf16x2(pr[0][0], pr[0][1]), pack_bf16x2(pr[0][2], pr[0][3]),
+                                     pack_bf16x2(pr[PPI - 1][0], pr[PPI - 1][1]),
+                                     pack_bf16x2(pr[PPI - 1][2], pr[PPI - 1][3]));
+          pa = __builtin_bit_cast(KFrag, u);
+        } else {
+          pa = pr[0][mm];
+        }
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) {
+          KFrag vb;
+          if constexpr (EPL == 8) {
+            vb = __builtin_bit_cast(KFrag, bv[dt]);
+          } else {
+            const uint4 u = bv[dt];
+            vb = __uint_as_float(mm == 0 ? u.x : mm == 1 ? u.y : mm == 2 ? u.z : u.w);
+          }
+          o[dt] = M::mma(pa, vb, o[dt]);
+        }
+      }
+      m = mx;
     };
-    if (t0 < t1) {
-      // two register batches in flight: the next batch loads while this one is consumed
-      V16<T> ka[U], va[U], kb[U], vb[U];
-      load(ka, va, t0);
-      for (int tb = t0; tb < t1; tb += 2 * STEP) {
-        if (tb + STEP < t1) load(kb, vb, tb + STEP);
-        consume(ka, va, tb);
-        if (tb + STEP >= t1) break;
-        if (tb + 2 * STEP < t1) load(ka, va, tb + 2 * STEP);
-        consume(kb, vb, tb + STEP);
+    if (p0 < p1) {
+      KFrag ka[PPI][KSTEPS];
+      uint4 va[DT];
+      if constexpr (NBUF == 2) {
+        KFrag kb[PPI][KSTEPS];
+        uint4 vb2[DT];
+        load(ka, va, p0);
+        for (int pg = p0; pg < p1; pg += 2 * PPI) {
+          load(kb, vb2, pg + PPI);
+          consume(ka, va, pg);
+          load(ka, va, pg + 2 * PPI);
+          consume(kb, vb2, pg + PPI);
+        }
+      } else {
+        for (int pg = p0; pg < p1; pg += PPI) {
+          load(ka, va, pg);
+          consume(ka, va, pg);
+        }
       }
     }
-    // merge the TPI token slots that share this lane's dimension slice
+    // the four lane quads hold different tokens: add their softmax sums
+    lsum += shfl_xor(lsum, 16);
+    lsum += shfl_xor(lsum, 32);
+    if (quad == 0) {
 #pragma unroll
-    for (int o = G; o < kWave; o <<= 1) {
-      const float m2 = shfl_xor(m, o), l2 = shfl_xor(l, o);
-      const float mn = fmaxf(m, m2);
-      const float a1 = merge_scale(m, mn), a2 = merge_scale(m2, mn);
-      l = l * a1 + l2 * a2;
-#pragma unroll
-      for (int e = 0; e < EPL; ++e) acc[e] = acc[e] * a1 + shfl_xor(acc[e], o) * a2;
-      m = mn;
-    }
-    if (tr == 0) {
-#pragma unroll
-      for (int e = 0; e < EPL; ++e) s_red[w][2 + gl * EPL + e] = acc[e];
-      if (gl == 0) { s_red[w][0] = m; s_red[w][1] = l; }
+      for (int dt = 0; dt < DT; ++dt) s_red[w][2 + dt * 16 + c16] = o[dt][0];
+      if (c16 == 0) { s_red[w][0] = m; s_red[w][1] = lsum; }
     }
     __syncthreads();
     // merge the W waves' partial softmax states (log-sum-exp) and write o
-    if (w == 0 && tr == 0) {
-      float M = kNegInf, Ls = 0.f, O[EPL];
+    if (w == 0) {
+      for (int dim = lane; dim < D; dim += kWave) {
+        float Mx = kNegInf, Ls = 0.f, O = 0.f;
 #pragma unroll
-      for (int e = 0; e < EPL; ++e) O[e] = 0.f;
-#pragma unroll
-      for (int ww = 0; ww < W; ++ww) {
-        const float mc = s_red[ww][0], lc = s_red[ww][1];
-        const float mn = fmaxf(M, mc);
-        const float a1 = merge_scale(M, mn), a2 = merge_scale(mc, mn);
-        Ls = Ls * a1 + lc * a2;
-#pragma unroll
-        for (int e = 0; e < EPL; ++e) O[e] = O[e] * a1 + s_red[ww][2 + gl * EPL + e] * a2;
-        M = mn;
+        for (int ww = 0; ww < W; ++ww) {
+          const float mc = s_red[ww][0], lc = s_red[ww][1];
+          const float mn = fmaxf(Mx, mc);
+          const float a1 = merge_scale(Mx, mn), a2 = merge_scale(mc, mn);
+          Ls = Ls * a1 + lc * a2;
+          O = O * a1 + s_red[ww][2 + dim] * a2;
+          Mx = mn;
+        }
+        reinterpret_cast<T*>(a.o)[(int64_t)k * a.d + h * D + dim] = from_f<T>(O / Ls);
       }
-      V16<T> ov;
-      const float inv = 1.f / Ls;
-#pragma unroll
-      for (int e = 0; e < EPL; ++e) ov.e[e] = from_f<T>(O[e] * inv);
-      st16(reinterpret_cast<T*>(a.o) + (int64_t)k * a.d + h * D + gl * EPL, ov);
     }
   }
 }
@@ -203,7 +246,8 @@ __global__ __launch_bounds__(256) void k_attn_prefill(AttnPrefillArgs a) {
   if (q0 >= n) return;
   const int32_t* pt = c.page_table + ((int64_t)b * c.R + a.loop) * c.pages_per_seq;
   const T* pool = reinterpret_cast<const T*>(c.pool);
-  const int64_t koff = page_off(c, a.layer, 0, h, 0), voff = page_off(c, a.layer, 1, h, 0);
+  const int64_t koff = k_block(c, a.layer, h), voff = v_block(c, a.layer, h);
+  const int npages = (n + kPage - 1) / kPage;
 
   typename M::frag qf[D / KS];
   {
@@ -222,21 +266,26 @@ __global__ __launch_bounds__(256) void k_attn_prefill(AttnPrefillArgs a) {
   const int nkt = min(qt + 1, (n + BKEY - 1) / BKEY);
   for (int kt = 0; kt < nkt; ++kt) {
     __syncthreads();
+    // K rows: key-major, 16-byte pieces
     for (int ci = tid; ci < BKEY * CPK; ci += 256) {
       const int key = ci / CPK, col = (ci % CPK) * EPC;
       const int ka = kt * BKEY + key;
-      V16<T> kv, vv;
-      if (ka < n) {
-        const int64_t pb = (int64_t)pt[ka / kPage] * c.page_elems + (ka % kPage) * D + col;
-        kv = ld16(pool + pb + koff);
-        vv = ld16(pool + pb + voff);
-      } else {
-        kv.u = make_uint4(0, 0, 0, 0);
-        vv.u = make_uint4(0, 0, 0, 0);
-      }
+      V16<T> kv;
+      kv.u = make_uint4(0, 0, 0, 0);
+      if (ka < n) kv = ld16(pool + (int64_t)pt[ka / kPage] * c.page_elems + koff + (ka % kPage) * D + col);
       st16(&Ks[key * LDK + col], kv);
-#pragma unroll
-      for (int e = 0; e < EPC; ++e) Vt[(col + e) * LDV + key] = vv.e[e];
+    }
+    // V^T: each page holds [D][16 slots]; a 16-byte piece is EPC slots of one dimension
+    constexpr int VPC = kPage / EPC;  // pieces per (page, dimension)
+    for (int ci = tid; ci < (BKEY / kPage) * D * VPC; ci += 256) {
+      const int pg = ci / (D * VPC), rem = ci % (D * VPC), dim = rem / VPC, piece = rem % VPC;
+      const int pa = kt * (BKEY / kPage) + pg;  // page index within the (b, i) cache
+      V16<T> vv;
+      vv.u = make_uint4(0, 0, 0, 0);
+      // slots past n in the last page hold finite stale values; their P is 0
+      if (pa < npages)
+        vv = ld16(pool + (int64_t)pt[pa] * c.page_elems + voff + (int64_t)dim * kPage + piece * EPC);
+      st16(&Vt[dim * LDV + pg * kPage + piece * EPC], vv);
     }
     __syncthreads();
 

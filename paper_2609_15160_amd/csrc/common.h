@@ -15,6 +15,7 @@ constexpr int kWave = 64;          // CDNA wavefront width
 constexpr int kMaxLoops = 16;
 constexpr int kPlanThreads = 1024; // single-workgroup planners
 constexpr int kAttnMaxPages = 4096; // page list staged in LDS by the decode attention (max_pos <= 65536)
+constexpr int kMaxSplits = 8;       // split-K slabs of a decode residual projection
 
 // Sticky device error bits (reported through tlf_cache_stats).
 constexpr int kErrBadToken = 1;
@@ -48,9 +49,17 @@ struct CacheView {
   int max_pages, pages_per_seq, R, J, H, D;
 };
 
-// Element offset of (layer j, k-or-v, head h, slot) inside a page.
-__device__ __forceinline__ int64_t page_off(const CacheView& c, int j, int kv, int h, int slot) {
-  return ((int64_t)((j * 2 + kv) * c.H + h) * kPage + slot) * c.D;
+// Page layout: for each layer j and head h a K block [kPage slots][D] (row
+// per token) followed, after all heads' K blocks, by V blocks stored
+// transposed, [D][kPage slots], so that one dimension of four consecutive
+// slots is a single 8- or 16-byte load.
+//   K(j, h, slot, e) = k_block(j, h) + slot * D + e
+//   V(j, h, slot, e) = v_block(j, h) + e * kPage + slot
+__device__ __forceinline__ int64_t k_block(const CacheView& c, int j, int h) {
+  return (int64_t)((j * 2 + 0) * c.H + h) * kPage * c.D;
+}
+__device__ __forceinline__ int64_t v_block(const CacheView& c, int j, int h) {
+  return (int64_t)((j * 2 + 1) * c.H + h) * kPage * c.D;
 }
 
 template <typename T> __device__ __forceinline__ float to_f(T v);

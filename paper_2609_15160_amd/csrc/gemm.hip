@@ -1,23 +1,20 @@
 // MFMA GEMM for the shared block's projections and the LM head.
 //
 // out = A W^T on the active rows of a row map, with W [N][K] row-major
-// (linear-layer layout) and A either
-//   A_NORM: the float residual rows x[src(r)], normalised by RMSNorm without
-//           affine (Appendix A).  The row's sum of squares is accumulated
-//           while its K tiles stream through, and 1/rms scales the
-//           accumulator in the epilogue (RMSNorm commutes with the
-//           projection), so the norm costs no extra pass.
-//   A_BUF:  storage-dtype rows buf[r] (attention output, SwiGLU activation).
+// (linear-layer layout) and A in the storage dtype, either the normalised
+// residual rows y[src(r)] (A_SRC) or compact rows buf[r] (A_CMP).
 // Epilogues:
-//   E_QKV:    q to a buffer; k, v appended to the loop's cache pages (Eq. 11)
-//   E_RESID:  x[src(r)] += result (residual of the attention/FFN branch)
-//   E_SWIGLU: act = silu(gate) * up, gate/up columns interleaved in 16-column
-//             groups so every wave holds matching pairs
-//   E_LOGITS: float logits plus a packed (value, -index) atomicMax for greedy
+//   E_QKV:     q to a buffer; k, v appended to the loop's cache pages (Eq. 11)
+//   E_RESID:   x[src(r)] += result (residual of the attention/FFN branch)
+//   E_PARTIAL: split-K slab s of a residual projection, summed in split order
+//              by the following residual+norm kernel (deterministic, no atomics)
+//   E_SWIGLU:  act = silu(gate) * up, gate/up columns interleaved in 16-column
+//              groups so every wave holds matching pairs
+//   E_LOGITS:  float logits plus a packed (value, -index) atomicMax for greedy
 //
 // Tiling: 256 threads = 4 waves in a 2x2 grid; each wave owns MT x NT 16x16
-// MFMA tiles.  K advances 128 bytes per tile (64 bf16 / 32 f32), staged
-// through LDS with the next tile prefetched into registers.
+// MFMA tiles.  K advances 256 bytes per tile, staged through LDS from a ring
+// of PF tiles prefetched into registers; blockIdx.z selects the K split.
 #include "kernels.h"
 
 namespace tlf {
@@ -29,6 +26,8 @@ __device__ __forceinline__ unsigned int ordered_bits(float v) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
+// Element offset of the row's page plus its slot in the low 4 bits (the page
+// offset is a multiple of kPage elements), or -1.
 __device__ __forceinline__ int64_t kv_slot_base(const KvDst& kv, int r, int src) {
   const CacheView& c = kv.c;
   int b, slot;
@@ -41,50 +40,35 @@ __device__ __forceinline__ int64_t kv_slot_base(const KvDst& kv, int r, int src)
   }
   const int page = c.page_table[((int64_t)b * c.R + kv.loop) * c.pages_per_seq + slot / kPage];
   if (page < 0 || page >= c.max_pages) return -1;
-  return (int64_t)page * c.page_elems + page_off(c, kv.layer, 0, 0, slot % kPage);
+  return (int64_t)page * c.page_elems + (slot % kPage);
 }
 
-template <typename T, int MT, int NT, int AK, int EK>
+template <typename T, int MT, int NT, int PF, int AK, int EK>
 __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
   constexpr int BM = 2 * MT * 16, BN = 2 * NT * 16;
-  constexpr int BK = 128 / (int)sizeof(T);
-  constexpr int LDK = BK + 16 / (int)sizeof(T);
+  constexpr int BK = gemm_k_tile<T>();
+  constexpr int EPC = 16 / (int)sizeof(T);           // elements per 16-byte chunk
+  constexpr int CPR = BK / EPC;                      // chunks per row per K tile
+  constexpr int LDK = BK + EPC;                      // padded LDS row
   using M = Mfma<T>;
   constexpr int KS = M::KS, EPL = M::EPL;
-  // A chunks: 16-byte pieces of the source rows
-  constexpr int A_ELEM_BYTES = (AK == A_NORM) ? 4 : (int)sizeof(T);
-  constexpr int A_CPR = BK * A_ELEM_BYTES / 16;       // chunks per row per K tile
-  constexpr int A_EPC = 16 / A_ELEM_BYTES;            // elements per chunk
-  constexpr int ACH = BM * A_CPR / 256;               // chunks per thread
-  constexpr int B_CPR = 8;
-  constexpr int B_EPC = 16 / (int)sizeof(T);
-  constexpr int BCH = BN * B_CPR / 256;
-  static_assert(ACH >= 1 && BM * A_CPR % 256 == 0, "A tile split");
-  static_assert(BCH >= 1 && BN * B_CPR % 256 == 0, "B tile split");
+  constexpr int ACH = BM * CPR / 256;                // A chunks per thread
+  constexpr int BCH = BN * CPR / 256;                // B chunks per thread
+  static_assert(ACH >= 1 && BM * CPR % 256 == 0, "A tile split");
+  static_assert(BCH >= 1 && BN * CPR % 256 == 0, "B tile split");
 
   __shared__ __align__(16) T As[BM * LDK];
   __shared__ __align__(16) T Bs[BN * LDK];
-  __shared__ float inv_rms[BM];
   __shared__ int row_src_s[BM];
   __shared__ int64_t kv_base[EK == E_QKV ? BM : 1];
-  __shared__ int any_active;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
   const int r0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
+  const int split = blockIdx.z;
 
-  if (tid == 0) any_active = 0;
-  __syncthreads();
-  for (int i = tid; i < BM; i += 256) {
-    const int r = r0 + i;
-    int s = -1;
-    if (row_active(g.rm, r)) s = row_src(g.rm, r);
-    row_src_s[i] = s;
-    if (s >= 0) any_active = 1;
-    if constexpr (EK == E_QKV) kv_base[i] = (s >= 0) ? kv_slot_base(g.kv, r, s) : -1;
-  }
-  __syncthreads();
-  if (!any_active) return;
+  // decode: a tile whose first row has exited is empty (rows are depth-sorted)
+  if (g.rm.nact && r0 >= *g.rm.nact) return;
 
   // W row of output column n (clamped; columns >= N are never stored)
   auto w_row = [&](int n) -> int {
@@ -96,60 +80,70 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
     return wr < g.w_rows ? wr : g.w_rows - 1;
   };
 
-  typedef typename std::conditional<AK == A_NORM, float4, V16<T>>::type AReg;
-  AReg ra[ACH];
-  V16<T> rb[BCH];
-  float ss[ACH];
-#pragma unroll
-  for (int c = 0; c < ACH; ++c) ss[c] = 0.f;
-
-  const float* Af = reinterpret_cast<const float*>(g.A);
-  const T* Ab = reinterpret_cast<const T*>(g.A);
+  V16<T> ra[PF][ACH], rb[PF][BCH];  // ring of PF K tiles in flight
+  const T* A = reinterpret_cast<const T*>(g.A);
   const T* W = reinterpret_cast<const T*>(g.W);
+  const int k_per_split = g.K / g.splits;
+  const int k_base = split * k_per_split;
+  const int KT = k_per_split / BK;
 
-  auto load_tiles = [&](int kt) {
-#pragma unroll
-    for (int c = 0; c < ACH; ++c) {
-      const int ch = tid + c * 256, row = ch / A_CPR, col = (ch % A_CPR) * A_EPC;
-      const int s = row_src_s[row];
-      if constexpr (AK == A_NORM) {
-        float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (s >= 0) v = *reinterpret_cast<const float4*>(Af + (int64_t)s * g.lda + kt * BK + col);
-        ra[c] = v;
-      } else {
-        V16<T> v;
-        v.u = make_uint4(0, 0, 0, 0);
-        if (s >= 0) v = ld16(Ab + (int64_t)(r0 + row) * g.lda + kt * BK + col);
-        ra[c] = v;
-      }
-    }
+  auto load_b = [&](int kt, V16<T>* rb) {
+    const int kk = k_base + kt * BK;
 #pragma unroll
     for (int c = 0; c < BCH; ++c) {
-      const int ch = tid + c * 256, row = ch / B_CPR, col = (ch % B_CPR) * B_EPC;
-      rb[c] = ld16(W + (int64_t)w_row(n0 + row) * g.K + kt * BK + col);
+      const int ch = tid + c * 256, row = ch / CPR, col = (ch % CPR) * EPC;
+      rb[c] = ld16(W + (int64_t)w_row(n0 + row) * g.K + kk + col);
     }
   };
-  auto store_tiles = [&]() {
+  auto load_a = [&](int kt, V16<T>* ra) {
+    const int kk = k_base + kt * BK;
 #pragma unroll
     for (int c = 0; c < ACH; ++c) {
-      const int ch = tid + c * 256, row = ch / A_CPR, col = (ch % A_CPR) * A_EPC;
-      if constexpr (AK == A_NORM) {
-        const float4 v = ra[c];
-        // explicit fma chain: every row's sum of squares is formed the same way,
-        // whichever unrolled slot loads it
-        ss[c] = fmaf(v.w, v.w, fmaf(v.z, v.z, fmaf(v.y, v.y, fmaf(v.x, v.x, ss[c]))));
-        T* p = &As[row * LDK + col];
-        p[0] = from_f<T>(v.x); p[1] = from_f<T>(v.y); p[2] = from_f<T>(v.z); p[3] = from_f<T>(v.w);
-      } else {
-        st16(&As[row * LDK + col], ra[c]);
+      const int ch = tid + c * 256, row = ch / CPR, col = (ch % CPR) * EPC;
+      const int s = row_src_s[row];
+      V16<T> v;
+      v.u = make_uint4(0, 0, 0, 0);
+      if (s >= 0) {
+        const int64_t ar = (AK == A_SRC) ? (int64_t)s : (int64_t)(r0 + row);
+        v = ld16(A + ar * g.lda + kk + col);
       }
+      ra[c] = v;
+    }
+  };
+  auto store_tiles = [&](const V16<T>* ra, const V16<T>* rb) {
+#pragma unroll
+    for (int c = 0; c < ACH; ++c) {
+      const int ch = tid + c * 256, row = ch / CPR, col = (ch % CPR) * EPC;
+      st16(&As[row * LDK + col], ra[c]);
     }
 #pragma unroll
     for (int c = 0; c < BCH; ++c) {
-      const int ch = tid + c * 256, row = ch / B_CPR, col = (ch % B_CPR) * B_EPC;
+      const int ch = tid + c * 256, row = ch / CPR, col = (ch % CPR) * EPC;
       st16(&Bs[row * LDK + col], rb[c]);
     }
   };
+
+  // the weight tiles do not depend on which rows are active: start them first.
+  // Ring loads are never skipped (past the end they reread the last tile) so
+  // the compiler can count the tiles in flight.
+#pragma unroll
+  for (int p = 0; p < PF; ++p) load_b(min(p, KT - 1), rb[p]);
+
+  // thread t < BM resolves row r0 + t; the cache slot of a QKV row is looked
+  // up here and only consumed by the epilogue, so its latency hides behind K
+  int my_src = -1;
+  int64_t my_kv = -1;
+  if (tid < BM) {
+    const int r = r0 + tid;
+    if (row_active(g.rm, r)) my_src = row_src(g.rm, r);
+    row_src_s[tid] = my_src;
+    if constexpr (EK == E_QKV)
+      if (my_src >= 0) my_kv = kv_slot_base(g.kv, r, my_src);
+  }
+  if (!__syncthreads_or(my_src >= 0)) return;
+
+#pragma unroll
+  for (int p = 0; p < PF; ++p) load_a(min(p, KT - 1), ra[p]);
 
   f32x4 acc[MT][NT];
 #pragma unroll
@@ -157,39 +151,36 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
 #pragma unroll
     for (int j = 0; j < NT; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  const int KT = g.K / BK;
-  load_tiles(0);
-  for (int kt = 0; kt < KT; ++kt) {
-    __syncthreads();
-    store_tiles();
-    __syncthreads();
-    if (kt + 1 < KT) load_tiles(kt + 1);
+  // K tile kt lives in ring slot kt % PF; the loop is unrolled by PF so every
+  // slot index is a compile-time constant
+  for (int kt0 = 0; kt0 < KT; kt0 += PF) {
 #pragma unroll
-    for (int ks = 0; ks < BK / KS; ++ks) {
-      typename M::frag af[MT], bfr[NT];
+    for (int p = 0; p < PF; ++p) {
+      const int kt = kt0 + p;
+      if (kt >= KT) break;
+      __syncthreads();
+      store_tiles(ra[p], rb[p]);
+      __syncthreads();
+      load_b(min(kt + PF, KT - 1), rb[p]);
+      load_a(min(kt + PF, KT - 1), ra[p]);
 #pragma unroll
-      for (int i = 0; i < MT; ++i)
-        af[i] = M::load(&As[(wm * MT * 16 + i * 16 + (lane & 15)) * LDK + ks * KS + (lane >> 4) * EPL]);
+      for (int ks = 0; ks < BK / KS; ++ks) {
+        typename M::frag af[MT], bfr[NT];
 #pragma unroll
-      for (int j = 0; j < NT; ++j)
-        bfr[j] = M::load(&Bs[(wn * NT * 16 + j * 16 + (lane & 15)) * LDK + ks * KS + (lane >> 4) * EPL]);
+        for (int i = 0; i < MT; ++i)
+          af[i] = M::load(&As[(wm * MT * 16 + i * 16 + (lane & 15)) * LDK + ks * KS + (lane >> 4) * EPL]);
 #pragma unroll
-      for (int i = 0; i < MT; ++i)
+        for (int j = 0; j < NT; ++j)
+          bfr[j] = M::load(&Bs[(wn * NT * 16 + j * 16 + (lane & 15)) * LDK + ks * KS + (lane >> 4) * EPL]);
 #pragma unroll
-        for (int j = 0; j < NT; ++j) acc[i][j] = M::mma(af[i], bfr[j], acc[i][j]);
+        for (int i = 0; i < MT; ++i)
+#pragma unroll
+          for (int j = 0; j < NT; ++j) acc[i][j] = M::mma(af[i], bfr[j], acc[i][j]);
+      }
     }
   }
-
-  if constexpr (AK == A_NORM) {
-    // threads sharing a row are A_CPR consecutive lanes of one wave
-#pragma unroll
-    for (int c = 0; c < ACH; ++c) {
-      float v = ss[c];
-#pragma unroll
-      for (int o = 1; o < A_CPR; o <<= 1) v += shfl_xor(v, o);
-      const int ch = tid + c * 256;
-      if (ch % A_CPR == 0) inv_rms[ch / A_CPR] = rsqrtf(v / (float)g.K + g.eps);
-    }
+  if constexpr (EK == E_QKV) {
+    if (tid < BM) kv_base[tid] = my_kv;
     __syncthreads();
   }
 
@@ -201,13 +192,12 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
       const int rl = wm * MT * 16 + i * 16 + quad * 4 + r;
       const int src = row_src_s[rl];
       const int rg = r0 + rl;
-      const float sc = (AK == A_NORM) ? inv_rms[rl] : 1.f;
       if constexpr (EK == E_LOGITS) {
         unsigned long long best = 0ull;
 #pragma unroll
         for (int j = 0; j < NT; ++j) {
           const int n = n0 + wn * NT * 16 + j * 16 + col16;
-          const float v = acc[i][j][r] * sc;
+          const float v = acc[i][j][r];
           if (src >= 0 && n < g.N) {
             reinterpret_cast<float*>(g.out)[(int64_t)(g.out_row_off + rg) * g.ldo + n] = v;
             const unsigned long long key =
@@ -229,7 +219,7 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
           const int n = n0 + wn * NT * 16 + j * 16 + col16;  // gate column (n % 32 < 16)
           const int unit = (n >> 5) * 16 + col16;
           if (src >= 0 && unit < g.F) {
-            const float gt = acc[i][j][r] * sc, up = acc[i][j + 1][r] * sc;
+            const float gt = acc[i][j][r], up = acc[i][j + 1][r];
             const float a = gt / (1.f + __expf(-gt)) * up;
             reinterpret_cast<T*>(g.out)[(int64_t)rg * g.ldo + unit] = from_f<T>(a);
           }
@@ -239,19 +229,26 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
         for (int j = 0; j < NT; ++j) {
           const int n = n0 + wn * NT * 16 + j * 16 + col16;
           if (src < 0 || n >= g.N) continue;
-          const float v = acc[i][j][r] * sc;
+          const float v = acc[i][j][r];
           if constexpr (EK == E_RESID) {
             reinterpret_cast<float*>(g.out)[(int64_t)src * g.ldo + n] += v;
+          } else if constexpr (EK == E_PARTIAL) {
+            reinterpret_cast<float*>(g.out)[((int64_t)split * g.part_rows + rg) * g.ldo + n] = v;
           } else {  // E_QKV
             if (n < g.d) {
               reinterpret_cast<T*>(g.out)[(int64_t)rg * g.ldo + n] = from_f<T>(v);
             } else {
               const int64_t base = kv_base[rl];
               if (base >= 0) {
+                const int slot = (int)(base & (kPage - 1));
+                const int64_t page = base - slot;
                 const int nn = n - g.d, kvsel = nn / g.d, within = nn % g.d;
                 const int h = within / g.kv.c.D, e = within % g.kv.c.D;
                 T* pool = reinterpret_cast<T*>(g.kv.c.pool);
-                pool[base + (int64_t)((kvsel * g.kv.c.H + h) * kPage) * g.kv.c.D + e] = from_f<T>(v);
+                if (kvsel == 0)
+                  pool[page + k_block(g.kv.c, g.kv.layer, h) + (int64_t)slot * g.kv.c.D + e] = from_f<T>(v);
+                else
+                  pool[page + v_block(g.kv.c, g.kv.layer, h) + (int64_t)e * kPage + slot] = from_f<T>(v);
               }
             }
           }
@@ -261,32 +258,36 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
   }
 }
 
-template <typename T, int MT, int NT>
+template <typename T, int MT, int NT, int PF>
 hipError_t launch_tiles(const GemmArgs& a, AKind ak, EKind ek, hipStream_t s) {
   constexpr int BM = 2 * MT * 16, BN = 2 * NT * 16;
-  dim3 grid((a.N + BN - 1) / BN, (a.rm.rows + BM - 1) / BM);
+  const dim3 grid((a.N + BN - 1) / BN, (a.rm.rows + BM - 1) / BM, a.splits);
   if (grid.x == 0 || grid.y == 0) return hipSuccess;
-  if (ak == A_NORM && ek == E_QKV)
-    hipLaunchKernelGGL((k_gemm<T, MT, NT, A_NORM, E_QKV>), grid, dim3(256), 0, s, a);
-  else if (ak == A_BUF && ek == E_RESID)
-    hipLaunchKernelGGL((k_gemm<T, MT, NT, A_BUF, E_RESID>), grid, dim3(256), 0, s, a);
-  else if (ak == A_NORM && ek == E_SWIGLU)
-    hipLaunchKernelGGL((k_gemm<T, MT, NT, A_NORM, E_SWIGLU>), grid, dim3(256), 0, s, a);
-  else if (ak == A_NORM && ek == E_LOGITS)
-    hipLaunchKernelGGL((k_gemm<T, MT, NT, A_NORM, E_LOGITS>), grid, dim3(256), 0, s, a);
-  else
-    return hipErrorInvalidValue;
-  return hipGetLastError();
+#define TLF_GEMM_CASE(AKV, EKV)                                                       \
+  if (ak == AKV && ek == EKV) {                                                       \
+    hipLaunchKernelGGL((k_gemm<T, MT, NT, PF, AKV, EKV>), grid, dim3(256), 0, s, a);  \
+    return hipGetLastError();                                                         \
+  }
+  TLF_GEMM_CASE(A_SRC, E_QKV)
+  TLF_GEMM_CASE(A_SRC, E_SWIGLU)
+  TLF_GEMM_CASE(A_SRC, E_LOGITS)
+  TLF_GEMM_CASE(A_CMP, E_RESID)
+  TLF_GEMM_CASE(A_CMP, E_PARTIAL)
+#undef TLF_GEMM_CASE
+  return hipErrorInvalidValue;
 }
 
 }  // namespace
 
 template <typename T>
 hipError_t launch_gemm(const GemmArgs& a, AKind ak, EKind ek, bool big_tiles, hipStream_t s) {
-  constexpr int BK = 128 / (int)sizeof(T);
-  if (a.K % BK != 0) return hipErrorInvalidValue;
-  if (big_tiles) return launch_tiles<T, 4, 4>(a, ak, ek, s);
-  return launch_tiles<T, 1, 2>(a, ak, ek, s);
+  constexpr int BK = gemm_k_tile<T>();
+  if (a.splits < 1 || a.K % a.splits != 0 || (a.K / a.splits) % BK != 0) return hipErrorInvalidValue;
+  if (a.splits > 1 && ek != E_PARTIAL) return hipErrorInvalidValue;
+  // large row counts (prefill, LM head): 128x128 tiles, one K tile in flight;
+  // decode row counts: 32x64 tiles with three K tiles in flight to cover latency
+  if (big_tiles) return launch_tiles<T, 4, 4, 1>(a, ak, ek, s);
+  return launch_tiles<T, 1, 2, 3>(a, ak, ek, s);
 }
 
 template hipError_t launch_gemm<float>(const GemmArgs&, AKind, EKind, bool, hipStream_t);

@@ -42,20 +42,28 @@ struct KvDst {
   int b0 = 0, seg = 0;
 };
 
-enum AKind { A_NORM = 0, A_BUF = 1 };
-enum EKind { E_QKV = 0, E_RESID = 1, E_SWIGLU = 2, E_LOGITS = 3 };
+// A operand: A_SRC reads the normalised residual rows y[src(r)]; A_CMP reads
+// compact rows buf[r] (attention output, SwiGLU activation).  Both are in the
+// storage dtype.
+enum AKind { A_SRC = 0, A_CMP = 1 };
+// E_QKV: q to a buffer, k and v appended to the loop's cache pages.
+// E_RESID: x[src(r)] += result.  E_PARTIAL: split s writes P[s][r] (float).
+// E_SWIGLU: act = silu(gate) * up.  E_LOGITS: float logits + greedy keys.
+enum EKind { E_QKV = 0, E_RESID = 1, E_PARTIAL = 2, E_SWIGLU = 3, E_LOGITS = 4 };
 
 struct GemmArgs {
-  const void* A = nullptr;  // A_NORM: float residual rows (row = residual index); A_BUF: storage rows (row = r)
+  const void* A = nullptr;  // storage dtype rows
   int lda = 0;
   const void* W = nullptr;  // [W rows][K] storage dtype
   int N = 0;                // output columns (E_SWIGLU: 2F in the interleaved gate/up space)
   int K = 0;
   int w_rows = 0;           // rows of W (loads are clamped below it)
+  int splits = 1;           // split-K factor (E_PARTIAL only); K / splits must be a multiple of the K tile
   RowMap rm;
-  float eps = 1e-5f;
-  void* out = nullptr;      // E_QKV: q rows; E_RESID: float residual; E_SWIGLU: act rows; E_LOGITS: float logits
+  void* out = nullptr;      // E_QKV: q rows; E_RESID: float residual; E_PARTIAL: float [splits][part_rows][ldo];
+                            // E_SWIGLU: act rows; E_LOGITS: float logits
   int ldo = 0;
+  int part_rows = 0;        // E_PARTIAL: rows of one split's slab
   int out_row_off = 0;      // E_LOGITS: output row = out_row_off + r
   unsigned long long* argmax_keys = nullptr;  // E_LOGITS, may be nullptr
   KvDst kv;                 // E_QKV
@@ -65,10 +73,12 @@ struct GemmArgs {
 
 template <typename T>
 hipError_t launch_gemm(const GemmArgs& a, AKind ak, EKind ek, bool big_tiles, hipStream_t s);
+// K elements per tile of the GEMM (splits must divide K into multiples of it).
+template <typename T> constexpr int gemm_k_tile() { return 256 / (int)sizeof(T); }
 
 // ---------------------------------------------------------------------------
 // Embedding + router (Section 3.2): h0 = E[x] + P[pos], z = W_r h0 + b_r,
-// depth rule, margin.
+// depth rule, margin, and y = RMSNorm(h0).
 // ---------------------------------------------------------------------------
 struct EmbedArgs {
   const void* tok_emb = nullptr;
@@ -79,7 +89,9 @@ struct EmbedArgs {
   int rows = 0, V = 0, d = 0, R = 0;
   int prefill_T = 0;              // > 0: pos = row % T; 0: pos = seq_len[row]
   const int32_t* seq_len = nullptr;
-  float* x = nullptr;             // [rows][d]
+  float* x = nullptr;             // [rows][d] float residual
+  void* y = nullptr;              // [rows][d] RMSNorm(x) in the storage dtype
+  float eps = 1e-5f;
   int32_t* depth = nullptr;       // [rows]
   int32_t* out_depth = nullptr;   // optional [rows]
   float* out_margin = nullptr;    // optional [rows]
@@ -88,6 +100,17 @@ struct EmbedArgs {
   int32_t* err = nullptr;
 };
 template <typename T> hipError_t launch_embed_route(const EmbedArgs& a, hipStream_t s);
+
+// x[src(r)] += sum over splits of P[s][r]; y[src(r)] = RMSNorm(x[src(r)]).
+struct ResidNormArgs {
+  RowMap rm;
+  float* x = nullptr;
+  void* y = nullptr;
+  const float* partial = nullptr;  // [splits][part_rows][d]
+  int splits = 0, part_rows = 0, d = 0;
+  float eps = 1e-5f;
+};
+template <typename T> hipError_t launch_resid_norm(const ResidNormArgs& a, hipStream_t s);
 
 // ---------------------------------------------------------------------------
 // Decode planner (one workgroup): depth-sorted row order, active counts n_i,

@@ -1,83 +1,9 @@
-// Embedding + router, the decode and prefill planners, and utility kernels.
+// The decode and prefill planners, and utility kernels.
 #include "kernels.h"
 
 namespace tlf {
 
 namespace {
-
-// ---------------------------------------------------------------------------
-// h0 = E[x] + P[pos] (learned absolute position added once, Section 3.2),
-// z = W_r h0 + b_r (Eq. 2's router as a linear map), then the depth rule.
-// One wave per row; the residual row is written in float32.
-// ---------------------------------------------------------------------------
-template <typename T>
-__global__ __launch_bounds__(256) void k_embed_route(EmbedArgs a) {
-  const int lane = lane_id();
-  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (row >= a.rows) return;
-  int tok = a.tokens[row];
-  if (tok < 0 || tok >= a.V) {
-    if (lane == 0) set_err(a.err, kErrBadToken);
-    tok = 0;
-  }
-  const int pos = a.prefill_T > 0 ? row % a.prefill_T : a.seq_len[row];
-  const T* e = reinterpret_cast<const T*>(a.tok_emb) + (int64_t)tok * a.d;
-  const T* p = reinterpret_cast<const T*>(a.pos_emb) + (int64_t)pos * a.d;
-  float* x = a.x + (int64_t)row * a.d;
-  float z[kMaxLoops];
-#pragma unroll
-  for (int i = 0; i < kMaxLoops; ++i) z[i] = 0.f;
-  for (int k = lane; k < a.d; k += kWave) {
-    const float h = to_f<T>(e[k]) + to_f<T>(p[k]);
-    x[k] = h;
-#pragma unroll
-    for (int i = 0; i < kMaxLoops; ++i)
-      if (i < a.R) z[i] += a.Wr[(int64_t)i * a.d + k] * h;
-  }
-#pragma unroll
-  for (int i = 0; i < kMaxLoops; ++i) {
-    if (i < a.R) {
-      float v = z[i];
-#pragma unroll
-      for (int o = 1; o < kWave; o <<= 1) v += shfl_xor(v, o);
-      z[i] = v + a.br[i];
-    }
-  }
-  if (lane != 0) return;
-  const int R = a.R;
-  int m = 1;
-  float margin = __builtin_inff();
-  if (a.rule == 0) {  // argmax, lowest index on ties
-    int best = 0;
-    for (int i = 1; i < R; ++i)
-      if (z[i] > z[best]) best = i;
-    float second = -__builtin_inff();
-    for (int i = 0; i < R; ++i)
-      if (i != best && z[i] > second) second = z[i];
-    m = best + 1;
-    if (R > 1) margin = z[best] - second;
-  } else if (a.rule == 1) {  // cumulative probability (Eq. 2-5)
-    float mx = z[0];
-    for (int i = 1; i < R; ++i) mx = fmaxf(mx, z[i]);
-    float ex[kMaxLoops];
-    float tot = 0.f;
-    for (int i = 0; i < R; ++i) { ex[i] = __expf(z[i] - mx); tot += ex[i]; }
-    float p_sfx[kMaxLoops + 1];
-    p_sfx[R] = 0.f;
-    float run = 0.f;
-    for (int i = R - 1; i >= 0; --i) { run += ex[i]; p_sfx[i] = run / tot; }
-    p_sfx[0] = 1.f;  // p^(1) = 1: every token runs loop 1
-    m = 1;
-    for (int i = 1; i < R; ++i)
-      if (p_sfx[i] > a.threshold) m = i + 1;
-    margin = fminf(p_sfx[m - 1] - a.threshold, a.threshold - p_sfx[m]);
-  } else {
-    m = a.fixed;
-  }
-  a.depth[row] = m;
-  if (a.out_depth) a.out_depth[row] = m;
-  if (a.out_margin) a.out_margin[row] = margin;
-}
 
 // ---------------------------------------------------------------------------
 // Decode planner: one workgroup of kPlanThreads threads.
@@ -280,14 +206,6 @@ int fill_grid(int64_t n) {
 }
 
 }  // namespace
-
-template <typename T> hipError_t launch_embed_route(const EmbedArgs& a, hipStream_t s) {
-  if (a.rows <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_embed_route<T>, dim3((a.rows + 3) / 4), dim3(256), 0, s, a);
-  return hipGetLastError();
-}
-template hipError_t launch_embed_route<float>(const EmbedArgs&, hipStream_t);
-template hipError_t launch_embed_route<bf16>(const EmbedArgs&, hipStream_t);
 
 hipError_t launch_plan_decode(const DecodePlanArgs& a, hipStream_t s) {
   hipLaunchKernelGGL(k_plan_decode, dim3(1), dim3(kPlanThreads), 0, s, a);

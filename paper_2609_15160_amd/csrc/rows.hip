@@ -1,0 +1,223 @@
+// Per-row kernels: embedding + router, and residual reduction + RMSNorm.
+//
+// Both keep the float32 residual row x and write y = RMSNorm(x) (no affine,
+// Appendix A) in the storage dtype: y is the A operand of the next
+// projection (QKV, gate/up, LM head), so the norm is computed once per row
+// instead of once per output tile.  Rows of up to 4096 elements stay in
+// registers between the sum of squares and the write of y.
+#include "kernels.h"
+
+namespace tlf {
+
+namespace {
+
+constexpr int kRowChunks = 16;  // 16 x 256 elements: rows up to 4096 wide
+
+template <int CTRL>
+__device__ __forceinline__ float dpp(float x) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, 0xF, 0xF, false));
+}
+
+// Sum over the 64 lanes of a wave; every lane gets the total.
+__device__ __forceinline__ float wave_sum(float v) {
+  v += dpp<0xB1>(v);   // lane ^ 1
+  v += dpp<0x4E>(v);   // lane ^ 2
+  v += dpp<0x141>(v);  // other quad of the 8
+  v += dpp<0x140>(v);  // other half of the 16
+  v += shfl_xor(v, 16);
+  v += shfl_xor(v, 32);
+  return v;
+}
+
+template <typename T> struct V4;  // 4 storage elements
+template <> struct V4<float> {
+  static __device__ __forceinline__ float4 load(const float* p) { return *reinterpret_cast<const float4*>(p); }
+  static __device__ __forceinline__ void store(float* p, float4 v) { *reinterpret_cast<float4*>(p) = v; }
+};
+template <> struct V4<bf16> {
+  static __device__ __forceinline__ float4 load(const bf16* p) {
+    const uint2 u = *reinterpret_cast<const uint2*>(p);
+    return make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xFFFF0000u),
+                       __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xFFFF0000u));
+  }
+  static __device__ __forceinline__ void store(bf16* p, float4 v) {
+    union { bf16 h[4]; uint2 u; } o;
+    o.h[0] = (bf16)v.x; o.h[1] = (bf16)v.y; o.h[2] = (bf16)v.z; o.h[3] = (bf16)v.w;
+    *reinterpret_cast<uint2*>(p) = o.u;
+  }
+};
+
+__device__ __forceinline__ float sumsq(float4 v, float acc) {
+  return fmaf(v.w, v.w, fmaf(v.z, v.z, fmaf(v.y, v.y, fmaf(v.x, v.x, acc))));
+}
+__device__ __forceinline__ float4 scale4(float4 v, float s) { return make_float4(v.x * s, v.y * s, v.z * s, v.w * s); }
+
+// ---------------------------------------------------------------------------
+// h0 = E[x] + P[pos] (learned absolute position added once, Section 3.2),
+// z = W_r h0 + b_r (Eq. 2's router as a linear map), the depth rule, and
+// y = RMSNorm(h0) for the first projection.  One wave per row; lane l holds
+// elements 4l + 256c.
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(256) void k_embed_route(EmbedArgs a) {
+  const int lane = lane_id();
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= a.rows) return;
+  int tok = a.tokens[row];
+  if (tok < 0 || tok >= a.V) {
+    if (lane == 0) set_err(a.err, kErrBadToken);
+    tok = 0;
+  }
+  const int pos = a.prefill_T > 0 ? row % a.prefill_T : a.seq_len[row];
+  const T* e = reinterpret_cast<const T*>(a.tok_emb) + (int64_t)tok * a.d;
+  const T* p = reinterpret_cast<const T*>(a.pos_emb) + (int64_t)pos * a.d;
+  float* x = a.x + (int64_t)row * a.d;
+  float4 h[kRowChunks];
+  float ss = 0.f;
+  float z[kMaxLoops];
+#pragma unroll
+  for (int i = 0; i < kMaxLoops; ++i) z[i] = 0.f;
+#pragma unroll
+  for (int c = 0; c < kRowChunks; ++c) {
+    const int k = 4 * lane + 256 * c;
+    if (k < a.d) {
+      const float4 ev = V4<T>::load(e + k), pv = V4<T>::load(p + k);
+      h[c] = make_float4(ev.x + pv.x, ev.y + pv.y, ev.z + pv.z, ev.w + pv.w);
+    }
+  }
+#pragma unroll
+  for (int c = 0; c < kRowChunks; ++c) {
+    const int k = 4 * lane + 256 * c;
+    if (k < a.d) {
+      V4<float>::store(x + k, h[c]);
+      ss = sumsq(h[c], ss);
+#pragma unroll
+      for (int i = 0; i < kMaxLoops; ++i) {
+        if (i < a.R) {
+          const float4 w = V4<float>::load(a.Wr + (int64_t)i * a.d + k);
+          z[i] = fmaf(w.w, h[c].w, fmaf(w.z, h[c].z, fmaf(w.y, h[c].y, fmaf(w.x, h[c].x, z[i]))));
+        }
+      }
+    }
+  }
+  ss = wave_sum(ss);
+  const float inv = rsqrtf(ss / (float)a.d + a.eps);
+  T* y = reinterpret_cast<T*>(a.y) + (int64_t)row * a.d;
+#pragma unroll
+  for (int c = 0; c < kRowChunks; ++c) {
+    const int k = 4 * lane + 256 * c;
+    if (k < a.d) V4<T>::store(y + k, scale4(h[c], inv));
+  }
+#pragma unroll
+  for (int i = 0; i < kMaxLoops; ++i)
+    if (i < a.R) z[i] = wave_sum(z[i]) + a.br[i];
+  if (lane != 0) return;
+  const int R = a.R;
+  int m = 1;
+  float margin = __builtin_inff();
+  if (a.rule == 0) {  // argmax, lowest index on ties
+    int best = 0;
+    for (int i = 1; i < R; ++i)
+      if (z[i] > z[best]) best = i;
+    float second = -__builtin_inff();
+    for (int i = 0; i < R; ++i)
+      if (i != best && z[i] > second) second = z[i];
+    m = best + 1;
+    if (R > 1) margin = z[best] - second;
+  } else if (a.rule == 1) {  // cumulative probability (Eq. 2-5)
+    float mx = z[0];
+    for (int i = 1; i < R; ++i) mx = fmaxf(mx, z[i]);
+    float ex[kMaxLoops];
+    float tot = 0.f;
+    for (int i = 0; i < R; ++i) { ex[i] = __expf(z[i] - mx); tot += ex[i]; }
+    float p_sfx[kMaxLoops + 1];
+    p_sfx[R] = 0.f;
+    float run = 0.f;
+    for (int i = R - 1; i >= 0; --i) { run += ex[i]; p_sfx[i] = run / tot; }
+    p_sfx[0] = 1.f;  // p^(1) = 1: every token runs loop 1
+    m = 1;
+    for (int i = 1; i < R; ++i)
+      if (p_sfx[i] > a.threshold) m = i + 1;
+    margin = fminf(p_sfx[m - 1] - a.threshold, a.threshold - p_sfx[m]);
+  } else {
+    m = a.fixed;
+  }
+  a.depth[row] = m;
+  if (a.out_depth) a.out_depth[row] = m;
+  if (a.out_margin) a.out_margin[row] = margin;
+}
+
+// ---------------------------------------------------------------------------
+// x[src(r)] += sum_s P[s][r] (split-K partials of a residual projection, in
+// split order), then y[src(r)] = RMSNorm(x[src(r)]).  One workgroup per row:
+// thread t holds elements 4t + 1024c, and every partial slab is loaded before
+// the sum so a row costs one memory round trip.
+// ---------------------------------------------------------------------------
+constexpr int kNormChunks = 4;  // 4 x 1024 elements per row
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_resid_norm(ResidNormArgs a) {
+  __shared__ float s_part[4];
+  const int r = blockIdx.x;
+  if (!row_active(a.rm, r)) return;
+  const int tid = threadIdx.x, lane = lane_id(), w = tid >> 6;
+  const int src = row_src(a.rm, r);
+  float* x = a.x + (int64_t)src * a.d;
+  float4 h[kNormChunks];
+  float4 pv[kNormChunks][kMaxSplits];
+#pragma unroll
+  for (int c = 0; c < kNormChunks; ++c) {
+    const int k = 4 * tid + 1024 * c;
+    if (k < a.d) {
+      h[c] = V4<float>::load(x + k);
+#pragma unroll
+      for (int sp = 0; sp < kMaxSplits; ++sp)
+        if (sp < a.splits) pv[c][sp] = V4<float>::load(a.partial + ((int64_t)sp * a.part_rows + r) * a.d + k);
+    }
+  }
+  float ss = 0.f;
+#pragma unroll
+  for (int c = 0; c < kNormChunks; ++c) {
+    const int k = 4 * tid + 1024 * c;
+    if (k < a.d) {
+#pragma unroll
+      for (int sp = 0; sp < kMaxSplits; ++sp)
+        if (sp < a.splits)
+          h[c] = make_float4(h[c].x + pv[c][sp].x, h[c].y + pv[c][sp].y, h[c].z + pv[c][sp].z,
+                             h[c].w + pv[c][sp].w);
+      if (a.splits > 0) V4<float>::store(x + k, h[c]);
+      ss = sumsq(h[c], ss);
+    }
+  }
+  ss = wave_sum(ss);
+  if (lane == 0) s_part[w] = ss;
+  __syncthreads();
+  ss = (s_part[0] + s_part[1]) + (s_part[2] + s_part[3]);
+  const float inv = rsqrtf(ss / (float)a.d + a.eps);
+  T* y = reinterpret_cast<T*>(a.y) + (int64_t)src * a.d;
+#pragma unroll
+  for (int c = 0; c < kNormChunks; ++c) {
+    const int k = 4 * tid + 1024 * c;
+    if (k < a.d) V4<T>::store(y + k, scale4(h[c], inv));
+  }
+}
+
+}  // namespace
+
+template <typename T> hipError_t launch_embed_route(const EmbedArgs& a, hipStream_t s) {
+  if (a.rows <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_embed_route<T>, dim3((a.rows + 3) / 4), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+template hipError_t launch_embed_route<float>(const EmbedArgs&, hipStream_t);
+template hipError_t launch_embed_route<bf16>(const EmbedArgs&, hipStream_t);
+
+template <typename T> hipError_t launch_resid_norm(const ResidNormArgs& a, hipStream_t s) {
+  if (a.rm.rows <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_resid_norm<T>, dim3(a.rm.rows), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+template hipError_t launch_resid_norm<float>(const ResidNormArgs&, hipStream_t);
+template hipError_t launch_resid_norm<bf16>(const ResidNormArgs&, hipStream_t);
+
+}  // namespace tlf

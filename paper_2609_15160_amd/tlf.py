@@ -42,7 +42,7 @@ class Config(ctypes.Structure):
         ("max_pos", ctypes.c_int32), ("max_batch", ctypes.c_int32), ("page_tokens", ctypes.c_int32),
         ("max_pages", ctypes.c_int32), ("max_prefill_tokens", ctypes.c_int32),
         ("route_rule", ctypes.c_int32), ("route_threshold", ctypes.c_float),
-        ("fixed_depth", ctypes.c_int32), ("rms_eps", ctypes.c_float),
+        ("fixed_depth", ctypes.c_int32), ("rms_eps", ctypes.c_float), ("decode_graph", ctypes.c_int32),
     ]
 
 
@@ -129,7 +129,8 @@ def status_str(status: int) -> str:
 
 
 def make_config(model, max_batch: int, max_pos: int, max_pages: int, route_rule: str = "argmax",
-                threshold: float = 0.5, fixed_depth: int = 1, max_prefill_tokens: int = 65536) -> Config:
+                threshold: float = 0.5, fixed_depth: int = 1, max_prefill_tokens: int = 65536,
+                decode_graph: bool = True) -> Config:
     """Config from a model description with attributes like ``synth.ModelConfig``."""
     return Config(
         abi_version=ABI_VERSION, dtype=DTYPE_BF16 if model.dtype == "bf16" else DTYPE_F32,
@@ -137,7 +138,8 @@ def make_config(model, max_batch: int, max_pos: int, max_pages: int, route_rule:
         d_ff=model.d_ff, n_layers=model.n_layers, max_loops=model.max_loops, max_pos=max_pos,
         max_batch=max_batch, page_tokens=PAGE_TOKENS, max_pages=max_pages,
         max_prefill_tokens=max_prefill_tokens, route_rule=ROUTE[route_rule],
-        route_threshold=threshold, fixed_depth=fixed_depth, rms_eps=model.rms_eps)
+        route_threshold=threshold, fixed_depth=fixed_depth, rms_eps=model.rms_eps,
+        decode_graph=1 if decode_graph else 0)
 
 
 def workspace_bytes(cfg: Config) -> int:
@@ -159,7 +161,8 @@ class Session:
 
     def __init__(self, model, weights: Dict, max_batch: int, max_pos: Optional[int] = None,
                  max_pages: Optional[int] = None, route_rule: str = "argmax", threshold: float = 0.5,
-                 fixed_depth: int = 1, max_prefill_tokens: int = 65536, device: str = "cuda"):
+                 fixed_depth: int = 1, max_prefill_tokens: int = 65536, device: str = "cuda",
+                 decode_graph: bool = True):
         import torch
         self.torch = torch
         self.lib = load()
@@ -169,7 +172,7 @@ class Session:
         if max_pages is None:
             max_pages = worst_case_pages(max_batch, max_pos, model.max_loops)
         self.cfg = make_config(model, max_batch, max_pos, max_pages, route_rule, threshold,
-                               fixed_depth, max_prefill_tokens)
+                               fixed_depth, max_prefill_tokens, decode_graph)
         sdt = torch.bfloat16 if model.dtype == "bf16" else torch.float32
 
         def dev(a, dt):

@@ -156,6 +156,30 @@ def test_fp32_runs_are_bitwise_deterministic():
         assert np.array_equal(a.step_logits[s], b.step_logits[s])
 
 
+@pytest.mark.parametrize("name", ["c1", "f32-small", "c2-small"])
+def test_graph_replays_match_eager_launches(name):
+    """Decode steps replayed from the captured HIP graph equal eager launches,
+    every replay, with host reads (eager work and a sync) between replays."""
+    if name == "c1":
+        m = synth.CONFIGS["c1"]
+    elif name == "f32-small":
+        m = _f32_small(steps=12)
+    else:
+        m = synth.CONFIGS["c2"].replace(batch=6, prompt_len=80, steps=12)
+    w = synth.make_weights(m if name != "c2-small" else synth.CONFIGS["c2"])
+    prompts = synth.make_prompts(m)
+    steps = min(m.steps, 12)
+    g = parity.run_gpu(m, w, prompts, steps, max_pos=m.max_pos, decode_graph=True)
+    e = parity.run_gpu(m, w, prompts, steps, max_pos=m.max_pos, decode_graph=False)
+    for s in range(steps):
+        assert np.array_equal(g.step_tokens[s], e.step_tokens[s]), s
+        assert np.array_equal(g.step_logits[s], e.step_logits[s]), s
+        assert np.array_equal(g.step_depths[s], e.step_depths[s]), s
+    for b in range(prompts.shape[0]):
+        for i in range(m.max_loops):
+            assert np.array_equal(g.stats["index"][b][i], e.stats["index"][b][i])
+
+
 def _check_bf16(m, w, prompts, g, o, sample, tag, route_rule="argmax", fixed_depth=None):
     B, T = prompts.shape
     # router decisions of every token against the oracle router
