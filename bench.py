@@ -44,6 +44,7 @@ def decode_run(sess, torch, B, V, warmup, steps, profiled, first_tokens):
     for _ in range(warmup):
         sess.decode_into(tok[k % 2], logits, next_tok=tok[(k + 1) % 2])
         k += 1
+    log(f"warmup: {warmup} steps enqueued")
     stream = torch.cuda.current_stream()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -54,10 +55,13 @@ def decode_run(sess, torch, B, V, warmup, steps, profiled, first_tokens):
     e1.record(stream)
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1)
+    log(f"timed: {steps} steps in {ms:.1f} ms")
     sess.set_profiling(True)
-    for _ in range(profiled):
+    for p in range(profiled):
         sess.decode_into(tok[k % 2], logits, next_tok=tok[(k + 1) % 2])
         k += 1
+        if p % 4 == 3:
+            log(f"profiled: {p + 1} of {profiled} steps enqueued")
     torch.cuda.synchronize()
     st = sess.stats()
     sess.set_profiling(False)
@@ -159,6 +163,78 @@ def prefill_measure(torch, tlf, synth, name):
             "mfma_frac": flops / ms / 1e9 / BF16_PEAK_TFLOPS}
 
 
+ATTN_SOURCE = os.path.join(ROOT, "paper_2609_15160_amd", "csrc", "attn.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_decode_bf16_d768_b256x2048_traffic.json")
+CALIB_BYTES = 1 << 30  # the counted copy reads and writes exactly this many bytes
+
+
+def source_digest(path=ATTN_SOURCE):
+    import hashlib
+    return hashlib.sha256(open(path, "rb").read()).hexdigest()
+
+
+def measured_traffic():
+    """Per-launch HBM bytes of the decode attention from committed rocprofv3
+    counter runs, if they were taken on the current kernel source; else None."""
+    try:
+        rec = json.load(open(TRAFFIC_FILE))
+    except (OSError, ValueError):
+        return None
+    if rec.get("attn_source_sha256") != source_digest():
+        return None
+    return rec.get("traffic_bytes_per_launch")
+
+
+def counter_summary(fetch_csv, write_csv, last_dispatches):
+    """Summarize two rocprofv3 --pmc runs (FETCH_SIZE, then WRITE_SIZE).
+
+    Each counter (KiB per dispatch) is scaled by what it reads for the
+    calibration copy of CALIB_BYTES (the first copy kernel of the run), and
+    averaged over the last `last_dispatches` decode-attention dispatches,
+    which are the benchmark's event-timed region.
+    """
+    import csv
+
+    def load(path, counter):
+        rows = [r for r in csv.DictReader(open(path)) if r["Counter_Name"] == counter]
+        rows.sort(key=lambda r: int(r["Dispatch_Id"]))
+        copy = next(r for r in rows if "copy" in r["Kernel_Name"])
+        attn = [r for r in rows if "k_attn_decode" in r["Kernel_Name"]][-last_dispatches:]
+        factor = CALIB_BYTES / (float(copy["Counter_Value"]) * 1024.0)
+        per = sum(float(r["Counter_Value"]) for r in attn) * 1024.0 * factor / len(attn)
+        return factor, per, len(attn), float(copy["Counter_Value"])
+
+    ff, fetch, n, fcopy = load(fetch_csv, "FETCH_SIZE")
+    wf, write, n2, wcopy = load(write_csv, "WRITE_SIZE")
+    return {"attn_source_sha256": source_digest(), "dispatches": n,
+            "fetch_bytes_per_launch": fetch, "write_bytes_per_launch": write,
+            "traffic_bytes_per_launch": fetch + write,
+            "fetch_scale": ff, "write_scale": wf,
+            "calibration": f"copy of {CALIB_BYTES} bytes read {fcopy:.1f} KiB FETCH_SIZE and "
+                           f"{wcopy:.1f} KiB WRITE_SIZE"}
+
+
+def trace_summary(trace_csv, routed_launches, last_dispatches):
+    """Per-kernel durations from a rocprofv3 kernel trace of the default run,
+    plus the decode attention's average over the routed run's event-timed
+    region: its launches are the first `routed_launches` attention dispatches
+    of the trace, and the timed region is the last `last_dispatches` of those."""
+    import csv
+    import collections
+    rows = list(csv.DictReader(open(trace_csv)))
+    rows.sort(key=lambda r: int(r["Start_Timestamp"]))
+    agg = collections.defaultdict(lambda: [0, 0.0])
+    for r in rows:
+        d = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+        agg[r["Kernel_Name"]][0] += 1
+        agg[r["Kernel_Name"]][1] += d
+    attn = [r for r in rows if "k_attn_decode" in r["Kernel_Name"]][:routed_launches][-last_dispatches:]
+    durs = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in attn]
+    top = sorted(agg.items(), key=lambda kv: -kv[1][1])[:12]
+    return {"kernels": [{"name": n, "calls": c, "total_ms": t / 1e3, "avg_us": t / c} for n, (c, t) in top],
+            "attn_routed_timed_region": {"dispatches": len(durs), "avg_us": sum(durs) / len(durs)}}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -166,12 +242,31 @@ def main():
     ap.add_argument("--warmup", type=int, default=8)
     ap.add_argument("--profiled-steps", type=int, default=20,
                     help="steps after the timed region launched eagerly with HIP events around each attention launch")
-    ap.add_argument("--config", default="c3")
+    ap.add_argument("--config", default="bf16_d768_b256x2048")
     ap.add_argument("--no-fixed", action="store_true", help="skip the fixed-depth comparison")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-prefill", action="store_true", help="skip the prefill measurement")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help=f"first run a device copy of {CALIB_BYTES} bytes (counter calibration)")
+    ap.add_argument("--counter-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="summarize rocprofv3 FETCH_SIZE / WRITE_SIZE runs of this benchmark and exit")
+    ap.add_argument("--trace-summary", metavar="TRACE_CSV",
+                    help="summarize a rocprofv3 kernel trace of this benchmark's default run and exit")
     args = ap.parse_args()
+    if args.trace_summary:
+        import synth
+        m = synth.CONFIGS[args.config]
+        per_step = m.max_loops * m.n_layers
+        routed = (args.warmup + args.steps + args.profiled_steps) * per_step
+        print(json.dumps(trace_summary(args.trace_summary, routed, args.profiled_steps * per_step)))
+        return
+    if args.counter_summary:
+        import synth
+        m = synth.CONFIGS[args.config]
+        last = args.profiled_steps * m.max_loops * m.n_layers  # attention launches per step: R x J
+        print(json.dumps(counter_summary(*args.counter_summary, last)))
+        return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path (decode shards by sequence "
@@ -187,6 +282,14 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
     torch.cuda.set_device(0)
+    if args.copy_calibration:
+        src = torch.ones(CALIB_BYTES // 4, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+        torch.cuda.empty_cache()
     base = synth.CONFIGS[args.config]
     if args.warmup + args.steps + args.profiled_steps > base.steps or args.profiled_steps < 1:
         print(f"warmup + steps + profiled-steps must be <= {base.steps} for {args.config} "
@@ -230,7 +333,7 @@ def main():
                    "batch": B, "prompt": T, "max_loops": model.max_loops, "layers": model.n_layers,
                    "mean_depth": mean_depth},
         "roofline": {"bound": "hbm", "kernel": "k_attn_decode", "achieved": attn_gbs, "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": attn_gbs / HBM_PEAK_GBS, "traffic": None,
+                     "unit": "GB/s", "frac": attn_gbs / HBM_PEAK_GBS, "traffic": measured_traffic(),
                      "launches": st["attn_launches"], "avg_launch_us": st["attn_ms"] * 1e3 / st["attn_launches"],
                      "algo_bytes_per_launch": per_launch,
                      "measured": f"HIP events around each attention launch over {args.profiled_steps} decode "
@@ -252,8 +355,8 @@ def main():
                               "routed_speedup": fms / ms}
         log(f"fixed depth {model.max_loops}: {fms / args.steps:.3f} ms/step")
     if not args.no_prefill:
-        out["prefill_c5"] = prefill_measure(torch, tlf, synth, "c5")
-        log(f"prefill c5: {out['prefill_c5']['ms']:.2f} ms")
+        out["prefill"] = prefill_measure(torch, tlf, synth, "bf16_d1024_prefill_b8x4096")
+        log(f"prefill 8x4096: {out['prefill']['ms']:.2f} ms")
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline(model, w, prompts, args.cpu_seconds)
         log(f"cpu baseline: {out['cpu_baseline']['value']:.3f} tokens/s")

@@ -183,23 +183,23 @@ class ModelConfig:
 
 CONFIGS: Dict[str, ModelConfig] = {
     # Tiny fp32 model: one-layer shared block, batch 1, 32-token prompt.
-    "c1": ModelConfig("c1", "f32", vocab=512, d_model=64, n_heads=4, head_dim=16,
+    "f32_tiny_b1x32": ModelConfig("f32_tiny_b1x32", "f32", vocab=512, d_model=64, n_heads=4, head_dim=16,
                       d_ff=256, n_layers=1, max_loops=4, batch=1, prompt_len=32,
                       steps=32, router_bias="zero"),
     # 2-layer shared block, d=768, bf16, batch 32 x 512 prompt, 256 steps.
-    "c2": ModelConfig("c2", "bf16", vocab=32000, d_model=768, n_heads=12, head_dim=64,
+    "bf16_d768_b32x512": ModelConfig("bf16_d768_b32x512", "bf16", vocab=32000, d_model=768, n_heads=12, head_dim=64,
                       d_ff=2048, n_layers=2, max_loops=8, batch=32, prompt_len=512,
                       steps=256, router_bias="calibrated"),
     # Same model, cache-bound regime: batch 256 x 2048 prompt, 128 steps.
-    "c3": ModelConfig("c3", "bf16", vocab=32000, d_model=768, n_heads=12, head_dim=64,
+    "bf16_d768_b256x2048": ModelConfig("bf16_d768_b256x2048", "bf16", vocab=32000, d_model=768, n_heads=12, head_dim=64,
                       d_ff=2048, n_layers=2, max_loops=8, batch=256, prompt_len=2048,
                       steps=128, router_bias="calibrated"),
     # Larger model: d=2048, 16 heads x 128, batch 64 x 4096 prompt, 128 steps.
-    "c4": ModelConfig("c4", "bf16", vocab=32000, d_model=2048, n_heads=16, head_dim=128,
+    "bf16_d2048_b64x4096": ModelConfig("bf16_d2048_b64x4096", "bf16", vocab=32000, d_model=2048, n_heads=16, head_dim=128,
                       d_ff=5504, n_layers=2, max_loops=8, batch=64, prompt_len=4096,
                       steps=128, router_bias="calibrated"),
     # Prefill-only: d=1024, 16 x 64, batch 8 x 4096.
-    "c5": ModelConfig("c5", "bf16", vocab=32000, d_model=1024, n_heads=16, head_dim=64,
+    "bf16_d1024_prefill_b8x4096": ModelConfig("bf16_d1024_prefill_b8x4096", "bf16", vocab=32000, d_model=1024, n_heads=16, head_dim=64,
                       d_ff=2816, n_layers=2, max_loops=8, batch=8, prompt_len=4096,
                       steps=0, router_bias="calibrated"),
 }

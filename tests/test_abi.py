@@ -55,7 +55,7 @@ int main(void) {
 
 
 def _cfg(**kw):
-    m = synth.CONFIGS["c3"]
+    m = synth.CONFIGS["bf16_d768_b256x2048"]
     c = tlf.make_config(m, max_batch=256, max_pos=m.max_pos,
                         max_pages=tlf.worst_case_pages(256, m.max_pos, m.max_loops))
     for k, v in kw.items():
@@ -65,7 +65,7 @@ def _cfg(**kw):
 
 def test_size_query_needs_no_device(lib):
     need = tlf.workspace_bytes(_cfg())
-    m = synth.CONFIGS["c3"]
+    m = synth.CONFIGS["bf16_d768_b256x2048"]
     page_bytes = m.n_layers * 2 * m.d_model * 16 * 2
     pool = tlf.worst_case_pages(256, m.max_pos, m.max_loops) * page_bytes
     assert pool < need < pool * 1.2
@@ -97,7 +97,7 @@ def test_route_parameters_validated(lib):
 
 def test_bf16_head_dim_16_rejected_f32_accepted(lib):
     need = ctypes.c_size_t(0)
-    c = tlf.make_config(synth.CONFIGS["c1"], 1, 64, 64)
+    c = tlf.make_config(synth.CONFIGS["f32_tiny_b1x32"], 1, 64, 64)
     assert lib.tlf_init(ctypes.byref(c), None, None, 0, ctypes.byref(need), None, None) == tlf.E_NEED_WORKSPACE
     c.dtype = tlf.DTYPE_BF16
     assert lib.tlf_init(ctypes.byref(c), None, None, 0, ctypes.byref(need), None, None) == tlf.E_INVALID_ARG

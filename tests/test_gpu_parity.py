@@ -65,13 +65,13 @@ def _check_f32(m, w, prompts, g, o, tag):
     assert np.all(np.isfinite(g.prefill_logits))
 
 
-def test_c1_fp32_decode_parity():
-    m = synth.CONFIGS["c1"]
+def test_f32_tiny_decode_parity():
+    m = synth.CONFIGS["f32_tiny_b1x32"]
     w = synth.make_weights(m)
     prompts = synth.make_prompts(m)
     g = parity.run_gpu(m, w, prompts, m.steps)
     o = parity.run_oracle(m, w, prompts, g.step_tokens)
-    _check_f32(m, w, prompts, g, o, "c1")
+    _check_f32(m, w, prompts, g, o, "f32_tiny_b1x32")
     # the oracle's own greedy choice agrees wherever its top-2 gap exceeds the tolerance
     for s in range(m.steps):
         lo = o.step_logits[s]
@@ -80,14 +80,14 @@ def test_c1_fp32_decode_parity():
         assert np.all(g.step_next[s][clear] == np.argmax(lo, axis=-1)[clear])
 
 
-def test_c1_prefill_all_positions():
-    m = synth.CONFIGS["c1"]
+def test_f32_tiny_prefill_all_positions():
+    m = synth.CONFIGS["f32_tiny_b1x32"]
     w = synth.make_weights(m)
     prompts = synth.make_prompts(m)
     g = parity.run_gpu(m, w, prompts, 0, all_logits=True, max_pos=m.max_pos)
     o = parity.run_oracle(m, w, prompts, [], all_logits=True)
     err = _max_err(g.prefill_logits, o.prefill_logits)
-    _report("c1-all-logits", max_abs_logit_err=f"{err:.3g}")
+    _report("f32_tiny-all-logits", max_abs_logit_err=f"{err:.3g}")
     assert err <= F32_TOL
 
 
@@ -147,7 +147,7 @@ def test_prefill_in_sequence_groups_is_identical():
 
 
 def test_fp32_runs_are_bitwise_deterministic():
-    m = synth.CONFIGS["c1"]
+    m = synth.CONFIGS["f32_tiny_b1x32"]
     w = synth.make_weights(m)
     prompts = synth.make_prompts(m)
     a = parity.run_gpu(m, w, prompts, 8)
@@ -156,17 +156,17 @@ def test_fp32_runs_are_bitwise_deterministic():
         assert np.array_equal(a.step_logits[s], b.step_logits[s])
 
 
-@pytest.mark.parametrize("name", ["c1", "f32-small", "c2-small"])
+@pytest.mark.parametrize("name", ["f32_tiny_b1x32", "f32-small", "bf16_d768-small"])
 def test_graph_replays_match_eager_launches(name):
     """Decode steps replayed from the captured HIP graph equal eager launches,
     every replay, with host reads (eager work and a sync) between replays."""
-    if name == "c1":
-        m = synth.CONFIGS["c1"]
+    if name == "f32_tiny_b1x32":
+        m = synth.CONFIGS["f32_tiny_b1x32"]
     elif name == "f32-small":
         m = _f32_small(steps=12)
     else:
-        m = synth.CONFIGS["c2"].replace(batch=6, prompt_len=80, steps=12)
-    w = synth.make_weights(m if name != "c2-small" else synth.CONFIGS["c2"])
+        m = synth.CONFIGS["bf16_d768_b32x512"].replace(batch=6, prompt_len=80, steps=12)
+    w = synth.make_weights(m if name != "bf16_d768-small" else synth.CONFIGS["bf16_d768_b32x512"])
     prompts = synth.make_prompts(m)
     steps = min(m.steps, 12)
     g = parity.run_gpu(m, w, prompts, steps, max_pos=m.max_pos, decode_graph=True)
@@ -211,20 +211,20 @@ def _check_bf16(m, w, prompts, g, o, sample, tag, route_rule="argmax", fixed_dep
     assert np.all(np.isfinite(g.prefill_logits))
 
 
-def test_c2_bf16_parity_sampled_sequences():
-    m = synth.CONFIGS["c2"]
+def test_bf16_d768_b32x512_parity_sampled_sequences():
+    m = synth.CONFIGS["bf16_d768_b32x512"]
     w = synth.make_weights(m)
     prompts = synth.make_prompts(m)
     steps = 12
     sample = [0, 13, 31]
     g = parity.run_gpu(m, w, prompts, steps, max_pos=m.max_pos, keep_logits_rows=sample)
     o = parity.run_oracle(m, w, prompts[sample], [t[sample] for t in g.step_tokens])
-    _check_bf16(m, w, prompts, g, o, sample, "c2")
+    _check_bf16(m, w, prompts, g, o, sample, "bf16_d768_b32x512")
 
 
 def test_bf16_fixed_depth_ragged_prompt():
-    m = synth.CONFIGS["c2"].replace(batch=4, prompt_len=77, steps=6)
-    w = synth.make_weights(synth.CONFIGS["c2"])
+    m = synth.CONFIGS["bf16_d768_b32x512"].replace(batch=4, prompt_len=77, steps=6)
+    w = synth.make_weights(synth.CONFIGS["bf16_d768_b32x512"])
     prompts = synth.make_prompts(m)
     sample = [1, 3]
     g = parity.run_gpu(m, w, prompts, m.steps, route_rule="fixed", fixed_depth=8, max_pos=m.max_pos,
@@ -236,16 +236,16 @@ def test_bf16_fixed_depth_ragged_prompt():
 
 
 @pytest.mark.slow
-def test_c3_full_size_sampled_sequences():
+def test_bf16_d768_b256x2048_sampled_sequences():
     """The benchmark's workload (batch 256 x 2048 prompt) with the oracle on two sequences."""
-    m = synth.CONFIGS["c3"]
+    m = synth.CONFIGS["bf16_d768_b256x2048"]
     w = synth.make_weights(m)
     prompts = synth.make_prompts(m)
     steps = 3
     sample = [0, 255]
     g = parity.run_gpu(m, w, prompts, steps, max_pos=m.max_pos, keep_logits_rows=sample)
     o = parity.run_oracle(m, w, prompts[sample], [t[sample] for t in g.step_tokens])
-    _check_bf16(m, w, prompts, g, o, sample, "c3")
+    _check_bf16(m, w, prompts, g, o, sample, "bf16_d768_b256x2048")
 
 
 # ---------------------------------------------------------------------------
