@@ -64,9 +64,12 @@ extern "C" {
 #define TLF_E_HIP (-5)            /* a HIP runtime call failed; the context is poisoned */
 #define TLF_E_DEVICE (-6)         /* the device found a bad input (token id out of range) */
 
-/* Storage dtype of embeddings, block weights, activations between kernels and
- * the KV cache.  The residual stream, router, softmax, accumulators and logits
- * are float32 in both cases. */
+/* Storage dtype of embeddings, block weights and the KV cache.  The residual
+ * stream, the activations passed between kernels (normalised rows, q,
+ * attention output, SwiGLU output), router, softmax, accumulators and logits
+ * are float32 in both cases; with bf16 weights each float32 activation enters
+ * a matrix product as the sum of two bf16 parts (hi + lo), so only the weights,
+ * the cached k and v, and the attention probabilities are rounded to bf16. */
 #define TLF_DTYPE_F32 0
 #define TLF_DTYPE_BF16 1
 

@@ -68,7 +68,8 @@ class Model:
     ``weights`` is the dict from ``synth.make_weights``: tok_emb [V][d],
     pos_emb [P][d], router_w [R][d], router_b [R], and per layer w_qkv [3d][d],
     w_o [d][d], w_gate_up [2F][d], w_down [d][F] (linear-layer [out][in] layout,
-    so a projection is ``y @ W.T``).
+    so a projection is ``y @ W.T``).  An optional ``lm_head`` [V][d] replaces
+    the head tied to the token embedding (the tied head is the default).
 
     ``round_bf16=True`` rounds q, k, v, the normalised GEMM inputs, the
     attention output and the SwiGLU activation to bf16, which are the points
@@ -85,6 +86,8 @@ class Model:
         self.Wr = f64(weights["router_w"])
         self.br = f64(weights["router_b"])
         self.V, self.d = self.E.shape
+        head = weights.get("lm_head")
+        self.head = self.E if head is None else f64(head)
         self.R = self.Wr.shape[0]
         self.H, self.D = n_heads, head_dim
         if self.H * self.D != self.d:
@@ -318,8 +321,8 @@ def _layer(model: Model, j: int, X: np.ndarray, attn_fn) -> np.ndarray:
 
 
 def lm_head(model: Model, h: np.ndarray) -> np.ndarray:
-    """Final RMSNorm and tied LM head: logits = RMSNorm(h) E^T."""
-    return model.st(rms_norm(h, model.eps)) @ model.E.T
+    """Final RMSNorm and LM head: logits = RMSNorm(h) E^T for the tied head."""
+    return model.st(rms_norm(h, model.eps)) @ model.head.T
 
 
 def greedy(logits: np.ndarray) -> np.ndarray:

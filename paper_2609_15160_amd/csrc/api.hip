@@ -50,22 +50,22 @@ bool make_layout(const tlf_config& c, Layout* L) {
   sz[B_DEPTH_HIST] = R * 8;
   sz[B_STEP_STATS] = kStatCount * 8;
   sz[B_X_DEC] = B * d * 4;
-  sz[B_Y_DEC] = B * d * s;
+  sz[B_Y_DEC] = B * d * 4;
   sz[B_DEPTH_DEC] = B * 4;
   sz[B_PERM] = B * 4;
   sz[B_NACT] = R * 4;
-  sz[B_Q_DEC] = B * d * s;
-  sz[B_O_DEC] = B * d * s;
-  sz[B_ACT_DEC] = B * F * s;
+  sz[B_Q_DEC] = B * d * 4;
+  sz[B_O_DEC] = B * d * 4;
+  sz[B_ACT_DEC] = B * F * 4;
   sz[B_KEYS] = B * 8;
   sz[B_PARTIAL] = (int64_t)kMaxSplits * B * d * 4;
   sz[B_X_PRE] = P * d * 4;
-  sz[B_Y_PRE] = P * d * s;
+  sz[B_Y_PRE] = P * d * 4;
   sz[B_DEPTH_PRE] = P * 4;
   sz[B_TOK_IDX] = R * P * 4;
-  sz[B_Q_PRE] = P * d * s;
-  sz[B_O_PRE] = P * d * s;
-  sz[B_ACT_PRE] = P * F * s;
+  sz[B_Q_PRE] = P * d * 4;
+  sz[B_O_PRE] = P * d * 4;
+  sz[B_ACT_PRE] = P * F * 4;
   size_t off = 0;
   for (int i = 0; i < B_COUNT; ++i) {
     if (sz[i] < 0) return false;
@@ -231,7 +231,7 @@ int run_prefill(tlf_ctx* ctx, int B, int T_, const int32_t* tokens, float* logit
   TLF_HIP(launch_fill_u64(ctx->cv.depth_hist, 0ull, R, s));
   const int G = std::max(1, ctx->L.pre_rows / T_);
   float* x = ctx->buf<float>(B_X_PRE);
-  void* y = ctx->buf<void>(B_Y_PRE);
+  float* y = ctx->buf<float>(B_Y_PRE);
   for (int b0 = 0; b0 < B; b0 += G) {
     const int Gc = std::min(G, B - b0);
     const int rows = Gc * T_;
@@ -264,29 +264,29 @@ int run_prefill(tlf_ctx* ctx, int B, int T_, const int32_t* tokens, float* logit
         const tlf_layer_weights& lw = ctx->layers[j];
         GemmArgs q;
         q.A = y; q.lda = d; q.W = lw.w_qkv; q.N = 3 * d; q.K = d; q.w_rows = 3 * d; q.rm = rm;
-        q.out = ctx->buf<void>(B_Q_PRE); q.ldo = d; q.d = d;
+        q.out = ctx->buf<float>(B_Q_PRE); q.ldo = d; q.d = d;
         q.kv.c = ctx->cv; q.kv.loop = i; q.kv.layer = j; q.kv.prefill = 1; q.kv.b0 = b0; q.kv.seg = T_;
         TLF_HIP(launch_gemm<T>(q, A_SRC, E_QKV, true, s));
 
         AttnPrefillArgs at;
         at.c = ctx->cv; at.loop = i; at.layer = j; at.d = d; at.b0 = b0; at.G = Gc; at.T = T_;
-        at.q = ctx->buf<void>(B_Q_PRE); at.o = ctx->buf<void>(B_O_PRE);
+        at.q = ctx->buf<float>(B_Q_PRE); at.o = ctx->buf<float>(B_O_PRE);
         at.scale_log2 = 1.4426950408889634f / std::sqrt((float)c.head_dim);
         TLF_HIP(launch_attn_prefill<T>(at, s));
 
         GemmArgs o;
-        o.A = ctx->buf<void>(B_O_PRE); o.lda = d; o.W = lw.w_o; o.N = d; o.K = d; o.w_rows = d; o.rm = rm;
+        o.A = ctx->buf<float>(B_O_PRE); o.lda = d; o.W = lw.w_o; o.N = d; o.K = d; o.w_rows = d; o.rm = rm;
         o.out = x; o.ldo = d;
         TLF_HIP(launch_gemm<T>(o, A_CMP, E_RESID, true, s));
         TLF_HIP(launch_resid_norm<T>(rn, s));
 
         GemmArgs gu;
         gu.A = y; gu.lda = d; gu.W = lw.w_gate_up; gu.N = 2 * F; gu.K = d; gu.w_rows = 2 * F; gu.rm = rm;
-        gu.out = ctx->buf<void>(B_ACT_PRE); gu.ldo = F; gu.F = F;
+        gu.out = ctx->buf<float>(B_ACT_PRE); gu.ldo = F; gu.F = F;
         TLF_HIP(launch_gemm<T>(gu, A_SRC, E_SWIGLU, true, s));
 
         GemmArgs dn;
-        dn.A = ctx->buf<void>(B_ACT_PRE); dn.lda = F; dn.W = lw.w_down; dn.N = d; dn.K = F; dn.w_rows = d;
+        dn.A = ctx->buf<float>(B_ACT_PRE); dn.lda = F; dn.W = lw.w_down; dn.N = d; dn.K = F; dn.w_rows = d;
         dn.rm = rm; dn.out = x; dn.ldo = d;
         TLF_HIP(launch_gemm<T>(dn, A_CMP, E_RESID, true, s));
         TLF_HIP(launch_resid_norm<T>(rn, s));
@@ -313,7 +313,7 @@ int run_decode(tlf_ctx* ctx, hipStream_t s, const int32_t* tokens, float* logits
   const tlf_config& c = ctx->cfg;
   const int d = c.d_model, F = c.d_ff, R = c.max_loops, B = ctx->batch;
   float* x = ctx->buf<float>(B_X_DEC);
-  void* y = ctx->buf<void>(B_Y_DEC);
+  float* y = ctx->buf<float>(B_Y_DEC);
   int32_t* perm = ctx->buf<int32_t>(B_PERM);
   int32_t* nact = ctx->buf<int32_t>(B_NACT);
   float* part = ctx->buf<float>(B_PARTIAL);
@@ -349,13 +349,13 @@ int run_decode(tlf_ctx* ctx, hipStream_t s, const int32_t* tokens, float* logits
       const tlf_layer_weights& lw = ctx->layers[j];
       GemmArgs q;
       q.A = y; q.lda = d; q.W = lw.w_qkv; q.N = 3 * d; q.K = d; q.w_rows = 3 * d; q.rm = rm;
-      q.out = ctx->buf<void>(B_Q_DEC); q.ldo = d; q.d = d;
+      q.out = ctx->buf<float>(B_Q_DEC); q.ldo = d; q.d = d;
       q.kv.c = ctx->cv; q.kv.loop = i; q.kv.layer = j; q.kv.prefill = 0;
       TLF_HIP(launch_gemm<T>(q, A_SRC, E_QKV, false, s));
 
       AttnDecodeArgs at;
       at.c = ctx->cv; at.loop = i; at.layer = j; at.d = d; at.perm = perm; at.nact = nact + i;
-      at.q = ctx->buf<void>(B_Q_DEC); at.o = ctx->buf<void>(B_O_DEC);
+      at.q = ctx->buf<float>(B_Q_DEC); at.o = ctx->buf<float>(B_O_DEC);
       at.scale_log2 = 1.4426950408889634f / std::sqrt((float)c.head_dim);
       at.waves = attn_waves(ctx);
       at.grid = ctx->cus * ctx->attn_blocks[at.waves == 4 ? 0 : 1];
@@ -368,7 +368,7 @@ int run_decode(tlf_ctx* ctx, hipStream_t s, const int32_t* tokens, float* logits
       }
 
       GemmArgs o;
-      o.A = ctx->buf<void>(B_O_DEC); o.lda = d; o.W = lw.w_o; o.N = d; o.K = d; o.w_rows = d; o.rm = rm;
+      o.A = ctx->buf<float>(B_O_DEC); o.lda = d; o.W = lw.w_o; o.N = d; o.K = d; o.w_rows = d; o.rm = rm;
       o.splits = split_o; o.out = part; o.ldo = d; o.part_rows = c.max_batch;
       TLF_HIP(launch_gemm<T>(o, A_CMP, E_PARTIAL, false, s));
       ResidNormArgs rn;
@@ -378,11 +378,11 @@ int run_decode(tlf_ctx* ctx, hipStream_t s, const int32_t* tokens, float* logits
 
       GemmArgs gu;
       gu.A = y; gu.lda = d; gu.W = lw.w_gate_up; gu.N = 2 * F; gu.K = d; gu.w_rows = 2 * F; gu.rm = rm;
-      gu.out = ctx->buf<void>(B_ACT_DEC); gu.ldo = F; gu.F = F;
+      gu.out = ctx->buf<float>(B_ACT_DEC); gu.ldo = F; gu.F = F;
       TLF_HIP(launch_gemm<T>(gu, A_SRC, E_SWIGLU, false, s));
 
       GemmArgs dn;
-      dn.A = ctx->buf<void>(B_ACT_DEC); dn.lda = F; dn.W = lw.w_down; dn.N = d; dn.K = F; dn.w_rows = d;
+      dn.A = ctx->buf<float>(B_ACT_DEC); dn.lda = F; dn.W = lw.w_down; dn.N = d; dn.K = F; dn.w_rows = d;
       dn.rm = rm; dn.splits = split_d; dn.out = part; dn.ldo = d; dn.part_rows = c.max_batch;
       TLF_HIP(launch_gemm<T>(dn, A_CMP, E_PARTIAL, false, s));
       rn.splits = split_d;

@@ -23,13 +23,6 @@ namespace {
 
 constexpr float kNegInf = -__builtin_inff();
 
-// Two floats rounded to bf16 (nearest even) in one 32-bit word, low half first.
-__device__ __forceinline__ unsigned int pack_bf16x2(float lo, float hi) {
-  const bf16 a = (bf16)lo, b = (bf16)hi;
-  return (unsigned int)__builtin_bit_cast(unsigned short, a) |
-         ((unsigned int)__builtin_bit_cast(unsigned short, b) << 16);
-}
-
 __device__ __forceinline__ float merge_scale(float m, float mn) {
   return m == kNegInf ? 0.f : exp2f(m - mn);
 }
@@ -45,6 +38,7 @@ __global__ __launch_bounds__(W * 64) void k_attn_decode(AttnDecodeArgs a) {
   constexpr int DT = D / 16;                                // output dimension tiles
   constexpr int PVM = 4 * PPI / EPL;                        // P.V MFMAs per iteration
   constexpr int NBUF = D * (int)sizeof(T) <= 128 ? 2 : 1;   // batches in flight
+  constexpr int NQ = EPL == 8 ? 2 : 1;                      // parts of q (hi, lo)
   static_assert(KSTEPS >= 1 && D % 16 == 0, "head_dim");
   static_assert(4 * PPI % EPL == 0, "P.V k-slots");
   // V^T fragment per dimension tile: 4 consecutive slots of one dimension from
@@ -76,12 +70,16 @@ __global__ __launch_bounds__(W * 64) void k_attn_decode(AttnDecodeArgs a) {
     const int64_t koff = k_block(c, a.layer, h) + (int64_t)c16 * D + quad * EPL;
     const int64_t voff = v_block(c, a.layer, h) + (int64_t)c16 * kPage + quad * 4;
 
-    // q as the B operand of S = K q^T, the same in all 16 columns
-    KFrag qf[KSTEPS];
+    // q (float32) as the B operand of S = K q^T, the same in all 16 columns;
+    // against bf16 keys it is split into hi and lo parts, one product each
+    KFrag qf[NQ][KSTEPS];
     {
-      const T* qp = reinterpret_cast<const T*>(a.q) + (int64_t)k * a.d + h * D + quad * EPL;
+      const float* qp = a.q + (int64_t)k * a.d + h * D + quad * EPL;
 #pragma unroll
-      for (int ks = 0; ks < KSTEPS; ++ks) qf[ks] = M::load(qp + ks * KS);
+      for (int ks = 0; ks < KSTEPS; ++ks) {
+        if constexpr (NQ == 2) split_frag(qp + ks * KS, qf[0][ks], qf[NQ - 1][ks]);
+        else qf[0][ks] = qp[ks * KS];
+      }
     }
     f32x4 o[DT];
 #pragma unroll
@@ -120,7 +118,9 @@ __global__ __launch_bounds__(W * 64) void k_attn_decode(AttnDecodeArgs a) {
       for (int p = 0; p < PPI; ++p) {
         f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int ks = 0; ks < KSTEPS; ++ks) acc = M::mma(bk[p][ks], qf[ks], acc);
+        for (int ks = 0; ks < KSTEPS; ++ks)
+#pragma unroll
+          for (int qa = 0; qa < NQ; ++qa) acc = M::mma(bk[p][ks], qf[qa][ks], acc);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int t = (pg + p) * kPage + 4 * quad + r;
@@ -213,7 +213,7 @@ __global__ __launch_bounds__(W * 64) void k_attn_decode(AttnDecodeArgs a) {
           O = O * a1 + s_red[ww][2 + dim] * a2;
           Mx = mn;
         }
-        reinterpret_cast<T*>(a.o)[(int64_t)k * a.d + h * D + dim] = from_f<T>(O / Ls);
+        a.o[(int64_t)k * a.d + h * D + dim] = O / Ls;
       }
     }
   }
@@ -249,12 +249,18 @@ __global__ __launch_bounds__(256) void k_attn_prefill(AttnPrefillArgs a) {
   const int64_t koff = k_block(c, a.layer, h), voff = v_block(c, a.layer, h);
   const int npages = (n + kPage - 1) / kPage;
 
-  typename M::frag qf[D / KS];
+  // q (float32) as the A operand of S = Q K^T; against bf16 keys it is split
+  // into hi and lo parts, one product each
+  constexpr int NQ = EPL == 8 ? 2 : 1;
+  typename M::frag qf[NQ][D / KS];
   {
     const int qrow = min(q0 + w * 16 + c16, n - 1);
-    const T* qp = reinterpret_cast<const T*>(a.q) + ((int64_t)g * a.T + qrow) * a.d + h * D;
+    const float* qp = a.q + ((int64_t)g * a.T + qrow) * a.d + h * D + quad * EPL;
 #pragma unroll
-    for (int ks = 0; ks < D / KS; ++ks) qf[ks] = M::load(qp + ks * KS + quad * EPL);
+    for (int ks = 0; ks < D / KS; ++ks) {
+      if constexpr (NQ == 2) split_frag(qp + ks * KS, qf[0][ks], qf[NQ - 1][ks]);
+      else qf[0][ks] = qp[ks * KS];
+    }
   }
   f32x4 o[DT];
 #pragma unroll
@@ -294,8 +300,11 @@ __global__ __launch_bounds__(256) void k_attn_prefill(AttnPrefillArgs a) {
     for (int nt = 0; nt < 4; ++nt) {
       s[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int ks = 0; ks < D / KS; ++ks)
-        s[nt] = M::mma(qf[ks], M::load(&Ks[(nt * 16 + c16) * LDK + ks * KS + quad * EPL]), s[nt]);
+      for (int ks = 0; ks < D / KS; ++ks) {
+        const typename M::frag kf = M::load(&Ks[(nt * 16 + c16) * LDK + ks * KS + quad * EPL]);
+#pragma unroll
+        for (int qa = 0; qa < NQ; ++qa) s[nt] = M::mma(qf[qa][ks], kf, s[nt]);
+      }
     }
     float alpha[4];
 #pragma unroll
@@ -349,10 +358,10 @@ __global__ __launch_bounds__(256) void k_attn_prefill(AttnPrefillArgs a) {
     for (int off = 1; off < 16; off <<= 1) lt += shfl_xor(lt, off);
     const int row = q0 + w * 16 + quad * 4 + r;
     if (row >= n) continue;
-    T* op = reinterpret_cast<T*>(a.o) + ((int64_t)g * a.T + row) * a.d + h * D;
+    float* op = a.o + ((int64_t)g * a.T + row) * a.d + h * D;
     const float inv = 1.f / lt;
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt) op[dt * 16 + c16] = from_f<T>(o[dt][r] * inv);
+    for (int dt = 0; dt < DT; ++dt) op[dt * 16 + c16] = o[dt][r] * inv;
   }
 }
 

@@ -110,6 +110,44 @@ template <> struct Mfma<float> {
   }
 };
 
+// Activations are float32.  A bf16 MFMA takes one as the sum of two bf16
+// values, hi = bf16(v) and lo = bf16(v - hi), and runs once per part: the
+// product with a bf16 weight is then exact to about 2^-16 of |v| instead of
+// the 2^-9 of a single bf16 rounding.
+__device__ __forceinline__ void split_bf16(float v, bf16& hi, bf16& lo) {
+  hi = (bf16)v;
+  lo = (bf16)(v - (float)hi);
+}
+
+// Two bf16 values in one 32-bit word, a in the low half.
+__device__ __forceinline__ unsigned int pack2(bf16 a, bf16 b) {
+  return (unsigned int)__builtin_bit_cast(unsigned short, a) |
+         ((unsigned int)__builtin_bit_cast(unsigned short, b) << 16);
+}
+
+// Two floats rounded to bf16 (nearest even) in one 32-bit word, lo first.
+__device__ __forceinline__ unsigned int pack_bf16x2(float lo, float hi) { return pack2((bf16)lo, (bf16)hi); }
+
+// Four float32 values as the packed hi and lo bf16 parts (2 words each).
+__device__ __forceinline__ void split4(float4 v, uint2& hi, uint2& lo) {
+  bf16 h0, l0, h1, l1, h2, l2, h3, l3;
+  split_bf16(v.x, h0, l0);
+  split_bf16(v.y, h1, l1);
+  split_bf16(v.z, h2, l2);
+  split_bf16(v.w, h3, l3);
+  hi = make_uint2(pack2(h0, h1), pack2(h2, h3));
+  lo = make_uint2(pack2(l0, l1), pack2(l2, l3));
+}
+
+// Eight consecutive float32 values as the hi and lo fragments of a bf16 MFMA operand.
+__device__ __forceinline__ void split_frag(const float* p, bf16x8& hi, bf16x8& lo) {
+  uint2 h0, l0, h1, l1;
+  split4(*reinterpret_cast<const float4*>(p), h0, l0);
+  split4(*reinterpret_cast<const float4*>(p + 4), h1, l1);
+  hi = __builtin_bit_cast(bf16x8, make_uint4(h0.x, h0.y, h1.x, h1.y));
+  lo = __builtin_bit_cast(bf16x8, make_uint4(l0.x, l0.y, l1.x, l1.y));
+}
+
 __device__ __forceinline__ int lane_id() { return threadIdx.x & (kWave - 1); }
 
 template <typename V> __device__ __forceinline__ V shfl_xor(V v, int m) { return __shfl_xor(v, m, kWave); }

@@ -1,8 +1,11 @@
 // MFMA GEMM for the shared block's projections and the LM head.
 //
 // out = A W^T on the active rows of a row map, with W [N][K] row-major
-// (linear-layer layout) and A in the storage dtype, either the normalised
-// residual rows y[src(r)] (A_SRC) or compact rows buf[r] (A_CMP).
+// (linear-layer layout) in the storage dtype and A float32, either the
+// normalised residual rows y[src(r)] (A_SRC) or compact rows buf[r] (A_CMP).
+// With bf16 weights every A tile is split into bf16 hi and lo parts in LDS
+// and each product runs once per part, so the activations keep about 16
+// significant bits; the weights are exact in bf16.
 // Epilogues:
 //   E_QKV:     q to a buffer; k, v appended to the loop's cache pages (Eq. 11)
 //   E_RESID:   x[src(r)] += result (residual of the attention/FFN branch)
@@ -13,8 +16,8 @@
 //   E_LOGITS:  float logits plus a packed (value, -index) atomicMax for greedy
 //
 // Tiling: 256 threads = 4 waves in a 2x2 grid; each wave owns MT x NT 16x16
-// MFMA tiles.  K advances 256 bytes per tile, staged through LDS from a ring
-// of PF tiles prefetched into registers; blockIdx.z selects the K split.
+// MFMA tiles.  K advances BK elements per tile, staged through LDS from a
+// ring of PF tiles prefetched into registers; blockIdx.z selects the K split.
 #include "kernels.h"
 
 namespace tlf {
@@ -43,21 +46,24 @@ __device__ __forceinline__ int64_t kv_slot_base(const KvDst& kv, int r, int src)
   return (int64_t)page * c.page_elems + (slot % kPage);
 }
 
-template <typename T, int MT, int NT, int PF, int AK, int EK>
+template <typename T, int MT, int NT, int PF, int BK, int AK, int EK>
 __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
   constexpr int BM = 2 * MT * 16, BN = 2 * NT * 16;
-  constexpr int BK = gemm_k_tile<T>();
-  constexpr int EPC = 16 / (int)sizeof(T);           // elements per 16-byte chunk
-  constexpr int CPR = BK / EPC;                      // chunks per row per K tile
-  constexpr int LDK = BK + EPC;                      // padded LDS row
+  constexpr bool kSplit = sizeof(T) == 2;            // bf16 weights: A as hi + lo parts
+  constexpr int NA = kSplit ? 2 : 1;
+  constexpr int WPC = 16 / (int)sizeof(T);           // weight elements per 16-byte chunk
+  constexpr int WCR = BK / WPC;                      // weight chunks per row per K tile
+  constexpr int ACR = BK / 4;                        // A chunks (4 floats) per row per K tile
+  constexpr int LDK = BK + WPC;                      // padded LDS row, storage elements
   using M = Mfma<T>;
   constexpr int KS = M::KS, EPL = M::EPL;
-  constexpr int ACH = BM * CPR / 256;                // A chunks per thread
-  constexpr int BCH = BN * CPR / 256;                // B chunks per thread
-  static_assert(ACH >= 1 && BM * CPR % 256 == 0, "A tile split");
-  static_assert(BCH >= 1 && BN * CPR % 256 == 0, "B tile split");
+  constexpr int ACH = BM * ACR / 256;                // A chunks per thread
+  constexpr int BCH = BN * WCR / 256;                // B chunks per thread
+  static_assert(ACH >= 1 && BM * ACR % 256 == 0, "A tile split");
+  static_assert(BCH >= 1 && BN * WCR % 256 == 0, "B tile split");
+  static_assert(BK % KS == 0, "K tile");
 
-  __shared__ __align__(16) T As[BM * LDK];
+  __shared__ __align__(16) T As[NA][BM * LDK];
   __shared__ __align__(16) T Bs[BN * LDK];
   __shared__ int row_src_s[BM];
   __shared__ int64_t kv_base[EK == E_QKV ? BM : 1];
@@ -80,8 +86,9 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
     return wr < g.w_rows ? wr : g.w_rows - 1;
   };
 
-  V16<T> ra[PF][ACH], rb[PF][BCH];  // ring of PF K tiles in flight
-  const T* A = reinterpret_cast<const T*>(g.A);
+  float4 ra[PF][ACH];
+  V16<T> rb[PF][BCH];  // ring of PF K tiles in flight
+  const float* A = reinterpret_cast<const float*>(g.A);
   const T* W = reinterpret_cast<const T*>(g.W);
   const int k_per_split = g.K / g.splits;
   const int k_base = split * k_per_split;
@@ -91,34 +98,40 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
     const int kk = k_base + kt * BK;
 #pragma unroll
     for (int c = 0; c < BCH; ++c) {
-      const int ch = tid + c * 256, row = ch / CPR, col = (ch % CPR) * EPC;
+      const int ch = tid + c * 256, row = ch / WCR, col = (ch % WCR) * WPC;
       rb[c] = ld16(W + (int64_t)w_row(n0 + row) * g.K + kk + col);
     }
   };
-  auto load_a = [&](int kt, V16<T>* ra) {
+  auto load_a = [&](int kt, float4* ra) {
     const int kk = k_base + kt * BK;
 #pragma unroll
     for (int c = 0; c < ACH; ++c) {
-      const int ch = tid + c * 256, row = ch / CPR, col = (ch % CPR) * EPC;
+      const int ch = tid + c * 256, row = ch / ACR, col = (ch % ACR) * 4;
       const int s = row_src_s[row];
-      V16<T> v;
-      v.u = make_uint4(0, 0, 0, 0);
+      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
       if (s >= 0) {
         const int64_t ar = (AK == A_SRC) ? (int64_t)s : (int64_t)(r0 + row);
-        v = ld16(A + ar * g.lda + kk + col);
+        v = *reinterpret_cast<const float4*>(A + ar * g.lda + kk + col);
       }
       ra[c] = v;
     }
   };
-  auto store_tiles = [&](const V16<T>* ra, const V16<T>* rb) {
+  auto store_tiles = [&](const float4* ra, const V16<T>* rb) {
 #pragma unroll
     for (int c = 0; c < ACH; ++c) {
-      const int ch = tid + c * 256, row = ch / CPR, col = (ch % CPR) * EPC;
-      st16(&As[row * LDK + col], ra[c]);
+      const int ch = tid + c * 256, row = ch / ACR, col = (ch % ACR) * 4;
+      if constexpr (kSplit) {
+        uint2 hi, lo;
+        split4(ra[c], hi, lo);
+        *reinterpret_cast<uint2*>(&As[0][row * LDK + col]) = hi;
+        *reinterpret_cast<uint2*>(&As[NA - 1][row * LDK + col]) = lo;
+      } else {
+        *reinterpret_cast<float4*>(&As[0][row * LDK + col]) = ra[c];
+      }
     }
 #pragma unroll
     for (int c = 0; c < BCH; ++c) {
-      const int ch = tid + c * 256, row = ch / CPR, col = (ch % CPR) * EPC;
+      const int ch = tid + c * 256, row = ch / WCR, col = (ch % WCR) * WPC;
       st16(&Bs[row * LDK + col], rb[c]);
     }
   };
@@ -165,17 +178,21 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
       load_a(min(kt + PF, KT - 1), ra[p]);
 #pragma unroll
       for (int ks = 0; ks < BK / KS; ++ks) {
-        typename M::frag af[MT], bfr[NT];
+        typename M::frag af[NA][MT], bfr[NT];
 #pragma unroll
-        for (int i = 0; i < MT; ++i)
-          af[i] = M::load(&As[(wm * MT * 16 + i * 16 + (lane & 15)) * LDK + ks * KS + (lane >> 4) * EPL]);
+        for (int a = 0; a < NA; ++a)
+#pragma unroll
+          for (int i = 0; i < MT; ++i)
+            af[a][i] = M::load(&As[a][(wm * MT * 16 + i * 16 + (lane & 15)) * LDK + ks * KS + (lane >> 4) * EPL]);
 #pragma unroll
         for (int j = 0; j < NT; ++j)
           bfr[j] = M::load(&Bs[(wn * NT * 16 + j * 16 + (lane & 15)) * LDK + ks * KS + (lane >> 4) * EPL]);
 #pragma unroll
-        for (int i = 0; i < MT; ++i)
+        for (int a = 0; a < NA; ++a)
 #pragma unroll
-          for (int j = 0; j < NT; ++j) acc[i][j] = M::mma(af[i], bfr[j], acc[i][j]);
+          for (int i = 0; i < MT; ++i)
+#pragma unroll
+            for (int j = 0; j < NT; ++j) acc[i][j] = M::mma(af[a][i], bfr[j], acc[i][j]);
       }
     }
   }
@@ -221,7 +238,7 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
           if (src >= 0 && unit < g.F) {
             const float gt = acc[i][j][r], up = acc[i][j + 1][r];
             const float a = gt / (1.f + __expf(-gt)) * up;
-            reinterpret_cast<T*>(g.out)[(int64_t)rg * g.ldo + unit] = from_f<T>(a);
+            reinterpret_cast<float*>(g.out)[(int64_t)rg * g.ldo + unit] = a;
           }
         }
       } else {
@@ -236,7 +253,7 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
             reinterpret_cast<float*>(g.out)[((int64_t)split * g.part_rows + rg) * g.ldo + n] = v;
           } else {  // E_QKV
             if (n < g.d) {
-              reinterpret_cast<T*>(g.out)[(int64_t)rg * g.ldo + n] = from_f<T>(v);
+              reinterpret_cast<float*>(g.out)[(int64_t)rg * g.ldo + n] = v;
             } else {
               const int64_t base = kv_base[rl];
               if (base >= 0) {
@@ -258,14 +275,14 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
   }
 }
 
-template <typename T, int MT, int NT, int PF>
+template <typename T, int MT, int NT, int PF, int BK>
 hipError_t launch_tiles(const GemmArgs& a, AKind ak, EKind ek, hipStream_t s) {
   constexpr int BM = 2 * MT * 16, BN = 2 * NT * 16;
   const dim3 grid((a.N + BN - 1) / BN, (a.rm.rows + BM - 1) / BM, a.splits);
   if (grid.x == 0 || grid.y == 0) return hipSuccess;
 #define TLF_GEMM_CASE(AKV, EKV)                                                       \
   if (ak == AKV && ek == EKV) {                                                       \
-    hipLaunchKernelGGL((k_gemm<T, MT, NT, PF, AKV, EKV>), grid, dim3(256), 0, s, a);  \
+    hipLaunchKernelGGL((k_gemm<T, MT, NT, PF, BK, AKV, EKV>), grid, dim3(256), 0, s, a);  \
     return hipGetLastError();                                                         \
   }
   TLF_GEMM_CASE(A_SRC, E_QKV)
@@ -284,10 +301,14 @@ hipError_t launch_gemm(const GemmArgs& a, AKind ak, EKind ek, bool big_tiles, hi
   constexpr int BK = gemm_k_tile<T>();
   if (a.splits < 1 || a.K % a.splits != 0 || (a.K / a.splits) % BK != 0) return hipErrorInvalidValue;
   if (a.splits > 1 && ek != E_PARTIAL) return hipErrorInvalidValue;
-  // large row counts (prefill, LM head): 128x128 tiles, one K tile in flight;
-  // decode row counts: 32x64 tiles with three K tiles in flight to cover latency
-  if (big_tiles) return launch_tiles<T, 4, 4, 1>(a, ak, ek, s);
-  return launch_tiles<T, 1, 2, 3>(a, ak, ek, s);
+  // large row counts (prefill, LM head): 128x128 tiles of K 64, one K tile in
+  // flight; decode row counts: 32x64 tiles with three 256-byte K tiles of
+  // weights in flight to cover latency
+  if (big_tiles) {
+    if (a.K % 64 != 0) return hipErrorInvalidValue;
+    return launch_tiles<T, 4, 4, 1, 64>(a, ak, ek, s);
+  }
+  return launch_tiles<T, 1, 2, 2, BK>(a, ak, ek, s);
 }
 
 template hipError_t launch_gemm<float>(const GemmArgs&, AKind, EKind, bool, hipStream_t);

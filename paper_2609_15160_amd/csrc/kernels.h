@@ -43,8 +43,7 @@ struct KvDst {
 };
 
 // A operand: A_SRC reads the normalised residual rows y[src(r)]; A_CMP reads
-// compact rows buf[r] (attention output, SwiGLU activation).  Both are in the
-// storage dtype.
+// compact rows buf[r] (attention output, SwiGLU activation).  Both are float32.
 enum AKind { A_SRC = 0, A_CMP = 1 };
 // E_QKV: q to a buffer, k and v appended to the loop's cache pages.
 // E_RESID: x[src(r)] += result.  E_PARTIAL: split s writes P[s][r] (float).
@@ -52,7 +51,7 @@ enum AKind { A_SRC = 0, A_CMP = 1 };
 enum EKind { E_QKV = 0, E_RESID = 1, E_PARTIAL = 2, E_SWIGLU = 3, E_LOGITS = 4 };
 
 struct GemmArgs {
-  const void* A = nullptr;  // storage dtype rows
+  const float* A = nullptr; // float32 rows
   int lda = 0;
   const void* W = nullptr;  // [W rows][K] storage dtype
   int N = 0;                // output columns (E_SWIGLU: 2F in the interleaved gate/up space)
@@ -60,8 +59,8 @@ struct GemmArgs {
   int w_rows = 0;           // rows of W (loads are clamped below it)
   int splits = 1;           // split-K factor (E_PARTIAL only); K / splits must be a multiple of the K tile
   RowMap rm;
-  void* out = nullptr;      // E_QKV: q rows; E_RESID: float residual; E_PARTIAL: float [splits][part_rows][ldo];
-                            // E_SWIGLU: act rows; E_LOGITS: float logits
+  float* out = nullptr;     // E_QKV: q rows; E_RESID: residual; E_PARTIAL: [splits][part_rows][ldo];
+                            // E_SWIGLU: act rows; E_LOGITS: logits (all float32)
   int ldo = 0;
   int part_rows = 0;        // E_PARTIAL: rows of one split's slab
   int out_row_off = 0;      // E_LOGITS: output row = out_row_off + r
@@ -73,7 +72,8 @@ struct GemmArgs {
 
 template <typename T>
 hipError_t launch_gemm(const GemmArgs& a, AKind ak, EKind ek, bool big_tiles, hipStream_t s);
-// K elements per tile of the GEMM (splits must divide K into multiples of it).
+// K elements per tile of the decode-shaped GEMM (256 bytes of weights; splits
+// must divide K into multiples of it).  The 128x128 tiles take K 64 at a time.
 template <typename T> constexpr int gemm_k_tile() { return 256 / (int)sizeof(T); }
 
 // ---------------------------------------------------------------------------
@@ -90,7 +90,7 @@ struct EmbedArgs {
   int prefill_T = 0;              // > 0: pos = row % T; 0: pos = seq_len[row]
   const int32_t* seq_len = nullptr;
   float* x = nullptr;             // [rows][d] float residual
-  void* y = nullptr;              // [rows][d] RMSNorm(x) in the storage dtype
+  float* y = nullptr;             // [rows][d] RMSNorm(x)
   float eps = 1e-5f;
   int32_t* depth = nullptr;       // [rows]
   int32_t* out_depth = nullptr;   // optional [rows]
@@ -105,7 +105,7 @@ template <typename T> hipError_t launch_embed_route(const EmbedArgs& a, hipStrea
 struct ResidNormArgs {
   RowMap rm;
   float* x = nullptr;
-  void* y = nullptr;
+  float* y = nullptr;
   const float* partial = nullptr;  // [splits][part_rows][d]
   int splits = 0, part_rows = 0, d = 0;
   float eps = 1e-5f;
@@ -145,8 +145,8 @@ struct AttnDecodeArgs {
   int loop = 0, layer = 0, d = 0;
   const int32_t* perm = nullptr;   // depth-sorted row order
   const int32_t* nact = nullptr;   // n_i of this loop: rows [0, n_i) are active
-  const void* q = nullptr;         // [rows][d] compact rows
-  void* o = nullptr;               // [rows][d]
+  const float* q = nullptr;        // [rows][d] compact rows
+  float* o = nullptr;              // [rows][d]
   float scale_log2 = 0.f;          // log2(e) / sqrt(D)
   int grid = 0;                    // persistent workgroups
   int waves = 4;                   // waves per workgroup sharing one (row, head): 4 or 8
@@ -159,8 +159,8 @@ struct AttnPrefillArgs {
   CacheView c;
   int loop = 0, layer = 0, d = 0;
   int b0 = 0, G = 0, T = 0;
-  const void* q = nullptr;  // [G*T][d], row g*T + a
-  void* o = nullptr;        // [G*T][d]
+  const float* q = nullptr; // [G*T][d], row g*T + a
+  float* o = nullptr;       // [G*T][d]
   float scale_log2 = 0.f;
 };
 template <typename T> hipError_t launch_attn_prefill(const AttnPrefillArgs& a, hipStream_t s);

@@ -184,6 +184,8 @@ class Session:
             "router_w": dev(weights["router_w"], torch.float32),
             "router_b": dev(weights["router_b"], torch.float32),
         }
+        if weights.get("lm_head") is not None:
+            self.w["lm_head"] = dev(weights["lm_head"], sdt)
         if self.w["pos_emb"].shape[0] < max_pos:
             raise ValueError("position table shorter than max_pos")
         self.layers = []
@@ -193,7 +195,8 @@ class Session:
             LayerWeights(l["w_qkv"].data_ptr(), l["w_o"].data_ptr(), l["w_gate_up"].data_ptr(),
                          l["w_down"].data_ptr()) for l in self.layers])
         self._weights = Weights(self.w["tok_emb"].data_ptr(), self.w["pos_emb"].data_ptr(),
-                                self.w["router_w"].data_ptr(), self.w["router_b"].data_ptr(), None,
+                                self.w["router_w"].data_ptr(), self.w["router_b"].data_ptr(),
+                                self.w["lm_head"].data_ptr() if "lm_head" in self.w else None,
                                 len(self.layers), self._lw)
         need = workspace_bytes(self.cfg)
         self.workspace = torch.empty(need, dtype=torch.uint8, device=self.device)

@@ -39,6 +39,7 @@ _M2 = np.uint64(0x94D049BB133111EB)
 STREAM_TOK_EMB = 1
 STREAM_POS_EMB = 2
 STREAM_ROUTER_W = 3
+STREAM_LM_HEAD = 4      # optional untied LM head
 STREAM_LAYER_BASE = 16  # layer j uses 16 + 4j + {0: qkv, 1: o, 2: gate_up, 3: down}
 STREAM_PROMPT = 100
 STREAM_CALIB = 101
@@ -284,6 +285,12 @@ def make_weights(cfg: ModelConfig, seed: int = SEED, cache: bool = True) -> Dict
     if cache:
         _WEIGHT_CACHE[key] = w
     return w
+
+
+def make_lm_head(cfg: ModelConfig, seed: int = SEED) -> np.ndarray:
+    """A separate seeded LM head [V][d] (storage dtype), for models whose head
+    is not tied to the token embedding."""
+    return _mat(seed, STREAM_LM_HEAD, cfg.vocab, cfg.d_model, cfg)
 
 
 def make_prompts(cfg: ModelConfig, seed: int = SEED, batch: Optional[int] = None,

@@ -135,6 +135,20 @@ def test_f32_fixed_depth(depth):
     _check_f32(m, w, prompts, g, o, f"fixed{depth}")
 
 
+@pytest.mark.parametrize("head_dim", [64, 128])
+def test_f32_wide_heads(head_dim):
+    """fp32 kernels at head_dim 64 and 128; the 128 case also uses an untied LM head."""
+    m = _f32_small(d_model=2 * head_dim, n_heads=2, head_dim=head_dim, d_ff=192, batch=2, prompt_len=45,
+                   steps=10)
+    w = dict(synth.make_weights(m))
+    if head_dim == 128:
+        w["lm_head"] = synth.make_lm_head(m)
+    prompts = synth.make_prompts(m)
+    g = parity.run_gpu(m, w, prompts, m.steps)
+    o = parity.run_oracle(m, w, prompts, g.step_tokens)
+    _check_f32(m, w, prompts, g, o, f"f32-D{head_dim}")
+
+
 def test_prefill_in_sequence_groups_is_identical():
     m = _f32_small(batch=5, prompt_len=40, steps=3)
     w = synth.make_weights(m)
@@ -246,6 +260,31 @@ def test_bf16_d768_b256x2048_sampled_sequences():
     g = parity.run_gpu(m, w, prompts, steps, max_pos=m.max_pos, keep_logits_rows=sample)
     o = parity.run_oracle(m, w, prompts[sample], [t[sample] for t in g.step_tokens])
     _check_bf16(m, w, prompts, g, o, sample, "bf16_d768_b256x2048")
+
+
+def test_bf16_d2048_heads_of_128_small_batch():
+    """The d=2048 model (16 heads x 128) on a short ragged prompt: bf16 kernels at head_dim 128."""
+    full = synth.CONFIGS["bf16_d2048_b64x4096"]
+    m = full.replace(batch=5, prompt_len=70, steps=8)
+    w = synth.make_weights(full)
+    prompts = synth.make_prompts(m)
+    sample = [0, 2, 4]
+    g = parity.run_gpu(m, w, prompts, m.steps, max_pos=m.max_pos, keep_logits_rows=sample)
+    o = parity.run_oracle(m, w, prompts[sample], [t[sample] for t in g.step_tokens])
+    _check_bf16(m, w, prompts, g, o, sample, "bf16_d2048-small")
+
+
+@pytest.mark.slow
+def test_bf16_d2048_b64x4096_sampled_sequences():
+    """The d=2048 model at batch 64 x 4096 prompt with the oracle on one sequence."""
+    m = synth.CONFIGS["bf16_d2048_b64x4096"]
+    w = synth.make_weights(m)
+    prompts = synth.make_prompts(m)
+    steps = 3
+    sample = [63]
+    g = parity.run_gpu(m, w, prompts, steps, max_pos=m.max_pos, keep_logits_rows=sample)
+    o = parity.run_oracle(m, w, prompts[sample], [t[sample] for t in g.step_tokens])
+    _check_bf16(m, w, prompts, g, o, sample, "bf16_d2048_b64x4096")
 
 
 # ---------------------------------------------------------------------------

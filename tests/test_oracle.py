@@ -135,6 +135,22 @@ def test_fixed_depth_decode_equals_tied_weight_gpt():
         assert np.max(np.abs(lg[0] - ref[t])) < 1e-12
 
 
+def test_untied_head_equals_textbook_gpt():
+    """A separate LM head replaces E^T in the last product and nowhere else."""
+    cfg = synth.tiny_config(max_loops=3, prompt_len=11)
+    w = dict(synth.make_weights(cfg))
+    w["lm_head"] = synth.make_lm_head(cfg)
+    toks = synth.make_prompts(cfg)[0]
+    _, logits, _, _ = O.prefill(_model(cfg, w, route_rule=O.FIXED, fixed_depth=2), toks, all_logits=True)
+    ref = textbook.tied_gpt_logits(w, toks, cfg.n_heads, cfg.head_dim, 2, cfg.rms_eps)
+    assert np.max(np.abs(logits - ref)) < 1e-12
+    tied = dict(w)
+    del tied["lm_head"]
+    _, logits_tied, _, _ = O.prefill(_model(cfg, tied, route_rule=O.FIXED, fixed_depth=2), toks,
+                                     all_logits=True)
+    assert np.max(np.abs(logits - logits_tied)) > 1e-3
+
+
 def test_single_loop_model_is_plain_gpt():
     """R = 1: every token takes exactly one pass of the J-layer block."""
     cfg = synth.tiny_config(max_loops=1, n_layers=3, prompt_len=10)

@@ -39,7 +39,8 @@ def tied_gpt_logits(weights, tokens, H, D, loops, eps=1e-5):
     for _ in range(loops):
         for lw in weights["layers"]:
             x = _layer(x, lw, H, D, eps, is_causal=True)
-    return F.linear(_rms(x, eps), E).numpy()
+    head = E if weights.get("lm_head") is None else _t(weights["lm_head"])
+    return F.linear(_rms(x, eps), head).numpy()
 
 
 def routed_argmax_depths(weights, tokens):
