@@ -81,11 +81,12 @@ def hot_path_bytes(st, model, steps, B):
     return st["attn_algo_bytes"] + st["kv_write_bytes_total"] + weights
 
 
-def run_config(torch, tlf, model, w, prompts, warmup, steps, profiled, route_rule="argmax", fixed_depth=1):
+def run_config(torch, tlf, model, w, prompts, warmup, steps, profiled, route_rule="argmax", fixed_depth=1,
+               graph=True):
     B, T = prompts.shape
     max_pos = T + warmup + steps + profiled
     sess = tlf.Session(model, w, max_batch=B, max_pos=max_pos, route_rule=route_rule,
-                       fixed_depth=fixed_depth, max_prefill_tokens=65536)
+                       fixed_depth=fixed_depth, max_prefill_tokens=65536, decode_graph=graph)
     try:
         toks = torch.from_numpy(prompts).cuda()
         torch.cuda.synchronize()
@@ -244,6 +245,8 @@ def main():
                     help="steps after the timed region launched eagerly with HIP events around each attention launch")
     ap.add_argument("--config", default="bf16_d768_b256x2048")
     ap.add_argument("--no-fixed", action="store_true", help="skip the fixed-depth comparison")
+    ap.add_argument("--no-graph", action="store_true",
+                    help="launch the timed decode steps kernel by kernel instead of replaying a HIP graph")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-prefill", action="store_true", help="skip the prefill measurement")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
@@ -303,7 +306,7 @@ def main():
     log(f"inputs ready in {time.perf_counter() - t0:.1f}s: batch {B} x prompt {T}")
 
     ms, st, prefill_s, hist = run_config(torch, tlf, model, w, prompts, args.warmup, args.steps,
-                                         args.profiled_steps)
+                                         args.profiled_steps, graph=not args.no_graph)
     log(f"routed: {ms / args.steps:.3f} ms/step, prefill {prefill_s:.2f}s, depth hist {hist}")
     value = B * args.steps / (ms / 1e3)
     attn_gbs = st["attn_algo_bytes"] / (st["attn_ms"] / 1e3) / 1e9
@@ -347,7 +350,8 @@ def main():
     }
     if not args.no_fixed:
         fms, fst, fpre, _ = run_config(torch, tlf, model, w, prompts, args.warmup, args.steps,
-                                       args.profiled_steps, route_rule="fixed", fixed_depth=model.max_loops)
+                                       args.profiled_steps, route_rule="fixed", fixed_depth=model.max_loops,
+                                       graph=not args.no_graph)
         fgbs = fst["attn_algo_bytes"] / (fst["attn_ms"] / 1e3) / 1e9
         out["fixed_depth"] = {"depth": model.max_loops, "value": B * args.steps / (fms / 1e3),
                               "ms_per_step": fms / args.steps, "attn_achieved_gbs": fgbs,

@@ -19,7 +19,7 @@ int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 // Workspace buffers, in carve order.
 enum Buf {
   B_POOL, B_POS, B_PAGE_TABLE, B_CACHE_LEN, B_SEQ_LEN, B_SCALARS, B_DEPTH_HIST, B_STEP_STATS,
-  B_X_DEC, B_Y_DEC, B_DEPTH_DEC, B_PERM, B_NACT, B_Q_DEC, B_O_DEC, B_ACT_DEC, B_KEYS, B_PARTIAL,
+  B_X_DEC, B_XC_DEC, B_KVSLOT, B_DEPTH_DEC, B_PERM, B_NACT, B_Q_DEC, B_O_DEC, B_ACT_DEC, B_KEYS,
   B_X_PRE, B_Y_PRE, B_DEPTH_PRE, B_TOK_IDX, B_Q_PRE, B_O_PRE, B_ACT_PRE,
   B_COUNT
 };
@@ -50,7 +50,8 @@ bool make_layout(const tlf_config& c, Layout* L) {
   sz[B_DEPTH_HIST] = R * 8;
   sz[B_STEP_STATS] = kStatCount * 8;
   sz[B_X_DEC] = B * d * 4;
-  sz[B_Y_DEC] = B * d * 4;
+  sz[B_XC_DEC] = B * d * 4;
+  sz[B_KVSLOT] = R * B * 8;
   sz[B_DEPTH_DEC] = B * 4;
   sz[B_PERM] = B * 4;
   sz[B_NACT] = R * 4;
@@ -58,7 +59,6 @@ bool make_layout(const tlf_config& c, Layout* L) {
   sz[B_O_DEC] = B * d * 4;
   sz[B_ACT_DEC] = B * F * 4;
   sz[B_KEYS] = B * 8;
-  sz[B_PARTIAL] = (int64_t)kMaxSplits * B * d * 4;
   sz[B_X_PRE] = P * d * 4;
   sz[B_Y_PRE] = P * d * 4;
   sz[B_DEPTH_PRE] = P * 4;
@@ -76,6 +76,8 @@ bool make_layout(const tlf_config& c, Layout* L) {
   L->total = off;
   return true;
 }
+
+static_assert(kPlanThreads * 4 >= TLF_MAX_BATCH, "the decode planner covers the batch in 4 chunks");
 
 int validate_config(const tlf_config* c) {
   if (!c) return TLF_E_INVALID_ARG;
@@ -104,6 +106,10 @@ int validate_config(const tlf_config* c) {
   if (c->decode_graph != 0 && c->decode_graph != 1) return TLF_E_INVALID_ARG;
   // the decode attention stages one sequence's page list in LDS
   if (ceil_div(c->max_pos, kPage) > kAttnMaxPages) return TLF_E_INVALID_ARG;
+  // the decode projections address weights and activations with 32-bit element offsets
+  if ((int64_t)c->vocab * c->d_model >= INT32_MAX || 2 * (int64_t)c->d_ff * c->d_model >= INT32_MAX ||
+      (int64_t)TLF_MAX_BATCH * std::max(c->d_ff, 3 * c->d_model) >= INT32_MAX)
+    return TLF_E_INVALID_ARG;
   // positions, row indices and work-list offsets are int32
   if ((int64_t)std::max(c->max_prefill_tokens, c->max_pos) * std::max(c->d_ff, 3 * c->d_model) > INT32_MAX)
     return TLF_E_INVALID_ARG;
@@ -177,7 +183,8 @@ struct tlf_ctx {
   hipError_t end_timed(hipStream_t s) { return hipEventRecord(event_pending.back().stop, s); }
   hipError_t take_event(hipEvent_t* e) {
     if (!event_pool.empty()) { *e = event_pool.back(); event_pool.pop_back(); return hipSuccess; }
-    return hipEventCreate(e);
+    // timing only: no system-scope fence (cache writeback and invalidate) at each record
+    return hipEventCreateWithFlags(e, hipEventDisableSystemFence);
   }
 
   template <typename P> P* buf(Buf b) const { return reinterpret_cast<P*>(ws + L.off[b]); }
@@ -199,16 +206,6 @@ int precheck(tlf_ctx* ctx) {
   if (ctx->poisoned) return TLF_E_STATE;
   if (ctx->sticky != TLF_OK) return ctx->sticky;
   return TLF_OK;
-}
-
-// Split-K factor of a decode residual projection: at least two K tiles per
-// split, at most kMaxSplits splits, dividing the K tiles evenly.
-template <typename T>
-int decode_splits(int K) {
-  const int kt = K / gemm_k_tile<T>();
-  for (int sp = kMaxSplits; sp > 1; --sp)
-    if (kt % sp == 0 && kt / sp >= 2) return sp;
-  return 1;
 }
 
 // Waves sharing one (row, head) in the decode attention: enough waves in
@@ -259,14 +256,14 @@ int run_prefill(tlf_ctx* ctx, int B, int T_, const int32_t* tokens, float* logit
       rm.seg_cnt = ctx->cv.cache_len + (int64_t)b0 * R + i;
       rm.seg = T_; rm.seg_cnt_stride = R; rm.rows = rows;
       ResidNormArgs rn;
-      rn.rm = rm; rn.x = x; rn.y = y; rn.splits = 0; rn.d = d; rn.eps = c.rms_eps;
+      rn.rm = rm; rn.x = x; rn.y = y; rn.d = d; rn.eps = c.rms_eps;
       for (int j = 0; j < c.n_layers; ++j) {
         const tlf_layer_weights& lw = ctx->layers[j];
         GemmArgs q;
         q.A = y; q.lda = d; q.W = lw.w_qkv; q.N = 3 * d; q.K = d; q.w_rows = 3 * d; q.rm = rm;
         q.out = ctx->buf<float>(B_Q_PRE); q.ldo = d; q.d = d;
         q.kv.c = ctx->cv; q.kv.loop = i; q.kv.layer = j; q.kv.prefill = 1; q.kv.b0 = b0; q.kv.seg = T_;
-        TLF_HIP(launch_gemm<T>(q, A_SRC, E_QKV, true, s));
+        TLF_HIP(launch_gemm<T>(q, A_SRC, E_QKV, s));
 
         AttnPrefillArgs at;
         at.c = ctx->cv; at.loop = i; at.layer = j; at.d = d; at.b0 = b0; at.G = Gc; at.T = T_;
@@ -277,18 +274,18 @@ int run_prefill(tlf_ctx* ctx, int B, int T_, const int32_t* tokens, float* logit
         GemmArgs o;
         o.A = ctx->buf<float>(B_O_PRE); o.lda = d; o.W = lw.w_o; o.N = d; o.K = d; o.w_rows = d; o.rm = rm;
         o.out = x; o.ldo = d;
-        TLF_HIP(launch_gemm<T>(o, A_CMP, E_RESID, true, s));
+        TLF_HIP(launch_gemm<T>(o, A_CMP, E_RESID, s));
         TLF_HIP(launch_resid_norm<T>(rn, s));
 
         GemmArgs gu;
         gu.A = y; gu.lda = d; gu.W = lw.w_gate_up; gu.N = 2 * F; gu.K = d; gu.w_rows = 2 * F; gu.rm = rm;
         gu.out = ctx->buf<float>(B_ACT_PRE); gu.ldo = F; gu.F = F;
-        TLF_HIP(launch_gemm<T>(gu, A_SRC, E_SWIGLU, true, s));
+        TLF_HIP(launch_gemm<T>(gu, A_SRC, E_SWIGLU, s));
 
         GemmArgs dn;
         dn.A = ctx->buf<float>(B_ACT_PRE); dn.lda = F; dn.W = lw.w_down; dn.N = d; dn.K = F; dn.w_rows = d;
         dn.rm = rm; dn.out = x; dn.ldo = d;
-        TLF_HIP(launch_gemm<T>(dn, A_CMP, E_RESID, true, s));
+        TLF_HIP(launch_gemm<T>(dn, A_CMP, E_RESID, s));
         TLF_HIP(launch_resid_norm<T>(rn, s));
       }
     }
@@ -302,7 +299,7 @@ int run_prefill(tlf_ctx* ctx, int B, int T_, const int32_t* tokens, float* logit
       hd.rm.rows = Gc; hd.rm.src_stride = T_; hd.rm.src_off = T_ - 1;
       hd.out_row_off = b0;
     }
-    TLF_HIP(launch_gemm<T>(hd, A_SRC, E_LOGITS, true, s));
+    TLF_HIP(launch_gemm<T>(hd, A_SRC, E_LOGITS, s));
   }
   return TLF_OK;
 }
@@ -312,23 +309,24 @@ int run_decode(tlf_ctx* ctx, hipStream_t s, const int32_t* tokens, float* logits
                int32_t* depths, float* margin) {
   const tlf_config& c = ctx->cfg;
   const int d = c.d_model, F = c.d_ff, R = c.max_loops, B = ctx->batch;
-  float* x = ctx->buf<float>(B_X_DEC);
-  float* y = ctx->buf<float>(B_Y_DEC);
+  float* x = ctx->buf<float>(B_X_DEC);    // batch order (embedding)
+  float* xc = ctx->buf<float>(B_XC_DEC);  // compact order: row k is sequence perm[k]
+  int64_t* kv_slot = ctx->buf<int64_t>(B_KVSLOT);
   int32_t* perm = ctx->buf<int32_t>(B_PERM);
   int32_t* nact = ctx->buf<int32_t>(B_NACT);
-  float* part = ctx->buf<float>(B_PARTIAL);
-  const int split_o = decode_splits<T>(d), split_d = decode_splits<T>(F);
 
   EmbedArgs ea;
   ea.tok_emb = ctx->w.tok_emb; ea.pos_emb = ctx->w.pos_emb; ea.Wr = ctx->w.router_w; ea.br = ctx->w.router_b;
   ea.tokens = tokens; ea.rows = B; ea.V = c.vocab; ea.d = d; ea.R = R; ea.prefill_T = 0;
-  ea.seq_len = ctx->cv.seq_len; ea.x = x; ea.y = y; ea.eps = c.rms_eps; ea.depth = ctx->buf<int32_t>(B_DEPTH_DEC);
+  ea.seq_len = ctx->cv.seq_len; ea.x = x; ea.y = nullptr; ea.eps = c.rms_eps;
+  ea.depth = ctx->buf<int32_t>(B_DEPTH_DEC);
   ea.out_depth = depths; ea.out_margin = margin;
   ea.rule = c.route_rule; ea.threshold = c.route_threshold; ea.fixed = c.fixed_depth; ea.err = ctx->cv.err;
   TLF_HIP(launch_embed_route<T>(ea, s));
 
   DecodePlanArgs pa;
   pa.c = ctx->cv; pa.B = B; pa.depth = ctx->buf<int32_t>(B_DEPTH_DEC); pa.perm = perm; pa.nact = nact;
+  pa.kv_slot = kv_slot;
   pa.argmax_keys = ctx->buf<unsigned long long>(B_KEYS);
   pa.kv_entry_bytes = (int64_t)c.n_layers * 2 * c.d_model * ctx->L.s;
   TLF_HIP(launch_plan_decode(pa, s));
@@ -342,16 +340,19 @@ int run_decode(tlf_ctx* ctx, hipStream_t s, const int32_t* tokens, float* logits
     TLF_HIP(hipEventRecord(block_start, s));
   }
   for (int i = 0; i < R; ++i) {
-    // rows [0, n_i) of the depth-sorted order are the tokens still active at loop i
+    // rows [0, n_i) of the depth-sorted order are the tokens still active at
+    // loop i; row k is sequence perm[k], its residual xc[k]
     RowMap rm;
     rm.src = perm; rm.nact = nact + i; rm.rows = B;
     for (int j = 0; j < c.n_layers; ++j) {
       const tlf_layer_weights& lw = ctx->layers[j];
-      GemmArgs q;
-      q.A = y; q.lda = d; q.W = lw.w_qkv; q.N = 3 * d; q.K = d; q.w_rows = 3 * d; q.rm = rm;
-      q.out = ctx->buf<float>(B_Q_DEC); q.ldo = d; q.d = d;
-      q.kv.c = ctx->cv; q.kv.loop = i; q.kv.layer = j; q.kv.prefill = 0;
-      TLF_HIP(launch_gemm<T>(q, A_SRC, E_QKV, false, s));
+      GemmArgs q;  // q, k, v of RMSNorm(x); k, v appended to cache (b, i) of layer j
+      const bool first = i == 0 && j == 0;  // reads x through perm and writes xc
+      q.A = first ? x : xc; q.lda = d; q.a_copy = first ? xc : nullptr; q.W = lw.w_qkv; q.N = 3 * d; q.K = d; q.w_rows = 3 * d; q.rm = rm;
+      q.out = ctx->buf<float>(B_Q_DEC); q.ldo = d; q.d = d; q.eps = c.rms_eps;
+      q.kv.c = ctx->cv; q.kv.loop = i; q.kv.layer = j; q.kv.prefill = 0; q.kv.slot_base = kv_slot + (int64_t)i * B;
+      q.spec = i == 0;
+      TLF_HIP(launch_dgemm<T>(q, first ? A_SRC : A_CMP, E_QKV, true, s));
 
       AttnDecodeArgs at;
       at.c = ctx->cv; at.loop = i; at.layer = j; at.d = d; at.perm = perm; at.nact = nact + i;
@@ -367,38 +368,33 @@ int run_decode(tlf_ctx* ctx, hipStream_t s, const int32_t* tokens, float* logits
         TLF_HIP(launch_attn_decode<T>(at, s));
       }
 
-      GemmArgs o;
+      GemmArgs o;  // x += o W_o^T
       o.A = ctx->buf<float>(B_O_DEC); o.lda = d; o.W = lw.w_o; o.N = d; o.K = d; o.w_rows = d; o.rm = rm;
-      o.splits = split_o; o.out = part; o.ldo = d; o.part_rows = c.max_batch;
-      TLF_HIP(launch_gemm<T>(o, A_CMP, E_PARTIAL, false, s));
-      ResidNormArgs rn;
-      rn.rm = rm; rn.x = x; rn.y = y; rn.partial = part; rn.splits = split_o; rn.part_rows = c.max_batch;
-      rn.d = d; rn.eps = c.rms_eps;
-      TLF_HIP(launch_resid_norm<T>(rn, s));
+      o.out = xc; o.ldo = d; o.spec = i == 0;
+      TLF_HIP(launch_dgemm<T>(o, A_CMP, E_RESID, false, s));
 
-      GemmArgs gu;
-      gu.A = y; gu.lda = d; gu.W = lw.w_gate_up; gu.N = 2 * F; gu.K = d; gu.w_rows = 2 * F; gu.rm = rm;
-      gu.out = ctx->buf<float>(B_ACT_DEC); gu.ldo = F; gu.F = F;
-      TLF_HIP(launch_gemm<T>(gu, A_SRC, E_SWIGLU, false, s));
+      GemmArgs gu;  // act = silu(RMSNorm(x) W_g^T) * (RMSNorm(x) W_u^T)
+      gu.A = xc; gu.lda = d; gu.W = lw.w_gate_up; gu.N = 2 * F; gu.K = d; gu.w_rows = 2 * F; gu.rm = rm;
+      gu.out = ctx->buf<float>(B_ACT_DEC); gu.ldo = F; gu.F = F; gu.eps = c.rms_eps; gu.spec = i == 0;
+      TLF_HIP(launch_dgemm<T>(gu, A_CMP, E_SWIGLU, true, s));
 
-      GemmArgs dn;
+      GemmArgs dn;  // x += act W_d^T
       dn.A = ctx->buf<float>(B_ACT_DEC); dn.lda = F; dn.W = lw.w_down; dn.N = d; dn.K = F; dn.w_rows = d;
-      dn.rm = rm; dn.splits = split_d; dn.out = part; dn.ldo = d; dn.part_rows = c.max_batch;
-      TLF_HIP(launch_gemm<T>(dn, A_CMP, E_PARTIAL, false, s));
-      rn.splits = split_d;
-      TLF_HIP(launch_resid_norm<T>(rn, s));
+      dn.rm = rm; dn.out = xc; dn.ldo = d; dn.spec = i == 0;
+      TLF_HIP(launch_dgemm<T>(dn, A_CMP, E_RESID, false, s));
     }
   }
   if (ctx->profiling) {
     TLF_HIP(hipEventRecord(block_stop, s));
     ctx->event_pending.push_back(tlf_ctx::Timed{block_start, block_stop, false});
   }
-  // every row's y now holds RMSNorm of its last state h^(m_b)
+  // every compact row now holds its sequence's last state h^(m_b):
+  // logits[perm[k]] = RMSNorm(xc[k]) E^T
   GemmArgs hd;
-  hd.A = y; hd.lda = d; hd.W = head_weights(ctx); hd.N = c.vocab; hd.K = d; hd.w_rows = c.vocab;
-  hd.rm.rows = B; hd.out = logits; hd.ldo = c.vocab;
+  hd.A = xc; hd.lda = d; hd.W = head_weights(ctx); hd.N = c.vocab; hd.K = d; hd.w_rows = c.vocab;
+  hd.rm.src = perm; hd.rm.rows = B; hd.out = logits; hd.ldo = c.vocab; hd.eps = c.rms_eps; hd.spec = 1;
   hd.argmax_keys = ctx->buf<unsigned long long>(B_KEYS);
-  TLF_HIP(launch_gemm<T>(hd, A_SRC, E_LOGITS, true, s));
+  TLF_HIP(launch_dgemm<T>(hd, A_CMP, E_LOGITS, true, s));
   if (next) TLF_HIP(launch_argmax_finalize(ctx->buf<unsigned long long>(B_KEYS), next, B, s));
   return TLF_OK;
 }

@@ -15,7 +15,6 @@ constexpr int kWave = 64;          // CDNA wavefront width
 constexpr int kMaxLoops = 16;
 constexpr int kPlanThreads = 1024; // single-workgroup planners
 constexpr int kAttnMaxPages = 4096; // page list staged in LDS by the decode attention (max_pos <= 65536)
-constexpr int kMaxSplits = 8;       // split-K slabs of a decode residual projection
 
 // Sticky device error bits (reported through tlf_cache_stats).
 constexpr int kErrBadToken = 1;

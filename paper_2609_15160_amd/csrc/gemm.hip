@@ -1,4 +1,4 @@
-// MFMA GEMM for the shared block's projections and the LM head.
+// MFMA GEMM for the prefill projections and LM head (many rows per launch).
 //
 // out = A W^T on the active rows of a row map, with W [N][K] row-major
 // (linear-layer layout) in the storage dtype and A float32, either the
@@ -9,15 +9,13 @@
 // Epilogues:
 //   E_QKV:     q to a buffer; k, v appended to the loop's cache pages (Eq. 11)
 //   E_RESID:   x[src(r)] += result (residual of the attention/FFN branch)
-//   E_PARTIAL: split-K slab s of a residual projection, summed in split order
-//              by the following residual+norm kernel (deterministic, no atomics)
 //   E_SWIGLU:  act = silu(gate) * up, gate/up columns interleaved in 16-column
 //              groups so every wave holds matching pairs
 //   E_LOGITS:  float logits plus a packed (value, -index) atomicMax for greedy
 //
 // Tiling: 256 threads = 4 waves in a 2x2 grid; each wave owns MT x NT 16x16
 // MFMA tiles.  K advances BK elements per tile, staged through LDS from a
-// ring of PF tiles prefetched into registers; blockIdx.z selects the K split.
+// ring of PF tiles prefetched into registers.
 #include "kernels.h"
 
 namespace tlf {
@@ -71,7 +69,6 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
   const int r0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
-  const int split = blockIdx.z;
 
   // decode: a tile whose first row has exited is empty (rows are depth-sorted)
   if (g.rm.nact && r0 >= *g.rm.nact) return;
@@ -90,9 +87,8 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
   V16<T> rb[PF][BCH];  // ring of PF K tiles in flight
   const float* A = reinterpret_cast<const float*>(g.A);
   const T* W = reinterpret_cast<const T*>(g.W);
-  const int k_per_split = g.K / g.splits;
-  const int k_base = split * k_per_split;
-  const int KT = k_per_split / BK;
+  const int k_base = 0;
+  const int KT = g.K / BK;
 
   auto load_b = [&](int kt, V16<T>* rb) {
     const int kk = k_base + kt * BK;
@@ -249,8 +245,6 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
           const float v = acc[i][j][r];
           if constexpr (EK == E_RESID) {
             reinterpret_cast<float*>(g.out)[(int64_t)src * g.ldo + n] += v;
-          } else if constexpr (EK == E_PARTIAL) {
-            reinterpret_cast<float*>(g.out)[((int64_t)split * g.part_rows + rg) * g.ldo + n] = v;
           } else {  // E_QKV
             if (n < g.d) {
               reinterpret_cast<float*>(g.out)[(int64_t)rg * g.ldo + n] = v;
@@ -278,7 +272,7 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
 template <typename T, int MT, int NT, int PF, int BK>
 hipError_t launch_tiles(const GemmArgs& a, AKind ak, EKind ek, hipStream_t s) {
   constexpr int BM = 2 * MT * 16, BN = 2 * NT * 16;
-  const dim3 grid((a.N + BN - 1) / BN, (a.rm.rows + BM - 1) / BM, a.splits);
+  const dim3 grid((a.N + BN - 1) / BN, (a.rm.rows + BM - 1) / BM);
   if (grid.x == 0 || grid.y == 0) return hipSuccess;
 #define TLF_GEMM_CASE(AKV, EKV)                                                       \
   if (ak == AKV && ek == EKV) {                                                       \
@@ -289,7 +283,6 @@ hipError_t launch_tiles(const GemmArgs& a, AKind ak, EKind ek, hipStream_t s) {
   TLF_GEMM_CASE(A_SRC, E_SWIGLU)
   TLF_GEMM_CASE(A_SRC, E_LOGITS)
   TLF_GEMM_CASE(A_CMP, E_RESID)
-  TLF_GEMM_CASE(A_CMP, E_PARTIAL)
 #undef TLF_GEMM_CASE
   return hipErrorInvalidValue;
 }
@@ -297,21 +290,13 @@ hipError_t launch_tiles(const GemmArgs& a, AKind ak, EKind ek, hipStream_t s) {
 }  // namespace
 
 template <typename T>
-hipError_t launch_gemm(const GemmArgs& a, AKind ak, EKind ek, bool big_tiles, hipStream_t s) {
-  constexpr int BK = gemm_k_tile<T>();
-  if (a.splits < 1 || a.K % a.splits != 0 || (a.K / a.splits) % BK != 0) return hipErrorInvalidValue;
-  if (a.splits > 1 && ek != E_PARTIAL) return hipErrorInvalidValue;
-  // large row counts (prefill, LM head): 128x128 tiles of K 64, one K tile in
-  // flight; decode row counts: 32x64 tiles with three 256-byte K tiles of
-  // weights in flight to cover latency
-  if (big_tiles) {
-    if (a.K % 64 != 0) return hipErrorInvalidValue;
-    return launch_tiles<T, 4, 4, 1, 64>(a, ak, ek, s);
-  }
-  return launch_tiles<T, 1, 2, 2, BK>(a, ak, ek, s);
+hipError_t launch_gemm(const GemmArgs& a, AKind ak, EKind ek, hipStream_t s) {
+  // 128x128 tiles, K 64 at a time, one K tile in flight
+  if (a.K % 64 != 0) return hipErrorInvalidValue;
+  return launch_tiles<T, 4, 4, 1, 64>(a, ak, ek, s);
 }
 
-template hipError_t launch_gemm<float>(const GemmArgs&, AKind, EKind, bool, hipStream_t);
-template hipError_t launch_gemm<bf16>(const GemmArgs&, AKind, EKind, bool, hipStream_t);
+template hipError_t launch_gemm<float>(const GemmArgs&, AKind, EKind, hipStream_t);
+template hipError_t launch_gemm<bf16>(const GemmArgs&, AKind, EKind, hipStream_t);
 
 }  // namespace tlf

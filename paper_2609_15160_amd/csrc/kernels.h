@@ -40,15 +40,17 @@ struct KvDst {
   int prefill = 0;  // 0: decode, slot = cache_len[b][i] - 1 with b = residual row;
                     // 1: prefill, b = b0 + r / seg, slot = r % seg
   int b0 = 0, seg = 0;
+  const int64_t* slot_base = nullptr;  // decode projections: the planner's slot offset of
+                                       // compact row r at this loop (kv_slot + loop * B)
 };
 
 // A operand: A_SRC reads the normalised residual rows y[src(r)]; A_CMP reads
 // compact rows buf[r] (attention output, SwiGLU activation).  Both are float32.
 enum AKind { A_SRC = 0, A_CMP = 1 };
 // E_QKV: q to a buffer, k and v appended to the loop's cache pages.
-// E_RESID: x[src(r)] += result.  E_PARTIAL: split s writes P[s][r] (float).
-// E_SWIGLU: act = silu(gate) * up.  E_LOGITS: float logits + greedy keys.
-enum EKind { E_QKV = 0, E_RESID = 1, E_PARTIAL = 2, E_SWIGLU = 3, E_LOGITS = 4 };
+// E_RESID: x[src(r)] += result.  E_SWIGLU: act = silu(gate) * up.
+// E_LOGITS: float logits + greedy keys.
+enum EKind { E_QKV = 0, E_RESID = 1, E_SWIGLU = 3, E_LOGITS = 4 };
 
 struct GemmArgs {
   const float* A = nullptr; // float32 rows
@@ -57,24 +59,30 @@ struct GemmArgs {
   int N = 0;                // output columns (E_SWIGLU: 2F in the interleaved gate/up space)
   int K = 0;
   int w_rows = 0;           // rows of W (loads are clamped below it)
-  int splits = 1;           // split-K factor (E_PARTIAL only); K / splits must be a multiple of the K tile
   RowMap rm;
-  float* out = nullptr;     // E_QKV: q rows; E_RESID: residual; E_PARTIAL: [splits][part_rows][ldo];
-                            // E_SWIGLU: act rows; E_LOGITS: logits (all float32)
+  float* out = nullptr;     // E_QKV: q rows; E_RESID: residual; E_SWIGLU: act rows;
+                            // E_LOGITS: logits (all float32)
   int ldo = 0;
-  int part_rows = 0;        // E_PARTIAL: rows of one split's slab
   int out_row_off = 0;      // E_LOGITS: output row = out_row_off + r
   unsigned long long* argmax_keys = nullptr;  // E_LOGITS, may be nullptr
   KvDst kv;                 // E_QKV
   int d = 0;                // E_QKV: width of each of q, k, v
   int F = 0;                // E_SWIGLU: hidden width
+  float eps = 1e-5f;        // RMSNorm epsilon of the decode projections that fuse the norm
+  float* a_copy = nullptr;  // decode: the operand rows are also written here, compact (first projection)
+  int spec = 0;             // decode: every row is active; loads need not wait for the active count
 };
 
 template <typename T>
-hipError_t launch_gemm(const GemmArgs& a, AKind ak, EKind ek, bool big_tiles, hipStream_t s);
-// K elements per tile of the decode-shaped GEMM (256 bytes of weights; splits
-// must divide K into multiples of it).  The 128x128 tiles take K 64 at a time.
-template <typename T> constexpr int gemm_k_tile() { return 256 / (int)sizeof(T); }
+hipError_t launch_gemm(const GemmArgs& a, AKind ak, EKind ek, hipStream_t s);
+// Decode-shaped projections (few rows): K split across the waves of a
+// workgroup, all loads in flight at once, one writer per output, rows in
+// compact order (E_RESID: out[r] += result; E_LOGITS: logits row src(r)).
+// norm: A is the residual x and the product is taken with RMSNorm(x).
+// Supported: (A_SRC | A_CMP, E_QKV, norm), (A_CMP, E_SWIGLU | E_LOGITS,
+// norm), (A_CMP, E_RESID, no norm).
+template <typename T>
+hipError_t launch_dgemm(const GemmArgs& a, AKind ak, EKind ek, bool norm, hipStream_t s);
 
 // ---------------------------------------------------------------------------
 // Embedding + router (Section 3.2): h0 = E[x] + P[pos], z = W_r h0 + b_r,
@@ -90,7 +98,7 @@ struct EmbedArgs {
   int prefill_T = 0;              // > 0: pos = row % T; 0: pos = seq_len[row]
   const int32_t* seq_len = nullptr;
   float* x = nullptr;             // [rows][d] float residual
-  float* y = nullptr;             // [rows][d] RMSNorm(x)
+  float* y = nullptr;             // [rows][d] RMSNorm(x), or nullptr
   float eps = 1e-5f;
   int32_t* depth = nullptr;       // [rows]
   int32_t* out_depth = nullptr;   // optional [rows]
@@ -101,13 +109,12 @@ struct EmbedArgs {
 };
 template <typename T> hipError_t launch_embed_route(const EmbedArgs& a, hipStream_t s);
 
-// x[src(r)] += sum over splits of P[s][r]; y[src(r)] = RMSNorm(x[src(r)]).
+// y[src(r)] = RMSNorm(x[src(r)]) on the active rows of a row map.
 struct ResidNormArgs {
   RowMap rm;
-  float* x = nullptr;
+  const float* x = nullptr;
   float* y = nullptr;
-  const float* partial = nullptr;  // [splits][part_rows][d]
-  int splits = 0, part_rows = 0, d = 0;
+  int d = 0;
   float eps = 1e-5f;
 };
 template <typename T> hipError_t launch_resid_norm(const ResidNormArgs& a, hipStream_t s);
@@ -122,6 +129,8 @@ struct DecodePlanArgs {
   const int32_t* depth = nullptr;
   int32_t* perm = nullptr;         // [B]
   int32_t* nact = nullptr;         // [R]
+  int64_t* kv_slot = nullptr;      // [R][B]: element offset (page * page_elems + slot) of the
+                                   // slot that compact row k appends at loop i
   unsigned long long* argmax_keys = nullptr; // [B] cleared for the LM head
   int64_t kv_entry_bytes = 0;      // bytes of one (token, loop) cache entry over all layers
 };

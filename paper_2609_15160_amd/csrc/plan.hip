@@ -6,15 +6,29 @@ namespace tlf {
 namespace {
 
 // ---------------------------------------------------------------------------
-// Decode planner: one workgroup of kPlanThreads threads.
+// Decode planner: one workgroup of kPlanThreads threads, thread t owning
+// sequences t, t + kPlanThreads, ...  Steps:
+//   1. depth-sorted order, deepest first and stable in b, by a counting sort
+//      whose ranks come from wave ballots: A_i = rows [0, n_i) (Eq. 4-6);
+//   2. one new page for every executed (b, i) whose next slot starts a page,
+//      numbered by a block prefix sum (deterministic);
+//   3. per executed (b, i): the slot's position, cache_len += 1, and the
+//      slot's element offset for the QKV epilogue, by compact row;
+//   4. statistics and the greedy keys cleared for the LM head.
+// Every sequence's cache lengths and page-table entries are loaded together
+// (unrolled over loops), so a step costs a few memory round trips.
 // ---------------------------------------------------------------------------
+constexpr int kPlanWaves = kPlanThreads / kWave;
+constexpr int kPlanChunks = 4;  // kPlanThreads * kPlanChunks >= max batch
+
 __global__ __launch_bounds__(kPlanThreads) void k_plan_decode(DecodePlanArgs a) {
   const CacheView& c = a.c;
-  const int tid = threadIdx.x, B = a.B, R = c.R;
+  const int tid = threadIdx.x, lane = lane_id(), wv = tid >> 6, B = a.B, R = c.R;
   __shared__ int cnt[kMaxLoops + 1];
   __shared__ int start[kMaxLoops + 1];
   __shared__ int fill[kMaxLoops + 1];
-  __shared__ int scan_tmp[kPlanThreads / kWave + 1];
+  __shared__ int wcnt[kPlanWaves][kMaxLoops + 1];
+  __shared__ int scan_tmp[kPlanWaves + 1];
   __shared__ int s_carry, s_total, s_oom;
   __shared__ unsigned long long hist[kMaxLoops];
   __shared__ unsigned long long s_kvread, s_kvwrite;
@@ -22,9 +36,18 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan_decode(DecodePlanArgs a) 
 
   if (tid <= kMaxLoops) { cnt[tid] = 0; fill[tid] = 0; }
   if (tid < kMaxLoops) hist[tid] = 0ull;
-  if (tid == 0) { s_kvread = 0ull; s_kvwrite = 0ull; s_maxm = 0; s_oom = 0; }
+  if (tid == 0) { s_kvread = 0ull; s_kvwrite = 0ull; s_maxm = 0; s_oom = 0; s_carry = 0; }
+  int m_of[kPlanChunks], row_of[kPlanChunks];
+#pragma unroll
+  for (int ch = 0; ch < kPlanChunks; ++ch) {
+    const int b = ch * kPlanThreads + tid;
+    m_of[ch] = b < B ? a.depth[b] : 0;
+    row_of[ch] = -1;
+  }
   __syncthreads();
-  for (int b = tid; b < B; b += kPlanThreads) atomicAdd(&cnt[a.depth[b]], 1);
+#pragma unroll
+  for (int ch = 0; ch < kPlanChunks; ++ch)
+    if (m_of[ch] > 0) atomicAdd(&cnt[m_of[ch]], 1);
   __syncthreads();
   if (tid == 0) {
     int s = 0;
@@ -33,30 +56,47 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan_decode(DecodePlanArgs a) 
   }
   __syncthreads();
 
-  // 1. depth-sorted order (deepest first, stable in b): A_i = rows [0, n_i)
-  for (int b0 = 0; b0 < B; b0 += kPlanThreads) {
-    const int b = b0 + tid;
-    const int m = b < B ? a.depth[b] : 0;
-    for (int dv = R; dv >= 1; --dv) {
-      int tot;
-      const int ex = block_exclusive_scan(m == dv ? 1 : 0, scan_tmp, &tot);
-      if (m == dv) a.perm[start[dv] + fill[dv] + ex] = b;
-      __syncthreads();
-      if (tid == 0) fill[dv] += tot;
-      __syncthreads();
+  // 1. rank of b among the sequences of its depth with smaller b
+  const unsigned long long below = (1ull << lane) - 1ull;
+#pragma unroll
+  for (int ch = 0; ch < kPlanChunks; ++ch) {
+    if (ch * kPlanThreads >= B) break;  // uniform
+    const int m = m_of[ch];
+    int rank = 0;
+    for (int dv = 1; dv <= R; ++dv) {
+      const unsigned long long mask = __ballot(m == dv);
+      if (m == dv) rank = __popcll(mask & below);
+      if (lane == 0) wcnt[wv][dv] = __popcll(mask);
     }
+    __syncthreads();
+    if (m > 0) {
+      int off = 0;
+      for (int w = 0; w < wv; ++w) off += wcnt[w][m];
+      const int row = start[m] + fill[m] + off + rank;
+      row_of[ch] = row;
+      a.perm[row] = ch * kPlanThreads + tid;
+    }
+    __syncthreads();
+    if (tid >= 1 && tid <= R) {
+      int t = 0;
+      for (int w = 0; w < kPlanWaves; ++w) t += wcnt[w][tid];
+      fill[tid] += t;
+    }
+    __syncthreads();
   }
 
-  // 2. page allocation: (b, i) needs a new page when its next slot starts one
-  if (tid == 0) s_carry = 0;
-  __syncthreads();
-  for (int b0 = 0; b0 < B; b0 += kPlanThreads) {
-    const int b = b0 + tid;
+  // 2. pages needed: (b, i) for i < m_b whose next slot starts a page
+  int need_of[kPlanChunks];
+#pragma unroll
+  for (int ch = 0; ch < kPlanChunks; ++ch) {
+    need_of[ch] = 0;
+    if (ch * kPlanThreads >= B) break;
+    const int b = ch * kPlanThreads + tid, m = m_of[ch];
     int need = 0;
-    if (b < B) {
-      const int m = a.depth[b];
-      for (int i = 0; i < m; ++i) need += (c.cache_len[b * R + i] % kPage) == 0;
-    }
+#pragma unroll
+    for (int i = 0; i < kMaxLoops; ++i)
+      if (i < m) need += (c.cache_len[b * R + i] % kPage) == 0;
+    need_of[ch] = need;
     int tot;
     block_exclusive_scan(need, scan_tmp, &tot);
     if (tid == 0) s_carry += tot;
@@ -72,30 +112,46 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan_decode(DecodePlanArgs a) 
     s_carry = base;
   }
   __syncthreads();
-  for (int b0 = 0; b0 < B; b0 += kPlanThreads) {
-    const int b = b0 + tid;
-    int need = 0, m = 0;
-    if (b < B) {
-      m = a.depth[b];
-      for (int i = 0; i < m; ++i) need += (c.cache_len[b * R + i] % kPage) == 0;
-    }
+
+  // 3. slots of the executed (b, i)
+#pragma unroll
+  for (int ch = 0; ch < kPlanChunks; ++ch) {
+    if (ch * kPlanThreads >= B) break;
+    const int b = ch * kPlanThreads + tid, m = m_of[ch];
     int tot;
-    const int ex = block_exclusive_scan(need, scan_tmp, &tot);
-    if (b < B && !s_oom) {
+    const int ex = block_exclusive_scan(need_of[ch], scan_tmp, &tot);
+    if (m > 0 && !s_oom) {
+      int len[kMaxLoops], page[kMaxLoops];
+#pragma unroll
+      for (int i = 0; i < kMaxLoops; ++i) {
+        len[i] = i < m ? c.cache_len[b * R + i] : 0;
+        page[i] = -1;
+      }
+#pragma unroll
+      for (int i = 0; i < kMaxLoops; ++i)
+        if (i < m && len[i] % kPage != 0)
+          page[i] = c.page_table[((int64_t)b * R + i) * c.pages_per_seq + len[i] / kPage];
       int next = s_carry + ex;
       const int t = c.seq_len[b];
-      for (int i = 0; i < m; ++i) {
-        const int slot = c.cache_len[b * R + i];
-        int32_t* pt = c.page_table + ((int64_t)b * R + i) * c.pages_per_seq;
-        if (slot % kPage == 0) pt[slot / kPage] = next++;
-        const int page = pt[slot / kPage];
-        c.pos[(int64_t)page * kPage + slot % kPage] = t;
-        c.cache_len[b * R + i] = slot + 1;
-        atomicAdd(&s_kvread, (unsigned long long)(slot + 1));
+      unsigned long long rd = 0ull;
+#pragma unroll
+      for (int i = 0; i < kMaxLoops; ++i) {
+        if (i < m) {
+          const int slot = len[i];
+          if (slot % kPage == 0) {
+            page[i] = next++;
+            c.page_table[((int64_t)b * R + i) * c.pages_per_seq + slot / kPage] = page[i];
+          }
+          c.pos[(int64_t)page[i] * kPage + slot % kPage] = t;
+          c.cache_len[b * R + i] = slot + 1;
+          a.kv_slot[(int64_t)i * B + row_of[ch]] = (int64_t)page[i] * c.page_elems + slot % kPage;
+          rd += (unsigned long long)(slot + 1);
+        }
       }
+      atomicAdd(&s_kvread, rd);
       atomicAdd(&s_kvwrite, (unsigned long long)m);
     }
-    if (b < B) {
+    if (m > 0) {
       c.seq_len[b] += 1;
       atomicAdd(&hist[m - 1], 1ull);
       atomicMax(&s_maxm, m);
@@ -104,6 +160,8 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan_decode(DecodePlanArgs a) 
     if (tid == 0) s_carry += tot;
     __syncthreads();
   }
+
+  // 4. bookkeeping
   if (tid == 0 && !s_oom) *c.page_next += s_total;
   if (tid < R) atomicAdd(&c.depth_hist[tid], hist[tid]);
   if (tid == 0) {

@@ -1,4 +1,4 @@
-// Per-row kernels: embedding + router, and residual reduction + RMSNorm.
+// Per-row kernels: embedding + router, and RMSNorm of residual rows.
 //
 // Both keep the float32 residual row x and write y = RMSNorm(x) (no affine,
 // Appendix A), also float32: y is the A operand of the next projection
@@ -102,11 +102,13 @@ __global__ __launch_bounds__(256) void k_embed_route(EmbedArgs a) {
   }
   ss = wave_sum(ss);
   const float inv = rsqrtf(ss / (float)a.d + a.eps);
-  float* y = a.y + (int64_t)row * a.d;
+  if (a.y) {
+    float* y = a.y + (int64_t)row * a.d;
 #pragma unroll
-  for (int c = 0; c < kRowChunks; ++c) {
-    const int k = 4 * lane + 256 * c;
-    if (k < a.d) V4<float>::store(y + k, scale4(h[c], inv));
+    for (int c = 0; c < kRowChunks; ++c) {
+      const int k = 4 * lane + 256 * c;
+      if (k < a.d) V4<float>::store(y + k, scale4(h[c], inv));
+    }
   }
 #pragma unroll
   for (int i = 0; i < kMaxLoops; ++i)
@@ -148,10 +150,9 @@ __global__ __launch_bounds__(256) void k_embed_route(EmbedArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// x[src(r)] += sum_s P[s][r] (split-K partials of a residual projection, in
-// split order), then y[src(r)] = RMSNorm(x[src(r)]).  One workgroup per row:
-// thread t holds elements 4t + 1024c, and every partial slab is loaded before
-// the sum so a row costs one memory round trip.
+// y[src(r)] = RMSNorm(x[src(r)]) for the active rows of a row map (prefill,
+// after each residual projection).  One workgroup per row: thread t holds
+// elements 4t + 1024c.
 // ---------------------------------------------------------------------------
 constexpr int kNormChunks = 4;  // 4 x 1024 elements per row
 
@@ -161,30 +162,14 @@ __global__ __launch_bounds__(256) void k_resid_norm(ResidNormArgs a) {
   if (!row_active(a.rm, r)) return;
   const int tid = threadIdx.x, lane = lane_id(), w = tid >> 6;
   const int src = row_src(a.rm, r);
-  float* x = a.x + (int64_t)src * a.d;
+  const float* x = a.x + (int64_t)src * a.d;
   float4 h[kNormChunks];
-  float4 pv[kNormChunks][kMaxSplits];
-#pragma unroll
-  for (int c = 0; c < kNormChunks; ++c) {
-    const int k = 4 * tid + 1024 * c;
-    if (k < a.d) {
-      h[c] = V4<float>::load(x + k);
-#pragma unroll
-      for (int sp = 0; sp < kMaxSplits; ++sp)
-        if (sp < a.splits) pv[c][sp] = V4<float>::load(a.partial + ((int64_t)sp * a.part_rows + r) * a.d + k);
-    }
-  }
   float ss = 0.f;
 #pragma unroll
   for (int c = 0; c < kNormChunks; ++c) {
     const int k = 4 * tid + 1024 * c;
     if (k < a.d) {
-#pragma unroll
-      for (int sp = 0; sp < kMaxSplits; ++sp)
-        if (sp < a.splits)
-          h[c] = make_float4(h[c].x + pv[c][sp].x, h[c].y + pv[c][sp].y, h[c].z + pv[c][sp].z,
-                             h[c].w + pv[c][sp].w);
-      if (a.splits > 0) V4<float>::store(x + k, h[c]);
+      h[c] = V4<float>::load(x + k);
       ss = sumsq(h[c], ss);
     }
   }
