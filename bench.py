@@ -34,9 +34,11 @@ def log(msg):
 
 
 def decode_run(sess, torch, B, V, warmup, steps, profiled, first_tokens):
-    """Warmup, `steps` timed decode steps (HIP-graph replays), then `profiled`
-    steps launched kernel by kernel with HIP events around every attention
-    launch; greedy feedback throughout, no allocation inside either region."""
+    """Warmup, `steps` timed decode steps (HIP-graph replays), then two passes of
+    `profiled` steps launched kernel by kernel: the first with HIP events around
+    each step's loop-and-layer region only, the second with events around every
+    attention launch as well.  Greedy feedback throughout, no allocation inside
+    any region.  Returns (ms of the timed steps, block-pass stats, attention-pass stats)."""
     dev = sess.device
     tok = [first_tokens.to(torch.int32).contiguous(), torch.empty(B, dtype=torch.int32, device=dev)]
     logits = torch.empty((B, V), dtype=torch.float32, device=dev)
@@ -56,20 +58,23 @@ def decode_run(sess, torch, B, V, warmup, steps, profiled, first_tokens):
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1)
     log(f"timed: {steps} steps in {ms:.1f} ms")
-    sess.set_profiling(True)
-    for p in range(profiled):
-        sess.decode_into(tok[k % 2], logits, next_tok=tok[(k + 1) % 2])
-        k += 1
-        if p % 4 == 3:
-            log(f"profiled: {p + 1} of {profiled} steps enqueued")
-    torch.cuda.synchronize()
-    st = sess.stats()
-    sess.set_profiling(False)
-    if st["status"] != 0:
-        raise RuntimeError(f"device error {st['status']}")
+    stats = []
+    for mode in ("block", "attn"):
+        sess.set_profiling(mode)
+        for p in range(profiled):
+            sess.decode_into(tok[k % 2], logits, next_tok=tok[(k + 1) % 2])
+            k += 1
+            if p % 10 == 9:
+                log(f"profiled ({mode} events): {p + 1} of {profiled} steps enqueued")
+        torch.cuda.synchronize()
+        st = sess.stats()
+        sess.set_profiling(False)
+        if st["status"] != 0:
+            raise RuntimeError(f"device error {st['status']}")
+        stats.append(st)
     if not bool(torch.isfinite(logits).all()):
         raise RuntimeError("non-finite logits")
-    return ms, st
+    return ms, stats[0], stats[1]
 
 
 def hot_path_bytes(st, model, steps, B):
@@ -84,7 +89,7 @@ def hot_path_bytes(st, model, steps, B):
 def run_config(torch, tlf, model, w, prompts, warmup, steps, profiled, route_rule="argmax", fixed_depth=1,
                graph=True):
     B, T = prompts.shape
-    max_pos = T + warmup + steps + profiled
+    max_pos = T + warmup + steps + 2 * profiled
     sess = tlf.Session(model, w, max_batch=B, max_pos=max_pos, route_rule=route_rule,
                        fixed_depth=fixed_depth, max_prefill_tokens=65536, decode_graph=graph)
     try:
@@ -96,12 +101,31 @@ def run_config(torch, tlf, model, w, prompts, warmup, steps, profiled, route_rul
         prefill_s = time.perf_counter() - t0
         first = torch.argmax(logits, dim=-1)
         del logits
-        ms, st = decode_run(sess, torch, B, model.vocab, warmup, steps, profiled, first)
+        ms, st_block, st_attn = decode_run(sess, torch, B, model.vocab, warmup, steps, profiled, first)
         hist = sess.stats()["depth_hist"]
-        return ms, st, prefill_s, hist
+        return ms, (st_block, st_attn), prefill_s, hist
     finally:
         sess.close()
         torch.cuda.empty_cache()
+
+
+def stream_copy_gbs(torch, nbytes=1 << 30, reps=10):
+    """Device-to-device copy rate (bytes read + written per second) of a plain
+    torch copy of `nbytes`: a practical ceiling for streaming kernels."""
+    src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1)
+    del src, dst
+    torch.cuda.empty_cache()
+    return 2 * nbytes * reps / (ms / 1e3) / 1e9
 
 
 def cpu_baseline(model, w, prompts, budget_s, seqs=8):
@@ -241,8 +265,9 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=8)
-    ap.add_argument("--profiled-steps", type=int, default=20,
-                    help="steps after the timed region launched eagerly with HIP events around each attention launch")
+    ap.add_argument("--profiled-steps", type=int, default=10,
+                    help="steps per profiled pass after the timed region (two passes, launched eagerly: "
+                         "events around the loop region, then also around each attention launch)")
     ap.add_argument("--config", default="bf16_d768_b256x2048")
     ap.add_argument("--no-fixed", action="store_true", help="skip the fixed-depth comparison")
     ap.add_argument("--no-graph", action="store_true",
@@ -261,7 +286,7 @@ def main():
         import synth
         m = synth.CONFIGS[args.config]
         per_step = m.max_loops * m.n_layers
-        routed = (args.warmup + args.steps + args.profiled_steps) * per_step
+        routed = (args.warmup + args.steps + 2 * args.profiled_steps) * per_step
         print(json.dumps(trace_summary(args.trace_summary, routed, args.profiled_steps * per_step)))
         return
     if args.counter_summary:
@@ -294,8 +319,8 @@ def main():
         del src, dst
         torch.cuda.empty_cache()
     base = synth.CONFIGS[args.config]
-    if args.warmup + args.steps + args.profiled_steps > base.steps or args.profiled_steps < 1:
-        print(f"warmup + steps + profiled-steps must be <= {base.steps} for {args.config} "
+    if args.warmup + args.steps + 2 * args.profiled_steps > base.steps or args.profiled_steps < 1:
+        print(f"warmup + steps + 2 x profiled-steps must be <= {base.steps} for {args.config} "
               f"(profiled-steps >= 1)", file=sys.stderr)
         sys.exit(2)
     model = base
@@ -305,14 +330,14 @@ def main():
     B, T = prompts.shape
     log(f"inputs ready in {time.perf_counter() - t0:.1f}s: batch {B} x prompt {T}")
 
-    ms, st, prefill_s, hist = run_config(torch, tlf, model, w, prompts, args.warmup, args.steps,
-                                         args.profiled_steps, graph=not args.no_graph)
+    ms, (stb, st), prefill_s, hist = run_config(torch, tlf, model, w, prompts, args.warmup, args.steps,
+                                                args.profiled_steps, graph=not args.no_graph)
     log(f"routed: {ms / args.steps:.3f} ms/step, prefill {prefill_s:.2f}s, depth hist {hist}")
     value = B * args.steps / (ms / 1e3)
     attn_gbs = st["attn_algo_bytes"] / (st["attn_ms"] / 1e3) / 1e9
     per_launch = st["attn_algo_bytes"] / max(st["attn_launches"], 1)
-    hot_bytes = hot_path_bytes(st, model, args.profiled_steps, B)
-    hot_gbs = hot_bytes / (st["block_ms"] / 1e3) / 1e9
+    hot_bytes = hot_path_bytes(stb, model, args.profiled_steps, B)
+    hot_gbs = hot_bytes / (stb["block_ms"] / 1e3) / 1e9
     tot_hist = np.asarray(hist, dtype=np.float64)
     mean_depth = float((tot_hist * np.arange(1, len(hist) + 1)).sum() / max(tot_hist.sum(), 1))
 
@@ -340,16 +365,21 @@ def main():
                      "launches": st["attn_launches"], "avg_launch_us": st["attn_ms"] * 1e3 / st["attn_launches"],
                      "algo_bytes_per_launch": per_launch,
                      "measured": f"HIP events around each attention launch over {args.profiled_steps} decode "
-                                 f"steps right after the timed region"},
-        "hot_path": {"what": "loop-and-layer region per step (attention + QKV/O/SwiGLU GEMMs + norms, "
-                             "launch gaps of eager launches included)",
+                                 f"steps (the last profiled pass)"},
+        "hot_path": {"what": "loop-and-layer region per step: decode attention plus the QKV, O, gate/up "
+                             "and down projections with their fused norms, launched kernel by kernel; "
+                             "HIP events around the region only",
                      "achieved_gbs": hot_gbs, "frac": hot_gbs / HBM_PEAK_GBS,
-                     "ms_per_step": st["block_ms"] / args.profiled_steps,
+                     "ms_per_step": stb["block_ms"] / args.profiled_steps,
                      "algo_bytes_per_step": hot_bytes / args.profiled_steps},
         "prefill_s": prefill_s,
     }
+    copy_gbs = stream_copy_gbs(torch)
+    out["stream_copy"] = {"gbs": copy_gbs, "what": "torch device copy of 1 GiB, read + written bytes per second",
+                          "attn_frac_of_copy": attn_gbs / copy_gbs, "hot_path_frac_of_copy": hot_gbs / copy_gbs}
+    log(f"stream copy: {copy_gbs:.0f} GB/s")
     if not args.no_fixed:
-        fms, fst, fpre, _ = run_config(torch, tlf, model, w, prompts, args.warmup, args.steps,
+        fms, (_, fst), fpre, _ = run_config(torch, tlf, model, w, prompts, args.warmup, args.steps,
                                        args.profiled_steps, route_rule="fixed", fixed_depth=model.max_loops,
                                        graph=not args.no_graph)
         fgbs = fst["attn_algo_bytes"] / (fst["attn_ms"] / 1e3) / 1e9

@@ -206,12 +206,21 @@ int tlf_decode_step(tlf_ctx* ctx, const int32_t* d_tokens, float* d_logits, int3
 int tlf_cache_stats(tlf_ctx* ctx, tlf_cache_stats_t* out, int32_t* h_len, int32_t* h_pos,
                     size_t pos_cap);
 
-/* Measurement switch.  enable != 0 resets the totals reported by
- * tlf_cache_stats (decode_steps, attn_*) and brackets every later
- * decode-attention launch with a pair of HIP events on the context's stream;
- * enable == 0 stops the event recording.  It launches one small kernel and
- * does not wait for the stream. */
-int tlf_set_profiling(tlf_ctx* ctx, int enable);
+/* Measurement switch (decode steps are then launched kernel by kernel, not
+ * from the captured graph).
+ *   TLF_PROFILE_ATTN:  a pair of HIP events on the context's stream around
+ *                      every decode-attention launch (attn_ms) and around each
+ *                      step's loop-and-layer region (block_ms);
+ *   TLF_PROFILE_BLOCK: events around the loop-and-layer region only, so that
+ *                      block_ms carries no event overhead from inside it;
+ *   TLF_PROFILE_OFF:   no events.
+ * Any mode other than OFF resets the totals reported by tlf_cache_stats
+ * (decode_steps, attn_*, block_ms, ...).  It launches one small kernel and
+ * does not wait for the stream.  TLF_E_INVALID_ARG for an unknown mode. */
+#define TLF_PROFILE_OFF 0
+#define TLF_PROFILE_ATTN 1
+#define TLF_PROFILE_BLOCK 2
+int tlf_set_profiling(tlf_ctx* ctx, int mode);
 
 /* Releases the host context (waits for the stream first).  NULL is ignored. */
 void tlf_destroy(tlf_ctx* ctx);

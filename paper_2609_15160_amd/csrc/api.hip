@@ -142,7 +142,8 @@ struct tlf_ctx {
   int cus = 0;  // compute units of the device
   int attn_blocks[2] = {1, 1};  // resident decode-attention workgroups per CU (4 and 8 waves)
   // measurement: event pairs around decode-attention launches, resolved by tlf_cache_stats
-  bool profiling = false;
+  bool profiling = false;     // decode steps launched eagerly, block region timed
+  bool profile_attn = false;  // and every decode-attention launch timed
   std::vector<hipEvent_t> event_pool;
   struct Timed { hipEvent_t start, stop; bool attn; };
   std::vector<Timed> event_pending;
@@ -352,7 +353,7 @@ int run_decode(tlf_ctx* ctx, hipStream_t s, const int32_t* tokens, float* logits
       q.out = ctx->buf<float>(B_Q_DEC); q.ldo = d; q.d = d; q.eps = c.rms_eps;
       q.kv.c = ctx->cv; q.kv.loop = i; q.kv.layer = j; q.kv.prefill = 0; q.kv.slot_base = kv_slot + (int64_t)i * B;
       q.spec = i == 0;
-      TLF_HIP(launch_dgemm<T>(q, first ? A_SRC : A_CMP, E_QKV, true, s));
+      TLF_HIP(launch_dgemm<T>(q, first ? A_SRC : A_CMP, E_QKV, true, ctx->cus, s));
 
       AttnDecodeArgs at;
       at.c = ctx->cv; at.loop = i; at.layer = j; at.d = d; at.perm = perm; at.nact = nact + i;
@@ -360,7 +361,7 @@ int run_decode(tlf_ctx* ctx, hipStream_t s, const int32_t* tokens, float* logits
       at.scale_log2 = 1.4426950408889634f / std::sqrt((float)c.head_dim);
       at.waves = attn_waves(ctx);
       at.grid = ctx->cus * ctx->attn_blocks[at.waves == 4 ? 0 : 1];
-      if (ctx->profiling) {
+      if (ctx->profile_attn) {
         TLF_HIP(ctx->begin_timed(s, true));
         TLF_HIP(launch_attn_decode<T>(at, s));
         TLF_HIP(ctx->end_timed(s));
@@ -371,17 +372,17 @@ int run_decode(tlf_ctx* ctx, hipStream_t s, const int32_t* tokens, float* logits
       GemmArgs o;  // x += o W_o^T
       o.A = ctx->buf<float>(B_O_DEC); o.lda = d; o.W = lw.w_o; o.N = d; o.K = d; o.w_rows = d; o.rm = rm;
       o.out = xc; o.ldo = d; o.spec = i == 0;
-      TLF_HIP(launch_dgemm<T>(o, A_CMP, E_RESID, false, s));
+      TLF_HIP(launch_dgemm<T>(o, A_CMP, E_RESID, false, ctx->cus, s));
 
       GemmArgs gu;  // act = silu(RMSNorm(x) W_g^T) * (RMSNorm(x) W_u^T)
       gu.A = xc; gu.lda = d; gu.W = lw.w_gate_up; gu.N = 2 * F; gu.K = d; gu.w_rows = 2 * F; gu.rm = rm;
       gu.out = ctx->buf<float>(B_ACT_DEC); gu.ldo = F; gu.F = F; gu.eps = c.rms_eps; gu.spec = i == 0;
-      TLF_HIP(launch_dgemm<T>(gu, A_CMP, E_SWIGLU, true, s));
+      TLF_HIP(launch_dgemm<T>(gu, A_CMP, E_SWIGLU, true, ctx->cus, s));
 
       GemmArgs dn;  // x += act W_d^T
       dn.A = ctx->buf<float>(B_ACT_DEC); dn.lda = F; dn.W = lw.w_down; dn.N = d; dn.K = F; dn.w_rows = d;
       dn.rm = rm; dn.out = xc; dn.ldo = d; dn.spec = i == 0;
-      TLF_HIP(launch_dgemm<T>(dn, A_CMP, E_RESID, false, s));
+      TLF_HIP(launch_dgemm<T>(dn, A_CMP, E_RESID, false, ctx->cus, s));
     }
   }
   if (ctx->profiling) {
@@ -394,7 +395,7 @@ int run_decode(tlf_ctx* ctx, hipStream_t s, const int32_t* tokens, float* logits
   hd.A = xc; hd.lda = d; hd.W = head_weights(ctx); hd.N = c.vocab; hd.K = d; hd.w_rows = c.vocab;
   hd.rm.src = perm; hd.rm.rows = B; hd.out = logits; hd.ldo = c.vocab; hd.eps = c.rms_eps; hd.spec = 1;
   hd.argmax_keys = ctx->buf<unsigned long long>(B_KEYS);
-  TLF_HIP(launch_dgemm<T>(hd, A_CMP, E_LOGITS, true, s));
+  TLF_HIP(launch_dgemm<T>(hd, A_CMP, E_LOGITS, true, ctx->cus, s));
   if (next) TLF_HIP(launch_argmax_finalize(ctx->buf<unsigned long long>(B_KEYS), next, B, s));
   return TLF_OK;
 }
@@ -638,10 +639,11 @@ int tlf_cache_stats(tlf_ctx* ctx, tlf_cache_stats_t* out, int32_t* h_len, int32_
   return out->device_error;
 }
 
-int tlf_set_profiling(tlf_ctx* ctx, int enable) {
+int tlf_set_profiling(tlf_ctx* ctx, int mode) {
   if (!ctx) return TLF_E_INVALID_ARG;
+  if (mode != TLF_PROFILE_OFF && mode != TLF_PROFILE_ATTN && mode != TLF_PROFILE_BLOCK) return TLF_E_INVALID_ARG;
   if (ctx->poisoned) return TLF_E_STATE;
-  if (enable) {
+  if (mode != TLF_PROFILE_OFF) {
     // reset the totals: cumulative device counters and the host-side sums
     static_assert(kStatLoopsTotal == kStatAttnBytesTotal + 3, "cumulative counters are contiguous");
     TLF_HIP(launch_fill_u64(reinterpret_cast<unsigned long long*>(ctx->cv.step_stats) + kStatAttnBytesTotal, 0ull,
@@ -651,7 +653,8 @@ int tlf_set_profiling(tlf_ctx* ctx, int enable) {
     ctx->block_ms = 0.0;
     ctx->recycle_events();
   }
-  ctx->profiling = enable != 0;
+  ctx->profiling = mode != TLF_PROFILE_OFF;
+  ctx->profile_attn = mode == TLF_PROFILE_ATTN;
   return TLF_OK;
 }
 

@@ -28,9 +28,10 @@
 // With bf16 weights each float32 operand enters the MFMA as bf16 hi + lo
 // parts (one product each), as in the prefill GEMM.
 //
-// Workgroups are numbered so that all row tiles of one column tile run on
-// the same XCD (workgroup i runs on XCD i mod 8) and share its L2 copy of
-// the weight tile.
+// Only active tiles get workgroups, dealt to the XCDs in equal runs that
+// walk the row tiles of a column tile together (shared weight tiles in L2).
+#include <algorithm>
+
 #include "kernels.h"
 
 namespace tlf {
@@ -44,8 +45,17 @@ __device__ __forceinline__ unsigned int ordered_bits(float v) {
 
 constexpr int kXcds = 8;
 
+// Shared-memory scratch of one workgroup, sized by the caller for the larger shape.
+struct DgemmShared {
+  float* red;       // [SLOTS][BM * (BN + 1)] partial tiles
+  float* ss;        // [W][BM] partial sums of squares
+  float* inv;       // [BM] 1 / rms per row
+  int* orow;        // [BM] logits row of each tile row
+  int64_t* kv;      // [BM] cache slot offset of each tile row
+};
+
 template <typename T, int RM, int CN, int W, int KB, int AK, int EK, bool NORM>
-__global__ __launch_bounds__(W * 64) void k_dgemm(GemmArgs g, int tiles_n, int tiles_m) {
+__device__ __forceinline__ void dgemm_tile(const GemmArgs& g, int nact, int act_rows, const DgemmShared& sh) {
   using M = Mfma<T>;
   typedef typename M::frag Frag;
   constexpr int KS = M::KS, EPL = M::EPL;
@@ -60,29 +70,29 @@ __global__ __launch_bounds__(W * 64) void k_dgemm(GemmArgs g, int tiles_n, int t
   static_assert(EK != E_SWIGLU || CN % 2 == 0, "gate/up pairs");
   static_assert(EK != E_LOGITS || (BN == kWave && EOUT % NT == 0), "one wave per logits row");
 
-  __shared__ float red[SLOTS][BM * LDR];
-  __shared__ float s_ss[NORM ? W : 1][BM];
-  __shared__ float s_inv[BM];
-  __shared__ int s_orow[EK == E_LOGITS ? BM : 1];
-  __shared__ int64_t s_kv[EK == E_QKV ? BM : 1];
+  float* red = sh.red;
 
-  const int L = blockIdx.x;
-  const int tn = L % kXcds + kXcds * ((L / kXcds) / tiles_m), tm = (L / kXcds) % tiles_m;
-  if (tn >= tiles_n) return;
-  const int r0 = tm * BM, n0 = tn * BN;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int quad = lane >> 4, c16 = lane & 15;
+  // Active tiles only (rows past the active count form no tile), dealt to
+  // the XCDs in equal contiguous runs: workgroup L runs on XCD L mod 8 and
+  // takes tile (L mod 8) * per + L / 8, so no XCD holds more than its share,
+  // and a run walks the row tiles of one column tile before the next, which
+  // keeps weight tiles shared in that XCD's L2.
+  const int tiles_n = (g.N + BN - 1) / BN;
+  const int RT = (act_rows + BM - 1) / BM, ntiles = RT * tiles_n, per = (ntiles + kXcds - 1) / kXcds;
+  const int L = blockIdx.x, k = L / kXcds, t = (L % kXcds) * per + k;
+  if (k >= per || t >= ntiles) return;
+  const int tn = t / RT, tm = t % RT;
+  const int r0 = tm * BM, n0 = tn * BN;
 
   // Loads are issued in dependency order: the weight fragments, the
   // epilogue's bookkeeping and residual values, then the activation
   // fragments (after the row permutation for A_SRC).  With g.spec (every
-  // row active, e.g. the first loop) they go out before the active-row
-  // count arrives; otherwise a tile whose first row has exited returns on
-  // the count before loading anything, and activation rows past the count
-  // are not loaded.
-  const int nact = g.rm.nact ? *g.rm.nact : g.rm.rows;
-  if (!g.spec && r0 >= nact) return;
-  const int a_rows = g.spec ? g.rm.rows : min(nact, g.rm.rows);  // activation rows worth loading
+  // row active, e.g. the first loop) the tiles and loads do not wait for
+  // the active-row count; otherwise the count decides the tiles first, and
+  // activation rows past it are not loaded.
+  const int a_rows = act_rows;  // activation rows worth loading
   // 32-bit element offsets from uniform bases (the weight and activation
   // matrices hold fewer than 2^31 elements)
   const T* Wb = reinterpret_cast<const T*>(g.W);
@@ -102,8 +112,8 @@ __global__ __launch_bounds__(W * 64) void k_dgemm(GemmArgs g, int tiles_n, int t
 #pragma unroll
     for (int i = 0; i < RM; ++i) {
       const int rl = i * 16 + c16, r = min(r0 + rl, g.rm.rows - 1);
-      if constexpr (EK == E_QKV) s_kv[rl] = g.kv.slot_base[r];
-      if constexpr (EK == E_LOGITS) s_orow[rl] = g.rm.src ? g.rm.src[r] : g.out_row_off + r;
+      if constexpr (EK == E_QKV) sh.kv[rl] = g.kv.slot_base[r];
+      if constexpr (EK == E_LOGITS) sh.orow[rl] = g.rm.src ? g.rm.src[r] : g.out_row_off + r;
     }
   }
   float xr[EK == E_RESID ? EPT : 1];
@@ -212,7 +222,7 @@ __global__ __launch_bounds__(W * 64) void k_dgemm(GemmArgs g, int tiles_n, int t
 #pragma unroll
         for (int c = 0; c < CN; ++c)
 #pragma unroll
-          for (int r = 0; r < 4; ++r) red[w - SLOTS][(i * 16 + quad * 4 + r) * LDR + c * 16 + c16] = acc[i][c][r];
+          for (int r = 0; r < 4; ++r) red[(w - SLOTS) * BM * LDR + (i * 16 + quad * 4 + r) * LDR + c * 16 + c16] = acc[i][c][r];
     }
     __syncthreads();
     if (w < SLOTS) {
@@ -221,7 +231,7 @@ __global__ __launch_bounds__(W * 64) void k_dgemm(GemmArgs g, int tiles_n, int t
 #pragma unroll
         for (int c = 0; c < CN; ++c)
 #pragma unroll
-          for (int r = 0; r < 4; ++r) acc[i][c][r] += red[w][(i * 16 + quad * 4 + r) * LDR + c * 16 + c16];
+          for (int r = 0; r < 4; ++r) acc[i][c][r] += red[w * BM * LDR + (i * 16 + quad * 4 + r) * LDR + c * 16 + c16];
     }
     __syncthreads();
   }
@@ -231,7 +241,7 @@ __global__ __launch_bounds__(W * 64) void k_dgemm(GemmArgs g, int tiles_n, int t
 #pragma unroll
       for (int c = 0; c < CN; ++c)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) red[w][(i * 16 + quad * 4 + r) * LDR + c * 16 + c16] = acc[i][c][r];
+        for (int r = 0; r < 4; ++r) red[w * BM * LDR + (i * 16 + quad * 4 + r) * LDR + c * 16 + c16] = acc[i][c][r];
   }
   if constexpr (NORM) {
 #pragma unroll
@@ -239,7 +249,7 @@ __global__ __launch_bounds__(W * 64) void k_dgemm(GemmArgs g, int tiles_n, int t
       float t = ss[i];
       t += shfl_xor(t, 16);
       t += shfl_xor(t, 32);
-      if (quad == 0) s_ss[w][i * 16 + c16] = t;
+      if (quad == 0) sh.ss[w * BM + i * 16 + c16] = t;
     }
   }
   __syncthreads();
@@ -247,16 +257,16 @@ __global__ __launch_bounds__(W * 64) void k_dgemm(GemmArgs g, int tiles_n, int t
     if (tid < BM) {
       float t = 0.f;
 #pragma unroll
-      for (int ww = 0; ww < W; ++ww) t += s_ss[ww][tid];
-      s_inv[tid] = rsqrtf(t / (float)g.K + g.eps);
+      for (int ww = 0; ww < W; ++ww) t += sh.ss[ww * BM + tid];
+      sh.inv[tid] = rsqrtf(t / (float)g.K + g.eps);
     }
     __syncthreads();
   }
   auto tile_sum = [&](int row, int col) -> float {
     float v = 0.f;
 #pragma unroll
-    for (int ww = 0; ww < SLOTS; ++ww) v += red[ww][row * LDR + col];
-    if constexpr (NORM) v *= s_inv[row];
+    for (int ww = 0; ww < SLOTS; ++ww) v += red[ww * BM * LDR + row * LDR + col];
+    if constexpr (NORM) v *= sh.inv[row];
     return v;
   };
   const int row_end = min(g.rm.rows, nact);  // rows [r0, row_end) are active
@@ -275,7 +285,7 @@ __global__ __launch_bounds__(W * 64) void k_dgemm(GemmArgs g, int tiles_n, int t
     } else if constexpr (EK == E_LOGITS) {
       const int row = e / BN, n = n0 + e % BN;
       const bool ok = r0 + row < row_end && n < g.N;
-      const int orow = s_orow[row];
+      const int orow = sh.orow[row];
       unsigned long long key = 0ull;
       if (ok) {
         const float v = tile_sum(row, e % BN);
@@ -301,7 +311,7 @@ __global__ __launch_bounds__(W * 64) void k_dgemm(GemmArgs g, int tiles_n, int t
         if (n < g.d) {
           g.out[(int64_t)(r0 + row) * g.ldo + n] = v;
         } else {
-          const int64_t base = s_kv[row];
+          const int64_t base = sh.kv[row];
           const int slot = (int)(base & (kPage - 1));
           const int64_t page = base - slot;
           const int nn = n - g.d, kvsel = nn / g.d, within = nn % g.d;
@@ -317,63 +327,90 @@ __global__ __launch_bounds__(W * 64) void k_dgemm(GemmArgs g, int tiles_n, int t
   }
 }
 
-template <typename T, int RM, int CN, int W, int KB, int AK, int EK, bool NORM>
-hipError_t launch_cfg(const GemmArgs& a, hipStream_t s) {
-  constexpr int BM = RM * 16, BN = CN * 16;
-  const int tiles_n = (a.N + BN - 1) / BN, tiles_m = (a.rm.rows + BM - 1) / BM;
-  const int grid = kXcds * ((tiles_n + kXcds - 1) / kXcds) * tiles_m;
-  if (tiles_n == 0 || tiles_m == 0) return hipSuccess;
-  hipLaunchKernelGGL((k_dgemm<T, RM, CN, W, KB, AK, EK, NORM>), dim3(grid), dim3(W * 64), 0, s, a, tiles_n,
-                     tiles_m);
+// One kernel, two tile shapes: the wide shape when more than `wide_above`
+// rows are active (the narrow shape would need more than one workgroup per
+// compute unit), the narrow shape otherwise.  The choice is uniform over the
+// grid and made from the active-row count the tiles need anyway.
+template <int RM, int CN> struct Shape {
+  static constexpr int BM = RM * 16, BN = CN * 16;
+};
+
+template <typename T, int RMn, int CNn, int RMw, int CNw, int W, int KB, int AK, int EK, bool NORM>
+__global__ __launch_bounds__(W * 64) void k_dgemm(GemmArgs g, int wide_above) {
+  constexpr int SLOTS = W > 8 ? 8 : W;
+  constexpr int BMX = RMn > RMw ? RMn * 16 : RMw * 16;
+  constexpr int REDN = SLOTS * RMn * 16 * (CNn * 16 + 1), REDW = SLOTS * RMw * 16 * (CNw * 16 + 1);
+  __shared__ float red[REDN > REDW ? REDN : REDW];
+  __shared__ float s_ss[NORM ? W * BMX : 1];
+  __shared__ float s_inv[BMX];
+  __shared__ int s_orow[EK == E_LOGITS ? BMX : 1];
+  __shared__ int64_t s_kv[EK == E_QKV ? BMX : 1];
+  const DgemmShared sh{red, s_ss, s_inv, s_orow, s_kv};
+  const int nact = g.rm.nact ? *g.rm.nact : g.rm.rows;
+  const int act_rows = g.spec ? g.rm.rows : min(nact, g.rm.rows);
+  if constexpr (RMn != RMw || CNn != CNw) {
+    if (act_rows > wide_above) {
+      dgemm_tile<T, RMw, CNw, W, KB, AK, EK, NORM>(g, nact, act_rows, sh);
+      return;
+    }
+  }
+  dgemm_tile<T, RMn, CNn, W, KB, AK, EK, NORM>(g, nact, act_rows, sh);
+}
+
+template <typename T, int RMn, int CNn, int RMw, int CNw, int W, int KB, int AK, int EK, bool NORM>
+hipError_t launch_cfg(const GemmArgs& a, int cus, hipStream_t s) {
+  constexpr int BMn = RMn * 16, BNn = CNn * 16, BMw = RMw * 16, BNw = CNw * 16;
+  const int tn_n = (a.N + BNn - 1) / BNn, tm_n = (a.rm.rows + BMn - 1) / BMn;
+  const int tn_w = (a.N + BNw - 1) / BNw, tm_w = (a.rm.rows + BMw - 1) / BMw;
+  if (tn_n == 0 || tm_n == 0) return hipSuccess;
+  // wide above the row count at which the narrow tiles exceed one per compute unit
+  const int wide_above = (RMn == RMw && CNn == CNw) ? a.rm.rows : std::max(1, cus / tn_n) * BMn;
+  const int tiles = std::max(tn_n * tm_n, tn_w * tm_w);
+  const int grid = kXcds * ((tiles + kXcds - 1) / kXcds);
+  hipLaunchKernelGGL((k_dgemm<T, RMn, CNn, RMw, CNw, W, KB, AK, EK, NORM>), dim3(grid), dim3(W * 64), 0, s, a,
+                     wide_above);
   return hipGetLastError();
 }
 
 // K steps per wave in one batch of loads: all of a wave's steps when they
 // fit in KBMAX, else batches of KBMAX.
-template <typename T, int RM, int CN, int W, int KBMAX, int AK, int EK, bool NORM>
-hipError_t launch_w(const GemmArgs& a, hipStream_t s) {
+template <typename T, int RMn, int CNn, int RMw, int CNw, int W, int KBMAX, int AK, int EK, bool NORM>
+hipError_t launch_w(const GemmArgs& a, int cus, hipStream_t s) {
   const int nj = (a.K / Mfma<T>::KS + W - 1) / W;
-  if (nj <= 2 || KBMAX == 2) return launch_cfg<T, RM, CN, W, 2, AK, EK, NORM>(a, s);
-  if (nj <= 3 || KBMAX == 3) return launch_cfg<T, RM, CN, W, (KBMAX >= 3 ? 3 : 2), AK, EK, NORM>(a, s);
-  return launch_cfg<T, RM, CN, W, (KBMAX >= 4 ? 4 : 2), AK, EK, NORM>(a, s);
+  if (nj <= 2 || KBMAX == 2) return launch_cfg<T, RMn, CNn, RMw, CNw, W, 2, AK, EK, NORM>(a, cus, s);
+  if (nj <= 3 || KBMAX == 3)
+    return launch_cfg<T, RMn, CNn, RMw, CNw, W, (KBMAX >= 3 ? 3 : 2), AK, EK, NORM>(a, cus, s);
+  return launch_cfg<T, RMn, CNn, RMw, CNw, W, (KBMAX >= 4 ? 4 : 2), AK, EK, NORM>(a, cus, s);
 }
 
 }  // namespace
 
 // Tile shapes (rows x columns, waves), measured on the projections of a
-// 256-row batch: the first loop has every row of the batch active (g.spec),
-// so its shapes aim at about one workgroup per compute unit over all rows;
-// later loops have fewer rows and use narrower tiles.
-//   QKV:     first loop 32 x 80,  later 32 x 64   (8 waves)
-//   gate/up: first loop 32 x 128, later 32 x 64   (8 waves)
-//   O:       32 x 32 (8 waves)
-//   down:    first loop 16 x 64 (8 waves), later 16 x 32 (16 waves)  [K > 768 in bf16]
-//   LM head: 32 x 64 (8 waves)
+// 256-row batch; each kernel holds a narrow shape and a wide one and picks
+// the wide one when the narrow tiles would need more than one workgroup per
+// compute unit.
+//   QKV:     32 x 64 | 32 x 80   (8 waves)
+//   gate/up: 32 x 64 | 32 x 128  (8 waves)
+//   O:       32 x 32             (8 waves)
+//   down:    16 x 32 | 16 x 48   (16 waves)  [K > 768 in bf16; else as O]
+//   LM head: 32 x 64             (8 waves)
 template <typename T>
-hipError_t launch_dgemm(const GemmArgs& a, AKind ak, EKind ek, bool norm, hipStream_t s) {
-  if (a.K % Mfma<T>::KS != 0 || a.rm.rows <= 0) return hipErrorInvalidValue;
-  const bool full = a.spec != 0;
+hipError_t launch_dgemm(const GemmArgs& a, AKind ak, EKind ek, bool norm, int cus, hipStream_t s) {
+  if (a.K % Mfma<T>::KS != 0 || a.rm.rows <= 0 || cus <= 0) return hipErrorInvalidValue;
   if (ek == E_QKV && norm) {
-    if (ak == A_SRC) return launch_w<T, 2, 5, 8, 3, A_SRC, E_QKV, true>(a, s);
-    if (full) return launch_w<T, 2, 5, 8, 3, A_CMP, E_QKV, true>(a, s);
-    return launch_w<T, 2, 4, 8, 3, A_CMP, E_QKV, true>(a, s);
+    if (ak == A_SRC) return launch_w<T, 2, 4, 2, 5, 8, 3, A_SRC, E_QKV, true>(a, cus, s);
+    return launch_w<T, 2, 4, 2, 5, 8, 3, A_CMP, E_QKV, true>(a, cus, s);
   }
-  if (ak == A_CMP && ek == E_SWIGLU && norm) {
-    if (full) return launch_w<T, 2, 8, 8, 3, A_CMP, E_SWIGLU, true>(a, s);
-    return launch_w<T, 2, 4, 8, 3, A_CMP, E_SWIGLU, true>(a, s);
-  }
-  if (ak == A_CMP && ek == E_LOGITS && norm) return launch_w<T, 2, 4, 8, 3, A_CMP, E_LOGITS, true>(a, s);
+  if (ak == A_CMP && ek == E_SWIGLU && norm) return launch_w<T, 2, 4, 2, 8, 8, 3, A_CMP, E_SWIGLU, true>(a, cus, s);
+  if (ak == A_CMP && ek == E_LOGITS && norm) return launch_w<T, 2, 4, 2, 4, 8, 3, A_CMP, E_LOGITS, true>(a, cus, s);
   if (ak == A_CMP && ek == E_RESID && !norm) {
-    if (a.K / Mfma<T>::KS > 3 * 8) {
-      if (full) return launch_w<T, 1, 4, 8, 4, A_CMP, E_RESID, false>(a, s);
-      return launch_w<T, 1, 2, 16, 4, A_CMP, E_RESID, false>(a, s);
-    }
-    return launch_w<T, 2, 2, 8, 3, A_CMP, E_RESID, false>(a, s);
+    if (a.K / Mfma<T>::KS > 3 * 8) return launch_w<T, 1, 2, 1, 3, 16, 4, A_CMP, E_RESID, false>(a, cus, s);
+    return launch_w<T, 2, 2, 2, 2, 8, 3, A_CMP, E_RESID, false>(a, cus, s);
   }
   return hipErrorInvalidValue;
 }
 
-template hipError_t launch_dgemm<float>(const GemmArgs&, AKind, EKind, bool, hipStream_t);
-template hipError_t launch_dgemm<bf16>(const GemmArgs&, AKind, EKind, bool, hipStream_t);
+template hipError_t launch_dgemm<float>(const GemmArgs&, AKind, EKind, bool, int, hipStream_t);
+template hipError_t launch_dgemm<bf16>(const GemmArgs&, AKind, EKind, bool, int, hipStream_t);
 
 }  // namespace tlf

@@ -81,8 +81,9 @@ hipError_t launch_gemm(const GemmArgs& a, AKind ak, EKind ek, hipStream_t s);
 // norm: A is the residual x and the product is taken with RMSNorm(x).
 // Supported: (A_SRC | A_CMP, E_QKV, norm), (A_CMP, E_SWIGLU | E_LOGITS,
 // norm), (A_CMP, E_RESID, no norm).
+// cus: compute units of the device (chooses between a narrow and a wide tile shape).
 template <typename T>
-hipError_t launch_dgemm(const GemmArgs& a, AKind ak, EKind ek, bool norm, hipStream_t s);
+hipError_t launch_dgemm(const GemmArgs& a, AKind ak, EKind ek, bool norm, int cus, hipStream_t s);
 
 // ---------------------------------------------------------------------------
 // Embedding + router (Section 3.2): h0 = E[x] + P[pos], z = W_r h0 + b_r,

@@ -32,6 +32,9 @@ DTYPE_F32 = 0
 DTYPE_BF16 = 1
 ROUTE = {"argmax": 0, "cumprob": 1, "fixed": 2}
 PREFILL_ALL_LOGITS = 1
+PROFILE_OFF = 0
+PROFILE_ATTN = 1
+PROFILE_BLOCK = 2
 
 
 class Config(ctypes.Structure):
@@ -283,8 +286,12 @@ class Session:
             res["index"] = index
         return res
 
-    def set_profiling(self, enable: bool) -> None:
-        self._check(self.lib.tlf_set_profiling(self.ctx, 1 if enable else 0), "tlf_set_profiling")
+    def set_profiling(self, mode) -> None:
+        """mode: False/"off", True/"attn" (events around every attention launch and
+        the loop region), or "block" (events around the loop region only)."""
+        code = {False: PROFILE_OFF, "off": PROFILE_OFF, True: PROFILE_ATTN, "attn": PROFILE_ATTN,
+                "block": PROFILE_BLOCK}[mode]
+        self._check(self.lib.tlf_set_profiling(self.ctx, code), "tlf_set_profiling")
 
     def close(self) -> None:
         if getattr(self, "ctx", None):

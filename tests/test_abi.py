@@ -127,3 +127,26 @@ def test_status_strings(lib):
     assert lib.tlf_status_str(tlf.OK) == b"ok"
     assert b"page" in lib.tlf_status_str(tlf.E_OUT_OF_PAGES)
     assert lib.tlf_status_str(12345) == b"unknown status"
+
+
+def test_binding_constants_match_the_header():
+    import re
+    text = open(os.path.join(ROOT, "include", "tlf.h")).read()
+    defs = {m.group(1): int(m.group(2)) for m in
+            re.finditer(r"^#define TLF_(\w+)\s+\(?(-?\d+)u?\)?", text, re.M)}
+    pairs = {"ABI_VERSION": tlf.ABI_VERSION, "OK": tlf.OK, "E_INVALID_ARG": tlf.E_INVALID_ARG,
+             "E_NEED_WORKSPACE": tlf.E_NEED_WORKSPACE, "E_OUT_OF_PAGES": tlf.E_OUT_OF_PAGES,
+             "E_STATE": tlf.E_STATE, "E_HIP": tlf.E_HIP, "E_DEVICE": tlf.E_DEVICE,
+             "DTYPE_F32": tlf.DTYPE_F32, "DTYPE_BF16": tlf.DTYPE_BF16,
+             "ROUTE_ARGMAX": tlf.ROUTE["argmax"], "ROUTE_CUMPROB": tlf.ROUTE["cumprob"],
+             "ROUTE_FIXED": tlf.ROUTE["fixed"], "PREFILL_ALL_LOGITS": tlf.PREFILL_ALL_LOGITS,
+             "PROFILE_OFF": tlf.PROFILE_OFF, "PROFILE_ATTN": tlf.PROFILE_ATTN,
+             "PROFILE_BLOCK": tlf.PROFILE_BLOCK}
+    for name, value in pairs.items():
+        assert defs[name] == value, name
+
+
+def test_profiling_mode_validated(lib):
+    # an unknown mode is rejected
+    assert lib.tlf_set_profiling(None, 3) == tlf.E_INVALID_ARG
+    assert lib.tlf_set_profiling(None, -1) == tlf.E_INVALID_ARG
