@@ -274,6 +274,8 @@ def main():
                     help="launch the timed decode steps kernel by kernel instead of replaying a HIP graph")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-prefill", action="store_true", help="skip the prefill measurement")
+    ap.add_argument("--prefill-only", action="store_true",
+                    help="run only the prefill measurement (batch 8 x 4096) and print its JSON")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--copy-calibration", action="store_true",
                     help=f"first run a device copy of {CALIB_BYTES} bytes (counter calibration)")
@@ -318,6 +320,9 @@ def main():
         torch.cuda.synchronize()
         del src, dst
         torch.cuda.empty_cache()
+    if args.prefill_only:
+        print(json.dumps(prefill_measure(torch, tlf, synth, "bf16_d1024_prefill_b8x4096")), flush=True)
+        return
     base = synth.CONFIGS[args.config]
     if args.warmup + args.steps + 2 * args.profiled_steps > base.steps or args.profiled_steps < 1:
         print(f"warmup + steps + 2 x profiled-steps must be <= {base.steps} for {args.config} "

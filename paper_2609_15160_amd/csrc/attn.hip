@@ -23,6 +23,20 @@ namespace {
 
 constexpr float kNegInf = -__builtin_inff();
 
+// Streaming loads of cache entries: each K/V byte is read once per launch, so
+// the loads are marked non-temporal.
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+template <typename F, typename P> __device__ __forceinline__ F ld_stream(const P* p) {
+  if constexpr (sizeof(F) == 16) {
+    return __builtin_bit_cast(F, __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p)));
+  } else if constexpr (sizeof(F) == 8) {
+    return __builtin_bit_cast(F, __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(p)));
+  } else {
+    return __builtin_bit_cast(F, __builtin_nontemporal_load(reinterpret_cast<const unsigned int*>(p)));
+  }
+}
+
 __device__ __forceinline__ float merge_scale(float m, float mn) {
   return m == kNegInf ? 0.f : exp2f(m - mn);
 }
@@ -67,7 +81,7 @@ __global__ __launch_bounds__(W * 64) void k_attn_decode(AttnDecodeArgs a) {
     // this wave's pages [p0, p1), a multiple of PPI pages each
     const int per = ((np + W - 1) / W + PPI - 1) / PPI * PPI;
     const int p0 = w * per, p1 = min(np, p0 + per);
-    const int64_t koff = k_block(c, a.layer, h) + (int64_t)c16 * D + quad * EPL;
+    const int64_t koff = k_block(c, a.layer, h) + (int64_t)(quad * kPage + c16) * EPL;  // fragment order
     const int64_t voff = v_block(c, a.layer, h) + (int64_t)c16 * kPage + quad * 4;
 
     // q (float32) as the B operand of S = K q^T, the same in all 16 columns;
@@ -95,17 +109,18 @@ __global__ __launch_bounds__(W * 64) void k_attn_decode(AttnDecodeArgs a) {
         const int pp = min(pg + p, p1 - 1);
         base[p] = pool + (int64_t)s_pages[pp] * c.page_elems;
 #pragma unroll
-        for (int ks = 0; ks < KSTEPS; ++ks) bk[p][ks] = M::load(base[p] + koff + ks * KS);
+        for (int ks = 0; ks < KSTEPS; ++ks) bk[p][ks] = ld_stream<KFrag>(base[p] + koff + ks * (4 * kPage * EPL));
       }
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) {
         const int64_t off = voff + (int64_t)dt * 16 * kPage;
         if constexpr (EPL == 8) {
-          const uint2 lo = *reinterpret_cast<const uint2*>(base[0] + off);
-          const uint2 hi = *reinterpret_cast<const uint2*>(base[PPI - 1] + off);
+          const u32x2 lo = ld_stream<u32x2>(base[0] + off);
+          const u32x2 hi = ld_stream<u32x2>(base[PPI - 1] + off);
           bv[dt] = make_uint4(lo.x, lo.y, hi.x, hi.y);
         } else {
-          bv[dt] = *reinterpret_cast<const uint4*>(base[0] + off);
+          const u32x4 v = ld_stream<u32x4>(base[0] + off);
+          bv[dt] = make_uint4(v.x, v.y, v.z, v.w);
         }
       }
     };
@@ -278,7 +293,15 @@ __global__ __launch_bounds__(256) void k_attn_prefill(AttnPrefillArgs a) {
       const int ka = kt * BKEY + key;
       V16<T> kv;
       kv.u = make_uint4(0, 0, 0, 0);
-      if (ka < n) kv = ld16(pool + (int64_t)pt[ka / kPage] * c.page_elems + koff + (ka % kPage) * D + col);
+      if (ka < n) {
+        const T* kb = pool + (int64_t)pt[ka / kPage] * c.page_elems + koff;
+        if constexpr (EPC == EPL) {
+          kv = ld16(kb + k_frag_off<T>(ka % kPage, col));  // one fragment: EPL consecutive elements
+        } else {
+#pragma unroll
+          for (int t = 0; t < EPC; ++t) kv.e[t] = kb[k_frag_off<T>(ka % kPage, col + t)];
+        }
+      }
       st16(&Ks[key * LDK + col], kv);
     }
     // V^T: each page holds [D][16 slots]; a 16-byte piece is EPC slots of one dimension

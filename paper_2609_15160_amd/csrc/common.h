@@ -48,11 +48,11 @@ struct CacheView {
   int max_pages, pages_per_seq, R, J, H, D;
 };
 
-// Page layout: for each layer j and head h a K block [kPage slots][D] (row
-// per token) followed, after all heads' K blocks, by V blocks stored
-// transposed, [D][kPage slots], so that one dimension of four consecutive
-// slots is a single 8- or 16-byte load.
-//   K(j, h, slot, e) = k_block(j, h) + slot * D + e
+// Page layout: for each layer j and head h a K block of kPage x D elements
+// in MFMA-fragment order (k_frag_off below), followed, after all heads' K
+// blocks, by V blocks stored transposed, [D][kPage slots], so that one
+// dimension of four consecutive slots is a single 8- or 16-byte load.
+//   K(j, h, slot, e) = k_block(j, h) + k_frag_off<T>(slot, e)
 //   V(j, h, slot, e) = v_block(j, h) + e * kPage + slot
 __device__ __forceinline__ int64_t k_block(const CacheView& c, int j, int h) {
   return (int64_t)((j * 2 + 0) * c.H + h) * kPage * c.D;
@@ -145,6 +145,18 @@ __device__ __forceinline__ void split_frag(const float* p, bf16x8& hi, bf16x8& l
   split4(*reinterpret_cast<const float4*>(p + 4), h1, l1);
   hi = __builtin_bit_cast(bf16x8, make_uint4(h0.x, h0.y, h1.x, h1.y));
   lo = __builtin_bit_cast(bf16x8, make_uint4(l0.x, l0.y, l1.x, l1.y));
+}
+
+// Offset of K(slot, e) inside a K block.  The decode attention takes K as the
+// A operand of S = K q^T, one MFMA per K step of KS head dimensions; lane
+// (slot, q) of a step holds the EPL consecutive elements e = ks * KS + q * EPL
+// + j.  Storing fragment (ks, q, slot) at ((ks * 4 + q) * kPage + slot) * EPL
+// makes the 64 lanes of one step read one contiguous run (1 KB in bf16).
+template <typename T> __device__ __forceinline__ int k_frag_off(int slot, int e) {
+  constexpr int KS = Mfma<T>::KS, EPL = Mfma<T>::EPL;
+  static_assert(KS == 4 * EPL, "four lane groups per K step");
+  const int ks = e / KS, q = (e % KS) / EPL, j = e % EPL;
+  return ((ks * 4 + q) * kPage + slot) * EPL + j;
 }
 
 __device__ __forceinline__ int lane_id() { return threadIdx.x & (kWave - 1); }

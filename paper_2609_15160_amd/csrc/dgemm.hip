@@ -318,7 +318,7 @@ __device__ __forceinline__ void dgemm_tile(const GemmArgs& g, int nact, int act_
           const int h = within / g.kv.c.D, el = within % g.kv.c.D;
           T* pool = reinterpret_cast<T*>(g.kv.c.pool);
           if (kvsel == 0)
-            pool[page + k_block(g.kv.c, g.kv.layer, h) + (int64_t)slot * g.kv.c.D + el] = from_f<T>(v);
+            pool[page + k_block(g.kv.c, g.kv.layer, h) + k_frag_off<T>(slot, el)] = from_f<T>(v);
           else
             pool[page + v_block(g.kv.c, g.kv.layer, h) + (int64_t)el * kPage + slot] = from_f<T>(v);
         }

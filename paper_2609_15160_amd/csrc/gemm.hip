@@ -257,7 +257,7 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
                 const int h = within / g.kv.c.D, e = within % g.kv.c.D;
                 T* pool = reinterpret_cast<T*>(g.kv.c.pool);
                 if (kvsel == 0)
-                  pool[page + k_block(g.kv.c, g.kv.layer, h) + (int64_t)slot * g.kv.c.D + e] = from_f<T>(v);
+                  pool[page + k_block(g.kv.c, g.kv.layer, h) + k_frag_off<T>(slot, e)] = from_f<T>(v);
                 else
                   pool[page + v_block(g.kv.c, g.kv.layer, h) + (int64_t)e * kPage + slot] = from_f<T>(v);
               }
