@@ -152,6 +152,58 @@ def cpu_baseline(model, w, prompts, budget_s, seqs=8):
                       f"prompts (untimed), then {n} batched greedy decode steps timed ({dt:.1f} s)"}
 
 
+def threshold_sweep(torch, tlf, synth, name, thresholds=(0.3, 0.4, 0.5, 0.6, 0.7), warmup=4, steps=20):
+    """The workload with a two-layer MLP router (hidden width d) and the
+    cumulative-probability rule at several thresholds (the analogue of the
+    paper's threshold study): depth mix and decode speed per threshold, plus
+    the same router under argmax."""
+    import numpy as np
+    base = synth.CONFIGS[name]
+    m = base.replace(router_hidden=base.d_model)
+    w = synth.make_weights(m)
+    prompts = synth.make_prompts(m)
+    B, T = prompts.shape
+    rows = []
+    for rule, th in [("argmax", None)] + [("cumprob", t) for t in thresholds]:
+        sess = tlf.Session(m, w, max_batch=B, max_pos=T + warmup + steps, route_rule=rule,
+                           threshold=0.5 if th is None else th, max_prefill_tokens=65536)
+        try:
+            toks = torch.from_numpy(prompts).cuda()
+            logits, _ = sess.prefill(toks, want_depths=False)
+            tok = [torch.argmax(logits, dim=-1).to(torch.int32).contiguous(),
+                   torch.empty(B, dtype=torch.int32, device="cuda")]
+            del logits
+            out = torch.empty((B, m.vocab), dtype=torch.float32, device="cuda")
+            k = 0
+            for _ in range(warmup):
+                sess.decode_into(tok[k % 2], out, next_tok=tok[(k + 1) % 2])
+                k += 1
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            e0.record()
+            for _ in range(steps):
+                sess.decode_into(tok[k % 2], out, next_tok=tok[(k + 1) % 2])
+                k += 1
+            e1.record()
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1)
+            st = sess.stats()
+            if st["status"] != 0:
+                raise RuntimeError(f"device error {st['status']}")
+            hist = np.asarray(st["depth_hist"], dtype=np.float64)
+            rows.append({"rule": rule, "threshold": th, "tokens_per_s": B * steps / (ms / 1e3),
+                         "ms_per_step": ms / steps,
+                         "mean_depth": float((hist * np.arange(1, len(hist) + 1)).sum() / hist.sum()),
+                         "depth_hist": [int(v) for v in st["depth_hist"]]})
+            log(f"router sweep {rule} {th}: {ms / steps:.3f} ms/step, mean depth {rows[-1]['mean_depth']:.2f}")
+        finally:
+            sess.close()
+            torch.cuda.empty_cache()
+    return {"workload": f"{name} with a 2-layer MLP router (hidden {m.router_hidden}, SiLU), bias calibrated "
+                        f"for the argmax rule; {steps} graph-replayed steps per setting",
+            "rows": rows}
+
+
 def prefill_measure(torch, tlf, synth, name):
     """Prefill-only workload: time tlf_prefill and count the algorithmic FLOPs."""
     import numpy as np
@@ -274,6 +326,7 @@ def main():
                     help="launch the timed decode steps kernel by kernel instead of replaying a HIP graph")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-prefill", action="store_true", help="skip the prefill measurement")
+    ap.add_argument("--no-sweep", action="store_true", help="skip the MLP-router threshold sweep")
     ap.add_argument("--prefill-only", action="store_true",
                     help="run only the prefill measurement (batch 8 x 4096) and print its JSON")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
@@ -396,6 +449,8 @@ def main():
     if not args.no_prefill:
         out["prefill"] = prefill_measure(torch, tlf, synth, "bf16_d1024_prefill_b8x4096")
         log(f"prefill 8x4096: {out['prefill']['ms']:.2f} ms")
+    if not args.no_sweep:
+        out["router_threshold_sweep"] = threshold_sweep(torch, tlf, synth, args.config)
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline(model, w, prompts, args.cpu_seconds)
         log(f"cpu baseline: {out['cpu_baseline']['value']:.3f} tokens/s")

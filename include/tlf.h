@@ -49,7 +49,7 @@
 extern "C" {
 #endif
 
-#define TLF_ABI_VERSION 1
+#define TLF_ABI_VERSION 2
 #define TLF_MAX_LOOPS 16
 #define TLF_MAX_LAYERS 8
 #define TLF_MAX_BATCH 4096
@@ -103,6 +103,8 @@ typedef struct tlf_config {
   int32_t decode_graph;  /* 1: each decode step replays a captured HIP graph (captured on the first
                             step and again whenever the batch or an output pointer changes);
                             0: kernels are launched one by one */
+  int32_t router_hidden; /* 0: linear router z = W_r h0 + b_r; Hr > 0 (<= 4096, multiple of 64): the
+                            two-layer MLP router z = W_r silu(W_1 h0 + b_1) + b_r (Section 3.2) */
 } tlf_config;
 
 /* Weights of layer j of the shared block, row-major [out][in] (y = x W^T),
@@ -117,11 +119,13 @@ typedef struct tlf_layer_weights {
 typedef struct tlf_weights {
   const void* tok_emb;      /* [V][d] storage dtype; also the LM head when lm_head is NULL */
   const void* pos_emb;      /* [max_pos][d] storage dtype */
-  const float* router_w;    /* [R][d] float32 */
+  const float* router_w;    /* [R][d] float32 ([R][Hr], the output layer, for an MLP router) */
   const float* router_b;    /* [R] float32 */
   const void* lm_head;      /* [V][d] storage dtype, or NULL for a head tied to tok_emb */
   int32_t n_layers;         /* must equal config.n_layers */
   const tlf_layer_weights* layers; /* host array of n_layers entries (copied by tlf_init) */
+  const void* router_w1;    /* MLP router hidden layer [Hr][d] storage dtype; NULL for a linear router */
+  const float* router_b1;   /* [Hr] float32; NULL for a linear router */
 } tlf_weights;
 
 typedef struct tlf_cache_stats_t {

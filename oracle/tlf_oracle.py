@@ -85,6 +85,9 @@ class Model:
         self.P = f64(weights["pos_emb"])
         self.Wr = f64(weights["router_w"])
         self.br = f64(weights["router_b"])
+        # optional hidden layer of a 2-layer MLP router (Section 3.2)
+        self.Wr1 = f64(weights["router_w1"]) if weights.get("router_w1") is not None else None
+        self.br1 = f64(weights["router_b1"]) if self.Wr1 is not None else None
         self.V, self.d = self.E.shape
         head = weights.get("lm_head")
         self.head = self.E if head is None else f64(head)
@@ -153,8 +156,10 @@ def attend(q: np.ndarray, k: np.ndarray, v: np.ndarray, allowed: np.ndarray) -> 
 # ---------------------------------------------------------------------------
 
 def router_logits(model: Model, h0: np.ndarray) -> np.ndarray:
-    """f_theta(h^(0)) = W_r h^(0) + b_r, rounded to float32 where it decides depth."""
-    z = h0 @ model.Wr.T + model.br
+    """f_theta(h^(0)): W_r h^(0) + b_r for the linear router, or the two-layer MLP
+    W_r silu(W_1 h^(0) + b_1) + b_r; rounded to float32 where it decides depth."""
+    h = h0 if model.Wr1 is None else silu(h0 @ model.Wr1.T + model.br1)
+    z = h @ model.Wr.T + model.br
     return z.astype(np.float32).astype(np.float64)
 
 

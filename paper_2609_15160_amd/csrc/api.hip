@@ -20,7 +20,7 @@ int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 enum Buf {
   B_POOL, B_POS, B_PAGE_TABLE, B_CACHE_LEN, B_SEQ_LEN, B_SCALARS, B_DEPTH_HIST, B_STEP_STATS,
   B_X_DEC, B_XC_DEC, B_KVSLOT, B_DEPTH_DEC, B_PERM, B_NACT, B_Q_DEC, B_O_DEC, B_ACT_DEC, B_KEYS,
-  B_X_PRE, B_Y_PRE, B_DEPTH_PRE, B_TOK_IDX, B_Q_PRE, B_O_PRE, B_ACT_PRE,
+  B_X_PRE, B_Y_PRE, B_DEPTH_PRE, B_TOK_IDX, B_Q_PRE, B_O_PRE, B_ACT_PRE, B_HID,
   B_COUNT
 };
 
@@ -66,6 +66,7 @@ bool make_layout(const tlf_config& c, Layout* L) {
   sz[B_Q_PRE] = P * d * 4;
   sz[B_O_PRE] = P * d * 4;
   sz[B_ACT_PRE] = P * F * 4;
+  sz[B_HID] = std::max(P, B) * (int64_t)c.router_hidden * 4;  // MLP router hidden rows
   size_t off = 0;
   for (int i = 0; i < B_COUNT; ++i) {
     if (sz[i] < 0) return false;
@@ -104,6 +105,7 @@ int validate_config(const tlf_config* c) {
   }
   if (!(c->rms_eps > 0.f) || !std::isfinite(c->rms_eps)) return TLF_E_INVALID_ARG;
   if (c->decode_graph != 0 && c->decode_graph != 1) return TLF_E_INVALID_ARG;
+  if (c->router_hidden < 0 || c->router_hidden > 4096 || c->router_hidden % 64 != 0) return TLF_E_INVALID_ARG;
   // the decode attention stages one sequence's page list in LDS
   if (ceil_div(c->max_pos, kPage) > kAttnMaxPages) return TLF_E_INVALID_ARG;
   // the decode projections address weights and activations with 32-bit element offsets
@@ -119,6 +121,7 @@ int validate_config(const tlf_config* c) {
 int validate_weights(const tlf_config* c, const tlf_weights* w) {
   if (!w || !w->tok_emb || !w->pos_emb || !w->router_w || !w->router_b) return TLF_E_INVALID_ARG;
   if (w->n_layers != c->n_layers || !w->layers) return TLF_E_INVALID_ARG;
+  if ((c->router_hidden > 0) != (w->router_w1 != nullptr && w->router_b1 != nullptr)) return TLF_E_INVALID_ARG;
   for (int j = 0; j < w->n_layers; ++j) {
     const tlf_layer_weights& l = w->layers[j];
     if (!l.w_qkv || !l.w_o || !l.w_gate_up || !l.w_down) return TLF_E_INVALID_ARG;
@@ -209,6 +212,27 @@ int precheck(tlf_ctx* ctx) {
   return TLF_OK;
 }
 
+// The MLP router (Section 3.2) on `rows` rows of h0: hidden = silu(W_1 h0 + b_1)
+// by a projection, then z = W_r hidden + b_r and the depth rule per row.
+template <typename T>
+int run_mlp_router(tlf_ctx* ctx, hipStream_t s, const float* h0, int rows, bool decode_shape, int32_t* depth,
+                   int32_t* out_depth, float* out_margin) {
+  const tlf_config& c = ctx->cfg;
+  const int Hr = c.router_hidden;
+  float* hid = ctx->buf<float>(B_HID);
+  GemmArgs g;
+  g.A = h0; g.lda = c.d_model; g.W = ctx->w.router_w1; g.N = Hr; g.K = c.d_model; g.w_rows = Hr;
+  g.rm.rows = rows; g.out = hid; g.ldo = Hr; g.bias = ctx->w.router_b1; g.spec = 1;
+  if (decode_shape) TLF_HIP(launch_dgemm<T>(g, A_CMP, E_HIDDEN, false, ctx->cus, s));
+  else TLF_HIP(launch_gemm<T>(g, A_CMP, E_HIDDEN, s));
+  RouteArgs ra;
+  ra.h = hid; ra.rows = rows; ra.Hr = Hr; ra.R = c.max_loops; ra.Wr = ctx->w.router_w; ra.br = ctx->w.router_b;
+  ra.depth = depth; ra.out_depth = out_depth; ra.out_margin = out_margin;
+  ra.rule = c.route_rule; ra.threshold = c.route_threshold; ra.fixed = c.fixed_depth;
+  TLF_HIP(launch_route_rows(ra, s));
+  return TLF_OK;
+}
+
 // Waves sharing one (row, head) in the decode attention: enough waves in
 // flight to cover the device even when batch x heads is small.
 int attn_waves(const tlf_ctx* ctx) {
@@ -241,7 +265,12 @@ int run_prefill(tlf_ctx* ctx, int B, int T_, const int32_t* tokens, float* logit
     ea.out_depth = depths ? depths + (int64_t)b0 * T_ : nullptr;
     ea.rule = c.route_rule; ea.threshold = c.route_threshold; ea.fixed = c.fixed_depth;
     ea.err = ctx->cv.err;
+    ea.route = c.router_hidden == 0;
     TLF_HIP(launch_embed_route<T>(ea, s));
+    if (c.router_hidden > 0) {
+      const int st = run_mlp_router<T>(ctx, s, x, rows, false, ea.depth, ea.out_depth, nullptr);
+      if (st != TLF_OK) return st;
+    }
 
     PrefillPlanArgs pa;
     pa.c = ctx->cv; pa.b0 = b0; pa.G = Gc; pa.T = T_;
@@ -323,7 +352,12 @@ int run_decode(tlf_ctx* ctx, hipStream_t s, const int32_t* tokens, float* logits
   ea.depth = ctx->buf<int32_t>(B_DEPTH_DEC);
   ea.out_depth = depths; ea.out_margin = margin;
   ea.rule = c.route_rule; ea.threshold = c.route_threshold; ea.fixed = c.fixed_depth; ea.err = ctx->cv.err;
+  ea.route = c.router_hidden == 0;
   TLF_HIP(launch_embed_route<T>(ea, s));
+  if (c.router_hidden > 0) {
+    const int st = run_mlp_router<T>(ctx, s, x, B, true, ea.depth, depths, margin);
+    if (st != TLF_OK) return st;
+  }
 
   DecodePlanArgs pa;
   pa.c = ctx->cv; pa.B = B; pa.depth = ctx->buf<int32_t>(B_DEPTH_DEC); pa.perm = perm; pa.nact = nact;

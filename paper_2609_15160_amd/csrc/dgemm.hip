@@ -307,6 +307,9 @@ __device__ __forceinline__ void dgemm_tile(const GemmArgs& g, int nact, int act_
       const float v = tile_sum(row, col);
       if constexpr (EK == E_RESID) {
         g.out[(int64_t)(r0 + row) * g.ldo + n] = xr[k] + v;
+      } else if constexpr (EK == E_HIDDEN) {
+        const float u = v + g.bias[n];
+        g.out[(int64_t)(r0 + row) * g.ldo + n] = u / (1.f + __expf(-u));
       } else {  // E_QKV
         if (n < g.d) {
           g.out[(int64_t)(r0 + row) * g.ldo + n] = v;
@@ -394,6 +397,7 @@ hipError_t launch_w(const GemmArgs& a, int cus, hipStream_t s) {
 //   O:       32 x 32             (8 waves)
 //   down:    16 x 32 | 16 x 48   (16 waves)  [K > 768 in bf16; else as O]
 //   LM head: 32 x 64             (8 waves)
+//   router hidden layer: 32 x 32 (8 waves)
 template <typename T>
 hipError_t launch_dgemm(const GemmArgs& a, AKind ak, EKind ek, bool norm, int cus, hipStream_t s) {
   if (a.K % Mfma<T>::KS != 0 || a.rm.rows <= 0 || cus <= 0) return hipErrorInvalidValue;
@@ -403,6 +407,7 @@ hipError_t launch_dgemm(const GemmArgs& a, AKind ak, EKind ek, bool norm, int cu
   }
   if (ak == A_CMP && ek == E_SWIGLU && norm) return launch_w<T, 2, 4, 2, 8, 8, 3, A_CMP, E_SWIGLU, true>(a, cus, s);
   if (ak == A_CMP && ek == E_LOGITS && norm) return launch_w<T, 2, 4, 2, 4, 8, 3, A_CMP, E_LOGITS, true>(a, cus, s);
+  if (ak == A_CMP && ek == E_HIDDEN && !norm) return launch_w<T, 2, 2, 2, 2, 8, 3, A_CMP, E_HIDDEN, false>(a, cus, s);
   if (ak == A_CMP && ek == E_RESID && !norm) {
     if (a.K / Mfma<T>::KS > 3 * 8) return launch_w<T, 1, 2, 1, 3, 16, 4, A_CMP, E_RESID, false>(a, cus, s);
     return launch_w<T, 2, 2, 2, 2, 8, 3, A_CMP, E_RESID, false>(a, cus, s);

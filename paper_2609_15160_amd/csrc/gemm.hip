@@ -12,6 +12,7 @@
 //   E_SWIGLU:  act = silu(gate) * up, gate/up columns interleaved in 16-column
 //              groups so every wave holds matching pairs
 //   E_LOGITS:  float logits plus a packed (value, -index) atomicMax for greedy
+//   E_HIDDEN:  silu(result + bias), the MLP router's hidden layer
 //
 // Tiling: 256 threads = 4 waves in a 2x2 grid; each wave owns MT x NT 16x16
 // MFMA tiles.  K advances BK elements per tile, staged through LDS from a
@@ -245,6 +246,9 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
           const float v = acc[i][j][r];
           if constexpr (EK == E_RESID) {
             reinterpret_cast<float*>(g.out)[(int64_t)src * g.ldo + n] += v;
+          } else if constexpr (EK == E_HIDDEN) {
+            const float u = v + g.bias[n];
+            g.out[(int64_t)rg * g.ldo + n] = u / (1.f + __expf(-u));
           } else {  // E_QKV
             if (n < g.d) {
               reinterpret_cast<float*>(g.out)[(int64_t)rg * g.ldo + n] = v;
@@ -283,6 +287,7 @@ hipError_t launch_tiles(const GemmArgs& a, AKind ak, EKind ek, hipStream_t s) {
   TLF_GEMM_CASE(A_SRC, E_SWIGLU)
   TLF_GEMM_CASE(A_SRC, E_LOGITS)
   TLF_GEMM_CASE(A_CMP, E_RESID)
+  TLF_GEMM_CASE(A_CMP, E_HIDDEN)
 #undef TLF_GEMM_CASE
   return hipErrorInvalidValue;
 }

@@ -49,8 +49,9 @@ struct KvDst {
 enum AKind { A_SRC = 0, A_CMP = 1 };
 // E_QKV: q to a buffer, k and v appended to the loop's cache pages.
 // E_RESID: x[src(r)] += result.  E_SWIGLU: act = silu(gate) * up.
-// E_LOGITS: float logits + greedy keys.
-enum EKind { E_QKV = 0, E_RESID = 1, E_SWIGLU = 3, E_LOGITS = 4 };
+// E_LOGITS: float logits + greedy keys.  E_HIDDEN: out[r] = silu(result + bias)
+// (the MLP router's hidden layer).
+enum EKind { E_QKV = 0, E_RESID = 1, E_SWIGLU = 3, E_LOGITS = 4, E_HIDDEN = 5 };
 
 struct GemmArgs {
   const float* A = nullptr; // float32 rows
@@ -70,6 +71,7 @@ struct GemmArgs {
   int F = 0;                // E_SWIGLU: hidden width
   float eps = 1e-5f;        // RMSNorm epsilon of the decode projections that fuse the norm
   float* a_copy = nullptr;  // decode: the operand rows are also written here, compact (first projection)
+  const float* bias = nullptr;  // E_HIDDEN: [N] float32
   int spec = 0;             // decode: every row is active; loads need not wait for the active count
 };
 
@@ -80,7 +82,7 @@ hipError_t launch_gemm(const GemmArgs& a, AKind ak, EKind ek, hipStream_t s);
 // compact order (E_RESID: out[r] += result; E_LOGITS: logits row src(r)).
 // norm: A is the residual x and the product is taken with RMSNorm(x).
 // Supported: (A_SRC | A_CMP, E_QKV, norm), (A_CMP, E_SWIGLU | E_LOGITS,
-// norm), (A_CMP, E_RESID, no norm).
+// norm), (A_CMP, E_RESID | E_HIDDEN, no norm).
 // cus: compute units of the device (chooses between a narrow and a wide tile shape).
 template <typename T>
 hipError_t launch_dgemm(const GemmArgs& a, AKind ak, EKind ek, bool norm, int cus, hipStream_t s);
@@ -107,8 +109,24 @@ struct EmbedArgs {
   int rule = 0, fixed = 1;
   float threshold = 0.5f;
   int32_t* err = nullptr;
+  int route = 1;                  // 0: the router is an MLP, routed later by launch_route_rows
 };
 template <typename T> hipError_t launch_embed_route(const EmbedArgs& a, hipStream_t s);
+
+// Output layer of the MLP router and the depth rule: z = W_r h + b_r for the
+// hidden rows h [rows][Hr] (float32), depth and margin as in launch_embed_route.
+struct RouteArgs {
+  const float* h = nullptr;
+  int rows = 0, Hr = 0, R = 0;
+  const float* Wr = nullptr;      // [R][Hr]
+  const float* br = nullptr;      // [R]
+  int32_t* depth = nullptr;
+  int32_t* out_depth = nullptr;   // optional
+  float* out_margin = nullptr;    // optional
+  int rule = 0, fixed = 1;
+  float threshold = 0.5f;
+};
+hipError_t launch_route_rows(const RouteArgs& a, hipStream_t s);
 
 // y[src(r)] = RMSNorm(x[src(r)]) on the active rows of a row map.
 struct ResidNormArgs {

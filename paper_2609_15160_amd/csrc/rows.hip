@@ -52,6 +52,44 @@ __device__ __forceinline__ float sumsq(float4 v, float acc) {
 }
 __device__ __forceinline__ float4 scale4(float4 v, float s) { return make_float4(v.x * s, v.y * s, v.z * s, v.w * s); }
 
+// Routed depth m in [1, R] and decision margin from router logits z (Eq. 2-5):
+// rule 0 argmax (lowest on ties), 1 cumulative probability with a strict
+// threshold and p^(1) = 1, 2 fixed depth.
+__device__ void decide_depth(const float* z, int R, int rule, float threshold, int fixed, int* m_out,
+                             float* margin_out) {
+  int m = 1;
+  float margin = __builtin_inff();
+  if (rule == 0) {  // argmax, lowest index on ties
+    int best = 0;
+    for (int i = 1; i < R; ++i)
+      if (z[i] > z[best]) best = i;
+    float second = -__builtin_inff();
+    for (int i = 0; i < R; ++i)
+      if (i != best && z[i] > second) second = z[i];
+    m = best + 1;
+    if (R > 1) margin = z[best] - second;
+  } else if (rule == 1) {  // cumulative probability (Eq. 2-5)
+    float mx = z[0];
+    for (int i = 1; i < R; ++i) mx = fmaxf(mx, z[i]);
+    float ex[kMaxLoops];
+    float tot = 0.f;
+    for (int i = 0; i < R; ++i) { ex[i] = __expf(z[i] - mx); tot += ex[i]; }
+    float p_sfx[kMaxLoops + 1];
+    p_sfx[R] = 0.f;
+    float run = 0.f;
+    for (int i = R - 1; i >= 0; --i) { run += ex[i]; p_sfx[i] = run / tot; }
+    p_sfx[0] = 1.f;  // p^(1) = 1: every token runs loop 1
+    m = 1;
+    for (int i = 1; i < R; ++i)
+      if (p_sfx[i] > threshold) m = i + 1;
+    margin = fminf(p_sfx[m - 1] - threshold, threshold - p_sfx[m]);
+  } else {
+    m = fixed;
+  }
+  *m_out = m;
+  *margin_out = margin;
+}
+
 // ---------------------------------------------------------------------------
 // h0 = E[x] + P[pos] (learned absolute position added once, Section 3.2),
 // z = W_r h0 + b_r (Eq. 2's router as a linear map), the depth rule, and
@@ -93,7 +131,7 @@ __global__ __launch_bounds__(256) void k_embed_route(EmbedArgs a) {
       ss = sumsq(h[c], ss);
 #pragma unroll
       for (int i = 0; i < kMaxLoops; ++i) {
-        if (i < a.R) {
+        if (a.route && i < a.R) {
           const float4 w = V4<float>::load(a.Wr + (int64_t)i * a.d + k);
           z[i] = fmaf(w.w, h[c].w, fmaf(w.z, h[c].z, fmaf(w.y, h[c].y, fmaf(w.x, h[c].x, z[i]))));
         }
@@ -110,40 +148,52 @@ __global__ __launch_bounds__(256) void k_embed_route(EmbedArgs a) {
       if (k < a.d) V4<float>::store(y + k, scale4(h[c], inv));
     }
   }
+  if (!a.route) return;  // the MLP router runs after this kernel
 #pragma unroll
   for (int i = 0; i < kMaxLoops; ++i)
     if (i < a.R) z[i] = wave_sum(z[i]) + a.br[i];
   if (lane != 0) return;
-  const int R = a.R;
-  int m = 1;
-  float margin = __builtin_inff();
-  if (a.rule == 0) {  // argmax, lowest index on ties
-    int best = 0;
-    for (int i = 1; i < R; ++i)
-      if (z[i] > z[best]) best = i;
-    float second = -__builtin_inff();
-    for (int i = 0; i < R; ++i)
-      if (i != best && z[i] > second) second = z[i];
-    m = best + 1;
-    if (R > 1) margin = z[best] - second;
-  } else if (a.rule == 1) {  // cumulative probability (Eq. 2-5)
-    float mx = z[0];
-    for (int i = 1; i < R; ++i) mx = fmaxf(mx, z[i]);
-    float ex[kMaxLoops];
-    float tot = 0.f;
-    for (int i = 0; i < R; ++i) { ex[i] = __expf(z[i] - mx); tot += ex[i]; }
-    float p_sfx[kMaxLoops + 1];
-    p_sfx[R] = 0.f;
-    float run = 0.f;
-    for (int i = R - 1; i >= 0; --i) { run += ex[i]; p_sfx[i] = run / tot; }
-    p_sfx[0] = 1.f;  // p^(1) = 1: every token runs loop 1
-    m = 1;
-    for (int i = 1; i < R; ++i)
-      if (p_sfx[i] > a.threshold) m = i + 1;
-    margin = fminf(p_sfx[m - 1] - a.threshold, a.threshold - p_sfx[m]);
-  } else {
-    m = a.fixed;
+  int m;
+  float margin;
+  decide_depth(z, a.R, a.rule, a.threshold, a.fixed, &m, &margin);
+  a.depth[row] = m;
+  if (a.out_depth) a.out_depth[row] = m;
+  if (a.out_margin) a.out_margin[row] = margin;
+}
+
+// ---------------------------------------------------------------------------
+// Output layer of the MLP router on hidden rows (z = W_r h + b_r), then the
+// depth rule.  One wave per row; lane l holds elements 4l + 256c.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void k_route_rows(RouteArgs a) {
+  const int lane = lane_id();
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= a.rows) return;
+  const float* h = a.h + (int64_t)row * a.Hr;
+  float z[kMaxLoops];
+#pragma unroll
+  for (int i = 0; i < kMaxLoops; ++i) z[i] = 0.f;
+#pragma unroll
+  for (int c = 0; c < kRowChunks; ++c) {
+    const int k = 4 * lane + 256 * c;
+    if (k < a.Hr) {
+      const float4 hv = V4<float>::load(h + k);
+#pragma unroll
+      for (int i = 0; i < kMaxLoops; ++i) {
+        if (i < a.R) {
+          const float4 w = V4<float>::load(a.Wr + (int64_t)i * a.Hr + k);
+          z[i] = fmaf(w.w, hv.w, fmaf(w.z, hv.z, fmaf(w.y, hv.y, fmaf(w.x, hv.x, z[i]))));
+        }
+      }
+    }
   }
+#pragma unroll
+  for (int i = 0; i < kMaxLoops; ++i)
+    if (i < a.R) z[i] = wave_sum(z[i]) + a.br[i];
+  if (lane != 0) return;
+  int m;
+  float margin;
+  decide_depth(z, a.R, a.rule, a.threshold, a.fixed, &m, &margin);
   a.depth[row] = m;
   if (a.out_depth) a.out_depth[row] = m;
   if (a.out_margin) a.out_margin[row] = margin;
@@ -203,5 +253,12 @@ template <typename T> hipError_t launch_resid_norm(const ResidNormArgs& a, hipSt
 }
 template hipError_t launch_resid_norm<float>(const ResidNormArgs&, hipStream_t);
 template hipError_t launch_resid_norm<bf16>(const ResidNormArgs&, hipStream_t);
+
+hipError_t launch_route_rows(const RouteArgs& a, hipStream_t s) {
+  if (a.rows <= 0) return hipSuccess;
+  if (a.Hr > 4 * kWave * kRowChunks || a.Hr % 4 != 0) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_route_rows, dim3((a.rows + 3) / 4), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
 
 }  // namespace tlf

@@ -15,7 +15,7 @@ PKG_DIR = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG_DIR, "libtlf.so")
 HEADER = os.path.join(os.path.dirname(PKG_DIR), "include", "tlf.h")
 
-ABI_VERSION = 1
+ABI_VERSION = 2
 MAX_LOOPS = 16
 MAX_LAYERS = 8
 PAGE_TOKENS = 16
@@ -46,6 +46,7 @@ class Config(ctypes.Structure):
         ("max_pages", ctypes.c_int32), ("max_prefill_tokens", ctypes.c_int32),
         ("route_rule", ctypes.c_int32), ("route_threshold", ctypes.c_float),
         ("fixed_depth", ctypes.c_int32), ("rms_eps", ctypes.c_float), ("decode_graph", ctypes.c_int32),
+        ("router_hidden", ctypes.c_int32),
     ]
 
 
@@ -58,7 +59,7 @@ class Weights(ctypes.Structure):
     _fields_ = [
         ("tok_emb", ctypes.c_void_p), ("pos_emb", ctypes.c_void_p), ("router_w", ctypes.c_void_p),
         ("router_b", ctypes.c_void_p), ("lm_head", ctypes.c_void_p), ("n_layers", ctypes.c_int32),
-        ("layers", ctypes.POINTER(LayerWeights)),
+        ("layers", ctypes.POINTER(LayerWeights)), ("router_w1", ctypes.c_void_p), ("router_b1", ctypes.c_void_p),
     ]
 
 
@@ -142,7 +143,7 @@ def make_config(model, max_batch: int, max_pos: int, max_pages: int, route_rule:
         max_batch=max_batch, page_tokens=PAGE_TOKENS, max_pages=max_pages,
         max_prefill_tokens=max_prefill_tokens, route_rule=ROUTE[route_rule],
         route_threshold=threshold, fixed_depth=fixed_depth, rms_eps=model.rms_eps,
-        decode_graph=1 if decode_graph else 0)
+        decode_graph=1 if decode_graph else 0, router_hidden=getattr(model, "router_hidden", 0))
 
 
 def workspace_bytes(cfg: Config) -> int:
@@ -189,6 +190,9 @@ class Session:
         }
         if weights.get("lm_head") is not None:
             self.w["lm_head"] = dev(weights["lm_head"], sdt)
+        if weights.get("router_w1") is not None:
+            self.w["router_w1"] = dev(weights["router_w1"], sdt)
+            self.w["router_b1"] = dev(weights["router_b1"], torch.float32)
         if self.w["pos_emb"].shape[0] < max_pos:
             raise ValueError("position table shorter than max_pos")
         self.layers = []
@@ -200,7 +204,9 @@ class Session:
         self._weights = Weights(self.w["tok_emb"].data_ptr(), self.w["pos_emb"].data_ptr(),
                                 self.w["router_w"].data_ptr(), self.w["router_b"].data_ptr(),
                                 self.w["lm_head"].data_ptr() if "lm_head" in self.w else None,
-                                len(self.layers), self._lw)
+                                len(self.layers), self._lw,
+                                self.w["router_w1"].data_ptr() if "router_w1" in self.w else None,
+                                self.w["router_b1"].data_ptr() if "router_b1" in self.w else None)
         need = workspace_bytes(self.cfg)
         self.workspace = torch.empty(need, dtype=torch.uint8, device=self.device)
         self.stream = torch.cuda.current_stream(self.device)

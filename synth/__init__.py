@@ -40,6 +40,7 @@ STREAM_TOK_EMB = 1
 STREAM_POS_EMB = 2
 STREAM_ROUTER_W = 3
 STREAM_LM_HEAD = 4      # optional untied LM head
+STREAM_ROUTER_W1 = 5    # hidden layer of the MLP router
 STREAM_LAYER_BASE = 16  # layer j uses 16 + 4j + {0: qkv, 1: o, 2: gate_up, 3: down}
 STREAM_PROMPT = 100
 STREAM_CALIB = 101
@@ -173,6 +174,7 @@ class ModelConfig:
     page_tokens: int = 16
     rms_eps: float = 1e-5
     std: float = 0.02
+    router_hidden: int = 0  # 0: linear router; else the hidden width of a 2-layer MLP router
 
     @property
     def max_pos(self) -> int:
@@ -210,26 +212,23 @@ def _mat(seed: int, stream: int, rows: int, cols: int, cfg: ModelConfig) -> np.n
     return to_storage(normal(seed, stream, rows * cols, cfg.std).reshape(rows, cols), cfg.dtype)
 
 
-def calibrate_router_bias(router_w: np.ndarray, cfg: ModelConfig, seed: int = SEED,
-                          target=DEPTH_TARGET_R8, samples: int = 1 << 20,
-                          tol: float = 2e-3, max_iter: int = 200) -> np.ndarray:
-    """Router bias that gives the target depth histogram under a Gaussian input model.
+# Moments of x * sigmoid(x) for x ~ N(0, 1) (numerical quadrature), used to
+# model the MLP router's hidden units as i.i.d. with this mean and variance.
+SILU_GAUSS_MEAN = 0.2066209641
+SILU_GAUSS_VAR = 0.3130832970
 
-    The embedding rows are i.i.d. N(0, std^2), so the router's input ``E[x] + P[t]``
-    has i.i.d. N(0, 2 std^2) elements and the bias-free router outputs are jointly
-    Gaussian with covariance ``2 std^2 W W^T``.  The bias is fitted to that model by
-    Monte Carlo (stream ``STREAM_CALIB``) with the update
-    ``b <- b + 0.5 sigma (log q - log p_hat)``, bias[0] held at 0.  The realised
-    histogram on the actual tables is measured, not promised.
-    """
-    R = router_w.shape[0]
+
+def _fit_bias(mean: np.ndarray, cov: np.ndarray, seed: int, target, samples: int,
+              tol: float, max_iter: int) -> np.ndarray:
+    """Bias b such that argmax(z + b), z ~ N(mean, cov), has the target histogram
+    (Monte Carlo on stream STREAM_CALIB, update b <- b + 0.5 sigma (log q - log p_hat),
+    b[0] held at 0)."""
+    R = cov.shape[0]
     if len(target) != R:
         raise ValueError("depth target length must equal max_loops")
-    w = router_w.astype(np.float64)
-    cov = 2.0 * cfg.std ** 2 * (w @ w.T)
     L = np.linalg.cholesky(cov + 1e-18 * np.eye(R))
     g = normal(seed, STREAM_CALIB, samples * R).reshape(samples, R)
-    z0 = g @ L.T
+    z0 = g @ L.T + mean
     sigma = float(np.sqrt(np.mean(np.diag(cov))))
     q = np.asarray(target, dtype=np.float64)
     b = np.zeros(R)
@@ -242,6 +241,30 @@ def calibrate_router_bias(router_w: np.ndarray, cfg: ModelConfig, seed: int = SE
     return b.astype(np.float32)
 
 
+def calibrate_router_bias(router_w: np.ndarray, cfg: ModelConfig, seed: int = SEED,
+                          target=DEPTH_TARGET_R8, samples: int = 1 << 20,
+                          tol: float = 2e-3, max_iter: int = 200) -> np.ndarray:
+    """Router bias that gives the target depth histogram under a Gaussian input model.
+
+    Linear router: the embedding rows are i.i.d. N(0, std^2), so the router's input
+    ``E[x] + P[t]`` has i.i.d. N(0, 2 std^2) elements and the bias-free router
+    outputs are jointly Gaussian with covariance ``2 std^2 W W^T``.  MLP router
+    (``router_w`` is then the output layer [R][Hr]): its hidden units are modelled
+    as i.i.d. with the moments of x * sigmoid(x), x ~ N(0, 1) (the hidden layer is
+    scaled so that its pre-activations have unit variance), so the outputs have
+    mean ``SILU_GAUSS_MEAN * W 1`` and covariance ``SILU_GAUSS_VAR * W W^T``.
+    The realised histogram on the actual tables is measured, not promised.
+    """
+    w = router_w.astype(np.float64)
+    if cfg.router_hidden > 0:
+        mean = SILU_GAUSS_MEAN * w.sum(axis=1)
+        cov = SILU_GAUSS_VAR * (w @ w.T)
+    else:
+        mean = np.zeros(w.shape[0])
+        cov = 2.0 * cfg.std ** 2 * (w @ w.T)
+    return _fit_bias(mean, cov, seed, target, samples, tol, max_iter)
+
+
 _WEIGHT_CACHE: Dict[tuple, Dict] = {}
 
 
@@ -251,6 +274,8 @@ def make_weights(cfg: ModelConfig, seed: int = SEED, cache: bool = True) -> Dict
     Layouts (row-major, ``[out][in]`` like a linear layer's weight):
       tok_emb [V][d], pos_emb [max_pos][d], router_w [R][d] (fp32; bf16-rounded
       values for bf16 models), router_b [R] fp32, and per layer j:
+      (with router_hidden = Hr > 0: router_w1 [Hr][d] storage dtype, router_b1 [Hr]
+      fp32, and router_w [R][Hr] is the output layer)
       w_qkv [3d][d] (rows q | k | v, head-major within each), w_o [d][d],
       w_gate_up [2F][d] (rows gate | up), w_down [d][F].
     """
@@ -263,8 +288,18 @@ def make_weights(cfg: ModelConfig, seed: int = SEED, cache: bool = True) -> Dict
     w: Dict = {
         "tok_emb": _mat(seed, STREAM_TOK_EMB, V, d, cfg),
         "pos_emb": _mat(seed, STREAM_POS_EMB, cfg.max_pos, d, cfg),
-        "router_w": _mat(seed, STREAM_ROUTER_W, R, d, cfg).astype(np.float32),
     }
+    Hr = cfg.router_hidden
+    if Hr > 0:
+        # hidden layer scaled for unit-variance pre-activations on inputs with
+        # i.i.d. N(0, 2 std^2) elements; output layer with std 2 / sqrt(Hr)
+        w["router_w1"] = to_storage(normal(seed, STREAM_ROUTER_W1, Hr * d,
+                                           1.0 / (np.sqrt(2.0 * d) * cfg.std)).reshape(Hr, d), cfg.dtype)
+        w["router_b1"] = np.zeros(Hr, dtype=np.float32)
+        w["router_w"] = to_storage(normal(seed, STREAM_ROUTER_W, R * Hr, 2.0 / np.sqrt(Hr)).reshape(R, Hr),
+                                   cfg.dtype).astype(np.float32)
+    else:
+        w["router_w"] = _mat(seed, STREAM_ROUTER_W, R, d, cfg).astype(np.float32)
     layers: List[Dict[str, np.ndarray]] = []
     for j in range(cfg.n_layers):
         s = STREAM_LAYER_BASE + 4 * j

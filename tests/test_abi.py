@@ -72,10 +72,11 @@ def test_size_query_needs_no_device(lib):
 
 
 @pytest.mark.parametrize("field,value", [
-    ("abi_version", 2), ("dtype", 7), ("vocab", 0), ("d_model", 100), ("head_dim", 32),
+    ("abi_version", 1), ("abi_version", 3), ("dtype", 7), ("vocab", 0), ("d_model", 100), ("head_dim", 32),
     ("n_heads", 5), ("d_ff", 1000), ("n_layers", 0), ("n_layers", 9), ("max_loops", 0),
     ("max_loops", 17), ("max_pos", 0), ("max_batch", 0), ("max_batch", 5000), ("page_tokens", 32),
     ("max_pages", 0), ("max_prefill_tokens", 0), ("route_rule", 5), ("rms_eps", 0.0),
+    ("router_hidden", -64), ("router_hidden", 96), ("router_hidden", 8192),
 ])
 def test_invalid_config_rejected(lib, field, value):
     c = _cfg(**{field: value})
@@ -112,6 +113,27 @@ def test_missing_weights_rejected_before_device_work(lib):
     st = lib.tlf_init(ctypes.byref(c), ctypes.byref(w), fake_ws, 1 << 62, ctypes.byref(need), None,
                       ctypes.byref(ctx))
     assert st == tlf.E_INVALID_ARG and not ctx.value
+
+
+def test_mlp_router_weights_must_match_the_config(lib):
+    """router_hidden > 0 needs router_w1/router_b1 and a linear router must not get them;
+    the hidden layer takes workspace."""
+    need = ctypes.c_size_t(0)
+    c0 = _cfg()
+    assert lib.tlf_init(ctypes.byref(c0), None, None, 0, ctypes.byref(need), None, None) == tlf.E_NEED_WORKSPACE
+    lin = need.value
+    c = _cfg(router_hidden=768)
+    assert lib.tlf_init(ctypes.byref(c), None, None, 0, ctypes.byref(need), None, None) == tlf.E_NEED_WORKSPACE
+    assert need.value > lin
+    fake = ctypes.c_void_p(1 << 20)  # never dereferenced: validation fails first
+    lw = (tlf.LayerWeights * c.n_layers)(*[tlf.LayerWeights(fake, fake, fake, fake) for _ in range(c.n_layers)])
+    for hidden, w1 in ((768, None), (0, fake)):
+        cc = _cfg(router_hidden=hidden)
+        w = tlf.Weights(fake, fake, fake, fake, None, cc.n_layers, lw, w1, w1)
+        ctx = ctypes.c_void_p()
+        st = lib.tlf_init(ctypes.byref(cc), ctypes.byref(w), fake, 1 << 62, ctypes.byref(need), None,
+                          ctypes.byref(ctx))
+        assert st == tlf.E_INVALID_ARG and not ctx.value
 
 
 def test_null_context_calls(lib):

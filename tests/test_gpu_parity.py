@@ -149,6 +149,24 @@ def test_f32_wide_heads(head_dim):
     _check_f32(m, w, prompts, g, o, f"f32-D{head_dim}")
 
 
+@pytest.mark.parametrize("rule", ["argmax", "cumprob"])
+def test_f32_mlp_router(rule):
+    """Two-layer MLP router (hidden 64): decisions with a clear margin match the
+    oracle; when none is near a tie, depths, cache indices and logits match at
+    the fp32 bar."""
+    m = _f32_small(router_hidden=64, router_bias="calibrated", steps=10)
+    w = synth.make_weights(m)
+    prompts = synth.make_prompts(m)
+    g = parity.run_gpu(m, w, prompts, m.steps, route_rule=rule, threshold=0.5)
+    o = parity.run_oracle(m, w, prompts, g.step_tokens, route_rule=rule, threshold=0.5)
+    bad, flips = parity.depth_agreement(g.prefill_depths, o.prefill_depths, o.prefill_margin, 1e-5)
+    _report(f"mlp-router-{rule}", flips=flips, hist=g.stats["depth_hist"])
+    assert bad == 0
+    assert len(set(g.prefill_depths.ravel().tolist())) >= 2
+    if flips == 0:
+        _check_f32(m, w, prompts, g, o, f"mlp-router-{rule}")
+
+
 def test_prefill_in_sequence_groups_is_identical():
     m = _f32_small(batch=5, prompt_len=40, steps=3)
     w = synth.make_weights(m)
@@ -194,15 +212,17 @@ def test_graph_replays_match_eager_launches(name):
             assert np.array_equal(g.stats["index"][b][i], e.stats["index"][b][i])
 
 
-def _check_bf16(m, w, prompts, g, o, sample, tag, route_rule="argmax", fixed_depth=None):
+def _check_bf16(m, w, prompts, g, o, sample, tag, route_rule="argmax", fixed_depth=None, threshold=0.5):
     B, T = prompts.shape
     # router decisions of every token against the oracle router
     pos = np.broadcast_to(np.arange(T), (B, T))
-    od, om = parity.router_decisions(m, w, prompts.ravel(), pos.ravel(), route_rule, fixed_depth=fixed_depth)
+    od, om = parity.router_decisions(m, w, prompts.ravel(), pos.ravel(), route_rule, threshold=threshold,
+                                     fixed_depth=fixed_depth)
     bad, flips = parity.depth_agreement(g.prefill_depths.ravel(), od, om, BF16_MARGIN)
     nbad, nflips = 0, []
     for s, tok in enumerate(g.step_tokens):
-        sd, sm = parity.router_decisions(m, w, tok, np.full(B, T + s), route_rule, fixed_depth=fixed_depth)
+        sd, sm = parity.router_decisions(m, w, tok, np.full(B, T + s), route_rule, threshold=threshold,
+                                         fixed_depth=fixed_depth)
         b2, f2 = parity.depth_agreement(g.step_depths[s], sd, sm, BF16_MARGIN)
         nbad += b2
         nflips.append(f2)
@@ -247,6 +267,21 @@ def test_bf16_fixed_depth_ragged_prompt():
                           fixed_depth=8)
     assert np.all(g.prefill_depths == 8)
     _check_bf16(m, w, prompts, g, o, sample, "bf16-fixed8", route_rule="fixed", fixed_depth=8)
+
+
+@pytest.mark.parametrize("rule,threshold", [("argmax", 0.5), ("cumprob", 0.6)])
+def test_bf16_mlp_router(rule, threshold):
+    """The 2x768 model with a 768-wide MLP router on a ragged small batch."""
+    full = synth.CONFIGS["bf16_d768_b32x512"].replace(router_hidden=768)
+    m = full.replace(batch=6, prompt_len=70, steps=8)
+    w = synth.make_weights(full)
+    prompts = synth.make_prompts(m)
+    sample = [0, 3, 5]
+    g = parity.run_gpu(m, w, prompts, m.steps, max_pos=m.max_pos, keep_logits_rows=sample, route_rule=rule,
+                       threshold=threshold)
+    o = parity.run_oracle(m, w, prompts[sample], [t[sample] for t in g.step_tokens], route_rule=rule,
+                          threshold=threshold)
+    _check_bf16(m, w, prompts, g, o, sample, f"bf16-mlp-router-{rule}", route_rule=rule, threshold=threshold)
 
 
 @pytest.mark.slow

@@ -105,6 +105,65 @@ def test_silu_closed_form():
     assert O.silu(np.array([1.0]))[0] == pytest.approx(1.0 / (1.0 + math.exp(-1.0)))
 
 
+def _mlp_cfg(**kw):
+    base = dict(max_loops=4, prompt_len=24, router_hidden=32, router_bias="calibrated")
+    base.update(kw)
+    return synth.tiny_config(**base)
+
+
+def test_mlp_router_matches_library_layers():
+    """Two-layer MLP router (Section 3.2) against torch's Linear -> SiLU -> Linear."""
+    cfg = _mlp_cfg()
+    w = synth.make_weights(cfg)
+    toks = synth.make_prompts(cfg)[0]
+    M = _model(cfg, w)
+    h0 = M.E[toks] + M.P[: len(toks)]
+    z = O.router_logits(M, h0)
+    ref = textbook.router_logits(w, h0).numpy().astype(np.float32).astype(np.float64)
+    assert np.max(np.abs(z - ref)) <= 1e-6 * np.max(np.abs(ref))
+    # closed form: with W_1 = 0 every token's hidden layer is silu(b_1)
+    w0 = dict(w)
+    w0["router_w1"] = np.zeros_like(w["router_w1"])
+    w0["router_b1"] = np.linspace(-2.0, 2.0, cfg.router_hidden)
+    b1 = w0["router_b1"]
+    want = (b1 / (1.0 + np.exp(-b1))) @ np.asarray(w["router_w"], np.float64).T + w["router_b"]
+    z0 = O.router_logits(_model(cfg, w0), h0)
+    assert np.max(np.abs(z0 - want[None, :])) < 1e-6
+
+
+def test_mlp_router_depths_and_threshold_monotonicity():
+    """Argmax depths equal the library router's; under the cumulative rule a
+    higher threshold never deepens a token (p^(i) is non-increasing in i)."""
+    cfg = _mlp_cfg(prompt_len=64)
+    w = synth.make_weights(cfg)
+    toks = synth.make_prompts(cfg)[0]
+    M = _model(cfg, w)
+    h0 = M.E[toks] + M.P[: len(toks)]
+    z = O.router_logits(M, h0)
+    m, _ = O.depth_rule(z, O.ARGMAX)
+    assert np.array_equal(m, textbook.routed_argmax_depths(w, toks))
+    prev = None
+    for th in (0.1, 0.3, 0.5, 0.7, 0.9):
+        d, _ = O.depth_rule(z, O.CUMPROB, th)
+        if prev is not None:
+            assert np.all(d <= prev)
+        prev = d
+    assert len(set(O.depth_rule(z, O.CUMPROB, 0.5)[0].tolist())) >= 2
+
+
+def test_mlp_router_prefill_equals_dense_masked_model():
+    """The routed model with an MLP router against the dense masked PyTorch model
+    whose depths come from the library router."""
+    cfg = _mlp_cfg()
+    w = synth.make_weights(cfg)
+    toks = synth.make_prompts(cfg)[0]
+    _, logits, m, _ = O.prefill(_model(cfg, w), toks, all_logits=True)
+    assert np.array_equal(m, textbook.routed_argmax_depths(w, toks))
+    assert len(set(m.tolist())) >= 2
+    ref = textbook.routed_dense_logits(w, toks, m, cfg.n_heads, cfg.head_dim, cfg.rms_eps)
+    assert np.max(np.abs(logits - ref)) < 1e-12
+
+
 # ---------------------------------------------------------------------------
 # Block math against an independent dense PyTorch model
 # ---------------------------------------------------------------------------

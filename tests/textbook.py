@@ -43,11 +43,19 @@ def tied_gpt_logits(weights, tokens, H, D, loops, eps=1e-5):
     return F.linear(_rms(x, eps), head).numpy()
 
 
+def router_logits(weights, h0):
+    """Linear router, or Linear -> SiLU -> Linear when router_w1 is given (float64)."""
+    h = torch.as_tensor(np.asarray(h0, dtype=np.float64))
+    if weights.get("router_w1") is not None:
+        h = F.silu(F.linear(h, _t(weights["router_w1"]), _t(weights["router_b1"])))
+    return F.linear(h, _t(weights["router_w"]), _t(weights["router_b"]))
+
+
 def routed_argmax_depths(weights, tokens):
     """1 + argmax of the float32-rounded router logits of h0 = E[x] + P[t]."""
     tokens = np.asarray(tokens, dtype=np.int64)
     h0 = _t(weights["tok_emb"])[tokens] + _t(weights["pos_emb"])[: len(tokens)]
-    z = F.linear(h0, _t(weights["router_w"]), _t(weights["router_b"])).to(torch.float32)
+    z = router_logits(weights, h0).to(torch.float32)
     return (torch.argmax(z, dim=-1) + 1).numpy()
 
 
