@@ -80,6 +80,7 @@ extern "C" {
 
 /* tlf_prefill flags. */
 #define TLF_PREFILL_ALL_LOGITS 1u /* logits for every position ([B][T][V]) instead of the last */
+#define TLF_PREFILL_APPEND 2u     /* continue the current batch: the tokens are its next positions */
 
 typedef struct tlf_config {
   int32_t abi_version;   /* must be TLF_ABI_VERSION */
@@ -177,11 +178,21 @@ int tlf_init(const tlf_config* cfg, const tlf_weights* w, void* d_workspace, siz
  * the gathered original positions, Eq. 11, and causal attention among the
  * gathered tokens of each loop).  Resets every cache and starts a new batch of
  * `batch` sequences of `seq_len` tokens each.
+ * With TLF_PREFILL_APPEND the call is a later chunk of the current batch's
+ * prompts (chunked prefill; it may also follow decode steps): its tokens take
+ * positions [S, S + seq_len) after the S tokens each sequence holds, loop i
+ * appends the chunk's tokens of depth >= i to cache (b, i) after its existing
+ * entries, and each of them attends over every entry of that cache up to its
+ * own position (Eq. 10).  Prefilling a prompt in chunks gives the results of
+ * one call on the whole prompt.  Requires a batch (TLF_E_STATE otherwise),
+ * the same `batch`, and S + seq_len <= max_pos.
  *   d_tokens: [batch][seq_len] int32 token ids in [0, V).
- *   d_logits: [batch][V] float32 logits of the last position, or
+ *   d_logits: [batch][V] float32 logits of the call's last position, or
  *             [batch][seq_len][V] with TLF_PREFILL_ALL_LOGITS.
  *   d_depths: [batch][seq_len] int32 routed depths, or NULL.
- * Requires 1 <= batch <= max_batch, 1 <= seq_len <= max_pos. */
+ * Requires 1 <= batch <= max_batch, 1 <= seq_len <= max_pos.  Pages for an
+ * appended chunk are taken on the device; running out sets the sticky
+ * TLF_E_OUT_OF_PAGES reported by the next synchronizing call. */
 int tlf_prefill(tlf_ctx* ctx, int32_t batch, int32_t seq_len, const int32_t* d_tokens,
                 float* d_logits, int32_t* d_depths, uint32_t flags);
 

@@ -340,15 +340,24 @@ def greedy(logits: np.ndarray) -> np.ndarray:
 # ---------------------------------------------------------------------------
 
 def prefill(model: Model, tokens: Sequence[int], mode: str = "compact",
-            capacity: int = 0, use_mask: bool = True,
-            all_logits: bool = False) -> Tuple[SeqState, np.ndarray, np.ndarray, np.ndarray]:
+            capacity: int = 0, use_mask: bool = True, all_logits: bool = False,
+            state: Optional[SeqState] = None
+            ) -> Tuple[SeqState, np.ndarray, np.ndarray, np.ndarray]:
     """Prefill of one sequence; returns (state, logits, depths, margins).
 
     logits are for the last position, or [T][V] with ``all_logits``.
 
-    compact mode: loop i gathers rho = sort(A_i) (Eq. 6), runs the block on the
-    gathered rows with causal attention among them, writes k, v at positions
-    rho (Eq. 11), and scatters the rows back (Eq. 7).
+    The T tokens sit at positions t0 .. t0 + T - 1: t0 = 0 and empty caches
+    for a new sequence, or t0 = state.length when ``state`` is continued (a
+    later chunk of the prompt, or tokens after decode steps; ``mode`` and
+    ``use_mask`` are then the state's).
+
+    compact mode: loop i gathers rho = sort(A_i) over the T tokens (Eq. 6),
+    writes their k, v after the entries already in cache i (Eq. 11), and runs
+    the block on the gathered rows; each row attends over the entries of
+    cache i at positions up to its own (Eq. 10): the earlier entries plus
+    causal attention among the gathered rows.  The rows are scattered back
+    (Eq. 7).
     literal mode: the block runs on all T rows every loop; the cache is written
     only for rows in A_i, attention uses causality plus mu^(i), and only rows in
     A_i take the new state.
@@ -357,35 +366,37 @@ def prefill(model: Model, tokens: Sequence[int], mode: str = "compact",
     T = tokens.shape[0]
     if T == 0:
         raise ValueError("empty prompt")
-    if T > model.P.shape[0]:
+    st = state if state is not None else SeqState(model, mode, max(capacity, T), use_mask)
+    t0 = st.length
+    if t0 + T > model.P.shape[0]:
         raise ValueError("prompt longer than the position table")
-    st = SeqState(model, mode, max(capacity, T), use_mask)
-    Hs = model.E[tokens] + model.P[np.arange(T)]
+    pos = t0 + np.arange(T)
+    Hs = model.E[tokens] + model.P[pos]
     m, margin, _ = route(model, Hs)
-    st.depths = [int(x) for x in m]
+    st.depths += [int(x) for x in m]
     for i in range(1, model.R + 1):
-        if mode == "compact":
+        if st.mode == "compact":
             rho = np.flatnonzero(m >= i)
             if rho.size == 0:
                 break
             X = Hs[rho]
-            causal = np.tril(np.ones((rho.size, rho.size), dtype=bool))
+            qpos = pos[rho]
 
-            def attn_fn(j, q, k, v, i=i, rho=rho, causal=causal):
-                st.write(i - 1, j, rho, k, v)
-                return attend(q, k, v, causal)
+            def attn_fn(j, q, k, v, i=i, qpos=qpos):
+                st.write(i - 1, j, qpos, k, v)
+                kp, K, Vv = st.keys(i - 1, j, int(qpos[-1]))
+                return attend(q, K, Vv, kp[None, :] <= qpos[:, None])
 
             Hs[rho] = _layers(model, X, attn_fn)
         else:
             act = m >= i
             if not act.any():
                 break
-            rows = np.arange(T)
 
-            def attn_fn(j, q, k, v, i=i, act=act, rows=rows):
-                st.write(i - 1, j, rows[act], k[act], v[act])
-                kp, K, Vv = st.keys(i - 1, j, T - 1)
-                causal = kp[None, :] <= rows[:, None]
+            def attn_fn(j, q, k, v, i=i, act=act):
+                st.write(i - 1, j, pos[act], k[act], v[act])
+                kp, K, Vv = st.keys(i - 1, j, int(pos[-1]))
+                causal = kp[None, :] <= pos[:, None]
                 # rows outside A_i are computed and then discarded; they skip the
                 # mask only so that none of them is left without any key
                 valid = st.key_mask(i - 1, kp)[None, :] | ~act[:, None]
@@ -393,7 +404,7 @@ def prefill(model: Model, tokens: Sequence[int], mode: str = "compact",
 
             Xn = _layers(model, Hs.copy(), attn_fn)
             Hs[act] = Xn[act]
-    st.length = T
+    st.length = t0 + T
     logits = lm_head(model, Hs if all_logits else Hs[-1:])
     return st, (logits if all_logits else logits[0]), m, margin
 

@@ -18,7 +18,7 @@ int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 // Workspace buffers, in carve order.
 enum Buf {
-  B_POOL, B_POS, B_PAGE_TABLE, B_CACHE_LEN, B_SEQ_LEN, B_SCALARS, B_DEPTH_HIST, B_STEP_STATS,
+  B_POOL, B_POS, B_PAGE_TABLE, B_CACHE_LEN, B_CHUNK_LEN, B_SEQ_LEN, B_SCALARS, B_DEPTH_HIST, B_STEP_STATS,
   B_X_DEC, B_XC_DEC, B_KVSLOT, B_DEPTH_DEC, B_PERM, B_NACT, B_Q_DEC, B_O_DEC, B_ACT_DEC, B_KEYS,
   B_X_PRE, B_Y_PRE, B_DEPTH_PRE, B_TOK_IDX, B_Q_PRE, B_O_PRE, B_ACT_PRE, B_HID,
   B_COUNT
@@ -45,6 +45,7 @@ bool make_layout(const tlf_config& c, Layout* L) {
   sz[B_POS] = (int64_t)c.max_pages * kPage * 4;
   sz[B_PAGE_TABLE] = B * R * L->pages_per_seq * 4;
   sz[B_CACHE_LEN] = B * R * 4;
+  sz[B_CHUNK_LEN] = B * R * 4;
   sz[B_SEQ_LEN] = B * 4;
   sz[B_SCALARS] = 2 * 4;  // page_next, err
   sz[B_DEPTH_HIST] = R * 8;
@@ -244,13 +245,16 @@ int attn_waves(const tlf_ctx* ctx) {
 const void* head_weights(const tlf_ctx* ctx) { return ctx->w.lm_head ? ctx->w.lm_head : ctx->w.tok_emb; }
 
 template <typename T>
-int run_prefill(tlf_ctx* ctx, int B, int T_, const int32_t* tokens, float* logits, int32_t* depths,
+int run_prefill(tlf_ctx* ctx, int B, int T_, int pos0, const int32_t* tokens, float* logits, int32_t* depths,
                 uint32_t flags) {
   const tlf_config& c = ctx->cfg;
   hipStream_t s = ctx->stream;
   const int d = c.d_model, F = c.d_ff, R = c.max_loops;
-  TLF_HIP(launch_fill_i32(ctx->cv.page_next, 0, 1, s));
-  TLF_HIP(launch_fill_u64(ctx->cv.depth_hist, 0ull, R, s));
+  const bool append = (flags & TLF_PREFILL_APPEND) != 0;
+  if (!append) {
+    TLF_HIP(launch_fill_i32(ctx->cv.page_next, 0, 1, s));
+    TLF_HIP(launch_fill_u64(ctx->cv.depth_hist, 0ull, R, s));
+  }
   const int G = std::max(1, ctx->L.pre_rows / T_);
   float* x = ctx->buf<float>(B_X_PRE);
   float* y = ctx->buf<float>(B_Y_PRE);
@@ -260,7 +264,7 @@ int run_prefill(tlf_ctx* ctx, int B, int T_, const int32_t* tokens, float* logit
     EmbedArgs ea;
     ea.tok_emb = ctx->w.tok_emb; ea.pos_emb = ctx->w.pos_emb; ea.Wr = ctx->w.router_w; ea.br = ctx->w.router_b;
     ea.tokens = tokens + (int64_t)b0 * T_;
-    ea.rows = rows; ea.V = c.vocab; ea.d = d; ea.R = R; ea.prefill_T = T_;
+    ea.rows = rows; ea.V = c.vocab; ea.d = d; ea.R = R; ea.prefill_T = T_; ea.pos0 = pos0;
     ea.x = x; ea.y = y; ea.eps = c.rms_eps; ea.depth = ctx->buf<int32_t>(B_DEPTH_PRE);
     ea.out_depth = depths ? depths + (int64_t)b0 * T_ : nullptr;
     ea.rule = c.route_rule; ea.threshold = c.route_threshold; ea.fixed = c.fixed_depth;
@@ -273,17 +277,18 @@ int run_prefill(tlf_ctx* ctx, int B, int T_, const int32_t* tokens, float* logit
     }
 
     PrefillPlanArgs pa;
-    pa.c = ctx->cv; pa.b0 = b0; pa.G = Gc; pa.T = T_;
+    pa.c = ctx->cv; pa.b0 = b0; pa.G = Gc; pa.T = T_; pa.append = append; pa.pos0 = pos0;
     pa.depth = ctx->buf<int32_t>(B_DEPTH_PRE);
     pa.tok_idx = ctx->buf<int32_t>(B_TOK_IDX);
     TLF_HIP(launch_plan_prefill(pa, s));
 
     for (int i = 0; i < R; ++i) {
       // rows: G segments of T compact slots; slot a of segment g is the a-th
-      // token of sequence b0 + g with depth >= i + 1, residual row tok_idx[r]
+      // token of the call in sequence b0 + g with depth >= i + 1 (cache
+      // entry n_old + a), residual row tok_idx[r]
       RowMap rm;
       rm.src = ctx->buf<int32_t>(B_TOK_IDX) + (int64_t)i * rows;
-      rm.seg_cnt = ctx->cv.cache_len + (int64_t)b0 * R + i;
+      rm.seg_cnt = ctx->cv.chunk_len + (int64_t)b0 * R + i;
       rm.seg = T_; rm.seg_cnt_stride = R; rm.rows = rows;
       ResidNormArgs rn;
       rn.rm = rm; rn.x = x; rn.y = y; rn.d = d; rn.eps = c.rms_eps;
@@ -473,6 +478,7 @@ int tlf_init(const tlf_config* cfg, const tlf_weights* w, void* d_workspace, siz
   cv.page_table = ctx->buf<int32_t>(B_PAGE_TABLE);
   cv.cache_len = ctx->buf<int32_t>(B_CACHE_LEN);
   cv.seq_len = ctx->buf<int32_t>(B_SEQ_LEN);
+  cv.chunk_len = ctx->buf<int32_t>(B_CHUNK_LEN);
   cv.page_next = ctx->buf<int32_t>(B_SCALARS);
   cv.err = ctx->buf<int32_t>(B_SCALARS) + 1;
   cv.depth_hist = ctx->buf<unsigned long long>(B_DEPTH_HIST);
@@ -508,6 +514,7 @@ int tlf_init(const tlf_config* cfg, const tlf_weights* w, void* d_workspace, siz
   if (e == hipSuccess) e = launch_fill_i32(cv.pos, -1, (int64_t)cfg->max_pages * kPage, s);
   if (e == hipSuccess) e = launch_fill_i32(cv.page_table, -1, (int64_t)(L.size[B_PAGE_TABLE] / 4), s);
   if (e == hipSuccess) e = launch_fill_i32(cv.cache_len, 0, (int64_t)cfg->max_batch * cfg->max_loops, s);
+  if (e == hipSuccess) e = launch_fill_i32(cv.chunk_len, 0, (int64_t)cfg->max_batch * cfg->max_loops, s);
   if (e == hipSuccess) e = launch_fill_i32(cv.seq_len, 0, cfg->max_batch, s);
   if (e == hipSuccess) e = launch_fill_i32(cv.page_next, 0, 2, s);
   if (e == hipSuccess) e = launch_fill_u64(cv.depth_hist, 0ull, cfg->max_loops, s);
@@ -523,15 +530,24 @@ int tlf_prefill(tlf_ctx* ctx, int32_t batch, int32_t seq_len, const int32_t* d_t
   if (st != TLF_OK) return st;
   const tlf_config& c = ctx->cfg;
   if (batch < 1 || batch > c.max_batch || seq_len < 1 || seq_len > c.max_pos) return TLF_E_INVALID_ARG;
-  if (!d_tokens || !d_logits || (flags & ~TLF_PREFILL_ALL_LOGITS)) return TLF_E_INVALID_ARG;
-  // loop 1 alone needs one page per 16 tokens of every sequence
-  if ((int64_t)batch * ceil_div(seq_len, kPage) > c.max_pages) return TLF_E_OUT_OF_PAGES;
-  ctx->prefilled = false;
-  st = c.dtype == TLF_DTYPE_BF16 ? run_prefill<bf16>(ctx, batch, seq_len, d_tokens, d_logits, d_depths, flags)
-                                 : run_prefill<float>(ctx, batch, seq_len, d_tokens, d_logits, d_depths, flags);
+  if (!d_tokens || !d_logits || (flags & ~(TLF_PREFILL_ALL_LOGITS | TLF_PREFILL_APPEND))) return TLF_E_INVALID_ARG;
+  const bool append = (flags & TLF_PREFILL_APPEND) != 0;
+  int pos0 = 0;
+  if (append) {
+    if (!ctx->prefilled) return TLF_E_STATE;
+    if (batch != ctx->batch || seq_len > c.max_pos - ctx->seq_len) return TLF_E_INVALID_ARG;
+    pos0 = ctx->seq_len;
+  } else {
+    // loop 1 alone needs one page per 16 tokens of every sequence
+    if ((int64_t)batch * ceil_div(seq_len, kPage) > c.max_pages) return TLF_E_OUT_OF_PAGES;
+    ctx->prefilled = false;
+  }
+  st = c.dtype == TLF_DTYPE_BF16
+           ? run_prefill<bf16>(ctx, batch, seq_len, pos0, d_tokens, d_logits, d_depths, flags)
+           : run_prefill<float>(ctx, batch, seq_len, pos0, d_tokens, d_logits, d_depths, flags);
   if (st != TLF_OK) return st;
   ctx->batch = batch;
-  ctx->seq_len = seq_len;
+  ctx->seq_len = pos0 + seq_len;
   ctx->prefilled = true;
   return TLF_OK;
 }

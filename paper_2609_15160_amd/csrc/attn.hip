@@ -256,9 +256,13 @@ __global__ __launch_bounds__(256) void k_attn_prefill(AttnPrefillArgs a) {
   const int QT = (a.T + BQ - 1) / BQ;
   const int g = blockIdx.x / QT, qt = blockIdx.x % QT, h = blockIdx.y;
   const int b = a.b0 + g;
+  // the call's nq queries are cache entries [n - nq, n) of (b, loop): query
+  // row a (compact index n0 + a) sees keys [0, n0 + a]
   const int n = c.cache_len[b * c.R + a.loop];
+  const int nq = c.chunk_len[b * c.R + a.loop];
+  const int n0 = n - nq;
   const int q0 = qt * BQ;
-  if (q0 >= n) return;
+  if (q0 >= nq) return;
   const int32_t* pt = c.page_table + ((int64_t)b * c.R + a.loop) * c.pages_per_seq;
   const T* pool = reinterpret_cast<const T*>(c.pool);
   const int64_t koff = k_block(c, a.layer, h), voff = v_block(c, a.layer, h);
@@ -269,7 +273,7 @@ __global__ __launch_bounds__(256) void k_attn_prefill(AttnPrefillArgs a) {
   constexpr int NQ = EPL == 8 ? 2 : 1;
   typename M::frag qf[NQ][D / KS];
   {
-    const int qrow = min(q0 + w * 16 + c16, n - 1);
+    const int qrow = min(q0 + w * 16 + c16, nq - 1);
     const float* qp = a.q + ((int64_t)g * a.T + qrow) * a.d + h * D + quad * EPL;
 #pragma unroll
     for (int ks = 0; ks < D / KS; ++ks) {
@@ -284,7 +288,7 @@ __global__ __launch_bounds__(256) void k_attn_prefill(AttnPrefillArgs a) {
 #pragma unroll
   for (int r = 0; r < 4; ++r) { mrow[r] = kNegInf; lrow[r] = 0.f; }
 
-  const int nkt = min(qt + 1, (n + BKEY - 1) / BKEY);
+  const int nkt = min((n0 + q0 + BQ + BKEY - 1) / BKEY, (n + BKEY - 1) / BKEY);
   for (int kt = 0; kt < nkt; ++kt) {
     __syncthreads();
     // K rows: key-major, 16-byte pieces
@@ -332,7 +336,7 @@ __global__ __launch_bounds__(256) void k_attn_prefill(AttnPrefillArgs a) {
     float alpha[4];
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const int row = q0 + w * 16 + quad * 4 + r;
+      const int row = n0 + q0 + w * 16 + quad * 4 + r;
       float mx = kNegInf;
 #pragma unroll
       for (int nt = 0; nt < 4; ++nt) {
@@ -380,7 +384,7 @@ __global__ __launch_bounds__(256) void k_attn_prefill(AttnPrefillArgs a) {
 #pragma unroll
     for (int off = 1; off < 16; off <<= 1) lt += shfl_xor(lt, off);
     const int row = q0 + w * 16 + quad * 4 + r;
-    if (row >= n) continue;
+    if (row >= nq) continue;
     float* op = a.o + ((int64_t)g * a.T + row) * a.d + h * D;
     const float inv = 1.f / lt;
 #pragma unroll

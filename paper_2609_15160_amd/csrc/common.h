@@ -40,6 +40,7 @@ struct CacheView {
   int32_t* page_table;    // [max_batch][R][pages_per_seq] physical page of (b, i, p)
   int32_t* cache_len;     // [max_batch][R] entries n_{b,i}
   int32_t* seq_len;       // [max_batch] tokens of sequence b so far
+  int32_t* chunk_len;     // [max_batch][R] entries of (b, i) appended by the latest prefill call
   int32_t* page_next;     // [1] bump allocator: pages in use
   int32_t* err;           // [1] sticky error bits
   unsigned long long* depth_hist; // [R]

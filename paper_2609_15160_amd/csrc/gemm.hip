@@ -35,7 +35,8 @@ __device__ __forceinline__ int64_t kv_slot_base(const KvDst& kv, int r, int src)
   int b, slot;
   if (kv.prefill) {
     b = kv.b0 + r / kv.seg;
-    slot = r % kv.seg;
+    const int bi = b * c.R + kv.loop;
+    slot = c.cache_len[bi] - c.chunk_len[bi] + r % kv.seg;
   } else {
     b = src;
     slot = c.cache_len[b * c.R + kv.loop] - 1;

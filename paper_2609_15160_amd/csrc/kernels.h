@@ -38,7 +38,8 @@ struct KvDst {
   CacheView c;
   int loop = 0, layer = 0;
   int prefill = 0;  // 0: decode, slot = cache_len[b][i] - 1 with b = residual row;
-                    // 1: prefill, b = b0 + r / seg, slot = r % seg
+                    // 1: prefill, b = b0 + r / seg,
+                    //    slot = cache_len[b][i] - chunk_len[b][i] + r % seg
   int b0 = 0, seg = 0;
   const int64_t* slot_base = nullptr;  // decode projections: the planner's slot offset of
                                        // compact row r at this loop (kv_slot + loop * B)
@@ -98,7 +99,8 @@ struct EmbedArgs {
   const float* br = nullptr;
   const int32_t* tokens = nullptr;
   int rows = 0, V = 0, d = 0, R = 0;
-  int prefill_T = 0;              // > 0: pos = row % T; 0: pos = seq_len[row]
+  int prefill_T = 0;              // > 0: pos = pos0 + row % T; 0: pos = seq_len[row]
+  int pos0 = 0;
   const int32_t* seq_len = nullptr;
   float* x = nullptr;             // [rows][d] float residual
   float* y = nullptr;             // [rows][d] RMSNorm(x), or nullptr
@@ -160,6 +162,8 @@ hipError_t launch_plan_decode(const DecodePlanArgs& a, hipStream_t s);
 struct PrefillPlanArgs {
   CacheView c;
   int b0 = 0, G = 0, T = 0;
+  int append = 0;  // 1: continue every (b, i) cache after its cache_len entries; 0: start it empty
+  int pos0 = 0;    // position of the first token of the call
   const int32_t* depth = nullptr;  // [G][T]
   int32_t* tok_idx = nullptr;      // [R][G*T]
 };

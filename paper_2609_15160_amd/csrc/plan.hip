@@ -191,9 +191,13 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan_decode(DecodePlanArgs a) 
 
 // ---------------------------------------------------------------------------
 // Prefill planner: workgroup g handles sequence b0 + g.  For each loop i it
-// gathers rho^(i) = sort(A_i) (Eq. 6) by a block prefix sum over the flags
-// m_t >= i, allocates ceil(n / 16) pages, and records every slot's original
-// position (Section 3.3 address translation).
+// gathers rho^(i) = sort(A_i) over the call's T tokens (Eq. 6) by a block
+// prefix sum over the flags m_t >= i, and places those n entries in slots
+// [n_old, n_old + n) of cache (b, i): n_old = 0 for a new batch, the current
+// length when the call continues the caches (a later prompt chunk).  The
+// partly filled last page is used first, then ceil-rounded new pages are
+// taken from the pool; every new slot records its original position
+// (Section 3.3 address translation).  chunk_len[b][i] = n.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kPlanThreads) void k_plan_prefill(PrefillPlanArgs a) {
   const CacheView& c = a.c;
@@ -221,7 +225,10 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan_prefill(PrefillPlanArgs a
       __syncthreads();
     }
     const int n = s_carry;
-    const int np = (n + kPage - 1) / kPage;
+    const int bi = b * R + i;
+    const int old = a.append ? c.cache_len[bi] : 0;
+    const int p_old = (old + kPage - 1) / kPage;        // pages already holding entries
+    const int np = (old + n + kPage - 1) / kPage - p_old; // pages to take
     if (tid == 0) {
       int base = np > 0 ? atomicAdd(c.page_next, np) : 0;
       if ((int64_t)base + np > c.max_pages) {
@@ -233,16 +240,28 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan_prefill(PrefillPlanArgs a
     __syncthreads();
     const int base = s_base;
     const int nn = base < 0 ? 0 : n;
-    int32_t* pt = c.page_table + ((int64_t)b * R + i) * c.pages_per_seq;
+    int32_t* pt = c.page_table + (int64_t)bi * c.pages_per_seq;
     if (base >= 0) {
-      for (int p = tid; p < np; p += kPlanThreads) pt[p] = base + p;
-      for (int s = tid; s < np * kPage; s += kPlanThreads)
-        c.pos[(int64_t)base * kPage + s] = s < n ? idx[s] - g * T : -1;
+      for (int p = tid; p < np; p += kPlanThreads) pt[p_old + p] = base + p;
+      // tail of the partly filled page
+      const int tail = p_old * kPage - old;
+      if (tid < tail && tid < n) {
+        const int s = old + tid;
+        c.pos[(int64_t)pt[s / kPage] * kPage + s % kPage] = a.pos0 + idx[tid] - g * T;
+      }
+      // whole new pages; slots past the last entry are marked empty
+      for (int s = tid; s < np * kPage; s += kPlanThreads) {
+        const int e = p_old * kPage + s - old;  // entry index within the call
+        c.pos[(int64_t)base * kPage + s] = e < n ? a.pos0 + idx[e] - g * T : -1;
+      }
     }
-    if (tid == 0) c.cache_len[b * R + i] = nn;
+    if (tid == 0) {
+      c.cache_len[bi] = old + nn;
+      c.chunk_len[bi] = nn;
+    }
     __syncthreads();
   }
-  if (tid == 0) c.seq_len[b] = T;
+  if (tid == 0) c.seq_len[b] = a.pos0 + T;
   if (tid < R) atomicAdd(&c.depth_hist[tid], hist[tid]);
 }
 

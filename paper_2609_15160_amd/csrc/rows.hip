@@ -106,7 +106,7 @@ __global__ __launch_bounds__(256) void k_embed_route(EmbedArgs a) {
     if (lane == 0) set_err(a.err, kErrBadToken);
     tok = 0;
   }
-  const int pos = a.prefill_T > 0 ? row % a.prefill_T : a.seq_len[row];
+  const int pos = a.prefill_T > 0 ? a.pos0 + row % a.prefill_T : a.seq_len[row];
   const T* e = reinterpret_cast<const T*>(a.tok_emb) + (int64_t)tok * a.d;
   const T* p = reinterpret_cast<const T*>(a.pos_emb) + (int64_t)pos * a.d;
   float* x = a.x + (int64_t)row * a.d;

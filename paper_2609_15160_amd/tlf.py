@@ -32,6 +32,7 @@ DTYPE_F32 = 0
 DTYPE_BF16 = 1
 ROUTE = {"argmax": 0, "cumprob": 1, "fixed": 2}
 PREFILL_ALL_LOGITS = 1
+PREFILL_APPEND = 2
 PROFILE_OFF = 0
 PROFILE_ATTN = 1
 PROFILE_BLOCK = 2
@@ -225,19 +226,22 @@ class Session:
         if st != OK:
             raise TlfError(st, where)
 
-    def prefill(self, tokens, all_logits: bool = False, want_depths: bool = True):
-        """tokens: int32 [B][T] device tensor.  Returns (logits, depths)."""
+    def prefill(self, tokens, all_logits: bool = False, want_depths: bool = True, append: bool = False):
+        """tokens: int32 [B][T] device tensor.  Returns (logits, depths).
+
+        append=True continues the current batch (a later prompt chunk, or
+        tokens after decode steps) instead of starting a new one."""
         torch = self.torch
         B, T = tokens.shape
         tokens = tokens.to(self.device, torch.int32).contiguous()
         V = self.model.vocab
         logits = torch.empty((B, T, V) if all_logits else (B, V), dtype=torch.float32, device=self.device)
         depths = torch.empty((B, T), dtype=torch.int32, device=self.device) if want_depths else None
+        flags = (PREFILL_ALL_LOGITS if all_logits else 0) | (PREFILL_APPEND if append else 0)
         st = self.lib.tlf_prefill(self.ctx, B, T, tokens.data_ptr(), logits.data_ptr(),
-                                  depths.data_ptr() if depths is not None else None,
-                                  PREFILL_ALL_LOGITS if all_logits else 0)
+                                  depths.data_ptr() if depths is not None else None, flags)
         self._check(st, "tlf_prefill")
-        self.batch, self.seq_len = B, T
+        self.batch, self.seq_len = B, (self.seq_len + T if append else T)
         return logits, depths
 
     def decode_into(self, tokens, logits, next_tok=None, depths=None, margin=None) -> None:

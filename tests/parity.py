@@ -61,6 +61,52 @@ def run_gpu(model: synth.ModelConfig, weights: Dict, prompts: np.ndarray, steps:
 
 
 @dataclasses.dataclass
+class ScheduleRun:
+    logits: np.ndarray      # [B][L][V] logits of every position
+    depths: np.ndarray      # [B][L]
+    stats: Dict
+
+
+def run_gpu_schedule(model: synth.ModelConfig, weights: Dict, tokens: np.ndarray, schedule,
+                     route_rule: str = "argmax", threshold: float = 0.5, fixed_depth: int = 1,
+                     max_prefill_tokens: int = 65536, decode_graph: bool = True) -> ScheduleRun:
+    """Feeds the columns of tokens [B][L] left to right as the schedule says:
+    ("prefill", n) prefills the next n tokens (the first item starts the batch,
+    later ones append chunks to it) and ("decode", n) runs n decode steps, each
+    fed the next column (teacher forcing)."""
+    import torch
+    from paper_2609_15160_amd import tlf
+    B, L = tokens.shape
+    sess = tlf.Session(model, weights, max_batch=B, max_pos=L, route_rule=route_rule, threshold=threshold,
+                       fixed_depth=fixed_depth, max_prefill_tokens=max_prefill_tokens,
+                       decode_graph=decode_graph)
+    try:
+        toks = torch.from_numpy(tokens.astype(np.int32)).cuda()
+        logits = np.zeros((B, L, model.vocab), np.float32)
+        depths = np.zeros((B, L), np.int32)
+        t = 0
+        for k, (kind, n) in enumerate(schedule):
+            if kind == "prefill":
+                lg, dep = sess.prefill(toks[:, t:t + n], all_logits=True, append=k > 0)
+                logits[:, t:t + n] = lg.cpu().numpy()
+                depths[:, t:t + n] = dep.cpu().numpy()
+                t += n
+            else:
+                for _ in range(n):
+                    lg, _, dep, _ = sess.decode(toks[:, t])
+                    logits[:, t] = lg.cpu().numpy()
+                    depths[:, t] = dep.cpu().numpy()
+                    t += 1
+        if t != L:
+            raise ValueError("the schedule does not cover the tokens")
+        stats = sess.stats(with_index=True)
+        torch.cuda.synchronize()
+        return ScheduleRun(logits, depths, stats)
+    finally:
+        sess.close()
+
+
+@dataclasses.dataclass
 class OracleRun:
     prefill_logits: np.ndarray
     prefill_depths: np.ndarray

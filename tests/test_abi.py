@@ -162,6 +162,7 @@ def test_binding_constants_match_the_header():
              "DTYPE_F32": tlf.DTYPE_F32, "DTYPE_BF16": tlf.DTYPE_BF16,
              "ROUTE_ARGMAX": tlf.ROUTE["argmax"], "ROUTE_CUMPROB": tlf.ROUTE["cumprob"],
              "ROUTE_FIXED": tlf.ROUTE["fixed"], "PREFILL_ALL_LOGITS": tlf.PREFILL_ALL_LOGITS,
+             "PREFILL_APPEND": tlf.PREFILL_APPEND,
              "PROFILE_OFF": tlf.PROFILE_OFF, "PROFILE_ATTN": tlf.PROFILE_ATTN,
              "PROFILE_BLOCK": tlf.PROFILE_BLOCK}
     for name, value in pairs.items():

@@ -323,6 +323,81 @@ def test_bf16_d2048_b64x4096_sampled_sequences():
 
 
 # ---------------------------------------------------------------------------
+# Chunked prefill: prompt chunks appended to the caches, mixed with decode steps
+# ---------------------------------------------------------------------------
+
+# chunk sizes off the 16-token pages and the 64-row tiles; a chunk of one token;
+# decode steps between chunks (a graph captured before a chunk replays after it)
+SCHEDULE = [("prefill", 37), ("prefill", 1), ("prefill", 70), ("prefill", 12), ("decode", 5),
+            ("prefill", 9), ("decode", 3)]
+
+
+def _schedule_len(schedule):
+    return sum(n for _, n in schedule)
+
+
+def _oracle_one_shot(m, w, tokens, **kw):
+    return parity.run_oracle(m, w, tokens, [], all_logits=True, **kw)
+
+
+@pytest.mark.parametrize("head_dim", [16, 64])
+def test_f32_chunked_prefill_equals_one_shot(head_dim):
+    """Every position's logits and depth from a schedule of appended chunks and
+    decode steps equal one oracle prefill over the whole token sequence."""
+    L = _schedule_len(SCHEDULE)
+    m = _f32_small(batch=3, prompt_len=L, steps=0)
+    if head_dim == 64:
+        m = m.replace(n_heads=2, head_dim=64, d_model=128)
+    w = synth.make_weights(m)
+    tokens = synth.make_prompts(m, prompt_len=L)
+    g = parity.run_gpu_schedule(m, w, tokens, SCHEDULE)
+    o = _oracle_one_shot(m, w, tokens)
+    assert np.array_equal(g.depths, o.prefill_depths)
+    for b in range(tokens.shape[0]):
+        for i in range(m.max_loops):
+            assert np.array_equal(g.stats["index"][b][i], o.index[b][i]), (b, i)
+    err = _max_err(g.logits, o.prefill_logits)
+    _report(f"f32-chunked-D{head_dim}", max_abs_logit_err=f"{err:.3g}", depth_hist=g.stats["depth_hist"])
+    assert err <= F32_TOL
+
+
+def test_f32_chunked_prefill_in_sequence_groups():
+    """Appended chunks that run in sequence groups (small activation budget)."""
+    sched = [("prefill", 40), ("prefill", 23), ("decode", 2), ("prefill", 17)]
+    L = _schedule_len(sched)
+    m = _f32_small(batch=5, prompt_len=L, steps=0)
+    w = synth.make_weights(m)
+    tokens = synth.make_prompts(m, prompt_len=L)
+    g = parity.run_gpu_schedule(m, w, tokens, sched, max_prefill_tokens=2 * L)
+    o = _oracle_one_shot(m, w, tokens)
+    assert np.array_equal(g.depths, o.prefill_depths)
+    err = _max_err(g.logits, o.prefill_logits)
+    _report("f32-chunked-groups", max_abs_logit_err=f"{err:.3g}")
+    assert err <= F32_TOL
+
+
+def test_bf16_chunked_prefill_equals_one_shot():
+    m = synth.CONFIGS["bf16_d768_b32x512"].replace(batch=3)
+    w = synth.make_weights(synth.CONFIGS["bf16_d768_b32x512"])
+    sched = [("prefill", 100), ("prefill", 29), ("prefill", 200), ("decode", 4), ("prefill", 33)]
+    L = _schedule_len(sched)
+    tokens = synth.make_prompts(m, prompt_len=L)
+    g = parity.run_gpu_schedule(m, w, tokens, sched)
+    o = _oracle_one_shot(m, w, tokens)
+    B = tokens.shape[0]
+    pos = np.broadcast_to(np.arange(L), (B, L))
+    od, om = parity.router_decisions(m, w, tokens.ravel(), pos.ravel())
+    bad, flips = parity.depth_agreement(g.depths.ravel(), od, om, BF16_MARGIN)
+    err = _max_err(g.logits, o.prefill_logits)
+    _report("bf16-chunked", max_abs_logit_err=f"{err:.3g}", flip_rate=flips, depth_hist=g.stats["depth_hist"])
+    assert bad == 0
+    for b in range(B):
+        for i in range(m.max_loops):
+            assert np.array_equal(g.stats["index"][b][i], np.flatnonzero(g.depths[b] >= i + 1)), (b, i)
+    assert err <= BF16_TOL
+
+
+# ---------------------------------------------------------------------------
 # Error handling through the C ABI
 # ---------------------------------------------------------------------------
 
@@ -356,6 +431,34 @@ def test_state_errors():
         s.close()
 
 
+def test_append_errors():
+    import torch
+    from paper_2609_15160_amd import tlf
+    m = _f32_small(batch=2, prompt_len=5, steps=4)
+    w = synth.make_weights(m)
+    s = _session(m, w, max_batch=2, max_pos=9)
+    try:
+        z = lambda b, t: torch.zeros((b, t), dtype=torch.int32, device="cuda")
+        with pytest.raises(tlf.TlfError) as e:  # nothing to append to
+            s.prefill(z(2, 3), append=True)
+        assert e.value.status == tlf.E_STATE
+        s.prefill(z(2, 5))
+        with pytest.raises(tlf.TlfError) as e:  # another batch size
+            s.prefill(z(1, 2), append=True)
+        assert e.value.status == tlf.E_INVALID_ARG
+        with pytest.raises(tlf.TlfError) as e:  # 5 + 5 > max_pos
+            s.prefill(z(2, 5), append=True)
+        assert e.value.status == tlf.E_INVALID_ARG
+        s.prefill(z(2, 4), append=True)  # exactly max_pos
+        assert s.seq_len == 9 and s.stats()["seq_len"] == 9
+        with pytest.raises(tlf.TlfError) as e:
+            s.decode(torch.zeros(2, dtype=torch.int32, device="cuda"))
+        assert e.value.status == tlf.E_STATE
+        assert s.stats()["status"] == tlf.OK
+    finally:
+        s.close()
+
+
 def test_out_of_pages_detected():
     import torch
     from paper_2609_15160_amd import tlf
@@ -379,6 +482,22 @@ def test_out_of_pages_detected():
         with pytest.raises(tlf.TlfError) as e:
             s.decode(torch.zeros(1, dtype=torch.int32, device="cuda"))
         assert e.value.status == tlf.E_OUT_OF_PAGES
+    finally:
+        s.close()
+
+
+def test_out_of_pages_on_append_detected():
+    import torch
+    from paper_2609_15160_amd import tlf
+    m = _f32_small(batch=1, prompt_len=16, steps=4, max_loops=2)
+    w = synth.make_weights(m)
+    # the 16-token prompt fills one page per loop; one more token needs two more pages
+    s = _session(m, w, max_batch=1, max_pos=20, max_pages=2, route_rule="fixed", fixed_depth=2)
+    try:
+        s.prefill(torch.zeros((1, 16), dtype=torch.int32, device="cuda"))
+        assert s.stats()["status"] == tlf.OK
+        s.prefill(torch.zeros((1, 1), dtype=torch.int32, device="cuda"), append=True)
+        assert s.stats()["status"] == tlf.E_OUT_OF_PAGES
     finally:
         s.close()
 

@@ -284,6 +284,87 @@ def test_cached_decode_equals_full_recompute():
         assert np.max(np.abs(logits[0, s] - dense[-1])) < 1e-12
 
 
+# ---------------------------------------------------------------------------
+# Chunked prefill: a prompt prefilled in pieces onto the existing caches
+# ---------------------------------------------------------------------------
+
+def _prefill_chunks(M, toks, cuts, **kw):
+    st, logits, depths = None, [], []
+    for a, b in zip((0,) + tuple(cuts), tuple(cuts) + (len(toks),)):
+        st, lg, m, _ = O.prefill(M, toks[a:b], all_logits=True, state=st, **kw)
+        logits.append(lg)
+        depths.append(m)
+    return st, np.concatenate(logits), np.concatenate(depths)
+
+
+@pytest.mark.parametrize("cuts", [(5,), (1, 2, 17), (16, 32), (7, 8, 9, 10)])
+def test_chunked_prefill_equals_dense_masked_model(cuts):
+    """A prompt prefilled in chunks gives every position the logits of the
+    independent dense masked model, the library-argmax depths, and caches that
+    hold exactly the positions of depth >= i."""
+    cfg = synth.tiny_config(max_loops=4, prompt_len=40)
+    w = synth.make_weights(cfg, seed=5)
+    toks = synth.make_prompts(cfg, seed=5)[0]
+    M = _model(cfg, w)
+    st, logits, m = _prefill_chunks(M, toks, cuts)
+    assert len(set(m.tolist())) >= 3
+    assert np.array_equal(m, textbook.routed_argmax_depths(w, toks))
+    ref = textbook.routed_dense_logits(w, toks, m, cfg.n_heads, cfg.head_dim, cfg.rms_eps)
+    assert np.max(np.abs(logits - ref)) < 1e-12
+    idx = O.cache_index(st, M.R)
+    for i in range(M.R):
+        assert np.array_equal(idx[i], np.flatnonzero(m >= i + 1))
+    assert st.length == len(toks) and st.depths == m.tolist()
+
+
+def test_one_token_chunk_equals_decode_step():
+    """A chunk of one token is a decode step (Eq. 9-11): same depth, logits and cache."""
+    cfg = synth.tiny_config(batch=1, prompt_len=12, steps=7, max_loops=4)
+    w = synth.make_weights(cfg, seed=6)
+    toks = synth.make_prompts(cfg, seed=6, prompt_len=19)[0]
+    M = _model(cfg, w)
+    sa, _, _, _ = O.prefill(M, toks[:12])
+    sb, _, _, _ = O.prefill(M, toks[:12])
+    for t in range(12, 19):
+        la, ma, _ = O.decode(M, [sa], [toks[t]])
+        sb, lb, mb, _ = O.prefill(M, toks[t:t + 1], state=sb)
+        assert int(ma[0]) == int(mb[0])
+        assert np.max(np.abs(la[0] - lb)) < 1e-12
+    for i in range(M.R):
+        assert np.array_equal(sa.cache_positions(i), sb.cache_positions(i))
+        n = int(sa.n[i])
+        for j in range(M.J):
+            assert np.max(np.abs(sa.K[i][j][:, :n] - sb.K[i][j][:, :n]), initial=0.0) < 1e-12
+            assert np.max(np.abs(sa.V[i][j][:, :n] - sb.V[i][j][:, :n]), initial=0.0) < 1e-12
+
+
+@pytest.mark.parametrize("mode", ["compact", "literal"])
+def test_chunk_after_decode_steps_equals_one_shot_prefill(mode):
+    """prefill, decode steps, a further chunk, more decode steps: each output
+    equals the matching row of one prefill over the whole token sequence, in
+    both cache representations."""
+    cfg = synth.tiny_config(batch=1, prompt_len=10, steps=16, max_loops=4)
+    w = synth.make_weights(cfg, seed=7)
+    toks = synth.make_prompts(cfg, seed=7, prompt_len=26)[0]
+    M = _model(cfg, w)
+    _, ref, m_ref, _ = O.prefill(M, toks, all_logits=True)
+    st, lg, m, _ = O.prefill(M, toks[:10], mode=mode, capacity=26, all_logits=True)
+    got, depths = [lg], [m]
+    for t in range(10, 13):
+        lg, m, _ = O.decode(M, [st], [toks[t]])
+        got.append(lg)
+        depths.append(m)
+    st, lg, m, _ = O.prefill(M, toks[13:22], all_logits=True, state=st)
+    got.append(lg)
+    depths.append(m)
+    for t in range(22, 26):
+        lg, m, _ = O.decode(M, [st], [toks[t]])
+        got.append(lg)
+        depths.append(m)
+    assert np.array_equal(np.concatenate(depths), m_ref)
+    assert np.max(np.abs(np.concatenate(got) - ref)) < 1e-12
+
+
 def test_cache_holds_exactly_positions_with_depth_at_least_loop():
     cfg = synth.tiny_config(batch=3, prompt_len=20, steps=10, max_loops=4)
     w = synth.make_weights(cfg)
