@@ -11,8 +11,10 @@ O projection, SwiGLU FFN), the LM head and the greedy pick.
 
 Prints one JSON line: decoded tokens/s, the decode attention's achieved HBM
 bandwidth against 8 TB/s (HIP events around every attention launch on the
-library's stream), the same kernels forced to fixed depth R, a prefill
-measurement, and the CPU oracle on a bounded sample.
+library's stream), the same kernels forced to fixed depth R, the same step
+with gather-scatter off, time to first token over prompt lengths, a prefill
+measurement, the MLP-router threshold sweep, and the CPU oracle on a bounded
+sample.
 """
 import argparse
 import json
@@ -152,6 +154,90 @@ def cpu_baseline(model, w, prompts, budget_s, seqs=8):
                       f"prompts (untimed), then {n} batched greedy decode steps timed ({dt:.1f} s)"}
 
 
+def replay_decode_ms(sess, torch, B, V, first_tokens, warmup, steps):
+    """ms of `steps` graph-replayed greedy decode steps after `warmup` untimed ones."""
+    tok = [first_tokens.to(torch.int32).contiguous(), torch.empty(B, dtype=torch.int32, device=sess.device)]
+    out = torch.empty((B, V), dtype=torch.float32, device=sess.device)
+    k = 0
+    for _ in range(warmup):
+        sess.decode_into(tok[k % 2], out, next_tok=tok[(k + 1) % 2])
+        k += 1
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(steps):
+        sess.decode_into(tok[k % 2], out, next_tok=tok[(k + 1) % 2])
+        k += 1
+    e1.record()
+    torch.cuda.synchronize()
+    st = sess.stats()
+    if st["status"] != 0:
+        raise RuntimeError(f"device error {st['status']}")
+    return e0.elapsed_time(e1), st
+
+
+def gather_scatter_off(torch, tlf, model, w, prompts, routed_ms_per_step, warmup=4, steps=30):
+    """The decode workload with gather-scatter off (dense decode): every loop up
+    to the step's deepest token runs all rows, exited rows are discarded at the
+    scatter.  Same outputs; the analogue of the paper's latency ablation."""
+    B, T = prompts.shape
+    sess = tlf.Session(model, w, max_batch=B, max_pos=T + warmup + steps, max_prefill_tokens=65536,
+                       dense_decode=True)
+    try:
+        logits, _ = sess.prefill(torch.from_numpy(prompts).cuda(), want_depths=False)
+        first = torch.argmax(logits, dim=-1)
+        del logits
+        ms, st = replay_decode_ms(sess, torch, B, model.vocab, first, warmup, steps)
+    finally:
+        sess.close()
+        torch.cuda.empty_cache()
+    return {"what": "decode with every loop (up to the step's deepest token) run on all rows of the batch, "
+                    "exited rows computed and discarded; graph-replayed steps",
+            "steps": steps, "ms_per_step": ms / steps, "tokens_per_s": B * steps / (ms / 1e3),
+            "latency_increase": (ms / steps) / routed_ms_per_step - 1.0,
+            "rows_per_loop_last_step": st["last_step_active_rows"]}
+
+
+def ttft_sweep(torch, tlf, model, w, synth, lengths=(128, 512, 1024, 2048), chunk=512, reps=5):
+    """Time to first token of one request (batch 1): a prefill of T tokens that
+    returns the first generated token's logits, for each T; plus the longest
+    prompt prefilled in chunks appended to the caches."""
+    rows = []
+    top = max(lengths)
+    sess = tlf.Session(model, w, max_batch=1, max_pos=top, max_prefill_tokens=top)
+    try:
+        for T in list(lengths) + [("chunked", top)]:
+            chunked = isinstance(T, tuple)
+            n = top if chunked else T
+            toks = torch.from_numpy(synth.make_prompts(model, batch=1, prompt_len=n)).cuda()
+
+            def once():
+                if not chunked:
+                    return sess.prefill(toks, want_depths=False)[0]
+                for a in range(0, n, chunk):
+                    lg, _ = sess.prefill(toks[:, a:a + chunk], want_depths=False, append=a > 0)
+                return lg
+            once()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(reps):
+                lg = once()
+            e1.record()
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1) / reps
+            rows.append({"prompt": n, "chunk": chunk if chunked else n, "ttft_ms": ms})
+            log(f"ttft T={n}{' chunked by ' + str(chunk) if chunked else ''}: {ms:.2f} ms")
+        if sess.stats()["status"] != 0:
+            raise RuntimeError("device error in the TTFT sweep")
+    finally:
+        sess.close()
+        torch.cuda.empty_cache()
+    return {"workload": f"one request, {model.n_layers}-layer d={model.d_model} looped block, R={model.max_loops}, "
+                        f"argmax router; prefill including the first token's logits, mean of {reps} runs",
+            "rows": rows}
+
+
 def threshold_sweep(torch, tlf, synth, name, thresholds=(0.3, 0.4, 0.5, 0.6, 0.7), warmup=4, steps=20):
     """The workload with a two-layer MLP router (hidden width d) and the
     cumulative-probability rule at several thresholds (the analogue of the
@@ -170,26 +256,9 @@ def threshold_sweep(torch, tlf, synth, name, thresholds=(0.3, 0.4, 0.5, 0.6, 0.7
         try:
             toks = torch.from_numpy(prompts).cuda()
             logits, _ = sess.prefill(toks, want_depths=False)
-            tok = [torch.argmax(logits, dim=-1).to(torch.int32).contiguous(),
-                   torch.empty(B, dtype=torch.int32, device="cuda")]
+            first = torch.argmax(logits, dim=-1)
             del logits
-            out = torch.empty((B, m.vocab), dtype=torch.float32, device="cuda")
-            k = 0
-            for _ in range(warmup):
-                sess.decode_into(tok[k % 2], out, next_tok=tok[(k + 1) % 2])
-                k += 1
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            torch.cuda.synchronize()
-            e0.record()
-            for _ in range(steps):
-                sess.decode_into(tok[k % 2], out, next_tok=tok[(k + 1) % 2])
-                k += 1
-            e1.record()
-            torch.cuda.synchronize()
-            ms = e0.elapsed_time(e1)
-            st = sess.stats()
-            if st["status"] != 0:
-                raise RuntimeError(f"device error {st['status']}")
+            ms, st = replay_decode_ms(sess, torch, B, m.vocab, first, warmup, steps)
             hist = np.asarray(st["depth_hist"], dtype=np.float64)
             rows.append({"rule": rule, "threshold": th, "tokens_per_s": B * steps / (ms / 1e3),
                          "ms_per_step": ms / steps,
@@ -327,6 +396,8 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-prefill", action="store_true", help="skip the prefill measurement")
     ap.add_argument("--no-sweep", action="store_true", help="skip the MLP-router threshold sweep")
+    ap.add_argument("--no-ablation", action="store_true", help="skip the gather-scatter-off decode")
+    ap.add_argument("--no-ttft", action="store_true", help="skip the time-to-first-token sweep")
     ap.add_argument("--prefill-only", action="store_true",
                     help="run only the prefill measurement (batch 8 x 4096) and print its JSON")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
@@ -446,6 +517,11 @@ def main():
                               "attn_frac": fgbs / HBM_PEAK_GBS, "prefill_s": fpre,
                               "routed_speedup": fms / ms}
         log(f"fixed depth {model.max_loops}: {fms / args.steps:.3f} ms/step")
+    if not args.no_ablation:
+        out["gather_scatter_off"] = gather_scatter_off(torch, tlf, model, w, prompts, ms / args.steps)
+        log(f"gather-scatter off: {out['gather_scatter_off']['ms_per_step']:.3f} ms/step")
+    if not args.no_ttft:
+        out["ttft"] = ttft_sweep(torch, tlf, model, w, synth)
     if not args.no_prefill:
         out["prefill"] = prefill_measure(torch, tlf, synth, "bf16_d1024_prefill_b8x4096")
         log(f"prefill 8x4096: {out['prefill']['ms']:.2f} ms")

@@ -49,7 +49,7 @@
 extern "C" {
 #endif
 
-#define TLF_ABI_VERSION 2
+#define TLF_ABI_VERSION 3
 #define TLF_MAX_LOOPS 16
 #define TLF_MAX_LAYERS 8
 #define TLF_MAX_BATCH 4096
@@ -106,6 +106,12 @@ typedef struct tlf_config {
                             0: kernels are launched one by one */
   int32_t router_hidden; /* 0: linear router z = W_r h0 + b_r; Hr > 0 (<= 4096, multiple of 64): the
                             two-layer MLP router z = W_r silu(W_1 h0 + b_1) + b_r (Section 3.2) */
+  int32_t dense_decode;  /* 0: each decode loop runs on the gathered active rows (Eq. 6-7);
+                            1: gather-scatter off (the ablation of Section 4's latency study):
+                            every loop up to the step's deepest token runs on all rows of the
+                            batch, exited rows are computed and discarded at the scatter and
+                            write no cache entry, attention keeps the validity mask of Eq. 10.
+                            Same results as 0; prefill is not affected */
 } tlf_config;
 
 /* Weights of layer j of the shared block, row-major [out][in] (y = x W^T),
@@ -146,7 +152,8 @@ typedef struct tlf_cache_stats_t {
   int64_t last_step_kv_write_bytes;
   int64_t last_step_weight_bytes;
   int64_t last_step_loops_executed;       /* #{i : some token of the step has m >= i} */
-  int64_t last_step_active_rows[TLF_MAX_LOOPS]; /* n_i = #{b : m_b >= i} in the last step */
+  int64_t last_step_active_rows[TLF_MAX_LOOPS]; /* rows run at loop i in the last step: n_i = #{b : m_b >= i}
+                                                   (dense_decode: the batch, up to the deepest loop) */
   /* Totals since profiling was last enabled (tlf_set_profiling): */
   int64_t decode_steps;                   /* decode steps enqueued */
   int64_t attn_launches;                  /* decode-attention launches timed */

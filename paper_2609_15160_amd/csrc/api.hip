@@ -107,6 +107,7 @@ int validate_config(const tlf_config* c) {
   if (!(c->rms_eps > 0.f) || !std::isfinite(c->rms_eps)) return TLF_E_INVALID_ARG;
   if (c->decode_graph != 0 && c->decode_graph != 1) return TLF_E_INVALID_ARG;
   if (c->router_hidden < 0 || c->router_hidden > 4096 || c->router_hidden % 64 != 0) return TLF_E_INVALID_ARG;
+  if (c->dense_decode != 0 && c->dense_decode != 1) return TLF_E_INVALID_ARG;
   // the decode attention stages one sequence's page list in LDS
   if (ceil_div(c->max_pos, kPage) > kAttnMaxPages) return TLF_E_INVALID_ARG;
   // the decode projections address weights and activations with 32-bit element offsets
@@ -242,6 +243,10 @@ int attn_waves(const tlf_ctx* ctx) {
   return units * 4 >= slots ? 4 : 8;
 }
 
+// Prefill of a single sequence of at most this many tokens runs its
+// projections on the split-K decode GEMM.
+constexpr int kPrefillFewRows = 2048;
+
 const void* head_weights(const tlf_ctx* ctx) { return ctx->w.lm_head ? ctx->w.lm_head : ctx->w.tok_emb; }
 
 template <typename T>
@@ -261,18 +266,22 @@ int run_prefill(tlf_ctx* ctx, int B, int T_, int pos0, const int32_t* tokens, fl
   for (int b0 = 0; b0 < B; b0 += G) {
     const int Gc = std::min(G, B - b0);
     const int rows = Gc * T_;
+    // one short sequence: too few rows for the 128 x 128 tiles to fill the
+    // device, so the projections take the split-K decode GEMM with the
+    // RMSNorm fused (x is read through the gathered positions, no y)
+    const bool few = Gc == 1 && T_ <= kPrefillFewRows;
     EmbedArgs ea;
     ea.tok_emb = ctx->w.tok_emb; ea.pos_emb = ctx->w.pos_emb; ea.Wr = ctx->w.router_w; ea.br = ctx->w.router_b;
     ea.tokens = tokens + (int64_t)b0 * T_;
     ea.rows = rows; ea.V = c.vocab; ea.d = d; ea.R = R; ea.prefill_T = T_; ea.pos0 = pos0;
-    ea.x = x; ea.y = y; ea.eps = c.rms_eps; ea.depth = ctx->buf<int32_t>(B_DEPTH_PRE);
+    ea.x = x; ea.y = few ? nullptr : y; ea.eps = c.rms_eps; ea.depth = ctx->buf<int32_t>(B_DEPTH_PRE);
     ea.out_depth = depths ? depths + (int64_t)b0 * T_ : nullptr;
     ea.rule = c.route_rule; ea.threshold = c.route_threshold; ea.fixed = c.fixed_depth;
     ea.err = ctx->cv.err;
     ea.route = c.router_hidden == 0;
     TLF_HIP(launch_embed_route<T>(ea, s));
     if (c.router_hidden > 0) {
-      const int st = run_mlp_router<T>(ctx, s, x, rows, false, ea.depth, ea.out_depth, nullptr);
+      const int st = run_mlp_router<T>(ctx, s, x, rows, few, ea.depth, ea.out_depth, nullptr);
       if (st != TLF_OK) return st;
     }
 
@@ -290,15 +299,17 @@ int run_prefill(tlf_ctx* ctx, int B, int T_, int pos0, const int32_t* tokens, fl
       rm.src = ctx->buf<int32_t>(B_TOK_IDX) + (int64_t)i * rows;
       rm.seg_cnt = ctx->cv.chunk_len + (int64_t)b0 * R + i;
       rm.seg = T_; rm.seg_cnt_stride = R; rm.rows = rows;
+      if (few) rm.nact = rm.seg_cnt;  // one segment: rows [0, n) active
       ResidNormArgs rn;
       rn.rm = rm; rn.x = x; rn.y = y; rn.d = d; rn.eps = c.rms_eps;
       for (int j = 0; j < c.n_layers; ++j) {
         const tlf_layer_weights& lw = ctx->layers[j];
         GemmArgs q;
-        q.A = y; q.lda = d; q.W = lw.w_qkv; q.N = 3 * d; q.K = d; q.w_rows = 3 * d; q.rm = rm;
-        q.out = ctx->buf<float>(B_Q_PRE); q.ldo = d; q.d = d;
+        q.A = few ? x : y; q.lda = d; q.W = lw.w_qkv; q.N = 3 * d; q.K = d; q.w_rows = 3 * d; q.rm = rm;
+        q.out = ctx->buf<float>(B_Q_PRE); q.ldo = d; q.d = d; q.eps = c.rms_eps; q.spec = i == 0;
         q.kv.c = ctx->cv; q.kv.loop = i; q.kv.layer = j; q.kv.prefill = 1; q.kv.b0 = b0; q.kv.seg = T_;
-        TLF_HIP(launch_gemm<T>(q, A_SRC, E_QKV, s));
+        if (few) TLF_HIP(launch_dgemm<T>(q, A_SRC, E_QKV, true, ctx->cus, s));
+        else TLF_HIP(launch_gemm<T>(q, A_SRC, E_QKV, s));
 
         AttnPrefillArgs at;
         at.c = ctx->cv; at.loop = i; at.layer = j; at.d = d; at.b0 = b0; at.G = Gc; at.T = T_;
@@ -308,25 +319,34 @@ int run_prefill(tlf_ctx* ctx, int B, int T_, int pos0, const int32_t* tokens, fl
 
         GemmArgs o;
         o.A = ctx->buf<float>(B_O_PRE); o.lda = d; o.W = lw.w_o; o.N = d; o.K = d; o.w_rows = d; o.rm = rm;
-        o.out = x; o.ldo = d;
-        TLF_HIP(launch_gemm<T>(o, A_CMP, E_RESID, s));
-        TLF_HIP(launch_resid_norm<T>(rn, s));
+        o.out = x; o.ldo = d; o.scatter = 1; o.spec = i == 0;
+        if (few) {
+          TLF_HIP(launch_dgemm<T>(o, A_CMP, E_RESID, false, ctx->cus, s));
+        } else {
+          TLF_HIP(launch_gemm<T>(o, A_CMP, E_RESID, s));
+          TLF_HIP(launch_resid_norm<T>(rn, s));
+        }
 
         GemmArgs gu;
-        gu.A = y; gu.lda = d; gu.W = lw.w_gate_up; gu.N = 2 * F; gu.K = d; gu.w_rows = 2 * F; gu.rm = rm;
-        gu.out = ctx->buf<float>(B_ACT_PRE); gu.ldo = F; gu.F = F;
-        TLF_HIP(launch_gemm<T>(gu, A_SRC, E_SWIGLU, s));
+        gu.A = few ? x : y; gu.lda = d; gu.W = lw.w_gate_up; gu.N = 2 * F; gu.K = d; gu.w_rows = 2 * F; gu.rm = rm;
+        gu.out = ctx->buf<float>(B_ACT_PRE); gu.ldo = F; gu.F = F; gu.eps = c.rms_eps; gu.spec = i == 0;
+        if (few) TLF_HIP(launch_dgemm<T>(gu, A_SRC, E_SWIGLU, true, ctx->cus, s));
+        else TLF_HIP(launch_gemm<T>(gu, A_SRC, E_SWIGLU, s));
 
         GemmArgs dn;
         dn.A = ctx->buf<float>(B_ACT_PRE); dn.lda = F; dn.W = lw.w_down; dn.N = d; dn.K = F; dn.w_rows = d;
-        dn.rm = rm; dn.out = x; dn.ldo = d;
-        TLF_HIP(launch_gemm<T>(dn, A_CMP, E_RESID, s));
-        TLF_HIP(launch_resid_norm<T>(rn, s));
+        dn.rm = rm; dn.out = x; dn.ldo = d; dn.scatter = 1; dn.spec = i == 0;
+        if (few) {
+          TLF_HIP(launch_dgemm<T>(dn, A_CMP, E_RESID, false, ctx->cus, s));
+        } else {
+          TLF_HIP(launch_gemm<T>(dn, A_CMP, E_RESID, s));
+          TLF_HIP(launch_resid_norm<T>(rn, s));
+        }
       }
     }
     GemmArgs hd;
-    hd.A = y; hd.lda = d; hd.W = head_weights(ctx); hd.N = c.vocab; hd.K = d; hd.w_rows = c.vocab;
-    hd.out = logits; hd.ldo = c.vocab;
+    hd.A = few ? x : y; hd.lda = d; hd.W = head_weights(ctx); hd.N = c.vocab; hd.K = d; hd.w_rows = c.vocab;
+    hd.out = logits; hd.ldo = c.vocab; hd.eps = c.rms_eps; hd.spec = 1;
     if (flags & TLF_PREFILL_ALL_LOGITS) {
       hd.rm.rows = rows; hd.rm.src_stride = 1; hd.rm.src_off = 0;
       hd.out_row_off = b0 * T_;
@@ -334,7 +354,8 @@ int run_prefill(tlf_ctx* ctx, int B, int T_, int pos0, const int32_t* tokens, fl
       hd.rm.rows = Gc; hd.rm.src_stride = T_; hd.rm.src_off = T_ - 1;
       hd.out_row_off = b0;
     }
-    TLF_HIP(launch_gemm<T>(hd, A_SRC, E_LOGITS, s));
+    if (few) TLF_HIP(launch_dgemm<T>(hd, A_SRC, E_LOGITS, true, ctx->cus, s));
+    else TLF_HIP(launch_gemm<T>(hd, A_SRC, E_LOGITS, s));
   }
   return TLF_OK;
 }
@@ -369,7 +390,11 @@ int run_decode(tlf_ctx* ctx, hipStream_t s, const int32_t* tokens, float* logits
   pa.kv_slot = kv_slot;
   pa.argmax_keys = ctx->buf<unsigned long long>(B_KEYS);
   pa.kv_entry_bytes = (int64_t)c.n_layers * 2 * c.d_model * ctx->L.s;
+  pa.dense = c.dense_decode;
   TLF_HIP(launch_plan_decode(pa, s));
+  // dense decode: rows are in batch order and a row's result is kept while its
+  // token's depth exceeds the loop index
+  const int32_t* keep_depth = c.dense_decode ? ctx->buf<int32_t>(B_DEPTH_DEC) : nullptr;
 
   // the block region (every loop and layer) is timed as a whole when profiling;
   // the attention launches inside it get their own event pairs
@@ -381,7 +406,8 @@ int run_decode(tlf_ctx* ctx, hipStream_t s, const int32_t* tokens, float* logits
   }
   for (int i = 0; i < R; ++i) {
     // rows [0, n_i) of the depth-sorted order are the tokens still active at
-    // loop i; row k is sequence perm[k], its residual xc[k]
+    // loop i; row k is sequence perm[k], its residual xc[k] (dense decode:
+    // every row, perm the identity)
     RowMap rm;
     rm.src = perm; rm.nact = nact + i; rm.rows = B;
     for (int j = 0; j < c.n_layers; ++j) {
@@ -410,7 +436,7 @@ int run_decode(tlf_ctx* ctx, hipStream_t s, const int32_t* tokens, float* logits
 
       GemmArgs o;  // x += o W_o^T
       o.A = ctx->buf<float>(B_O_DEC); o.lda = d; o.W = lw.w_o; o.N = d; o.K = d; o.w_rows = d; o.rm = rm;
-      o.out = xc; o.ldo = d; o.spec = i == 0;
+      o.out = xc; o.ldo = d; o.spec = i == 0; o.keep_depth = keep_depth; o.keep_loop = i;
       TLF_HIP(launch_dgemm<T>(o, A_CMP, E_RESID, false, ctx->cus, s));
 
       GemmArgs gu;  // act = silu(RMSNorm(x) W_g^T) * (RMSNorm(x) W_u^T)
@@ -420,7 +446,7 @@ int run_decode(tlf_ctx* ctx, hipStream_t s, const int32_t* tokens, float* logits
 
       GemmArgs dn;  // x += act W_d^T
       dn.A = ctx->buf<float>(B_ACT_DEC); dn.lda = F; dn.W = lw.w_down; dn.N = d; dn.K = F; dn.w_rows = d;
-      dn.rm = rm; dn.out = xc; dn.ldo = d; dn.spec = i == 0;
+      dn.rm = rm; dn.out = xc; dn.ldo = d; dn.spec = i == 0; dn.keep_depth = keep_depth; dn.keep_loop = i;
       TLF_HIP(launch_dgemm<T>(dn, A_CMP, E_RESID, false, ctx->cus, s));
     }
   }

@@ -228,7 +228,8 @@ __global__ __launch_bounds__(W * 64) void k_attn_decode(AttnDecodeArgs a) {
           O = O * a1 + s_red[ww][2 + dim] * a2;
           Mx = mn;
         }
-        a.o[(int64_t)k * a.d + h * D + dim] = O / Ls;
+        // an empty cache (a discarded row of the dense decode) gives zeros
+        a.o[(int64_t)k * a.d + h * D + dim] = Ls > 0.f ? O / Ls : 0.f;
       }
     }
   }

@@ -51,7 +51,8 @@ struct DgemmShared {
   float* ss;        // [W][BM] partial sums of squares
   float* inv;       // [BM] 1 / rms per row
   int* orow;        // [BM] logits row of each tile row
-  int64_t* kv;      // [BM] cache slot offset of each tile row
+  int64_t* kv;      // [BM] cache slot offset of each tile row (-1: no cache entry)
+  int* keep;        // [BM] E_RESID: the row's result is stored
 };
 
 template <typename T, int RM, int CN, int W, int KB, int AK, int EK, bool NORM>
@@ -112,16 +113,20 @@ __device__ __forceinline__ void dgemm_tile(const GemmArgs& g, int nact, int act_
 #pragma unroll
     for (int i = 0; i < RM; ++i) {
       const int rl = i * 16 + c16, r = min(r0 + rl, g.rm.rows - 1);
-      if constexpr (EK == E_QKV) sh.kv[rl] = g.kv.slot_base[r];
+      if constexpr (EK == E_QKV) sh.kv[rl] = g.kv.prefill ? prefill_kv_slot(g.kv, r) : g.kv.slot_base[r];
+      if constexpr (EK == E_RESID) sh.keep[rl] = !g.keep_depth || g.keep_depth[r] > g.keep_loop;
       if constexpr (EK == E_LOGITS) sh.orow[rl] = g.rm.src ? g.rm.src[r] : g.out_row_off + r;
     }
   }
   float xr[EK == E_RESID ? EPT : 1];
+  int xrow[EK == E_RESID ? EPT : 1];  // residual row of each output (scatter: src(r))
   if constexpr (EK == E_RESID) {
 #pragma unroll
     for (int k = 0; k < EPT; ++k) {
       const int e = tid + k * NT, row = e / BN, n = n0 + e % BN;
-      xr[k] = (e < EOUT && r0 + row < a_rows && n < g.N) ? g.out[(int64_t)(r0 + row) * g.ldo + n] : 0.f;
+      const bool ok = e < EOUT && r0 + row < a_rows && n < g.N;
+      xrow[k] = ok && g.scatter ? row_src(g.rm, r0 + row) : r0 + row;
+      xr[k] = ok ? g.out[(int64_t)xrow[k] * g.ldo + n] : 0.f;
     }
   }
   const float* Ab = g.A;
@@ -306,7 +311,7 @@ __device__ __forceinline__ void dgemm_tile(const GemmArgs& g, int nact, int act_
       if (r0 + row >= row_end || n >= g.N) continue;
       const float v = tile_sum(row, col);
       if constexpr (EK == E_RESID) {
-        g.out[(int64_t)(r0 + row) * g.ldo + n] = xr[k] + v;
+        if (sh.keep[row]) g.out[(int64_t)xrow[k] * g.ldo + n] = xr[k] + v;
       } else if constexpr (EK == E_HIDDEN) {
         const float u = v + g.bias[n];
         g.out[(int64_t)(r0 + row) * g.ldo + n] = u / (1.f + __expf(-u));
@@ -315,6 +320,7 @@ __device__ __forceinline__ void dgemm_tile(const GemmArgs& g, int nact, int act_
           g.out[(int64_t)(r0 + row) * g.ldo + n] = v;
         } else {
           const int64_t base = sh.kv[row];
+          if (base < 0) continue;
           const int slot = (int)(base & (kPage - 1));
           const int64_t page = base - slot;
           const int nn = n - g.d, kvsel = nn / g.d, within = nn % g.d;
@@ -348,7 +354,8 @@ __global__ __launch_bounds__(W * 64) void k_dgemm(GemmArgs g, int wide_above) {
   __shared__ float s_inv[BMX];
   __shared__ int s_orow[EK == E_LOGITS ? BMX : 1];
   __shared__ int64_t s_kv[EK == E_QKV ? BMX : 1];
-  const DgemmShared sh{red, s_ss, s_inv, s_orow, s_kv};
+  __shared__ int s_keep[EK == E_RESID ? BMX : 1];
+  const DgemmShared sh{red, s_ss, s_inv, s_orow, s_kv, s_keep};
   const int nact = g.rm.nact ? *g.rm.nact : g.rm.rows;
   const int act_rows = g.spec ? g.rm.rows : min(nact, g.rm.rows);
   if constexpr (RMn != RMw || CNn != CNw) {
@@ -405,8 +412,14 @@ hipError_t launch_dgemm(const GemmArgs& a, AKind ak, EKind ek, bool norm, int cu
     if (ak == A_SRC) return launch_w<T, 2, 4, 2, 5, 8, 3, A_SRC, E_QKV, true>(a, cus, s);
     return launch_w<T, 2, 4, 2, 5, 8, 3, A_CMP, E_QKV, true>(a, cus, s);
   }
-  if (ak == A_CMP && ek == E_SWIGLU && norm) return launch_w<T, 2, 4, 2, 8, 8, 3, A_CMP, E_SWIGLU, true>(a, cus, s);
-  if (ak == A_CMP && ek == E_LOGITS && norm) return launch_w<T, 2, 4, 2, 4, 8, 3, A_CMP, E_LOGITS, true>(a, cus, s);
+  if (ek == E_SWIGLU && norm) {
+    if (ak == A_SRC) return launch_w<T, 2, 4, 2, 8, 8, 3, A_SRC, E_SWIGLU, true>(a, cus, s);
+    return launch_w<T, 2, 4, 2, 8, 8, 3, A_CMP, E_SWIGLU, true>(a, cus, s);
+  }
+  if (ek == E_LOGITS && norm) {
+    if (ak == A_SRC) return launch_w<T, 2, 4, 2, 4, 8, 3, A_SRC, E_LOGITS, true>(a, cus, s);
+    return launch_w<T, 2, 4, 2, 4, 8, 3, A_CMP, E_LOGITS, true>(a, cus, s);
+  }
   if (ak == A_CMP && ek == E_HIDDEN && !norm) return launch_w<T, 2, 2, 2, 2, 8, 3, A_CMP, E_HIDDEN, false>(a, cus, s);
   if (ak == A_CMP && ek == E_RESID && !norm) {
     if (a.K / Mfma<T>::KS > 3 * 8) return launch_w<T, 1, 2, 1, 3, 16, 4, A_CMP, E_RESID, false>(a, cus, s);

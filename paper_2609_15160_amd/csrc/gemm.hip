@@ -28,24 +28,6 @@ __device__ __forceinline__ unsigned int ordered_bits(float v) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
-// Element offset of the row's page plus its slot in the low 4 bits (the page
-// offset is a multiple of kPage elements), or -1.
-__device__ __forceinline__ int64_t kv_slot_base(const KvDst& kv, int r, int src) {
-  const CacheView& c = kv.c;
-  int b, slot;
-  if (kv.prefill) {
-    b = kv.b0 + r / kv.seg;
-    const int bi = b * c.R + kv.loop;
-    slot = c.cache_len[bi] - c.chunk_len[bi] + r % kv.seg;
-  } else {
-    b = src;
-    slot = c.cache_len[b * c.R + kv.loop] - 1;
-  }
-  const int page = c.page_table[((int64_t)b * c.R + kv.loop) * c.pages_per_seq + slot / kPage];
-  if (page < 0 || page >= c.max_pages) return -1;
-  return (int64_t)page * c.page_elems + (slot % kPage);
-}
-
 template <typename T, int MT, int NT, int PF, int BK, int AK, int EK>
 __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
   constexpr int BM = 2 * MT * 16, BN = 2 * NT * 16;
@@ -149,7 +131,7 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
     if (row_active(g.rm, r)) my_src = row_src(g.rm, r);
     row_src_s[tid] = my_src;
     if constexpr (EK == E_QKV)
-      if (my_src >= 0) my_kv = kv_slot_base(g.kv, r, my_src);
+      if (my_src >= 0) my_kv = prefill_kv_slot(g.kv, r);
   }
   if (!__syncthreads_or(my_src >= 0)) return;
 

@@ -37,7 +37,7 @@ __device__ __forceinline__ int row_src(const RowMap& m, int r) {
 struct KvDst {
   CacheView c;
   int loop = 0, layer = 0;
-  int prefill = 0;  // 0: decode, slot = cache_len[b][i] - 1 with b = residual row;
+  int prefill = 0;  // 0: decode, the slot comes from slot_base;
                     // 1: prefill, b = b0 + r / seg,
                     //    slot = cache_len[b][i] - chunk_len[b][i] + r % seg
   int b0 = 0, seg = 0;
@@ -45,8 +45,23 @@ struct KvDst {
                                        // compact row r at this loop (kv_slot + loop * B)
 };
 
-// A operand: A_SRC reads the normalised residual rows y[src(r)]; A_CMP reads
-// compact rows buf[r] (attention output, SwiGLU activation).  Both are float32.
+// Element offset of the cache slot that prefill row r writes: its page's
+// offset (a multiple of kPage elements) plus the slot in the low 4 bits, or
+// -1 when the page is missing.
+__device__ __forceinline__ int64_t prefill_kv_slot(const KvDst& kv, int r) {
+  const CacheView& c = kv.c;
+  const int b = kv.b0 + r / kv.seg;
+  const int bi = b * c.R + kv.loop;
+  const int slot = c.cache_len[bi] - c.chunk_len[bi] + r % kv.seg;
+  const int page = c.page_table[(int64_t)bi * c.pages_per_seq + slot / kPage];
+  if (page < 0 || page >= c.max_pages) return -1;
+  return (int64_t)page * c.page_elems + (slot % kPage);
+}
+
+// A operand: A_SRC reads rows src(r) of a position-ordered buffer (the
+// normalised residual y, or the residual x itself when the GEMM fuses the
+// norm); A_CMP reads compact rows buf[r] (attention output, SwiGLU
+// activation, the decode residual).  Both are float32.
 enum AKind { A_SRC = 0, A_CMP = 1 };
 // E_QKV: q to a buffer, k and v appended to the loop's cache pages.
 // E_RESID: x[src(r)] += result.  E_SWIGLU: act = silu(gate) * up.
@@ -74,6 +89,9 @@ struct GemmArgs {
   float* a_copy = nullptr;  // decode: the operand rows are also written here, compact (first projection)
   const float* bias = nullptr;  // E_HIDDEN: [N] float32
   int spec = 0;             // decode: every row is active; loads need not wait for the active count
+  int scatter = 0;          // E_RESID: the residual row of row r is src(r) (prefill), not r
+  const int32_t* keep_depth = nullptr;  // E_RESID (dense decode): row r is stored only while
+  int keep_loop = 0;                    // keep_depth[r] > keep_loop (its token runs this loop)
 };
 
 template <typename T>
@@ -82,8 +100,10 @@ hipError_t launch_gemm(const GemmArgs& a, AKind ak, EKind ek, hipStream_t s);
 // workgroup, all loads in flight at once, one writer per output, rows in
 // compact order (E_RESID: out[r] += result; E_LOGITS: logits row src(r)).
 // norm: A is the residual x and the product is taken with RMSNorm(x).
-// Supported: (A_SRC | A_CMP, E_QKV, norm), (A_CMP, E_SWIGLU | E_LOGITS,
-// norm), (A_CMP, E_RESID | E_HIDDEN, no norm).
+// Supported: (A_SRC | A_CMP, E_QKV | E_SWIGLU | E_LOGITS, norm),
+// (A_CMP, E_RESID | E_HIDDEN, no norm).  The prefill rows of one sequence use
+// it too: rows [0, *rm.nact) active, A_SRC through the gathered positions,
+// the residual scattered back (scatter) and the prefill cache slots.
 // cus: compute units of the device (chooses between a narrow and a wide tile shape).
 template <typename T>
 hipError_t launch_dgemm(const GemmArgs& a, AKind ak, EKind ek, bool norm, int cus, hipStream_t s);
@@ -154,6 +174,8 @@ struct DecodePlanArgs {
                                    // slot that compact row k appends at loop i
   unsigned long long* argmax_keys = nullptr; // [B] cleared for the LM head
   int64_t kv_entry_bytes = 0;      // bytes of one (token, loop) cache entry over all layers
+  int dense = 0;                   // 1: rows in batch order, every loop up to the deepest token
+                                   // runs all B rows; exited rows get kv_slot -1
 };
 hipError_t launch_plan_decode(const DecodePlanArgs& a, hipStream_t s);
 

@@ -15,6 +15,10 @@ namespace {
 //   3. per executed (b, i): the slot's position, cache_len += 1, and the
 //      slot's element offset for the QKV epilogue, by compact row;
 //   4. statistics and the greedy keys cleared for the LM head.
+// Dense mode (gather-scatter off): rows stay in batch order and every loop up
+// to the deepest token of the step has all B rows; the rows of exited tokens
+// get kv_slot -1 (no cache entry) and their attention reads the cache as it
+// stands, which the statistics count.
 // Every sequence's cache lengths and page-table entries are loaded together
 // (unrolled over loops), so a step costs a few memory round trips.
 // ---------------------------------------------------------------------------
@@ -32,7 +36,7 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan_decode(DecodePlanArgs a) 
   __shared__ int s_carry, s_total, s_oom;
   __shared__ unsigned long long hist[kMaxLoops];
   __shared__ unsigned long long s_kvread, s_kvwrite;
-  __shared__ int s_maxm;
+  __shared__ int s_maxm, s_top;
 
   if (tid <= kMaxLoops) { cnt[tid] = 0; fill[tid] = 0; }
   if (tid < kMaxLoops) hist[tid] = 0ull;
@@ -50,11 +54,13 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan_decode(DecodePlanArgs a) 
     if (m_of[ch] > 0) atomicAdd(&cnt[m_of[ch]], 1);
   __syncthreads();
   if (tid == 0) {
-    int s = 0;
-    for (int m = R; m >= 1; --m) { start[m] = s; s += cnt[m]; }
-    for (int i = 1; i <= R; ++i) a.nact[i - 1] = start[i] + cnt[i];  // n_i = #{m >= i}
+    int s = 0, top = 0;
+    for (int m = R; m >= 1; --m) { start[m] = s; s += cnt[m]; if (top == 0 && cnt[m] > 0) top = m; }
+    for (int i = 1; i <= R; ++i) a.nact[i - 1] = a.dense ? (i <= top ? B : 0) : start[i] + cnt[i];  // n_i = #{m >= i}
+    s_top = top;
   }
   __syncthreads();
+  const int top = s_top;
 
   // 1. rank of b among the sequences of its depth with smaller b
   const unsigned long long below = (1ull << lane) - 1ull;
@@ -72,9 +78,10 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan_decode(DecodePlanArgs a) 
     if (m > 0) {
       int off = 0;
       for (int w = 0; w < wv; ++w) off += wcnt[w][m];
-      const int row = start[m] + fill[m] + off + rank;
+      const int b = ch * kPlanThreads + tid;
+      const int row = a.dense ? b : start[m] + fill[m] + off + rank;
       row_of[ch] = row;
-      a.perm[row] = ch * kPlanThreads + tid;
+      a.perm[row] = b;
     }
     __syncthreads();
     if (tid >= 1 && tid <= R) {
@@ -122,9 +129,10 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan_decode(DecodePlanArgs a) 
     const int ex = block_exclusive_scan(need_of[ch], scan_tmp, &tot);
     if (m > 0 && !s_oom) {
       int len[kMaxLoops], page[kMaxLoops];
+      const int lim = a.dense ? top : m;  // loops whose cache this row reads
 #pragma unroll
       for (int i = 0; i < kMaxLoops; ++i) {
-        len[i] = i < m ? c.cache_len[b * R + i] : 0;
+        len[i] = i < lim ? c.cache_len[b * R + i] : 0;
         page[i] = -1;
       }
 #pragma unroll
@@ -146,6 +154,9 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan_decode(DecodePlanArgs a) 
           c.cache_len[b * R + i] = slot + 1;
           a.kv_slot[(int64_t)i * B + row_of[ch]] = (int64_t)page[i] * c.page_elems + slot % kPage;
           rd += (unsigned long long)(slot + 1);
+        } else if (i < lim) {  // dense: computed and discarded
+          a.kv_slot[(int64_t)i * B + row_of[ch]] = -1;
+          rd += (unsigned long long)len[i];
         }
       }
       atomicAdd(&s_kvread, rd);
@@ -176,7 +187,8 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan_decode(DecodePlanArgs a) 
       // cache plus one q row and writes one o row per active token; summed
       // over layers: entry bytes times (entries read + active rows)
       unsigned long long rows = 0;
-      for (int i = 0; i < R; ++i) rows += (unsigned long long)(start[i + 1] + cnt[i + 1]);
+      for (int i = 0; i < R; ++i)
+        rows += (unsigned long long)(a.dense ? (i < top ? B : 0) : start[i + 1] + cnt[i + 1]);
       c.step_stats[kStatAttnBytesTotal] += (long long)((s_kvread + rows) * (unsigned long long)a.kv_entry_bytes);
     }
   }

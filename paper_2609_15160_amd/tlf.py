@@ -15,7 +15,7 @@ PKG_DIR = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG_DIR, "libtlf.so")
 HEADER = os.path.join(os.path.dirname(PKG_DIR), "include", "tlf.h")
 
-ABI_VERSION = 2
+ABI_VERSION = 3
 MAX_LOOPS = 16
 MAX_LAYERS = 8
 PAGE_TOKENS = 16
@@ -47,7 +47,7 @@ class Config(ctypes.Structure):
         ("max_pages", ctypes.c_int32), ("max_prefill_tokens", ctypes.c_int32),
         ("route_rule", ctypes.c_int32), ("route_threshold", ctypes.c_float),
         ("fixed_depth", ctypes.c_int32), ("rms_eps", ctypes.c_float), ("decode_graph", ctypes.c_int32),
-        ("router_hidden", ctypes.c_int32),
+        ("router_hidden", ctypes.c_int32), ("dense_decode", ctypes.c_int32),
     ]
 
 
@@ -135,7 +135,7 @@ def status_str(status: int) -> str:
 
 def make_config(model, max_batch: int, max_pos: int, max_pages: int, route_rule: str = "argmax",
                 threshold: float = 0.5, fixed_depth: int = 1, max_prefill_tokens: int = 65536,
-                decode_graph: bool = True) -> Config:
+                decode_graph: bool = True, dense_decode: bool = False) -> Config:
     """Config from a model description with attributes like ``synth.ModelConfig``."""
     return Config(
         abi_version=ABI_VERSION, dtype=DTYPE_BF16 if model.dtype == "bf16" else DTYPE_F32,
@@ -144,7 +144,8 @@ def make_config(model, max_batch: int, max_pos: int, max_pages: int, route_rule:
         max_batch=max_batch, page_tokens=PAGE_TOKENS, max_pages=max_pages,
         max_prefill_tokens=max_prefill_tokens, route_rule=ROUTE[route_rule],
         route_threshold=threshold, fixed_depth=fixed_depth, rms_eps=model.rms_eps,
-        decode_graph=1 if decode_graph else 0, router_hidden=getattr(model, "router_hidden", 0))
+        decode_graph=1 if decode_graph else 0, router_hidden=getattr(model, "router_hidden", 0),
+        dense_decode=1 if dense_decode else 0)
 
 
 def workspace_bytes(cfg: Config) -> int:
@@ -167,7 +168,7 @@ class Session:
     def __init__(self, model, weights: Dict, max_batch: int, max_pos: Optional[int] = None,
                  max_pages: Optional[int] = None, route_rule: str = "argmax", threshold: float = 0.5,
                  fixed_depth: int = 1, max_prefill_tokens: int = 65536, device: str = "cuda",
-                 decode_graph: bool = True):
+                 decode_graph: bool = True, dense_decode: bool = False):
         import torch
         self.torch = torch
         self.lib = load()
@@ -177,7 +178,7 @@ class Session:
         if max_pages is None:
             max_pages = worst_case_pages(max_batch, max_pos, model.max_loops)
         self.cfg = make_config(model, max_batch, max_pos, max_pages, route_rule, threshold,
-                               fixed_depth, max_prefill_tokens, decode_graph)
+                               fixed_depth, max_prefill_tokens, decode_graph, dense_decode)
         sdt = torch.bfloat16 if model.dtype == "bf16" else torch.float32
 
         def dev(a, dt):

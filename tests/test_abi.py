@@ -72,11 +72,12 @@ def test_size_query_needs_no_device(lib):
 
 
 @pytest.mark.parametrize("field,value", [
-    ("abi_version", 1), ("abi_version", 3), ("dtype", 7), ("vocab", 0), ("d_model", 100), ("head_dim", 32),
+    ("abi_version", 2), ("abi_version", 4), ("dtype", 7), ("vocab", 0), ("d_model", 100), ("head_dim", 32),
     ("n_heads", 5), ("d_ff", 1000), ("n_layers", 0), ("n_layers", 9), ("max_loops", 0),
     ("max_loops", 17), ("max_pos", 0), ("max_batch", 0), ("max_batch", 5000), ("page_tokens", 32),
     ("max_pages", 0), ("max_prefill_tokens", 0), ("route_rule", 5), ("rms_eps", 0.0),
-    ("router_hidden", -64), ("router_hidden", 96), ("router_hidden", 8192),
+    ("router_hidden", -64), ("router_hidden", 96), ("router_hidden", 8192), ("dense_decode", 2),
+    ("dense_decode", -1),
 ])
 def test_invalid_config_rejected(lib, field, value):
     c = _cfg(**{field: value})

@@ -149,12 +149,14 @@ def test_f32_wide_heads(head_dim):
     _check_f32(m, w, prompts, g, o, f"f32-D{head_dim}")
 
 
-@pytest.mark.parametrize("rule", ["argmax", "cumprob"])
+@pytest.mark.parametrize("rule", ["argmax", "cumprob", "argmax-B1"])
 def test_f32_mlp_router(rule):
     """Two-layer MLP router (hidden 64): decisions with a clear margin match the
     oracle; when none is near a tie, depths, cache indices and logits match at
     the fp32 bar."""
-    m = _f32_small(router_hidden=64, router_bias="calibrated", steps=10)
+    batch = 1 if rule.endswith("-B1") else 3
+    rule = rule.split("-")[0]
+    m = _f32_small(router_hidden=64, router_bias="calibrated", steps=10, batch=batch, prompt_len=37 * (4 - batch))
     w = synth.make_weights(m)
     prompts = synth.make_prompts(m)
     g = parity.run_gpu(m, w, prompts, m.steps, route_rule=rule, threshold=0.5)
@@ -168,7 +170,10 @@ def test_f32_mlp_router(rule):
 
 
 def test_prefill_in_sequence_groups_is_identical():
-    m = _f32_small(batch=5, prompt_len=40, steps=3)
+    """Groups of two sequences give bitwise the one-group results; a group of
+    one sequence (the few-row projections, another summation order) agrees to
+    the fp32 bar."""
+    m = _f32_small(batch=6, prompt_len=40, steps=3)
     w = synth.make_weights(m)
     prompts = synth.make_prompts(m)
     a = parity.run_gpu(m, w, prompts, m.steps)
@@ -176,6 +181,11 @@ def test_prefill_in_sequence_groups_is_identical():
     assert np.array_equal(a.prefill_logits, b.prefill_logits)
     for s in range(m.steps):
         assert np.array_equal(a.step_logits[s], b.step_logits[s])
+    c = parity.run_gpu(m, w, prompts, m.steps, max_prefill_tokens=m.prompt_len)
+    assert np.array_equal(a.prefill_depths, c.prefill_depths)
+    err = max([_max_err(a.prefill_logits, c.prefill_logits)] +
+              [_max_err(a.step_logits[s], c.step_logits[s]) for s in range(m.steps)])
+    assert err <= F32_TOL
 
 
 def test_fp32_runs_are_bitwise_deterministic():
@@ -340,12 +350,13 @@ def _oracle_one_shot(m, w, tokens, **kw):
     return parity.run_oracle(m, w, tokens, [], all_logits=True, **kw)
 
 
-@pytest.mark.parametrize("head_dim", [16, 64])
-def test_f32_chunked_prefill_equals_one_shot(head_dim):
+@pytest.mark.parametrize("head_dim,batch", [(16, 3), (64, 3), (16, 1), (64, 1)])
+def test_f32_chunked_prefill_equals_one_shot(head_dim, batch):
     """Every position's logits and depth from a schedule of appended chunks and
-    decode steps equal one oracle prefill over the whole token sequence."""
+    decode steps equal one oracle prefill over the whole token sequence.  A
+    single sequence takes the few-row prefill projections."""
     L = _schedule_len(SCHEDULE)
-    m = _f32_small(batch=3, prompt_len=L, steps=0)
+    m = _f32_small(batch=batch, prompt_len=L, steps=0)
     if head_dim == 64:
         m = m.replace(n_heads=2, head_dim=64, d_model=128)
     w = synth.make_weights(m)
@@ -357,7 +368,7 @@ def test_f32_chunked_prefill_equals_one_shot(head_dim):
         for i in range(m.max_loops):
             assert np.array_equal(g.stats["index"][b][i], o.index[b][i]), (b, i)
     err = _max_err(g.logits, o.prefill_logits)
-    _report(f"f32-chunked-D{head_dim}", max_abs_logit_err=f"{err:.3g}", depth_hist=g.stats["depth_hist"])
+    _report(f"f32-chunked-D{head_dim}-B{batch}", max_abs_logit_err=f"{err:.3g}", depth_hist=g.stats["depth_hist"])
     assert err <= F32_TOL
 
 
@@ -376,8 +387,9 @@ def test_f32_chunked_prefill_in_sequence_groups():
     assert err <= F32_TOL
 
 
-def test_bf16_chunked_prefill_equals_one_shot():
-    m = synth.CONFIGS["bf16_d768_b32x512"].replace(batch=3)
+@pytest.mark.parametrize("batch", [3, 1])
+def test_bf16_chunked_prefill_equals_one_shot(batch):
+    m = synth.CONFIGS["bf16_d768_b32x512"].replace(batch=batch)
     w = synth.make_weights(synth.CONFIGS["bf16_d768_b32x512"])
     sched = [("prefill", 100), ("prefill", 29), ("prefill", 200), ("decode", 4), ("prefill", 33)]
     L = _schedule_len(sched)
@@ -389,12 +401,41 @@ def test_bf16_chunked_prefill_equals_one_shot():
     od, om = parity.router_decisions(m, w, tokens.ravel(), pos.ravel())
     bad, flips = parity.depth_agreement(g.depths.ravel(), od, om, BF16_MARGIN)
     err = _max_err(g.logits, o.prefill_logits)
-    _report("bf16-chunked", max_abs_logit_err=f"{err:.3g}", flip_rate=flips, depth_hist=g.stats["depth_hist"])
+    _report(f"bf16-chunked-B{batch}", max_abs_logit_err=f"{err:.3g}", flip_rate=flips, depth_hist=g.stats["depth_hist"])
     assert bad == 0
     for b in range(B):
         for i in range(m.max_loops):
             assert np.array_equal(g.stats["index"][b][i], np.flatnonzero(g.depths[b] >= i + 1)), (b, i)
     assert err <= BF16_TOL
+
+
+# ---------------------------------------------------------------------------
+# Gather-scatter off (dense decode): every row runs every loop, results discarded
+# for exited rows; the outputs are the gathered path's
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("prompt_len", [37, 1])
+def test_f32_dense_decode_equals_oracle(prompt_len):
+    """A one-token prompt leaves loop caches empty for rows that run a loop
+    their token exited: their attention output is discarded."""
+    m = _f32_small(prompt_len=prompt_len, steps=16 if prompt_len > 1 else 30)
+    w = synth.make_weights(m)
+    prompts = synth.make_prompts(m)
+    g = parity.run_gpu(m, w, prompts, m.steps, dense_decode=True)
+    o = parity.run_oracle(m, w, prompts, g.step_tokens)
+    _check_f32(m, w, prompts, g, o, f"f32-dense-T{prompt_len}")
+    top = int(g.step_depths[-1].max())
+    assert g.stats["last_step_active_rows"] == [m.batch] * top + [0] * (m.max_loops - top)
+
+
+def test_bf16_dense_decode_sampled_sequences():
+    m = synth.CONFIGS["bf16_d768_b32x512"].replace(batch=8, prompt_len=96, steps=10)
+    w = synth.make_weights(synth.CONFIGS["bf16_d768_b32x512"])
+    prompts = synth.make_prompts(m)
+    sample = [0, 5]
+    g = parity.run_gpu(m, w, prompts, m.steps, max_pos=m.max_pos, keep_logits_rows=sample, dense_decode=True)
+    o = parity.run_oracle(m, w, prompts[sample], [t[sample] for t in g.step_tokens])
+    _check_bf16(m, w, prompts, g, o, sample, "bf16-dense")
 
 
 # ---------------------------------------------------------------------------
