@@ -18,7 +18,17 @@ Model (T-LoopFormer, Section 3 and Appendix A):
     x += Attn(RMSNorm(x)) W_o ; x += SwiGLU(RMSNorm(x)).  RMSNorm has no
     learned affine (Appendix A).  The FFN is SwiGLU (the workloads' choice;
     the paper's own model uses a GELU MLP).  No biases, no AdaLN conditioning
-    (gamma = 0, unit gate), attention scale 1/sqrt(D), tied LM head.
+    (gamma = 0, unit gate) unless the weights carry it (below), attention
+    scale 1/sqrt(D), tied LM head.
+  * Optional AdaLN time/step conditioning (Section 3.1, Appendix A): a token
+    of depth m at loop i has cumulative time (i - 1) / m and step 1 / m (its
+    uniform trajectory, summing to 1 over its m loops); each scalar goes
+    through fixed Fourier features (256 wide, max period 10000) and its own
+    2-layer SiLU MLP, the two embeddings are summed, and layer j's modulator
+    (SiLU, then a linear map to 4d) gives (alpha_msa, alpha_mlp, gamma_msa,
+    gamma_mlp): x += (1 + alpha) * F(RMSNorm(x) * (1 + gamma)) for the
+    attention and FFN branches (the gate read as 1 + alpha, so that zero
+    modulator weights give the unconditioned block).
   * Router: linear map of h0 to R logits (Eq. 2's f_theta); the depth rule is
     argmax (the workloads), the cumulative-probability threshold of Eq. 3-5,
     or a fixed depth.
@@ -103,7 +113,13 @@ class Model:
             self.layers.append(dict(
                 Wq=qkv[0:self.d], Wk=qkv[self.d:2 * self.d], Wv=qkv[2 * self.d:3 * self.d],
                 Wo=f64(lw["w_o"]), Wg=gu[0:F], Wu=gu[F:2 * F], Wd=f64(lw["w_down"])))
+            if weights.get("cond") is not None:
+                self.layers[-1].update(Wmod=f64(lw["w_mod"]), bmod=f64(lw["b_mod"]))
         self.J = len(self.layers)
+        # AdaLN conditioning: time and step embedders (Appendix A)
+        cond = weights.get("cond")
+        self.cond = None if cond is None else {k: f64(v) for k, v in cond.items()}
+        self._mods: Dict[Tuple[int, int, int], Tuple[np.ndarray, ...]] = {}
         self.route_rule = route_rule
         self.threshold = float(threshold)
         self.fixed_depth = fixed_depth
@@ -149,6 +165,61 @@ def attend(q: np.ndarray, k: np.ndarray, v: np.ndarray, allowed: np.ndarray) -> 
         s = np.where(allowed, s, -np.inf)
         out[:, h, :] = softmax_rows(s) @ v[:, h, :]
     return out
+
+
+# ---------------------------------------------------------------------------
+# AdaLN time/step conditioning (Section 3.1, Appendix A)
+# ---------------------------------------------------------------------------
+
+FOURIER_DIM = 256           # D_f
+FOURIER_MAX_PERIOD = 10000.0
+
+
+def fourier_features(tau: float) -> np.ndarray:
+    """[cos(tau w_1), sin(tau w_1), ..., cos(tau w_K), sin(tau w_K)] with
+    K = D_f / 2 and w_k = exp(-(k - 1) / K * ln 10000)."""
+    K = FOURIER_DIM // 2
+    w = np.exp(-np.arange(K, dtype=np.float64) / K * math.log(FOURIER_MAX_PERIOD))
+    out = np.empty(FOURIER_DIM)
+    out[0::2] = np.cos(tau * w)
+    out[1::2] = np.sin(tau * w)
+    return out
+
+
+def trajectory(i: int, m: int) -> Tuple[float, float]:
+    """(cumulative time c_{i-1}, step Delta_i) of a token of depth m at loop i
+    (1-based) on its uniform trajectory: Delta = 1 / m, c_{i-1} = (i - 1) / m."""
+    return (i - 1) / m, 1.0 / m
+
+
+def scalar_embedding(model: Model, which: str, tau: float) -> np.ndarray:
+    """phi(tau) = W_2 silu(W_1 fourier(tau) + b_1) + b_2 for the "time" or "step" embedder."""
+    c = model.cond
+    h = silu(c[which + "_w1"] @ fourier_features(tau) + c[which + "_b1"])
+    return c[which + "_w2"] @ h + c[which + "_b2"]
+
+
+def modulation(model: Model, j: int, i: int, m: int) -> Tuple[np.ndarray, ...]:
+    """(alpha_msa, alpha_mlp, gamma_msa, gamma_mlp) of layer j for a token of
+    depth m at loop i: the modulator silu -> linear (4d) of e_t + e_Delta."""
+    key = (j, i, m)
+    if key not in model._mods:
+        t, dt = trajectory(i, m)
+        e = scalar_embedding(model, "time", t) + scalar_embedding(model, "step", dt)
+        L = model.layers[j]
+        v = L["Wmod"] @ silu(e) + L["bmod"]
+        d = model.d
+        model._mods[key] = (v[0:d], v[d:2 * d], v[2 * d:3 * d], v[3 * d:4 * d])
+    return model._mods[key]
+
+
+def row_modulation(model: Model, j: int, i: int, depths: np.ndarray) -> Optional[Tuple[np.ndarray, ...]]:
+    """Per-row (alpha_msa, alpha_mlp, gamma_msa, gamma_mlp) [n][d] for rows of the
+    given depths at loop i, or None without conditioning."""
+    if model.cond is None:
+        return None
+    parts = [modulation(model, j, i, int(m)) for m in depths]
+    return tuple(np.stack([p[k] for p in parts]) if parts else np.zeros((0, model.d)) for k in range(4))
 
 
 # ---------------------------------------------------------------------------
@@ -309,20 +380,29 @@ class SeqState:
 # The shared block on a gathered set of rows
 # ---------------------------------------------------------------------------
 
-def _layer(model: Model, j: int, X: np.ndarray, attn_fn) -> np.ndarray:
-    """One pre-norm layer of the shared block on the rows X [n][d]."""
+def _layer(model: Model, j: int, X: np.ndarray, attn_fn, mods=None) -> np.ndarray:
+    """One pre-norm layer of the shared block on the rows X [n][d]; ``mods`` is
+    the rows' AdaLN (alpha_msa, alpha_mlp, gamma_msa, gamma_mlp) or None."""
     L = model.layers[j]
     st = model.st
     n = X.shape[0]
-    Y = st(rms_norm(X, model.eps))
+    Y = rms_norm(X, model.eps)
+    if mods is not None:
+        Y = Y * (1.0 + mods[2])
+    Y = st(Y)
     q = st(Y @ L["Wq"].T).reshape(n, model.H, model.D)
     k = st(Y @ L["Wk"].T).reshape(n, model.H, model.D)
     v = st(Y @ L["Wv"].T).reshape(n, model.H, model.D)
     o = st(attn_fn(j, q, k, v).reshape(n, model.d))
-    X = X + o @ L["Wo"].T
-    Y2 = st(rms_norm(X, model.eps))
+    b = o @ L["Wo"].T
+    X = X + (b if mods is None else (1.0 + mods[0]) * b)
+    Y2 = rms_norm(X, model.eps)
+    if mods is not None:
+        Y2 = Y2 * (1.0 + mods[3])
+    Y2 = st(Y2)
     a = st(silu(Y2 @ L["Wg"].T) * (Y2 @ L["Wu"].T))
-    return X + a @ L["Wd"].T
+    b = a @ L["Wd"].T
+    return X + (b if mods is None else (1.0 + mods[1]) * b)
 
 
 def lm_head(model: Model, h: np.ndarray) -> np.ndarray:
@@ -387,7 +467,7 @@ def prefill(model: Model, tokens: Sequence[int], mode: str = "compact",
                 kp, K, Vv = st.keys(i - 1, j, int(qpos[-1]))
                 return attend(q, K, Vv, kp[None, :] <= qpos[:, None])
 
-            Hs[rho] = _layers(model, X, attn_fn)
+            Hs[rho] = _layers(model, X, attn_fn, i, m[rho])
         else:
             act = m >= i
             if not act.any():
@@ -402,16 +482,17 @@ def prefill(model: Model, tokens: Sequence[int], mode: str = "compact",
                 valid = st.key_mask(i - 1, kp)[None, :] | ~act[:, None]
                 return attend(q, K, Vv, causal & valid)
 
-            Xn = _layers(model, Hs.copy(), attn_fn)
+            Xn = _layers(model, Hs.copy(), attn_fn, i, m)
             Hs[act] = Xn[act]
     st.length = t0 + T
     logits = lm_head(model, Hs if all_logits else Hs[-1:])
     return st, (logits if all_logits else logits[0]), m, margin
 
 
-def _layers(model: Model, X: np.ndarray, attn_fn) -> np.ndarray:
+def _layers(model: Model, X: np.ndarray, attn_fn, i: int, depths: np.ndarray) -> np.ndarray:
+    """The shared block at loop i on rows X whose tokens have the given depths."""
     for j in range(model.J):
-        X = _layer(model, j, X, attn_fn)
+        X = _layer(model, j, X, attn_fn, row_modulation(model, j, i, depths))
     return X
 
 
@@ -454,7 +535,7 @@ def decode(model: Model, states: List[SeqState], tokens: Sequence[int]
                 out[r:r + 1] = attend(q[r:r + 1], K, Vv, allowed)
             return out
 
-        h[act] = _layers(model, h[act], attn_fn)
+        h[act] = _layers(model, h[act], attn_fn, i, m[act])
     for b, s in enumerate(states):
         s.depths.append(int(m[b]))
         s.length += 1

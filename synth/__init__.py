@@ -42,6 +42,9 @@ STREAM_ROUTER_W = 3
 STREAM_LM_HEAD = 4      # optional untied LM head
 STREAM_ROUTER_W1 = 5    # hidden layer of the MLP router
 STREAM_LAYER_BASE = 16  # layer j uses 16 + 4j + {0: qkv, 1: o, 2: gate_up, 3: down}
+STREAM_COND_BASE = 200  # AdaLN: 200-203 time embedder (w1, b1, w2, b2), 204-207 step embedder,
+                        # 210 + 2j / 211 + 2j layer j's modulator weight / bias
+FOURIER_DIM = 256       # width of the fixed Fourier features of a conditioning scalar
 STREAM_PROMPT = 100
 STREAM_CALIB = 101
 
@@ -175,6 +178,7 @@ class ModelConfig:
     rms_eps: float = 1e-5
     std: float = 0.02
     router_hidden: int = 0  # 0: linear router; else the hidden width of a 2-layer MLP router
+    adaln: bool = False     # AdaLN time/step conditioning weights
 
     @property
     def max_pos(self) -> int:
@@ -278,6 +282,11 @@ def make_weights(cfg: ModelConfig, seed: int = SEED, cache: bool = True) -> Dict
       fp32, and router_w [R][Hr] is the output layer)
       w_qkv [3d][d] (rows q | k | v, head-major within each), w_o [d][d],
       w_gate_up [2F][d] (rows gate | up), w_down [d][F].
+      With adaln: "cond" = {time_w1 [d][256], time_b1 [d], time_w2 [d][d],
+      time_b2 [d], and the same for step_*}, and per layer w_mod [4d][d]
+      (rows alpha_msa | alpha_mlp | gamma_msa | gamma_mlp), b_mod [4d]; matrices
+      in the storage dtype, biases fp32.  Scales: unit-variance hidden
+      pre-activations in the embedders, modulation entries of roughly 0.2.
     """
     key = (cfg, seed)
     if cache and key in _WEIGHT_CACHE:
@@ -310,6 +319,21 @@ def make_weights(cfg: ModelConfig, seed: int = SEED, cache: bool = True) -> Dict
             "w_down": _mat(seed, s + 3, d, F, cfg),
         })
     w["layers"] = layers
+    if cfg.adaln:
+        c = STREAM_COND_BASE
+        cond = {}
+        for k, name in enumerate(("time", "step")):
+            base = c + 4 * k
+            cond[name + "_w1"] = to_storage(normal(seed, base + 0, d * FOURIER_DIM, 1.0 / np.sqrt(FOURIER_DIM / 2))
+                                            .reshape(d, FOURIER_DIM), cfg.dtype)
+            cond[name + "_b1"] = normal(seed, base + 1, d, 0.1).astype(np.float32)
+            cond[name + "_w2"] = to_storage(normal(seed, base + 2, d * d, 1.0 / np.sqrt(d)).reshape(d, d), cfg.dtype)
+            cond[name + "_b2"] = normal(seed, base + 3, d, 0.1).astype(np.float32)
+        w["cond"] = cond
+        for j, lw in enumerate(layers):
+            lw["w_mod"] = to_storage(normal(seed, c + 10 + 2 * j, 4 * d * d, 0.5 / np.sqrt(d)).reshape(4 * d, d),
+                                     cfg.dtype)
+            lw["b_mod"] = normal(seed, c + 11 + 2 * j, 4 * d, 0.05).astype(np.float32)
     if cfg.router_bias == "zero":
         w["router_b"] = np.zeros(R, dtype=np.float32)
     elif cfg.router_bias == "calibrated":

@@ -418,6 +418,97 @@ def test_cumprob_rule_end_to_end_with_dense_model():
     assert np.max(np.abs(logits - ref)) < 1e-12
 
 
+# ---------------------------------------------------------------------------
+# AdaLN time/step conditioning (Section 3.1, Appendix A)
+# ---------------------------------------------------------------------------
+
+def test_fourier_features_closed_form():
+    f0 = O.fourier_features(0.0)
+    assert f0.shape == (256,)
+    assert np.array_equal(f0[0::2], np.ones(128)) and np.array_equal(f0[1::2], np.zeros(128))
+    f1 = O.fourier_features(1.0)
+    assert f1[0] == pytest.approx(math.cos(1.0), abs=1e-15) and f1[1] == pytest.approx(math.sin(1.0), abs=1e-15)
+    w_last = 10000.0 ** (-127.0 / 128.0)  # lowest frequency
+    assert f1[254] == pytest.approx(math.cos(w_last), abs=1e-15)
+    assert f1[255] == pytest.approx(math.sin(w_last), abs=1e-15)
+
+
+@pytest.mark.parametrize("m", [1, 2, 5])
+def test_uniform_trajectory_sums_to_one(m):
+    ts = [O.trajectory(i, m) for i in range(1, m + 1)]
+    assert ts[0][0] == 0.0
+    assert sum(dt for _, dt in ts) == pytest.approx(1.0, abs=1e-15)
+    for (c0, dt), (c1, _) in zip(ts, ts[1:]):
+        assert c1 == pytest.approx(c0 + dt, abs=1e-15)  # c_i = c_{i-1} + Delta_i
+
+
+def _adaln_cfg(**kw):
+    base = dict(max_loops=4, prompt_len=24, adaln=True)
+    base.update(kw)
+    return synth.tiny_config(**base)
+
+
+def test_adaln_zero_modulator_is_unconditioned_model():
+    """Zero modulator weights and bias (the paper's initialisation) leave the
+    unmodulated backbone, exactly, under the 1 + alpha reading of the gate."""
+    cfg = _adaln_cfg()
+    w = synth.make_weights(cfg)
+    w0 = dict(w, layers=[dict(lw, w_mod=np.zeros_like(lw["w_mod"]), b_mod=np.zeros_like(lw["b_mod"]))
+                         for lw in w["layers"]])
+    plain = {k: v for k, v in w.items() if k != "cond"}
+    plain["layers"] = [{k: v for k, v in lw.items() if k not in ("w_mod", "b_mod")} for lw in w["layers"]]
+    toks = synth.make_prompts(cfg)[0]
+    _, a, ma, _ = O.prefill(_model(cfg, w0), toks, all_logits=True)
+    _, b, mb, _ = O.prefill(_model(cfg, plain), toks, all_logits=True)
+    assert np.array_equal(ma, mb) and np.array_equal(a, b)
+    _, c, _, _ = O.prefill(_model(cfg, w), toks, all_logits=True)
+    assert np.max(np.abs(c - b)) > 1e-3  # the synthetic modulator does act
+
+
+@pytest.mark.parametrize("seed", [3, 4])
+def test_adaln_routed_prefill_equals_dense_masked_model(seed):
+    """Per-token conditioning on each token's own trajectory: the oracle's
+    gathered prefill equals the independent dense PyTorch model with library
+    embedders and the same modulation."""
+    cfg = _adaln_cfg()
+    w = synth.make_weights(cfg, seed=seed)
+    toks = synth.make_prompts(cfg, seed=seed)[0]
+    _, logits, m, _ = O.prefill(_model(cfg, w), toks, all_logits=True)
+    assert len(set(m.tolist())) >= 3
+    ref = textbook.routed_dense_logits(w, toks, m, cfg.n_heads, cfg.head_dim, cfg.rms_eps)
+    assert np.max(np.abs(logits - ref)) < 1e-12
+
+
+def test_adaln_fixed_depth_equals_conditioned_gpt():
+    cfg = _adaln_cfg(max_loops=3)
+    w = synth.make_weights(cfg)
+    toks = synth.make_prompts(cfg)[0]
+    M = _model(cfg, w, route_rule=O.FIXED, fixed_depth=3)
+    _, logits, _, _ = O.prefill(M, toks, all_logits=True)
+    ref = textbook.tied_gpt_logits(w, toks, cfg.n_heads, cfg.head_dim, 3, cfg.rms_eps)
+    assert np.max(np.abs(logits - ref)) < 1e-12
+
+
+def test_adaln_cached_decode_equals_full_recompute():
+    cfg = synth.tiny_config(batch=1, prompt_len=8, steps=6, max_loops=4, adaln=True)
+    w = synth.make_weights(cfg, seed=12)
+    M, states, logits, toks = _run(cfg, w, seed=12)
+    for s in range(cfg.steps + 1):
+        T = cfg.prompt_len + s
+        _, lg_full, m_full, _ = O.prefill(M, toks[0, :T])
+        assert np.max(np.abs(logits[0, s] - lg_full)) < 1e-12
+        dense = textbook.routed_dense_logits(w, toks[0, :T], m_full, cfg.n_heads, cfg.head_dim, cfg.rms_eps)
+        assert np.max(np.abs(logits[0, s] - dense[-1])) < 1e-12
+
+
+def test_adaln_literal_cache_equals_compact_cache():
+    cfg = synth.tiny_config(batch=2, prompt_len=10, steps=5, adaln=True)
+    w = synth.make_weights(cfg)
+    _, _, a, _ = _run(cfg, w, "compact")
+    _, _, b, _ = _run(cfg, w, "literal")
+    assert np.max(np.abs(a - b)) < 1e-12
+
+
 def test_bf16_rounding_mode_stays_close():
     cfg = synth.tiny_config(batch=1, prompt_len=12, steps=3)
     w = synth.make_weights(cfg)

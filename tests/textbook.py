@@ -19,26 +19,59 @@ def _rms(x, eps):
     return x * torch.rsqrt((x * x).mean(-1, keepdim=True) + eps)
 
 
-def _layer(x, lw, H, D, eps, attn_mask=None, is_causal=False):
+def _layer(x, lw, H, D, eps, attn_mask=None, is_causal=False, mod=None):
+    """Pre-norm layer; ``mod`` = per-row AdaLN (shift-free) modulation
+    [T][4d] split as (alpha_msa, alpha_mlp, gamma_msa, gamma_mlp), or None."""
     T, d = x.shape
+    if mod is not None:
+        a_msa, a_mlp, g_msa, g_mlp = mod.split(d, dim=-1)
     y = _rms(x, eps)
+    if mod is not None:
+        y = y * (1 + g_msa)
     qkv = F.linear(y, _t(lw["w_qkv"]))
     q, k, v = (t.reshape(T, H, D).transpose(0, 1) for t in qkv.split(d, dim=-1))
     o = F.scaled_dot_product_attention(q, k, v, attn_mask=attn_mask, is_causal=is_causal)
-    x = x + F.linear(o.transpose(0, 1).reshape(T, d), _t(lw["w_o"]))
+    b = F.linear(o.transpose(0, 1).reshape(T, d), _t(lw["w_o"]))
+    x = x + (b if mod is None else (1 + a_msa) * b)
     y2 = _rms(x, eps)
+    if mod is not None:
+        y2 = y2 * (1 + g_mlp)
     g, u = F.linear(y2, _t(lw["w_gate_up"])).chunk(2, dim=-1)
-    return x + F.linear(F.silu(g) * u, _t(lw["w_down"]))
+    b = F.linear(F.silu(g) * u, _t(lw["w_down"]))
+    return x + (b if mod is None else (1 + a_mlp) * b)
+
+
+def _scalar_embed(cond, which, tau):
+    """DiT-style embedder of scalars tau [T]: sinusoidal features (256 wide,
+    cos/sin interleaved per frequency, max period 10000), Linear-SiLU-Linear."""
+    half = 128
+    freqs = torch.exp(-torch.log(torch.tensor(10000.0, dtype=f64)) * torch.arange(half, dtype=f64) / half)
+    ang = tau[:, None] * freqs[None, :]
+    feats = torch.stack([torch.cos(ang), torch.sin(ang)], dim=-1).reshape(tau.shape[0], 2 * half)
+    h = F.silu(F.linear(feats, _t(cond[which + "_w1"]), _t(cond[which + "_b1"])))
+    return F.linear(h, _t(cond[which + "_w2"]), _t(cond[which + "_b2"]))
+
+
+def adaln_modulation(weights, lw, loop, depths):
+    """Layer modulation [T][4d] for rows of the given depths at 1-based ``loop``:
+    cumulative time (loop - 1) / m and step 1 / m, summed embeddings, SiLU, Linear."""
+    m = torch.as_tensor(np.asarray(depths, dtype=np.float64))
+    cond = weights["cond"]
+    c = _scalar_embed(cond, "time", (loop - 1) / m) + _scalar_embed(cond, "step", 1.0 / m)
+    return F.linear(F.silu(c), _t(lw["w_mod"]), _t(lw["b_mod"]))
 
 
 def tied_gpt_logits(weights, tokens, H, D, loops, eps=1e-5):
-    """Pre-norm GPT whose layer stack is the J-layer block repeated ``loops`` times."""
+    """Pre-norm GPT whose layer stack is the J-layer block repeated ``loops``
+    times (every token of depth ``loops`` when the weights carry AdaLN)."""
     tokens = torch.as_tensor(np.asarray(tokens, dtype=np.int64))
     E, P = _t(weights["tok_emb"]), _t(weights["pos_emb"])
     x = E[tokens] + P[: tokens.shape[0]]
-    for _ in range(loops):
+    T = tokens.shape[0]
+    for i in range(1, loops + 1):
         for lw in weights["layers"]:
-            x = _layer(x, lw, H, D, eps, is_causal=True)
+            mod = adaln_modulation(weights, lw, i, [loops] * T) if weights.get("cond") else None
+            x = _layer(x, lw, H, D, eps, is_causal=True, mod=mod)
     head = E if weights.get("lm_head") is None else _t(weights["lm_head"])
     return F.linear(_rms(x, eps), head).numpy()
 
@@ -79,6 +112,7 @@ def routed_dense_logits(weights, tokens, depths, H, D, eps=1e-5):
         mask = causal & (act[None, :] | ~act[:, None])
         xn = x
         for lw in weights["layers"]:
-            xn = _layer(xn, lw, H, D, eps, attn_mask=mask)
+            mod = adaln_modulation(weights, lw, i, depths.numpy()) if weights.get("cond") else None
+            xn = _layer(xn, lw, H, D, eps, attn_mask=mask, mod=mod)
         x = torch.where(act[:, None], xn, x)
     return F.linear(_rms(x, eps), E).numpy()
