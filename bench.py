@@ -12,7 +12,8 @@ O projection, SwiGLU FFN), the LM head and the greedy pick.
 Prints one JSON line: decoded tokens/s, the decode attention's achieved HBM
 bandwidth against 8 TB/s (HIP events around every attention launch on the
 library's stream), the same kernels forced to fixed depth R, the same step
-with gather-scatter off, time to first token over prompt lengths, a prefill
+with gather-scatter off, the step with AdaLN conditioning, time to first
+token over prompt lengths, a prefill
 measurement, the MLP-router threshold sweep, and the CPU oracle on a bounded
 sample.
 """
@@ -196,6 +197,27 @@ def gather_scatter_off(torch, tlf, model, w, prompts, routed_ms_per_step, warmup
             "steps": steps, "ms_per_step": ms / steps, "tokens_per_s": B * steps / (ms / 1e3),
             "latency_increase": (ms / steps) / routed_ms_per_step - 1.0,
             "rows_per_loop_last_step": st["last_step_active_rows"]}
+
+
+def adaln_decode(torch, tlf, synth, name, routed_ms_per_step, warmup=4, steps=30):
+    """The decode workload with AdaLN time/step conditioning: every projection
+    row gathers the modulation of its token's (loop, depth) pair."""
+    m = synth.CONFIGS[name].replace(adaln=True)
+    w = synth.make_weights(m)
+    prompts = synth.make_prompts(m)
+    B, T = prompts.shape
+    sess = tlf.Session(m, w, max_batch=B, max_pos=T + warmup + steps, max_prefill_tokens=65536)
+    try:
+        logits, _ = sess.prefill(torch.from_numpy(prompts).cuda(), want_depths=False)
+        first = torch.argmax(logits, dim=-1)
+        del logits
+        ms, _ = replay_decode_ms(sess, torch, B, m.vocab, first, warmup, steps)
+    finally:
+        sess.close()
+        torch.cuda.empty_cache()
+    return {"what": "decode with AdaLN conditioning (synthetic conditioning weights); graph-replayed steps",
+            "steps": steps, "ms_per_step": ms / steps, "tokens_per_s": B * steps / (ms / 1e3),
+            "overhead": (ms / steps) / routed_ms_per_step - 1.0}
 
 
 def ttft_sweep(torch, tlf, model, w, synth, lengths=(128, 512, 1024, 2048), chunk=512, reps=5):
@@ -398,6 +420,7 @@ def main():
     ap.add_argument("--no-sweep", action="store_true", help="skip the MLP-router threshold sweep")
     ap.add_argument("--no-ablation", action="store_true", help="skip the gather-scatter-off decode")
     ap.add_argument("--no-ttft", action="store_true", help="skip the time-to-first-token sweep")
+    ap.add_argument("--no-adaln", action="store_true", help="skip the AdaLN-conditioned decode")
     ap.add_argument("--prefill-only", action="store_true",
                     help="run only the prefill measurement (batch 8 x 4096) and print its JSON")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
@@ -520,6 +543,9 @@ def main():
     if not args.no_ablation:
         out["gather_scatter_off"] = gather_scatter_off(torch, tlf, model, w, prompts, ms / args.steps)
         log(f"gather-scatter off: {out['gather_scatter_off']['ms_per_step']:.3f} ms/step")
+    if not args.no_adaln:
+        out["adaln"] = adaln_decode(torch, tlf, synth, args.config, ms / args.steps)
+        log(f"adaln: {out['adaln']['ms_per_step']:.3f} ms/step")
     if not args.no_ttft:
         out["ttft"] = ttft_sweep(torch, tlf, model, w, synth)
     if not args.no_prefill:

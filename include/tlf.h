@@ -49,7 +49,7 @@
 extern "C" {
 #endif
 
-#define TLF_ABI_VERSION 3
+#define TLF_ABI_VERSION 4
 #define TLF_MAX_LOOPS 16
 #define TLF_MAX_LAYERS 8
 #define TLF_MAX_BATCH 4096
@@ -112,6 +112,11 @@ typedef struct tlf_config {
                             batch, exited rows are computed and discarded at the scatter and
                             write no cache entry, attention keeps the validity mask of Eq. 10.
                             Same results as 0; prefill is not affected */
+  int32_t adaln;         /* 0: unconditioned block; 1: AdaLN time/step conditioning (Section 3.1,
+                            Appendix A; weights in tlf_weights.adaln): a token of depth m at
+                            loop i has cumulative time (i-1)/m and step 1/m, and layer j's
+                            modulation (alpha_msa, alpha_mlp, gamma_msa, gamma_mlp) enters as
+                            x += (1 + alpha) * F(RMSNorm(x) * (1 + gamma)) */
 } tlf_config;
 
 /* Weights of layer j of the shared block, row-major [out][in] (y = x W^T),
@@ -123,6 +128,27 @@ typedef struct tlf_layer_weights {
   const void* w_down;    /* [d][F] */
 } tlf_layer_weights;
 
+/* AdaLN conditioning weights (config.adaln = 1), row-major [out][in]:
+ * matrices in the storage dtype, biases float32.  Each conditioning scalar
+ * s becomes 256 Fourier features [cos(s w_1), sin(s w_1), ..., cos(s w_128),
+ * sin(s w_128)], w_k = 10000^(-(k-1)/128), then phi(s) = W_2 silu(W_1 f + b_1)
+ * + b_2; the embedding is phi_time(c) + phi_step(Delta), and layer j's
+ * modulation is mod_w[j] silu(embedding) + mod_b[j].  Read by tlf_init only:
+ * the modulation of every (layer, loop, depth) is tabulated there. */
+typedef struct tlf_adaln_weights {
+  const void* time_w1;  /* [d][256] */
+  const float* time_b1; /* [d] */
+  const void* time_w2;  /* [d][d] */
+  const float* time_b2; /* [d] */
+  const void* step_w1;  /* [d][256] */
+  const float* step_b1; /* [d] */
+  const void* step_w2;  /* [d][d] */
+  const float* step_b2; /* [d] */
+  const void* const* mod_w;  /* host array of n_layers device pointers: [4d][d], output rows
+                                alpha_msa | alpha_mlp | gamma_msa | gamma_mlp */
+  const float* const* mod_b; /* host array of n_layers device pointers: [4d] */
+} tlf_adaln_weights;
+
 typedef struct tlf_weights {
   const void* tok_emb;      /* [V][d] storage dtype; also the LM head when lm_head is NULL */
   const void* pos_emb;      /* [max_pos][d] storage dtype */
@@ -133,6 +159,7 @@ typedef struct tlf_weights {
   const tlf_layer_weights* layers; /* host array of n_layers entries (copied by tlf_init) */
   const void* router_w1;    /* MLP router hidden layer [Hr][d] storage dtype; NULL for a linear router */
   const float* router_b1;   /* [Hr] float32; NULL for a linear router */
+  const tlf_adaln_weights* adaln; /* host pointer; required when config.adaln = 1, else NULL */
 } tlf_weights;
 
 typedef struct tlf_cache_stats_t {

@@ -21,6 +21,7 @@ enum Buf {
   B_POOL, B_POS, B_PAGE_TABLE, B_CACHE_LEN, B_CHUNK_LEN, B_SEQ_LEN, B_SCALARS, B_DEPTH_HIST, B_STEP_STATS,
   B_X_DEC, B_XC_DEC, B_KVSLOT, B_DEPTH_DEC, B_PERM, B_NACT, B_Q_DEC, B_O_DEC, B_ACT_DEC, B_KEYS,
   B_X_PRE, B_Y_PRE, B_DEPTH_PRE, B_TOK_IDX, B_Q_PRE, B_O_PRE, B_ACT_PRE, B_HID,
+  B_ROW_DEPTH, B_MOD, B_COND_TMP,
   B_COUNT
 };
 
@@ -68,6 +69,10 @@ bool make_layout(const tlf_config& c, Layout* L) {
   sz[B_O_PRE] = P * d * 4;
   sz[B_ACT_PRE] = P * F * 4;
   sz[B_HID] = std::max(P, B) * (int64_t)c.router_hidden * 4;  // MLP router hidden rows
+  sz[B_ROW_DEPTH] = B * 4;
+  // AdaLN: modulation of every (layer, loop, depth), and its set-up scratch
+  sz[B_MOD] = c.adaln ? (int64_t)c.n_layers * R * R * 4 * d * 4 : 0;
+  sz[B_COND_TMP] = c.adaln ? (int64_t)cond_scratch_floats((int)R, (int)d) * 4 : 0;
   size_t off = 0;
   for (int i = 0; i < B_COUNT; ++i) {
     if (sz[i] < 0) return false;
@@ -108,6 +113,7 @@ int validate_config(const tlf_config* c) {
   if (c->decode_graph != 0 && c->decode_graph != 1) return TLF_E_INVALID_ARG;
   if (c->router_hidden < 0 || c->router_hidden > 4096 || c->router_hidden % 64 != 0) return TLF_E_INVALID_ARG;
   if (c->dense_decode != 0 && c->dense_decode != 1) return TLF_E_INVALID_ARG;
+  if (c->adaln != 0 && c->adaln != 1) return TLF_E_INVALID_ARG;
   // the decode attention stages one sequence's page list in LDS
   if (ceil_div(c->max_pos, kPage) > kAttnMaxPages) return TLF_E_INVALID_ARG;
   // the decode projections address weights and activations with 32-bit element offsets
@@ -127,6 +133,14 @@ int validate_weights(const tlf_config* c, const tlf_weights* w) {
   for (int j = 0; j < w->n_layers; ++j) {
     const tlf_layer_weights& l = w->layers[j];
     if (!l.w_qkv || !l.w_o || !l.w_gate_up || !l.w_down) return TLF_E_INVALID_ARG;
+  }
+  if ((c->adaln != 0) != (w->adaln != nullptr)) return TLF_E_INVALID_ARG;
+  if (const tlf_adaln_weights* a = w->adaln) {
+    if (!a->time_w1 || !a->time_b1 || !a->time_w2 || !a->time_b2 || !a->step_w1 || !a->step_b1 ||
+        !a->step_w2 || !a->step_b2 || !a->mod_w || !a->mod_b)
+      return TLF_E_INVALID_ARG;
+    for (int j = 0; j < w->n_layers; ++j)
+      if (!a->mod_w[j] || !a->mod_b[j]) return TLF_E_INVALID_ARG;
   }
   return TLF_OK;
 }
@@ -247,6 +261,22 @@ int attn_waves(const tlf_ctx* ctx) {
 // projections on the split-K decode GEMM.
 constexpr int kPrefillFewRows = 2048;
 
+// AdaLN: point a projection at its rows' modulation at (loop i, layer j):
+// part 0..3 = alpha_msa, alpha_mlp, gamma_msa, gamma_mlp of the table
+// [j][i][m][4d]; gamma scales the operand rows, alpha gates a residual
+// epilogue.  depth(r) = depth[src(r)] (by_src) or depth[r].
+void set_mod(const tlf_ctx* ctx, GemmArgs* g, int i, int j, int part, const int32_t* depth, int by_src) {
+  const tlf_config& c = ctx->cfg;
+  if (!c.adaln) return;
+  const int64_t R = c.max_loops, d = c.d_model;
+  const float* p = ctx->buf<float>(B_MOD) + ((int64_t)j * R + i) * R * 4 * d + part * d;
+  if (part >= 2) g->mod_g = p;
+  else g->mod_a = p;
+  g->mod_ld = (int)(4 * d);
+  g->mod_depth = depth;
+  g->mod_by_src = by_src;
+}
+
 const void* head_weights(const tlf_ctx* ctx) { return ctx->w.lm_head ? ctx->w.lm_head : ctx->w.tok_emb; }
 
 template <typename T>
@@ -263,6 +293,7 @@ int run_prefill(tlf_ctx* ctx, int B, int T_, int pos0, const int32_t* tokens, fl
   const int G = std::max(1, ctx->L.pre_rows / T_);
   float* x = ctx->buf<float>(B_X_PRE);
   float* y = ctx->buf<float>(B_Y_PRE);
+  const int32_t* pre_depth = ctx->buf<int32_t>(B_DEPTH_PRE);  // by residual row
   for (int b0 = 0; b0 < B; b0 += G) {
     const int Gc = std::min(G, B - b0);
     const int rows = Gc * T_;
@@ -308,6 +339,7 @@ int run_prefill(tlf_ctx* ctx, int B, int T_, int pos0, const int32_t* tokens, fl
         q.A = few ? x : y; q.lda = d; q.W = lw.w_qkv; q.N = 3 * d; q.K = d; q.w_rows = 3 * d; q.rm = rm;
         q.out = ctx->buf<float>(B_Q_PRE); q.ldo = d; q.d = d; q.eps = c.rms_eps; q.spec = i == 0;
         q.kv.c = ctx->cv; q.kv.loop = i; q.kv.layer = j; q.kv.prefill = 1; q.kv.b0 = b0; q.kv.seg = T_;
+        set_mod(ctx, &q, i, j, 2, pre_depth, 1);
         if (few) TLF_HIP(launch_dgemm<T>(q, A_SRC, E_QKV, true, ctx->cus, s));
         else TLF_HIP(launch_gemm<T>(q, A_SRC, E_QKV, s));
 
@@ -320,6 +352,7 @@ int run_prefill(tlf_ctx* ctx, int B, int T_, int pos0, const int32_t* tokens, fl
         GemmArgs o;
         o.A = ctx->buf<float>(B_O_PRE); o.lda = d; o.W = lw.w_o; o.N = d; o.K = d; o.w_rows = d; o.rm = rm;
         o.out = x; o.ldo = d; o.scatter = 1; o.spec = i == 0;
+        set_mod(ctx, &o, i, j, 0, pre_depth, 1);
         if (few) {
           TLF_HIP(launch_dgemm<T>(o, A_CMP, E_RESID, false, ctx->cus, s));
         } else {
@@ -330,12 +363,14 @@ int run_prefill(tlf_ctx* ctx, int B, int T_, int pos0, const int32_t* tokens, fl
         GemmArgs gu;
         gu.A = few ? x : y; gu.lda = d; gu.W = lw.w_gate_up; gu.N = 2 * F; gu.K = d; gu.w_rows = 2 * F; gu.rm = rm;
         gu.out = ctx->buf<float>(B_ACT_PRE); gu.ldo = F; gu.F = F; gu.eps = c.rms_eps; gu.spec = i == 0;
+        set_mod(ctx, &gu, i, j, 3, pre_depth, 1);
         if (few) TLF_HIP(launch_dgemm<T>(gu, A_SRC, E_SWIGLU, true, ctx->cus, s));
         else TLF_HIP(launch_gemm<T>(gu, A_SRC, E_SWIGLU, s));
 
         GemmArgs dn;
         dn.A = ctx->buf<float>(B_ACT_PRE); dn.lda = F; dn.W = lw.w_down; dn.N = d; dn.K = F; dn.w_rows = d;
         dn.rm = rm; dn.out = x; dn.ldo = d; dn.scatter = 1; dn.spec = i == 0;
+        set_mod(ctx, &dn, i, j, 1, pre_depth, 1);
         if (few) {
           TLF_HIP(launch_dgemm<T>(dn, A_CMP, E_RESID, false, ctx->cus, s));
         } else {
@@ -391,6 +426,7 @@ int run_decode(tlf_ctx* ctx, hipStream_t s, const int32_t* tokens, float* logits
   pa.argmax_keys = ctx->buf<unsigned long long>(B_KEYS);
   pa.kv_entry_bytes = (int64_t)c.n_layers * 2 * c.d_model * ctx->L.s;
   pa.dense = c.dense_decode;
+  pa.row_depth = ctx->buf<int32_t>(B_ROW_DEPTH);
   TLF_HIP(launch_plan_decode(pa, s));
   // dense decode: rows are in batch order and a row's result is kept while its
   // token's depth exceeds the loop index
@@ -418,6 +454,7 @@ int run_decode(tlf_ctx* ctx, hipStream_t s, const int32_t* tokens, float* logits
       q.out = ctx->buf<float>(B_Q_DEC); q.ldo = d; q.d = d; q.eps = c.rms_eps;
       q.kv.c = ctx->cv; q.kv.loop = i; q.kv.layer = j; q.kv.prefill = 0; q.kv.slot_base = kv_slot + (int64_t)i * B;
       q.spec = i == 0;
+      set_mod(ctx, &q, i, j, 2, pa.row_depth, 0);
       TLF_HIP(launch_dgemm<T>(q, first ? A_SRC : A_CMP, E_QKV, true, ctx->cus, s));
 
       AttnDecodeArgs at;
@@ -437,16 +474,19 @@ int run_decode(tlf_ctx* ctx, hipStream_t s, const int32_t* tokens, float* logits
       GemmArgs o;  // x += o W_o^T
       o.A = ctx->buf<float>(B_O_DEC); o.lda = d; o.W = lw.w_o; o.N = d; o.K = d; o.w_rows = d; o.rm = rm;
       o.out = xc; o.ldo = d; o.spec = i == 0; o.keep_depth = keep_depth; o.keep_loop = i;
+      set_mod(ctx, &o, i, j, 0, pa.row_depth, 0);
       TLF_HIP(launch_dgemm<T>(o, A_CMP, E_RESID, false, ctx->cus, s));
 
       GemmArgs gu;  // act = silu(RMSNorm(x) W_g^T) * (RMSNorm(x) W_u^T)
       gu.A = xc; gu.lda = d; gu.W = lw.w_gate_up; gu.N = 2 * F; gu.K = d; gu.w_rows = 2 * F; gu.rm = rm;
       gu.out = ctx->buf<float>(B_ACT_DEC); gu.ldo = F; gu.F = F; gu.eps = c.rms_eps; gu.spec = i == 0;
+      set_mod(ctx, &gu, i, j, 3, pa.row_depth, 0);
       TLF_HIP(launch_dgemm<T>(gu, A_CMP, E_SWIGLU, true, ctx->cus, s));
 
       GemmArgs dn;  // x += act W_d^T
       dn.A = ctx->buf<float>(B_ACT_DEC); dn.lda = F; dn.W = lw.w_down; dn.N = d; dn.K = F; dn.w_rows = d;
       dn.rm = rm; dn.out = xc; dn.ldo = d; dn.spec = i == 0; dn.keep_depth = keep_depth; dn.keep_loop = i;
+      set_mod(ctx, &dn, i, j, 1, pa.row_depth, 0);
       TLF_HIP(launch_dgemm<T>(dn, A_CMP, E_RESID, false, ctx->cus, s));
     }
   }
@@ -545,6 +585,21 @@ int tlf_init(const tlf_config* cfg, const tlf_weights* w, void* d_workspace, siz
   if (e == hipSuccess) e = launch_fill_i32(cv.page_next, 0, 2, s);
   if (e == hipSuccess) e = launch_fill_u64(cv.depth_hist, 0ull, cfg->max_loops, s);
   if (e == hipSuccess) e = launch_fill_u64(reinterpret_cast<unsigned long long*>(cv.step_stats), 0ull, kStatCount, s);
+  if (e == hipSuccess && cfg->adaln) {
+    // the modulation of every (layer, loop, depth); the caller's conditioning
+    // weights are not read again
+    const tlf_adaln_weights& a = *w->adaln;
+    CondWeights cw;
+    cw.w1[0] = a.time_w1; cw.b1[0] = a.time_b1; cw.w2[0] = a.time_w2; cw.b2[0] = a.time_b2;
+    cw.w1[1] = a.step_w1; cw.b1[1] = a.step_b1; cw.w2[1] = a.step_w2; cw.b2[1] = a.step_b2;
+    cw.mod_w = a.mod_w; cw.mod_b = a.mod_b;
+    float* table = ctx->buf<float>(B_MOD);
+    float* tmp = ctx->buf<float>(B_COND_TMP);
+    e = cfg->dtype == TLF_DTYPE_BF16
+            ? launch_cond_table<bf16>(cw, cfg->n_layers, cfg->max_loops, cfg->d_model, table, tmp, s)
+            : launch_cond_table<float>(cw, cfg->n_layers, cfg->max_loops, cfg->d_model, table, tmp, s);
+  }
+  ctx->w.adaln = nullptr;
   if (e != hipSuccess) { delete ctx; return TLF_E_HIP; }
   *out = ctx;
   return TLF_OK;

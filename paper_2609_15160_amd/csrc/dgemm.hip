@@ -53,9 +53,15 @@ struct DgemmShared {
   int* orow;        // [BM] logits row of each tile row
   int64_t* kv;      // [BM] cache slot offset of each tile row (-1: no cache entry)
   int* keep;        // [BM] E_RESID: the row's result is stored
+  int* moff;        // [BM] E_RESID with a gate: the row's modulation row offset
 };
 
-template <typename T, int RM, int CN, int W, int KB, int AK, int EK, bool NORM>
+// depth of row r for the AdaLN table (valid for active rows only)
+__device__ __forceinline__ int mod_row_depth(const GemmArgs& g, int r) {
+  return g.mod_depth[g.mod_by_src ? row_src(g.rm, r) : r];
+}
+
+template <typename T, int RM, int CN, int W, int KB, int AK, int EK, bool NORM, bool MOD>
 __device__ __forceinline__ void dgemm_tile(const GemmArgs& g, int nact, int act_rows, const DgemmShared& sh) {
   using M = Mfma<T>;
   typedef typename M::frag Frag;
@@ -114,7 +120,10 @@ __device__ __forceinline__ void dgemm_tile(const GemmArgs& g, int nact, int act_
     for (int i = 0; i < RM; ++i) {
       const int rl = i * 16 + c16, r = min(r0 + rl, g.rm.rows - 1);
       if constexpr (EK == E_QKV) sh.kv[rl] = g.kv.prefill ? prefill_kv_slot(g.kv, r) : g.kv.slot_base[r];
-      if constexpr (EK == E_RESID) sh.keep[rl] = !g.keep_depth || g.keep_depth[r] > g.keep_loop;
+      if constexpr (EK == E_RESID) {
+        sh.keep[rl] = !g.keep_depth || g.keep_depth[r] > g.keep_loop;
+        sh.moff[rl] = g.mod_a && r0 + rl < a_rows ? (mod_row_depth(g, r) - 1) * g.mod_ld : 0;
+      }
       if constexpr (EK == E_LOGITS) sh.orow[rl] = g.rm.src ? g.rm.src[r] : g.out_row_off + r;
     }
   }
@@ -137,6 +146,15 @@ __device__ __forceinline__ void dgemm_tile(const GemmArgs& g, int nact, int act_
     const int arow = (AK == A_SRC) ? row_src(g.rm, r) : r;
     ao[i] = arow * g.lda + quad * EPL;
   }
+  // MOD: the lane's rows are scaled by (1 + gamma) of their modulation rows
+  int go[MOD ? RM : 1];
+  if constexpr (MOD) {
+#pragma unroll
+    for (int i = 0; i < RM; ++i) {
+      const int r = r0 + i * 16 + c16;
+      go[i] = (r < a_rows ? (mod_row_depth(g, r) - 1) * g.mod_ld : 0) + quad * EPL;
+    }
+  }
 
   const int S = g.K / KS;              // K steps
   const int NJ = (S - w + W - 1) / W;  // steps of this wave (w, w + W, ...)
@@ -151,6 +169,7 @@ __device__ __forceinline__ void dgemm_tile(const GemmArgs& g, int nact, int act_
 
   for (int jb = 0; jb < (S + W - 1) / W; jb += KB) {
     float av[KB][RM][EPL];
+    float gv[MOD ? KB : 1][RM][EPL];
     Frag bw[KB][CN];
     // past this wave's last step the last step is reread (its product is skipped)
 #pragma unroll
@@ -166,6 +185,10 @@ __device__ __forceinline__ void dgemm_tile(const GemmArgs& g, int nact, int act_
       for (int i = 0; i < RM; ++i) {
 #pragma unroll
         for (int e = 0; e < EPL; ++e) av[j][i][e] = 0.f;
+        if constexpr (MOD) {
+#pragma unroll
+          for (int e = 0; e < EPL; ++e) gv[j][i][e] = 0.f;
+        }
         if (r0 + i * 16 >= a_rows) continue;  // uniform: the fragment's rows have exited
         if (r0 + i * 16 + c16 < a_rows) {
           if constexpr (EPL == 8) {
@@ -173,8 +196,15 @@ __device__ __forceinline__ void dgemm_tile(const GemmArgs& g, int nact, int act_
             const float4 hi = *reinterpret_cast<const float4*>(Ab + (ao[i] + k0 + 4));
             av[j][i][0] = lo.x; av[j][i][1] = lo.y; av[j][i][2] = lo.z; av[j][i][3] = lo.w;
             av[j][i][4] = hi.x; av[j][i][5] = hi.y; av[j][i][6] = hi.z; av[j][i][7] = hi.w;
+            if constexpr (MOD) {
+              const float4 glo = *reinterpret_cast<const float4*>(g.mod_g + (go[i] + k0));
+              const float4 ghi = *reinterpret_cast<const float4*>(g.mod_g + (go[i] + k0 + 4));
+              gv[j][i][0] = glo.x; gv[j][i][1] = glo.y; gv[j][i][2] = glo.z; gv[j][i][3] = glo.w;
+              gv[j][i][4] = ghi.x; gv[j][i][5] = ghi.y; gv[j][i][6] = ghi.z; gv[j][i][7] = ghi.w;
+            }
           } else {
             av[j][i][0] = Ab[ao[i] + k0];
+            if constexpr (MOD) gv[j][i][0] = g.mod_g[go[i] + k0];
           }
         }
       }
@@ -198,6 +228,11 @@ __device__ __forceinline__ void dgemm_tile(const GemmArgs& g, int nact, int act_
         if constexpr (NORM) {
 #pragma unroll
           for (int e = 0; e < EPL; ++e) ss[i] = fmaf(av[j][i][e], av[j][i][e], ss[i]);
+        }
+        if constexpr (MOD) {
+          // RMSNorm(x) (1 + gamma): the norm's sum of squares above takes x itself
+#pragma unroll
+          for (int e = 0; e < EPL; ++e) av[j][i][e] *= 1.f + gv[j][i][e];
         }
         if constexpr (kSplit) {
           uint2 h0, l0, h1, l1;
@@ -311,7 +346,10 @@ __device__ __forceinline__ void dgemm_tile(const GemmArgs& g, int nact, int act_
       if (r0 + row >= row_end || n >= g.N) continue;
       const float v = tile_sum(row, col);
       if constexpr (EK == E_RESID) {
-        if (sh.keep[row]) g.out[(int64_t)xrow[k] * g.ldo + n] = xr[k] + v;
+        if (sh.keep[row]) {
+          const float gate = g.mod_a ? 1.f + g.mod_a[sh.moff[row] + n] : 1.f;
+          g.out[(int64_t)xrow[k] * g.ldo + n] = xr[k] + gate * v;
+        }
       } else if constexpr (EK == E_HIDDEN) {
         const float u = v + g.bias[n];
         g.out[(int64_t)(r0 + row) * g.ldo + n] = u / (1.f + __expf(-u));
@@ -344,7 +382,7 @@ template <int RM, int CN> struct Shape {
   static constexpr int BM = RM * 16, BN = CN * 16;
 };
 
-template <typename T, int RMn, int CNn, int RMw, int CNw, int W, int KB, int AK, int EK, bool NORM>
+template <typename T, int RMn, int CNn, int RMw, int CNw, int W, int KB, int AK, int EK, bool NORM, bool MOD>
 __global__ __launch_bounds__(W * 64) void k_dgemm(GemmArgs g, int wide_above) {
   constexpr int SLOTS = W > 8 ? 8 : W;
   constexpr int BMX = RMn > RMw ? RMn * 16 : RMw * 16;
@@ -355,19 +393,20 @@ __global__ __launch_bounds__(W * 64) void k_dgemm(GemmArgs g, int wide_above) {
   __shared__ int s_orow[EK == E_LOGITS ? BMX : 1];
   __shared__ int64_t s_kv[EK == E_QKV ? BMX : 1];
   __shared__ int s_keep[EK == E_RESID ? BMX : 1];
-  const DgemmShared sh{red, s_ss, s_inv, s_orow, s_kv, s_keep};
+  __shared__ int s_moff[EK == E_RESID ? BMX : 1];
+  const DgemmShared sh{red, s_ss, s_inv, s_orow, s_kv, s_keep, s_moff};
   const int nact = g.rm.nact ? *g.rm.nact : g.rm.rows;
   const int act_rows = g.spec ? g.rm.rows : min(nact, g.rm.rows);
   if constexpr (RMn != RMw || CNn != CNw) {
     if (act_rows > wide_above) {
-      dgemm_tile<T, RMw, CNw, W, KB, AK, EK, NORM>(g, nact, act_rows, sh);
+      dgemm_tile<T, RMw, CNw, W, KB, AK, EK, NORM, MOD>(g, nact, act_rows, sh);
       return;
     }
   }
-  dgemm_tile<T, RMn, CNn, W, KB, AK, EK, NORM>(g, nact, act_rows, sh);
+  dgemm_tile<T, RMn, CNn, W, KB, AK, EK, NORM, MOD>(g, nact, act_rows, sh);
 }
 
-template <typename T, int RMn, int CNn, int RMw, int CNw, int W, int KB, int AK, int EK, bool NORM>
+template <typename T, int RMn, int CNn, int RMw, int CNw, int W, int KB, int AK, int EK, bool NORM, bool MOD>
 hipError_t launch_cfg(const GemmArgs& a, int cus, hipStream_t s) {
   constexpr int BMn = RMn * 16, BNn = CNn * 16, BMw = RMw * 16, BNw = CNw * 16;
   const int tn_n = (a.N + BNn - 1) / BNn, tm_n = (a.rm.rows + BMn - 1) / BMn;
@@ -377,20 +416,21 @@ hipError_t launch_cfg(const GemmArgs& a, int cus, hipStream_t s) {
   const int wide_above = (RMn == RMw && CNn == CNw) ? a.rm.rows : std::max(1, cus / tn_n) * BMn;
   const int tiles = std::max(tn_n * tm_n, tn_w * tm_w);
   const int grid = kXcds * ((tiles + kXcds - 1) / kXcds);
-  hipLaunchKernelGGL((k_dgemm<T, RMn, CNn, RMw, CNw, W, KB, AK, EK, NORM>), dim3(grid), dim3(W * 64), 0, s, a,
+  hipLaunchKernelGGL((k_dgemm<T, RMn, CNn, RMw, CNw, W, KB, AK, EK, NORM, MOD>), dim3(grid), dim3(W * 64), 0, s, a,
                      wide_above);
   return hipGetLastError();
 }
 
 // K steps per wave in one batch of loads: all of a wave's steps when they
 // fit in KBMAX, else batches of KBMAX.
-template <typename T, int RMn, int CNn, int RMw, int CNw, int W, int KBMAX, int AK, int EK, bool NORM>
+template <typename T, int RMn, int CNn, int RMw, int CNw, int W, int KBMAX, int AK, int EK, bool NORM,
+          bool MOD = false>
 hipError_t launch_w(const GemmArgs& a, int cus, hipStream_t s) {
   const int nj = (a.K / Mfma<T>::KS + W - 1) / W;
-  if (nj <= 2 || KBMAX == 2) return launch_cfg<T, RMn, CNn, RMw, CNw, W, 2, AK, EK, NORM>(a, cus, s);
+  if (nj <= 2 || KBMAX == 2) return launch_cfg<T, RMn, CNn, RMw, CNw, W, 2, AK, EK, NORM, MOD>(a, cus, s);
   if (nj <= 3 || KBMAX == 3)
-    return launch_cfg<T, RMn, CNn, RMw, CNw, W, (KBMAX >= 3 ? 3 : 2), AK, EK, NORM>(a, cus, s);
-  return launch_cfg<T, RMn, CNn, RMw, CNw, W, (KBMAX >= 4 ? 4 : 2), AK, EK, NORM>(a, cus, s);
+    return launch_cfg<T, RMn, CNn, RMw, CNw, W, (KBMAX >= 3 ? 3 : 2), AK, EK, NORM, MOD>(a, cus, s);
+  return launch_cfg<T, RMn, CNn, RMw, CNw, W, (KBMAX >= 4 ? 4 : 2), AK, EK, NORM, MOD>(a, cus, s);
 }
 
 }  // namespace
@@ -408,14 +448,23 @@ hipError_t launch_w(const GemmArgs& a, int cus, hipStream_t s) {
 template <typename T>
 hipError_t launch_dgemm(const GemmArgs& a, AKind ak, EKind ek, bool norm, int cus, hipStream_t s) {
   if (a.K % Mfma<T>::KS != 0 || a.rm.rows <= 0 || cus <= 0) return hipErrorInvalidValue;
+  const bool mod = a.mod_g != nullptr;
   if (ek == E_QKV && norm) {
-    if (ak == A_SRC) return launch_w<T, 2, 4, 2, 5, 8, 3, A_SRC, E_QKV, true>(a, cus, s);
-    return launch_w<T, 2, 4, 2, 5, 8, 3, A_CMP, E_QKV, true>(a, cus, s);
+    if (ak == A_SRC)
+      return mod ? launch_w<T, 2, 4, 2, 5, 8, 3, A_SRC, E_QKV, true, true>(a, cus, s)
+                 : launch_w<T, 2, 4, 2, 5, 8, 3, A_SRC, E_QKV, true>(a, cus, s);
+    return mod ? launch_w<T, 2, 4, 2, 5, 8, 3, A_CMP, E_QKV, true, true>(a, cus, s)
+               : launch_w<T, 2, 4, 2, 5, 8, 3, A_CMP, E_QKV, true>(a, cus, s);
   }
   if (ek == E_SWIGLU && norm) {
-    if (ak == A_SRC) return launch_w<T, 2, 4, 2, 8, 8, 3, A_SRC, E_SWIGLU, true>(a, cus, s);
-    return launch_w<T, 2, 4, 2, 8, 8, 3, A_CMP, E_SWIGLU, true>(a, cus, s);
+    // with the gamma operands, two K batches in flight (three would spill)
+    if (ak == A_SRC)
+      return mod ? launch_w<T, 2, 4, 2, 8, 8, 2, A_SRC, E_SWIGLU, true, true>(a, cus, s)
+                 : launch_w<T, 2, 4, 2, 8, 8, 3, A_SRC, E_SWIGLU, true>(a, cus, s);
+    return mod ? launch_w<T, 2, 4, 2, 8, 8, 2, A_CMP, E_SWIGLU, true, true>(a, cus, s)
+               : launch_w<T, 2, 4, 2, 8, 8, 3, A_CMP, E_SWIGLU, true>(a, cus, s);
   }
+  if (mod) return hipErrorInvalidValue;  // the operand scale is for the normalised projections
   if (ek == E_LOGITS && norm) {
     if (ak == A_SRC) return launch_w<T, 2, 4, 2, 4, 8, 3, A_SRC, E_LOGITS, true>(a, cus, s);
     return launch_w<T, 2, 4, 2, 4, 8, 3, A_CMP, E_LOGITS, true>(a, cus, s);

@@ -28,7 +28,8 @@ __device__ __forceinline__ unsigned int ordered_bits(float v) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
-template <typename T, int MT, int NT, int PF, int BK, int AK, int EK>
+// MOD: the A rows are scaled by (1 + gamma) of their AdaLN modulation rows.
+template <typename T, int MT, int NT, int PF, int BK, int AK, int EK, bool MOD>
 __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
   constexpr int BM = 2 * MT * 16, BN = 2 * NT * 16;
   constexpr bool kSplit = sizeof(T) == 2;            // bf16 weights: A as hi + lo parts
@@ -48,6 +49,7 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
   __shared__ __align__(16) T As[NA][BM * LDK];
   __shared__ __align__(16) T Bs[BN * LDK];
   __shared__ int row_src_s[BM];
+  __shared__ int row_mod_s[BM];  // modulation row offset (AdaLN), 0 without
   __shared__ int64_t kv_base[EK == E_QKV ? BM : 1];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -68,6 +70,7 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
   };
 
   float4 ra[PF][ACH];
+  float4 rg[MOD ? PF : 1][MOD ? ACH : 1];  // gamma of the A chunks in flight
   V16<T> rb[PF][BCH];  // ring of PF K tiles in flight
   const float* A = reinterpret_cast<const float*>(g.A);
   const T* W = reinterpret_cast<const T*>(g.W);
@@ -82,31 +85,37 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
       rb[c] = ld16(W + (int64_t)w_row(n0 + row) * g.K + kk + col);
     }
   };
-  auto load_a = [&](int kt, float4* ra) {
+  auto load_a = [&](int kt, float4* ra, float4* rg) {
     const int kk = k_base + kt * BK;
 #pragma unroll
     for (int c = 0; c < ACH; ++c) {
       const int ch = tid + c * 256, row = ch / ACR, col = (ch % ACR) * 4;
       const int s = row_src_s[row];
-      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+      float4 v = make_float4(0.f, 0.f, 0.f, 0.f), gm = v;
       if (s >= 0) {
         const int64_t ar = (AK == A_SRC) ? (int64_t)s : (int64_t)(r0 + row);
         v = *reinterpret_cast<const float4*>(A + ar * g.lda + kk + col);
+        if constexpr (MOD) gm = *reinterpret_cast<const float4*>(g.mod_g + row_mod_s[row] + kk + col);
       }
       ra[c] = v;
+      if constexpr (MOD) rg[c] = gm;
     }
   };
-  auto store_tiles = [&](const float4* ra, const V16<T>* rb) {
+  auto store_tiles = [&](const float4* ra, const float4* rg, const V16<T>* rb) {
 #pragma unroll
     for (int c = 0; c < ACH; ++c) {
       const int ch = tid + c * 256, row = ch / ACR, col = (ch % ACR) * 4;
+      float4 av = ra[c];
+      if constexpr (MOD)
+        av = make_float4(av.x * (1.f + rg[c].x), av.y * (1.f + rg[c].y), av.z * (1.f + rg[c].z),
+                         av.w * (1.f + rg[c].w));
       if constexpr (kSplit) {
         uint2 hi, lo;
-        split4(ra[c], hi, lo);
+        split4(av, hi, lo);
         *reinterpret_cast<uint2*>(&As[0][row * LDK + col]) = hi;
         *reinterpret_cast<uint2*>(&As[NA - 1][row * LDK + col]) = lo;
       } else {
-        *reinterpret_cast<float4*>(&As[0][row * LDK + col]) = ra[c];
+        *reinterpret_cast<float4*>(&As[0][row * LDK + col]) = av;
       }
     }
 #pragma unroll
@@ -130,13 +139,15 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
     const int r = r0 + tid;
     if (row_active(g.rm, r)) my_src = row_src(g.rm, r);
     row_src_s[tid] = my_src;
+    row_mod_s[tid] = (g.mod_depth && my_src >= 0)
+                         ? (g.mod_depth[g.mod_by_src ? my_src : r] - 1) * g.mod_ld : 0;
     if constexpr (EK == E_QKV)
       if (my_src >= 0) my_kv = prefill_kv_slot(g.kv, r);
   }
   if (!__syncthreads_or(my_src >= 0)) return;
 
 #pragma unroll
-  for (int p = 0; p < PF; ++p) load_a(min(p, KT - 1), ra[p]);
+  for (int p = 0; p < PF; ++p) load_a(min(p, KT - 1), ra[p], rg[MOD ? p : 0]);
 
   f32x4 acc[MT][NT];
 #pragma unroll
@@ -152,10 +163,10 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
       const int kt = kt0 + p;
       if (kt >= KT) break;
       __syncthreads();
-      store_tiles(ra[p], rb[p]);
+      store_tiles(ra[p], rg[MOD ? p : 0], rb[p]);
       __syncthreads();
       load_b(min(kt + PF, KT - 1), rb[p]);
-      load_a(min(kt + PF, KT - 1), ra[p]);
+      load_a(min(kt + PF, KT - 1), ra[p], rg[MOD ? p : 0]);
 #pragma unroll
       for (int ks = 0; ks < BK / KS; ++ks) {
         typename M::frag af[NA][MT], bfr[NT];
@@ -228,7 +239,8 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
           if (src < 0 || n >= g.N) continue;
           const float v = acc[i][j][r];
           if constexpr (EK == E_RESID) {
-            reinterpret_cast<float*>(g.out)[(int64_t)src * g.ldo + n] += v;
+            const float gate = g.mod_a ? 1.f + g.mod_a[row_mod_s[rl] + n] : 1.f;
+            reinterpret_cast<float*>(g.out)[(int64_t)src * g.ldo + n] += gate * v;
           } else if constexpr (EK == E_HIDDEN) {
             const float u = v + g.bias[n];
             g.out[(int64_t)rg * g.ldo + n] = u / (1.f + __expf(-u));
@@ -261,16 +273,19 @@ hipError_t launch_tiles(const GemmArgs& a, AKind ak, EKind ek, hipStream_t s) {
   constexpr int BM = 2 * MT * 16, BN = 2 * NT * 16;
   const dim3 grid((a.N + BN - 1) / BN, (a.rm.rows + BM - 1) / BM);
   if (grid.x == 0 || grid.y == 0) return hipSuccess;
-#define TLF_GEMM_CASE(AKV, EKV)                                                       \
-  if (ak == AKV && ek == EKV) {                                                       \
-    hipLaunchKernelGGL((k_gemm<T, MT, NT, PF, BK, AKV, EKV>), grid, dim3(256), 0, s, a);  \
-    return hipGetLastError();                                                         \
+  const bool mod = a.mod_g != nullptr;
+#define TLF_GEMM_CASE(AKV, EKV, MODV)                                                          \
+  if (ak == AKV && ek == EKV && mod == MODV) {                                                 \
+    hipLaunchKernelGGL((k_gemm<T, MT, NT, PF, BK, AKV, EKV, MODV>), grid, dim3(256), 0, s, a); \
+    return hipGetLastError();                                                                  \
   }
-  TLF_GEMM_CASE(A_SRC, E_QKV)
-  TLF_GEMM_CASE(A_SRC, E_SWIGLU)
-  TLF_GEMM_CASE(A_SRC, E_LOGITS)
-  TLF_GEMM_CASE(A_CMP, E_RESID)
-  TLF_GEMM_CASE(A_CMP, E_HIDDEN)
+  TLF_GEMM_CASE(A_SRC, E_QKV, false)
+  TLF_GEMM_CASE(A_SRC, E_QKV, true)
+  TLF_GEMM_CASE(A_SRC, E_SWIGLU, false)
+  TLF_GEMM_CASE(A_SRC, E_SWIGLU, true)
+  TLF_GEMM_CASE(A_SRC, E_LOGITS, false)
+  TLF_GEMM_CASE(A_CMP, E_RESID, false)
+  TLF_GEMM_CASE(A_CMP, E_HIDDEN, false)
 #undef TLF_GEMM_CASE
   return hipErrorInvalidValue;
 }

@@ -90,6 +90,13 @@ struct GemmArgs {
   const float* bias = nullptr;  // E_HIDDEN: [N] float32
   int spec = 0;             // decode: every row is active; loads need not wait for the active count
   int scatter = 0;          // E_RESID: the residual row of row r is src(r) (prefill), not r
+  // AdaLN (Section 3.1, Appendix A): row r's modulation row sits at
+  // (depth(r) - 1) * mod_ld, depth(r) = mod_depth[mod_by_src ? src(r) : r]
+  const float* mod_g = nullptr;  // QKV, gate/up: the operand row is scaled by (1 + mod_g[k])
+  const float* mod_a = nullptr;  // E_RESID: out = x + (1 + mod_a[n]) * result
+  int mod_ld = 0;
+  const int32_t* mod_depth = nullptr;
+  int mod_by_src = 0;
   const int32_t* keep_depth = nullptr;  // E_RESID (dense decode): row r is stored only while
   int keep_loop = 0;                    // keep_depth[r] > keep_loop (its token runs this loop)
 };
@@ -174,6 +181,7 @@ struct DecodePlanArgs {
                                    // slot that compact row k appends at loop i
   unsigned long long* argmax_keys = nullptr; // [B] cleared for the LM head
   int64_t kv_entry_bytes = 0;      // bytes of one (token, loop) cache entry over all layers
+  int32_t* row_depth = nullptr;    // [B] depth of the token of compact row k
   int dense = 0;                   // 1: rows in batch order, every loop up to the deepest token
                                    // runs all B rows; exited rows get kv_slot -1
 };
@@ -226,5 +234,23 @@ template <typename T> hipError_t launch_attn_prefill(const AttnPrefillArgs& a, h
 hipError_t launch_fill_i32(int32_t* p, int32_t v, int64_t n, hipStream_t s);
 hipError_t launch_fill_u64(unsigned long long* p, unsigned long long v, int64_t n, hipStream_t s);
 hipError_t launch_argmax_finalize(const unsigned long long* keys, int32_t* next, int B, hipStream_t s);
+
+// ---------------------------------------------------------------------------
+// AdaLN conditioning table: modulation of every (layer, loop, depth),
+// table[j][i][m][4d] (0-based loop i and depth m + 1), rows alpha_msa |
+// alpha_mlp | gamma_msa | gamma_mlp.  Matrices in the storage dtype.
+// ---------------------------------------------------------------------------
+struct CondWeights {
+  const void* w1[2] = {nullptr, nullptr};  // time, step: [d][256]
+  const float* b1[2] = {nullptr, nullptr};
+  const void* w2[2] = {nullptr, nullptr};  // [d][d]
+  const float* b2[2] = {nullptr, nullptr};
+  const void* const* mod_w = nullptr;      // host array of J: [4d][d]
+  const float* const* mod_b = nullptr;     // host array of J: [4d]
+};
+size_t cond_scratch_floats(int R, int d);
+template <typename T>
+hipError_t launch_cond_table(const CondWeights& w, int J, int R, int d, float* table, float* scratch,
+                             hipStream_t s);
 
 }  // namespace tlf

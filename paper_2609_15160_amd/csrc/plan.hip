@@ -82,6 +82,7 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan_decode(DecodePlanArgs a) 
       const int row = a.dense ? b : start[m] + fill[m] + off + rank;
       row_of[ch] = row;
       a.perm[row] = b;
+      if (a.row_depth) a.row_depth[row] = m;
     }
     __syncthreads();
     if (tid >= 1 && tid <= R) {

@@ -15,7 +15,7 @@ PKG_DIR = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG_DIR, "libtlf.so")
 HEADER = os.path.join(os.path.dirname(PKG_DIR), "include", "tlf.h")
 
-ABI_VERSION = 3
+ABI_VERSION = 4
 MAX_LOOPS = 16
 MAX_LAYERS = 8
 PAGE_TOKENS = 16
@@ -47,7 +47,7 @@ class Config(ctypes.Structure):
         ("max_pages", ctypes.c_int32), ("max_prefill_tokens", ctypes.c_int32),
         ("route_rule", ctypes.c_int32), ("route_threshold", ctypes.c_float),
         ("fixed_depth", ctypes.c_int32), ("rms_eps", ctypes.c_float), ("decode_graph", ctypes.c_int32),
-        ("router_hidden", ctypes.c_int32), ("dense_decode", ctypes.c_int32),
+        ("router_hidden", ctypes.c_int32), ("dense_decode", ctypes.c_int32), ("adaln", ctypes.c_int32),
     ]
 
 
@@ -56,11 +56,21 @@ class LayerWeights(ctypes.Structure):
                 ("w_gate_up", ctypes.c_void_p), ("w_down", ctypes.c_void_p)]
 
 
+class AdalnWeights(ctypes.Structure):
+    _fields_ = [
+        ("time_w1", ctypes.c_void_p), ("time_b1", ctypes.c_void_p), ("time_w2", ctypes.c_void_p),
+        ("time_b2", ctypes.c_void_p), ("step_w1", ctypes.c_void_p), ("step_b1", ctypes.c_void_p),
+        ("step_w2", ctypes.c_void_p), ("step_b2", ctypes.c_void_p),
+        ("mod_w", ctypes.POINTER(ctypes.c_void_p)), ("mod_b", ctypes.POINTER(ctypes.c_void_p)),
+    ]
+
+
 class Weights(ctypes.Structure):
     _fields_ = [
         ("tok_emb", ctypes.c_void_p), ("pos_emb", ctypes.c_void_p), ("router_w", ctypes.c_void_p),
         ("router_b", ctypes.c_void_p), ("lm_head", ctypes.c_void_p), ("n_layers", ctypes.c_int32),
         ("layers", ctypes.POINTER(LayerWeights)), ("router_w1", ctypes.c_void_p), ("router_b1", ctypes.c_void_p),
+        ("adaln", ctypes.POINTER(AdalnWeights)),
     ]
 
 
@@ -145,7 +155,7 @@ def make_config(model, max_batch: int, max_pos: int, max_pages: int, route_rule:
         max_prefill_tokens=max_prefill_tokens, route_rule=ROUTE[route_rule],
         route_threshold=threshold, fixed_depth=fixed_depth, rms_eps=model.rms_eps,
         decode_graph=1 if decode_graph else 0, router_hidden=getattr(model, "router_hidden", 0),
-        dense_decode=1 if dense_decode else 0)
+        dense_decode=1 if dense_decode else 0, adaln=1 if getattr(model, "adaln", False) else 0)
 
 
 def workspace_bytes(cfg: Config) -> int:
@@ -203,12 +213,27 @@ class Session:
         self._lw = (LayerWeights * len(self.layers))(*[
             LayerWeights(l["w_qkv"].data_ptr(), l["w_o"].data_ptr(), l["w_gate_up"].data_ptr(),
                          l["w_down"].data_ptr()) for l in self.layers])
+        adaln = None
+        if weights.get("cond") is not None:
+            cond = weights["cond"]
+            self.cond = {k: dev(cond[k], sdt if k.endswith(("_w1", "_w2")) else torch.float32)
+                         for k in ("time_w1", "time_b1", "time_w2", "time_b2",
+                                   "step_w1", "step_b1", "step_w2", "step_b2")}
+            self.mods = [(dev(lw["w_mod"], sdt), dev(lw["b_mod"], torch.float32)) for lw in weights["layers"]]
+            J = len(self.mods)
+            self._mod_w = (ctypes.c_void_p * J)(*[m[0].data_ptr() for m in self.mods])
+            self._mod_b = (ctypes.c_void_p * J)(*[m[1].data_ptr() for m in self.mods])
+            self._adaln = AdalnWeights(*[self.cond[k].data_ptr() for k in (
+                "time_w1", "time_b1", "time_w2", "time_b2", "step_w1", "step_b1", "step_w2", "step_b2")],
+                ctypes.cast(self._mod_w, ctypes.POINTER(ctypes.c_void_p)),
+                ctypes.cast(self._mod_b, ctypes.POINTER(ctypes.c_void_p)))
+            adaln = ctypes.pointer(self._adaln)
         self._weights = Weights(self.w["tok_emb"].data_ptr(), self.w["pos_emb"].data_ptr(),
                                 self.w["router_w"].data_ptr(), self.w["router_b"].data_ptr(),
                                 self.w["lm_head"].data_ptr() if "lm_head" in self.w else None,
                                 len(self.layers), self._lw,
                                 self.w["router_w1"].data_ptr() if "router_w1" in self.w else None,
-                                self.w["router_b1"].data_ptr() if "router_b1" in self.w else None)
+                                self.w["router_b1"].data_ptr() if "router_b1" in self.w else None, adaln)
         need = workspace_bytes(self.cfg)
         self.workspace = torch.empty(need, dtype=torch.uint8, device=self.device)
         self.stream = torch.cuda.current_stream(self.device)

@@ -72,11 +72,11 @@ def test_size_query_needs_no_device(lib):
 
 
 @pytest.mark.parametrize("field,value", [
-    ("abi_version", 2), ("abi_version", 4), ("dtype", 7), ("vocab", 0), ("d_model", 100), ("head_dim", 32),
+    ("abi_version", 3), ("abi_version", 5), ("dtype", 7), ("vocab", 0), ("d_model", 100), ("head_dim", 32),
     ("n_heads", 5), ("d_ff", 1000), ("n_layers", 0), ("n_layers", 9), ("max_loops", 0),
     ("max_loops", 17), ("max_pos", 0), ("max_batch", 0), ("max_batch", 5000), ("page_tokens", 32),
     ("max_pages", 0), ("max_prefill_tokens", 0), ("route_rule", 5), ("rms_eps", 0.0),
-    ("router_hidden", -64), ("router_hidden", 96), ("router_hidden", 8192), ("dense_decode", 2),
+    ("router_hidden", -64), ("router_hidden", 96), ("router_hidden", 8192), ("dense_decode", 2), ("adaln", 2),
     ("dense_decode", -1),
 ])
 def test_invalid_config_rejected(lib, field, value):
@@ -135,6 +135,35 @@ def test_mlp_router_weights_must_match_the_config(lib):
         st = lib.tlf_init(ctypes.byref(cc), ctypes.byref(w), fake, 1 << 62, ctypes.byref(need), None,
                           ctypes.byref(ctx))
         assert st == tlf.E_INVALID_ARG and not ctx.value
+
+
+def test_adaln_weights_must_match_the_config(lib):
+    """adaln = 1 needs every conditioning pointer (one modulator per layer) and
+    takes workspace for its table; adaln = 0 must not get them."""
+    need = ctypes.c_size_t(0)
+    c0 = _cfg()
+    assert lib.tlf_init(ctypes.byref(c0), None, None, 0, ctypes.byref(need), None, None) == tlf.E_NEED_WORKSPACE
+    plain = need.value
+    c = _cfg(adaln=1)
+    assert lib.tlf_init(ctypes.byref(c), None, None, 0, ctypes.byref(need), None, None) == tlf.E_NEED_WORKSPACE
+    # table [J][R][R][4d] float32 plus its set-up scratch
+    assert need.value >= plain + c.n_layers * c.max_loops ** 2 * 4 * c.d_model * 4
+    fake = ctypes.c_void_p(1 << 20)  # never dereferenced: validation fails first
+    lw = (tlf.LayerWeights * c.n_layers)(*[tlf.LayerWeights(fake, fake, fake, fake) for _ in range(c.n_layers)])
+    mods = (ctypes.c_void_p * c.n_layers)(*([fake.value] * c.n_layers))
+    holes = (ctypes.c_void_p * c.n_layers)(*([fake.value] * (c.n_layers - 1) + [None]))
+    P = ctypes.POINTER(ctypes.c_void_p)
+    full = tlf.AdalnWeights(*([fake] * 8), ctypes.cast(mods, P), ctypes.cast(mods, P))
+    missing_layer = tlf.AdalnWeights(*([fake] * 8), ctypes.cast(mods, P), ctypes.cast(holes, P))
+    missing_bias = tlf.AdalnWeights(*([fake] * 7), None, ctypes.cast(mods, P), ctypes.cast(mods, P))
+    for flag, aw in ((1, None), (0, full), (1, missing_layer), (1, missing_bias)):
+        cc = _cfg(adaln=flag)
+        w = tlf.Weights(fake, fake, fake, fake, None, cc.n_layers, lw, None, None,
+                        ctypes.pointer(aw) if aw is not None else None)
+        ctx = ctypes.c_void_p()
+        st = lib.tlf_init(ctypes.byref(cc), ctypes.byref(w), fake, 1 << 62, ctypes.byref(need), None,
+                          ctypes.byref(ctx))
+        assert st == tlf.E_INVALID_ARG and not ctx.value, (flag, aw)
 
 
 def test_null_context_calls(lib):

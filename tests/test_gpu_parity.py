@@ -439,6 +439,50 @@ def test_bf16_dense_decode_sampled_sequences():
 
 
 # ---------------------------------------------------------------------------
+# AdaLN time/step conditioning: every row gathers the modulation of its own
+# (loop, depth) pair
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("variant", ["routed", "fixed4", "dense", "single-sequence"])
+def test_f32_adaln_parity(variant):
+    kw = dict(adaln=True, steps=12)
+    if variant == "single-sequence":
+        kw.update(batch=1, prompt_len=90)
+    m = _f32_small(**kw)
+    w = synth.make_weights(m)
+    prompts = synth.make_prompts(m)
+    rule = dict(route_rule="fixed", fixed_depth=4) if variant == "fixed4" else {}
+    g = parity.run_gpu(m, w, prompts, m.steps, dense_decode=variant == "dense", **rule)
+    o = parity.run_oracle(m, w, prompts, g.step_tokens, **rule)
+    _check_f32(m, w, prompts, g, o, f"f32-adaln-{variant}")
+
+
+def test_f32_adaln_chunked_prefill_equals_one_shot():
+    L = _schedule_len(SCHEDULE)
+    m = _f32_small(batch=2, prompt_len=L, steps=0, adaln=True)
+    w = synth.make_weights(m)
+    tokens = synth.make_prompts(m, prompt_len=L)
+    g = parity.run_gpu_schedule(m, w, tokens, SCHEDULE)
+    o = _oracle_one_shot(m, w, tokens)
+    assert np.array_equal(g.depths, o.prefill_depths)
+    err = _max_err(g.logits, o.prefill_logits)
+    _report("f32-adaln-chunked", max_abs_logit_err=f"{err:.3g}")
+    assert err <= F32_TOL
+
+
+@pytest.mark.parametrize("batch", [8, 1])
+def test_bf16_adaln_sampled_sequences(batch):
+    base = synth.CONFIGS["bf16_d768_b32x512"].replace(adaln=True)
+    m = base.replace(batch=batch, prompt_len=96, steps=10)
+    w = synth.make_weights(base)
+    prompts = synth.make_prompts(m)
+    sample = [0, 5] if batch > 1 else [0]
+    g = parity.run_gpu(m, w, prompts, m.steps, max_pos=m.max_pos, keep_logits_rows=sample)
+    o = parity.run_oracle(m, w, prompts[sample], [t[sample] for t in g.step_tokens])
+    _check_bf16(m, w, prompts, g, o, sample, f"bf16-adaln-B{batch}")
+
+
+# ---------------------------------------------------------------------------
 # Error handling through the C ABI
 # ---------------------------------------------------------------------------
 
