@@ -240,7 +240,7 @@ int run_mlp_router(tlf_ctx* ctx, hipStream_t s, const float* h0, int rows, bool 
   g.A = h0; g.lda = c.d_model; g.W = ctx->w.router_w1; g.N = Hr; g.K = c.d_model; g.w_rows = Hr;
   g.rm.rows = rows; g.out = hid; g.ldo = Hr; g.bias = ctx->w.router_b1; g.spec = 1;
   if (decode_shape) TLF_HIP(launch_dgemm<T>(g, A_CMP, E_HIDDEN, false, ctx->cus, s));
-  else TLF_HIP(launch_gemm<T>(g, A_CMP, E_HIDDEN, s));
+  else TLF_HIP(launch_gemm<T>(g, A_CMP, E_HIDDEN, false, s));
   RouteArgs ra;
   ra.h = hid; ra.rows = rows; ra.Hr = Hr; ra.R = c.max_loops; ra.Wr = ctx->w.router_w; ra.br = ctx->w.router_b;
   ra.depth = depth; ra.out_depth = out_depth; ra.out_margin = out_margin;
@@ -256,6 +256,9 @@ int attn_waves(const tlf_ctx* ctx) {
   const int64_t slots = (int64_t)ctx->cus * ctx->attn_blocks[0] * 4;  // resident waves with 4-wave groups
   return units * 4 >= slots ? 4 : 8;
 }
+
+// Decode batches of at least this many rows run the LM head on the 128 x 128 GEMM.
+constexpr int kHeadGemmRows = 128;
 
 // Prefill of a single sequence of at most this many tokens runs its
 // projections on the split-K decode GEMM.
@@ -341,7 +344,7 @@ int run_prefill(tlf_ctx* ctx, int B, int T_, int pos0, const int32_t* tokens, fl
         q.kv.c = ctx->cv; q.kv.loop = i; q.kv.layer = j; q.kv.prefill = 1; q.kv.b0 = b0; q.kv.seg = T_;
         set_mod(ctx, &q, i, j, 2, pre_depth, 1);
         if (few) TLF_HIP(launch_dgemm<T>(q, A_SRC, E_QKV, true, ctx->cus, s));
-        else TLF_HIP(launch_gemm<T>(q, A_SRC, E_QKV, s));
+        else TLF_HIP(launch_gemm<T>(q, A_SRC, E_QKV, false, s));
 
         AttnPrefillArgs at;
         at.c = ctx->cv; at.loop = i; at.layer = j; at.d = d; at.b0 = b0; at.G = Gc; at.T = T_;
@@ -356,7 +359,7 @@ int run_prefill(tlf_ctx* ctx, int B, int T_, int pos0, const int32_t* tokens, fl
         if (few) {
           TLF_HIP(launch_dgemm<T>(o, A_CMP, E_RESID, false, ctx->cus, s));
         } else {
-          TLF_HIP(launch_gemm<T>(o, A_CMP, E_RESID, s));
+          TLF_HIP(launch_gemm<T>(o, A_CMP, E_RESID, false, s));
           TLF_HIP(launch_resid_norm<T>(rn, s));
         }
 
@@ -365,7 +368,7 @@ int run_prefill(tlf_ctx* ctx, int B, int T_, int pos0, const int32_t* tokens, fl
         gu.out = ctx->buf<float>(B_ACT_PRE); gu.ldo = F; gu.F = F; gu.eps = c.rms_eps; gu.spec = i == 0;
         set_mod(ctx, &gu, i, j, 3, pre_depth, 1);
         if (few) TLF_HIP(launch_dgemm<T>(gu, A_SRC, E_SWIGLU, true, ctx->cus, s));
-        else TLF_HIP(launch_gemm<T>(gu, A_SRC, E_SWIGLU, s));
+        else TLF_HIP(launch_gemm<T>(gu, A_SRC, E_SWIGLU, false, s));
 
         GemmArgs dn;
         dn.A = ctx->buf<float>(B_ACT_PRE); dn.lda = F; dn.W = lw.w_down; dn.N = d; dn.K = F; dn.w_rows = d;
@@ -374,7 +377,7 @@ int run_prefill(tlf_ctx* ctx, int B, int T_, int pos0, const int32_t* tokens, fl
         if (few) {
           TLF_HIP(launch_dgemm<T>(dn, A_CMP, E_RESID, false, ctx->cus, s));
         } else {
-          TLF_HIP(launch_gemm<T>(dn, A_CMP, E_RESID, s));
+          TLF_HIP(launch_gemm<T>(dn, A_CMP, E_RESID, false, s));
           TLF_HIP(launch_resid_norm<T>(rn, s));
         }
       }
@@ -390,7 +393,7 @@ int run_prefill(tlf_ctx* ctx, int B, int T_, int pos0, const int32_t* tokens, fl
       hd.out_row_off = b0;
     }
     if (few) TLF_HIP(launch_dgemm<T>(hd, A_SRC, E_LOGITS, true, ctx->cus, s));
-    else TLF_HIP(launch_gemm<T>(hd, A_SRC, E_LOGITS, s));
+    else TLF_HIP(launch_gemm<T>(hd, A_SRC, E_LOGITS, false, s));
   }
   return TLF_OK;
 }
@@ -500,7 +503,10 @@ int run_decode(tlf_ctx* ctx, hipStream_t s, const int32_t* tokens, float* logits
   hd.A = xc; hd.lda = d; hd.W = head_weights(ctx); hd.N = c.vocab; hd.K = d; hd.w_rows = c.vocab;
   hd.rm.src = perm; hd.rm.rows = B; hd.out = logits; hd.ldo = c.vocab; hd.eps = c.rms_eps; hd.spec = 1;
   hd.argmax_keys = ctx->buf<unsigned long long>(B_KEYS);
-  TLF_HIP(launch_dgemm<T>(hd, A_CMP, E_LOGITS, true, ctx->cus, s));
+  // a large batch makes the head a real GEMM (128 x 128 tiles read each
+  // weight row B / 128 times); a small one is the split-K projection
+  if (B >= kHeadGemmRows) TLF_HIP(launch_gemm<T>(hd, A_CMP, E_LOGITS, true, s));
+  else TLF_HIP(launch_dgemm<T>(hd, A_CMP, E_LOGITS, true, ctx->cus, s));
   if (next) TLF_HIP(launch_argmax_finalize(ctx->buf<unsigned long long>(B_KEYS), next, B, s));
   return TLF_OK;
 }

@@ -11,7 +11,8 @@
 //   E_RESID:   x[src(r)] += result (residual of the attention/FFN branch)
 //   E_SWIGLU:  act = silu(gate) * up, gate/up columns interleaved in 16-column
 //              groups so every wave holds matching pairs
-//   E_LOGITS:  float logits plus a packed (value, -index) atomicMax for greedy
+//   E_LOGITS:  float logits plus a packed (value, -index) atomicMax for greedy;
+//              compact rows (A_CMP, the decode LM head) go to row src(r)
 //   E_HIDDEN:  silu(result + bias), the MLP router's hidden layer
 //
 // Tiling: 256 threads = 4 waves in a 2x2 grid; each wave owns MT x NT 16x16
@@ -29,7 +30,10 @@ __device__ __forceinline__ unsigned int ordered_bits(float v) {
 }
 
 // MOD: the A rows are scaled by (1 + gamma) of their AdaLN modulation rows.
-template <typename T, int MT, int NT, int PF, int BK, int AK, int EK, bool MOD>
+// NORM: A holds residual rows x and the product is taken with RMSNorm(x): the
+// sum of squares of each row is accumulated from the A chunks as they pass
+// and the output row is scaled by 1 / rms, since (x / rms) W^T = (x W^T) / rms.
+template <typename T, int MT, int NT, int PF, int BK, int AK, int EK, bool MOD, bool NORM>
 __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
   constexpr int BM = 2 * MT * 16, BN = 2 * NT * 16;
   constexpr bool kSplit = sizeof(T) == 2;            // bf16 weights: A as hi + lo parts
@@ -50,6 +54,7 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
   __shared__ __align__(16) T Bs[BN * LDK];
   __shared__ int row_src_s[BM];
   __shared__ int row_mod_s[BM];  // modulation row offset (AdaLN), 0 without
+  __shared__ float row_inv_s[NORM ? BM : 1];  // 1 / rms of each row
   __shared__ int64_t kv_base[EK == E_QKV ? BM : 1];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -101,11 +106,16 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
       if constexpr (MOD) rg[c] = gm;
     }
   };
+  // NORM: this thread's rows are tid / ACR + c * (256 / ACR), c < ACH
+  float ssq[NORM ? ACH : 1];
+#pragma unroll
+  for (int c = 0; c < (NORM ? ACH : 1); ++c) ssq[c] = 0.f;
   auto store_tiles = [&](const float4* ra, const float4* rg, const V16<T>* rb) {
 #pragma unroll
     for (int c = 0; c < ACH; ++c) {
       const int ch = tid + c * 256, row = ch / ACR, col = (ch % ACR) * 4;
       float4 av = ra[c];
+      if constexpr (NORM) ssq[c] += av.x * av.x + av.y * av.y + av.z * av.z + av.w * av.w;
       if constexpr (MOD)
         av = make_float4(av.x * (1.f + rg[c].x), av.y * (1.f + rg[c].y), av.z * (1.f + rg[c].z),
                          av.w * (1.f + rg[c].w));
@@ -191,6 +201,18 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
     if (tid < BM) kv_base[tid] = my_kv;
     __syncthreads();
   }
+  if constexpr (NORM) {
+    static_assert(256 % ACR == 0 && ACR <= kWave, "rows of the A chunks");
+    // the ACR threads of a row are consecutive lanes of one wave
+#pragma unroll
+    for (int c = 0; c < ACH; ++c) {
+      float t = ssq[c];
+#pragma unroll
+      for (int o = 1; o < ACR; o <<= 1) t += shfl_xor(t, o);
+      if (tid % ACR == 0) row_inv_s[tid / ACR + c * (256 / ACR)] = rsqrtf(t / (float)g.K + g.eps);
+    }
+    __syncthreads();
+  }
 
   const int quad = lane >> 4, col16 = lane & 15;
 #pragma unroll
@@ -200,14 +222,17 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
       const int rl = wm * MT * 16 + i * 16 + quad * 4 + r;
       const int src = row_src_s[rl];
       const int rg = r0 + rl;
+      const float rs = NORM ? row_inv_s[rl] : 1.f;
       if constexpr (EK == E_LOGITS) {
+        // compact rows (A_CMP) write their logits to row src(r), the sequence's
+        const int orow = AK == A_CMP ? src : g.out_row_off + rg;
         unsigned long long best = 0ull;
 #pragma unroll
         for (int j = 0; j < NT; ++j) {
           const int n = n0 + wn * NT * 16 + j * 16 + col16;
-          const float v = acc[i][j][r];
+          const float v = acc[i][j][r] * rs;
           if (src >= 0 && n < g.N) {
-            reinterpret_cast<float*>(g.out)[(int64_t)(g.out_row_off + rg) * g.ldo + n] = v;
+            reinterpret_cast<float*>(g.out)[(int64_t)orow * g.ldo + n] = v;
             const unsigned long long key =
                 ((unsigned long long)ordered_bits(v) << 32) | (unsigned long long)(0xFFFFFFFFu - (unsigned)n);
             best = key > best ? key : best;
@@ -219,7 +244,7 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
             const unsigned long long other = shfl_xor(best, o);
             best = other > best ? other : best;
           }
-          if (col16 == 0 && src >= 0 && best != 0ull) atomicMax(&g.argmax_keys[g.out_row_off + rg], best);
+          if (col16 == 0 && src >= 0 && best != 0ull) atomicMax(&g.argmax_keys[orow], best);
         }
       } else if constexpr (EK == E_SWIGLU) {
 #pragma unroll
@@ -269,23 +294,24 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
 }
 
 template <typename T, int MT, int NT, int PF, int BK>
-hipError_t launch_tiles(const GemmArgs& a, AKind ak, EKind ek, hipStream_t s) {
+hipError_t launch_tiles(const GemmArgs& a, AKind ak, EKind ek, bool norm, hipStream_t s) {
   constexpr int BM = 2 * MT * 16, BN = 2 * NT * 16;
   const dim3 grid((a.N + BN - 1) / BN, (a.rm.rows + BM - 1) / BM);
   if (grid.x == 0 || grid.y == 0) return hipSuccess;
   const bool mod = a.mod_g != nullptr;
-#define TLF_GEMM_CASE(AKV, EKV, MODV)                                                          \
-  if (ak == AKV && ek == EKV && mod == MODV) {                                                 \
-    hipLaunchKernelGGL((k_gemm<T, MT, NT, PF, BK, AKV, EKV, MODV>), grid, dim3(256), 0, s, a); \
-    return hipGetLastError();                                                                  \
+#define TLF_GEMM_CASE(AKV, EKV, MODV, NORMV)                                                          \
+  if (ak == AKV && ek == EKV && mod == MODV && norm == NORMV) {                                       \
+    hipLaunchKernelGGL((k_gemm<T, MT, NT, PF, BK, AKV, EKV, MODV, NORMV>), grid, dim3(256), 0, s, a); \
+    return hipGetLastError();                                                                         \
   }
-  TLF_GEMM_CASE(A_SRC, E_QKV, false)
-  TLF_GEMM_CASE(A_SRC, E_QKV, true)
-  TLF_GEMM_CASE(A_SRC, E_SWIGLU, false)
-  TLF_GEMM_CASE(A_SRC, E_SWIGLU, true)
-  TLF_GEMM_CASE(A_SRC, E_LOGITS, false)
-  TLF_GEMM_CASE(A_CMP, E_RESID, false)
-  TLF_GEMM_CASE(A_CMP, E_HIDDEN, false)
+  TLF_GEMM_CASE(A_SRC, E_QKV, false, false)
+  TLF_GEMM_CASE(A_SRC, E_QKV, true, false)
+  TLF_GEMM_CASE(A_SRC, E_SWIGLU, false, false)
+  TLF_GEMM_CASE(A_SRC, E_SWIGLU, true, false)
+  TLF_GEMM_CASE(A_SRC, E_LOGITS, false, false)
+  TLF_GEMM_CASE(A_CMP, E_LOGITS, false, true)
+  TLF_GEMM_CASE(A_CMP, E_RESID, false, false)
+  TLF_GEMM_CASE(A_CMP, E_HIDDEN, false, false)
 #undef TLF_GEMM_CASE
   return hipErrorInvalidValue;
 }
@@ -293,13 +319,13 @@ hipError_t launch_tiles(const GemmArgs& a, AKind ak, EKind ek, hipStream_t s) {
 }  // namespace
 
 template <typename T>
-hipError_t launch_gemm(const GemmArgs& a, AKind ak, EKind ek, hipStream_t s) {
+hipError_t launch_gemm(const GemmArgs& a, AKind ak, EKind ek, bool norm, hipStream_t s) {
   // 128x128 tiles, K 64 at a time, one K tile in flight
   if (a.K % 64 != 0) return hipErrorInvalidValue;
-  return launch_tiles<T, 4, 4, 1, 64>(a, ak, ek, s);
+  return launch_tiles<T, 4, 4, 1, 64>(a, ak, ek, norm, s);
 }
 
-template hipError_t launch_gemm<float>(const GemmArgs&, AKind, EKind, hipStream_t);
-template hipError_t launch_gemm<bf16>(const GemmArgs&, AKind, EKind, hipStream_t);
+template hipError_t launch_gemm<float>(const GemmArgs&, AKind, EKind, bool, hipStream_t);
+template hipError_t launch_gemm<bf16>(const GemmArgs&, AKind, EKind, bool, hipStream_t);
 
 }  // namespace tlf

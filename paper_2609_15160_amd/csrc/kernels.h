@@ -101,8 +101,12 @@ struct GemmArgs {
   int keep_loop = 0;                    // keep_depth[r] > keep_loop (its token runs this loop)
 };
 
+// Many-row projections (prefill, and the decode LM head of a large batch):
+// 128 x 128 MFMA tiles staged through LDS.  norm: A is the residual x and the
+// product is taken with RMSNorm(x) (supported for (A_CMP, E_LOGITS), whose
+// rows write their logits to row src(r)).
 template <typename T>
-hipError_t launch_gemm(const GemmArgs& a, AKind ak, EKind ek, hipStream_t s);
+hipError_t launch_gemm(const GemmArgs& a, AKind ak, EKind ek, bool norm, hipStream_t s);
 // Decode-shaped projections (few rows): K split across the waves of a
 // workgroup, all loads in flight at once, one writer per output, rows in
 // compact order (E_RESID: out[r] += result; E_LOGITS: logits row src(r)).

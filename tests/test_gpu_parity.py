@@ -100,6 +100,17 @@ def test_f32_two_layers_ragged_batch():
     _check_f32(m, w, prompts, g, o, "f32-small")
 
 
+def test_f32_batch_over_head_gemm_rows():
+    """A decode batch of 130 rows runs the LM head on the 128 x 128 GEMM with
+    the norm fused: two row tiles, the second with 2 rows."""
+    m = _f32_small(batch=130, prompt_len=9, steps=4, vocab=300)
+    w = synth.make_weights(m)
+    prompts = synth.make_prompts(m)
+    g = parity.run_gpu(m, w, prompts, m.steps)
+    o = parity.run_oracle(m, w, prompts, g.step_tokens)
+    _check_f32(m, w, prompts, g, o, "f32-b130")
+
+
 def test_f32_single_token_prompt_and_deep_tail():
     m = _f32_small(batch=2, prompt_len=1, steps=40)
     w = synth.make_weights(m)
