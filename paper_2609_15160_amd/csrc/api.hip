@@ -60,7 +60,7 @@ bool make_layout(const tlf_config& c, Layout* L) {
   sz[B_Q_DEC] = B * d * 4;
   sz[B_O_DEC] = B * d * 4;
   sz[B_ACT_DEC] = B * F * 4;
-  sz[B_KEYS] = B * 8;
+  sz[B_KEYS] = B * ceil_div(c.vocab, kWave) * 8;  // greedy key per 64-column group of each row
   sz[B_X_PRE] = P * d * 4;
   sz[B_Y_PRE] = P * d * 4;
   sz[B_DEPTH_PRE] = P * 4;
@@ -426,7 +426,6 @@ int run_decode(tlf_ctx* ctx, hipStream_t s, const int32_t* tokens, float* logits
   DecodePlanArgs pa;
   pa.c = ctx->cv; pa.B = B; pa.depth = ctx->buf<int32_t>(B_DEPTH_DEC); pa.perm = perm; pa.nact = nact;
   pa.kv_slot = kv_slot;
-  pa.argmax_keys = ctx->buf<unsigned long long>(B_KEYS);
   pa.kv_entry_bytes = (int64_t)c.n_layers * 2 * c.d_model * ctx->L.s;
   pa.dense = c.dense_decode;
   pa.row_depth = ctx->buf<int32_t>(B_ROW_DEPTH);
@@ -503,11 +502,12 @@ int run_decode(tlf_ctx* ctx, hipStream_t s, const int32_t* tokens, float* logits
   hd.A = xc; hd.lda = d; hd.W = head_weights(ctx); hd.N = c.vocab; hd.K = d; hd.w_rows = c.vocab;
   hd.rm.src = perm; hd.rm.rows = B; hd.out = logits; hd.ldo = c.vocab; hd.eps = c.rms_eps; hd.spec = 1;
   hd.argmax_keys = ctx->buf<unsigned long long>(B_KEYS);
+  hd.key_groups = (int)ceil_div(c.vocab, kWave);
   // a large batch makes the head a real GEMM (128 x 128 tiles read each
   // weight row B / 128 times); a small one is the split-K projection
   if (B >= kHeadGemmRows) TLF_HIP(launch_gemm<T>(hd, A_CMP, E_LOGITS, true, s));
   else TLF_HIP(launch_dgemm<T>(hd, A_CMP, E_LOGITS, true, ctx->cus, s));
-  if (next) TLF_HIP(launch_argmax_finalize(ctx->buf<unsigned long long>(B_KEYS), next, B, s));
+  if (next) TLF_HIP(launch_argmax_finalize(ctx->buf<unsigned long long>(B_KEYS), hd.key_groups, next, B, s));
   return TLF_OK;
 }
 

@@ -333,13 +333,13 @@ __device__ __forceinline__ void dgemm_tile(const GemmArgs& g, int nact, int act_
         key = ((unsigned long long)ordered_bits(v) << 32) | (unsigned long long)(0xFFFFFFFFu - (unsigned)n);
       }
       if (g.argmax_keys) {
-        // the 64 lanes of a wave hold one row's 64 columns
+        // the 64 lanes of a wave hold one row's 64 columns: one key per group
 #pragma unroll
         for (int o = 1; o < kWave; o <<= 1) {
           const unsigned long long other = shfl_xor(key, o);
           key = other > key ? other : key;
         }
-        if (lane == 0 && key != 0ull) atomicMax(&g.argmax_keys[orow], key);
+        if (lane == 0 && key != 0ull) g.argmax_keys[(int64_t)orow * g.key_groups + n0 / kWave] = key;
       }
     } else {
       const int row = e / BN, col = e % BN, n = n0 + col;

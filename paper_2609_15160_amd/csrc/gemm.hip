@@ -11,7 +11,7 @@
 //   E_RESID:   x[src(r)] += result (residual of the attention/FFN branch)
 //   E_SWIGLU:  act = silu(gate) * up, gate/up columns interleaved in 16-column
 //              groups so every wave holds matching pairs
-//   E_LOGITS:  float logits plus a packed (value, -index) atomicMax for greedy;
+//   E_LOGITS:  float logits plus a packed (value, -index) greedy key per 64 columns;
 //              compact rows (A_CMP, the decode LM head) go to row src(r)
 //   E_HIDDEN:  silu(result + bias), the MLP router's hidden layer
 //
@@ -224,6 +224,7 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
       const int rg = r0 + rl;
       const float rs = NORM ? row_inv_s[rl] : 1.f;
       if constexpr (EK == E_LOGITS) {
+        static_assert(NT * 16 == 64, "one greedy key group per wave");
         // compact rows (A_CMP) write their logits to row src(r), the sequence's
         const int orow = AK == A_CMP ? src : g.out_row_off + rg;
         unsigned long long best = 0ull;
@@ -244,7 +245,9 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
             const unsigned long long other = shfl_xor(best, o);
             best = other > best ? other : best;
           }
-          if (col16 == 0 && src >= 0 && best != 0ull) atomicMax(&g.argmax_keys[orow], best);
+          // this wave's NT x 16 = 64 columns form one key group
+          if (col16 == 0 && src >= 0 && best != 0ull)
+            g.argmax_keys[(int64_t)orow * g.key_groups + (n0 + wn * NT * 16) / 64] = best;
         }
       } else if constexpr (EK == E_SWIGLU) {
 #pragma unroll

@@ -81,7 +81,8 @@ struct GemmArgs {
                             // E_LOGITS: logits (all float32)
   int ldo = 0;
   int out_row_off = 0;      // E_LOGITS: output row = out_row_off + r
-  unsigned long long* argmax_keys = nullptr;  // E_LOGITS, may be nullptr
+  unsigned long long* argmax_keys = nullptr;  // E_LOGITS, may be nullptr: [rows][key_groups] greedy keys,
+  int key_groups = 0;                         // one per 64-column group of each logits row
   KvDst kv;                 // E_QKV
   int d = 0;                // E_QKV: width of each of q, k, v
   int F = 0;                // E_SWIGLU: hidden width
@@ -183,7 +184,6 @@ struct DecodePlanArgs {
   int32_t* nact = nullptr;         // [R]
   int64_t* kv_slot = nullptr;      // [R][B]: element offset (page * page_elems + slot) of the
                                    // slot that compact row k appends at loop i
-  unsigned long long* argmax_keys = nullptr; // [B] cleared for the LM head
   int64_t kv_entry_bytes = 0;      // bytes of one (token, loop) cache entry over all layers
   int32_t* row_depth = nullptr;    // [B] depth of the token of compact row k
   int dense = 0;                   // 1: rows in batch order, every loop up to the deepest token
@@ -237,7 +237,8 @@ template <typename T> hipError_t launch_attn_prefill(const AttnPrefillArgs& a, h
 // ---------------------------------------------------------------------------
 hipError_t launch_fill_i32(int32_t* p, int32_t v, int64_t n, hipStream_t s);
 hipError_t launch_fill_u64(unsigned long long* p, unsigned long long v, int64_t n, hipStream_t s);
-hipError_t launch_argmax_finalize(const unsigned long long* keys, int32_t* next, int B, hipStream_t s);
+// next[b] = the column of the largest key among row b's `groups` keys (lowest id on ties).
+hipError_t launch_argmax_finalize(const unsigned long long* keys, int groups, int32_t* next, int B, hipStream_t s);
 
 // ---------------------------------------------------------------------------
 // AdaLN conditioning table: modulation of every (layer, loop, depth),

@@ -14,7 +14,7 @@ namespace {
 //      numbered by a block prefix sum (deterministic);
 //   3. per executed (b, i): the slot's position, cache_len += 1, and the
 //      slot's element offset for the QKV epilogue, by compact row;
-//   4. statistics and the greedy keys cleared for the LM head.
+//   4. statistics.
 // Dense mode (gather-scatter off): rows stay in batch order and every loop up
 // to the deepest token of the step has all B rows; the rows of exited tokens
 // get kv_slot -1 (no cache entry) and their attention reads the cache as it
@@ -198,8 +198,6 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan_decode(DecodePlanArgs a) 
   }
   __syncthreads();
   if (tid < R) c.step_stats[kStatRows + tid] = a.nact[tid];
-
-  for (int b = tid; b < B; b += kPlanThreads) a.argmax_keys[b] = 0ull;
 }
 
 // ---------------------------------------------------------------------------
@@ -284,9 +282,21 @@ __global__ void k_fill_i32(int32_t* p, int32_t v, int64_t n) {
 __global__ void k_fill_u64(unsigned long long* p, unsigned long long v, int64_t n) {
   for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) p[i] = v;
 }
-__global__ void k_argmax_finalize(const unsigned long long* keys, int32_t* next, int B) {
-  const int b = blockIdx.x * blockDim.x + threadIdx.x;
-  if (b < B) next[b] = (int32_t)(0xFFFFFFFFu - (unsigned)(keys[b] & 0xFFFFFFFFull));
+// one wave per row: the largest of its group keys (value, then lowest id)
+__global__ void k_argmax_finalize(const unsigned long long* keys, int groups, int32_t* next, int B) {
+  const int b = blockIdx.x * (blockDim.x / kWave) + (int)(threadIdx.x / kWave), lane = lane_id();
+  if (b >= B) return;
+  unsigned long long key = 0ull;
+  for (int gi = lane; gi < groups; gi += kWave) {
+    const unsigned long long k = keys[(int64_t)b * groups + gi];
+    key = k > key ? k : key;
+  }
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    const unsigned long long other = shfl_xor(key, o);
+    key = other > key ? other : key;
+  }
+  if (lane == 0) next[b] = (int32_t)(0xFFFFFFFFu - (unsigned)(key & 0xFFFFFFFFull));
 }
 
 int fill_grid(int64_t n) {
@@ -318,9 +328,10 @@ hipError_t launch_fill_u64(unsigned long long* p, unsigned long long v, int64_t 
   hipLaunchKernelGGL(k_fill_u64, dim3(fill_grid(n)), dim3(256), 0, s, p, v, n);
   return hipGetLastError();
 }
-hipError_t launch_argmax_finalize(const unsigned long long* keys, int32_t* next, int B, hipStream_t s) {
+hipError_t launch_argmax_finalize(const unsigned long long* keys, int groups, int32_t* next, int B, hipStream_t s) {
   if (B <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_argmax_finalize, dim3((B + 255) / 256), dim3(256), 0, s, keys, next, B);
+  if (B <= 0 || groups <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_argmax_finalize, dim3((B + 3) / 4), dim3(4 * kWave), 0, s, keys, groups, next, B);
   return hipGetLastError();
 }
 
