@@ -12,9 +12,13 @@
 //
 // Prefill: causal attention among the gathered tokens of each loop (Section
 // 3.3), which in compact order is a plain causal mask on the (b, i) slot
-// sequence.  One workgroup per (sequence, 64-query tile, head); K tiles and
-// transposed V tiles of 64 keys are gathered from the pages into LDS and
-// both products run on MFMA with an online softmax.
+// sequence.  One workgroup per (sequence, 64-query tile, head), 16 queries
+// per wave, the longest query tiles dispatched first.  Key tiles of four pages are copied into LDS verbatim (the K
+// blocks are already in MFMA-fragment order), the next tile loading into
+// registers while the current one is in use.  Scores are computed transposed,
+// S^T = K q^T, so that the P^T operand of O^T = V^T P^T is exactly the scores
+// each lane holds (no data movement between the two products); both run on
+// MFMA with an online softmax per query.
 #include "kernels.h"
 
 namespace tlf {
@@ -36,6 +40,11 @@ template <typename F, typename P> __device__ __forceinline__ F ld_stream(const P
     return __builtin_bit_cast(F, __builtin_nontemporal_load(reinterpret_cast<const unsigned int*>(p)));
   }
 }
+
+// Queries per wave of the prefill attention (four waves per workgroup).
+constexpr int kPreQW = 16;
+
+__device__ __forceinline__ float4 scale4(float4 v, float s) { return make_float4(v.x * s, v.y * s, v.z * s, v.w * s); }
 
 __device__ __forceinline__ float merge_scale(float m, float mn) {
   return m == kNegInf ? 0.f : exp2f(m - mn);
@@ -236,26 +245,39 @@ __global__ __launch_bounds__(W * 64) void k_attn_decode(AttnDecodeArgs a) {
 }
 
 template <typename T, int D>
-__global__ __launch_bounds__(256) void k_attn_prefill(AttnPrefillArgs a) {
+__global__ __launch_bounds__(256, 4) void k_attn_prefill(AttnPrefillArgs a) {
   using M = Mfma<T>;
+  typedef typename M::frag Frag;
   constexpr int KS = M::KS, EPL = M::EPL;
-  constexpr int BQ = 64, BKEY = 64;
-  constexpr int PADT = 16 / (int)sizeof(T);
-  constexpr int LDK = D + PADT;
-  constexpr int LDV = BKEY + PADT;
-  constexpr int LDP = BKEY + PADT;
-  constexpr int CPK = D * (int)sizeof(T) / 16;  // 16-byte chunks per key row
-  constexpr int EPC = 16 / (int)sizeof(T);
+  constexpr int QW = kPreQW;                      // queries per wave
+  constexpr int QN = QW / 16;                     // query column tiles per wave
+  constexpr int BQ = 4 * QW;                      // queries per workgroup
+  constexpr int BKEY = 4 * kPage;                 // keys per tile: four pages
+  constexpr int NT = BKEY / 16;                   // 16-key subtiles
+  constexpr int KSTEPS = D / KS;
   constexpr int DT = D / 16;
-  __shared__ __align__(16) T Ks[BKEY * LDK];
-  __shared__ __align__(16) T Vt[D * LDV];
-  __shared__ __align__(16) T Ps[4 * 16 * LDP];
+  constexpr int NQ = EPL == 8 ? 2 : 1;            // parts of q (hi, lo)
+  constexpr int KBLK = kPage * D;                 // elements of one page's K (or V) block
+  constexpr int EPC = 16 / (int)sizeof(T);        // elements per 16-byte chunk
+  constexpr int VLD = kPage + (sizeof(T) == 2 ? 4 : 2);  // padded LDS row of one dimension of a V block
+  constexpr int CH = 2 * 4 * KBLK / EPC;          // 16-byte chunks of one K + V tile
+  static_assert(CH % 256 == 0, "tile chunks per thread");
+  constexpr int CPT = CH / 256;
+  static_assert(kPage % EPC == 0, "V chunk inside one dimension row");
+  // K tile: four pages' K blocks verbatim (fragment order: lane (key, quad) of a
+  // K step reads EPL contiguous elements, 64 lanes one contiguous run);
+  // V tile: four pages' V blocks [dim][slot], rows padded against bank conflicts
+  __shared__ __align__(16) T Ks[2][4 * KBLK];
+  __shared__ __align__(16) T Vs[2][4 * D * VLD];
 
   const CacheView& c = a.c;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int quad = lane >> 4, c16 = lane & 15;
   const int QT = (a.T + BQ - 1) / BQ;
-  const int g = blockIdx.x / QT, qt = blockIdx.x % QT, h = blockIdx.y;
+  // workgroup u = (QT - 1 - qt) * G * H + g * H + h: the last query tiles see
+  // the most keys, so they are dispatched first
+  const int GH = a.G * c.H, u = blockIdx.x;
+  const int qt = QT - 1 - u / GH, g = (u % GH) / c.H, h = u % c.H;
   const int b = a.b0 + g;
   // the call's nq queries are cache entries [n - nq, n) of (b, loop): query
   // row a (compact index n0 + a) sees keys [0, n0 + a]
@@ -268,128 +290,190 @@ __global__ __launch_bounds__(256) void k_attn_prefill(AttnPrefillArgs a) {
   const T* pool = reinterpret_cast<const T*>(c.pool);
   const int64_t koff = k_block(c, a.layer, h), voff = v_block(c, a.layer, h);
   const int npages = (n + kPage - 1) / kPage;
+  const int nkt = (min(n, n0 + min(nq, q0 + BQ)) + BKEY - 1) / BKEY;  // key tiles of the workgroup
+  const int wq0 = n0 + q0 + w * QW;               // compact index of the wave's first query
 
-  // q (float32) as the A operand of S = Q K^T; against bf16 keys it is split
+  // q (float32, scaled by log2(e) / sqrt(D) so scores come out in log2
+  // units) as the B operand of S^T = K q^T; against bf16 keys it is split
   // into hi and lo parts, one product each
-  constexpr int NQ = EPL == 8 ? 2 : 1;
-  typename M::frag qf[NQ][D / KS];
-  {
-    const int qrow = min(q0 + w * 16 + c16, nq - 1);
+  Frag qf[QN][NQ][KSTEPS];
+#pragma unroll
+  for (int qn = 0; qn < QN; ++qn) {
+    const int qrow = min(q0 + w * QW + qn * 16 + c16, nq - 1);
     const float* qp = a.q + ((int64_t)g * a.T + qrow) * a.d + h * D + quad * EPL;
 #pragma unroll
-    for (int ks = 0; ks < D / KS; ++ks) {
-      if constexpr (NQ == 2) split_frag(qp + ks * KS, qf[0][ks], qf[NQ - 1][ks]);
-      else qf[0][ks] = qp[ks * KS];
+    for (int ks = 0; ks < KSTEPS; ++ks) {
+      if constexpr (NQ == 2) {
+        const float4 v0 = *reinterpret_cast<const float4*>(qp + ks * KS);
+        const float4 v1 = *reinterpret_cast<const float4*>(qp + ks * KS + 4);
+        uint2 h0, l0, h1, l1;
+        split4(scale4(v0, a.scale_log2), h0, l0);
+        split4(scale4(v1, a.scale_log2), h1, l1);
+        qf[qn][0][ks] = __builtin_bit_cast(Frag, make_uint4(h0.x, h0.y, h1.x, h1.y));
+        qf[qn][1][ks] = __builtin_bit_cast(Frag, make_uint4(l0.x, l0.y, l1.x, l1.y));
+      } else {
+        qf[qn][0][ks] = qp[ks * KS] * a.scale_log2;
+      }
     }
   }
-  f32x4 o[DT];
-#pragma unroll
-  for (int dt = 0; dt < DT; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float mrow[4], lrow[4];
-#pragma unroll
-  for (int r = 0; r < 4; ++r) { mrow[r] = kNegInf; lrow[r] = 0.f; }
 
-  const int nkt = min((n0 + q0 + BQ + BKEY - 1) / BKEY, (n + BKEY - 1) / BKEY);
-  for (int kt = 0; kt < nkt; ++kt) {
-    __syncthreads();
-    // K rows: key-major, 16-byte pieces
-    for (int ci = tid; ci < BKEY * CPK; ci += 256) {
-      const int key = ci / CPK, col = (ci % CPK) * EPC;
-      const int ka = kt * BKEY + key;
-      V16<T> kv;
-      kv.u = make_uint4(0, 0, 0, 0);
-      if (ka < n) {
-        const T* kb = pool + (int64_t)pt[ka / kPage] * c.page_elems + koff;
-        if constexpr (EPC == EPL) {
-          kv = ld16(kb + k_frag_off<T>(ka % kPage, col));  // one fragment: EPL consecutive elements
-        } else {
+  // one K + V tile: chunk ci < CH/2 is K chunk ci, else V chunk ci - CH/2;
+  // pages past the cache read as zeros (their scores are masked)
+  uint4 pre[CPT];
+  auto load_tile = [&](int kt) __attribute__((always_inline)) {
 #pragma unroll
-          for (int t = 0; t < EPC; ++t) kv.e[t] = kb[k_frag_off<T>(ka % kPage, col + t)];
+    for (int u = 0; u < CPT; ++u) {
+      const int ci = tid + u * 256;
+      const int kv = ci / (CH / 2), cc = ci % (CH / 2);
+      const int p = cc / (KBLK / EPC), off = (cc % (KBLK / EPC)) * EPC;
+      const int pa = kt * 4 + p;
+      pre[u] = make_uint4(0, 0, 0, 0);
+      if (pa < npages)
+        pre[u] = *reinterpret_cast<const uint4*>(pool + (int64_t)pt[pa] * c.page_elems + (kv ? voff : koff) + off);
+    }
+  };
+  auto store_tile = [&](int buf) __attribute__((always_inline)) {
+#pragma unroll
+    for (int u = 0; u < CPT; ++u) {
+      const int ci = tid + u * 256;
+      const int kv = ci / (CH / 2), cc = ci % (CH / 2);
+      const int p = cc / (KBLK / EPC), off = (cc % (KBLK / EPC)) * EPC;
+      if (kv == 0) {
+        *reinterpret_cast<uint4*>(&Ks[buf][p * KBLK + off]) = pre[u];
+      } else {
+        const int dim = off / kPage, slot = off % kPage;  // EPC slots of one dimension
+        T* dst = &Vs[buf][(p * D + dim) * VLD + slot];
+        *reinterpret_cast<uint2*>(dst) = make_uint2(pre[u].x, pre[u].y);
+        *reinterpret_cast<uint2*>(dst + EPC / 2) = make_uint2(pre[u].z, pre[u].w);
+      }
+    }
+  };
+
+  f32x4 o[DT][QN];  // O^T: lane holds dims 4 quad + r of tile dt for query c16 of column tile qn
+#pragma unroll
+  for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+    for (int qn = 0; qn < QN; ++qn) o[dt][qn] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float mq[QN], lq[QN];  // running max (per query, replicated over quads) and this lane's sum
+#pragma unroll
+  for (int qn = 0; qn < QN; ++qn) { mq[qn] = kNegInf; lq[qn] = 0.f; }
+
+  load_tile(0);
+  store_tile(0);
+  __syncthreads();
+  for (int kt = 0; kt < nkt; ++kt) {
+    const int buf = kt & 1;
+    if (kt + 1 < nkt) load_tile(kt + 1);
+    // the wave's queries see keys <= their compact index: skip tiles past its last query
+    if (kt * BKEY <= wq0 + QW - 1) {
+      const T* kb = Ks[buf];
+      // S^T tile (nt, qn): lane holds keys nt * 16 + 4 quad + r of query c16
+      f32x4 s[NT][QN];
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+#pragma unroll
+        for (int qn = 0; qn < QN; ++qn) s[nt][qn] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < KSTEPS; ++ks) {
+          const Frag kf = M::load(kb + nt * KBLK + ((ks * 4 + quad) * kPage + c16) * EPL);
+#pragma unroll
+          for (int qn = 0; qn < QN; ++qn)
+#pragma unroll
+            for (int qa = 0; qa < NQ; ++qa) s[nt][qn] = M::mma(kf, qf[qn][qa][ks], s[nt][qn]);
         }
       }
-      st16(&Ks[key * LDK + col], kv);
+      // online softmax per query (column): mask (only a tile that reaches
+      // past the wave's first query or the cache end), max, rescale
+      const bool edge = kt * BKEY + BKEY - 1 > wq0 || kt * BKEY + BKEY > n;
+#pragma unroll
+      for (int qn = 0; qn < QN; ++qn) {
+        const int qidx = wq0 + qn * 16 + c16;
+        if (edge) {
+#pragma unroll
+          for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const int kidx = kt * BKEY + nt * 16 + 4 * quad + r;
+              if (kidx > qidx || kidx >= n) s[nt][qn][r] = kNegInf;
+            }
+        }
+        float mx = mq[qn];
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) mx = fmaxf(mx, s[nt][qn][r]);
+        mx = fmaxf(mx, shfl_xor(mx, 16));
+        mx = fmaxf(mx, shfl_xor(mx, 32));
+        const float alpha = merge_scale(mq[qn], mx);
+        float ps = 0.f;
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const float p = mx == kNegInf ? 0.f : exp2f(s[nt][qn][r] - mx);
+            s[nt][qn][r] = p;
+            ps += p;
+          }
+        lq[qn] = lq[qn] * alpha + ps;
+        mq[qn] = mx;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) o[dt][qn] *= alpha;
+      }
+      // O^T += V^T P^T: the k-slots of one MFMA are keys this lane holds
+      // scores for, in the same order on both operands
+      const T* vb = Vs[buf];
+      if constexpr (EPL == 8) {
+#pragma unroll
+        for (int np = 0; np < NT; np += 2) {  // keys (np, 4 quad + r) and (np + 1, 4 quad + r)
+          Frag pf[QN];
+#pragma unroll
+          for (int qn = 0; qn < QN; ++qn) {
+            const uint4 u = make_uint4(pack_bf16x2(s[np][qn][0], s[np][qn][1]), pack_bf16x2(s[np][qn][2], s[np][qn][3]),
+                                       pack_bf16x2(s[np + 1][qn][0], s[np + 1][qn][1]),
+                                       pack_bf16x2(s[np + 1][qn][2], s[np + 1][qn][3]));
+            pf[qn] = __builtin_bit_cast(Frag, u);
+          }
+#pragma unroll
+          for (int dt = 0; dt < DT; ++dt) {
+            const int dim = dt * 16 + c16;
+            const uint2 v0 = *reinterpret_cast<const uint2*>(vb + (np * D + dim) * VLD + 4 * quad);
+            const uint2 v1 = *reinterpret_cast<const uint2*>(vb + ((np + 1) * D + dim) * VLD + 4 * quad);
+            const Frag vf = __builtin_bit_cast(Frag, make_uint4(v0.x, v0.y, v1.x, v1.y));
+#pragma unroll
+            for (int qn = 0; qn < QN; ++qn) o[dt][qn] = M::mma(vf, pf[qn], o[dt][qn]);
+          }
+        }
+      } else {
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r)  // one key (nt, 4 quad + r) per lane per MFMA
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt) {
+              const Frag vf = vb[(nt * D + dt * 16 + c16) * VLD + 4 * quad + r];
+#pragma unroll
+              for (int qn = 0; qn < QN; ++qn) o[dt][qn] = M::mma(vf, s[nt][qn][r], o[dt][qn]);
+            }
+      }
     }
-    // V^T: each page holds [D][16 slots]; a 16-byte piece is EPC slots of one dimension
-    constexpr int VPC = kPage / EPC;  // pieces per (page, dimension)
-    for (int ci = tid; ci < (BKEY / kPage) * D * VPC; ci += 256) {
-      const int pg = ci / (D * VPC), rem = ci % (D * VPC), dim = rem / VPC, piece = rem % VPC;
-      const int pa = kt * (BKEY / kPage) + pg;  // page index within the (b, i) cache
-      V16<T> vv;
-      vv.u = make_uint4(0, 0, 0, 0);
-      // slots past n in the last page hold finite stale values; their P is 0
-      if (pa < npages)
-        vv = ld16(pool + (int64_t)pt[pa] * c.page_elems + voff + (int64_t)dim * kPage + piece * EPC);
-      st16(&Vt[dim * LDV + pg * kPage + piece * EPC], vv);
-    }
+    if (kt + 1 < nkt) store_tile(buf ^ 1);
     __syncthreads();
-
-    f32x4 s[4];
-#pragma unroll
-    for (int nt = 0; nt < 4; ++nt) {
-      s[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int ks = 0; ks < D / KS; ++ks) {
-        const typename M::frag kf = M::load(&Ks[(nt * 16 + c16) * LDK + ks * KS + quad * EPL]);
-#pragma unroll
-        for (int qa = 0; qa < NQ; ++qa) s[nt] = M::mma(qf[qa][ks], kf, s[nt]);
-      }
-    }
-    float alpha[4];
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int row = n0 + q0 + w * 16 + quad * 4 + r;
-      float mx = kNegInf;
-#pragma unroll
-      for (int nt = 0; nt < 4; ++nt) {
-        const int key = kt * BKEY + nt * 16 + c16;
-        float v = s[nt][r] * a.scale_log2;
-        if (key > row || key >= n) v = kNegInf;
-        s[nt][r] = v;
-        mx = fmaxf(mx, v);
-      }
-#pragma unroll
-      for (int off = 1; off < 16; off <<= 1) mx = fmaxf(mx, shfl_xor(mx, off));
-      const float mn = fmaxf(mrow[r], mx);
-      alpha[r] = (mn == kNegInf) ? 1.f : merge_scale(mrow[r], mn);
-      float ps = 0.f;
-#pragma unroll
-      for (int nt = 0; nt < 4; ++nt) {
-        const float p = (s[nt][r] == kNegInf) ? 0.f : exp2f(s[nt][r] - mn);
-        s[nt][r] = p;
-        ps += p;
-      }
-      lrow[r] = lrow[r] * alpha[r] + ps;
-      mrow[r] = mn;
-    }
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) o[dt][r] *= alpha[r];
-    T* pw = Ps + w * 16 * LDP;
-#pragma unroll
-    for (int nt = 0; nt < 4; ++nt)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) pw[(quad * 4 + r) * LDP + nt * 16 + c16] = from_f<T>(s[nt][r]);
-    __syncthreads();
-#pragma unroll
-    for (int kk = 0; kk < BKEY / KS; ++kk) {
-      const typename M::frag pa = M::load(&pw[c16 * LDP + kk * KS + quad * EPL]);
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt)
-        o[dt] = M::mma(pa, M::load(&Vt[(dt * 16 + c16) * LDV + kk * KS + quad * EPL]), o[dt]);
-    }
   }
+  // the four lane quads hold different keys: add their softmax sums, then
+  // write o[query][dims 4 quad .. 4 quad + 3] of every dimension tile
 #pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    float lt = lrow[r];
-#pragma unroll
-    for (int off = 1; off < 16; off <<= 1) lt += shfl_xor(lt, off);
-    const int row = q0 + w * 16 + quad * 4 + r;
+  for (int qn = 0; qn < QN; ++qn) {
+    float lt = lq[qn];
+    lt += shfl_xor(lt, 16);
+    lt += shfl_xor(lt, 32);
+    const int row = q0 + w * QW + qn * 16 + c16;
     if (row >= nq) continue;
-    float* op = a.o + ((int64_t)g * a.T + row) * a.d + h * D;
+    float* op = a.o + ((int64_t)g * a.T + row) * a.d + h * D + 4 * quad;
     const float inv = 1.f / lt;
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt) op[dt * 16 + c16] = o[dt][r] * inv;
+    for (int dt = 0; dt < DT; ++dt)
+      *reinterpret_cast<float4*>(op + dt * 16) =
+          make_float4(o[dt][qn][0] * inv, o[dt][qn][1] * inv, o[dt][qn][2] * inv, o[dt][qn][3] * inv);
   }
 }
 
@@ -441,8 +525,9 @@ hipError_t attn_decode_blocks_per_cu(int D, int waves, int* blocks) {
 
 template <typename T>
 hipError_t launch_attn_prefill(const AttnPrefillArgs& a, hipStream_t s) {
-  const int QT = (a.T + 63) / 64;
-  const dim3 grid(a.G * QT, a.c.H), block(256);
+  const int BQ = 4 * kPreQW;
+  const int QT = (a.T + BQ - 1) / BQ;
+  const dim3 grid(a.G * QT * a.c.H), block(256);
   if (a.G <= 0) return hipSuccess;
   switch (a.c.D) {
     case 16:
