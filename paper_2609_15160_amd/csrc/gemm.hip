@@ -15,43 +15,58 @@
 //              compact rows (A_CMP, the decode LM head) go to row src(r)
 //   E_HIDDEN:  silu(result + bias), the MLP router's hidden layer
 //
-// Tiling: 256 threads = 4 waves in a 2x2 grid; each wave owns MT x NT 16x16
-// MFMA tiles.  K advances BK elements per tile, staged through LDS from a
-// ring of PF tiles prefetched into registers.
+// Tiling: 256 threads = 4 waves in a 2 x 2 grid, a 128 x 256 output tile
+// per workgroup (64 x 128 per wave; 128 x 128 when there are few row tiles).  K advances 32
+// elements per tile through two LDS stages: the next tile's global loads
+// are in flight while the current one is multiplied, then stored to the
+// other stage (one barrier per tile).  LDS rows are XOR-swizzled by 16-byte
+// chunk instead of padded, so two workgroups fit on a compute unit.
 #include "kernels.h"
 
 namespace tlf {
 
 namespace {
 
+// Tiling: 256 threads = 4 waves in a 2 x 2 grid, each wave kGemmMT x NT
+// MFMA tiles of 16 x 16 (64 rows x 128 or 64 columns), K kGemmBK at a time.
+constexpr int kGemmMT = 4, kGemmBK = 32;
+
 __device__ __forceinline__ unsigned int ordered_bits(float v) {
   unsigned int u = __float_as_uint(v);
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+// 16-byte chunk c of LDS row `row` is stored at chunk c ^ key(row): the 16
+// rows that one MFMA fragment read touches land in distinct banks without
+// padding (bf16 rows of 32 elements hold 4 chunks, float rows 8).
+template <typename T> __device__ __forceinline__ int swz(int row, int c) {
+  if constexpr (sizeof(T) == 2) return c ^ ((row >> 2) & 3);
+  else return c ^ (row & 7);
 }
 
 // MOD: the A rows are scaled by (1 + gamma) of their AdaLN modulation rows.
 // NORM: A holds residual rows x and the product is taken with RMSNorm(x): the
 // sum of squares of each row is accumulated from the A chunks as they pass
 // and the output row is scaled by 1 / rms, since (x / rms) W^T = (x W^T) / rms.
-template <typename T, int MT, int NT, int PF, int BK, int AK, int EK, bool MOD, bool NORM>
-__global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
+template <typename T, int NT, int AK, int EK, bool MOD, bool NORM>
+__global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs g) {
+  constexpr int MT = kGemmMT, BK = kGemmBK;
   constexpr int BM = 2 * MT * 16, BN = 2 * NT * 16;
   constexpr bool kSplit = sizeof(T) == 2;            // bf16 weights: A as hi + lo parts
   constexpr int NA = kSplit ? 2 : 1;
-  constexpr int WPC = 16 / (int)sizeof(T);           // weight elements per 16-byte chunk
-  constexpr int WCR = BK / WPC;                      // weight chunks per row per K tile
+  constexpr int CE = 16 / (int)sizeof(T);            // storage elements per 16-byte chunk
+  constexpr int WCR = BK / CE;                       // weight chunks per row per K tile
   constexpr int ACR = BK / 4;                        // A chunks (4 floats) per row per K tile
-  constexpr int LDK = BK + WPC;                      // padded LDS row, storage elements
   using M = Mfma<T>;
   constexpr int KS = M::KS, EPL = M::EPL;
   constexpr int ACH = BM * ACR / 256;                // A chunks per thread
   constexpr int BCH = BN * WCR / 256;                // B chunks per thread
   static_assert(ACH >= 1 && BM * ACR % 256 == 0, "A tile split");
   static_assert(BCH >= 1 && BN * WCR % 256 == 0, "B tile split");
-  static_assert(BK % KS == 0, "K tile");
+  static_assert(BK % KS == 0 && (KS * (int)sizeof(T)) % 16 == 0 || EPL == 1, "K tile");
 
-  __shared__ __align__(16) T As[NA][BM * LDK];
-  __shared__ __align__(16) T Bs[BN * LDK];
+  __shared__ __align__(16) T As[2][NA][BM * BK];
+  __shared__ __align__(16) T Bs[2][BN * BK];
   __shared__ int row_src_s[BM];
   __shared__ int row_mod_s[BM];  // modulation row offset (AdaLN), 0 without
   __shared__ float row_inv_s[NORM ? BM : 1];  // 1 / rms of each row
@@ -74,24 +89,25 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
     return wr < g.w_rows ? wr : g.w_rows - 1;
   };
 
-  float4 ra[PF][ACH];
-  float4 rg[MOD ? PF : 1][MOD ? ACH : 1];  // gamma of the A chunks in flight
-  V16<T> rb[PF][BCH];  // ring of PF K tiles in flight
+  float4 ra[ACH];
+  float4 rg[MOD ? ACH : 1];  // gamma of the A chunks in flight
+  V16<T> rb[BCH];
   const float* A = reinterpret_cast<const float*>(g.A);
   const T* W = reinterpret_cast<const T*>(g.W);
-  const int k_base = 0;
   const int KT = g.K / BK;
 
-  auto load_b = [&](int kt, V16<T>* rb) {
-    const int kk = k_base + kt * BK;
+  // chunk u of thread t: A row (t + 256 u) / ACR, floats 4 ((t + 256 u) % ACR)
+  // .. + 3; W row (t + 256 u) / WCR, chunk (t + 256 u) % WCR
+  auto load_b = [&](int kt) {
+    const int kk = kt * BK;
 #pragma unroll
     for (int c = 0; c < BCH; ++c) {
-      const int ch = tid + c * 256, row = ch / WCR, col = (ch % WCR) * WPC;
+      const int ch = tid + c * 256, row = ch / WCR, col = (ch % WCR) * CE;
       rb[c] = ld16(W + (int64_t)w_row(n0 + row) * g.K + kk + col);
     }
   };
-  auto load_a = [&](int kt, float4* ra, float4* rg) {
-    const int kk = k_base + kt * BK;
+  auto load_a = [&](int kt) {
+    const int kk = kt * BK;
 #pragma unroll
     for (int c = 0; c < ACH; ++c) {
       const int ch = tid + c * 256, row = ch / ACR, col = (ch % ACR) * 4;
@@ -110,36 +126,35 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
   float ssq[NORM ? ACH : 1];
 #pragma unroll
   for (int c = 0; c < (NORM ? ACH : 1); ++c) ssq[c] = 0.f;
-  auto store_tiles = [&](const float4* ra, const float4* rg, const V16<T>* rb) {
+  auto store_tiles = [&](int st) {
 #pragma unroll
     for (int c = 0; c < ACH; ++c) {
-      const int ch = tid + c * 256, row = ch / ACR, col = (ch % ACR) * 4;
+      const int ch = tid + c * 256, row = ch / ACR, f = ch % ACR;  // floats 4f .. 4f + 3 of the row
       float4 av = ra[c];
       if constexpr (NORM) ssq[c] += av.x * av.x + av.y * av.y + av.z * av.z + av.w * av.w;
       if constexpr (MOD)
         av = make_float4(av.x * (1.f + rg[c].x), av.y * (1.f + rg[c].y), av.z * (1.f + rg[c].z),
                          av.w * (1.f + rg[c].w));
+      const int e = 4 * f;  // first element: chunk e / CE, offset e % CE
+      T* dst = &As[st][0][row * BK + swz<T>(row, e / CE) * CE + e % CE];
       if constexpr (kSplit) {
         uint2 hi, lo;
         split4(av, hi, lo);
-        *reinterpret_cast<uint2*>(&As[0][row * LDK + col]) = hi;
-        *reinterpret_cast<uint2*>(&As[NA - 1][row * LDK + col]) = lo;
+        *reinterpret_cast<uint2*>(dst) = hi;
+        *reinterpret_cast<uint2*>(dst + BM * BK) = lo;  // As[st][1]
       } else {
-        *reinterpret_cast<float4*>(&As[0][row * LDK + col]) = av;
+        *reinterpret_cast<float4*>(dst) = av;
       }
     }
 #pragma unroll
     for (int c = 0; c < BCH; ++c) {
-      const int ch = tid + c * 256, row = ch / WCR, col = (ch % WCR) * WPC;
-      st16(&Bs[row * LDK + col], rb[c]);
+      const int ch = tid + c * 256, row = ch / WCR, cc = ch % WCR;
+      st16(&Bs[st][row * BK + swz<T>(row, cc) * CE], rb[c]);
     }
   };
 
-  // the weight tiles do not depend on which rows are active: start them first.
-  // Ring loads are never skipped (past the end they reread the last tile) so
-  // the compiler can count the tiles in flight.
-#pragma unroll
-  for (int p = 0; p < PF; ++p) load_b(min(p, KT - 1), rb[p]);
+  // the weight tile does not depend on which rows are active: start it first
+  load_b(0);
 
   // thread t < BM resolves row r0 + t; the cache slot of a QKV row is looked
   // up here and only consumed by the epilogue, so its latency hides behind K
@@ -155,9 +170,7 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
       if (my_src >= 0) my_kv = prefill_kv_slot(g.kv, r);
   }
   if (!__syncthreads_or(my_src >= 0)) return;
-
-#pragma unroll
-  for (int p = 0; p < PF; ++p) load_a(min(p, KT - 1), ra[p], rg[MOD ? p : 0]);
+  load_a(0);
 
   f32x4 acc[MT][NT];
 #pragma unroll
@@ -165,37 +178,42 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
 #pragma unroll
     for (int j = 0; j < NT; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // K tile kt lives in ring slot kt % PF; the loop is unrolled by PF so every
-  // slot index is a compile-time constant
-  for (int kt0 = 0; kt0 < KT; kt0 += PF) {
-#pragma unroll
-    for (int p = 0; p < PF; ++p) {
-      const int kt = kt0 + p;
-      if (kt >= KT) break;
-      __syncthreads();
-      store_tiles(ra[p], rg[MOD ? p : 0], rb[p]);
-      __syncthreads();
-      load_b(min(kt + PF, KT - 1), rb[p]);
-      load_a(min(kt + PF, KT - 1), ra[p], rg[MOD ? p : 0]);
-#pragma unroll
-      for (int ks = 0; ks < BK / KS; ++ks) {
-        typename M::frag af[NA][MT], bfr[NT];
-#pragma unroll
-        for (int a = 0; a < NA; ++a)
-#pragma unroll
-          for (int i = 0; i < MT; ++i)
-            af[a][i] = M::load(&As[a][(wm * MT * 16 + i * 16 + (lane & 15)) * LDK + ks * KS + (lane >> 4) * EPL]);
-#pragma unroll
-        for (int j = 0; j < NT; ++j)
-          bfr[j] = M::load(&Bs[(wn * NT * 16 + j * 16 + (lane & 15)) * LDK + ks * KS + (lane >> 4) * EPL]);
-#pragma unroll
-        for (int a = 0; a < NA; ++a)
-#pragma unroll
-          for (int i = 0; i < MT; ++i)
-#pragma unroll
-            for (int j = 0; j < NT; ++j) acc[i][j] = M::mma(af[a][i], bfr[j], acc[i][j]);
-      }
+  // double-buffered LDS: tile kt + 1 loads into registers while tile kt is
+  // multiplied, then goes to the other stage; one barrier per tile
+  store_tiles(0);
+  __syncthreads();
+  const int frow = lane & 15, quad = lane >> 4;
+  for (int kt = 0; kt < KT; ++kt) {
+    const int st = kt & 1;
+    if (kt + 1 < KT) {
+      load_b(kt + 1);
+      load_a(kt + 1);
     }
+#pragma unroll
+    for (int ks = 0; ks < BK / KS; ++ks) {
+      const int k0 = ks * KS + quad * EPL;  // the lane's first element of this K step
+      typename M::frag af[NA][MT], bfr[NT];
+#pragma unroll
+      for (int i = 0; i < MT; ++i) {
+        const int row = wm * MT * 16 + i * 16 + frow;
+        const int off = row * BK + swz<T>(row, k0 / CE) * CE + k0 % CE;
+#pragma unroll
+        for (int a = 0; a < NA; ++a) af[a][i] = M::load(&As[st][a][off]);
+      }
+#pragma unroll
+      for (int j = 0; j < NT; ++j) {
+        const int row = wn * NT * 16 + j * 16 + frow;
+        bfr[j] = M::load(&Bs[st][row * BK + swz<T>(row, k0 / CE) * CE + k0 % CE]);
+      }
+#pragma unroll
+      for (int a = 0; a < NA; ++a)
+#pragma unroll
+        for (int i = 0; i < MT; ++i)
+#pragma unroll
+          for (int j = 0; j < NT; ++j) acc[i][j] = M::mma(af[a][i], bfr[j], acc[i][j]);
+    }
+    if (kt + 1 < KT) store_tiles(st ^ 1);
+    __syncthreads();
   }
   if constexpr (EK == E_QKV) {
     if (tid < BM) kv_base[tid] = my_kv;
@@ -214,7 +232,7 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
     __syncthreads();
   }
 
-  const int quad = lane >> 4, col16 = lane & 15;
+  const int col16 = lane & 15;
 #pragma unroll
   for (int i = 0; i < MT; ++i) {
 #pragma unroll
@@ -224,30 +242,32 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
       const int rg = r0 + rl;
       const float rs = NORM ? row_inv_s[rl] : 1.f;
       if constexpr (EK == E_LOGITS) {
-        static_assert(NT * 16 == 64, "one greedy key group per wave");
+        static_assert(NT * 16 % 64 == 0, "whole greedy key groups per wave");
         // compact rows (A_CMP) write their logits to row src(r), the sequence's
         const int orow = AK == A_CMP ? src : g.out_row_off + rg;
-        unsigned long long best = 0ull;
 #pragma unroll
-        for (int j = 0; j < NT; ++j) {
-          const int n = n0 + wn * NT * 16 + j * 16 + col16;
-          const float v = acc[i][j][r] * rs;
-          if (src >= 0 && n < g.N) {
-            reinterpret_cast<float*>(g.out)[(int64_t)orow * g.ldo + n] = v;
-            const unsigned long long key =
-                ((unsigned long long)ordered_bits(v) << 32) | (unsigned long long)(0xFFFFFFFFu - (unsigned)n);
-            best = key > best ? key : best;
-          }
-        }
-        if (g.argmax_keys) {
+        for (int j0 = 0; j0 < NT; j0 += 4) {  // one key group: 4 x 16 columns
+          unsigned long long best = 0ull;
 #pragma unroll
-          for (int o = 1; o < 16; o <<= 1) {
-            const unsigned long long other = shfl_xor(best, o);
-            best = other > best ? other : best;
+          for (int j = j0; j < j0 + 4; ++j) {
+            const int n = n0 + wn * NT * 16 + j * 16 + col16;
+            const float v = acc[i][j][r] * rs;
+            if (src >= 0 && n < g.N) {
+              reinterpret_cast<float*>(g.out)[(int64_t)orow * g.ldo + n] = v;
+              const unsigned long long key =
+                  ((unsigned long long)ordered_bits(v) << 32) | (unsigned long long)(0xFFFFFFFFu - (unsigned)n);
+              best = key > best ? key : best;
+            }
           }
-          // this wave's NT x 16 = 64 columns form one key group
-          if (col16 == 0 && src >= 0 && best != 0ull)
-            g.argmax_keys[(int64_t)orow * g.key_groups + (n0 + wn * NT * 16) / 64] = best;
+          if (g.argmax_keys) {
+#pragma unroll
+            for (int o = 1; o < 16; o <<= 1) {
+              const unsigned long long other = shfl_xor(best, o);
+              best = other > best ? other : best;
+            }
+            if (col16 == 0 && src >= 0 && best != 0ull)
+              g.argmax_keys[(int64_t)orow * g.key_groups + (n0 + wn * NT * 16 + j0 * 16) / 64] = best;
+          }
         }
       } else if constexpr (EK == E_SWIGLU) {
 #pragma unroll
@@ -296,16 +316,16 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
   }
 }
 
-template <typename T, int MT, int NT, int PF, int BK>
+template <typename T, int NT>
 hipError_t launch_tiles(const GemmArgs& a, AKind ak, EKind ek, bool norm, hipStream_t s) {
-  constexpr int BM = 2 * MT * 16, BN = 2 * NT * 16;
+  constexpr int BM = 2 * kGemmMT * 16, BN = 2 * NT * 16;
   const dim3 grid((a.N + BN - 1) / BN, (a.rm.rows + BM - 1) / BM);
   if (grid.x == 0 || grid.y == 0) return hipSuccess;
   const bool mod = a.mod_g != nullptr;
-#define TLF_GEMM_CASE(AKV, EKV, MODV, NORMV)                                                          \
-  if (ak == AKV && ek == EKV && mod == MODV && norm == NORMV) {                                       \
-    hipLaunchKernelGGL((k_gemm<T, MT, NT, PF, BK, AKV, EKV, MODV, NORMV>), grid, dim3(256), 0, s, a); \
-    return hipGetLastError();                                                                         \
+#define TLF_GEMM_CASE(AKV, EKV, MODV, NORMV)                                                \
+  if (ak == AKV && ek == EKV && mod == MODV && norm == NORMV) {                             \
+    hipLaunchKernelGGL((k_gemm<T, NT, AKV, EKV, MODV, NORMV>), grid, dim3(256), 0, s, a);   \
+    return hipGetLastError();                                                               \
   }
   TLF_GEMM_CASE(A_SRC, E_QKV, false, false)
   TLF_GEMM_CASE(A_SRC, E_QKV, true, false)
@@ -323,9 +343,11 @@ hipError_t launch_tiles(const GemmArgs& a, AKind ak, EKind ek, bool norm, hipStr
 
 template <typename T>
 hipError_t launch_gemm(const GemmArgs& a, AKind ak, EKind ek, bool norm, hipStream_t s) {
-  // 128x128 tiles, K 64 at a time, one K tile in flight
-  if (a.K % 64 != 0) return hipErrorInvalidValue;
-  return launch_tiles<T, 4, 4, 1, 64>(a, ak, ek, norm, s);
+  if (a.K % kGemmBK != 0) return hipErrorInvalidValue;
+  // a few row tiles (the decode LM head) take 128-column tiles so the grid
+  // still holds about two workgroups per compute unit; prefill takes 256
+  if ((a.rm.rows + 2 * kGemmMT * 16 - 1) / (2 * kGemmMT * 16) <= 4) return launch_tiles<T, 4>(a, ak, ek, norm, s);
+  return launch_tiles<T, 8>(a, ak, ek, norm, s);
 }
 
 template hipError_t launch_gemm<float>(const GemmArgs&, AKind, EKind, bool, hipStream_t);
