@@ -12,10 +12,10 @@ O projection, SwiGLU FFN), the LM head and the greedy pick.
 Prints one JSON line: decoded tokens/s, the decode attention's achieved HBM
 bandwidth against 8 TB/s (HIP events around every attention launch on the
 library's stream), the same kernels forced to fixed depth R, the same step
-with gather-scatter off, the step with AdaLN conditioning, time to first
-token over prompt lengths, a prefill
-measurement, the MLP-router threshold sweep, and the CPU oracle on a bounded
-sample.
+with gather-scatter off, the step with AdaLN conditioning, the batch 32 x 512
+and batch 64 x 4096 (d=2048) decode workloads, time to first token over
+prompt lengths, a prefill measurement, the MLP-router threshold sweep, and
+the CPU oracle on a bounded sample.
 """
 import argparse
 import json
@@ -295,6 +295,35 @@ def threshold_sweep(torch, tlf, synth, name, thresholds=(0.3, 0.4, 0.5, 0.6, 0.7
             "rows": rows}
 
 
+def other_workloads(torch, tlf, synth, names=("bf16_d768_b32x512", "bf16_d2048_b64x4096"),
+                    warmup=4, steps=20, profiled=4):
+    """The other decode workloads of the same family, measured like the main
+    one but briefly: decoded tokens/s over graph-replayed steps, the decode
+    attention's algorithmic bytes over its event-timed launches, and the same
+    kernels at fixed depth R."""
+    import numpy as np
+    rows = []
+    for name in names:
+        m = synth.CONFIGS[name]
+        w = synth.make_weights(m)
+        prompts = synth.make_prompts(m)
+        B, T = prompts.shape
+        row = {"workload": f"{name} decode: batch {B} x prompt {T}, {m.n_layers}-layer d={m.d_model} looped block "
+                           f"({m.n_heads}x{m.head_dim} heads, SwiGLU {m.d_ff}), R={m.max_loops}"}
+        for rule in ("argmax", "fixed"):
+            ms, (_, st), pre_s, hist = run_config(torch, tlf, m, w, prompts, warmup, steps, profiled,
+                                                  route_rule=rule, fixed_depth=m.max_loops)
+            gbs = st["attn_algo_bytes"] / (st["attn_ms"] / 1e3) / 1e9
+            h = np.asarray(hist, dtype=np.float64)
+            rec = {"tokens_per_s": B * steps / (ms / 1e3), "ms_per_step": ms / steps, "attn_achieved_gbs": gbs,
+                   "attn_frac": gbs / HBM_PEAK_GBS, "mean_depth": float((h * np.arange(1, len(h) + 1)).sum() / h.sum()),
+                   "prefill_s": pre_s}
+            row["routed" if rule == "argmax" else "fixed_depth"] = rec
+            log(f"{name} {rule}: {ms / steps:.3f} ms/step, attention {gbs:.0f} GB/s")
+        rows.append(row)
+    return {"steps": steps, "rows": rows}
+
+
 def prefill_measure(torch, tlf, synth, name):
     """Prefill-only workload: time tlf_prefill and count the algorithmic FLOPs."""
     import numpy as np
@@ -421,6 +450,8 @@ def main():
     ap.add_argument("--no-ablation", action="store_true", help="skip the gather-scatter-off decode")
     ap.add_argument("--no-ttft", action="store_true", help="skip the time-to-first-token sweep")
     ap.add_argument("--no-adaln", action="store_true", help="skip the AdaLN-conditioned decode")
+    ap.add_argument("--no-others", action="store_true",
+                    help="skip the batch 32 x 512 and batch 64 x 4096 (d=2048) decode workloads")
     ap.add_argument("--prefill-only", action="store_true",
                     help="run only the prefill measurement (batch 8 x 4096) and print its JSON")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
@@ -546,6 +577,8 @@ def main():
     if not args.no_adaln:
         out["adaln"] = adaln_decode(torch, tlf, synth, args.config, ms / args.steps)
         log(f"adaln: {out['adaln']['ms_per_step']:.3f} ms/step")
+    if not args.no_others:
+        out["other_workloads"] = other_workloads(torch, tlf, synth)
     if not args.no_ttft:
         out["ttft"] = ttft_sweep(torch, tlf, model, w, synth)
     if not args.no_prefill:
