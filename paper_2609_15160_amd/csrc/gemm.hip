@@ -233,6 +233,58 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs g) {
   }
 
   const int col16 = lane & 15;
+  if constexpr (EK == E_QKV) {
+    // q to its buffer; k and v into the cache pages.  A lane holds rows
+    // 4 quad .. 4 quad + 3 of its column: when they are consecutive slots
+    // of one page from a multiple of 4 (a fresh prefill), their four v
+    // values of that dimension are one aligned run in the transposed V
+    // block and go out as one store; otherwise element by element.
+    T* pool = reinterpret_cast<T*>(g.kv.c.pool);
+#pragma unroll
+    for (int i = 0; i < MT; ++i) {
+      const int rl0 = wm * MT * 16 + i * 16 + quad * 4;
+#pragma unroll
+      for (int j = 0; j < NT; ++j) {
+        const int n = n0 + wn * NT * 16 + j * 16 + col16;
+        if (n >= g.N) continue;
+        if (n < g.d) {
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            if (row_src_s[rl0 + r] >= 0) reinterpret_cast<float*>(g.out)[(int64_t)(r0 + rl0 + r) * g.ldo + n] = acc[i][j][r];
+          continue;
+        }
+        const int nn = n - g.d, kvsel = nn / g.d, within = nn % g.d;
+        const int h = within / g.kv.c.D, e = within % g.kv.c.D;
+        const int64_t b0 = kv_base[rl0];
+        const bool run4 = kvsel == 1 && b0 >= 0 && (b0 & 3) == 0 && kv_base[rl0 + 1] == b0 + 1 &&
+                          kv_base[rl0 + 2] == b0 + 2 && kv_base[rl0 + 3] == b0 + 3;
+        if (run4) {
+          const int slot = (int)(b0 & (kPage - 1));
+          T* dst = pool + (b0 - slot) + v_block(g.kv.c, g.kv.layer, h) + (int64_t)e * kPage + slot;
+          if constexpr (sizeof(T) == 2) {
+            *reinterpret_cast<uint2*>(dst) = make_uint2(pack_bf16x2(acc[i][j][0], acc[i][j][1]),
+                                                        pack_bf16x2(acc[i][j][2], acc[i][j][3]));
+          } else {
+            *reinterpret_cast<float4*>(dst) = make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
+          }
+          continue;
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int64_t base = kv_base[rl0 + r];
+          if (base < 0) continue;
+          const int slot = (int)(base & (kPage - 1));
+          const int64_t page = base - slot;
+          const float v = acc[i][j][r];
+          if (kvsel == 0)
+            pool[page + k_block(g.kv.c, g.kv.layer, h) + k_frag_off<T>(slot, e)] = from_f<T>(v);
+          else
+            pool[page + v_block(g.kv.c, g.kv.layer, h) + (int64_t)e * kPage + slot] = from_f<T>(v);
+        }
+      }
+    }
+    return;
+  }
 #pragma unroll
   for (int i = 0; i < MT; ++i) {
 #pragma unroll
@@ -289,26 +341,9 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs g) {
           if constexpr (EK == E_RESID) {
             const float gate = g.mod_a ? 1.f + g.mod_a[row_mod_s[rl] + n] : 1.f;
             reinterpret_cast<float*>(g.out)[(int64_t)src * g.ldo + n] += gate * v;
-          } else if constexpr (EK == E_HIDDEN) {
+          } else {  // E_HIDDEN
             const float u = v + g.bias[n];
             g.out[(int64_t)rg * g.ldo + n] = u / (1.f + __expf(-u));
-          } else {  // E_QKV
-            if (n < g.d) {
-              reinterpret_cast<float*>(g.out)[(int64_t)rg * g.ldo + n] = v;
-            } else {
-              const int64_t base = kv_base[rl];
-              if (base >= 0) {
-                const int slot = (int)(base & (kPage - 1));
-                const int64_t page = base - slot;
-                const int nn = n - g.d, kvsel = nn / g.d, within = nn % g.d;
-                const int h = within / g.kv.c.D, e = within % g.kv.c.D;
-                T* pool = reinterpret_cast<T*>(g.kv.c.pool);
-                if (kvsel == 0)
-                  pool[page + k_block(g.kv.c, g.kv.layer, h) + k_frag_off<T>(slot, e)] = from_f<T>(v);
-                else
-                  pool[page + v_block(g.kv.c, g.kv.layer, h) + (int64_t)e * kPage + slot] = from_f<T>(v);
-              }
-            }
           }
         }
       }
