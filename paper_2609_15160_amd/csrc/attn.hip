@@ -91,7 +91,7 @@ __global__ __launch_bounds__(W * 64) void k_attn_decode(AttnDecodeArgs a) {
     const int per = ((np + W - 1) / W + PPI - 1) / PPI * PPI;
     const int p0 = w * per, p1 = min(np, p0 + per);
     const int64_t koff = k_block(c, a.layer, h) + (int64_t)(quad * kPage + c16) * EPL;  // fragment order
-    const int64_t voff = v_block(c, a.layer, h) + (int64_t)c16 * kPage + quad * 4;
+    const int64_t voff = v_block(c, a.layer, h) + (int64_t)(quad * D + c16) * 4;  // slots 4 quad .. + 3 of dim c16
 
     // q (float32) as the B operand of S = K q^T, the same in all 16 columns;
     // against bf16 keys it is split into hi and lo parts, one product each
@@ -122,7 +122,7 @@ __global__ __launch_bounds__(W * 64) void k_attn_decode(AttnDecodeArgs a) {
       }
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) {
-        const int64_t off = voff + (int64_t)dt * 16 * kPage;
+        const int64_t off = voff + (int64_t)dt * 16 * 4;
         if constexpr (EPL == 8) {
           const u32x2 lo = ld_stream<u32x2>(base[0] + off);
           const u32x2 hi = ld_stream<u32x2>(base[PPI - 1] + off);
@@ -263,10 +263,10 @@ __global__ __launch_bounds__(256, 4) void k_attn_prefill(AttnPrefillArgs a) {
   constexpr int CH = 2 * 4 * KBLK / EPC;          // 16-byte chunks of one K + V tile
   static_assert(CH % 256 == 0, "tile chunks per thread");
   constexpr int CPT = CH / 256;
-  static_assert(kPage % EPC == 0, "V chunk inside one dimension row");
+  static_assert(EPC % 4 == 0 && (4 * D) % EPC == 0, "V chunk: whole 4-slot groups of one slot group");
   // K tile: four pages' K blocks verbatim (fragment order: lane (key, quad) of a
   // K step reads EPL contiguous elements, 64 lanes one contiguous run);
-  // V tile: four pages' V blocks [dim][slot], rows padded against bank conflicts
+  // V tile: four pages' V blocks rearranged to [dim][slot] rows, padded against bank conflicts
   __shared__ __align__(16) T Ks[2][4 * KBLK];
   __shared__ __align__(16) T Vs[2][4 * D * VLD];
 
@@ -341,10 +341,16 @@ __global__ __launch_bounds__(256, 4) void k_attn_prefill(AttnPrefillArgs a) {
       if (kv == 0) {
         *reinterpret_cast<uint4*>(&Ks[buf][p * KBLK + off]) = pre[u];
       } else {
-        const int dim = off / kPage, slot = off % kPage;  // EPC slots of one dimension
-        T* dst = &Vs[buf][(p * D + dim) * VLD + slot];
-        *reinterpret_cast<uint2*>(dst) = make_uint2(pre[u].x, pre[u].y);
-        *reinterpret_cast<uint2*>(dst + EPC / 2) = make_uint2(pre[u].z, pre[u].w);
+        // the chunk holds slots 4 g4 .. 4 g4 + 3 of EPC / 4 consecutive dimensions
+        const int g4 = off / (4 * D), d0 = (off % (4 * D)) / 4;
+        if constexpr (sizeof(T) == 2) {
+          *reinterpret_cast<uint2*>(&Vs[buf][(p * D + d0) * VLD + 4 * g4]) = make_uint2(pre[u].x, pre[u].y);
+          *reinterpret_cast<uint2*>(&Vs[buf][(p * D + d0 + 1) * VLD + 4 * g4]) = make_uint2(pre[u].z, pre[u].w);
+        } else {
+          T* dst = &Vs[buf][(p * D + d0) * VLD + 4 * g4];
+          *reinterpret_cast<uint2*>(dst) = make_uint2(pre[u].x, pre[u].y);
+          *reinterpret_cast<uint2*>(dst + 2) = make_uint2(pre[u].z, pre[u].w);
+        }
       }
     }
   };

@@ -51,10 +51,11 @@ struct CacheView {
 
 // Page layout: for each layer j and head h a K block of kPage x D elements
 // in MFMA-fragment order (k_frag_off below), followed, after all heads' K
-// blocks, by V blocks stored transposed, [D][kPage slots], so that one
-// dimension of four consecutive slots is a single 8- or 16-byte load.
+// blocks, by V blocks in groups of four slots, [kPage / 4][D][4] (v_frag_off
+// below): one dimension of four consecutive slots is a single 8- or 16-byte
+// load, and the D values of one slot lie four elements apart.
 //   K(j, h, slot, e) = k_block(j, h) + k_frag_off<T>(slot, e)
-//   V(j, h, slot, e) = v_block(j, h) + e * kPage + slot
+//   V(j, h, slot, e) = v_block(j, h) + v_frag_off(slot, e, D)
 __device__ __forceinline__ int64_t k_block(const CacheView& c, int j, int h) {
   return (int64_t)((j * 2 + 0) * c.H + h) * kPage * c.D;
 }
@@ -159,6 +160,9 @@ template <typename T> __device__ __forceinline__ int k_frag_off(int slot, int e)
   const int ks = e / KS, q = (e % KS) / EPL, j = e % EPL;
   return ((ks * 4 + q) * kPage + slot) * EPL + j;
 }
+
+// Offset of V(slot, e) inside a V block: [slot / 4][D][slot % 4].
+__device__ __forceinline__ int v_frag_off(int slot, int e, int D) { return ((slot >> 2) * D + e) * 4 + (slot & 3); }
 
 __device__ __forceinline__ int lane_id() { return threadIdx.x & (kWave - 1); }
 

@@ -367,7 +367,7 @@ __device__ __forceinline__ void dgemm_tile(const GemmArgs& g, int nact, int act_
           if (kvsel == 0)
             pool[page + k_block(g.kv.c, g.kv.layer, h) + k_frag_off<T>(slot, el)] = from_f<T>(v);
           else
-            pool[page + v_block(g.kv.c, g.kv.layer, h) + (int64_t)el * kPage + slot] = from_f<T>(v);
+            pool[page + v_block(g.kv.c, g.kv.layer, h) + v_frag_off(slot, el, g.kv.c.D)] = from_f<T>(v);
         }
       }
     }

@@ -237,8 +237,8 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs g) {
     // q to its buffer; k and v into the cache pages.  A lane holds rows
     // 4 quad .. 4 quad + 3 of its column: when they are consecutive slots
     // of one page from a multiple of 4 (a fresh prefill), their four v
-    // values of that dimension are one aligned run in the transposed V
-    // block and go out as one store; otherwise element by element.
+    // values of that dimension are one aligned run in the V block and go
+    // out as one store; otherwise element by element.
     T* pool = reinterpret_cast<T*>(g.kv.c.pool);
 #pragma unroll
     for (int i = 0; i < MT; ++i) {
@@ -260,7 +260,7 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs g) {
                           kv_base[rl0 + 2] == b0 + 2 && kv_base[rl0 + 3] == b0 + 3;
         if (run4) {
           const int slot = (int)(b0 & (kPage - 1));
-          T* dst = pool + (b0 - slot) + v_block(g.kv.c, g.kv.layer, h) + (int64_t)e * kPage + slot;
+          T* dst = pool + (b0 - slot) + v_block(g.kv.c, g.kv.layer, h) + v_frag_off(slot, e, g.kv.c.D);
           if constexpr (sizeof(T) == 2) {
             *reinterpret_cast<uint2*>(dst) = make_uint2(pack_bf16x2(acc[i][j][0], acc[i][j][1]),
                                                         pack_bf16x2(acc[i][j][2], acc[i][j][3]));
@@ -279,7 +279,7 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs g) {
           if (kvsel == 0)
             pool[page + k_block(g.kv.c, g.kv.layer, h) + k_frag_off<T>(slot, e)] = from_f<T>(v);
           else
-            pool[page + v_block(g.kv.c, g.kv.layer, h) + (int64_t)e * kPage + slot] = from_f<T>(v);
+            pool[page + v_block(g.kv.c, g.kv.layer, h) + v_frag_off(slot, e, g.kv.c.D)] = from_f<T>(v);
         }
       }
     }
