@@ -36,11 +36,14 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan_decode(DecodePlanArgs a) 
   __shared__ int s_carry, s_total, s_oom;
   __shared__ unsigned long long hist[kMaxLoops];
   __shared__ unsigned long long s_kvread, s_kvwrite;
-  __shared__ int s_maxm, s_top;
+  __shared__ int s_maxm, s_top, s_base;
+  __shared__ int s_nact[kMaxLoops];
 
-  if (tid <= kMaxLoops) { cnt[tid] = 0; fill[tid] = 0; }
-  if (tid < kMaxLoops) hist[tid] = 0ull;
-  if (tid == 0) { s_kvread = 0ull; s_kvwrite = 0ull; s_maxm = 0; s_oom = 0; s_carry = 0; }
+  // the global reads of the first kPlanThreads sequences (every batch up to
+  // that size) are issued here: depth, sequence length, the R cache lengths
+  // and the allocator in one round trip, then the page-table entry of each
+  // cache's partly filled last page; sequences beyond (chunks >= 1) read
+  // theirs where they are used
   int m_of[kPlanChunks], row_of[kPlanChunks];
 #pragma unroll
   for (int ch = 0; ch < kPlanChunks; ++ch) {
@@ -48,6 +51,25 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan_decode(DecodePlanArgs a) 
     m_of[ch] = b < B ? a.depth[b] : 0;
     row_of[ch] = -1;
   }
+  int seq0, len0[kMaxLoops], page0[kMaxLoops];
+  {
+    const bool in = tid < B;
+    seq0 = in ? c.seq_len[tid] : 0;
+#pragma unroll
+    for (int i = 0; i < kMaxLoops; ++i) len0[i] = in && i < R ? c.cache_len[tid * R + i] : 0;
+  }
+  const int base0 = tid == 0 ? *c.page_next : 0;
+#pragma unroll
+  for (int i = 0; i < kMaxLoops; ++i)
+    page0[i] = (i < m_of[0] && len0[i] % kPage != 0)
+                   ? c.page_table[((int64_t)tid * R + i) * c.pages_per_seq + len0[i] / kPage]
+                   : -1;
+  auto len_at = [&](int ch, int b, int i) __attribute__((always_inline)) {
+    return ch == 0 ? len0[i] : c.cache_len[b * R + i];
+  };
+  if (tid <= kMaxLoops) { cnt[tid] = 0; fill[tid] = 0; }
+  if (tid < kMaxLoops) hist[tid] = 0ull;
+  if (tid == 0) { s_kvread = 0ull; s_kvwrite = 0ull; s_maxm = 0; s_oom = 0; s_carry = 0; s_base = base0; }
   __syncthreads();
 #pragma unroll
   for (int ch = 0; ch < kPlanChunks; ++ch)
@@ -56,7 +78,11 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan_decode(DecodePlanArgs a) 
   if (tid == 0) {
     int s = 0, top = 0;
     for (int m = R; m >= 1; --m) { start[m] = s; s += cnt[m]; if (top == 0 && cnt[m] > 0) top = m; }
-    for (int i = 1; i <= R; ++i) a.nact[i - 1] = a.dense ? (i <= top ? B : 0) : start[i] + cnt[i];  // n_i = #{m >= i}
+    for (int i = 1; i <= R; ++i) {
+      const int n = a.dense ? (i <= top ? B : 0) : start[i] + cnt[i];  // n_i = #{m >= i}
+      a.nact[i - 1] = n;
+      s_nact[i - 1] = n;
+    }
     s_top = top;
   }
   __syncthreads();
@@ -103,7 +129,7 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan_decode(DecodePlanArgs a) 
     int need = 0;
 #pragma unroll
     for (int i = 0; i < kMaxLoops; ++i)
-      if (i < m) need += (c.cache_len[b * R + i] % kPage) == 0;
+      if (i < m) need += (len_at(ch, b, i) % kPage) == 0;
     need_of[ch] = need;
     int tot;
     block_exclusive_scan(need, scan_tmp, &tot);
@@ -112,7 +138,7 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan_decode(DecodePlanArgs a) 
   }
   if (tid == 0) {
     s_total = s_carry;
-    const int base = *c.page_next;
+    const int base = s_base;
     if ((int64_t)base + s_total > c.max_pages) {
       s_oom = 1;
       set_err(c.err, kErrOutOfPages);
@@ -133,15 +159,17 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan_decode(DecodePlanArgs a) 
       const int lim = a.dense ? top : m;  // loops whose cache this row reads
 #pragma unroll
       for (int i = 0; i < kMaxLoops; ++i) {
-        len[i] = i < lim ? c.cache_len[b * R + i] : 0;
-        page[i] = -1;
+        len[i] = i < lim ? len_at(ch, b, i) : 0;
+        page[i] = ch == 0 ? page0[i] : -1;
       }
+      if (ch > 0) {
 #pragma unroll
-      for (int i = 0; i < kMaxLoops; ++i)
-        if (i < m && len[i] % kPage != 0)
-          page[i] = c.page_table[((int64_t)b * R + i) * c.pages_per_seq + len[i] / kPage];
+        for (int i = 0; i < kMaxLoops; ++i)
+          if (i < m && len[i] % kPage != 0)
+            page[i] = c.page_table[((int64_t)b * R + i) * c.pages_per_seq + len[i] / kPage];
+      }
       int next = s_carry + ex;
-      const int t = c.seq_len[b];
+      const int t = ch == 0 ? seq0 : c.seq_len[b];
       unsigned long long rd = 0ull;
 #pragma unroll
       for (int i = 0; i < kMaxLoops; ++i) {
@@ -164,7 +192,7 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan_decode(DecodePlanArgs a) 
       atomicAdd(&s_kvwrite, (unsigned long long)m);
     }
     if (m > 0) {
-      c.seq_len[b] += 1;
+      c.seq_len[b] = (ch == 0 ? seq0 : c.seq_len[b]) + 1;
       atomicAdd(&hist[m - 1], 1ull);
       atomicMax(&s_maxm, m);
     }
@@ -196,8 +224,7 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan_decode(DecodePlanArgs a) 
   if (s_oom) {  // the step becomes a no-op for the block: no active rows
     if (tid < R) a.nact[tid] = 0;
   }
-  __syncthreads();
-  if (tid < R) c.step_stats[kStatRows + tid] = a.nact[tid];
+  if (tid < R) c.step_stats[kStatRows + tid] = s_oom ? 0 : s_nact[tid];
 }
 
 // ---------------------------------------------------------------------------

@@ -12,6 +12,7 @@ namespace tlf {
 namespace {
 
 constexpr int kRowChunks = 16;  // 16 x 256 elements: rows up to 4096 wide
+constexpr int kNormChunks = 4;  // 4 x 1024 elements: rows up to 4096 wide (RMSNorm, a workgroup per row)
 
 template <int CTRL>
 __device__ __forceinline__ float dpp(float x) {
@@ -90,65 +91,75 @@ __device__ void decide_depth(const float* z, int R, int rule, float threshold, i
   *margin_out = margin;
 }
 
+// Row kernels take the number of 256-element chunks of a row (NC) as a
+// template argument and load every chunk unconditionally, the element index
+// clamped into the row (the tail's surplus lanes read the row's last four
+// elements, finite values, and multiply them by zero: a select would let the
+// compiler move each load under a branch again), so all of a row's loads are
+// in flight at once instead of one guarded chunk after another.
+__device__ __forceinline__ int clamp_k(int k, int n) { return k < n ? k : n - 4; }
+
 // ---------------------------------------------------------------------------
 // h0 = E[x] + P[pos] (learned absolute position added once, Section 3.2),
 // z = W_r h0 + b_r (Eq. 2's router as a linear map), the depth rule, and
 // y = RMSNorm(h0) for the first projection.  One wave per row; lane l holds
 // elements 4l + 256c.
 // ---------------------------------------------------------------------------
-template <typename T>
+template <typename T, int NC>
 __global__ __launch_bounds__(256) void k_embed_route(EmbedArgs a) {
   const int lane = lane_id();
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= a.rows) return;
+  // both row reads in one round trip (prefill reads its token twice instead
+  // of a branch around the sequence length)
   int tok = a.tokens[row];
+  const int sl = (a.prefill_T > 0 ? a.tokens : a.seq_len)[row];
   if (tok < 0 || tok >= a.V) {
     if (lane == 0) set_err(a.err, kErrBadToken);
     tok = 0;
   }
-  const int pos = a.prefill_T > 0 ? a.pos0 + row % a.prefill_T : a.seq_len[row];
+  const int pos = a.prefill_T > 0 ? a.pos0 + row % a.prefill_T : sl;
   const T* e = reinterpret_cast<const T*>(a.tok_emb) + (int64_t)tok * a.d;
   const T* p = reinterpret_cast<const T*>(a.pos_emb) + (int64_t)pos * a.d;
   float* x = a.x + (int64_t)row * a.d;
-  float4 h[kRowChunks];
+  float4 h[NC];
   float ss = 0.f;
-  float z[kMaxLoops];
 #pragma unroll
-  for (int i = 0; i < kMaxLoops; ++i) z[i] = 0.f;
-#pragma unroll
-  for (int c = 0; c < kRowChunks; ++c) {
-    const int k = 4 * lane + 256 * c;
-    if (k < a.d) {
-      const float4 ev = V4<T>::load(e + k), pv = V4<T>::load(p + k);
-      h[c] = make_float4(ev.x + pv.x, ev.y + pv.y, ev.z + pv.z, ev.w + pv.w);
-    }
+  for (int c = 0; c < NC; ++c) {
+    const int k = 4 * lane + 256 * c, kk = clamp_k(k, a.d);
+    const float4 ev = V4<T>::load(e + kk), pv = V4<T>::load(p + kk);
+    h[c] = scale4(make_float4(ev.x + pv.x, ev.y + pv.y, ev.z + pv.z, ev.w + pv.w), k < a.d ? 1.f : 0.f);
+    ss = sumsq(h[c], ss);
   }
 #pragma unroll
-  for (int c = 0; c < kRowChunks; ++c) {
+  for (int c = 0; c < NC; ++c) {
     const int k = 4 * lane + 256 * c;
-    if (k < a.d) {
-      V4<float>::store(x + k, h[c]);
-      ss = sumsq(h[c], ss);
-#pragma unroll
-      for (int i = 0; i < kMaxLoops; ++i) {
-        if (a.route && i < a.R) {
-          const float4 w = V4<float>::load(a.Wr + (int64_t)i * a.d + k);
-          z[i] = fmaf(w.w, h[c].w, fmaf(w.z, h[c].z, fmaf(w.y, h[c].y, fmaf(w.x, h[c].x, z[i]))));
-        }
-      }
-    }
+    if (k < a.d) V4<float>::store(x + k, h[c]);
   }
   ss = wave_sum(ss);
   const float inv = rsqrtf(ss / (float)a.d + a.eps);
   if (a.y) {
     float* y = a.y + (int64_t)row * a.d;
 #pragma unroll
-    for (int c = 0; c < kRowChunks; ++c) {
+    for (int c = 0; c < NC; ++c) {
       const int k = 4 * lane + 256 * c;
       if (k < a.d) V4<float>::store(y + k, scale4(h[c], inv));
     }
   }
   if (!a.route) return;  // the MLP router runs after this kernel
+  float z[kMaxLoops];
+#pragma unroll
+  for (int i = 0; i < kMaxLoops; ++i) {
+    // rows of W_r past R repeat row 0; their sums are never used
+    const float* wr = a.Wr + (int64_t)(i < a.R ? i : 0) * a.d;
+    float acc = 0.f;
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      const float4 w = V4<float>::load(wr + clamp_k(4 * lane + 256 * c, a.d));
+      acc = fmaf(w.w, h[c].w, fmaf(w.z, h[c].z, fmaf(w.y, h[c].y, fmaf(w.x, h[c].x, acc))));
+    }
+    z[i] = acc;
+  }
 #pragma unroll
   for (int i = 0; i < kMaxLoops; ++i)
     if (i < a.R) z[i] = wave_sum(z[i]) + a.br[i];
@@ -165,27 +176,29 @@ __global__ __launch_bounds__(256) void k_embed_route(EmbedArgs a) {
 // Output layer of the MLP router on hidden rows (z = W_r h + b_r), then the
 // depth rule.  One wave per row; lane l holds elements 4l + 256c.
 // ---------------------------------------------------------------------------
+template <int NC>
 __global__ __launch_bounds__(256) void k_route_rows(RouteArgs a) {
   const int lane = lane_id();
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= a.rows) return;
   const float* h = a.h + (int64_t)row * a.Hr;
+  float4 hv[NC];
+#pragma unroll
+  for (int c = 0; c < NC; ++c) {
+    const int k = 4 * lane + 256 * c;
+    hv[c] = scale4(V4<float>::load(h + clamp_k(k, a.Hr)), k < a.Hr ? 1.f : 0.f);
+  }
   float z[kMaxLoops];
 #pragma unroll
-  for (int i = 0; i < kMaxLoops; ++i) z[i] = 0.f;
+  for (int i = 0; i < kMaxLoops; ++i) {
+    const float* wr = a.Wr + (int64_t)(i < a.R ? i : 0) * a.Hr;
+    float acc = 0.f;
 #pragma unroll
-  for (int c = 0; c < kRowChunks; ++c) {
-    const int k = 4 * lane + 256 * c;
-    if (k < a.Hr) {
-      const float4 hv = V4<float>::load(h + k);
-#pragma unroll
-      for (int i = 0; i < kMaxLoops; ++i) {
-        if (i < a.R) {
-          const float4 w = V4<float>::load(a.Wr + (int64_t)i * a.Hr + k);
-          z[i] = fmaf(w.w, hv.w, fmaf(w.z, hv.z, fmaf(w.y, hv.y, fmaf(w.x, hv.x, z[i]))));
-        }
-      }
+    for (int c = 0; c < NC; ++c) {
+      const float4 w = V4<float>::load(wr + clamp_k(4 * lane + 256 * c, a.Hr));
+      acc = fmaf(w.w, hv[c].w, fmaf(w.z, hv[c].z, fmaf(w.y, hv[c].y, fmaf(w.x, hv[c].x, acc))));
     }
+    z[i] = acc;
   }
 #pragma unroll
   for (int i = 0; i < kMaxLoops; ++i)
@@ -202,10 +215,9 @@ __global__ __launch_bounds__(256) void k_route_rows(RouteArgs a) {
 // ---------------------------------------------------------------------------
 // y[src(r)] = RMSNorm(x[src(r)]) for the active rows of a row map (prefill,
 // after each residual projection).  One workgroup per row: thread t holds
-// elements 4t + 1024c.
+// elements 4t + 1024c, c < NC.
 // ---------------------------------------------------------------------------
-constexpr int kNormChunks = 4;  // 4 x 1024 elements per row
-
+template <int NC>
 __global__ __launch_bounds__(256) void k_resid_norm(ResidNormArgs a) {
   __shared__ float s_part[4];
   const int r = blockIdx.x;
@@ -213,15 +225,13 @@ __global__ __launch_bounds__(256) void k_resid_norm(ResidNormArgs a) {
   const int tid = threadIdx.x, lane = lane_id(), w = tid >> 6;
   const int src = row_src(a.rm, r);
   const float* x = a.x + (int64_t)src * a.d;
-  float4 h[kNormChunks];
+  float4 h[NC];
   float ss = 0.f;
 #pragma unroll
-  for (int c = 0; c < kNormChunks; ++c) {
+  for (int c = 0; c < NC; ++c) {
     const int k = 4 * tid + 1024 * c;
-    if (k < a.d) {
-      h[c] = V4<float>::load(x + k);
-      ss = sumsq(h[c], ss);
-    }
+    h[c] = scale4(V4<float>::load(x + clamp_k(k, a.d)), k < a.d ? 1.f : 0.f);
+    ss = sumsq(h[c], ss);
   }
   ss = wave_sum(ss);
   if (lane == 0) s_part[w] = ss;
@@ -230,7 +240,7 @@ __global__ __launch_bounds__(256) void k_resid_norm(ResidNormArgs a) {
   const float inv = rsqrtf(ss / (float)a.d + a.eps);
   float* y = a.y + (int64_t)src * a.d;
 #pragma unroll
-  for (int c = 0; c < kNormChunks; ++c) {
+  for (int c = 0; c < NC; ++c) {
     const int k = 4 * tid + 1024 * c;
     if (k < a.d) V4<float>::store(y + k, scale4(h[c], inv));
   }
@@ -238,9 +248,24 @@ __global__ __launch_bounds__(256) void k_resid_norm(ResidNormArgs a) {
 
 }  // namespace
 
+// Launches kernel K<NC> for NC = n, 1 <= n <= 16.
+#define TLF_NC_SWITCH(n, LAUNCH)                                                                   \
+  switch (n) {                                                                                     \
+    case 1: LAUNCH(1); break;   case 2: LAUNCH(2); break;   case 3: LAUNCH(3); break;             \
+    case 4: LAUNCH(4); break;   case 5: LAUNCH(5); break;   case 6: LAUNCH(6); break;             \
+    case 7: LAUNCH(7); break;   case 8: LAUNCH(8); break;   case 9: LAUNCH(9); break;             \
+    case 10: LAUNCH(10); break; case 11: LAUNCH(11); break; case 12: LAUNCH(12); break;           \
+    case 13: LAUNCH(13); break; case 14: LAUNCH(14); break; case 15: LAUNCH(15); break;           \
+    case 16: LAUNCH(16); break;                                                                    \
+    default: return hipErrorInvalidValue;                                                          \
+  }
+
 template <typename T> hipError_t launch_embed_route(const EmbedArgs& a, hipStream_t s) {
   if (a.rows <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_embed_route<T>, dim3((a.rows + 3) / 4), dim3(256), 0, s, a);
+  if (a.d <= 0 || a.d % 4 != 0 || a.d > 256 * kRowChunks) return hipErrorInvalidValue;
+#define TLF_EMBED(NC) hipLaunchKernelGGL((k_embed_route<T, NC>), dim3((a.rows + 3) / 4), dim3(256), 0, s, a)
+  TLF_NC_SWITCH((a.d + 255) / 256, TLF_EMBED)
+#undef TLF_EMBED
   return hipGetLastError();
 }
 template hipError_t launch_embed_route<float>(const EmbedArgs&, hipStream_t);
@@ -248,7 +273,15 @@ template hipError_t launch_embed_route<bf16>(const EmbedArgs&, hipStream_t);
 
 template <typename T> hipError_t launch_resid_norm(const ResidNormArgs& a, hipStream_t s) {
   if (a.rm.rows <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_resid_norm, dim3(a.rm.rows), dim3(256), 0, s, a);
+  if (a.d <= 0 || a.d % 4 != 0 || a.d > 1024 * kNormChunks) return hipErrorInvalidValue;
+#define TLF_NORM(NC) hipLaunchKernelGGL((k_resid_norm<NC>), dim3(a.rm.rows), dim3(256), 0, s, a)
+  switch ((a.d + 1023) / 1024) {
+    case 1: TLF_NORM(1); break;
+    case 2: TLF_NORM(2); break;
+    case 3: TLF_NORM(3); break;
+    default: TLF_NORM(4); break;
+  }
+#undef TLF_NORM
   return hipGetLastError();
 }
 template hipError_t launch_resid_norm<float>(const ResidNormArgs&, hipStream_t);
@@ -256,9 +289,12 @@ template hipError_t launch_resid_norm<bf16>(const ResidNormArgs&, hipStream_t);
 
 hipError_t launch_route_rows(const RouteArgs& a, hipStream_t s) {
   if (a.rows <= 0) return hipSuccess;
-  if (a.Hr > 4 * kWave * kRowChunks || a.Hr % 4 != 0) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_route_rows, dim3((a.rows + 3) / 4), dim3(256), 0, s, a);
+  if (a.Hr <= 0 || a.Hr > 4 * kWave * kRowChunks || a.Hr % 4 != 0) return hipErrorInvalidValue;
+#define TLF_ROUTE(NC) hipLaunchKernelGGL((k_route_rows<NC>), dim3((a.rows + 3) / 4), dim3(256), 0, s, a)
+  TLF_NC_SWITCH((a.Hr + 255) / 256, TLF_ROUTE)
+#undef TLF_ROUTE
   return hipGetLastError();
 }
+#undef TLF_NC_SWITCH
 
 }  // namespace tlf
