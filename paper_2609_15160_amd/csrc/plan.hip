@@ -6,40 +6,46 @@ namespace tlf {
 namespace {
 
 // ---------------------------------------------------------------------------
-// Decode planner: one workgroup of kPlanThreads threads, thread t owning
-// sequences t, t + kPlanThreads, ...  Steps:
+// Decode planner: one workgroup of NT threads (the batch rounded up to whole
+// waves, at most kPlanThreads), thread t owning sequences t, t + NT, ...
+// Steps:
 //   1. depth-sorted order, deepest first and stable in b, by a counting sort
 //      whose ranks come from wave ballots: A_i = rows [0, n_i) (Eq. 4-6);
 //   2. one new page for every executed (b, i) whose next slot starts a page,
 //      numbered by a block prefix sum (deterministic);
-//   3. per executed (b, i): the slot's position, cache_len += 1, and the
-//      slot's element offset for the QKV epilogue, by compact row;
-//   4. statistics.
+//   3. statistics;
+//   4. per executed (b, i): the slot's position, cache_len += 1, and the
+//      slot's element offset for the QKV epilogue, by compact row.
+// All global reads are issued at the start and all slot stores come last,
+// after the final barrier (a barrier waits for outstanding stores).
 // Dense mode (gather-scatter off): rows stay in batch order and every loop up
 // to the deepest token of the step has all B rows; the rows of exited tokens
 // get kv_slot -1 (no cache entry) and their attention reads the cache as it
 // stands, which the statistics count.
-// Every sequence's cache lengths and page-table entries are loaded together
-// (unrolled over loops), so a step costs a few memory round trips.
 // ---------------------------------------------------------------------------
 constexpr int kPlanWaves = kPlanThreads / kWave;
-constexpr int kPlanChunks = 4;  // kPlanThreads * kPlanChunks >= max batch
+
+// Running totals of the step statistics: an atomic add returns nothing to
+// wait for, where a read-modify-write would cost a memory round trip.
+__device__ __forceinline__ void add_stat(long long* p, unsigned long long v) {
+  atomicAdd(reinterpret_cast<unsigned long long*>(p), v);
+}
+constexpr int kPlanChunks = 4;  // kPlanThreads * kPlanChunks >= max batch (NT = kPlanThreads above kPlanThreads sequences)
 
 __global__ __launch_bounds__(kPlanThreads) void k_plan_decode(DecodePlanArgs a) {
   const CacheView& c = a.c;
   const int tid = threadIdx.x, lane = lane_id(), wv = tid >> 6, B = a.B, R = c.R;
+  const int NT = blockDim.x, NW = NT / kWave;  // threads (a multiple of the wave) and waves
   __shared__ int cnt[kMaxLoops + 1];
   __shared__ int start[kMaxLoops + 1];
   __shared__ int fill[kMaxLoops + 1];
   __shared__ int wcnt[kPlanWaves][kMaxLoops + 1];
   __shared__ int scan_tmp[kPlanWaves + 1];
-  __shared__ int s_carry, s_total, s_oom;
-  __shared__ unsigned long long hist[kMaxLoops];
-  __shared__ unsigned long long s_kvread, s_kvwrite;
-  __shared__ int s_maxm, s_top, s_base;
+  __shared__ unsigned long long s_kvread;
+  __shared__ int s_top, s_base;
   __shared__ int s_nact[kMaxLoops];
 
-  // the global reads of the first kPlanThreads sequences (every batch up to
+  // the global reads of the first NT sequences (every batch up to
   // that size) are issued here: depth, sequence length, the R cache lengths
   // and the allocator in one round trip, then the page-table entry of each
   // cache's partly filled last page; sequences beyond (chunks >= 1) read
@@ -47,7 +53,7 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan_decode(DecodePlanArgs a) 
   int m_of[kPlanChunks], row_of[kPlanChunks];
 #pragma unroll
   for (int ch = 0; ch < kPlanChunks; ++ch) {
-    const int b = ch * kPlanThreads + tid;
+    const int b = ch * NT + tid;
     m_of[ch] = b < B ? a.depth[b] : 0;
     row_of[ch] = -1;
   }
@@ -68,8 +74,7 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan_decode(DecodePlanArgs a) 
     return ch == 0 ? len0[i] : c.cache_len[b * R + i];
   };
   if (tid <= kMaxLoops) { cnt[tid] = 0; fill[tid] = 0; }
-  if (tid < kMaxLoops) hist[tid] = 0ull;
-  if (tid == 0) { s_kvread = 0ull; s_kvwrite = 0ull; s_maxm = 0; s_oom = 0; s_carry = 0; s_base = base0; }
+  if (tid == 0) { s_kvread = 0ull; s_base = base0; }
   __syncthreads();
 #pragma unroll
   for (int ch = 0; ch < kPlanChunks; ++ch)
@@ -92,7 +97,7 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan_decode(DecodePlanArgs a) 
   const unsigned long long below = (1ull << lane) - 1ull;
 #pragma unroll
   for (int ch = 0; ch < kPlanChunks; ++ch) {
-    if (ch * kPlanThreads >= B) break;  // uniform
+    if (ch * NT >= B) break;  // uniform
     const int m = m_of[ch];
     int rank = 0;
     for (int dv = 1; dv <= R; ++dv) {
@@ -104,57 +109,97 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan_decode(DecodePlanArgs a) 
     if (m > 0) {
       int off = 0;
       for (int w = 0; w < wv; ++w) off += wcnt[w][m];
-      const int b = ch * kPlanThreads + tid;
+      const int b = ch * NT + tid;
       const int row = a.dense ? b : start[m] + fill[m] + off + rank;
       row_of[ch] = row;
-      a.perm[row] = b;
-      if (a.row_depth) a.row_depth[row] = m;
     }
     __syncthreads();
     if (tid >= 1 && tid <= R) {
       int t = 0;
-      for (int w = 0; w < kPlanWaves; ++w) t += wcnt[w][tid];
+      for (int w = 0; w < NW; ++w) t += wcnt[w][tid];
       fill[tid] += t;
     }
     __syncthreads();
   }
 
-  // 2. pages needed: (b, i) for i < m_b whose next slot starts a page
-  int need_of[kPlanChunks];
+  // 2. pages needed: (b, i) for i < m_b whose next slot starts a page; each
+  // row's first new page follows from a block prefix sum (every thread
+  // carries the running total, so no barrier is needed between chunks), and
+  // the entries each row's attention reads
+  int ex_of[kPlanChunks];
+  int total = 0;
+  unsigned long long rd_sum = 0ull;
+  const int lim_all = a.dense ? top : 0;  // dense: loops every row reads
 #pragma unroll
   for (int ch = 0; ch < kPlanChunks; ++ch) {
-    need_of[ch] = 0;
-    if (ch * kPlanThreads >= B) break;
-    const int b = ch * kPlanThreads + tid, m = m_of[ch];
+    ex_of[ch] = 0;
+    if (ch * NT >= B) break;  // uniform
+    const int b = ch * NT + tid, m = m_of[ch];
     int need = 0;
+    unsigned long long rd = 0ull;
 #pragma unroll
-    for (int i = 0; i < kMaxLoops; ++i)
-      if (i < m) need += (len_at(ch, b, i) % kPage) == 0;
-    need_of[ch] = need;
-    int tot;
-    block_exclusive_scan(need, scan_tmp, &tot);
-    if (tid == 0) s_carry += tot;
-    __syncthreads();
-  }
-  if (tid == 0) {
-    s_total = s_carry;
-    const int base = s_base;
-    if ((int64_t)base + s_total > c.max_pages) {
-      s_oom = 1;
-      set_err(c.err, kErrOutOfPages);
+    for (int i = 0; i < kMaxLoops; ++i) {
+      if (m > 0 && i < m) {
+        const int len = len_at(ch, b, i);
+        need += len % kPage == 0;
+        rd += (unsigned long long)(len + 1);
+      } else if (m > 0 && i < lim_all) {  // dense: computed and discarded
+        rd += (unsigned long long)len_at(ch, b, i);
+      }
     }
-    s_carry = base;
+    rd_sum += rd;
+    int tot;
+    ex_of[ch] = total + block_exclusive_scan(need, scan_tmp, &tot);
+    total += tot;
   }
+  // one LDS atomic per wave (a same-address atomic from every lane serialises)
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) rd_sum += shfl_xor(rd_sum, o);
+  if (lane == 0 && rd_sum != 0ull) atomicAdd(&s_kvread, rd_sum);
+  const int base = s_base;
+  const bool oom = (int64_t)base + total > c.max_pages;
+  if (tid == 0 && oom) set_err(c.err, kErrOutOfPages);
   __syncthreads();
 
-  // 3. slots of the executed (b, i)
+  // 3. bookkeeping, before any slot is written (a barrier after global
+  // stores would wait for them): the depth histogram, the deepest depth and
+  // the entries written follow from the per-depth counts
+  if (tid == 0 && !oom) *c.page_next = base + total;
+  if (tid < R) atomicAdd(&c.depth_hist[tid], (unsigned long long)cnt[tid + 1]);
+  if (tid == 0) {
+    unsigned long long kvw = 0ull;
+    for (int dv = 1; dv <= R; ++dv) kvw += (unsigned long long)dv * cnt[dv];
+    if (oom) kvw = 0ull;
+    const unsigned long long kvr = oom ? 0ull : s_kvread;
+    c.step_stats[kStatKvRead] = (long long)(kvr * (unsigned long long)a.kv_entry_bytes);
+    c.step_stats[kStatKvWrite] = (long long)(kvw * (unsigned long long)a.kv_entry_bytes);
+    c.step_stats[kStatLoops] = top;
+    add_stat(c.step_stats + kStatStepsTotal, 1ull);
+    add_stat(c.step_stats + kStatKvWriteTotal, kvw * (unsigned long long)a.kv_entry_bytes);
+    add_stat(c.step_stats + kStatLoopsTotal, (unsigned long long)top);
+    if (!oom) {
+      // each executed (loop, layer) attention reads every valid entry of its
+      // cache plus one q row and writes one o row per active token; summed
+      // over layers: entry bytes times (entries read + active rows)
+      unsigned long long rows = 0;
+      for (int i = 0; i < R; ++i)
+        rows += (unsigned long long)(a.dense ? (i < top ? B : 0) : start[i + 1] + cnt[i + 1]);
+      add_stat(c.step_stats + kStatAttnBytesTotal, (kvr + rows) * (unsigned long long)a.kv_entry_bytes);
+    }
+  }
+  if (tid < R) {
+    if (oom) a.nact[tid] = 0;  // the step becomes a no-op: no active rows
+    c.step_stats[kStatRows + tid] = oom ? 0 : s_nact[tid];
+  }
+
+  // 4. slots of the executed (b, i): positions, cache lengths, new pages and
+  // each compact row's slot offset, and the row order; no barrier follows
+  // these stores
 #pragma unroll
   for (int ch = 0; ch < kPlanChunks; ++ch) {
-    if (ch * kPlanThreads >= B) break;
-    const int b = ch * kPlanThreads + tid, m = m_of[ch];
-    int tot;
-    const int ex = block_exclusive_scan(need_of[ch], scan_tmp, &tot);
-    if (m > 0 && !s_oom) {
+    if (ch * NT >= B) break;  // uniform
+    const int b = ch * NT + tid, m = m_of[ch];
+    if (m > 0 && !oom) {
       int len[kMaxLoops], page[kMaxLoops];
       const int lim = a.dense ? top : m;  // loops whose cache this row reads
 #pragma unroll
@@ -168,9 +213,8 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan_decode(DecodePlanArgs a) 
           if (i < m && len[i] % kPage != 0)
             page[i] = c.page_table[((int64_t)b * R + i) * c.pages_per_seq + len[i] / kPage];
       }
-      int next = s_carry + ex;
+      int next = base + ex_of[ch];
       const int t = ch == 0 ? seq0 : c.seq_len[b];
-      unsigned long long rd = 0ull;
 #pragma unroll
       for (int i = 0; i < kMaxLoops; ++i) {
         if (i < m) {
@@ -182,49 +226,17 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan_decode(DecodePlanArgs a) 
           c.pos[(int64_t)page[i] * kPage + slot % kPage] = t;
           c.cache_len[b * R + i] = slot + 1;
           a.kv_slot[(int64_t)i * B + row_of[ch]] = (int64_t)page[i] * c.page_elems + slot % kPage;
-          rd += (unsigned long long)(slot + 1);
         } else if (i < lim) {  // dense: computed and discarded
           a.kv_slot[(int64_t)i * B + row_of[ch]] = -1;
-          rd += (unsigned long long)len[i];
         }
       }
-      atomicAdd(&s_kvread, rd);
-      atomicAdd(&s_kvwrite, (unsigned long long)m);
     }
     if (m > 0) {
       c.seq_len[b] = (ch == 0 ? seq0 : c.seq_len[b]) + 1;
-      atomicAdd(&hist[m - 1], 1ull);
-      atomicMax(&s_maxm, m);
-    }
-    __syncthreads();
-    if (tid == 0) s_carry += tot;
-    __syncthreads();
-  }
-
-  // 4. bookkeeping
-  if (tid == 0 && !s_oom) *c.page_next += s_total;
-  if (tid < R) atomicAdd(&c.depth_hist[tid], hist[tid]);
-  if (tid == 0) {
-    c.step_stats[kStatKvRead] = (long long)(s_kvread * (unsigned long long)a.kv_entry_bytes);
-    c.step_stats[kStatKvWrite] = (long long)(s_kvwrite * (unsigned long long)a.kv_entry_bytes);
-    c.step_stats[kStatLoops] = s_maxm;
-    c.step_stats[kStatStepsTotal] += 1;
-    c.step_stats[kStatKvWriteTotal] += (long long)(s_kvwrite * (unsigned long long)a.kv_entry_bytes);
-    c.step_stats[kStatLoopsTotal] += s_maxm;
-    if (!s_oom) {
-      // each executed (loop, layer) attention reads every valid entry of its
-      // cache plus one q row and writes one o row per active token; summed
-      // over layers: entry bytes times (entries read + active rows)
-      unsigned long long rows = 0;
-      for (int i = 0; i < R; ++i)
-        rows += (unsigned long long)(a.dense ? (i < top ? B : 0) : start[i + 1] + cnt[i + 1]);
-      c.step_stats[kStatAttnBytesTotal] += (long long)((s_kvread + rows) * (unsigned long long)a.kv_entry_bytes);
+      a.perm[row_of[ch]] = b;
+      if (a.row_depth) a.row_depth[row_of[ch]] = m;
     }
   }
-  if (s_oom) {  // the step becomes a no-op for the block: no active rows
-    if (tid < R) a.nact[tid] = 0;
-  }
-  if (tid < R) c.step_stats[kStatRows + tid] = s_oom ? 0 : s_nact[tid];
 }
 
 // ---------------------------------------------------------------------------
@@ -335,7 +347,11 @@ int fill_grid(int64_t n) {
 }  // namespace
 
 hipError_t launch_plan_decode(const DecodePlanArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(k_plan_decode, dim3(1), dim3(kPlanThreads), 0, s, a);
+  if (a.B < 0 || a.B > kPlanThreads * kPlanChunks) return hipErrorInvalidValue;
+  // fewer threads for a small batch: the planner's many barriers then wait
+  // for fewer waves
+  const int nt = std::min(kPlanThreads, std::max(kWave, (a.B + kWave - 1) / kWave * kWave));
+  hipLaunchKernelGGL(k_plan_decode, dim3(1), dim3(nt), 0, s, a);
   return hipGetLastError();
 }
 
