@@ -36,6 +36,22 @@ __device__ __forceinline__ unsigned int ordered_bits(float v) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
+// 4 x 4 transpose inside each group of four lanes: lane t of the group holds
+// v[r] = (row r, column t) of a 4 x 4 block on entry and (row t, column r) on
+// return, so an accumulator tile's four consecutive columns of one row meet
+// in one lane (one 16-byte access instead of four 4-byte ones).
+__device__ __forceinline__ void transpose4(float& v0, float& v1, float& v2, float& v3, int t) {
+  float a = (t & 1) ? v0 : v1, b = (t & 1) ? v2 : v3;
+  a = shfl_xor(a, 1);
+  b = shfl_xor(b, 1);
+  if (t & 1) { v0 = a; v2 = b; } else { v1 = a; v3 = b; }
+  a = (t & 2) ? v0 : v2;
+  b = (t & 2) ? v1 : v3;
+  a = shfl_xor(a, 2);
+  b = shfl_xor(b, 2);
+  if (t & 2) { v0 = a; v1 = b; } else { v2 = a; v3 = b; }
+}
+
 // 16-byte chunk c of LDS row `row` is stored at chunk c ^ key(row): the 16
 // rows that one MFMA fragment read touches land in distinct banks without
 // padding (bf16 rows of 32 elements hold 4 chunks, float rows 8).
@@ -285,6 +301,52 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs g) {
     }
     return;
   }
+  if constexpr (EK == E_RESID || EK == E_SWIGLU) {
+    // lane t = col16 % 4 of each group of four writes row 4 quad + t of the
+    // group's four columns (SwiGLU: four consecutive hidden units) as one
+    // 16-byte access (the launcher checks that the widths allow it)
+    const int t = col16 & 3;
+#pragma unroll
+    for (int i = 0; i < MT; ++i) {
+      const int rl = wm * MT * 16 + i * 16 + quad * 4 + t;
+      const int src = row_src_s[rl];
+      if constexpr (EK == E_RESID) {
+#pragma unroll
+        for (int j = 0; j < NT; ++j) {
+          float v0 = acc[i][j][0], v1 = acc[i][j][1], v2 = acc[i][j][2], v3 = acc[i][j][3];
+          transpose4(v0, v1, v2, v3, t);
+          const int nb = n0 + wn * NT * 16 + j * 16 + (col16 & ~3);
+          if (src < 0 || nb >= g.N) continue;
+          if (g.mod_a) {  // AdaLN gate (1 + alpha) per column
+            const float4 ga = *reinterpret_cast<const float4*>(g.mod_a + row_mod_s[rl] + nb);
+            v0 *= 1.f + ga.x; v1 *= 1.f + ga.y; v2 *= 1.f + ga.z; v3 *= 1.f + ga.w;
+          }
+          float4* px = reinterpret_cast<float4*>(reinterpret_cast<float*>(g.out) + (int64_t)src * g.ldo + nb);
+          float4 x = *px;
+          x.x += v0; x.y += v1; x.z += v2; x.w += v3;
+          *px = x;
+        }
+      } else {
+#pragma unroll
+        for (int j = 0; j < NT; j += 2) {
+          // gate columns j, up columns j + 1 of the same 16 hidden units
+          float h[4];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const float gt = acc[i][j][r], up = acc[i][j + 1][r];
+            h[r] = gt / (1.f + __expf(-gt)) * up;
+          }
+          transpose4(h[0], h[1], h[2], h[3], t);
+          const int n = n0 + wn * NT * 16 + j * 16;  // first gate column of the group
+          const int unit = (n >> 5) * 16 + (col16 & ~3);
+          if (src < 0 || unit >= g.F) continue;
+          *reinterpret_cast<float4*>(reinterpret_cast<float*>(g.out) + (int64_t)(r0 + rl) * g.ldo + unit) =
+              make_float4(h[0], h[1], h[2], h[3]);
+        }
+      }
+    }
+    return;
+  }
 #pragma unroll
   for (int i = 0; i < MT; ++i) {
 #pragma unroll
@@ -321,30 +383,13 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs g) {
               g.argmax_keys[(int64_t)orow * g.key_groups + (n0 + wn * NT * 16 + j0 * 16) / 64] = best;
           }
         }
-      } else if constexpr (EK == E_SWIGLU) {
-#pragma unroll
-        for (int j = 0; j < NT; j += 2) {
-          const int n = n0 + wn * NT * 16 + j * 16 + col16;  // gate column (n % 32 < 16)
-          const int unit = (n >> 5) * 16 + col16;
-          if (src >= 0 && unit < g.F) {
-            const float gt = acc[i][j][r], up = acc[i][j + 1][r];
-            const float a = gt / (1.f + __expf(-gt)) * up;
-            reinterpret_cast<float*>(g.out)[(int64_t)rg * g.ldo + unit] = a;
-          }
-        }
-      } else {
+      } else {  // E_HIDDEN
 #pragma unroll
         for (int j = 0; j < NT; ++j) {
           const int n = n0 + wn * NT * 16 + j * 16 + col16;
           if (src < 0 || n >= g.N) continue;
-          const float v = acc[i][j][r];
-          if constexpr (EK == E_RESID) {
-            const float gate = g.mod_a ? 1.f + g.mod_a[row_mod_s[rl] + n] : 1.f;
-            reinterpret_cast<float*>(g.out)[(int64_t)src * g.ldo + n] += gate * v;
-          } else {  // E_HIDDEN
-            const float u = v + g.bias[n];
-            g.out[(int64_t)rg * g.ldo + n] = u / (1.f + __expf(-u));
-          }
+          const float u = acc[i][j][r] + g.bias[n];
+          g.out[(int64_t)rg * g.ldo + n] = u / (1.f + __expf(-u));
         }
       }
     }
@@ -379,6 +424,10 @@ hipError_t launch_tiles(const GemmArgs& a, AKind ak, EKind ek, bool norm, hipStr
 template <typename T>
 hipError_t launch_gemm(const GemmArgs& a, AKind ak, EKind ek, bool norm, hipStream_t s) {
   if (a.K % kGemmBK != 0) return hipErrorInvalidValue;
+  // the residual and SwiGLU epilogues write four consecutive columns at once
+  if ((ek == E_RESID && (a.N % 4 != 0 || a.ldo % 4 != 0 || (a.mod_a && a.mod_ld % 4 != 0))) ||
+      (ek == E_SWIGLU && (a.F % 4 != 0 || a.ldo % 4 != 0)))
+    return hipErrorInvalidValue;
   // a few row tiles (the decode LM head) take 128-column tiles so the grid
   // still holds about two workgroups per compute unit; prefill takes 256
   if ((a.rm.rows + 2 * kGemmMT * 16 - 1) / (2 * kGemmMT * 16) <= 4) return launch_tiles<T, 4>(a, ak, ek, norm, s);
