@@ -250,25 +250,44 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs g) {
 
   const int col16 = lane & 15;
   if constexpr (EK == E_QKV) {
-    // q to its buffer; k and v into the cache pages.  A lane holds rows
-    // 4 quad .. 4 quad + 3 of its column: when they are consecutive slots
-    // of one page from a multiple of 4 (a fresh prefill), their four v
-    // values of that dimension are one aligned run in the V block and go
-    // out as one store; otherwise element by element.
+    // q to its buffer; k and v into the cache pages.  A 16-column tile lies
+    // in one of q, k and v (d is a multiple of 16).  q and (bf16) k tiles go
+    // through an in-group 4 x 4 transpose, after which lane t holds four
+    // consecutive columns of row 4 quad + t: one 16-byte q store, or one
+    // 8-byte k store (four dimensions of one slot are adjacent in the
+    // fragment order).  A v tile keeps the lane's column: when its four rows
+    // are consecutive slots of one page from a multiple of 4 (a fresh
+    // prefill), their values of that dimension are one aligned run in the V
+    // block and go out as one store; otherwise element by element.
     T* pool = reinterpret_cast<T*>(g.kv.c.pool);
+    const int t = col16 & 3;
 #pragma unroll
     for (int i = 0; i < MT; ++i) {
       const int rl0 = wm * MT * 16 + i * 16 + quad * 4;
 #pragma unroll
       for (int j = 0; j < NT; ++j) {
-        const int n = n0 + wn * NT * 16 + j * 16 + col16;
-        if (n >= g.N) continue;
-        if (n < g.d) {
-#pragma unroll
-          for (int r = 0; r < 4; ++r)
-            if (row_src_s[rl0 + r] >= 0) reinterpret_cast<float*>(g.out)[(int64_t)(r0 + rl0 + r) * g.ldo + n] = acc[i][j][r];
+        const int nt = n0 + wn * NT * 16 + j * 16;  // the tile's first column (wave-uniform)
+        if (nt >= g.N) continue;
+        if (nt < g.d || (sizeof(T) == 2 && nt < 2 * g.d)) {
+          float v0 = acc[i][j][0], v1 = acc[i][j][1], v2 = acc[i][j][2], v3 = acc[i][j][3];
+          transpose4(v0, v1, v2, v3, t);
+          const int rl = rl0 + t, cb = nt + (col16 & ~3);
+          if (nt < g.d) {
+            if (row_src_s[rl] >= 0)
+              *reinterpret_cast<float4*>(reinterpret_cast<float*>(g.out) + (int64_t)(r0 + rl) * g.ldo + cb) =
+                  make_float4(v0, v1, v2, v3);
+          } else {
+            const int64_t base = kv_base[rl];
+            if (base >= 0) {
+              const int slot = (int)(base & (kPage - 1)), within = cb - g.d;
+              T* dst = pool + (base - slot) + k_block(g.kv.c, g.kv.layer, within / g.kv.c.D) +
+                       k_frag_off<T>(slot, within % g.kv.c.D);
+              *reinterpret_cast<uint2*>(dst) = make_uint2(pack_bf16x2(v0, v1), pack_bf16x2(v2, v3));
+            }
+          }
           continue;
         }
+        const int n = nt + col16;
         const int nn = n - g.d, kvsel = nn / g.d, within = nn % g.d;
         const int h = within / g.kv.c.D, e = within % g.kv.c.D;
         const int64_t b0 = kv_base[rl0];
@@ -424,6 +443,8 @@ hipError_t launch_tiles(const GemmArgs& a, AKind ak, EKind ek, bool norm, hipStr
 template <typename T>
 hipError_t launch_gemm(const GemmArgs& a, AKind ak, EKind ek, bool norm, hipStream_t s) {
   if (a.K % kGemmBK != 0) return hipErrorInvalidValue;
+  // the QKV epilogue takes each 16-column tile as wholly q, k or v
+  if (ek == E_QKV && (a.d % 16 != 0 || a.ldo % 4 != 0 || a.kv.c.D % 16 != 0)) return hipErrorInvalidValue;
   // the residual and SwiGLU epilogues write four consecutive columns at once
   if ((ek == E_RESID && (a.N % 4 != 0 || a.ldo % 4 != 0 || (a.mod_a && a.mod_ld % 4 != 0))) ||
       (ek == E_SWIGLU && (a.F % 4 != 0 || a.ldo % 4 != 0)))
