@@ -111,6 +111,30 @@ def test_f32_batch_over_head_gemm_rows():
     _check_f32(m, w, prompts, g, o, "f32-b130")
 
 
+def test_f32_batch_over_planner_threads():
+    """1100 sequences: the decode planner's second chunk of sequences (past
+    its 1024 threads) reads its cache lengths and page-table entries where it
+    uses them.  Every sequence's cache index is checked against its depths;
+    four sampled sequences against the oracle."""
+    m = _f32_small(batch=1100, prompt_len=6, steps=5, vocab=300)
+    w = synth.make_weights(m)
+    prompts = synth.make_prompts(m)
+    sample = [0, 511, 1024, 1099]
+    g = parity.run_gpu(m, w, prompts, m.steps, keep_logits_rows=sample)
+    o = parity.run_oracle(m, w, prompts[sample], [t[sample] for t in g.step_tokens])
+    assert np.array_equal(g.prefill_depths[sample], o.prefill_depths)
+    for s in range(m.steps):
+        assert np.array_equal(g.step_depths[s][sample], o.step_depths[s]), s
+    _check_index_matches_depths(g, m.max_loops)
+    hist = np.bincount(_all_depths(g).ravel(), minlength=m.max_loops + 1)[1:]
+    assert np.array_equal(np.asarray(g.stats["depth_hist"]), hist)
+    err = _max_err(g.prefill_logits, o.prefill_logits)
+    for s in range(m.steps):
+        err = max(err, _max_err(g.step_logits[s], o.step_logits[s]))
+    _report("f32-b1100", max_abs_logit_err=f"{err:.3g}")
+    assert err <= F32_TOL
+
+
 def test_f32_single_token_prompt_and_deep_tail():
     m = _f32_small(batch=2, prompt_len=1, steps=40)
     w = synth.make_weights(m)
