@@ -201,12 +201,23 @@ __global__ __launch_bounds__(W * 64) void k_attn_decode(AttnDecodeArgs a) {
       if constexpr (NBUF == 2) {
         KFrag kb[PPI][KSTEPS];
         uint4 vb2[DT];
+        // batches of PPI pages; every load stays inside the wave's range (a
+        // load past it would fetch its last page from memory again), so the
+        // last one or two batches are peeled
         load(ka, va, p0);
-        for (int pg = p0; pg < p1; pg += 2 * PPI) {
+        int pg = p0;
+        for (; pg + 2 * PPI < p1; pg += 2 * PPI) {
           load(kb, vb2, pg + PPI);
           consume(ka, va, pg);
           load(ka, va, pg + 2 * PPI);
           consume(kb, vb2, pg + PPI);
+        }
+        if (pg + PPI < p1) {
+          load(kb, vb2, pg + PPI);
+          consume(ka, va, pg);
+          consume(kb, vb2, pg + PPI);
+        } else {
+          consume(ka, va, pg);
         }
       } else {
         for (int pg = p0; pg < p1; pg += PPI) {
