@@ -414,7 +414,11 @@ hipError_t launch_cfg(const GemmArgs& a, int cus, hipStream_t s) {
   if (tn_n == 0 || tm_n == 0) return hipSuccess;
   // wide above the row count at which the narrow tiles exceed one per compute unit
   const int wide_above = (RMn == RMw && CNn == CNw) ? a.rm.rows : std::max(1, cus / tn_n) * BMn;
-  const int tiles = std::max(tn_n * tm_n, tn_w * tm_w);
+  // workgroups for the larger of the two shapes' tile counts; the narrow
+  // shape never runs on more than wide_above rows.  No workgroup beyond
+  // that: a workgroup past one per compute unit waits for a free one only
+  // to find no tile, and the launch is not over until it has run
+  const int tiles = std::max(tn_n * std::min(tm_n, (wide_above + BMn - 1) / BMn), tn_w * tm_w);
   const int grid = kXcds * ((tiles + kXcds - 1) / kXcds);
   hipLaunchKernelGGL((k_dgemm<T, RMn, CNn, RMw, CNw, W, KB, AK, EK, NORM, MOD>), dim3(grid), dim3(W * 64), 0, s, a,
                      wide_above);
