@@ -29,7 +29,9 @@
  *     current when tlf_init is called.  Host pointers ("h_") are host memory.
  *   - Weights and the workspace are borrowed: the caller keeps them alive and
  *     unchanged until tlf_destroy.  Outputs are caller-allocated.  The context
- *     owns only host-side state.
+ *     owns only host-side state.  tlf_init also writes a copy of every
+ *     layer's block weights into the workspace, reordered for the decode
+ *     projections' matrix-core loads (counted in the workspace size).
  *   - Work is enqueued asynchronously on the stream given to tlf_init; only
  *     tlf_cache_stats waits for the stream.  A context is not thread-safe.
  *   - Arguments are validated on the host before any device work; an argument

@@ -21,7 +21,7 @@ enum Buf {
   B_POOL, B_POS, B_PAGE_TABLE, B_CACHE_LEN, B_CHUNK_LEN, B_SEQ_LEN, B_SCALARS, B_DEPTH_HIST, B_STEP_STATS,
   B_X_DEC, B_XC_DEC, B_KVSLOT, B_DEPTH_DEC, B_PERM, B_NACT, B_Q_DEC, B_O_DEC, B_ACT_DEC, B_KEYS,
   B_X_PRE, B_Y_PRE, B_DEPTH_PRE, B_TOK_IDX, B_Q_PRE, B_O_PRE, B_ACT_PRE, B_HID,
-  B_ROW_DEPTH, B_MOD, B_COND_TMP,
+  B_ROW_DEPTH, B_MOD, B_COND_TMP, B_WFRAG,
   B_COUNT
 };
 
@@ -73,6 +73,8 @@ bool make_layout(const tlf_config& c, Layout* L) {
   // AdaLN: modulation of every (layer, loop, depth), and its set-up scratch
   sz[B_MOD] = c.adaln ? (int64_t)c.n_layers * R * R * 4 * d * 4 : 0;
   sz[B_COND_TMP] = c.adaln ? (int64_t)cond_scratch_floats((int)R, (int)d) * 4 : 0;
+  // every layer's block weights in MFMA fragment order (the decode projections' copy)
+  sz[B_WFRAG] = (int64_t)c.n_layers * (4 * d * d + 3 * d * F) * s;
   size_t off = 0;
   for (int i = 0; i < B_COUNT; ++i) {
     if (sz[i] < 0) return false;
@@ -208,6 +210,14 @@ struct tlf_ctx {
   }
 
   template <typename P> P* buf(Buf b) const { return reinterpret_cast<P*>(ws + L.off[b]); }
+  // layer j's weights in fragment order: qkv [3d][d], o [d][d], gate/up [2F][d], down [d][F]
+  const void* wfrag(int j, int part) const {
+    const int64_t d = cfg.d_model, F = cfg.d_ff;
+    const int64_t sizes[4] = {3 * d * d, d * d, 2 * F * d, d * F};
+    int64_t off = (int64_t)j * (4 * d * d + 3 * d * F);
+    for (int k = 0; k < part; ++k) off += sizes[k];
+    return ws + L.off[B_WFRAG] + off * L.s;
+  }
 };
 
 #define TLF_HIP(expr)                  \
@@ -339,7 +349,7 @@ int run_prefill(tlf_ctx* ctx, int B, int T_, int pos0, const int32_t* tokens, fl
       for (int j = 0; j < c.n_layers; ++j) {
         const tlf_layer_weights& lw = ctx->layers[j];
         GemmArgs q;
-        q.A = few ? x : y; q.lda = d; q.W = lw.w_qkv; q.N = 3 * d; q.K = d; q.w_rows = 3 * d; q.rm = rm;
+        q.A = few ? x : y; q.lda = d; q.W = lw.w_qkv; q.Wf = ctx->wfrag(j, 0); q.N = 3 * d; q.K = d; q.w_rows = 3 * d; q.rm = rm;
         q.out = ctx->buf<float>(B_Q_PRE); q.ldo = d; q.d = d; q.eps = c.rms_eps; q.spec = i == 0;
         q.kv.c = ctx->cv; q.kv.loop = i; q.kv.layer = j; q.kv.prefill = 1; q.kv.b0 = b0; q.kv.seg = T_;
         set_mod(ctx, &q, i, j, 2, pre_depth, 1);
@@ -353,7 +363,7 @@ int run_prefill(tlf_ctx* ctx, int B, int T_, int pos0, const int32_t* tokens, fl
         TLF_HIP(launch_attn_prefill<T>(at, s));
 
         GemmArgs o;
-        o.A = ctx->buf<float>(B_O_PRE); o.lda = d; o.W = lw.w_o; o.N = d; o.K = d; o.w_rows = d; o.rm = rm;
+        o.A = ctx->buf<float>(B_O_PRE); o.lda = d; o.W = lw.w_o; o.Wf = ctx->wfrag(j, 1); o.N = d; o.K = d; o.w_rows = d; o.rm = rm;
         o.out = x; o.ldo = d; o.scatter = 1; o.spec = i == 0;
         set_mod(ctx, &o, i, j, 0, pre_depth, 1);
         if (few) {
@@ -364,14 +374,14 @@ int run_prefill(tlf_ctx* ctx, int B, int T_, int pos0, const int32_t* tokens, fl
         }
 
         GemmArgs gu;
-        gu.A = few ? x : y; gu.lda = d; gu.W = lw.w_gate_up; gu.N = 2 * F; gu.K = d; gu.w_rows = 2 * F; gu.rm = rm;
+        gu.A = few ? x : y; gu.lda = d; gu.W = lw.w_gate_up; gu.Wf = ctx->wfrag(j, 2); gu.N = 2 * F; gu.K = d; gu.w_rows = 2 * F; gu.rm = rm;
         gu.out = ctx->buf<float>(B_ACT_PRE); gu.ldo = F; gu.F = F; gu.eps = c.rms_eps; gu.spec = i == 0;
         set_mod(ctx, &gu, i, j, 3, pre_depth, 1);
         if (few) TLF_HIP(launch_dgemm<T>(gu, A_SRC, E_SWIGLU, true, ctx->cus, s));
         else TLF_HIP(launch_gemm<T>(gu, A_SRC, E_SWIGLU, false, s));
 
         GemmArgs dn;
-        dn.A = ctx->buf<float>(B_ACT_PRE); dn.lda = F; dn.W = lw.w_down; dn.N = d; dn.K = F; dn.w_rows = d;
+        dn.A = ctx->buf<float>(B_ACT_PRE); dn.lda = F; dn.W = lw.w_down; dn.Wf = ctx->wfrag(j, 3); dn.N = d; dn.K = F; dn.w_rows = d;
         dn.rm = rm; dn.out = x; dn.ldo = d; dn.scatter = 1; dn.spec = i == 0;
         set_mod(ctx, &dn, i, j, 1, pre_depth, 1);
         if (few) {
@@ -452,7 +462,7 @@ int run_decode(tlf_ctx* ctx, hipStream_t s, const int32_t* tokens, float* logits
       const tlf_layer_weights& lw = ctx->layers[j];
       GemmArgs q;  // q, k, v of RMSNorm(x); k, v appended to cache (b, i) of layer j
       const bool first = i == 0 && j == 0;  // reads x through perm and writes xc
-      q.A = first ? x : xc; q.lda = d; q.a_copy = first ? xc : nullptr; q.W = lw.w_qkv; q.N = 3 * d; q.K = d; q.w_rows = 3 * d; q.rm = rm;
+      q.A = first ? x : xc; q.lda = d; q.a_copy = first ? xc : nullptr; q.W = lw.w_qkv; q.Wf = ctx->wfrag(j, 0); q.N = 3 * d; q.K = d; q.w_rows = 3 * d; q.rm = rm;
       q.out = ctx->buf<float>(B_Q_DEC); q.ldo = d; q.d = d; q.eps = c.rms_eps;
       q.kv.c = ctx->cv; q.kv.loop = i; q.kv.layer = j; q.kv.prefill = 0; q.kv.slot_base = kv_slot + (int64_t)i * B;
       q.spec = i == 0;
@@ -474,19 +484,19 @@ int run_decode(tlf_ctx* ctx, hipStream_t s, const int32_t* tokens, float* logits
       }
 
       GemmArgs o;  // x += o W_o^T
-      o.A = ctx->buf<float>(B_O_DEC); o.lda = d; o.W = lw.w_o; o.N = d; o.K = d; o.w_rows = d; o.rm = rm;
+      o.A = ctx->buf<float>(B_O_DEC); o.lda = d; o.W = lw.w_o; o.Wf = ctx->wfrag(j, 1); o.N = d; o.K = d; o.w_rows = d; o.rm = rm;
       o.out = xc; o.ldo = d; o.spec = i == 0; o.keep_depth = keep_depth; o.keep_loop = i;
       set_mod(ctx, &o, i, j, 0, pa.row_depth, 0);
       TLF_HIP(launch_dgemm<T>(o, A_CMP, E_RESID, false, ctx->cus, s));
 
       GemmArgs gu;  // act = silu(RMSNorm(x) W_g^T) * (RMSNorm(x) W_u^T)
-      gu.A = xc; gu.lda = d; gu.W = lw.w_gate_up; gu.N = 2 * F; gu.K = d; gu.w_rows = 2 * F; gu.rm = rm;
+      gu.A = xc; gu.lda = d; gu.W = lw.w_gate_up; gu.Wf = ctx->wfrag(j, 2); gu.N = 2 * F; gu.K = d; gu.w_rows = 2 * F; gu.rm = rm;
       gu.out = ctx->buf<float>(B_ACT_DEC); gu.ldo = F; gu.F = F; gu.eps = c.rms_eps; gu.spec = i == 0;
       set_mod(ctx, &gu, i, j, 3, pa.row_depth, 0);
       TLF_HIP(launch_dgemm<T>(gu, A_CMP, E_SWIGLU, true, ctx->cus, s));
 
       GemmArgs dn;  // x += act W_d^T
-      dn.A = ctx->buf<float>(B_ACT_DEC); dn.lda = F; dn.W = lw.w_down; dn.N = d; dn.K = F; dn.w_rows = d;
+      dn.A = ctx->buf<float>(B_ACT_DEC); dn.lda = F; dn.W = lw.w_down; dn.Wf = ctx->wfrag(j, 3); dn.N = d; dn.K = F; dn.w_rows = d;
       dn.rm = rm; dn.out = xc; dn.ldo = d; dn.spec = i == 0; dn.keep_depth = keep_depth; dn.keep_loop = i;
       set_mod(ctx, &dn, i, j, 1, pa.row_depth, 0);
       TLF_HIP(launch_dgemm<T>(dn, A_CMP, E_RESID, false, ctx->cus, s));
@@ -591,6 +601,20 @@ int tlf_init(const tlf_config* cfg, const tlf_weights* w, void* d_workspace, siz
   if (e == hipSuccess) e = launch_fill_i32(cv.page_next, 0, 2, s);
   if (e == hipSuccess) e = launch_fill_u64(cv.depth_hist, 0ull, cfg->max_loops, s);
   if (e == hipSuccess) e = launch_fill_u64(reinterpret_cast<unsigned long long*>(cv.step_stats), 0ull, kStatCount, s);
+  // the decode projections read the block weights in MFMA fragment order
+  for (int j = 0; j < cfg->n_layers && e == hipSuccess; ++j) {
+    const tlf_layer_weights& lw = ctx->layers[j];
+    const int d = cfg->d_model, F = cfg->d_ff;
+    const bool bf = cfg->dtype == TLF_DTYPE_BF16;
+    auto relayout = [&](const void* W, int part, int N, int K, int sF) {
+      void* dst = const_cast<void*>(ctx->wfrag(j, part));
+      return bf ? launch_wfrag<bf16>(W, dst, N, K, sF, s) : launch_wfrag<float>(W, dst, N, K, sF, s);
+    };
+    e = relayout(lw.w_qkv, 0, 3 * d, d, 0);
+    if (e == hipSuccess) e = relayout(lw.w_o, 1, d, d, 0);
+    if (e == hipSuccess) e = relayout(lw.w_gate_up, 2, 2 * F, d, F);
+    if (e == hipSuccess) e = relayout(lw.w_down, 3, d, F, 0);
+  }
   if (e == hipSuccess && cfg->adaln) {
     // the modulation of every (layer, loop, depth); the caller's conditioning
     // weights are not read again

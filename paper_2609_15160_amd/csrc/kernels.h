@@ -73,6 +73,7 @@ struct GemmArgs {
   const float* A = nullptr; // float32 rows
   int lda = 0;
   const void* W = nullptr;  // [W rows][K] storage dtype
+  const void* Wf = nullptr; // launch_dgemm: the same weights in MFMA fragment order (launch_wfrag), or nullptr
   int N = 0;                // output columns (E_SWIGLU: 2F in the interleaved gate/up space)
   int K = 0;
   int w_rows = 0;           // rows of W (loads are clamped below it)
@@ -119,6 +120,17 @@ hipError_t launch_gemm(const GemmArgs& a, AKind ak, EKind ek, bool norm, hipStre
 // cus: compute units of the device (chooses between a narrow and a wide tile shape).
 template <typename T>
 hipError_t launch_dgemm(const GemmArgs& a, AKind ak, EKind ek, bool norm, int cus, hipStream_t s);
+// Weights in MFMA fragment order for the decode projections: the B operand
+// of one 16 x 16 x KS product (16 output columns, one K step) is 64 lanes x
+// EPL elements, stored contiguously in lane order, blocks of 16 columns
+// outermost and K steps inside them:
+//   Wf[((blk * S + step) * 64 + lane) * EPL + e] = W[row(16 blk + lane % 16)][step * KS + (lane / 16) * EPL + e]
+// with S = K / KS; row(n) = n, or the SwiGLU interleave (16 gate rows of a
+// group of 16 hidden units, then their 16 up rows) when swiglu_F > 0.  One
+// fragment load then reads 64 x 16 contiguous bytes (bf16) instead of 16
+// rows x 64 bytes.  N must be a multiple of 16 and K of KS.
+template <typename T>
+hipError_t launch_wfrag(const void* W, void* Wf, int N, int K, int swiglu_F, hipStream_t s);
 
 // ---------------------------------------------------------------------------
 // Embedding + router (Section 3.2): h0 = E[x] + P[pos], z = W_r h0 + b_r,
