@@ -360,6 +360,77 @@ def prefill_measure(torch, tlf, synth, name):
             "mfma_frac": flops / ms / 1e9 / BF16_PEAK_TFLOPS}
 
 
+def train_gather_scatter(torch, synth, B=8, T=4096, d=1024, R=8, reps=20):
+    """Training-side gather-scatter over all R loops of a batch of B x T tokens
+    (float32 states of width d, depths drawn from the routed decode's depth
+    mix): forward gather + out-of-place scatter per loop, backward gather of
+    the state gradient + in-place scatter of the compact gradient per loop.
+    Launched from a captured HIP graph (the host enqueues slower than these
+    kernels run); HIP events around the replays on the capture's stream."""
+    from paper_2609_15160_amd import train
+    rows = B * T
+    depth = torch.from_numpy(synth.make_train_depths(rows, R)).cuda()
+    plans = [train.plan(depth, B, T, i) for i in range(1, R + 1)]
+    H = [torch.from_numpy(synth.make_train_states(rows, d)).cuda()]
+    H += [torch.empty_like(H[0]) for _ in range(R)]
+    Y = [torch.randn(p.count, d, device="cuda") for p in plans]
+    X = [torch.empty(p.count, d, device="cuda") for p in plans]
+    dH = torch.randn(rows, d, device="cuda")
+    dY = [torch.empty(p.count, d, device="cuda") for p in plans]
+
+    def forward():
+        for i, p in enumerate(plans):
+            train.gather_raw(H[i], p, out=X[i])
+            train.scatter_raw(H[i], Y[i], p, out=H[i + 1])
+
+    def backward():
+        for i in reversed(range(R)):
+            train.gather_raw(dH, plans[i], out=dY[i])
+            train.scatter_raw(dH, Y[i], plans[i], out=dH)
+
+    def plan_all():
+        for i in range(1, R + 1):
+            train.tlf.load().tlf_gs_plan(train._ptr(depth), B, T, i, train._ptr(plans[i - 1].index),
+                                         train._ptr(plans[i - 1].slot), train._ptr(plans[i - 1].offsets),
+                                         train._ptr(plans[i - 1].count_dev), train._stream())
+
+    def timed(fn):
+        s = torch.cuda.Stream()
+        s.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(s):
+            fn()  # warm
+        torch.cuda.current_stream().wait_stream(s)
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            fn()
+        g.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            g.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    fwd_ms, bwd_ms, plan_ms = timed(forward), timed(backward), timed(plan_all)
+    n = [p.count for p in plans]
+    fwd_bytes = sum(4 * c + 2 * 4 * c * d + 4 * rows + 4 * rows * d * 2 + 4 * c * d for c in n)
+    bwd_bytes = sum(4 * c + 2 * 4 * c * d + 4 * rows + 3 * 4 * c * d for c in n)
+    plan_bytes = sum(4 * rows + 4 * c + 4 * rows + 4 * (B + 1) for c in n)
+    return {"workload": f"training gather-scatter: batch {B} x {T} tokens, d={d} float32, R={R}, "
+                        f"mean depth {float(depth.float().mean()):.2f}",
+            "active_rows_per_loop": n,
+            "forward_ms": fwd_ms, "forward_gbs": fwd_bytes / fwd_ms / 1e6,
+            "backward_ms": bwd_ms, "backward_gbs": bwd_bytes / bwd_ms / 1e6,
+            "plan_us_per_loop": plan_ms * 1e3 / R, "plan_gbs": plan_bytes / plan_ms / 1e6,
+            "frac": (fwd_bytes + bwd_bytes) / (fwd_ms + bwd_ms) / 1e6 / HBM_PEAK_GBS,
+            "what": "per pass over all loops; algorithmic bytes: each gathered row read and written once, "
+                    "an out-of-place scatter reads and writes every row and reads each block-output row, "
+                    "an in-place scatter reads two and writes one row per active row; indices and slots "
+                    "4 bytes each"}
+
+
 ATTN_SOURCE = os.path.join(ROOT, "paper_2609_15160_amd", "csrc", "attn.hip")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_decode_bf16_d768_b256x2048_traffic.json")
 CALIB_BYTES = 1 << 30  # the counted copy reads and writes exactly this many bytes
@@ -449,6 +520,9 @@ def main():
     ap.add_argument("--no-sweep", action="store_true", help="skip the MLP-router threshold sweep")
     ap.add_argument("--no-ablation", action="store_true", help="skip the gather-scatter-off decode")
     ap.add_argument("--no-ttft", action="store_true", help="skip the time-to-first-token sweep")
+    ap.add_argument("--no-train", action="store_true", help="skip the training-side gather-scatter measurement")
+    ap.add_argument("--train-only", action="store_true",
+                    help="measure only the training-side gather-scatter and print its JSON")
     ap.add_argument("--no-adaln", action="store_true", help="skip the AdaLN-conditioned decode")
     ap.add_argument("--no-others", action="store_true",
                     help="skip the batch 32 x 512 and batch 64 x 4096 (d=2048) decode workloads")
@@ -500,6 +574,9 @@ def main():
         torch.cuda.empty_cache()
     if args.prefill_only:
         print(json.dumps(prefill_measure(torch, tlf, synth, "bf16_d1024_prefill_b8x4096")), flush=True)
+        return
+    if args.train_only:
+        print(json.dumps(train_gather_scatter(torch, synth)), flush=True)
         return
     base = synth.CONFIGS[args.config]
     if args.warmup + args.steps + 2 * args.profiled_steps > base.steps or args.profiled_steps < 1:
@@ -584,6 +661,11 @@ def main():
     if not args.no_prefill:
         out["prefill"] = prefill_measure(torch, tlf, synth, "bf16_d1024_prefill_b8x4096")
         log(f"prefill 8x4096: {out['prefill']['ms']:.2f} ms")
+    if not args.no_train:
+        out["train_gather_scatter"] = train_gather_scatter(torch, synth)
+        t = out["train_gather_scatter"]
+        log(f"train gather-scatter: fwd {t['forward_ms']:.3f} ms {t['forward_gbs']:.0f} GB/s, "
+            f"bwd {t['backward_ms']:.3f} ms {t['backward_gbs']:.0f} GB/s, plan {t['plan_us_per_loop']:.1f} us/loop")
     if not args.no_sweep:
         out["router_threshold_sweep"] = threshold_sweep(torch, tlf, synth, args.config)
     if not args.no_cpu:

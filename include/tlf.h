@@ -279,6 +279,60 @@ void tlf_destroy(tlf_ctx* ctx);
 /* Static text for a status code. */
 const char* tlf_status_str(int status);
 
+/* ---------------------------------------------------------------------------
+ * Training-side gather-scatter (Section 3.2, Eq. 6-7) and the router's
+ * straight-through estimator (Appendix B).
+ *
+ * These calls need no context: they work on caller-owned device buffers and
+ * enqueue on `stream` (a hipStream_t; NULL is the null stream) without
+ * waiting for it.  The tokens of a batch of B sequences of T tokens are the
+ * rows b*T + t of one [B*T, d] float32 tensor (row-major, 16-byte aligned,
+ * d a multiple of 4).  Token t takes part in loop i exactly when its depth
+ * m_t >= i.  Backward passes reuse the same calls: the gradient of the
+ * gather is an in-place tlf_gs_scatter of the compact gradient into the row
+ * gradients, and the gradient of the scatter is the incoming gradient itself
+ * for the previous state plus its tlf_gs_gather for the block output.
+ * Argument errors return TLF_E_INVALID_ARG before anything is enqueued; a
+ * failed launch returns TLF_E_HIP.  Indices and slots are trusted: they must
+ * be what tlf_gs_plan wrote for the same depths.
+ * ------------------------------------------------------------------------- */
+
+/* Active set of loop `loop` (Section 3.2 and Eq. 6).
+ *   d_depth   [batch*seq_len] int32 depths m_t;
+ *   d_index   [batch*seq_len] capacity; receives the active rows in
+ *             increasing row order (each sequence's run contiguous and in
+ *             causal order), *d_count of them;
+ *   d_slot    [batch*seq_len] or NULL; receives each row's position in the
+ *             compact tensor, -1 for a row not in the loop;
+ *   d_offsets [batch+1] or NULL; receives where each sequence's run starts in
+ *             the compact tensor, and the total last;
+ *   d_count   [1]; the number of active rows.
+ * One workgroup; batch*seq_len may be 0. */
+int tlf_gs_plan(const int32_t* d_depth, int32_t batch, int32_t seq_len, int32_t loop, int32_t* d_index,
+                int32_t* d_slot, int32_t* d_offsets, int32_t* d_count, void* d_stream);
+
+/* Gather (Eq. 6): d_out[r] = d_h[d_index[r]] for r < min(*d_count, max_rows).
+ * d_out holds max_rows x d floats; rows past the count are not written.  The
+ * count stays on the device (no host synchronisation); max_rows bounds the
+ * launch. */
+int tlf_gs_gather(const float* d_h, const int32_t* d_index, const int32_t* d_count, int32_t max_rows,
+                  int32_t d, float* d_out, void* d_stream);
+
+/* Scatter (Eq. 7): d_h_out[r] = d_y[d_slot[r]] + d_h_prev[r] where
+ * d_slot[r] >= 0, else d_h_prev[r]; `rows` rows of d floats.  d_h_out may be
+ * d_h_prev (in place: rows not in the loop are then neither read nor written);
+ * otherwise the two must not overlap, and d_y must overlap neither. */
+int tlf_gs_scatter(const float* d_h_prev, const float* d_y, const int32_t* d_slot, int32_t rows, int32_t d,
+                   float* d_h_out, void* d_stream);
+
+/* Straight-through estimator of the depth (Appendix B), elementwise over n
+ * tokens.  Forward value: d_value[t] = (float)d_depth[t].  Backward: with
+ * sigma the logistic function, d_grad_score[t] = d_grad_value[t] *
+ * sigma(d_score[t]) * (1 - sigma(d_score[t])).  Either output may be NULL
+ * (then its inputs may be NULL too). */
+int tlf_ste(const int32_t* d_depth, const float* d_score, const float* d_grad_value, int32_t n, float* d_value,
+            float* d_grad_score, void* d_stream);
+
 #ifdef __cplusplus
 }
 #endif

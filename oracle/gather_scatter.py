@@ -96,9 +96,11 @@ def ste_value(depth: np.ndarray) -> np.ndarray:
 
 
 def ste_grad(score: np.ndarray, grad_value: np.ndarray) -> np.ndarray:
-    """Appendix B: only sigma(s) carries a gradient, so dL/ds = dL/dm * sigma'(s)."""
-    p = sigmoid(score)
-    return np.asarray(grad_value, np.float64) * p * (1.0 - p)
+    """Appendix B: only sigma(s) carries a gradient, so dL/ds = dL/dm * sigma'(s).
+    sigma'(s) = sigma(s) (1 - sigma(s)), evaluated as exp(-|s|) / (1 + exp(-|s|))^2
+    (the same quantity, without the cancellation of 1 - sigma(s) at large |s|)."""
+    t = np.exp(-np.abs(np.asarray(score, np.float64)))
+    return np.asarray(grad_value, np.float64) * t / (1.0 + t) ** 2
 
 
 def loop_forward(H0: np.ndarray, depth: np.ndarray, block, loops: int) -> np.ndarray:

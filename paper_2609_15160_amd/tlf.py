@@ -90,7 +90,7 @@ class CacheStats(ctypes.Structure):
 
 
 EXPORTS = ("tlf_init", "tlf_prefill", "tlf_decode_step", "tlf_cache_stats", "tlf_set_profiling", "tlf_destroy",
-           "tlf_status_str")
+           "tlf_status_str", "tlf_gs_plan", "tlf_gs_gather", "tlf_gs_scatter", "tlf_ste")
 
 
 def header_exports(path: str = HEADER):
@@ -132,6 +132,14 @@ def load(path: str = LIB_PATH):
     lib.tlf_destroy.restype = None
     lib.tlf_status_str.argtypes = [ctypes.c_int]
     lib.tlf_status_str.restype = ctypes.c_char_p
+    lib.tlf_gs_plan.argtypes = [vp, i32, i32, i32, vp, vp, vp, vp, vp]
+    lib.tlf_gs_plan.restype = ctypes.c_int
+    lib.tlf_gs_gather.argtypes = [vp, vp, vp, i32, i32, vp, vp]
+    lib.tlf_gs_gather.restype = ctypes.c_int
+    lib.tlf_gs_scatter.argtypes = [vp, vp, vp, i32, i32, vp, vp]
+    lib.tlf_gs_scatter.restype = ctypes.c_int
+    lib.tlf_ste.argtypes = [vp, vp, vp, i32, vp, vp, vp]
+    lib.tlf_ste.restype = ctypes.c_int
     _lib = lib
     return lib
 

@@ -372,3 +372,26 @@ def tiny_config(**kw) -> ModelConfig:
                 router_bias="zero")
     base.update(kw)
     return ModelConfig(**base)
+
+
+STREAM_TRAIN_DEPTH = 102
+STREAM_TRAIN_STATE = 103
+
+# Depth mix of the routed decode workload (batch 256 x 2048, argmax router):
+# share of tokens at depth 1..8, used as the depth law of the synthetic
+# training batches of the gather-scatter operators.
+TRAIN_DEPTH_MIX = (0.1315, 0.1791, 0.2033, 0.1950, 0.1180, 0.0901, 0.0638, 0.0192)
+
+
+def make_train_depths(rows: int, loops: int = 8, seed: int = SEED, mix=TRAIN_DEPTH_MIX) -> np.ndarray:
+    """int32 depths in [1, loops] for `rows` tokens, drawn from `mix` (its
+    first `loops` entries, renormalised) by inverting the cumulative shares."""
+    p = np.asarray(mix[:loops], np.float64)
+    cdf = np.cumsum(p / p.sum())
+    u = uniform01(seed, STREAM_TRAIN_DEPTH, 0, rows)
+    return (np.minimum(np.searchsorted(cdf, u, side="right"), loops - 1) + 1).astype(np.int32)
+
+
+def make_train_states(rows: int, d: int, seed: int = SEED, stream: int = STREAM_TRAIN_STATE) -> np.ndarray:
+    """float32 [rows, d] standard-normal hidden states."""
+    return normal(seed, stream, rows * d).reshape(rows, d).astype(np.float32)

@@ -203,3 +203,25 @@ def test_profiling_mode_validated(lib):
     # an unknown mode is rejected
     assert lib.tlf_set_profiling(None, 3) == tlf.E_INVALID_ARG
     assert lib.tlf_set_profiling(None, -1) == tlf.E_INVALID_ARG
+
+
+def test_gather_scatter_argument_errors_need_no_device():
+    """Shape errors of the gather-scatter calls are caught on the host, before
+    any HIP call, so they can be checked without a GPU."""
+    lib = tlf.load()
+    bad = tlf.E_INVALID_ARG
+    dummy = ctypes.c_void_p(16)
+    assert lib.tlf_gs_plan(dummy, -1, 4, 1, dummy, None, None, dummy, None) == bad
+    assert lib.tlf_gs_plan(dummy, 2, 4, 1, dummy, None, None, None, None) == bad
+    assert lib.tlf_gs_plan(None, 2, 4, 1, dummy, None, None, dummy, None) == bad
+    assert lib.tlf_gs_gather(dummy, dummy, dummy, 8, 6, dummy, None) == bad     # d % 4
+    assert lib.tlf_gs_gather(dummy, dummy, dummy, -1, 8, dummy, None) == bad
+    assert lib.tlf_gs_gather(ctypes.c_void_p(20), dummy, dummy, 8, 8, dummy, None) == bad  # alignment
+    assert lib.tlf_gs_gather(dummy, dummy, dummy, 0, 8, dummy, None) == tlf.OK   # nothing to do
+    assert lib.tlf_gs_scatter(dummy, dummy, dummy, 8, 0, dummy, None) == bad
+    assert lib.tlf_gs_scatter(dummy, None, dummy, 8, 8, dummy, None) == bad
+    assert lib.tlf_gs_scatter(dummy, dummy, dummy, 0, 8, dummy, None) == tlf.OK
+    assert lib.tlf_ste(dummy, dummy, dummy, -1, dummy, dummy, None) == bad
+    assert lib.tlf_ste(None, dummy, dummy, 4, dummy, None, None) == bad
+    assert lib.tlf_ste(dummy, None, dummy, 4, None, dummy, None) == bad
+    assert lib.tlf_ste(dummy, dummy, dummy, 4, None, None, None) == tlf.OK

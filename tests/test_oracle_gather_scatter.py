@@ -146,3 +146,6 @@ def test_ste():
     # sigma'(0) = 1/4; far tails vanish
     assert gs.ste_grad(np.zeros(1), np.ones(1))[0] == pytest.approx(0.25, abs=0)
     assert gs.ste_grad(np.array([40.0, -40.0]), np.ones(2)).max() < 1e-16
+    # far tails keep full relative precision: sigma'(s) ~ exp(-|s|)
+    far = gs.ste_grad(np.array([60.0, -60.0]), np.ones(2))
+    np.testing.assert_allclose(far, np.exp(-60.0) * np.ones(2), rtol=1e-12)
