@@ -363,7 +363,8 @@ def prefill_measure(torch, tlf, synth, name):
 def train_gather_scatter(torch, synth, B=8, T=4096, d=1024, R=8, reps=20):
     """Training-side gather-scatter over all R loops of a batch of B x T tokens
     (float32 states of width d, depths drawn from the routed decode's depth
-    mix): forward gather + out-of-place scatter per loop, backward gather of
+    mix): forward gather + out-of-place (and, separately, in-place) scatter
+    per loop, backward gather of
     the state gradient + in-place scatter of the compact gradient per loop.
     Launched from a captured HIP graph (the host enqueues slower than these
     kernels run); HIP events around the replays on the capture's stream."""
@@ -382,6 +383,13 @@ def train_gather_scatter(torch, synth, B=8, T=4096, d=1024, R=8, reps=20):
         for i, p in enumerate(plans):
             train.gather_raw(H[i], p, out=X[i])
             train.scatter_raw(H[i], Y[i], p, out=H[i + 1])
+
+    Hin = torch.empty_like(H[0])
+
+    def forward_in_place():
+        for i, p in enumerate(plans):
+            train.gather_raw(Hin, p, out=X[i])
+            train.scatter_raw(Hin, Y[i], p, out=Hin)
 
     def backward():
         for i in reversed(range(R)):
@@ -414,17 +422,22 @@ def train_gather_scatter(torch, synth, B=8, T=4096, d=1024, R=8, reps=20):
         return e0.elapsed_time(e1) / reps
 
     fwd_ms, bwd_ms, plan_ms = timed(forward), timed(backward), timed(plan_all)
+    Hin.copy_(H[0])
+    fwi_ms = timed(forward_in_place)
     n = [p.count for p in plans]
     fwd_bytes = sum(4 * c + 2 * 4 * c * d + 4 * rows + 4 * rows * d * 2 + 4 * c * d for c in n)
     bwd_bytes = sum(4 * c + 2 * 4 * c * d + 4 * rows + 3 * 4 * c * d for c in n)
+    fwi_bytes = sum(4 * c + 2 * 4 * c * d + 4 * rows + 3 * 4 * c * d for c in n)
     plan_bytes = sum(4 * rows + 4 * c + 4 * rows + 4 * (B + 1) for c in n)
     return {"workload": f"training gather-scatter: batch {B} x {T} tokens, d={d} float32, R={R}, "
                         f"mean depth {float(depth.float().mean()):.2f}",
             "active_rows_per_loop": n,
             "forward_ms": fwd_ms, "forward_gbs": fwd_bytes / fwd_ms / 1e6,
+            "forward_in_place_ms": fwi_ms, "forward_in_place_gbs": fwi_bytes / fwi_ms / 1e6,
             "backward_ms": bwd_ms, "backward_gbs": bwd_bytes / bwd_ms / 1e6,
             "plan_us_per_loop": plan_ms * 1e3 / R, "plan_gbs": plan_bytes / plan_ms / 1e6,
             "frac": (fwd_bytes + bwd_bytes) / (fwd_ms + bwd_ms) / 1e6 / HBM_PEAK_GBS,
+            "frac_in_place": (fwi_bytes + bwd_bytes) / (fwi_ms + bwd_ms) / 1e6 / HBM_PEAK_GBS,
             "what": "per pass over all loops; algorithmic bytes: each gathered row read and written once, "
                     "an out-of-place scatter reads and writes every row and reads each block-output row, "
                     "an in-place scatter reads two and writes one row per active row; indices and slots "
@@ -665,7 +678,7 @@ def main():
         out["train_gather_scatter"] = train_gather_scatter(torch, synth)
         t = out["train_gather_scatter"]
         log(f"train gather-scatter: fwd {t['forward_ms']:.3f} ms {t['forward_gbs']:.0f} GB/s, "
-            f"bwd {t['backward_ms']:.3f} ms {t['backward_gbs']:.0f} GB/s, plan {t['plan_us_per_loop']:.1f} us/loop")
+            f"in place {t['forward_in_place_ms']:.3f} ms, bwd {t['backward_ms']:.3f} ms {t['backward_gbs']:.0f} GB/s, plan {t['plan_us_per_loop']:.1f} us/loop")
     if not args.no_sweep:
         out["router_threshold_sweep"] = threshold_sweep(torch, tlf, synth, args.config)
     if not args.no_cpu:

@@ -7,7 +7,7 @@ torch stream.  The shared block between gather and scatter is the caller's.
 
     p = plan(depth, batch, seq_len, loop)     # loop i's active rows
     x = gather(h, p)                          # [p.count, d], Eq. 6
-    h = scatter(h, block(x), p)               # Eq. 7
+    h = scatter(h, block(x), p)               # Eq. 7 (scatter_ writes into h)
 """
 from __future__ import annotations
 
@@ -122,6 +122,23 @@ class _Scatter(torch.autograd.Function):
         return g, gather_raw(g, ctx.p), None
 
 
+class _ScatterInPlace(torch.autograd.Function):
+    """Eq. 7 written into h_prev: neither gradient needs the previous state
+    (the block's backward uses its own compact input), so the rows that no
+    loop touches need not be copied."""
+    @staticmethod
+    def forward(ctx, h_prev, y, p):
+        ctx.p = p
+        scatter_raw(h_prev, y.contiguous(), p, out=h_prev)
+        ctx.mark_dirty(h_prev)
+        return h_prev
+
+    @staticmethod
+    def backward(ctx, g):
+        g = g.contiguous()
+        return g, gather_raw(g, ctx.p), None
+
+
 class _Ste(torch.autograd.Function):
     @staticmethod
     def forward(ctx, score, depth):
@@ -147,6 +164,12 @@ def gather(h: torch.Tensor, p: LoopPlan) -> torch.Tensor:
 def scatter(h_prev: torch.Tensor, y: torch.Tensor, p: LoopPlan) -> torch.Tensor:
     """Eq. 7 with its gradient (identity to h_prev, gathered rows to y)."""
     return _Scatter.apply(h_prev, y, p)
+
+
+def scatter_(h_prev: torch.Tensor, y: torch.Tensor, p: LoopPlan) -> torch.Tensor:
+    """Eq. 7 in place on h_prev (which must be contiguous and not a leaf that
+    requires grad); same gradients as `scatter`, traffic only on active rows."""
+    return _ScatterInPlace.apply(h_prev, y, p)
 
 
 def ste(score: torch.Tensor, depth: torch.Tensor) -> torch.Tensor:

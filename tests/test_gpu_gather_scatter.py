@@ -153,6 +153,19 @@ def test_autograd_through_loops_matches_oracle_backward():
         h = train.scatter(h, torch.tanh(train.gather(h, p) @ a), p)
     loss = (h * _dev(W)).sum()
     loss.backward()
+    # the in-place scatter (after an out-of-place first loop) gives the same
+    # values and gradients
+    h0b = _dev(H0).requires_grad_(True)
+    ab = _dev(A).requires_grad_(True)
+    hb = h0b
+    for i in range(1, R + 1):
+        p = train.plan(depth, B, T, i)
+        y = torch.tanh(train.gather(hb, p) @ ab)
+        hb = train.scatter(hb, y, p) if i == 1 else train.scatter_(hb, y, p)
+    (hb * _dev(W)).sum().backward()
+    assert torch.equal(hb.detach(), h.detach())
+    assert torch.equal(h0b.grad, h0.grad)
+    assert torch.equal(ab.grad, a.grad)
 
     H, saved = H0.astype(np.float64), []
     A64 = A.astype(np.float64)
