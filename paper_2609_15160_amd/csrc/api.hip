@@ -59,7 +59,7 @@ bool make_layout(const tlf_config& c, Layout* L) {
   sz[B_NACT] = R * 4;
   sz[B_Q_DEC] = B * d * 4;
   sz[B_O_DEC] = B * d * 4;
-  sz[B_ACT_DEC] = B * F * 4;
+  sz[B_ACT_DEC] = (int64_t)((B + 15) / 16 * 16) * F * 4;  // whole groups of 16 rows (fragment order)
   sz[B_KEYS] = B * ceil_div(c.vocab, kWave) * 8;  // greedy key per 64-column group of each row
   sz[B_X_PRE] = P * d * 4;
   sz[B_Y_PRE] = P * d * 4;
@@ -492,11 +492,13 @@ int run_decode(tlf_ctx* ctx, hipStream_t s, const int32_t* tokens, float* logits
       GemmArgs gu;  // act = silu(RMSNorm(x) W_g^T) * (RMSNorm(x) W_u^T)
       gu.A = xc; gu.lda = d; gu.W = lw.w_gate_up; gu.Wf = ctx->wfrag(j, 2); gu.N = 2 * F; gu.K = d; gu.w_rows = 2 * F; gu.rm = rm;
       gu.out = ctx->buf<float>(B_ACT_DEC); gu.ldo = F; gu.F = F; gu.eps = c.rms_eps; gu.spec = i == 0;
+      gu.out_frag = F % 32 == 0;  // act in MFMA fragment order for the down projection
       set_mod(ctx, &gu, i, j, 3, pa.row_depth, 0);
       TLF_HIP(launch_dgemm<T>(gu, A_CMP, E_SWIGLU, true, ctx->cus, s));
 
       GemmArgs dn;  // x += act W_d^T
       dn.A = ctx->buf<float>(B_ACT_DEC); dn.lda = F; dn.W = lw.w_down; dn.Wf = ctx->wfrag(j, 3); dn.N = d; dn.K = F; dn.w_rows = d;
+      dn.a_frag = F % 32 == 0;
       dn.rm = rm; dn.out = xc; dn.ldo = d; dn.spec = i == 0; dn.keep_depth = keep_depth; dn.keep_loop = i;
       set_mod(ctx, &dn, i, j, 1, pa.row_depth, 0);
       TLF_HIP(launch_dgemm<T>(dn, A_CMP, E_RESID, false, ctx->cus, s));

@@ -156,7 +156,7 @@ __device__ __forceinline__ void dgemm_tile(const GemmArgs& g, int nact, int act_
   for (int i = 0; i < RM; ++i) {
     const int r = min(r0 + i * 16 + c16, g.rm.rows - 1);
     const int arow = (AK == A_SRC) ? row_src(g.rm, r) : r;
-    ao[i] = arow * g.lda + quad * EPL;
+    ao[i] = g.a_frag ? ((arow >> 4) * S * kWave + quad * 16 + (arow & 15)) * EPL : arow * g.lda + quad * EPL;
   }
   // MOD: the lane's rows are scaled by (1 + gamma) of their modulation rows
   int go[MOD ? RM : 1];
@@ -191,7 +191,8 @@ __device__ __forceinline__ void dgemm_tile(const GemmArgs& g, int nact, int act_
     }
 #pragma unroll
     for (int j = 0; j < KB; ++j) {
-      const int k0 = min(w + W * (jb + j), S - 1) * KS;
+      const int stj = min(w + W * (jb + j), S - 1);
+      const int k0 = stj * KS, ka = stj * (g.a_frag ? kWave * EPL : KS);
 #pragma unroll
       for (int i = 0; i < RM; ++i) {
 #pragma unroll
@@ -203,8 +204,8 @@ __device__ __forceinline__ void dgemm_tile(const GemmArgs& g, int nact, int act_
         if (r0 + i * 16 >= a_rows) continue;  // uniform: the fragment's rows have exited
         if (r0 + i * 16 + c16 < a_rows) {
           if constexpr (EPL == 8) {
-            const float4 lo = *reinterpret_cast<const float4*>(Ab + (ao[i] + k0));
-            const float4 hi = *reinterpret_cast<const float4*>(Ab + (ao[i] + k0 + 4));
+            const float4 lo = *reinterpret_cast<const float4*>(Ab + (ao[i] + ka));
+            const float4 hi = *reinterpret_cast<const float4*>(Ab + (ao[i] + ka + 4));
             av[j][i][0] = lo.x; av[j][i][1] = lo.y; av[j][i][2] = lo.z; av[j][i][3] = lo.w;
             av[j][i][4] = hi.x; av[j][i][5] = hi.y; av[j][i][6] = hi.z; av[j][i][7] = hi.w;
             if constexpr (MOD) {
@@ -214,7 +215,7 @@ __device__ __forceinline__ void dgemm_tile(const GemmArgs& g, int nact, int act_
               gv[j][i][4] = ghi.x; gv[j][i][5] = ghi.y; gv[j][i][6] = ghi.z; gv[j][i][7] = ghi.w;
             }
           } else {
-            av[j][i][0] = Ab[ao[i] + k0];
+            av[j][i][0] = Ab[ao[i] + ka];
             if constexpr (MOD) gv[j][i][0] = g.mod_g[go[i] + k0];
           }
         }
@@ -332,7 +333,11 @@ __device__ __forceinline__ void dgemm_tile(const GemmArgs& g, int nact, int act_
       const int unit = ((n0 + gcol) >> 5) * 16 + (u % 16);
       if (r0 + row >= row_end || unit >= g.F) continue;
       const float gt = tile_sum(row, gcol), up = tile_sum(row, gcol + 16);
-      g.out[(int64_t)(r0 + row) * g.ldo + unit] = gt / (1.f + __expf(-gt)) * up;
+      const int R = r0 + row;
+      const int64_t o = g.out_frag ? ((int64_t)((R >> 4) * (g.F / KS) + unit / KS) * kWave +
+                                      (unit % KS) / EPL * 16 + (R & 15)) * EPL + unit % EPL
+                                   : (int64_t)R * g.ldo + unit;
+      g.out[o] = gt / (1.f + __expf(-gt)) * up;
     } else if constexpr (EK == E_LOGITS) {
       const int row = e / BN, n = n0 + e % BN;
       const bool ok = r0 + row < row_end && n < g.N;
@@ -463,6 +468,8 @@ hipError_t launch_w(const GemmArgs& a, int cus, hipStream_t s) {
 template <typename T>
 hipError_t launch_dgemm(const GemmArgs& a, AKind ak, EKind ek, bool norm, int cus, hipStream_t s) {
   if (a.K % Mfma<T>::KS != 0 || a.rm.rows <= 0 || cus <= 0) return hipErrorInvalidValue;
+  if (a.a_frag && (ak != A_CMP || norm || a.mod_g || a.a_copy)) return hipErrorInvalidValue;
+  if (a.out_frag && (ek != E_SWIGLU || a.F % Mfma<T>::KS != 0)) return hipErrorInvalidValue;
   const bool mod = a.mod_g != nullptr;
   if (ek == E_QKV && norm) {
     if (ak == A_SRC)

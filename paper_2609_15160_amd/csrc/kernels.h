@@ -74,6 +74,15 @@ struct GemmArgs {
   int lda = 0;
   const void* W = nullptr;  // [W rows][K] storage dtype
   const void* Wf = nullptr; // launch_dgemm: the same weights in MFMA fragment order (launch_wfrag), or nullptr
+  // launch_dgemm: activations in MFMA fragment order.  For rows R and
+  // columns k of a [rows][K] operand, element (R, k) sits at
+  //   ((R / 16 * (K / KS) + k / KS) * 64 + (k % KS) / EPL * 16 + R % 16) * EPL + k % EPL
+  // (KS, EPL of the model dtype's MFMA), so the 64 lanes' fragments of one
+  // K step of 16 rows are one contiguous run.  a_frag: A is stored so (A_CMP,
+  // no norm, no a_copy); out_frag: an E_SWIGLU epilogue writes act so (K = F).
+  // Buffers hold whole groups of 16 rows.
+  int a_frag = 0;
+  int out_frag = 0;
   int N = 0;                // output columns (E_SWIGLU: 2F in the interleaved gate/up space)
   int K = 0;
   int w_rows = 0;           // rows of W (loads are clamped below it)
