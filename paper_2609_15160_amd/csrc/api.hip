@@ -58,7 +58,7 @@ bool make_layout(const tlf_config& c, Layout* L) {
   sz[B_PERM] = B * 4;
   sz[B_NACT] = R * 4;
   sz[B_Q_DEC] = B * d * 4;
-  sz[B_O_DEC] = B * d * 4;
+  sz[B_O_DEC] = (int64_t)((B + 15) / 16 * 16) * d * 4;  // whole groups of 16 rows (fragment order)
   sz[B_ACT_DEC] = (int64_t)((B + 15) / 16 * 16) * F * 4;  // whole groups of 16 rows (fragment order)
   sz[B_KEYS] = B * ceil_div(c.vocab, kWave) * 8;  // greedy key per 64-column group of each row
   sz[B_X_PRE] = P * d * 4;
@@ -472,6 +472,7 @@ int run_decode(tlf_ctx* ctx, hipStream_t s, const int32_t* tokens, float* logits
       AttnDecodeArgs at;
       at.c = ctx->cv; at.loop = i; at.layer = j; at.d = d; at.perm = perm; at.nact = nact + i;
       at.q = ctx->buf<float>(B_Q_DEC); at.o = ctx->buf<float>(B_O_DEC);
+      if (d % 32 == 0) { at.o_ks = Mfma<T>::KS; at.o_epl = Mfma<T>::EPL; }  // o in fragment order for O
       at.scale_log2 = 1.4426950408889634f / std::sqrt((float)c.head_dim);
       at.waves = attn_waves(ctx);
       at.grid = ctx->cus * ctx->attn_blocks[at.waves == 4 ? 0 : 1];
@@ -485,6 +486,7 @@ int run_decode(tlf_ctx* ctx, hipStream_t s, const int32_t* tokens, float* logits
 
       GemmArgs o;  // x += o W_o^T
       o.A = ctx->buf<float>(B_O_DEC); o.lda = d; o.W = lw.w_o; o.Wf = ctx->wfrag(j, 1); o.N = d; o.K = d; o.w_rows = d; o.rm = rm;
+      o.a_frag = d % 32 == 0;
       o.out = xc; o.ldo = d; o.spec = i == 0; o.keep_depth = keep_depth; o.keep_loop = i;
       set_mod(ctx, &o, i, j, 0, pa.row_depth, 0);
       TLF_HIP(launch_dgemm<T>(o, A_CMP, E_RESID, false, ctx->cus, s));

@@ -249,7 +249,11 @@ __global__ __launch_bounds__(W * 64) void k_attn_decode(AttnDecodeArgs a) {
           Mx = mn;
         }
         // an empty cache (a discarded row of the dense decode) gives zeros
-        a.o[(int64_t)k * a.d + h * D + dim] = Ls > 0.f ? O / Ls : 0.f;
+        const int c = h * D + dim;
+        const int64_t oi = a.o_ks > 0 ? ((int64_t)((k >> 4) * (a.d / a.o_ks) + c / a.o_ks) * kWave +
+                                         (c % a.o_ks) / a.o_epl * 16 + (k & 15)) * a.o_epl + c % a.o_epl
+                                      : (int64_t)k * a.d + c;
+        a.o[oi] = Ls > 0.f ? O / Ls : 0.f;
       }
     }
   }

@@ -233,7 +233,8 @@ struct AttnDecodeArgs {
   const int32_t* perm = nullptr;   // depth-sorted row order
   const int32_t* nact = nullptr;   // n_i of this loop: rows [0, n_i) are active
   const float* q = nullptr;        // [rows][d] compact rows
-  float* o = nullptr;              // [rows][d]
+  float* o = nullptr;              // [rows][d], or in MFMA fragment order (o_ks > 0)
+  int o_ks = 0, o_epl = 0;         // o in the fragment order of GemmArgs::a_frag with this KS, EPL
   float scale_log2 = 0.f;          // log2(e) / sqrt(D)
   int grid = 0;                    // persistent workgroups
   int waves = 4;                   // waves per workgroup sharing one (row, head): 4 or 8
