@@ -472,7 +472,9 @@ int run_decode(tlf_ctx* ctx, hipStream_t s, const int32_t* tokens, float* logits
       AttnDecodeArgs at;
       at.c = ctx->cv; at.loop = i; at.layer = j; at.d = d; at.perm = perm; at.nact = nact + i;
       at.q = ctx->buf<float>(B_Q_DEC); at.o = ctx->buf<float>(B_O_DEC);
-      if (d % 32 == 0) { at.o_ks = Mfma<T>::KS; at.o_epl = Mfma<T>::EPL; }  // o in fragment order for O
+      // o and act in MFMA fragment order for the O and down projections (d and F
+      // are multiples of 64 or 128, so of KS: validate_config)
+      at.o_ks = Mfma<T>::KS; at.o_epl = Mfma<T>::EPL;
       at.scale_log2 = 1.4426950408889634f / std::sqrt((float)c.head_dim);
       at.waves = attn_waves(ctx);
       at.grid = ctx->cus * ctx->attn_blocks[at.waves == 4 ? 0 : 1];
@@ -486,7 +488,7 @@ int run_decode(tlf_ctx* ctx, hipStream_t s, const int32_t* tokens, float* logits
 
       GemmArgs o;  // x += o W_o^T
       o.A = ctx->buf<float>(B_O_DEC); o.lda = d; o.W = lw.w_o; o.Wf = ctx->wfrag(j, 1); o.N = d; o.K = d; o.w_rows = d; o.rm = rm;
-      o.a_frag = d % 32 == 0;
+      o.a_frag = 1;
       o.out = xc; o.ldo = d; o.spec = i == 0; o.keep_depth = keep_depth; o.keep_loop = i;
       set_mod(ctx, &o, i, j, 0, pa.row_depth, 0);
       TLF_HIP(launch_dgemm<T>(o, A_CMP, E_RESID, false, ctx->cus, s));
@@ -494,13 +496,13 @@ int run_decode(tlf_ctx* ctx, hipStream_t s, const int32_t* tokens, float* logits
       GemmArgs gu;  // act = silu(RMSNorm(x) W_g^T) * (RMSNorm(x) W_u^T)
       gu.A = xc; gu.lda = d; gu.W = lw.w_gate_up; gu.Wf = ctx->wfrag(j, 2); gu.N = 2 * F; gu.K = d; gu.w_rows = 2 * F; gu.rm = rm;
       gu.out = ctx->buf<float>(B_ACT_DEC); gu.ldo = F; gu.F = F; gu.eps = c.rms_eps; gu.spec = i == 0;
-      gu.out_frag = F % 32 == 0;  // act in MFMA fragment order for the down projection
+      gu.out_frag = 1;
       set_mod(ctx, &gu, i, j, 3, pa.row_depth, 0);
       TLF_HIP(launch_dgemm<T>(gu, A_CMP, E_SWIGLU, true, ctx->cus, s));
 
       GemmArgs dn;  // x += act W_d^T
       dn.A = ctx->buf<float>(B_ACT_DEC); dn.lda = F; dn.W = lw.w_down; dn.Wf = ctx->wfrag(j, 3); dn.N = d; dn.K = F; dn.w_rows = d;
-      dn.a_frag = F % 32 == 0;
+      dn.a_frag = 1;
       dn.rm = rm; dn.out = xc; dn.ldo = d; dn.spec = i == 0; dn.keep_depth = keep_depth; dn.keep_loop = i;
       set_mod(ctx, &dn, i, j, 1, pa.row_depth, 0);
       TLF_HIP(launch_dgemm<T>(dn, A_CMP, E_RESID, false, ctx->cus, s));
