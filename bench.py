@@ -374,9 +374,10 @@ def train_gather_scatter(torch, synth, B=8, T=4096, d=1024, R=8, reps=20):
     plans = [train.plan(depth, B, T, i) for i in range(1, R + 1)]
     H = [torch.from_numpy(synth.make_train_states(rows, d)).cuda()]
     H += [torch.empty_like(H[0]) for _ in range(R)]
-    Y = [torch.randn(p.count, d, device="cuda") for p in plans]
+    gen = torch.Generator(device="cuda").manual_seed(synth.SEED)  # seeded block outputs and gradients
+    Y = [torch.randn(p.count, d, device="cuda", generator=gen) for p in plans]
     X = [torch.empty(p.count, d, device="cuda") for p in plans]
-    dH = torch.randn(rows, d, device="cuda")
+    dH = torch.randn(rows, d, device="cuda", generator=gen)
     dY = [torch.empty(p.count, d, device="cuda") for p in plans]
 
     def forward():
