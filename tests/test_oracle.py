@@ -509,6 +509,117 @@ def test_adaln_literal_cache_equals_compact_cache():
     assert np.max(np.abs(a - b)) < 1e-12
 
 
+# ---------------------------------------------------------------------------
+# bf16 rounding mode of the oracle (the storage points of a bf16 implementation)
+# ---------------------------------------------------------------------------
+
+def _f32_from_bits(bits):
+    return np.asarray(bits, dtype=np.uint32).view(np.float32)
+
+
+def _bf16_by_definition(x32: float) -> float:
+    """Nearest bfloat16 to a finite float32 value, ties to the even
+    significand, found by comparing exact distances (fractions) to the two
+    bfloat16 values that bracket it: the one with the low 16 bits of the
+    float32 encoding cleared (toward zero) and the next one away from zero."""
+    from fractions import Fraction
+    b = int(np.float32(x32).view(np.uint32))
+    lo = b & 0xFFFF0000
+    if lo == b:
+        return float(np.float32(x32))
+    hi = lo + 0x10000
+    x = Fraction(float(np.float32(x32)))
+    vlo = Fraction(float(_f32_from_bits([lo])[0]))
+    if (hi & 0x7FFFFFFF) >= 0x7F800000:      # the next one up is infinite
+        top = Fraction(2) ** 128              # where the bf16 ladder would put it
+        vhi = top if x > 0 else -top
+    else:
+        vhi = Fraction(float(_f32_from_bits([hi])[0]))
+    dlo, dhi = abs(x - vlo), abs(vhi - x)
+    if dlo < dhi or (dlo == dhi and ((lo >> 16) & 1) == 0):
+        return float(vlo)
+    return float(_f32_from_bits([hi])[0])
+
+
+_BF16_EDGE_BITS = [
+    0x3F808000, 0x3F818000, 0xBF808000, 0xBF818000,   # ties: 1 + 2^-8, 1 + 3 * 2^-8 and negatives
+    0x3F807FFF, 0x3F808001, 0x3F817FFF, 0x3F818001,   # one float32 step either side of a tie
+    0x3F7FFFFF, 0x3FFF8000, 0x3FFF7FFF, 0xBFFF8000,   # carries into the exponent (up to 1.0, 2.0)
+    0x00000001, 0x00008000, 0x00018000, 0x00017FFF,   # subnormals: ties at 0 and at the first step
+    0x80008000, 0x807FFFFF, 0x00800000, 0x007FFFFF,   # the normal / subnormal boundary
+    0x7F7F7FFF, 0x7F7F8000, 0x7F7FFFFF, 0xFF7FFFFF,   # the largest values (the last two overflow)
+    0x00000000, 0x80000000, 0x3F800000, 0x42F6E979,   # exact values and one arbitrary value
+]
+
+
+def test_round_bf16_against_definition_and_torch_cast():
+    """The oracle's bf16 rounding is round-to-nearest-even: it equals the
+    exact nearest-value definition on ties, near-ties, exponent carries,
+    subnormals and overflow, and torch's float32 -> bfloat16 cast on those and
+    on random float32 encodings."""
+    import torch
+    x = _f32_from_bits(_BF16_EDGE_BITS)
+    got = O._round_bf16(x.astype(np.float64))
+    want = np.array([_bf16_by_definition(v) for v in x])
+    assert np.array_equal(got, want)
+    torch_cast = torch.from_numpy(x).to(torch.bfloat16).to(torch.float64).numpy()
+    assert np.array_equal(got, torch_cast)
+    assert got[0] == 1.0 and got[1] == 1.0 + 2 ** -6 and got[8] == 1.0 and got[9] == 2.0
+    assert np.isinf(got[22]) and np.isinf(got[23])
+    rng = np.random.default_rng(5)
+    bits = rng.integers(0, 2 ** 32, size=200000, dtype=np.uint64).astype(np.uint32)
+    bits = bits[(bits & 0x7F800000) != 0x7F800000]          # finite encodings
+    r = _f32_from_bits(bits)
+    got = O._round_bf16(r.astype(np.float64))
+    assert np.array_equal(got, torch.from_numpy(r).to(torch.bfloat16).to(torch.float64).numpy())
+    for v, g in zip(r[:300], got[:300]):
+        assert g == _bf16_by_definition(v)
+
+
+def test_round_bf16_of_float64_goes_through_float32():
+    """A float64 value is rounded as the float32 value a kernel would hold: to
+    float32 first, then to bf16 (1 + 2^-8 + 2^-30 is a float32 tie, so it goes
+    to 1.0, where rounding the float64 value directly would give 1 + 2^-7)."""
+    import torch
+    x = np.array([1.0 + 2 ** -8 + 2 ** -30, -(1.0 + 2 ** -8 + 2 ** -30), 0.1, 1e-40, 3.0e38])
+    want = torch.from_numpy(x).to(torch.float32).to(torch.bfloat16).to(torch.float64).numpy()
+    assert np.array_equal(O._round_bf16(x), want)
+    assert O._round_bf16(x)[0] == 1.0
+
+
+@pytest.mark.parametrize("variant", ["fixed3", "routed"])
+def test_bf16_rounding_points_equal_library_casts(variant):
+    """round_bf16=True rounds exactly where a bf16 implementation stores a
+    value (projection inputs, q/k/v, attention output, SwiGLU product, the
+    head's normalised input): it equals an independent PyTorch model that
+    applies torch's bfloat16 cast at those points, and differs from the
+    unrounded model."""
+    import torch
+    cfg = synth.tiny_config(max_loops=4, prompt_len=14)
+    w = synth.make_weights(cfg)
+    toks = synth.make_prompts(cfg)[0]
+    kw = dict(route_rule=O.FIXED, fixed_depth=3) if variant == "fixed3" else {}
+    M = _model(cfg, w, round_bf16=True, **kw)
+    st, logits, m, _ = O.prefill(M, toks, all_logits=True)
+    if variant == "fixed3":
+        ref = textbook.tied_gpt_logits(w, toks, cfg.n_heads, cfg.head_dim, 3, cfg.rms_eps,
+                                       rnd=textbook.bf16_cast)
+    else:
+        assert len(set(m.tolist())) >= 2
+        ref = textbook.routed_dense_logits(w, toks, m, cfg.n_heads, cfg.head_dim, cfg.rms_eps,
+                                           rnd=textbook.bf16_cast)
+    assert np.max(np.abs(logits - ref)) < 1e-12
+    _, plain, _, _ = O.prefill(_model(cfg, w, **kw), toks, all_logits=True)
+    assert np.max(np.abs(plain - logits)) > 1e-5
+    # the cached keys and values are bf16 values
+    for i in range(M.R):
+        for j in range(M.J):
+            for a in (st.K[i][j], st.V[i][j]):
+                f = a.astype(np.float32)
+                assert np.array_equal(f.astype(np.float64), a)
+                assert np.all((f.view(np.uint32) & 0xFFFF) == 0)
+
+
 def test_bf16_rounding_mode_stays_close():
     cfg = synth.tiny_config(batch=1, prompt_len=12, steps=3)
     w = synth.make_weights(cfg)
@@ -516,6 +627,24 @@ def test_bf16_rounding_mode_stays_close():
     _, _, b, _ = _run(cfg, w, model_kw=dict(round_bf16=True))
     err = np.max(np.abs(a - b))
     assert 0 < err < 3e-2
+
+
+def test_greedy_lowest_id_among_float32_maxima():
+    """The greedy token is the lowest id among the maxima of the float32
+    rounding of the logits (values equal after that rounding are ties)."""
+    import torch
+    lg = np.array([[0.1, 0.3, 0.3, -1.0],
+                   [1.0, 1.0 + 1e-12, 0.5, 1.0],      # equal in float32: id 0
+                   [-2.0, -1.0, -1.0 - 1e-9, -3.0],   # equal in float32: id 1
+                   [0.0, 0.0, 0.0, 0.0],
+                   [-np.inf, 5.0, np.inf, np.inf]])
+    assert O.greedy(lg).tolist() == [1, 0, 1, 0, 2]
+    rng = np.random.default_rng(9)
+    big = rng.standard_normal((64, 32000))
+    big[:, 17] = big[:, 4000] = big.max(axis=1) + 1.0      # two exact maxima per row
+    assert np.array_equal(O.greedy(big), np.full(64, 17))
+    r = np.round(rng.standard_normal((64, 1000)), 1)        # many ties
+    assert np.array_equal(O.greedy(r), torch.argmax(torch.from_numpy(r.astype(np.float32)), -1).numpy())
 
 
 # ---------------------------------------------------------------------------

@@ -19,25 +19,38 @@ def _rms(x, eps):
     return x * torch.rsqrt((x * x).mean(-1, keepdim=True) + eps)
 
 
-def _layer(x, lw, H, D, eps, attn_mask=None, is_causal=False, mod=None):
+def _keep(x):
+    return x
+
+
+def bf16_cast(x):
+    """torch's own casts: float64 -> float32 -> bfloat16 (round to nearest even),
+    widened back to float64."""
+    return x.to(torch.float32).to(torch.bfloat16).to(f64)
+
+
+def _layer(x, lw, H, D, eps, attn_mask=None, is_causal=False, mod=None, rnd=_keep):
     """Pre-norm layer; ``mod`` = per-row AdaLN (shift-free) modulation
-    [T][4d] split as (alpha_msa, alpha_mlp, gamma_msa, gamma_mlp), or None."""
+    [T][4d] split as (alpha_msa, alpha_mlp, gamma_msa, gamma_mlp), or None.
+    ``rnd`` is applied where a bf16 implementation stores a value: the
+    normalised inputs of the projections, q, k and v, the attention output
+    and the SwiGLU product."""
     T, d = x.shape
     if mod is not None:
         a_msa, a_mlp, g_msa, g_mlp = mod.split(d, dim=-1)
     y = _rms(x, eps)
     if mod is not None:
         y = y * (1 + g_msa)
-    qkv = F.linear(y, _t(lw["w_qkv"]))
+    qkv = rnd(F.linear(rnd(y), _t(lw["w_qkv"])))
     q, k, v = (t.reshape(T, H, D).transpose(0, 1) for t in qkv.split(d, dim=-1))
     o = F.scaled_dot_product_attention(q, k, v, attn_mask=attn_mask, is_causal=is_causal)
-    b = F.linear(o.transpose(0, 1).reshape(T, d), _t(lw["w_o"]))
+    b = F.linear(rnd(o.transpose(0, 1).reshape(T, d)), _t(lw["w_o"]))
     x = x + (b if mod is None else (1 + a_msa) * b)
     y2 = _rms(x, eps)
     if mod is not None:
         y2 = y2 * (1 + g_mlp)
-    g, u = F.linear(y2, _t(lw["w_gate_up"])).chunk(2, dim=-1)
-    b = F.linear(F.silu(g) * u, _t(lw["w_down"]))
+    g, u = F.linear(rnd(y2), _t(lw["w_gate_up"])).chunk(2, dim=-1)
+    b = F.linear(rnd(F.silu(g) * u), _t(lw["w_down"]))
     return x + (b if mod is None else (1 + a_mlp) * b)
 
 
@@ -61,7 +74,7 @@ def adaln_modulation(weights, lw, loop, depths):
     return F.linear(F.silu(c), _t(lw["w_mod"]), _t(lw["b_mod"]))
 
 
-def tied_gpt_logits(weights, tokens, H, D, loops, eps=1e-5):
+def tied_gpt_logits(weights, tokens, H, D, loops, eps=1e-5, rnd=_keep):
     """Pre-norm GPT whose layer stack is the J-layer block repeated ``loops``
     times (every token of depth ``loops`` when the weights carry AdaLN)."""
     tokens = torch.as_tensor(np.asarray(tokens, dtype=np.int64))
@@ -71,9 +84,9 @@ def tied_gpt_logits(weights, tokens, H, D, loops, eps=1e-5):
     for i in range(1, loops + 1):
         for lw in weights["layers"]:
             mod = adaln_modulation(weights, lw, i, [loops] * T) if weights.get("cond") else None
-            x = _layer(x, lw, H, D, eps, is_causal=True, mod=mod)
+            x = _layer(x, lw, H, D, eps, is_causal=True, mod=mod, rnd=rnd)
     head = E if weights.get("lm_head") is None else _t(weights["lm_head"])
-    return F.linear(_rms(x, eps), head).numpy()
+    return F.linear(rnd(_rms(x, eps)), head).numpy()
 
 
 def router_logits(weights, h0):
@@ -92,7 +105,7 @@ def routed_argmax_depths(weights, tokens):
     return (torch.argmax(z, dim=-1) + 1).numpy()
 
 
-def routed_dense_logits(weights, tokens, depths, H, D, eps=1e-5):
+def routed_dense_logits(weights, tokens, depths, H, D, eps=1e-5, rnd=_keep):
     """Routed model computed densely: every loop runs on all rows, attention
     is causal and restricted to keys whose depth reaches the loop, and only
     rows whose depth reaches the loop take the new state."""
@@ -113,6 +126,6 @@ def routed_dense_logits(weights, tokens, depths, H, D, eps=1e-5):
         xn = x
         for lw in weights["layers"]:
             mod = adaln_modulation(weights, lw, i, depths.numpy()) if weights.get("cond") else None
-            xn = _layer(xn, lw, H, D, eps, attn_mask=mask, mod=mod)
+            xn = _layer(xn, lw, H, D, eps, attn_mask=mask, mod=mod, rnd=rnd)
         x = torch.where(act[:, None], xn, x)
-    return F.linear(_rms(x, eps), E).numpy()
+    return F.linear(rnd(_rms(x, eps)), E).numpy()
