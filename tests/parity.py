@@ -122,11 +122,22 @@ class OracleRun:
 
 def run_oracle(model: synth.ModelConfig, weights: Dict, prompts: np.ndarray,
                step_tokens: Sequence[np.ndarray], route_rule: str = "argmax", threshold: float = 0.5,
-               fixed_depth: Optional[int] = None, all_logits: bool = False) -> OracleRun:
+               fixed_depth: Optional[int] = None, all_logits: bool = False, threads: int = 1) -> OracleRun:
+    """The oracle on the same prompts, teacher-forced on ``step_tokens``.
+    ``threads`` > 1 prefills the (independent) sequences concurrently."""
     M = O.Model(weights, model.n_heads, model.head_dim, route_rule=route_rule, threshold=threshold,
                 fixed_depth=fixed_depth, rms_eps=model.rms_eps)
     t0 = time.perf_counter()
-    states, lg, dep, mg = O.prefill_batch(M, prompts, all_logits=all_logits)
+    if threads > 1 and len(prompts) > 1:
+        import concurrent.futures
+        cap = prompts.shape[1] + len(step_tokens)
+        with concurrent.futures.ThreadPoolExecutor(max_workers=threads) as ex:
+            outs = list(ex.map(lambda row: O.prefill(M, row, capacity=cap, all_logits=all_logits),
+                               np.asarray(prompts)))
+        states = [x[0] for x in outs]
+        lg, dep, mg = (np.stack([x[k] for x in outs]) for k in (1, 2, 3))
+    else:
+        states, lg, dep, mg = O.prefill_batch(M, prompts, all_logits=all_logits)
     t1 = time.perf_counter()
     run = OracleRun(lg, dep, mg, [], [], [], [])
     for tok in step_tokens:

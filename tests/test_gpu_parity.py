@@ -47,6 +47,15 @@ def _f32_small(**kw):
     return synth.ModelConfig(**base)
 
 
+def _oracle_depths(o: parity.OracleRun):
+    """The oracle's depth of every token, prompt then decode steps: [B][T+S]."""
+    return np.concatenate([o.prefill_depths] + [d[:, None] for d in o.step_depths], axis=1)
+
+
+def _oracle_margins(o: parity.OracleRun):
+    return np.concatenate([o.prefill_margin] + [mg[:, None] for mg in o.step_margin], axis=1)
+
+
 def _check_f32(m, w, prompts, g, o, tag):
     assert np.array_equal(g.prefill_depths, o.prefill_depths)
     for s in range(len(g.step_depths)):
@@ -61,6 +70,34 @@ def _check_f32(m, w, prompts, g, o, tag):
         assert np.array_equal(g.step_next[s], np.argmax(g.step_logits[s], axis=-1))
     _report(tag, max_abs_logit_err=f"{err:.3g}", steps=len(g.step_logits),
             depth_hist=g.stats["depth_hist"])
+    assert err <= F32_TOL
+    assert np.all(np.isfinite(g.prefill_logits))
+
+
+def _check_f32_near_ties(m, w, prompts, g, o, tag, tie_margin=1e-5):
+    """For depth rules whose decisions can sit at a near tie (the cumulative
+    rule, an MLP router): every decision, prompt and decode steps, that differs
+    from the oracle's has an oracle margin <= tie_margin; every sequence whose
+    whole depth stream equals the oracle's is checked like _check_f32 (logits,
+    cache index), and at least one sequence is.  Greedy ids equal the first
+    argmax of the GPU's own logits everywhere."""
+    gd, od, om = _all_depths(g), _oracle_depths(o), _oracle_margins(o)
+    differ = gd != od
+    assert np.all(om[differ] <= tie_margin), om[differ]
+    same = [b for b in range(prompts.shape[0]) if not differ[b].any()]
+    assert len(same) >= 1, "no sequence with the oracle's depth stream"
+    err = 0.0
+    for b in same:
+        err = max(err, _max_err(g.prefill_logits[b], o.prefill_logits[b]))
+        for s in range(len(g.step_logits)):
+            err = max(err, _max_err(g.step_logits[s][b], o.step_logits[s][b]))
+        for i in range(m.max_loops):
+            assert np.array_equal(g.stats["index"][b][i], o.index[b][i]), (b, i)
+    _check_index_matches_depths(g, m.max_loops)
+    for s in range(len(g.step_next)):
+        assert np.array_equal(g.step_next[s], np.argmax(g.step_logits[s], axis=-1))
+    _report(tag, compared_sequences=f"{len(same)}/{prompts.shape[0]}", near_tie_flips=int(differ.sum()),
+            max_abs_logit_err=f"{err:.3g}", depth_hist=g.stats["depth_hist"])
     assert err <= F32_TOL
     assert np.all(np.isfinite(g.prefill_logits))
 
@@ -151,12 +188,8 @@ def test_f32_cumprob_rule():
     prompts = synth.make_prompts(m)
     g = parity.run_gpu(m, w, prompts, m.steps, route_rule="cumprob", threshold=0.5)
     o = parity.run_oracle(m, w, prompts, g.step_tokens, route_rule="cumprob", threshold=0.5)
-    bad, flips = parity.depth_agreement(g.prefill_depths, o.prefill_depths, o.prefill_margin, 1e-5)
-    _report("cumprob", flips=flips, hist=g.stats["depth_hist"])
-    assert bad == 0
     assert len(set(g.prefill_depths.ravel().tolist())) >= 3
-    if flips == 0:
-        _check_f32(m, w, prompts, g, o, "cumprob")
+    _check_f32_near_ties(m, w, prompts, g, o, "cumprob")
 
 
 @pytest.mark.parametrize("depth", [1, 4])
@@ -186,9 +219,8 @@ def test_f32_wide_heads(head_dim):
 
 @pytest.mark.parametrize("rule", ["argmax", "cumprob", "argmax-B1"])
 def test_f32_mlp_router(rule):
-    """Two-layer MLP router (hidden 64): decisions with a clear margin match the
-    oracle; when none is near a tie, depths, cache indices and logits match at
-    the fp32 bar."""
+    """Two-layer MLP router (hidden 64): decisions differ from the oracle's only
+    at near ties; sequences with the oracle's depths match it at the fp32 bar."""
     batch = 1 if rule.endswith("-B1") else 3
     rule = rule.split("-")[0]
     m = _f32_small(router_hidden=64, router_bias="calibrated", steps=10, batch=batch, prompt_len=37 * (4 - batch))
@@ -196,12 +228,8 @@ def test_f32_mlp_router(rule):
     prompts = synth.make_prompts(m)
     g = parity.run_gpu(m, w, prompts, m.steps, route_rule=rule, threshold=0.5)
     o = parity.run_oracle(m, w, prompts, g.step_tokens, route_rule=rule, threshold=0.5)
-    bad, flips = parity.depth_agreement(g.prefill_depths, o.prefill_depths, o.prefill_margin, 1e-5)
-    _report(f"mlp-router-{rule}", flips=flips, hist=g.stats["depth_hist"])
-    assert bad == 0
     assert len(set(g.prefill_depths.ravel().tolist())) >= 2
-    if flips == 0:
-        _check_f32(m, w, prompts, g, o, f"mlp-router-{rule}")
+    _check_f32_near_ties(m, w, prompts, g, o, f"mlp-router-{rule}")
 
 
 def test_prefill_in_sequence_groups_is_identical():
@@ -258,6 +286,13 @@ def test_graph_replays_match_eager_launches(name):
 
 
 def _check_bf16(m, w, prompts, g, o, sample, tag, route_rule="argmax", fixed_depth=None, threshold=0.5):
+    """bf16 bar.  Every token's depth (all sequences, prompt and decode steps)
+    against the oracle router: decisions with margin > 1e-2 match.  Every
+    cache index equals {t : m_t >= i} for the GPU's depths.  On the sampled
+    sequences (the oracle's rows): the greedy id is the first argmax of the
+    GPU's own logits at every step; each sampled sequence whose depth stream
+    equals the oracle's has logits within 3e-2 and the oracle's cache index,
+    and at least one sampled sequence is compared."""
     B, T = prompts.shape
     # router decisions of every token against the oracle router
     pos = np.broadcast_to(np.arange(T), (B, T))
@@ -273,19 +308,23 @@ def _check_bf16(m, w, prompts, g, o, sample, tag, route_rule="argmax", fixed_dep
         nflips.append(f2)
     assert bad == 0 and nbad == 0
     _check_index_matches_depths(g, m.max_loops)
-    err = _max_err(g.prefill_logits, o.prefill_logits)
-    for s in range(len(g.step_logits)):
-        err = max(err, _max_err(g.step_logits[s], o.step_logits[s]))
+    for s in range(len(g.step_next)):
+        assert np.array_equal(g.step_next[s][sample], np.argmax(g.step_logits[s], axis=-1)), s
+    gd, odep = _all_depths(g), _oracle_depths(o)
+    same = [j for j, b in enumerate(sample) if np.array_equal(gd[b], odep[j])]
+    assert len(same) >= 1, "no sampled sequence with the oracle's depth stream"
+    err = 0.0
+    for j in same:
+        err = max(err, _max_err(g.prefill_logits[j], o.prefill_logits[j]))
+        for s in range(len(g.step_logits)):
+            err = max(err, _max_err(g.step_logits[s][j], o.step_logits[s][j]))
+        for i in range(m.max_loops):
+            assert np.array_equal(g.stats["index"][sample[j]][i], o.index[j][i]), (sample[j], i)
     agree = np.mean([np.mean(g.step_next[s][sample] == np.argmax(o.step_logits[s], -1))
                      for s in range(len(g.step_next))]) if g.step_next else 1.0
-    _report(tag, max_abs_logit_err=f"{err:.3g}", prefill_flip_rate=flips,
-            decode_flip_rate=float(np.mean(nflips)) if nflips else 0.0, greedy_agreement=f"{agree:.3f}",
-            depth_hist=g.stats["depth_hist"])
-    for j, b in enumerate(sample):
-        for i in range(m.max_loops):
-            if np.array_equal(_all_depths(g)[b], np.concatenate([o.prefill_depths[j],
-                                                                  [d[j] for d in o.step_depths]])):
-                assert np.array_equal(g.stats["index"][b][i], o.index[j][i])
+    _report(tag, max_abs_logit_err=f"{err:.3g}", compared_sequences=f"{len(same)}/{len(sample)}",
+            prefill_flip_rate=flips, decode_flip_rate=float(np.mean(nflips)) if nflips else 0.0,
+            greedy_agreement=f"{agree:.3f}", depth_hist=g.stats["depth_hist"])
     assert err <= BF16_TOL
     assert np.all(np.isfinite(g.prefill_logits))
 
@@ -340,6 +379,24 @@ def test_bf16_d768_b256x2048_sampled_sequences():
     g = parity.run_gpu(m, w, prompts, steps, max_pos=m.max_pos, keep_logits_rows=sample)
     o = parity.run_oracle(m, w, prompts[sample], [t[sample] for t in g.step_tokens])
     _check_bf16(m, w, prompts, g, o, sample, "bf16_d768_b256x2048")
+
+
+@pytest.mark.slow
+@pytest.mark.timeout(900)
+def test_bf16_d1024_prefill_b8x4096_sampled_sequences():
+    """The prefill workload's own shape (d 1024, 16 x 64 heads, SwiGLU 2816,
+    R 8, J 2) at batch 8 x 4096 in one 32768-row group, as the benchmark runs
+    it (Section 3.3 batched prefill, Eq. 6-7, 10-11): every token's depth, every
+    cache index, the last-position logits of two sequences against the oracle,
+    then three decode steps."""
+    m = synth.CONFIGS["bf16_d1024_prefill_b8x4096"].replace(steps=3)
+    w = synth.make_weights(m)
+    prompts = synth.make_prompts(m)
+    sample = [0, 7]
+    g = parity.run_gpu(m, w, prompts, m.steps, max_pos=m.max_pos, keep_logits_rows=sample,
+                       max_prefill_tokens=m.batch * m.prompt_len)
+    o = parity.run_oracle(m, w, prompts[sample], [t[sample] for t in g.step_tokens], threads=2)
+    _check_bf16(m, w, prompts, g, o, sample, "bf16_d1024_prefill_b8x4096")
 
 
 def test_bf16_d2048_heads_of_128_small_batch():
