@@ -403,6 +403,15 @@ def train_gather_scatter(torch, synth, B=8, T=4096, d=1024, R=8, reps=20):
                                          train._ptr(plans[i - 1].slot), train._ptr(plans[i - 1].offsets),
                                          train._ptr(plans[i - 1].count_dev), train._stream())
 
+    plan_ws = train.plan_workspace(B, T)
+
+    def plan_all_chunked():
+        for i in range(1, R + 1):
+            train.tlf.load().tlf_gs_plan_ws(train._ptr(depth), B, T, i, train._ptr(plans[i - 1].index),
+                                            train._ptr(plans[i - 1].slot), train._ptr(plans[i - 1].offsets),
+                                            train._ptr(plans[i - 1].count_dev), train._ptr(plan_ws),
+                                            plan_ws.numel(), train._stream())
+
     def timed(fn):
         s = torch.cuda.Stream()
         s.wait_stream(torch.cuda.current_stream())
@@ -423,6 +432,7 @@ def train_gather_scatter(torch, synth, B=8, T=4096, d=1024, R=8, reps=20):
         return e0.elapsed_time(e1) / reps
 
     fwd_ms, bwd_ms, plan_ms = timed(forward), timed(backward), timed(plan_all)
+    plan_chunked_ms = timed(plan_all_chunked)
     Hin.copy_(H[0])
     fwi_ms = timed(forward_in_place)
     n = [p.count for p in plans]
@@ -437,6 +447,7 @@ def train_gather_scatter(torch, synth, B=8, T=4096, d=1024, R=8, reps=20):
             "forward_in_place_ms": fwi_ms, "forward_in_place_gbs": fwi_bytes / fwi_ms / 1e6,
             "backward_ms": bwd_ms, "backward_gbs": bwd_bytes / bwd_ms / 1e6,
             "plan_us_per_loop": plan_ms * 1e3 / R, "plan_gbs": plan_bytes / plan_ms / 1e6,
+            "plan_chunked_us_per_loop": plan_chunked_ms * 1e3 / R,
             "frac": (fwd_bytes + bwd_bytes) / (fwd_ms + bwd_ms) / 1e6 / HBM_PEAK_GBS,
             "frac_in_place": (fwi_bytes + bwd_bytes) / (fwi_ms + bwd_ms) / 1e6 / HBM_PEAK_GBS,
             "what": "per pass over all loops; algorithmic bytes: each gathered row read and written once, "
@@ -679,7 +690,8 @@ def main():
         out["train_gather_scatter"] = train_gather_scatter(torch, synth)
         t = out["train_gather_scatter"]
         log(f"train gather-scatter: fwd {t['forward_ms']:.3f} ms {t['forward_gbs']:.0f} GB/s, "
-            f"in place {t['forward_in_place_ms']:.3f} ms, bwd {t['backward_ms']:.3f} ms {t['backward_gbs']:.0f} GB/s, plan {t['plan_us_per_loop']:.1f} us/loop")
+            f"in place {t['forward_in_place_ms']:.3f} ms, bwd {t['backward_ms']:.3f} ms {t['backward_gbs']:.0f} GB/s, "
+            f"plan {t['plan_us_per_loop']:.1f} us/loop (chunked {t['plan_chunked_us_per_loop']:.1f})")
     if not args.no_sweep:
         out["router_threshold_sweep"] = threshold_sweep(torch, tlf, synth, args.config)
     if not args.no_cpu:

@@ -311,6 +311,26 @@ const char* tlf_status_str(int status);
 int tlf_gs_plan(const int32_t* d_depth, int32_t batch, int32_t seq_len, int32_t loop, int32_t* d_index,
                 int32_t* d_slot, int32_t* d_offsets, int32_t* d_count, void* d_stream);
 
+/* The same plan (same outputs) from many workgroups: one launch counts the
+ * active rows of each chunk of TLF_GS_PLAN_CHUNK_ROWS rows into the
+ * workspace, a second places every chunk's rows after the counts before it
+ * (Section 3.2 and Eq. 6).
+ *   d_workspace  device scratch of at least tlf_gs_plan_ws_bytes(batch *
+ *                seq_len) bytes, 4-byte aligned, borrowed for the call (it may
+ *                be reused once the stream has passed this call); NULL when
+ *                that size is 0.  Its contents need no initialisation.
+ *   ws_bytes     its size.
+ * Other arguments as tlf_gs_plan.  TLF_E_INVALID_ARG for a missing or short
+ * workspace or batch * seq_len > TLF_GS_PLAN_MAX_ROWS. */
+#define TLF_GS_PLAN_CHUNK_ROWS 2048
+#define TLF_GS_PLAN_MAX_ROWS 8388608 /* 4096 chunks */
+static inline size_t tlf_gs_plan_ws_bytes(int64_t rows) {
+  return rows <= 0 ? 0 : (size_t)((rows + TLF_GS_PLAN_CHUNK_ROWS - 1) / TLF_GS_PLAN_CHUNK_ROWS) * 4u;
+}
+int tlf_gs_plan_ws(const int32_t* d_depth, int32_t batch, int32_t seq_len, int32_t loop, int32_t* d_index,
+                   int32_t* d_slot, int32_t* d_offsets, int32_t* d_count, void* d_workspace, size_t ws_bytes,
+                   void* d_stream);
+
 /* Gather (Eq. 6): d_out[r] = d_h[d_index[r]] for r < min(*d_count, max_rows).
  * d_out holds max_rows x d floats; rows past the count are not written.  The
  * count stays on the device (no host synchronisation); max_rows bounds the

@@ -4,11 +4,13 @@
 //
 // The operations are pure data movement plus one add per element, so every
 // kernel is bound by HBM bandwidth: rows move as 16-byte vectors, each thread
-// keeps four of them in flight, and only the active-set planner (integer work
-// over one depth per row) runs as a single workgroup.
+// keeps four of them in flight.  The active-set planner (integer work over one
+// depth per row) runs as a single workgroup, or, with scratch for one count
+// per chunk of rows, as one workgroup per chunk in two launches.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "kernels.h"
 #include "tlf.h"
 
 namespace {
@@ -95,6 +97,116 @@ __global__ __launch_bounds__(kPlanThreads) void k_gs_plan(PlanArgs a) {
   if (tid == 0) {
     a.count[0] = total;
     if (a.offsets) a.offsets[a.batch] = total;
+  }
+}
+
+// Multi-workgroup form of the same plan, in two launches that communicate
+// through a caller-provided array of per-chunk counts (no workgroup waits
+// for another).  Chunk c holds rows [c * kChunkRows, (c + 1) * kChunkRows);
+// thread tid of its workgroup takes rows base + k * kChunkThreads + tid.
+constexpr int kChunkThreads = 256;
+constexpr int kChunkWaves = kChunkThreads / 64;
+constexpr int kChunkPer = 8;  // rows per thread
+constexpr int kChunkRows = kChunkThreads * kChunkPer;
+static_assert(kChunkRows == TLF_GS_PLAN_CHUNK_ROWS, "chunk size in tlf.h");
+
+// Pass 1: counts[c] = active rows of chunk c.
+__global__ __launch_bounds__(kChunkThreads) void k_gs_count(const int32_t* __restrict__ depth, int32_t rows,
+                                                            int32_t loop, int32_t* __restrict__ counts) {
+  __shared__ int s_w[kChunkWaves];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int base = blockIdx.x * kChunkRows;
+  int m[kChunkPer];
+#pragma unroll
+  for (int k = 0; k < kChunkPer; ++k) {
+    const int r = base + k * kChunkThreads + tid;
+    m[k] = depth[r < rows ? r : rows - 1];
+  }
+  int n = 0;
+#pragma unroll
+  for (int k = 0; k < kChunkPer; ++k) {
+    const int r = base + k * kChunkThreads + tid;
+    n += __popcll(__ballot(r < rows && m[k] >= loop));
+  }
+  if (lane == 0) s_w[wave] = n;
+  __syncthreads();
+  if (tid == 0) {
+    int t = 0;
+#pragma unroll
+    for (int w = 0; w < kChunkWaves; ++w) t += s_w[w];
+    counts[blockIdx.x] = t;
+  }
+}
+
+// Pass 2: each chunk starts at the sum of the counts before it and places
+// its rows as the single-workgroup planner does; the last chunk writes the
+// total.  With no rows, one workgroup writes the empty plan.
+__global__ __launch_bounds__(kChunkThreads) void k_gs_place(PlanArgs a, const int32_t* __restrict__ counts,
+                                                            int32_t nchunks) {
+  __shared__ int s_cnt[kChunkPer * kChunkWaves];
+  __shared__ int s_pre[kChunkWaves];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  if (nchunks == 0) {
+    for (int b = tid; b <= a.batch; b += kChunkThreads)
+      if (a.offsets) a.offsets[b] = 0;
+    if (tid == 0) a.count[0] = 0;
+    return;
+  }
+  const int c = blockIdx.x, base = c * kChunkRows;
+  const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  int m[kChunkPer];
+#pragma unroll
+  for (int k = 0; k < kChunkPer; ++k) {
+    const int r = base + k * kChunkThreads + tid;
+    m[k] = a.depth[r < a.rows ? r : a.rows - 1];
+  }
+  // rows placed by the chunks before this one
+  int pre = 0;
+  for (int q = tid; q < c; q += kChunkThreads) pre += counts[q];
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) pre += __shfl_xor(pre, o);
+  if (lane == 0) s_pre[wave] = pre;
+  uint64_t bal[kChunkPer];
+#pragma unroll
+  for (int k = 0; k < kChunkPer; ++k) {
+    const int r = base + k * kChunkThreads + tid;
+    bal[k] = __ballot(r < a.rows && m[k] >= a.loop);
+    if (lane == 0) s_cnt[k * kChunkWaves + wave] = __popcll(bal[k]);
+  }
+  __syncthreads();
+  // exclusive scan of the kChunkPer x kChunkWaves group counts (32 values) by wave 0
+  if (wave == 0) {
+    constexpr int G = kChunkPer * kChunkWaves;
+    const int v = lane < G ? s_cnt[lane] : 0;
+    int incl = v;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int t = __shfl_up(incl, o);
+      if (lane >= o) incl += t;
+    }
+    if (lane < G) s_cnt[lane] = incl - v;
+    if (lane == G - 1 && c == nchunks - 1) {
+      int total = incl;
+#pragma unroll
+      for (int w = 0; w < kChunkWaves; ++w) total += s_pre[w];
+      a.count[0] = total;
+      if (a.offsets) a.offsets[a.batch] = total;
+    }
+  }
+  __syncthreads();
+  int start = 0;
+#pragma unroll
+  for (int w = 0; w < kChunkWaves; ++w) start += s_pre[w];
+#pragma unroll
+  for (int k = 0; k < kChunkPer; ++k) {
+    const int r = base + k * kChunkThreads + tid;
+    if (r < a.rows) {
+      const bool act = m[k] >= a.loop;
+      const int pos = start + s_cnt[k * kChunkWaves + wave] + __popcll(bal[k] & below);
+      if (act) a.index[pos] = r;
+      if (a.slot) a.slot[r] = act ? pos : -1;
+      if (a.offsets && r % a.seq_len == 0) a.offsets[r / a.seq_len] = pos;
+    }
   }
 }
 
@@ -192,6 +304,33 @@ int copy_blocks(int64_t elems4) {
 
 }  // namespace
 
+namespace tlf {
+
+int gs_plan_chunked_args(const int32_t* d_depth, int32_t batch, int32_t seq_len, int32_t* d_index,
+                         const int32_t* d_count, int64_t max_rows, int64_t* rows_out) {
+  if (batch < 0 || seq_len < 0 || !d_count) return TLF_E_INVALID_ARG;
+  const int64_t rows = (int64_t)batch * seq_len;
+  if (rows > max_rows) return TLF_E_INVALID_ARG;
+  if (rows > 0 && (!d_depth || !d_index)) return TLF_E_INVALID_ARG;
+  *rows_out = rows;
+  return TLF_OK;
+}
+
+int launch_gs_plan_chunked(const int32_t* d_depth, int32_t batch, int32_t seq_len, int32_t loop, int32_t* d_index,
+                           int32_t* d_slot, int32_t* d_offsets, int32_t* d_count, int32_t* counts, int64_t rows,
+                           hipStream_t stream) {
+  const int nchunks = (int)((rows + kChunkRows - 1) / kChunkRows);
+  PlanArgs a{d_depth, (int32_t)rows, seq_len, batch, loop, d_index, d_slot, d_offsets, d_count};
+  if (nchunks > 0)
+    hipLaunchKernelGGL(k_gs_count, dim3(nchunks), dim3(kChunkThreads), 0, stream, d_depth, (int32_t)rows, loop,
+                       counts);
+  hipLaunchKernelGGL(k_gs_place, dim3(nchunks > 0 ? nchunks : 1), dim3(kChunkThreads), 0, stream, a,
+                     (const int32_t*)counts, nchunks);
+  return launch_status();
+}
+
+}  // namespace tlf
+
 extern "C" {
 
 int tlf_gs_plan(const int32_t* d_depth, int32_t batch, int32_t seq_len, int32_t loop, int32_t* d_index,
@@ -203,6 +342,19 @@ int tlf_gs_plan(const int32_t* d_depth, int32_t batch, int32_t seq_len, int32_t 
   PlanArgs a{d_depth, (int32_t)rows, seq_len, batch, loop, d_index, d_slot, d_offsets, d_count};
   hipLaunchKernelGGL(k_gs_plan, dim3(1), dim3(kPlanThreads), 0, (hipStream_t)stream, a);
   return launch_status();
+}
+
+int tlf_gs_plan_ws(const int32_t* d_depth, int32_t batch, int32_t seq_len, int32_t loop, int32_t* d_index,
+                   int32_t* d_slot, int32_t* d_offsets, int32_t* d_count, void* d_workspace, size_t ws_bytes,
+                   void* stream) {
+  int64_t rows = 0;
+  const int st = tlf::gs_plan_chunked_args(d_depth, batch, seq_len, d_index, d_count, TLF_GS_PLAN_MAX_ROWS, &rows);
+  if (st != TLF_OK) return st;
+  const size_t need = tlf_gs_plan_ws_bytes(rows);
+  if (need > 0 && (!d_workspace || ws_bytes < need || ((uintptr_t)d_workspace & 3u) != 0))
+    return TLF_E_INVALID_ARG;
+  return tlf::launch_gs_plan_chunked(d_depth, batch, seq_len, loop, d_index, d_slot, d_offsets, d_count,
+                                     (int32_t*)d_workspace, rows, (hipStream_t)stream);
 }
 
 int tlf_gs_gather(const float* d_h, const int32_t* d_index, const int32_t* d_count, int32_t max_rows,

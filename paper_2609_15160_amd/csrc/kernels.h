@@ -280,4 +280,14 @@ template <typename T>
 hipError_t launch_cond_table(const CondWeights& w, int J, int R, int d, float* table, float* scratch,
                              hipStream_t s);
 
+// Multi-workgroup active-set planner of the training gather-scatter (gs.hip):
+// argument checks (host only, no device work; rows <= max_rows) and the two
+// launches, with `counts` holding one int32 per chunk of TLF_GS_PLAN_CHUNK_ROWS
+// rows.  Both return a TLF_* status.
+int gs_plan_chunked_args(const int32_t* d_depth, int32_t batch, int32_t seq_len, int32_t* d_index,
+                         const int32_t* d_count, int64_t max_rows, int64_t* rows_out);
+int launch_gs_plan_chunked(const int32_t* d_depth, int32_t batch, int32_t seq_len, int32_t loop, int32_t* d_index,
+                           int32_t* d_slot, int32_t* d_offsets, int32_t* d_count, int32_t* counts, int64_t rows,
+                           hipStream_t stream);
+
 }  // namespace tlf

@@ -90,7 +90,15 @@ class CacheStats(ctypes.Structure):
 
 
 EXPORTS = ("tlf_init", "tlf_prefill", "tlf_decode_step", "tlf_cache_stats", "tlf_set_profiling", "tlf_destroy",
-           "tlf_status_str", "tlf_gs_plan", "tlf_gs_gather", "tlf_gs_scatter", "tlf_ste")
+           "tlf_status_str", "tlf_gs_plan", "tlf_gs_plan_ws", "tlf_gs_gather", "tlf_gs_scatter", "tlf_ste")
+
+GS_PLAN_CHUNK_ROWS = 2048
+GS_PLAN_MAX_ROWS = 8388608
+
+
+def gs_plan_ws_bytes(rows: int) -> int:
+    """Workspace bytes of tlf_gs_plan_ws for `rows` rows (tlf_gs_plan_ws_bytes in tlf.h)."""
+    return 0 if rows <= 0 else 4 * ((rows + GS_PLAN_CHUNK_ROWS - 1) // GS_PLAN_CHUNK_ROWS)
 
 
 def header_exports(path: str = HEADER):
@@ -134,6 +142,8 @@ def load(path: str = LIB_PATH):
     lib.tlf_status_str.restype = ctypes.c_char_p
     lib.tlf_gs_plan.argtypes = [vp, i32, i32, i32, vp, vp, vp, vp, vp]
     lib.tlf_gs_plan.restype = ctypes.c_int
+    lib.tlf_gs_plan_ws.argtypes = [vp, i32, i32, i32, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
+    lib.tlf_gs_plan_ws.restype = ctypes.c_int
     lib.tlf_gs_gather.argtypes = [vp, vp, vp, i32, i32, vp, vp]
     lib.tlf_gs_gather.restype = ctypes.c_int
     lib.tlf_gs_scatter.argtypes = [vp, vp, vp, i32, i32, vp, vp]

@@ -51,9 +51,16 @@ class LoopPlan:
     count: int
 
 
-def plan(depth: torch.Tensor, batch: int, seq_len: int, loop: int) -> LoopPlan:
+def plan_workspace(batch: int, seq_len: int, device="cuda") -> torch.Tensor:
+    """Scratch for the multi-workgroup planner (one int32 count per chunk of rows)."""
+    return torch.empty(max(tlf.gs_plan_ws_bytes(batch * seq_len), 4), dtype=torch.uint8, device=device)
+
+
+def plan(depth: torch.Tensor, batch: int, seq_len: int, loop: int, workspace: torch.Tensor = None) -> LoopPlan:
     """Active rows of loop `loop`; reads the count back to the host (one
-    synchronisation), since the compact tensor's size must be known there."""
+    synchronisation), since the compact tensor's size must be known there.
+    With a `workspace` (plan_workspace) the multi-workgroup planner runs,
+    otherwise the single-workgroup one; both give the same plan."""
     if depth.dtype != torch.int32 or not depth.is_cuda or not depth.is_contiguous():
         raise ValueError("depth: expected a contiguous int32 CUDA tensor")
     rows = batch * seq_len
@@ -64,8 +71,15 @@ def plan(depth: torch.Tensor, batch: int, seq_len: int, loop: int) -> LoopPlan:
     slot = torch.empty(max(rows, 1), dtype=torch.int32, device=dev)
     offsets = torch.empty(batch + 1, dtype=torch.int32, device=dev)
     count = torch.empty(1, dtype=torch.int32, device=dev)
-    _check(tlf.load().tlf_gs_plan(_ptr(depth), batch, seq_len, loop, _ptr(index), _ptr(slot), _ptr(offsets),
-                                  _ptr(count), _stream()), "tlf_gs_plan")
+    if workspace is None:
+        _check(tlf.load().tlf_gs_plan(_ptr(depth), batch, seq_len, loop, _ptr(index), _ptr(slot), _ptr(offsets),
+                                      _ptr(count), _stream()), "tlf_gs_plan")
+    else:
+        if workspace.dtype != torch.uint8 or not workspace.is_cuda or not workspace.is_contiguous():
+            raise ValueError("workspace: expected a contiguous uint8 CUDA tensor (plan_workspace)")
+        _check(tlf.load().tlf_gs_plan_ws(_ptr(depth), batch, seq_len, loop, _ptr(index), _ptr(slot),
+                                         _ptr(offsets), _ptr(count), _ptr(workspace), workspace.numel(),
+                                         _stream()), "tlf_gs_plan_ws")
     n = int(count.item())
     return LoopPlan(loop, rows, index[:n], slot[:rows], offsets, count, n)
 

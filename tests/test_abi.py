@@ -194,7 +194,8 @@ def test_binding_constants_match_the_header():
              "ROUTE_FIXED": tlf.ROUTE["fixed"], "PREFILL_ALL_LOGITS": tlf.PREFILL_ALL_LOGITS,
              "PREFILL_APPEND": tlf.PREFILL_APPEND,
              "PROFILE_OFF": tlf.PROFILE_OFF, "PROFILE_ATTN": tlf.PROFILE_ATTN,
-             "PROFILE_BLOCK": tlf.PROFILE_BLOCK}
+             "PROFILE_BLOCK": tlf.PROFILE_BLOCK, "GS_PLAN_CHUNK_ROWS": tlf.GS_PLAN_CHUNK_ROWS,
+             "GS_PLAN_MAX_ROWS": tlf.GS_PLAN_MAX_ROWS}
     for name, value in pairs.items():
         assert defs[name] == value, name
 
@@ -214,6 +215,16 @@ def test_gather_scatter_argument_errors_need_no_device():
     assert lib.tlf_gs_plan(dummy, -1, 4, 1, dummy, None, None, dummy, None) == bad
     assert lib.tlf_gs_plan(dummy, 2, 4, 1, dummy, None, None, None, None) == bad
     assert lib.tlf_gs_plan(None, 2, 4, 1, dummy, None, None, dummy, None) == bad
+    # the multi-workgroup planner: workspace size, presence and alignment, row cap
+    need = tlf.gs_plan_ws_bytes(5000)
+    assert need == 12
+    assert lib.tlf_gs_plan_ws(dummy, 1, 5000, 1, dummy, None, None, dummy, None, 0, None) == bad
+    assert lib.tlf_gs_plan_ws(dummy, 1, 5000, 1, dummy, None, None, dummy, dummy, need - 4, None) == bad
+    assert lib.tlf_gs_plan_ws(dummy, 1, 5000, 1, dummy, None, None, dummy, ctypes.c_void_p(18), need, None) == bad
+    assert lib.tlf_gs_plan_ws(dummy, 1, tlf.GS_PLAN_MAX_ROWS + 1, 1, dummy, None, None, dummy, dummy,
+                              1 << 30, None) == bad
+    assert lib.tlf_gs_plan_ws(dummy, 2, 4, 1, dummy, None, None, None, dummy, need, None) == bad
+    assert lib.tlf_gs_plan_ws(dummy, -1, 4, 1, dummy, None, None, dummy, dummy, need, None) == bad
     assert lib.tlf_gs_gather(dummy, dummy, dummy, 8, 6, dummy, None) == bad     # d % 4
     assert lib.tlf_gs_gather(dummy, dummy, dummy, -1, 8, dummy, None) == bad
     assert lib.tlf_gs_gather(ctypes.c_void_p(20), dummy, dummy, 8, 8, dummy, None) == bad  # alignment

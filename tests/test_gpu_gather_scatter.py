@@ -33,8 +33,8 @@ def _report(tag, **kv):
     print(f"[gs] {tag} " + " ".join(f"{k}={v}" for k, v in kv.items()), flush=True)
 
 
-def _check_plan(train, m, batch, seq_len, loop):
-    p = train.plan(_dev(m), batch, seq_len, loop)
+def _check_plan(train, m, batch, seq_len, loop, ws=None):
+    p = train.plan(_dev(m), batch, seq_len, loop, workspace=ws)
     want = O.active_rows(m, loop)
     assert p.count == want.shape[0]
     assert np.array_equal(p.index.cpu().numpy(), want)
@@ -44,29 +44,69 @@ def _check_plan(train, m, batch, seq_len, loop):
     return p
 
 
-@pytest.mark.parametrize("batch,seq_len", [(1, 1), (3, 17), (5, 7001), (2, 16384), (1, 16385)])
-def test_plan_bit_exact(batch, seq_len):
+@pytest.mark.parametrize("planner", ["single", "chunked"])
+@pytest.mark.parametrize("batch,seq_len", [(1, 1), (3, 17), (1, 2048), (1, 2049), (5, 7001), (2, 16384),
+                                           (1, 16385)])
+def test_plan_bit_exact(batch, seq_len, planner):
     """Several passes of the single-workgroup planner, ragged last pass,
-    sequence starts anywhere inside a pass."""
+    sequence starts anywhere inside a pass; the multi-workgroup planner on
+    one chunk, one chunk plus one row, and many chunks with a ragged last."""
     train = _train()
     R = 8
     m = synth.make_train_depths(batch * seq_len, R, seed=batch * 1000 + seq_len)
-    _report("plan", batch=batch, seq_len=seq_len)
+    ws = train.plan_workspace(batch, seq_len) if planner == "chunked" else None
+    _report("plan", planner=planner, batch=batch, seq_len=seq_len)
     for i in range(0, R + 2):
-        _check_plan(train, m, batch, seq_len, i)
+        _check_plan(train, m, batch, seq_len, i, ws)
 
 
-def test_plan_empty_and_degenerate():
+@pytest.mark.parametrize("planner", ["single", "chunked"])
+def test_plan_empty_and_degenerate(planner):
     train = _train()
     for batch, seq_len in [(0, 5), (3, 0), (0, 0)]:
-        _report("plan-empty", batch=batch, seq_len=seq_len)
+        _report("plan-empty", planner=planner, batch=batch, seq_len=seq_len)
+        ws = train.plan_workspace(batch, seq_len) if planner == "chunked" else None
         m = np.zeros(batch * seq_len, np.int32)
-        p = train.plan(_dev(m) if m.size else torch.zeros(0, dtype=torch.int32, device="cuda"), batch, seq_len, 1)
+        p = train.plan(_dev(m) if m.size else torch.zeros(0, dtype=torch.int32, device="cuda"), batch, seq_len, 1,
+                       workspace=ws)
         assert p.count == 0
         assert p.offsets.cpu().numpy().tolist() == [0] * (batch + 1)
+    ws = train.plan_workspace(4, 10) if planner == "chunked" else None
     m = np.ones(40, np.int32)
-    assert _check_plan(train, m, 4, 10, 2).count == 0     # nobody reaches loop 2
-    assert _check_plan(train, m, 4, 10, 1).count == 40    # everybody in loop 1
+    assert _check_plan(train, m, 4, 10, 2, ws).count == 0     # nobody reaches loop 2
+    assert _check_plan(train, m, 4, 10, 1, ws).count == 40    # everybody in loop 1
+
+
+def test_chunked_plan_equals_single_workgroup_plan():
+    """The two planners give bitwise the same plan on the training workload's
+    shape (batch 8 x 4096, depths of the decode workload's mix), every loop,
+    with the workspace reused from call to call and a stale count left in it
+    by a larger call."""
+    train = _train()
+    B, T = 8, 4096
+    m = _dev(synth.make_train_depths(B * T, 8))
+    ws = train.plan_workspace(B, T)
+    ws.fill_(0x7F)                      # contents need no initialisation
+    for i in range(1, 10):
+        a = train.plan(m, B, T, i)
+        b = train.plan(m, B, T, i, workspace=ws)
+        assert a.count == b.count
+        for f in ("index", "slot", "offsets"):
+            assert torch.equal(getattr(a, f), getattr(b, f)), (i, f)
+    small = _dev(synth.make_train_depths(3 * 999, 8, seed=4))
+    for i in (1, 3):
+        a = train.plan(small, 3, 999, i)
+        b = train.plan(small, 3, 999, i, workspace=ws)
+        assert a.count == b.count and torch.equal(a.index, b.index) and torch.equal(a.offsets, b.offsets)
+
+
+def test_chunked_plan_rejects_short_workspace():
+    train = _train()
+    m = _dev(synth.make_train_depths(5000, 8))
+    ws = torch.empty(4, dtype=torch.uint8, device="cuda")   # needs 3 chunk counts
+    with pytest.raises(train.tlf.TlfError) as e:
+        train.plan(m, 1, 5000, 1, workspace=ws)
+    assert e.value.status == train.tlf.E_INVALID_ARG
 
 
 def _fp32_sum_ok(got, h, y_rows):
