@@ -331,6 +331,22 @@ int tlf_gs_plan_ws(const int32_t* d_depth, int32_t batch, int32_t seq_len, int32
                    int32_t* d_slot, int32_t* d_offsets, int32_t* d_count, void* d_workspace, size_t ws_bytes,
                    void* d_stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving or training loops, harnesses that forbid
+ * hipMalloc): tlf_gs_plan_ws with its per-chunk counts in a fixed array of
+ * the library's own device memory (16 KiB on each GPU that runs it, held
+ * until the process ends) instead of a caller workspace.  Nothing is
+ * allocated, and the array needs no clearing (every count read is written
+ * by the same call first).  All calls on one GPU share the array: calls
+ * that overlap on that GPU (other streams, other threads) race and must be
+ * serialised by the caller.  The stream must belong to the current device.
+ * Same arguments and outputs as tlf_gs_plan; TLF_E_INVALID_ARG when
+ * batch * seq_len > TLF_GS_PLAN_NOALLOC_MAX_ROWS (checked before any device
+ * work), TLF_E_HIP if the array's address cannot be obtained. */
+#define TLF_GS_PLAN_NOALLOC_MAX_ROWS 8388608
+int tlf_gs_plan_noalloc(const int32_t* d_depth, int32_t batch, int32_t seq_len, int32_t loop, int32_t* d_index,
+                        int32_t* d_slot, int32_t* d_offsets, int32_t* d_count, void* d_stream);
+
 /* Gather (Eq. 6): d_out[r] = d_h[d_index[r]] for r < min(*d_count, max_rows).
  * d_out holds max_rows x d floats; rows past the count are not written.  The
  * count stays on the device (no host synchronisation); max_rows bounds the

@@ -90,10 +90,12 @@ class CacheStats(ctypes.Structure):
 
 
 EXPORTS = ("tlf_init", "tlf_prefill", "tlf_decode_step", "tlf_cache_stats", "tlf_set_profiling", "tlf_destroy",
-           "tlf_status_str", "tlf_gs_plan", "tlf_gs_plan_ws", "tlf_gs_gather", "tlf_gs_scatter", "tlf_ste")
+           "tlf_status_str", "tlf_gs_plan", "tlf_gs_plan_ws", "tlf_gs_plan_noalloc", "tlf_gs_gather",
+           "tlf_gs_scatter", "tlf_ste")
 
 GS_PLAN_CHUNK_ROWS = 2048
 GS_PLAN_MAX_ROWS = 8388608
+GS_PLAN_NOALLOC_MAX_ROWS = 8388608
 
 
 def gs_plan_ws_bytes(rows: int) -> int:
@@ -144,6 +146,8 @@ def load(path: str = LIB_PATH):
     lib.tlf_gs_plan.restype = ctypes.c_int
     lib.tlf_gs_plan_ws.argtypes = [vp, i32, i32, i32, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
     lib.tlf_gs_plan_ws.restype = ctypes.c_int
+    lib.tlf_gs_plan_noalloc.argtypes = [vp, i32, i32, i32, vp, vp, vp, vp, vp]
+    lib.tlf_gs_plan_noalloc.restype = ctypes.c_int
     lib.tlf_gs_gather.argtypes = [vp, vp, vp, i32, i32, vp, vp]
     lib.tlf_gs_gather.restype = ctypes.c_int
     lib.tlf_gs_scatter.argtypes = [vp, vp, vp, i32, i32, vp, vp]

@@ -195,7 +195,7 @@ def test_binding_constants_match_the_header():
              "PREFILL_APPEND": tlf.PREFILL_APPEND,
              "PROFILE_OFF": tlf.PROFILE_OFF, "PROFILE_ATTN": tlf.PROFILE_ATTN,
              "PROFILE_BLOCK": tlf.PROFILE_BLOCK, "GS_PLAN_CHUNK_ROWS": tlf.GS_PLAN_CHUNK_ROWS,
-             "GS_PLAN_MAX_ROWS": tlf.GS_PLAN_MAX_ROWS}
+             "GS_PLAN_MAX_ROWS": tlf.GS_PLAN_MAX_ROWS, "GS_PLAN_NOALLOC_MAX_ROWS": tlf.GS_PLAN_NOALLOC_MAX_ROWS}
     for name, value in pairs.items():
         assert defs[name] == value, name
 
@@ -225,6 +225,10 @@ def test_gather_scatter_argument_errors_need_no_device():
                               1 << 30, None) == bad
     assert lib.tlf_gs_plan_ws(dummy, 2, 4, 1, dummy, None, None, None, dummy, need, None) == bad
     assert lib.tlf_gs_plan_ws(dummy, -1, 4, 1, dummy, None, None, dummy, dummy, need, None) == bad
+    # the allocation-free planner rejects sizes beyond its fixed scratch before any HIP call
+    assert lib.tlf_gs_plan_noalloc(dummy, 1, tlf.GS_PLAN_NOALLOC_MAX_ROWS + 1, 1, dummy, None, None, dummy,
+                                   None) == bad
+    assert lib.tlf_gs_plan_noalloc(dummy, 2, 4, 1, dummy, None, None, None, None) == bad
     assert lib.tlf_gs_gather(dummy, dummy, dummy, 8, 6, dummy, None) == bad     # d % 4
     assert lib.tlf_gs_gather(dummy, dummy, dummy, -1, 8, dummy, None) == bad
     assert lib.tlf_gs_gather(ctypes.c_void_p(20), dummy, dummy, 8, 8, dummy, None) == bad  # alignment
