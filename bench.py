@@ -13,9 +13,11 @@ Prints one JSON line: decoded tokens/s, the decode attention's achieved HBM
 bandwidth against 8 TB/s (HIP events around every attention launch on the
 library's stream), the same kernels forced to fixed depth R, the same step
 with gather-scatter off, the step with AdaLN conditioning, the batch 32 x 512
-and batch 64 x 4096 (d=2048) decode workloads, time to first token over
-prompt lengths, a prefill measurement, the MLP-router threshold sweep, and
-the CPU oracle on a bounded sample.
+and batch 64 x 4096 (d=2048) decode workloads, the tiny fp32 model's
+per-step latency, time to first token over prompt lengths, a prefill
+measurement, the MLP-router threshold sweep, the per-step latency
+distribution, a streaming-read ceiling, and the CPU oracle on a bounded
+sample (all host threads) and on one thread for the small workloads.
 """
 import argparse
 import json
@@ -36,12 +38,14 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def decode_run(sess, torch, B, V, warmup, steps, profiled, first_tokens):
+def decode_run(sess, torch, B, V, warmup, steps, profiled, first_tokens, latency_steps=0):
     """Warmup, `steps` timed decode steps (HIP-graph replays), then two passes of
     `profiled` steps launched kernel by kernel: the first with HIP events around
     each step's loop-and-layer region only, the second with events around every
-    attention launch as well.  Greedy feedback throughout, no allocation inside
-    any region.  Returns (ms of the timed steps, block-pass stats, attention-pass stats)."""
+    attention launch as well; then `latency_steps` graph-replayed steps with an
+    event pair around each (the per-step latency distribution).  Greedy
+    feedback throughout, no allocation inside any region.  Returns (ms of the
+    timed steps, block-pass stats, attention-pass stats, per-step ms list)."""
     dev = sess.device
     tok = [first_tokens.to(torch.int32).contiguous(), torch.empty(B, dtype=torch.int32, device=dev)]
     logits = torch.empty((B, V), dtype=torch.float32, device=dev)
@@ -75,9 +79,21 @@ def decode_run(sess, torch, B, V, warmup, steps, profiled, first_tokens):
         if st["status"] != 0:
             raise RuntimeError(f"device error {st['status']}")
         stats.append(st)
+    lat = []
+    if latency_steps:
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(latency_steps + 1)]
+        torch.cuda.synchronize()
+        ev[0].record(stream)
+        for p in range(latency_steps):
+            sess.decode_into(tok[k % 2], logits, next_tok=tok[(k + 1) % 2])
+            k += 1
+            ev[p + 1].record(stream)
+        torch.cuda.synchronize()
+        lat = [ev[p].elapsed_time(ev[p + 1]) for p in range(latency_steps)]
+        log(f"latency pass: {latency_steps} steps, median {sorted(lat)[len(lat) // 2]:.3f} ms")
     if not bool(torch.isfinite(logits).all()):
         raise RuntimeError("non-finite logits")
-    return ms, stats[0], stats[1]
+    return ms, stats[0], stats[1], lat
 
 
 def hot_path_bytes(st, model, steps, B):
@@ -90,9 +106,9 @@ def hot_path_bytes(st, model, steps, B):
 
 
 def run_config(torch, tlf, model, w, prompts, warmup, steps, profiled, route_rule="argmax", fixed_depth=1,
-               graph=True):
+               graph=True, latency_steps=0):
     B, T = prompts.shape
-    max_pos = T + warmup + steps + 2 * profiled
+    max_pos = T + warmup + steps + 2 * profiled + latency_steps
     sess = tlf.Session(model, w, max_batch=B, max_pos=max_pos, route_rule=route_rule,
                        fixed_depth=fixed_depth, max_prefill_tokens=65536, decode_graph=graph)
     try:
@@ -104,55 +120,122 @@ def run_config(torch, tlf, model, w, prompts, warmup, steps, profiled, route_rul
         prefill_s = time.perf_counter() - t0
         first = torch.argmax(logits, dim=-1)
         del logits
-        ms, st_block, st_attn = decode_run(sess, torch, B, model.vocab, warmup, steps, profiled, first)
+        ms, st_block, st_attn, lat = decode_run(sess, torch, B, model.vocab, warmup, steps, profiled, first,
+                                                latency_steps)
         hist = sess.stats()["depth_hist"]
+        if latency_steps:
+            return ms, (st_block, st_attn), prefill_s, hist, lat
         return ms, (st_block, st_attn), prefill_s, hist
     finally:
         sess.close()
         torch.cuda.empty_cache()
 
 
-def stream_copy_gbs(torch, nbytes=1 << 30, reps=10):
-    """Device-to-device copy rate (bytes read + written per second) of a plain
-    torch copy of `nbytes`: a practical ceiling for streaming kernels."""
-    src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
-    dst = torch.empty_like(src)
-    dst.copy_(src)
+def stream_read_gbs(torch, tlf, nbytes=4 << 30, reps=10):
+    """Read rate of libtlf's streaming probe (the decode attention's 16-byte
+    non-temporal loads) over `nbytes` of device memory: bytes read per second,
+    the practical ceiling of a streaming kernel on this device."""
+    buf = torch.ones(nbytes // 2, dtype=torch.bfloat16, device="cuda")
+    sink = torch.zeros(1, dtype=torch.int32, device="cuda")
+    lib = tlf.load()
+    stream = torch.cuda.current_stream().cuda_stream
+
+    def once():
+        st = lib.tlf_probe_read(buf.data_ptr(), nbytes, sink.data_ptr(), stream)
+        if st != tlf.OK:
+            raise RuntimeError(f"tlf_probe_read: {st}")
+    once()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     e0.record()
     for _ in range(reps):
-        dst.copy_(src)
+        once()
     e1.record()
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1)
-    del src, dst
+    del buf, sink
     torch.cuda.empty_cache()
-    return 2 * nbytes * reps / (ms / 1e3) / 1e9
+    return nbytes * reps / (ms / 1e3) / 1e9
+
+
+def _oracle_threads():
+    try:
+        from threadpoolctl import threadpool_info
+        return max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:
+        return os.cpu_count() or 1
+
+
+def _oracle_decode(model, w, prompts, budget_s, max_steps):
+    """Oracle prefill of `prompts` (timed), then greedy decode steps until
+    `budget_s` is spent or `max_steps` are done (at least 2).  Returns
+    (prefill seconds, steps, decode seconds)."""
+    from oracle import tlf_oracle as O
+    M = O.Model(w, model.n_heads, model.head_dim, rms_eps=model.rms_eps)
+    t0 = time.perf_counter()
+    states, lg, _, _ = O.prefill_batch(M, prompts)
+    pre = time.perf_counter() - t0
+    tok = O.greedy(lg)
+    n = 0
+    t0 = time.perf_counter()
+    while n < 2 or (time.perf_counter() - t0 < budget_s and n < max_steps):
+        lg2, _, _ = O.decode(M, states, tok)
+        tok = O.greedy(lg2)
+        n += 1
+    return pre, n, time.perf_counter() - t0
 
 
 def cpu_baseline(model, w, prompts, budget_s, seqs=8):
     """The oracle (untuned) decoding `seqs` sequences of the same workload on the host."""
-    import numpy as np
-    from oracle import tlf_oracle as O
-    try:
-        from threadpoolctl import threadpool_info
-        cores = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
-    except Exception:
-        cores = os.cpu_count() or 1
-    M = O.Model(w, model.n_heads, model.head_dim, rms_eps=model.rms_eps)
-    states, lg, _, _ = O.prefill_batch(M, prompts[:seqs])
-    tok = O.greedy(lg)
-    n = 0
-    t0 = time.perf_counter()
-    while n < 2 or (time.perf_counter() - t0 < budget_s and n < model.steps):
-        lg2, _, _ = O.decode(M, states, tok)
-        tok = O.greedy(lg2)
-        n += 1
-    dt = time.perf_counter() - t0
+    cores = _oracle_threads()
+    pre, n, dt = _oracle_decode(model, w, prompts[:seqs], budget_s, model.steps)
     return {"value": seqs * n / dt, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
+            "prefill_s": pre,
             "sample": f"{seqs} of {prompts.shape[0]} sequences: oracle prefill of their {prompts.shape[1]}-token "
-                      f"prompts (untimed), then {n} batched greedy decode steps timed ({dt:.1f} s)"}
+                      f"prompts ({pre:.1f} s, timed separately), then {n} batched greedy decode steps timed "
+                      f"({dt:.1f} s)"}
+
+
+def cpu_one_core(synth, budget_s=6.0):
+    """The oracle on one host thread (BLAS limited to one thread) for the two
+    small decode workloads: the tiny fp32 model at its full batch, and the
+    batch 32 x 512 model on a sample of 2 sequences."""
+    try:
+        from threadpoolctl import threadpool_limits
+    except Exception:
+        return None
+    rows = []
+    with threadpool_limits(limits=1):
+        for name, seqs in (("f32_tiny_b1x32", None), ("bf16_d768_b32x512", 2)):
+            m = synth.CONFIGS[name]
+            w = synth.make_weights(m)
+            prompts = synth.make_prompts(m)
+            sample = prompts if seqs is None else prompts[:seqs]
+            pre, n, dt = _oracle_decode(m, w, sample, budget_s, m.steps)
+            rows.append({"workload": name, "sequences": int(sample.shape[0]), "prompt": int(sample.shape[1]),
+                         "prefill_s": pre, "steps": n, "tokens_per_s": sample.shape[0] * n / dt})
+    return {"cores": 1, "kind": "oracle", "rows": rows}
+
+
+def tiny_decode(torch, tlf, synth, warmup=4):
+    """The tiny fp32 model (batch 1, 32-token prompt, 32 greedy steps): per-step
+    latency of graph-replayed and of kernel-by-kernel decode steps."""
+    m = synth.CONFIGS["f32_tiny_b1x32"]
+    w = synth.make_weights(m)
+    prompts = synth.make_prompts(m)
+    out = {"workload": "f32_tiny_b1x32 decode: batch 1 x prompt 32, 1-layer d=64 looped block (4x16 heads, "
+                       "SwiGLU 256, vocab 512), R=4, float32", "steps": m.steps - warmup}
+    for graph in (True, False):
+        sess = tlf.Session(m, w, max_batch=1, max_pos=m.max_pos, decode_graph=graph)
+        try:
+            logits, _ = sess.prefill(torch.from_numpy(prompts).cuda(), want_depths=False)
+            first = torch.argmax(logits, dim=-1)
+            ms, _ = replay_decode_ms(sess, torch, 1, m.vocab, first, warmup, m.steps - warmup)
+        finally:
+            sess.close()
+        out["us_per_step_graph" if graph else "us_per_step_eager"] = ms * 1e3 / (m.steps - warmup)
+    out["tokens_per_s"] = 1e6 / out["us_per_step_graph"]
+    return out
 
 
 def replay_decode_ms(sess, torch, B, V, first_tokens, warmup, steps):
@@ -466,25 +549,44 @@ def source_digest(path=ATTN_SOURCE):
     return hashlib.sha256(open(path, "rb").read()).hexdigest()
 
 
-def measured_traffic():
+def measured_traffic(window, algo_bytes_per_launch):
     """Per-launch HBM bytes of the decode attention from committed rocprofv3
-    counter runs, if they were taken on the current kernel source; else None."""
+    counter runs.  They are reported only when they were taken on the current
+    kernel source and over the same step window (warmup, timed and profiled
+    step counts) with the same algorithmic bytes per launch as this run, since
+    the work per step drifts with the greedy trajectory.  Returns (bytes or
+    None, a record of the stored measurement and its traffic/algorithmic ratio)."""
     try:
         rec = json.load(open(TRAFFIC_FILE))
     except (OSError, ValueError):
-        return None
+        return None, None
+    info = {"file": os.path.relpath(TRAFFIC_FILE, ROOT), "window": rec.get("window"),
+            "algo_bytes_per_launch": rec.get("algo_bytes_per_launch"),
+            "traffic_bytes_per_launch": rec.get("traffic_bytes_per_launch")}
+    if rec.get("algo_bytes_per_launch"):
+        info["ratio"] = rec["traffic_bytes_per_launch"] / rec["algo_bytes_per_launch"]
     if rec.get("attn_source_sha256") != source_digest():
-        return None
-    return rec.get("traffic_bytes_per_launch")
+        info["status"] = "not reported: the kernel source changed since the counters were taken"
+        return None, info
+    same = rec.get("window") == window and rec.get("algo_bytes_per_launch") is not None and \
+        abs(rec["algo_bytes_per_launch"] - algo_bytes_per_launch) <= 1e-9 * algo_bytes_per_launch
+    if not same:
+        info["status"] = "not reported: taken over another step window"
+        return None, info
+    info["status"] = "same kernel source, step window and algorithmic bytes as this run"
+    return rec["traffic_bytes_per_launch"], info
 
 
-def counter_summary(fetch_csv, write_csv, last_dispatches):
-    """Summarize two rocprofv3 --pmc runs (FETCH_SIZE, then WRITE_SIZE).
+def counter_summary(fetch_csv, write_csv, first, count, bench_json, window):
+    """Summarize two rocprofv3 --pmc runs (FETCH_SIZE, then WRITE_SIZE) of
+    this benchmark.
 
     Each counter (KiB per dispatch) is scaled by what it reads for the
     calibration copy of CALIB_BYTES (the first copy kernel of the run), and
-    averaged over the last `last_dispatches` decode-attention dispatches,
-    which are the benchmark's event-timed region.
+    averaged over the decode-attention dispatches [first, first + count) of
+    the run, which are the routed run's attention-event pass.  The algorithmic
+    bytes per launch of that pass come from the run's own JSON line
+    (`bench_json`, the same command's output), together with the step window.
     """
     import csv
 
@@ -492,50 +594,85 @@ def counter_summary(fetch_csv, write_csv, last_dispatches):
         rows = [r for r in csv.DictReader(open(path)) if r["Counter_Name"] == counter]
         rows.sort(key=lambda r: int(r["Dispatch_Id"]))
         copy = next(r for r in rows if "copy" in r["Kernel_Name"])
-        attn = [r for r in rows if "k_attn_decode" in r["Kernel_Name"]][-last_dispatches:]
+        attn = [r for r in rows if "k_attn_decode" in r["Kernel_Name"]][first:first + count]
+        if len(attn) != count:
+            raise SystemExit(f"{path}: {len(attn)} attention dispatches in the window, expected {count}")
         factor = CALIB_BYTES / (float(copy["Counter_Value"]) * 1024.0)
         per = sum(float(r["Counter_Value"]) for r in attn) * 1024.0 * factor / len(attn)
         return factor, per, len(attn), float(copy["Counter_Value"])
 
     ff, fetch, n, fcopy = load(fetch_csv, "FETCH_SIZE")
     wf, write, n2, wcopy = load(write_csv, "WRITE_SIZE")
-    return {"attn_source_sha256": source_digest(), "dispatches": n,
+    run = json.loads(open(bench_json).read().strip().splitlines()[-1])
+    algo = run["roofline"]["algo_bytes_per_launch"]
+    return {"attn_source_sha256": source_digest(), "dispatches": n, "window": window,
+            "algo_bytes_per_launch": algo,
             "fetch_bytes_per_launch": fetch, "write_bytes_per_launch": write,
-            "traffic_bytes_per_launch": fetch + write,
+            "traffic_bytes_per_launch": fetch + write, "ratio": (fetch + write) / algo,
             "fetch_scale": ff, "write_scale": wf,
             "calibration": f"copy of {CALIB_BYTES} bytes read {fcopy:.1f} KiB FETCH_SIZE and "
                            f"{wcopy:.1f} KiB WRITE_SIZE"}
 
 
-def trace_summary(trace_csv, routed_launches, last_dispatches):
-    """Per-kernel durations from a rocprofv3 kernel trace of the default run,
-    plus the decode attention's average over the routed run's event-timed
-    region: its launches are the first `routed_launches` attention dispatches
-    of the trace, and the timed region is the last `last_dispatches` of those."""
+def trace_summary(trace_csv, routed_launches, last_dispatches, loops, layers, first_step, last_step):
+    """Per-kernel durations from a rocprofv3 kernel trace of this benchmark,
+    the decode attention's average over the routed run's event-timed region
+    (its launches are the first `routed_launches` attention dispatches of the
+    trace, and the timed region is the last `last_dispatches` of those), and
+    the average duration of every (loop, layer, kernel) of the routed run's
+    decode steps [first_step, last_step) (step k starts at the k-th decode
+    planner dispatch; each (loop, layer) runs QKV, attention, O, gate/up, down)."""
     import csv
     import collections
     rows = list(csv.DictReader(open(trace_csv)))
     rows.sort(key=lambda r: int(r["Start_Timestamp"]))
+    dur = lambda r: (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
     agg = collections.defaultdict(lambda: [0, 0.0])
     for r in rows:
-        d = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
         agg[r["Kernel_Name"]][0] += 1
-        agg[r["Kernel_Name"]][1] += d
+        agg[r["Kernel_Name"]][1] += dur(r)
     attn = [r for r in rows if "k_attn_decode" in r["Kernel_Name"]][:routed_launches][-last_dispatches:]
-    durs = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in attn]
+    durs = [dur(r) for r in attn]
     top = sorted(agg.items(), key=lambda kv: -kv[1][1])[:12]
+    plans = [k for k, r in enumerate(rows) if "k_plan_decode" in r["Kernel_Name"]]
+    names = ("qkv", "attn", "o", "gate_up", "down")
+    per = collections.defaultdict(list)
+    spans, gaps = [], []
+    for st in range(first_step, last_step):
+        a = plans[st]
+        b = plans[st + 1] if st + 1 < len(plans) else len(rows)
+        blk = [r for r in rows[a + 1:b] if "k_attn_decode" in r["Kernel_Name"] or "k_dgemm" in r["Kernel_Name"]]
+        blk = blk[:loops * layers * 5]
+        for q, r in enumerate(blk):
+            i, rem = divmod(q, layers * 5)
+            j, p = divmod(rem, 5)
+            per[(i, j, names[p])].append(dur(r))
+        step_rows = rows[a - 1:b - 1]  # the step's embedding + router kernel precedes its planner
+        spans.append((int(step_rows[-1]["End_Timestamp"]) - int(step_rows[0]["Start_Timestamp"])) / 1e3)
+        gaps.append(sum((int(y["Start_Timestamp"]) - int(x["End_Timestamp"])) / 1e3
+                        for x, y in zip(step_rows, step_rows[1:])))
+    table = [{"loop": i + 1, "layer": j + 1,
+              **{n: sum(per[(i, j, n)]) / len(per[(i, j, n)]) for n in names if per[(i, j, n)]}}
+             for i in range(loops) for j in range(layers)]
+    totals = {n: sum(t.get(n, 0.0) for t in table) for n in names}
     return {"kernels": [{"name": n, "calls": c, "total_ms": t / 1e3, "avg_us": t / c} for n, (c, t) in top],
-            "attn_routed_timed_region": {"dispatches": len(durs), "avg_us": sum(durs) / len(durs)}}
+            "attn_routed_timed_region": {"dispatches": len(durs), "avg_us": sum(durs) / max(len(durs), 1)},
+            "decode_steps": {"steps": [first_step, last_step],
+                             "span_us": sum(spans) / max(len(spans), 1),
+                             "gaps_us": sum(gaps) / max(len(gaps), 1),
+                             "per_step_us": totals, "per_loop_layer_us": table}}
 
 
 def main():
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--steps", type=int, default=80)
     ap.add_argument("--warmup", type=int, default=8)
     ap.add_argument("--profiled-steps", type=int, default=10,
                     help="steps per profiled pass after the timed region (two passes, launched eagerly: "
                          "events around the loop region, then also around each attention launch)")
+    ap.add_argument("--latency-steps", type=int, default=20,
+                    help="graph-replayed steps after the profiled passes, each timed on its own (p50/p99)")
     ap.add_argument("--config", default="bf16_d768_b256x2048")
     ap.add_argument("--no-fixed", action="store_true", help="skip the fixed-depth comparison")
     ap.add_argument("--no-graph", action="store_true",
@@ -556,8 +693,10 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--copy-calibration", action="store_true",
                     help=f"first run a device copy of {CALIB_BYTES} bytes (counter calibration)")
-    ap.add_argument("--counter-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
-                    help="summarize rocprofv3 FETCH_SIZE / WRITE_SIZE runs of this benchmark and exit")
+    ap.add_argument("--counter-summary", nargs=3, metavar=("FETCH_CSV", "WRITE_CSV", "BENCH_JSON"),
+                    help="summarize rocprofv3 FETCH_SIZE / WRITE_SIZE runs of this benchmark (run with the same "
+                         "--warmup/--steps/--profiled-steps; BENCH_JSON is that run's output) and exit")
+    ap.add_argument("--no-tiny", action="store_true", help="skip the tiny fp32 model's per-step latency")
     ap.add_argument("--trace-summary", metavar="TRACE_CSV",
                     help="summarize a rocprofv3 kernel trace of this benchmark's default run and exit")
     args = ap.parse_args()
@@ -566,13 +705,17 @@ def main():
         m = synth.CONFIGS[args.config]
         per_step = m.max_loops * m.n_layers
         routed = (args.warmup + args.steps + 2 * args.profiled_steps) * per_step
-        print(json.dumps(trace_summary(args.trace_summary, routed, args.profiled_steps * per_step)))
+        print(json.dumps(trace_summary(args.trace_summary, routed, args.profiled_steps * per_step,
+                                       m.max_loops, m.n_layers, args.warmup, args.warmup + args.steps)))
         return
     if args.counter_summary:
         import synth
         m = synth.CONFIGS[args.config]
-        last = args.profiled_steps * m.max_loops * m.n_layers  # attention launches per step: R x J
-        print(json.dumps(counter_summary(*args.counter_summary, last)))
+        per_step = m.max_loops * m.n_layers  # attention launches per step: R x J
+        first = (args.warmup + args.steps + args.profiled_steps) * per_step
+        window = {"warmup": args.warmup, "steps": args.steps, "profiled_steps": args.profiled_steps}
+        print(json.dumps(counter_summary(*args.counter_summary[:2], first, args.profiled_steps * per_step,
+                                         args.counter_summary[2], window)))
         return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -604,8 +747,9 @@ def main():
         print(json.dumps(train_gather_scatter(torch, synth)), flush=True)
         return
     base = synth.CONFIGS[args.config]
-    if args.warmup + args.steps + 2 * args.profiled_steps > base.steps or args.profiled_steps < 1:
-        print(f"warmup + steps + 2 x profiled-steps must be <= {base.steps} for {args.config} "
+    if (args.warmup + args.steps + 2 * args.profiled_steps + args.latency_steps > base.steps
+            or args.profiled_steps < 1 or args.latency_steps < 0):
+        print(f"warmup + steps + 2 x profiled-steps + latency-steps must be <= {base.steps} for {args.config} "
               f"(profiled-steps >= 1)", file=sys.stderr)
         sys.exit(2)
     model = base
@@ -615,8 +759,9 @@ def main():
     B, T = prompts.shape
     log(f"inputs ready in {time.perf_counter() - t0:.1f}s: batch {B} x prompt {T}")
 
-    ms, (stb, st), prefill_s, hist = run_config(torch, tlf, model, w, prompts, args.warmup, args.steps,
-                                                args.profiled_steps, graph=not args.no_graph)
+    ms, (stb, st), prefill_s, hist, lat = run_config(torch, tlf, model, w, prompts, args.warmup, args.steps,
+                                                     args.profiled_steps, graph=not args.no_graph,
+                                                     latency_steps=args.latency_steps)
     log(f"routed: {ms / args.steps:.3f} ms/step, prefill {prefill_s:.2f}s, depth hist {hist}")
     value = B * args.steps / (ms / 1e3)
     attn_gbs = st["attn_algo_bytes"] / (st["attn_ms"] / 1e3) / 1e9
@@ -625,6 +770,8 @@ def main():
     hot_gbs = hot_bytes / (stb["block_ms"] / 1e3) / 1e9
     tot_hist = np.asarray(hist, dtype=np.float64)
     mean_depth = float((tot_hist * np.arange(1, len(hist) + 1)).sum() / max(tot_hist.sum(), 1))
+    window = {"warmup": args.warmup, "steps": args.steps, "profiled_steps": args.profiled_steps}
+    traffic, traffic_info = measured_traffic(window, per_launch)
 
     out = {
         "metric": METRIC,
@@ -646,7 +793,8 @@ def main():
                    "batch": B, "prompt": T, "max_loops": model.max_loops, "layers": model.n_layers,
                    "mean_depth": mean_depth},
         "roofline": {"bound": "hbm", "kernel": "k_attn_decode", "achieved": attn_gbs, "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": attn_gbs / HBM_PEAK_GBS, "traffic": measured_traffic(),
+                     "unit": "GB/s", "frac": attn_gbs / HBM_PEAK_GBS, "traffic": traffic,
+                     "traffic_counters": traffic_info,
                      "launches": st["attn_launches"], "avg_launch_us": st["attn_ms"] * 1e3 / st["attn_launches"],
                      "algo_bytes_per_launch": per_launch,
                      "measured": f"HIP events around each attention launch over {args.profiled_steps} decode "
@@ -659,10 +807,21 @@ def main():
                      "algo_bytes_per_step": hot_bytes / args.profiled_steps},
         "prefill_s": prefill_s,
     }
-    copy_gbs = stream_copy_gbs(torch)
-    out["stream_copy"] = {"gbs": copy_gbs, "what": "torch device copy of 1 GiB, read + written bytes per second",
-                          "attn_frac_of_copy": attn_gbs / copy_gbs, "hot_path_frac_of_copy": hot_gbs / copy_gbs}
-    log(f"stream copy: {copy_gbs:.0f} GB/s")
+    if lat:
+        q = np.percentile(np.asarray(lat), [50, 99])
+        out["step_latency_ms"] = {"steps": len(lat), "p50": float(q[0]), "p99": float(q[1]), "max": float(max(lat)),
+                                  "mean": float(np.mean(lat)),
+                                  "what": "graph-replayed steps after the profiled passes, an event pair "
+                                          "around each step"}
+    read_gbs = stream_read_gbs(torch, tlf)
+    out["stream_read"] = {"gbs": read_gbs,
+                          "what": "tlf_probe_read over 4 GiB: the decode attention's 16-byte non-temporal "
+                                  "loads, bytes read per second",
+                          "attn_frac_of_read": attn_gbs / read_gbs, "hot_path_frac_of_read": hot_gbs / read_gbs}
+    log(f"stream read: {read_gbs:.0f} GB/s")
+    if not args.no_tiny:
+        out["tiny_f32"] = tiny_decode(torch, tlf, synth)
+        log(f"tiny f32: {out['tiny_f32']['us_per_step_graph']:.1f} us/step")
     if not args.no_fixed:
         fms, (_, fst), fpre, _ = run_config(torch, tlf, model, w, prompts, args.warmup, args.steps,
                                        args.profiled_steps, route_rule="fixed", fixed_depth=model.max_loops,
@@ -697,6 +856,8 @@ def main():
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline(model, w, prompts, args.cpu_seconds)
         log(f"cpu baseline: {out['cpu_baseline']['value']:.3f} tokens/s")
+        out["cpu_one_core"] = cpu_one_core(synth)
+        log("cpu one core: done")
     print(json.dumps(out), flush=True)
 
 

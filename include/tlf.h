@@ -51,7 +51,7 @@
 extern "C" {
 #endif
 
-#define TLF_ABI_VERSION 4
+#define TLF_ABI_VERSION 5
 #define TLF_MAX_LOOPS 16
 #define TLF_MAX_LAYERS 8
 #define TLF_MAX_BATCH 4096
@@ -59,12 +59,13 @@ extern "C" {
 
 /* Status codes. */
 #define TLF_OK 0
-#define TLF_E_INVALID_ARG (-1)    /* bad argument or unsupported shape */
+#define TLF_E_INVALID_ARG (-1)    /* bad argument: no valid model, call or buffer */
 #define TLF_E_NEED_WORKSPACE (-2) /* tlf_init size query: *ws_needed is set */
 #define TLF_E_OUT_OF_PAGES (-3)   /* the KV page pool (max_pages) is exhausted */
 #define TLF_E_STATE (-4)          /* call not valid in this state (e.g. decode before prefill) */
 #define TLF_E_HIP (-5)            /* a HIP runtime call failed; the context is poisoned */
 #define TLF_E_DEVICE (-6)         /* the device found a bad input (token id out of range) */
+#define TLF_E_UNSUPPORTED (-7)    /* a valid config outside this build's shapes and sizes (tlf_init) */
 
 /* Storage dtype of embeddings, block weights and the KV cache.  The residual
  * stream, the activations passed between kernels (normalised rows, q,
@@ -168,7 +169,7 @@ typedef struct tlf_cache_stats_t {
   int64_t slots_per_loop[TLF_MAX_LOOPS];  /* sum over sequences of cache entries of loop i */
   int64_t pages_per_loop[TLF_MAX_LOOPS];  /* pages held by loop i's caches */
   int64_t depth_hist[TLF_MAX_LOOPS];      /* routed depth counts of every token seen (index m-1) */
-  int64_t pages_used;
+  int64_t pages_used;                     /* pages in use (free pages: pages_total - pages_used) */
   int64_t pages_total;
   int64_t kv_bytes_resident;              /* pages_used * bytes per page */
   int64_t batch;                          /* sequences in the current batch */
@@ -206,7 +207,10 @@ typedef struct tlf_ctx tlf_ctx;
  *   hip_stream:   hipStream_t on which all work is enqueued (NULL = default).
  *   out:          receives the context.
  * Returns TLF_E_NEED_WORKSPACE (with *ws_needed set) when d_workspace is NULL
- * or ws_bytes is too small, TLF_E_INVALID_ARG on a bad config or weight set. */
+ * or ws_bytes is too small, TLF_E_INVALID_ARG on a bad config or weight set,
+ * TLF_E_UNSUPPORTED on a valid config outside the shapes and sizes listed in
+ * tlf_config (head_dim, the multiples of d_model and d_ff, the TLF_MAX_* limits,
+ * router_hidden, max_pos and the 32-bit offset limits). */
 int tlf_init(const tlf_config* cfg, const tlf_weights* w, void* d_workspace, size_t ws_bytes,
              size_t* ws_needed, void* hip_stream, tlf_ctx** out);
 
@@ -247,7 +251,9 @@ int tlf_prefill(tlf_ctx* ctx, int32_t batch, int32_t seq_len, const int32_t* d_t
 int tlf_decode_step(tlf_ctx* ctx, const int32_t* d_tokens, float* d_logits, int32_t* d_next,
                     int32_t* d_depths, float* d_margin);
 
-/* Waits for the stream, then fills *out and, optionally, the logical cache index.
+/* Waits for the stream, then fills *out and, optionally, the logical cache
+ * index: which original positions each recursion-wise cache (b, i) holds
+ * (Eq. 8; each token of depth m appended to the caches of loops 1..m, Eq. 11).
  *   h_len: [batch][R] int32 host array of cache lengths n_{b,i}, or NULL.
  *   h_pos: host array receiving, for b = 0..batch-1 and i = 1..R in that order,
  *          the ascending original positions held by cache (b, i), or NULL.
@@ -272,6 +278,17 @@ int tlf_cache_stats(tlf_ctx* ctx, tlf_cache_stats_t* out, int32_t* h_len, int32_
 #define TLF_PROFILE_ATTN 1
 #define TLF_PROFILE_BLOCK 2
 int tlf_set_profiling(tlf_ctx* ctx, int mode);
+
+/* Measurement probe (no context): reads `bytes` of device memory at d_buf
+ * once with the 16-byte non-temporal vector loads the decode attention
+ * streams its cache with, one workgroup per TLF_PROBE_READ_GRAIN bytes, and
+ * writes nothing except, with negligible probability, one word of d_sink.
+ * The read rate it reaches is the practical ceiling for the decode
+ * attention's streaming.  bytes must be a positive multiple of
+ * TLF_PROBE_READ_GRAIN and d_buf 16-byte aligned (else TLF_E_INVALID_ARG);
+ * enqueued on `d_stream` without waiting. */
+#define TLF_PROBE_READ_GRAIN 32768
+int tlf_probe_read(const void* d_buf, size_t bytes, unsigned int* d_sink, void* d_stream);
 
 /* Releases the host context (waits for the stream first).  NULL is ignored. */
 void tlf_destroy(tlf_ctx* ctx);

@@ -12,7 +12,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libtlf.so")
 SOURCES = ["api.hip", "gemm.hip", "dgemm.hip", "plan.hip", "attn.hip", "rows.hip", "cond.hip", "gs.hip",
-           "noalloc.hip"]
+           "noalloc.hip", "probe.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",

@@ -88,22 +88,17 @@ bool make_layout(const tlf_config& c, Layout* L) {
 
 static_assert(kPlanThreads * 4 >= TLF_MAX_BATCH, "the decode planner covers the batch in 4 chunks");
 
+// TLF_E_INVALID_ARG for a config that describes no valid model or call
+// setting, TLF_E_UNSUPPORTED for a valid one outside the shapes and sizes the
+// kernels are built for.
 int validate_config(const tlf_config* c) {
   if (!c) return TLF_E_INVALID_ARG;
   if (c->abi_version != TLF_ABI_VERSION) return TLF_E_INVALID_ARG;
   if (c->dtype != TLF_DTYPE_F32 && c->dtype != TLF_DTYPE_BF16) return TLF_E_INVALID_ARG;
-  // GEMM K tiles are 256 bytes: 128 bf16 or 64 float32 elements; rows up to 4096 wide
-  const int kq = c->dtype == TLF_DTYPE_BF16 ? 128 : 64;
-  if (c->vocab < 1 || c->d_model < kq || c->d_model % kq != 0 || c->d_model > 4096) return TLF_E_INVALID_ARG;
-  if (c->head_dim != 16 && c->head_dim != 64 && c->head_dim != 128) return TLF_E_INVALID_ARG;
-  if (c->dtype == TLF_DTYPE_BF16 && c->head_dim == 16) return TLF_E_INVALID_ARG;
+  if (c->vocab < 1 || c->d_model < 1 || c->head_dim < 1 || c->d_ff < 1) return TLF_E_INVALID_ARG;
   if (c->n_heads < 1 || (int64_t)c->n_heads * c->head_dim != c->d_model) return TLF_E_INVALID_ARG;
-  if (c->d_ff < kq || c->d_ff % kq != 0) return TLF_E_INVALID_ARG;
-  if (c->n_layers < 1 || c->n_layers > TLF_MAX_LAYERS) return TLF_E_INVALID_ARG;
-  if (c->max_loops < 1 || c->max_loops > TLF_MAX_LOOPS) return TLF_E_INVALID_ARG;
-  if (c->max_pos < 1 || c->max_batch < 1 || c->max_batch > TLF_MAX_BATCH) return TLF_E_INVALID_ARG;
-  if (c->page_tokens != TLF_PAGE_TOKENS || c->max_pages < 1) return TLF_E_INVALID_ARG;
-  if (c->max_prefill_tokens < 1) return TLF_E_INVALID_ARG;
+  if (c->n_layers < 1 || c->max_loops < 1 || c->max_pos < 1 || c->max_batch < 1) return TLF_E_INVALID_ARG;
+  if (c->page_tokens < 1 || c->max_pages < 1 || c->max_prefill_tokens < 1) return TLF_E_INVALID_ARG;
   if (c->route_rule == TLF_ROUTE_CUMPROB) {
     if (!(c->route_threshold > 0.f && c->route_threshold < 1.f)) return TLF_E_INVALID_ARG;
   } else if (c->route_rule == TLF_ROUTE_FIXED) {
@@ -113,18 +108,29 @@ int validate_config(const tlf_config* c) {
   }
   if (!(c->rms_eps > 0.f) || !std::isfinite(c->rms_eps)) return TLF_E_INVALID_ARG;
   if (c->decode_graph != 0 && c->decode_graph != 1) return TLF_E_INVALID_ARG;
-  if (c->router_hidden < 0 || c->router_hidden > 4096 || c->router_hidden % 64 != 0) return TLF_E_INVALID_ARG;
+  if (c->router_hidden < 0) return TLF_E_INVALID_ARG;
   if (c->dense_decode != 0 && c->dense_decode != 1) return TLF_E_INVALID_ARG;
   if (c->adaln != 0 && c->adaln != 1) return TLF_E_INVALID_ARG;
+  // shapes and sizes of this build's kernels:
+  // GEMM K tiles are 256 bytes: 128 bf16 or 64 float32 elements; rows up to 4096 wide
+  const int kq = c->dtype == TLF_DTYPE_BF16 ? 128 : 64;
+  if (c->d_model < kq || c->d_model % kq != 0 || c->d_model > 4096) return TLF_E_UNSUPPORTED;
+  if (c->head_dim != 16 && c->head_dim != 64 && c->head_dim != 128) return TLF_E_UNSUPPORTED;
+  if (c->dtype == TLF_DTYPE_BF16 && c->head_dim == 16) return TLF_E_UNSUPPORTED;
+  if (c->d_ff < kq || c->d_ff % kq != 0) return TLF_E_UNSUPPORTED;
+  if (c->n_layers > TLF_MAX_LAYERS || c->max_loops > TLF_MAX_LOOPS || c->max_batch > TLF_MAX_BATCH)
+    return TLF_E_UNSUPPORTED;
+  if (c->page_tokens != TLF_PAGE_TOKENS) return TLF_E_UNSUPPORTED;
+  if (c->router_hidden > 4096 || c->router_hidden % 64 != 0) return TLF_E_UNSUPPORTED;
   // the decode attention stages one sequence's page list in LDS
-  if (ceil_div(c->max_pos, kPage) > kAttnMaxPages) return TLF_E_INVALID_ARG;
+  if (ceil_div(c->max_pos, kPage) > kAttnMaxPages) return TLF_E_UNSUPPORTED;
   // the decode projections address weights and activations with 32-bit element offsets
   if ((int64_t)c->vocab * c->d_model >= INT32_MAX || 2 * (int64_t)c->d_ff * c->d_model >= INT32_MAX ||
       (int64_t)TLF_MAX_BATCH * std::max(c->d_ff, 3 * c->d_model) >= INT32_MAX)
-    return TLF_E_INVALID_ARG;
+    return TLF_E_UNSUPPORTED;
   // positions, row indices and work-list offsets are int32
   if ((int64_t)std::max(c->max_prefill_tokens, c->max_pos) * std::max(c->d_ff, 3 * c->d_model) > INT32_MAX)
-    return TLF_E_INVALID_ARG;
+    return TLF_E_UNSUPPORTED;
   return TLF_OK;
 }
 
@@ -840,6 +846,7 @@ const char* tlf_status_str(int status) {
     case TLF_E_STATE: return "invalid state";
     case TLF_E_HIP: return "HIP runtime error";
     case TLF_E_DEVICE: return "device-detected input error";
+    case TLF_E_UNSUPPORTED: return "shape or size not supported by this build";
     default: return "unknown status";
   }
 }

@@ -15,7 +15,7 @@ PKG_DIR = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG_DIR, "libtlf.so")
 HEADER = os.path.join(os.path.dirname(PKG_DIR), "include", "tlf.h")
 
-ABI_VERSION = 4
+ABI_VERSION = 5
 MAX_LOOPS = 16
 MAX_LAYERS = 8
 PAGE_TOKENS = 16
@@ -27,6 +27,7 @@ E_OUT_OF_PAGES = -3
 E_STATE = -4
 E_HIP = -5
 E_DEVICE = -6
+E_UNSUPPORTED = -7
 
 DTYPE_F32 = 0
 DTYPE_BF16 = 1
@@ -91,7 +92,9 @@ class CacheStats(ctypes.Structure):
 
 EXPORTS = ("tlf_init", "tlf_prefill", "tlf_decode_step", "tlf_cache_stats", "tlf_set_profiling", "tlf_destroy",
            "tlf_status_str", "tlf_gs_plan", "tlf_gs_plan_ws", "tlf_gs_plan_noalloc", "tlf_gs_gather",
-           "tlf_gs_scatter", "tlf_ste")
+           "tlf_gs_scatter", "tlf_ste", "tlf_probe_read")
+
+PROBE_READ_GRAIN = 32768
 
 GS_PLAN_CHUNK_ROWS = 2048
 GS_PLAN_MAX_ROWS = 8388608
@@ -148,6 +151,8 @@ def load(path: str = LIB_PATH):
     lib.tlf_gs_plan_ws.restype = ctypes.c_int
     lib.tlf_gs_plan_noalloc.argtypes = [vp, i32, i32, i32, vp, vp, vp, vp, vp]
     lib.tlf_gs_plan_noalloc.restype = ctypes.c_int
+    lib.tlf_probe_read.argtypes = [vp, ctypes.c_size_t, vp, vp]
+    lib.tlf_probe_read.restype = ctypes.c_int
     lib.tlf_gs_gather.argtypes = [vp, vp, vp, i32, i32, vp, vp]
     lib.tlf_gs_gather.restype = ctypes.c_int
     lib.tlf_gs_scatter.argtypes = [vp, vp, vp, i32, i32, vp, vp]

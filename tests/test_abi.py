@@ -71,19 +71,34 @@ def test_size_query_needs_no_device(lib):
     assert pool < need < pool * 1.2
 
 
-@pytest.mark.parametrize("field,value", [
-    ("abi_version", 3), ("abi_version", 5), ("dtype", 7), ("vocab", 0), ("d_model", 100), ("head_dim", 32),
-    ("n_heads", 5), ("d_ff", 1000), ("n_layers", 0), ("n_layers", 9), ("max_loops", 0),
-    ("max_loops", 17), ("max_pos", 0), ("max_batch", 0), ("max_batch", 5000), ("page_tokens", 32),
-    ("max_pages", 0), ("max_prefill_tokens", 0), ("route_rule", 5), ("rms_eps", 0.0),
-    ("router_hidden", -64), ("router_hidden", 96), ("router_hidden", 8192), ("dense_decode", 2), ("adaln", 2),
-    ("dense_decode", -1),
+_BAD, _UNS = tlf.E_INVALID_ARG, tlf.E_UNSUPPORTED
+
+
+@pytest.mark.parametrize("field,value,status", [
+    ("abi_version", 4, _BAD), ("abi_version", 6, _BAD), ("dtype", 7, _BAD), ("vocab", 0, _BAD),
+    ("d_model", 100, _BAD), ("n_heads", 5, _BAD), ("d_ff", 0, _BAD), ("n_layers", 0, _BAD),
+    ("max_loops", 0, _BAD), ("max_pos", 0, _BAD), ("max_batch", 0, _BAD), ("max_pages", 0, _BAD),
+    ("max_prefill_tokens", 0, _BAD), ("route_rule", 5, _BAD), ("rms_eps", 0.0, _BAD),
+    ("router_hidden", -64, _BAD), ("dense_decode", 2, _BAD), ("adaln", 2, _BAD), ("dense_decode", -1, _BAD),
+    # well-formed, outside this build's kernels
+    ("d_ff", 1000, _UNS), ("n_layers", 9, _UNS), ("max_loops", 17, _UNS), ("max_batch", 5000, _UNS),
+    ("page_tokens", 32, _UNS), ("router_hidden", 96, _UNS), ("router_hidden", 8192, _UNS),
+    ("max_pos", 70000, _UNS),
 ])
-def test_invalid_config_rejected(lib, field, value):
+def test_invalid_config_rejected(lib, field, value, status):
     c = _cfg(**{field: value})
     need = ctypes.c_size_t(0)
     st = lib.tlf_init(ctypes.byref(c), None, None, 0, ctypes.byref(need), None, None)
-    assert st == tlf.E_INVALID_ARG
+    assert st == status
+
+
+def test_unsupported_head_dim_and_width(lib):
+    """A consistent model with 32-wide heads, or a width that is not a multiple
+    of the 128-element K tile, is valid but outside the kernels."""
+    need = ctypes.c_size_t(0)
+    for kw in (dict(head_dim=32, n_heads=24), dict(d_model=704, n_heads=11)):
+        c = _cfg(**kw)
+        assert lib.tlf_init(ctypes.byref(c), None, None, 0, ctypes.byref(need), None, None) == _UNS
 
 
 def test_route_parameters_validated(lib):
@@ -102,7 +117,7 @@ def test_bf16_head_dim_16_rejected_f32_accepted(lib):
     c = tlf.make_config(synth.CONFIGS["f32_tiny_b1x32"], 1, 64, 64)
     assert lib.tlf_init(ctypes.byref(c), None, None, 0, ctypes.byref(need), None, None) == tlf.E_NEED_WORKSPACE
     c.dtype = tlf.DTYPE_BF16
-    assert lib.tlf_init(ctypes.byref(c), None, None, 0, ctypes.byref(need), None, None) == tlf.E_INVALID_ARG
+    assert lib.tlf_init(ctypes.byref(c), None, None, 0, ctypes.byref(need), None, None) == tlf.E_UNSUPPORTED
 
 
 def test_missing_weights_rejected_before_device_work(lib):
@@ -189,13 +204,15 @@ def test_binding_constants_match_the_header():
     pairs = {"ABI_VERSION": tlf.ABI_VERSION, "OK": tlf.OK, "E_INVALID_ARG": tlf.E_INVALID_ARG,
              "E_NEED_WORKSPACE": tlf.E_NEED_WORKSPACE, "E_OUT_OF_PAGES": tlf.E_OUT_OF_PAGES,
              "E_STATE": tlf.E_STATE, "E_HIP": tlf.E_HIP, "E_DEVICE": tlf.E_DEVICE,
+             "E_UNSUPPORTED": tlf.E_UNSUPPORTED,
              "DTYPE_F32": tlf.DTYPE_F32, "DTYPE_BF16": tlf.DTYPE_BF16,
              "ROUTE_ARGMAX": tlf.ROUTE["argmax"], "ROUTE_CUMPROB": tlf.ROUTE["cumprob"],
              "ROUTE_FIXED": tlf.ROUTE["fixed"], "PREFILL_ALL_LOGITS": tlf.PREFILL_ALL_LOGITS,
              "PREFILL_APPEND": tlf.PREFILL_APPEND,
              "PROFILE_OFF": tlf.PROFILE_OFF, "PROFILE_ATTN": tlf.PROFILE_ATTN,
              "PROFILE_BLOCK": tlf.PROFILE_BLOCK, "GS_PLAN_CHUNK_ROWS": tlf.GS_PLAN_CHUNK_ROWS,
-             "GS_PLAN_MAX_ROWS": tlf.GS_PLAN_MAX_ROWS, "GS_PLAN_NOALLOC_MAX_ROWS": tlf.GS_PLAN_NOALLOC_MAX_ROWS}
+             "GS_PLAN_MAX_ROWS": tlf.GS_PLAN_MAX_ROWS, "GS_PLAN_NOALLOC_MAX_ROWS": tlf.GS_PLAN_NOALLOC_MAX_ROWS,
+             "PROBE_READ_GRAIN": tlf.PROBE_READ_GRAIN}
     for name, value in pairs.items():
         assert defs[name] == value, name
 
@@ -240,3 +257,9 @@ def test_gather_scatter_argument_errors_need_no_device():
     assert lib.tlf_ste(None, dummy, dummy, 4, dummy, None, None) == bad
     assert lib.tlf_ste(dummy, None, dummy, 4, None, dummy, None) == bad
     assert lib.tlf_ste(dummy, dummy, dummy, 4, None, None, None) == tlf.OK
+    # the read probe takes whole grains of a 16-byte aligned buffer
+    g = tlf.PROBE_READ_GRAIN
+    assert lib.tlf_probe_read(dummy, g + 16, dummy, None) == bad
+    assert lib.tlf_probe_read(dummy, 0, dummy, None) == bad
+    assert lib.tlf_probe_read(ctypes.c_void_p(24), g, dummy, None) == bad
+    assert lib.tlf_probe_read(dummy, g, None, None) == bad
