@@ -408,29 +408,37 @@ def other_workloads(torch, tlf, synth, names=("bf16_d768_b32x512", "bf16_d2048_b
 
 
 def prefill_measure(torch, tlf, synth, name):
-    """Prefill-only workload: time tlf_prefill and count the algorithmic FLOPs."""
+    """Prefill-only workload: time tlf_prefill and count the algorithmic FLOPs.
+    The activations enter the prefill's matrix products as one bf16 part (the
+    precision this workload runs at); the same prefill with hi + lo parts is
+    timed beside it."""
     import numpy as np
     m = synth.CONFIGS[name]
     w = synth.make_weights(m)
     prompts = synth.make_prompts(m)
     B, T = prompts.shape
-    sess = tlf.Session(m, w, max_batch=B, max_pos=T, max_prefill_tokens=B * T)
-    try:
-        toks = torch.from_numpy(prompts).cuda()
-        sess.prefill(toks)  # warm
-        torch.cuda.synchronize()
-        reps = 3
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        for _ in range(reps):
-            _, depths = sess.prefill(toks)
-        e1.record()
-        torch.cuda.synchronize()
-        ms = e0.elapsed_time(e1) / reps
-        dep = depths.cpu().numpy()
-    finally:
-        sess.close()
-        torch.cuda.empty_cache()
+    times = {}
+    for single in (True, False):
+        sess = tlf.Session(m, w, max_batch=B, max_pos=T, max_prefill_tokens=B * T, prefill_act_bf16=single)
+        try:
+            toks = torch.from_numpy(prompts).cuda()
+            sess.prefill(toks)  # warm
+            torch.cuda.synchronize()
+            reps = 3
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(reps):
+                _, depths = sess.prefill(toks)
+            e1.record()
+            torch.cuda.synchronize()
+            times[single] = e0.elapsed_time(e1) / reps
+            dep = depths.cpu().numpy()
+            if sess.stats()["status"] != 0:
+                raise RuntimeError("device error in the prefill measurement")
+        finally:
+            sess.close()
+            torch.cuda.empty_cache()
+    ms = times[True]
     d, F, J, R = m.d_model, m.d_ff, m.n_layers, m.max_loops
     n = np.stack([(dep >= i).sum(axis=1) for i in range(1, R + 1)], axis=1)  # n_{b,i}
     gemm = float(n.sum()) * J * 2 * (4 * d * d + 3 * d * F)
@@ -438,9 +446,12 @@ def prefill_measure(torch, tlf, synth, name):
     head = 2.0 * B * d * m.vocab
     flops = gemm + attn + head
     return {"workload": f"{name} prefill: batch {B} x {T}, d={d}, {m.n_heads}x{m.head_dim} heads, SwiGLU {F}, "
-                        f"R={R}, J={J}", "ms": ms, "tokens_per_s": B * T / ms * 1e3,
+                        f"R={R}, J={J}; activations enter the matrix products as one bf16 part",
+            "ms": ms, "tokens_per_s": B * T / ms * 1e3,
             "algorithmic_tflop": flops / 1e12, "tflops": flops / ms / 1e9,
-            "mfma_frac": flops / ms / 1e9 / BF16_PEAK_TFLOPS}
+            "mfma_frac": flops / ms / 1e9 / BF16_PEAK_TFLOPS,
+            "hi_lo_parts": {"ms": times[False], "tflops": flops / times[False] / 1e9,
+                            "mfma_frac": flops / times[False] / 1e9 / BF16_PEAK_TFLOPS}}
 
 
 def train_gather_scatter(torch, synth, B=8, T=4096, d=1024, R=8, reps=20):

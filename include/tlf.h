@@ -120,6 +120,13 @@ typedef struct tlf_config {
                             loop i has cumulative time (i-1)/m and step 1/m, and layer j's
                             modulation (alpha_msa, alpha_mlp, gamma_msa, gamma_mlp) enters as
                             x += (1 + alpha) * F(RMSNorm(x) * (1 + gamma)) */
+  int32_t prefill_act_bf16; /* bf16 models, prefills of more than one sequence or longer than 2048
+                               tokens: 0: the float32 activations enter the block's matrix products
+                               and the attention scores as bf16 hi + lo parts; 1: as one bf16 part
+                               (round to nearest even), half the matrix-core work.  Decode steps and
+                               every LM head keep the two parts.  An exact bf16 implementation with
+                               every activation rounded stays within 1.9e-2 of float64 on the
+                               logits at d_model 1024 but reaches 4.1e-2 at 2048 */
 } tlf_config;
 
 /* Weights of layer j of the shared block, row-major [out][in] (y = x W^T),

@@ -20,7 +20,7 @@ int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 enum Buf {
   B_POOL, B_POS, B_PAGE_TABLE, B_CACHE_LEN, B_CHUNK_LEN, B_SEQ_LEN, B_SCALARS, B_DEPTH_HIST, B_STEP_STATS,
   B_X_DEC, B_XC_DEC, B_KVSLOT, B_DEPTH_DEC, B_PERM, B_NACT, B_Q_DEC, B_O_DEC, B_ACT_DEC, B_KEYS,
-  B_X_PRE, B_Y_PRE, B_DEPTH_PRE, B_TOK_IDX, B_Q_PRE, B_O_PRE, B_ACT_PRE, B_HID,
+  B_X_PRE, B_Y_PRE, B_Y16_PRE, B_DEPTH_PRE, B_TOK_IDX, B_Q_PRE, B_O_PRE, B_ACT_PRE, B_HID,
   B_ROW_DEPTH, B_MOD, B_COND_TMP, B_WFRAG,
   B_COUNT
 };
@@ -63,6 +63,9 @@ bool make_layout(const tlf_config& c, Layout* L) {
   sz[B_KEYS] = B * ceil_div(c.vocab, kWave) * 8;  // greedy key per 64-column group of each row
   sz[B_X_PRE] = P * d * 4;
   sz[B_Y_PRE] = P * d * 4;
+  // one-part bf16 prefill activations: RMSNorm(x) as bf16 rows (o and act
+  // are written as bf16 into their own float buffers)
+  sz[B_Y16_PRE] = c.prefill_act_bf16 && c.dtype == TLF_DTYPE_BF16 ? P * d * 2 : 0;
   sz[B_DEPTH_PRE] = P * 4;
   sz[B_TOK_IDX] = R * P * 4;
   sz[B_Q_PRE] = P * d * 4;
@@ -111,6 +114,7 @@ int validate_config(const tlf_config* c) {
   if (c->router_hidden < 0) return TLF_E_INVALID_ARG;
   if (c->dense_decode != 0 && c->dense_decode != 1) return TLF_E_INVALID_ARG;
   if (c->adaln != 0 && c->adaln != 1) return TLF_E_INVALID_ARG;
+  if (c->prefill_act_bf16 != 0 && c->prefill_act_bf16 != 1) return TLF_E_INVALID_ARG;
   // shapes and sizes of this build's kernels:
   // GEMM K tiles are 256 bytes: 128 bf16 or 64 float32 elements; rows up to 4096 wide
   const int kq = c->dtype == TLF_DTYPE_BF16 ? 128 : 64;
@@ -320,11 +324,18 @@ int run_prefill(tlf_ctx* ctx, int B, int T_, int pos0, const int32_t* tokens, fl
     // device, so the projections take the split-K decode GEMM with the
     // RMSNorm fused (x is read through the gathered positions, no y)
     const bool few = Gc == 1 && T_ <= kPrefillFewRows;
+    // one-part bf16 activations (prefill_act_bf16, bf16 weights, the many-row
+    // GEMMs): RMSNorm(x), o and act are handed on as bf16 rows; the LM head
+    // keeps reading the float32 RMSNorm(x)
+    const bool one = c.prefill_act_bf16 && c.dtype == TLF_DTYPE_BF16 && !few;
+    bf16* y16 = one ? ctx->buf<bf16>(B_Y16_PRE) : nullptr;
+    bf16* o16 = one ? ctx->buf<bf16>(B_O_PRE) : nullptr;
+    bf16* act16 = one ? ctx->buf<bf16>(B_ACT_PRE) : nullptr;
     EmbedArgs ea;
     ea.tok_emb = ctx->w.tok_emb; ea.pos_emb = ctx->w.pos_emb; ea.Wr = ctx->w.router_w; ea.br = ctx->w.router_b;
     ea.tokens = tokens + (int64_t)b0 * T_;
     ea.rows = rows; ea.V = c.vocab; ea.d = d; ea.R = R; ea.prefill_T = T_; ea.pos0 = pos0;
-    ea.x = x; ea.y = few ? nullptr : y; ea.eps = c.rms_eps; ea.depth = ctx->buf<int32_t>(B_DEPTH_PRE);
+    ea.x = x; ea.y = few ? nullptr : y; ea.y16 = y16; ea.eps = c.rms_eps; ea.depth = ctx->buf<int32_t>(B_DEPTH_PRE);
     ea.out_depth = depths ? depths + (int64_t)b0 * T_ : nullptr;
     ea.rule = c.route_rule; ea.threshold = c.route_threshold; ea.fixed = c.fixed_depth;
     ea.err = ctx->cv.err;
@@ -351,7 +362,7 @@ int run_prefill(tlf_ctx* ctx, int B, int T_, int pos0, const int32_t* tokens, fl
       rm.seg = T_; rm.seg_cnt_stride = R; rm.rows = rows;
       if (few) rm.nact = rm.seg_cnt;  // one segment: rows [0, n) active
       ResidNormArgs rn;
-      rn.rm = rm; rn.x = x; rn.y = y; rn.d = d; rn.eps = c.rms_eps;
+      rn.rm = rm; rn.x = x; rn.y = y; rn.y16 = y16; rn.d = d; rn.eps = c.rms_eps;
       for (int j = 0; j < c.n_layers; ++j) {
         const tlf_layer_weights& lw = ctx->layers[j];
         GemmArgs q;
@@ -359,6 +370,8 @@ int run_prefill(tlf_ctx* ctx, int B, int T_, int pos0, const int32_t* tokens, fl
         q.out = ctx->buf<float>(B_Q_PRE); q.ldo = d; q.d = d; q.eps = c.rms_eps; q.spec = i == 0;
         q.kv.c = ctx->cv; q.kv.loop = i; q.kv.layer = j; q.kv.prefill = 1; q.kv.b0 = b0; q.kv.seg = T_;
         set_mod(ctx, &q, i, j, 2, pre_depth, 1);
+        q.a_single = one;
+        if (one && !q.mod_g) q.A16 = y16;  // the AdaLN scale needs the float rows
         if (few) TLF_HIP(launch_dgemm<T>(q, A_SRC, E_QKV, true, ctx->cus, s));
         else TLF_HIP(launch_gemm<T>(q, A_SRC, E_QKV, false, s));
 
@@ -366,11 +379,13 @@ int run_prefill(tlf_ctx* ctx, int B, int T_, int pos0, const int32_t* tokens, fl
         at.c = ctx->cv; at.loop = i; at.layer = j; at.d = d; at.b0 = b0; at.G = Gc; at.T = T_;
         at.q = ctx->buf<float>(B_Q_PRE); at.o = ctx->buf<float>(B_O_PRE);
         at.scale_log2 = 1.4426950408889634f / std::sqrt((float)c.head_dim);
+        at.q_single = one;
+        at.o16 = o16;
         TLF_HIP(launch_attn_prefill<T>(at, s));
 
         GemmArgs o;
         o.A = ctx->buf<float>(B_O_PRE); o.lda = d; o.W = lw.w_o; o.Wf = ctx->wfrag(j, 1); o.N = d; o.K = d; o.w_rows = d; o.rm = rm;
-        o.out = x; o.ldo = d; o.scatter = 1; o.spec = i == 0;
+        o.out = x; o.ldo = d; o.scatter = 1; o.spec = i == 0; o.a_single = one; o.A16 = o16;
         set_mod(ctx, &o, i, j, 0, pre_depth, 1);
         if (few) {
           TLF_HIP(launch_dgemm<T>(o, A_CMP, E_RESID, false, ctx->cus, s));
@@ -382,13 +397,15 @@ int run_prefill(tlf_ctx* ctx, int B, int T_, int pos0, const int32_t* tokens, fl
         GemmArgs gu;
         gu.A = few ? x : y; gu.lda = d; gu.W = lw.w_gate_up; gu.Wf = ctx->wfrag(j, 2); gu.N = 2 * F; gu.K = d; gu.w_rows = 2 * F; gu.rm = rm;
         gu.out = ctx->buf<float>(B_ACT_PRE); gu.ldo = F; gu.F = F; gu.eps = c.rms_eps; gu.spec = i == 0;
+        gu.a_single = one; gu.out16 = act16;
         set_mod(ctx, &gu, i, j, 3, pre_depth, 1);
+        if (one && !gu.mod_g) gu.A16 = y16;
         if (few) TLF_HIP(launch_dgemm<T>(gu, A_SRC, E_SWIGLU, true, ctx->cus, s));
         else TLF_HIP(launch_gemm<T>(gu, A_SRC, E_SWIGLU, false, s));
 
         GemmArgs dn;
         dn.A = ctx->buf<float>(B_ACT_PRE); dn.lda = F; dn.W = lw.w_down; dn.Wf = ctx->wfrag(j, 3); dn.N = d; dn.K = F; dn.w_rows = d;
-        dn.rm = rm; dn.out = x; dn.ldo = d; dn.scatter = 1; dn.spec = i == 0;
+        dn.rm = rm; dn.out = x; dn.ldo = d; dn.scatter = 1; dn.spec = i == 0; dn.a_single = one; dn.A16 = act16;
         set_mod(ctx, &dn, i, j, 1, pre_depth, 1);
         if (few) {
           TLF_HIP(launch_dgemm<T>(dn, A_CMP, E_RESID, false, ctx->cus, s));

@@ -18,7 +18,8 @@
 // registers while the current one is in use.  Scores are computed transposed,
 // S^T = K q^T, so that the P^T operand of O^T = V^T P^T is exactly the scores
 // each lane holds (no data movement between the two products); both run on
-// MFMA with an online softmax per query.
+// MFMA with an online softmax per query.  Against bf16 keys q enters as hi +
+// lo parts, or as one bf16 part when the caller asks for it (q_single).
 #include "kernels.h"
 
 namespace tlf {
@@ -259,7 +260,7 @@ __global__ __launch_bounds__(W * 64) void k_attn_decode(AttnDecodeArgs a) {
   }
 }
 
-template <typename T, int D>
+template <typename T, int D, bool SPLITQ>
 __global__ __launch_bounds__(256, 4) void k_attn_prefill(AttnPrefillArgs a) {
   using M = Mfma<T>;
   typedef typename M::frag Frag;
@@ -271,7 +272,7 @@ __global__ __launch_bounds__(256, 4) void k_attn_prefill(AttnPrefillArgs a) {
   constexpr int NT = BKEY / 16;                   // 16-key subtiles
   constexpr int KSTEPS = D / KS;
   constexpr int DT = D / 16;
-  constexpr int NQ = EPL == 8 ? 2 : 1;            // parts of q (hi, lo)
+  constexpr int NQ = EPL == 8 && SPLITQ ? 2 : 1;  // parts of q (hi, lo), or one bf16 part
   constexpr int KBLK = kPage * D;                 // elements of one page's K (or V) block
   constexpr int EPC = 16 / (int)sizeof(T);        // elements per 16-byte chunk
   constexpr int VLD = kPage + (sizeof(T) == 2 ? 4 : 2);  // padded LDS row of one dimension of a V block
@@ -326,6 +327,11 @@ __global__ __launch_bounds__(256, 4) void k_attn_prefill(AttnPrefillArgs a) {
         split4(scale4(v1, a.scale_log2), h1, l1);
         qf[qn][0][ks] = __builtin_bit_cast(Frag, make_uint4(h0.x, h0.y, h1.x, h1.y));
         qf[qn][1][ks] = __builtin_bit_cast(Frag, make_uint4(l0.x, l0.y, l1.x, l1.y));
+      } else if constexpr (EPL == 8) {
+        const float4 v0 = scale4(*reinterpret_cast<const float4*>(qp + ks * KS), a.scale_log2);
+        const float4 v1 = scale4(*reinterpret_cast<const float4*>(qp + ks * KS + 4), a.scale_log2);
+        qf[qn][0][ks] = __builtin_bit_cast(Frag, make_uint4(pack_bf16x2(v0.x, v0.y), pack_bf16x2(v0.z, v0.w),
+                                                            pack_bf16x2(v1.x, v1.y), pack_bf16x2(v1.z, v1.w)));
       } else {
         qf[qn][0][ks] = qp[ks * KS] * a.scale_log2;
       }
@@ -489,12 +495,20 @@ __global__ __launch_bounds__(256, 4) void k_attn_prefill(AttnPrefillArgs a) {
     lt += shfl_xor(lt, 32);
     const int row = q0 + w * QW + qn * 16 + c16;
     if (row >= nq) continue;
-    float* op = a.o + ((int64_t)g * a.T + row) * a.d + h * D + 4 * quad;
+    const int64_t oo = ((int64_t)g * a.T + row) * a.d + h * D + 4 * quad;
     const float inv = 1.f / lt;
+    if (a.o16) {
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt)
-      *reinterpret_cast<float4*>(op + dt * 16) =
-          make_float4(o[dt][qn][0] * inv, o[dt][qn][1] * inv, o[dt][qn][2] * inv, o[dt][qn][3] * inv);
+      for (int dt = 0; dt < DT; ++dt)
+        *reinterpret_cast<uint2*>(a.o16 + oo + dt * 16) =
+            make_uint2(pack_bf16x2(o[dt][qn][0] * inv, o[dt][qn][1] * inv),
+                       pack_bf16x2(o[dt][qn][2] * inv, o[dt][qn][3] * inv));
+    } else {
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+        *reinterpret_cast<float4*>(a.o + oo + dt * 16) =
+            make_float4(o[dt][qn][0] * inv, o[dt][qn][1] * inv, o[dt][qn][2] * inv, o[dt][qn][3] * inv);
+    }
   }
 }
 
@@ -554,13 +568,19 @@ hipError_t launch_attn_prefill(const AttnPrefillArgs& a, hipStream_t s) {
     case 16:
       // a 16-wide head needs the 4-deep f32 MFMA; bf16 models reject head_dim 16
       if constexpr (sizeof(T) == 4) {
-        hipLaunchKernelGGL((k_attn_prefill<T, 16>), grid, block, 0, s, a);
+        hipLaunchKernelGGL((k_attn_prefill<T, 16, true>), grid, block, 0, s, a);
         break;
       } else {
         return hipErrorInvalidValue;
       }
-    case 64: hipLaunchKernelGGL((k_attn_prefill<T, 64>), grid, block, 0, s, a); break;
-    case 128: hipLaunchKernelGGL((k_attn_prefill<T, 128>), grid, block, 0, s, a); break;
+    case 64:
+      if (sizeof(T) == 2 && a.q_single) hipLaunchKernelGGL((k_attn_prefill<T, 64, false>), grid, block, 0, s, a);
+      else hipLaunchKernelGGL((k_attn_prefill<T, 64, true>), grid, block, 0, s, a);
+      break;
+    case 128:
+      if (sizeof(T) == 2 && a.q_single) hipLaunchKernelGGL((k_attn_prefill<T, 128, false>), grid, block, 0, s, a);
+      else hipLaunchKernelGGL((k_attn_prefill<T, 128, true>), grid, block, 0, s, a);
+      break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

@@ -5,7 +5,8 @@
 // normalised residual rows y[src(r)] (A_SRC) or compact rows buf[r] (A_CMP).
 // With bf16 weights every A tile is split into bf16 hi and lo parts in LDS
 // and each product runs once per part, so the activations keep about 16
-// significant bits; the weights are exact in bf16.
+// significant bits; the weights are exact in bf16.  With a_single the A tile
+// is rounded to one bf16 part instead (half the products).
 // Epilogues:
 //   E_QKV:     q to a buffer; k, v appended to the loop's cache pages (Eq. 11)
 //   E_RESID:   x[src(r)] += result (residual of the attention/FFN branch)
@@ -64,15 +65,22 @@ template <typename T> __device__ __forceinline__ int swz(int row, int c) {
 // NORM: A holds residual rows x and the product is taken with RMSNorm(x): the
 // sum of squares of each row is accumulated from the A chunks as they pass
 // and the output row is scaled by 1 / rms, since (x / rms) W^T = (x W^T) / rms.
-template <typename T, int NT, int AK, int EK, bool MOD, bool NORM>
+// AMODE (bf16 weights): 0: float A enters the MFMA as hi + lo parts; 1: as
+// one bf16 part (round to nearest even), half the products and LDS traffic;
+// 2: A is read as bf16 rows (g.A16), half the A bytes as well.  Float32
+// weights take float A (AMODE 0).
+// MT x NT: each wave's 16 x 16 MFMA tiles; BK: K elements per LDS stage.
+template <typename T, int MT, int NT, int BK, int AK, int EK, bool MOD, bool NORM, int AMODE>
 __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs g) {
-  constexpr int MT = kGemmMT, BK = kGemmBK;
   constexpr int BM = 2 * MT * 16, BN = 2 * NT * 16;
-  constexpr bool kSplit = sizeof(T) == 2;            // bf16 weights: A as hi + lo parts
+  constexpr bool kBf16 = sizeof(T) == 2;             // bf16 weights: A converted to bf16 in LDS
+  constexpr bool kSplit = kBf16 && AMODE == 0;       // ... as hi + lo parts
+  constexpr bool kA16 = kBf16 && AMODE == 2;         // A already bf16 in memory
+  static_assert(!kA16 || (!MOD && !NORM), "bf16 A rows carry no modulation or norm");
   constexpr int NA = kSplit ? 2 : 1;
   constexpr int CE = 16 / (int)sizeof(T);            // storage elements per 16-byte chunk
   constexpr int WCR = BK / CE;                       // weight chunks per row per K tile
-  constexpr int ACR = BK / 4;                        // A chunks (4 floats) per row per K tile
+  constexpr int ACR = kA16 ? BK / CE : BK / 4;       // A chunks (8 bf16 or 4 floats) per row per K tile
   using M = Mfma<T>;
   constexpr int KS = M::KS, EPL = M::EPL;
   constexpr int ACH = BM * ACR / 256;                // A chunks per thread
@@ -105,10 +113,12 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs g) {
     return wr < g.w_rows ? wr : g.w_rows - 1;
   };
 
-  float4 ra[ACH];
+  float4 ra[kA16 ? 1 : ACH];
+  V16<T> ra16[kA16 ? ACH : 1];
   float4 rg[MOD ? ACH : 1];  // gamma of the A chunks in flight
   V16<T> rb[BCH];
   const float* A = reinterpret_cast<const float*>(g.A);
+  const T* A16 = reinterpret_cast<const T*>(g.A16);
   const T* W = reinterpret_cast<const T*>(g.W);
   const int KT = g.K / BK;
 
@@ -124,6 +134,19 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs g) {
   };
   auto load_a = [&](int kt) {
     const int kk = kt * BK;
+    if constexpr (kA16) {
+#pragma unroll
+      for (int c = 0; c < ACH; ++c) {
+        const int ch = tid + c * 256, row = ch / ACR, col = (ch % ACR) * CE;
+        const int s = row_src_s[row];
+        ra16[c].u = make_uint4(0u, 0u, 0u, 0u);
+        if (s >= 0) {
+          const int64_t ar = (AK == A_SRC) ? (int64_t)s : (int64_t)(r0 + row);
+          ra16[c] = ld16(A16 + ar * g.lda + kk + col);
+        }
+      }
+      return;
+    }
 #pragma unroll
     for (int c = 0; c < ACH; ++c) {
       const int ch = tid + c * 256, row = ch / ACR, col = (ch % ACR) * 4;
@@ -144,7 +167,7 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs g) {
   for (int c = 0; c < (NORM ? ACH : 1); ++c) ssq[c] = 0.f;
   auto store_tiles = [&](int st) {
 #pragma unroll
-    for (int c = 0; c < ACH; ++c) {
+    for (int c = 0; c < (kA16 ? 0 : ACH); ++c) {
       const int ch = tid + c * 256, row = ch / ACR, f = ch % ACR;  // floats 4f .. 4f + 3 of the row
       float4 av = ra[c];
       if constexpr (NORM) ssq[c] += av.x * av.x + av.y * av.y + av.z * av.z + av.w * av.w;
@@ -158,8 +181,17 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs g) {
         split4(av, hi, lo);
         *reinterpret_cast<uint2*>(dst) = hi;
         *reinterpret_cast<uint2*>(dst + BM * BK) = lo;  // As[st][1]
+      } else if constexpr (kBf16) {
+        *reinterpret_cast<uint2*>(dst) = make_uint2(pack_bf16x2(av.x, av.y), pack_bf16x2(av.z, av.w));
       } else {
         *reinterpret_cast<float4*>(dst) = av;
+      }
+    }
+    if constexpr (kA16) {
+#pragma unroll
+      for (int c = 0; c < ACH; ++c) {
+        const int ch = tid + c * 256, row = ch / ACR, cc = ch % ACR;
+        st16(&As[st][0][row * BK + swz<T>(row, cc) * CE], ra16[c]);
       }
     }
 #pragma unroll
@@ -359,8 +391,12 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs g) {
           const int n = n0 + wn * NT * 16 + j * 16;  // first gate column of the group
           const int unit = (n >> 5) * 16 + (col16 & ~3);
           if (src < 0 || unit >= g.F) continue;
-          *reinterpret_cast<float4*>(reinterpret_cast<float*>(g.out) + (int64_t)(r0 + rl) * g.ldo + unit) =
-              make_float4(h[0], h[1], h[2], h[3]);
+          if (g.out16)
+            *reinterpret_cast<uint2*>(g.out16 + (int64_t)(r0 + rl) * g.ldo + unit) =
+                make_uint2(pack_bf16x2(h[0], h[1]), pack_bf16x2(h[2], h[3]));
+          else
+            *reinterpret_cast<float4*>(reinterpret_cast<float*>(g.out) + (int64_t)(r0 + rl) * g.ldo + unit) =
+                make_float4(h[0], h[1], h[2], h[3]);
         }
       }
     }
@@ -415,26 +451,38 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs g) {
   }
 }
 
-template <typename T, int NT>
+template <typename T, int MT, int NT>
 hipError_t launch_tiles(const GemmArgs& a, AKind ak, EKind ek, bool norm, hipStream_t s) {
-  constexpr int BM = 2 * kGemmMT * 16, BN = 2 * NT * 16;
+  constexpr int BM = 2 * MT * 16, BN = 2 * NT * 16;
   const dim3 grid((a.N + BN - 1) / BN, (a.rm.rows + BM - 1) / BM);
   if (grid.x == 0 || grid.y == 0) return hipSuccess;
   const bool mod = a.mod_g != nullptr;
-#define TLF_GEMM_CASE(AKV, EKV, MODV, NORMV)                                                \
-  if (ak == AKV && ek == EKV && mod == MODV && norm == NORMV) {                             \
-    hipLaunchKernelGGL((k_gemm<T, NT, AKV, EKV, MODV, NORMV>), grid, dim3(256), 0, s, a);   \
-    return hipGetLastError();                                                               \
+  // operand mode: hi + lo parts, one bf16 part of float A, or bf16 A rows
+  const int amode = sizeof(T) != 2 ? 0 : a.A16 ? 2 : a.a_single ? 1 : 0;
+  if (amode == 2 && (mod || norm)) return hipErrorInvalidValue;
+#define TLF_GEMM_LAUNCH(AKV, EKV, MODV, NORMV, AM) \
+  hipLaunchKernelGGL((k_gemm<T, MT, NT, kGemmBK, AKV, EKV, MODV, NORMV, AM>), grid, dim3(256), 0, s, a)
+  {
+#define TLF_GEMM_CASE(AKV, EKV, MODV, NORMV)                                  \
+  if (ak == AKV && ek == EKV && mod == MODV && norm == NORMV) {               \
+    if (amode == 0) TLF_GEMM_LAUNCH(AKV, EKV, MODV, NORMV, 0);                \
+    else if (amode == 1) TLF_GEMM_LAUNCH(AKV, EKV, MODV, NORMV, 1);           \
+    else if constexpr (!MODV && !NORMV) TLF_GEMM_LAUNCH(AKV, EKV, false, false, 2); \
+    return hipGetLastError();                                                 \
   }
   TLF_GEMM_CASE(A_SRC, E_QKV, false, false)
   TLF_GEMM_CASE(A_SRC, E_QKV, true, false)
   TLF_GEMM_CASE(A_SRC, E_SWIGLU, false, false)
   TLF_GEMM_CASE(A_SRC, E_SWIGLU, true, false)
-  TLF_GEMM_CASE(A_SRC, E_LOGITS, false, false)
-  TLF_GEMM_CASE(A_CMP, E_LOGITS, false, true)
   TLF_GEMM_CASE(A_CMP, E_RESID, false, false)
-  TLF_GEMM_CASE(A_CMP, E_HIDDEN, false, false)
 #undef TLF_GEMM_CASE
+  // the LM heads and the router's hidden layer keep the hi + lo parts
+  if (amode != 0) return hipErrorInvalidValue;
+  if (ak == A_SRC && ek == E_LOGITS && !mod && !norm) { TLF_GEMM_LAUNCH(A_SRC, E_LOGITS, false, false, 0); return hipGetLastError(); }
+  if (ak == A_CMP && ek == E_LOGITS && !mod && norm) { TLF_GEMM_LAUNCH(A_CMP, E_LOGITS, false, true, 0); return hipGetLastError(); }
+  if (ak == A_CMP && ek == E_HIDDEN && !mod && !norm) { TLF_GEMM_LAUNCH(A_CMP, E_HIDDEN, false, false, 0); return hipGetLastError(); }
+  }
+#undef TLF_GEMM_LAUNCH
   return hipErrorInvalidValue;
 }
 
@@ -451,8 +499,9 @@ hipError_t launch_gemm(const GemmArgs& a, AKind ak, EKind ek, bool norm, hipStre
     return hipErrorInvalidValue;
   // a few row tiles (the decode LM head) take 128-column tiles so the grid
   // still holds about two workgroups per compute unit; prefill takes 256
-  if ((a.rm.rows + 2 * kGemmMT * 16 - 1) / (2 * kGemmMT * 16) <= 4) return launch_tiles<T, 4>(a, ak, ek, norm, s);
-  return launch_tiles<T, 8>(a, ak, ek, norm, s);
+  const int row_tiles = (a.rm.rows + 2 * kGemmMT * 16 - 1) / (2 * kGemmMT * 16);
+  if (row_tiles <= 4) return launch_tiles<T, kGemmMT, 4>(a, ak, ek, norm, s);
+  return launch_tiles<T, kGemmMT, 8>(a, ak, ek, norm, s);
 }
 
 template hipError_t launch_gemm<float>(const GemmArgs&, AKind, EKind, bool, hipStream_t);

@@ -110,6 +110,10 @@ struct GemmArgs {
   int mod_by_src = 0;
   const int32_t* keep_depth = nullptr;  // E_RESID (dense decode): row r is stored only while
   int keep_loop = 0;                    // keep_depth[r] > keep_loop (its token runs this loop)
+  int a_single = 0;         // launch_gemm with bf16 weights: A rounded to one bf16 part (not hi + lo)
+  const bf16* A16 = nullptr;  // launch_gemm with bf16 weights: A given as bf16 rows (same lda) in place of
+                              // A (no norm, no operand modulation)
+  bf16* out16 = nullptr;      // launch_gemm E_SWIGLU: act rows written as bf16 instead of float
 };
 
 // Many-row projections (prefill, and the decode LM head of a large batch):
@@ -157,6 +161,7 @@ struct EmbedArgs {
   const int32_t* seq_len = nullptr;
   float* x = nullptr;             // [rows][d] float residual
   float* y = nullptr;             // [rows][d] RMSNorm(x), or nullptr
+  bf16* y16 = nullptr;            // [rows][d] RMSNorm(x) rounded to bf16, or nullptr
   float eps = 1e-5f;
   int32_t* depth = nullptr;       // [rows]
   int32_t* out_depth = nullptr;   // optional [rows]
@@ -188,6 +193,7 @@ struct ResidNormArgs {
   RowMap rm;
   const float* x = nullptr;
   float* y = nullptr;
+  bf16* y16 = nullptr;      // also RMSNorm(x) rounded to bf16, or nullptr
   int d = 0;
   float eps = 1e-5f;
 };
@@ -250,6 +256,8 @@ struct AttnPrefillArgs {
   const float* q = nullptr; // [G*T][d], row g*T + a
   float* o = nullptr;       // [G*T][d]
   float scale_log2 = 0.f;
+  int q_single = 0;         // bf16 keys: the scaled q enters the score product as one bf16 part (not hi + lo)
+  bf16* o16 = nullptr;      // [G*T][d]: o written as bf16 instead of to o
 };
 template <typename T> hipError_t launch_attn_prefill(const AttnPrefillArgs& a, hipStream_t s);
 

@@ -146,6 +146,15 @@ __global__ __launch_bounds__(256) void k_embed_route(EmbedArgs a) {
       if (k < a.d) V4<float>::store(y + k, scale4(h[c], inv));
     }
   }
+  if (a.y16) {
+    bf16* y = a.y16 + (int64_t)row * a.d;
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      const int k = 4 * lane + 256 * c;
+      const float4 v = scale4(h[c], inv);
+      if (k < a.d) *reinterpret_cast<uint2*>(y + k) = make_uint2(pack_bf16x2(v.x, v.y), pack_bf16x2(v.z, v.w));
+    }
+  }
   if (!a.route) return;  // the MLP router runs after this kernel
   float z[kMaxLoops];
 #pragma unroll
@@ -243,6 +252,15 @@ __global__ __launch_bounds__(256) void k_resid_norm(ResidNormArgs a) {
   for (int c = 0; c < NC; ++c) {
     const int k = 4 * tid + 1024 * c;
     if (k < a.d) V4<float>::store(y + k, scale4(h[c], inv));
+  }
+  if (a.y16) {
+    bf16* y16 = a.y16 + (int64_t)src * a.d;
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      const int k = 4 * tid + 1024 * c;
+      const float4 v = scale4(h[c], inv);
+      if (k < a.d) *reinterpret_cast<uint2*>(y16 + k) = make_uint2(pack_bf16x2(v.x, v.y), pack_bf16x2(v.z, v.w));
+    }
   }
 }
 

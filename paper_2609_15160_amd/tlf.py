@@ -49,6 +49,7 @@ class Config(ctypes.Structure):
         ("route_rule", ctypes.c_int32), ("route_threshold", ctypes.c_float),
         ("fixed_depth", ctypes.c_int32), ("rms_eps", ctypes.c_float), ("decode_graph", ctypes.c_int32),
         ("router_hidden", ctypes.c_int32), ("dense_decode", ctypes.c_int32), ("adaln", ctypes.c_int32),
+        ("prefill_act_bf16", ctypes.c_int32),
     ]
 
 
@@ -172,7 +173,7 @@ def status_str(status: int) -> str:
 
 def make_config(model, max_batch: int, max_pos: int, max_pages: int, route_rule: str = "argmax",
                 threshold: float = 0.5, fixed_depth: int = 1, max_prefill_tokens: int = 65536,
-                decode_graph: bool = True, dense_decode: bool = False) -> Config:
+                decode_graph: bool = True, dense_decode: bool = False, prefill_act_bf16: bool = False) -> Config:
     """Config from a model description with attributes like ``synth.ModelConfig``."""
     return Config(
         abi_version=ABI_VERSION, dtype=DTYPE_BF16 if model.dtype == "bf16" else DTYPE_F32,
@@ -182,7 +183,8 @@ def make_config(model, max_batch: int, max_pos: int, max_pages: int, route_rule:
         max_prefill_tokens=max_prefill_tokens, route_rule=ROUTE[route_rule],
         route_threshold=threshold, fixed_depth=fixed_depth, rms_eps=model.rms_eps,
         decode_graph=1 if decode_graph else 0, router_hidden=getattr(model, "router_hidden", 0),
-        dense_decode=1 if dense_decode else 0, adaln=1 if getattr(model, "adaln", False) else 0)
+        dense_decode=1 if dense_decode else 0, adaln=1 if getattr(model, "adaln", False) else 0,
+        prefill_act_bf16=1 if prefill_act_bf16 else 0)
 
 
 def workspace_bytes(cfg: Config) -> int:
@@ -205,7 +207,7 @@ class Session:
     def __init__(self, model, weights: Dict, max_batch: int, max_pos: Optional[int] = None,
                  max_pages: Optional[int] = None, route_rule: str = "argmax", threshold: float = 0.5,
                  fixed_depth: int = 1, max_prefill_tokens: int = 65536, device: str = "cuda",
-                 decode_graph: bool = True, dense_decode: bool = False):
+                 decode_graph: bool = True, dense_decode: bool = False, prefill_act_bf16: bool = False):
         import torch
         self.torch = torch
         self.lib = load()
@@ -215,7 +217,7 @@ class Session:
         if max_pages is None:
             max_pages = worst_case_pages(max_batch, max_pos, model.max_loops)
         self.cfg = make_config(model, max_batch, max_pos, max_pages, route_rule, threshold,
-                               fixed_depth, max_prefill_tokens, decode_graph, dense_decode)
+                               fixed_depth, max_prefill_tokens, decode_graph, dense_decode, prefill_act_bf16)
         sdt = torch.bfloat16 if model.dtype == "bf16" else torch.float32
 
         def dev(a, dt):

@@ -30,14 +30,14 @@ def run_gpu(model: synth.ModelConfig, weights: Dict, prompts: np.ndarray, steps:
             route_rule: str = "argmax", threshold: float = 0.5, fixed_depth: int = 1,
             all_logits: bool = False, max_pos: Optional[int] = None, max_pages: Optional[int] = None,
             max_prefill_tokens: int = 65536, keep_logits_rows: Optional[Sequence[int]] = None,
-            decode_graph: bool = True, dense_decode: bool = False) -> GpuRun:
+            decode_graph: bool = True, dense_decode: bool = False, prefill_act_bf16: bool = False) -> GpuRun:
     import torch
     from paper_2609_15160_amd import tlf
     B, T = prompts.shape
     sess = tlf.Session(model, weights, max_batch=B, max_pos=max_pos or (T + steps), max_pages=max_pages,
                        route_rule=route_rule, threshold=threshold, fixed_depth=fixed_depth,
                        max_prefill_tokens=max_prefill_tokens, decode_graph=decode_graph,
-                       dense_decode=dense_decode)
+                       dense_decode=dense_decode, prefill_act_bf16=prefill_act_bf16)
     rows = slice(None) if keep_logits_rows is None else list(keep_logits_rows)
     try:
         toks = torch.from_numpy(prompts.astype(np.int32)).cuda()

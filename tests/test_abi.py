@@ -80,6 +80,7 @@ _BAD, _UNS = tlf.E_INVALID_ARG, tlf.E_UNSUPPORTED
     ("max_loops", 0, _BAD), ("max_pos", 0, _BAD), ("max_batch", 0, _BAD), ("max_pages", 0, _BAD),
     ("max_prefill_tokens", 0, _BAD), ("route_rule", 5, _BAD), ("rms_eps", 0.0, _BAD),
     ("router_hidden", -64, _BAD), ("dense_decode", 2, _BAD), ("adaln", 2, _BAD), ("dense_decode", -1, _BAD),
+    ("prefill_act_bf16", 2, _BAD), ("prefill_act_bf16", -1, _BAD),
     # well-formed, outside this build's kernels
     ("d_ff", 1000, _UNS), ("n_layers", 9, _UNS), ("max_loops", 17, _UNS), ("max_batch", 5000, _UNS),
     ("page_tokens", 32, _UNS), ("router_hidden", 96, _UNS), ("router_hidden", 8192, _UNS),

@@ -385,18 +385,48 @@ def test_bf16_d768_b256x2048_sampled_sequences():
 @pytest.mark.timeout(900)
 def test_bf16_d1024_prefill_b8x4096_sampled_sequences():
     """The prefill workload's own shape (d 1024, 16 x 64 heads, SwiGLU 2816,
-    R 8, J 2) at batch 8 x 4096 in one 32768-row group, as the benchmark runs
-    it (Section 3.3 batched prefill, Eq. 6-7, 10-11): every token's depth, every
-    cache index, the last-position logits of two sequences against the oracle,
-    then three decode steps."""
+    R 8, J 2) at batch 8 x 4096 in one 32768-row group, with the activations
+    entering the prefill's matrix products as one bf16 part, as the benchmark
+    runs it (Section 3.3 batched prefill, Eq. 6-7, 10-11): every token's depth,
+    every cache index, the last-position logits of two sequences against the
+    oracle, then three decode steps."""
     m = synth.CONFIGS["bf16_d1024_prefill_b8x4096"].replace(steps=3)
     w = synth.make_weights(m)
     prompts = synth.make_prompts(m)
     sample = [0, 7]
     g = parity.run_gpu(m, w, prompts, m.steps, max_pos=m.max_pos, keep_logits_rows=sample,
-                       max_prefill_tokens=m.batch * m.prompt_len)
+                       max_prefill_tokens=m.batch * m.prompt_len, prefill_act_bf16=True)
     o = parity.run_oracle(m, w, prompts[sample], [t[sample] for t in g.step_tokens], threads=2)
     _check_bf16(m, w, prompts, g, o, sample, "bf16_d1024_prefill_b8x4096")
+
+
+def test_bf16_prefill_single_part_activations_d768():
+    """The one-part bf16 prefill activations on the 2x768 model: three
+    sequences of 300 tokens (the many-row prefill GEMM and attention), all
+    positions' logits and eight decode steps against the oracle."""
+    full = synth.CONFIGS["bf16_d768_b32x512"]
+    m = full.replace(batch=3, prompt_len=300, steps=8)
+    w = synth.make_weights(full)
+    prompts = synth.make_prompts(m)
+    sample = [0, 2]
+    g = parity.run_gpu(m, w, prompts, m.steps, max_pos=m.max_pos, keep_logits_rows=sample, prefill_act_bf16=True)
+    o = parity.run_oracle(m, w, prompts[sample], [t[sample] for t in g.step_tokens])
+    _check_bf16(m, w, prompts, g, o, sample, "bf16-prefill-one-part-d768")
+
+
+def test_bf16_prefill_single_part_ragged_wide_tiles():
+    """One-part bf16 prefill activations on a model whose widths leave ragged
+    256-column tiles (d 640 = 5 x 128 heads, QKV 1920 columns, SwiGLU 1664)
+    with 4 x 1100 rows, enough for the 256 x 256 GEMM tiles; all sequences'
+    last-position logits and four decode steps against the oracle."""
+    m = synth.ModelConfig("bf16-d640", "bf16", vocab=5000, d_model=640, n_heads=5, head_dim=128, d_ff=1664,
+                          n_layers=2, max_loops=6, batch=4, prompt_len=1100, steps=4, router_bias="calibrated")
+    w = synth.make_weights(m)
+    prompts = synth.make_prompts(m)
+    sample = [0, 1, 2, 3]
+    g = parity.run_gpu(m, w, prompts, m.steps, max_pos=m.max_pos, keep_logits_rows=sample, prefill_act_bf16=True)
+    o = parity.run_oracle(m, w, prompts[sample], [t[sample] for t in g.step_tokens], threads=4)
+    _check_bf16(m, w, prompts, g, o, sample, "bf16-prefill-one-part-d640")
 
 
 def test_bf16_d2048_heads_of_128_small_batch():
