@@ -52,7 +52,7 @@ bool make_layout(const tlf_config& c, Layout* L) {
   sz[B_DEPTH_HIST] = R * 8;
   sz[B_STEP_STATS] = kStatCount * 8;
   sz[B_X_DEC] = B * d * 4;
-  sz[B_XC_DEC] = B * d * 4;
+  sz[B_XC_DEC] = (int64_t)((B + 15) / 16 * 16) * d * 4;  // whole groups of 16 rows (fragment order)
   sz[B_KVSLOT] = R * B * 8;
   sz[B_DEPTH_DEC] = B * 4;
   sz[B_PERM] = B * 4;
@@ -466,6 +466,11 @@ int run_decode(tlf_ctx* ctx, hipStream_t s, const int32_t* tokens, float* logits
   // dense decode: rows are in batch order and a row's result is kept while its
   // token's depth exceeds the loop index
   const int32_t* keep_depth = c.dense_decode ? ctx->buf<int32_t>(B_DEPTH_DEC) : nullptr;
+  // bf16 models keep the step's compact residual xc in MFMA fragment order
+  // (element (R, k) at frag_index(R, k, d)): the QKV and gate/up projections
+  // and the LM head load whole fragments, the O and down epilogues update it
+  // in place; float32 fragments hold one element per lane and keep rows
+  const bool xfrag = c.dtype == TLF_DTYPE_BF16;
 
   // the block region (every loop and layer) is timed as a whole when profiling;
   // the attention launches inside it get their own event pairs
@@ -486,6 +491,7 @@ int run_decode(tlf_ctx* ctx, hipStream_t s, const int32_t* tokens, float* logits
       GemmArgs q;  // q, k, v of RMSNorm(x); k, v appended to cache (b, i) of layer j
       const bool first = i == 0 && j == 0;  // reads x through perm and writes xc
       q.A = first ? x : xc; q.lda = d; q.a_copy = first ? xc : nullptr; q.W = lw.w_qkv; q.Wf = ctx->wfrag(j, 0); q.N = 3 * d; q.K = d; q.w_rows = 3 * d; q.rm = rm;
+      q.copy_frag = first && xfrag; q.a_frag = !first && xfrag;
       q.out = ctx->buf<float>(B_Q_DEC); q.ldo = d; q.d = d; q.eps = c.rms_eps;
       q.kv.c = ctx->cv; q.kv.loop = i; q.kv.layer = j; q.kv.prefill = 0; q.kv.slot_base = kv_slot + (int64_t)i * B;
       q.spec = i == 0;
@@ -512,14 +518,14 @@ int run_decode(tlf_ctx* ctx, hipStream_t s, const int32_t* tokens, float* logits
       GemmArgs o;  // x += o W_o^T
       o.A = ctx->buf<float>(B_O_DEC); o.lda = d; o.W = lw.w_o; o.Wf = ctx->wfrag(j, 1); o.N = d; o.K = d; o.w_rows = d; o.rm = rm;
       o.a_frag = 1;
-      o.out = xc; o.ldo = d; o.spec = i == 0; o.keep_depth = keep_depth; o.keep_loop = i;
+      o.out = xc; o.ldo = d; o.spec = i == 0; o.keep_depth = keep_depth; o.keep_loop = i; o.out_frag = xfrag;
       set_mod(ctx, &o, i, j, 0, pa.row_depth, 0);
       TLF_HIP(launch_dgemm<T>(o, A_CMP, E_RESID, false, ctx->cus, s));
 
       GemmArgs gu;  // act = silu(RMSNorm(x) W_g^T) * (RMSNorm(x) W_u^T)
       gu.A = xc; gu.lda = d; gu.W = lw.w_gate_up; gu.Wf = ctx->wfrag(j, 2); gu.N = 2 * F; gu.K = d; gu.w_rows = 2 * F; gu.rm = rm;
       gu.out = ctx->buf<float>(B_ACT_DEC); gu.ldo = F; gu.F = F; gu.eps = c.rms_eps; gu.spec = i == 0;
-      gu.out_frag = 1;
+      gu.out_frag = 1; gu.a_frag = xfrag;
       set_mod(ctx, &gu, i, j, 3, pa.row_depth, 0);
       TLF_HIP(launch_dgemm<T>(gu, A_CMP, E_SWIGLU, true, ctx->cus, s));
 
@@ -527,6 +533,7 @@ int run_decode(tlf_ctx* ctx, hipStream_t s, const int32_t* tokens, float* logits
       dn.A = ctx->buf<float>(B_ACT_DEC); dn.lda = F; dn.W = lw.w_down; dn.Wf = ctx->wfrag(j, 3); dn.N = d; dn.K = F; dn.w_rows = d;
       dn.a_frag = 1;
       dn.rm = rm; dn.out = xc; dn.ldo = d; dn.spec = i == 0; dn.keep_depth = keep_depth; dn.keep_loop = i;
+      dn.out_frag = xfrag;
       set_mod(ctx, &dn, i, j, 1, pa.row_depth, 0);
       TLF_HIP(launch_dgemm<T>(dn, A_CMP, E_RESID, false, ctx->cus, s));
     }
@@ -540,6 +547,7 @@ int run_decode(tlf_ctx* ctx, hipStream_t s, const int32_t* tokens, float* logits
   GemmArgs hd;
   hd.A = xc; hd.lda = d; hd.W = head_weights(ctx); hd.N = c.vocab; hd.K = d; hd.w_rows = c.vocab;
   hd.rm.src = perm; hd.rm.rows = B; hd.out = logits; hd.ldo = c.vocab; hd.eps = c.rms_eps; hd.spec = 1;
+  hd.a_frag = xfrag;
   hd.argmax_keys = ctx->buf<unsigned long long>(B_KEYS);
   hd.key_groups = (int)ceil_div(c.vocab, kWave);
   // a large batch makes the head a real GEMM (128 x 128 tiles read each

@@ -147,7 +147,7 @@ __device__ __forceinline__ void dgemm_tile(const GemmArgs& g, int nact, int act_
       const int e = tid + k * NT, row = e / BN, n = n0 + e % BN;
       const bool ok = e < EOUT && r0 + row < a_rows && n < g.N;
       xrow[k] = ok && g.scatter ? row_src(g.rm, r0 + row) : r0 + row;
-      xr[k] = ok ? g.out[(int64_t)xrow[k] * g.ldo + n] : 0.f;
+      xr[k] = ok ? g.out[g.out_frag ? frag_index<T>(xrow[k], n, g.N) : (int64_t)xrow[k] * g.ldo + n] : 0.f;
     }
   }
   const float* Ab = g.A;
@@ -232,7 +232,8 @@ __device__ __forceinline__ void dgemm_tile(const GemmArgs& g, int nact, int act_
           // the compact copy of the operand rows (first projection of a step)
           const int r = r0 + i * 16 + c16;
           if (r < g.rm.rows) {
-            float* dst = g.a_copy + (int64_t)r * g.lda + k0 + quad * EPL;
+            float* dst = g.a_copy + (g.copy_frag ? frag_index<T>(r, k0 + quad * EPL, g.K)
+                                                  : (int64_t)r * g.lda + k0 + quad * EPL);
 #pragma unroll
             for (int e = 0; e < EPL; ++e) dst[e] = av[j][i][e];
           }
@@ -364,7 +365,7 @@ __device__ __forceinline__ void dgemm_tile(const GemmArgs& g, int nact, int act_
       if constexpr (EK == E_RESID) {
         if (sh.keep[row]) {
           const float gate = g.mod_a ? 1.f + g.mod_a[sh.moff[row] + n] : 1.f;
-          g.out[(int64_t)xrow[k] * g.ldo + n] = xr[k] + gate * v;
+          g.out[g.out_frag ? frag_index<T>(xrow[k], n, g.N) : (int64_t)xrow[k] * g.ldo + n] = xr[k] + gate * v;
         }
       } else if constexpr (EK == E_HIDDEN) {
         const float u = v + g.bias[n];
@@ -468,8 +469,10 @@ hipError_t launch_w(const GemmArgs& a, int cus, hipStream_t s) {
 template <typename T>
 hipError_t launch_dgemm(const GemmArgs& a, AKind ak, EKind ek, bool norm, int cus, hipStream_t s) {
   if (a.K % Mfma<T>::KS != 0 || a.rm.rows <= 0 || cus <= 0) return hipErrorInvalidValue;
-  if (a.a_frag && (ak != A_CMP || norm || a.mod_g || a.a_copy)) return hipErrorInvalidValue;
-  if (a.out_frag && (ek != E_SWIGLU || a.F % Mfma<T>::KS != 0)) return hipErrorInvalidValue;
+  if (a.a_frag && (ak != A_CMP || a.a_copy)) return hipErrorInvalidValue;
+  if (a.copy_frag && !a.a_copy) return hipErrorInvalidValue;
+  if (a.out_frag && !((ek == E_SWIGLU && a.F % Mfma<T>::KS == 0) || (ek == E_RESID && !a.scatter)))
+    return hipErrorInvalidValue;
   const bool mod = a.mod_g != nullptr;
   if (ek == E_QKV && norm) {
     if (ak == A_SRC)

@@ -154,7 +154,9 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs g) {
       float4 v = make_float4(0.f, 0.f, 0.f, 0.f), gm = v;
       if (s >= 0) {
         const int64_t ar = (AK == A_SRC) ? (int64_t)s : (int64_t)(r0 + row);
-        v = *reinterpret_cast<const float4*>(A + ar * g.lda + kk + col);
+        // fragment order (bf16 MFMA): the four floats lie in one run of EPL = 8
+        v = *reinterpret_cast<const float4*>(A + (g.a_frag ? frag_index<T>((int)ar, kk + col, g.K)
+                                                            : ar * g.lda + kk + col));
         if constexpr (MOD) gm = *reinterpret_cast<const float4*>(g.mod_g + row_mod_s[row] + kk + col);
       }
       ra[c] = v;
@@ -491,6 +493,8 @@ hipError_t launch_tiles(const GemmArgs& a, AKind ak, EKind ek, bool norm, hipStr
 template <typename T>
 hipError_t launch_gemm(const GemmArgs& a, AKind ak, EKind ek, bool norm, hipStream_t s) {
   if (a.K % kGemmBK != 0) return hipErrorInvalidValue;
+  // float A in fragment order: bf16 weights (8 consecutive k per run), compact rows
+  if (a.a_frag && (sizeof(T) != 2 || ak != A_CMP || a.A16)) return hipErrorInvalidValue;
   // the QKV epilogue takes each 16-column tile as wholly q, k or v
   if (ek == E_QKV && (a.d % 16 != 0 || a.ldo % 4 != 0 || a.kv.c.D % 16 != 0)) return hipErrorInvalidValue;
   // the residual and SwiGLU epilogues write four consecutive columns at once

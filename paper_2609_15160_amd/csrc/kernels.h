@@ -77,12 +77,13 @@ struct GemmArgs {
   // launch_dgemm: activations in MFMA fragment order.  For rows R and
   // columns k of a [rows][K] operand, element (R, k) sits at
   //   ((R / 16 * (K / KS) + k / KS) * 64 + (k % KS) / EPL * 16 + R % 16) * EPL + k % EPL
-  // (KS, EPL of the model dtype's MFMA), so the 64 lanes' fragments of one
-  // K step of 16 rows are one contiguous run.  a_frag: A is stored so (A_CMP,
-  // no norm, no a_copy); out_frag: an E_SWIGLU epilogue writes act so (K = F).
-  // Buffers hold whole groups of 16 rows.
+  // (KS, EPL of the model dtype's MFMA; frag_index below), so the 64 lanes'
+  // fragments of one K step of 16 rows are one contiguous run.  a_frag: A is
+  // stored so (A_CMP).  Buffers hold whole groups of 16 rows.
   int a_frag = 0;
-  int out_frag = 0;
+  int out_frag = 0;         // E_SWIGLU: act in fragment order (K = F); E_RESID: the residual rows in
+                            // fragment order (K = N), no scatter
+  int copy_frag = 0;        // a_copy is written in fragment order (K = K)
   int N = 0;                // output columns (E_SWIGLU: 2F in the interleaved gate/up space)
   int K = 0;
   int w_rows = 0;           // rows of W (loads are clamped below it)
@@ -115,6 +116,12 @@ struct GemmArgs {
                               // A (no norm, no operand modulation)
   bf16* out16 = nullptr;      // launch_gemm E_SWIGLU: act rows written as bf16 instead of float
 };
+
+// Offset of element (R, k) of a [rows][K] operand stored in MFMA fragment order.
+template <typename T> __device__ __forceinline__ int64_t frag_index(int R, int k, int K) {
+  constexpr int KS = Mfma<T>::KS, EPL = Mfma<T>::EPL;
+  return ((int64_t)((R >> 4) * (K / KS) + k / KS) * kWave + (k % KS) / EPL * 16 + (R & 15)) * EPL + k % EPL;
+}
 
 // Many-row projections (prefill, and the decode LM head of a large batch):
 // 128 x 128 MFMA tiles staged through LDS.  norm: A is the residual x and the
