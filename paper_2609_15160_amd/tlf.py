@@ -18,6 +18,7 @@ HEADER = os.path.join(os.path.dirname(PKG_DIR), "include", "tlf.h")
 ABI_VERSION = 5
 MAX_LOOPS = 16
 MAX_LAYERS = 8
+MAX_BATCH = 4096
 PAGE_TOKENS = 16
 
 OK = 0

@@ -70,7 +70,8 @@ class ScheduleRun:
 
 def run_gpu_schedule(model: synth.ModelConfig, weights: Dict, tokens: np.ndarray, schedule,
                      route_rule: str = "argmax", threshold: float = 0.5, fixed_depth: int = 1,
-                     max_prefill_tokens: int = 65536, decode_graph: bool = True) -> ScheduleRun:
+                     max_prefill_tokens: int = 65536, decode_graph: bool = True,
+                     prefill_act_bf16: bool = False) -> ScheduleRun:
     """Feeds the columns of tokens [B][L] left to right as the schedule says:
     ("prefill", n) prefills the next n tokens (the first item starts the batch,
     later ones append chunks to it) and ("decode", n) runs n decode steps, each
@@ -80,7 +81,7 @@ def run_gpu_schedule(model: synth.ModelConfig, weights: Dict, tokens: np.ndarray
     B, L = tokens.shape
     sess = tlf.Session(model, weights, max_batch=B, max_pos=L, route_rule=route_rule, threshold=threshold,
                        fixed_depth=fixed_depth, max_prefill_tokens=max_prefill_tokens,
-                       decode_graph=decode_graph)
+                       decode_graph=decode_graph, prefill_act_bf16=prefill_act_bf16)
     try:
         toks = torch.from_numpy(tokens.astype(np.int32)).cuda()
         logits = np.zeros((B, L, model.vocab), np.float32)

@@ -213,7 +213,8 @@ def test_binding_constants_match_the_header():
              "PROFILE_OFF": tlf.PROFILE_OFF, "PROFILE_ATTN": tlf.PROFILE_ATTN,
              "PROFILE_BLOCK": tlf.PROFILE_BLOCK, "GS_PLAN_CHUNK_ROWS": tlf.GS_PLAN_CHUNK_ROWS,
              "GS_PLAN_MAX_ROWS": tlf.GS_PLAN_MAX_ROWS, "GS_PLAN_NOALLOC_MAX_ROWS": tlf.GS_PLAN_NOALLOC_MAX_ROWS,
-             "PROBE_READ_GRAIN": tlf.PROBE_READ_GRAIN}
+             "PROBE_READ_GRAIN": tlf.PROBE_READ_GRAIN, "MAX_BATCH": tlf.MAX_BATCH, "MAX_LOOPS": tlf.MAX_LOOPS,
+             "MAX_LAYERS": tlf.MAX_LAYERS, "PAGE_TOKENS": tlf.PAGE_TOKENS}
     for name, value in pairs.items():
         assert defs[name] == value, name
 

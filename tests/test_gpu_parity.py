@@ -509,21 +509,25 @@ def test_f32_chunked_prefill_in_sequence_groups():
     assert err <= F32_TOL
 
 
-@pytest.mark.parametrize("batch", [3, 1])
-def test_bf16_chunked_prefill_equals_one_shot(batch):
+@pytest.mark.parametrize("batch,one_part", [(3, False), (1, False), (3, True)])
+def test_bf16_chunked_prefill_equals_one_shot(batch, one_part):
+    """Appended chunks and decode steps against one oracle prefill; with
+    one_part the multi-sequence chunks feed their activations as one bf16
+    part (queries attending over cache entries of earlier chunks)."""
     m = synth.CONFIGS["bf16_d768_b32x512"].replace(batch=batch)
     w = synth.make_weights(synth.CONFIGS["bf16_d768_b32x512"])
     sched = [("prefill", 100), ("prefill", 29), ("prefill", 200), ("decode", 4), ("prefill", 33)]
     L = _schedule_len(sched)
     tokens = synth.make_prompts(m, prompt_len=L)
-    g = parity.run_gpu_schedule(m, w, tokens, sched)
+    g = parity.run_gpu_schedule(m, w, tokens, sched, prefill_act_bf16=one_part)
     o = _oracle_one_shot(m, w, tokens)
     B = tokens.shape[0]
     pos = np.broadcast_to(np.arange(L), (B, L))
     od, om = parity.router_decisions(m, w, tokens.ravel(), pos.ravel())
     bad, flips = parity.depth_agreement(g.depths.ravel(), od, om, BF16_MARGIN)
     err = _max_err(g.logits, o.prefill_logits)
-    _report(f"bf16-chunked-B{batch}", max_abs_logit_err=f"{err:.3g}", flip_rate=flips, depth_hist=g.stats["depth_hist"])
+    _report(f"bf16-chunked-B{batch}{'-one-part' if one_part else ''}", max_abs_logit_err=f"{err:.3g}",
+            flip_rate=flips, depth_hist=g.stats["depth_hist"])
     assert bad == 0
     for b in range(B):
         for i in range(m.max_loops):
@@ -592,6 +596,20 @@ def test_f32_adaln_chunked_prefill_equals_one_shot():
     assert err <= F32_TOL
 
 
+def test_bf16_adaln_prefill_single_part():
+    """AdaLN with one-part bf16 prefill activations: the QKV and gate/up rows
+    carry the (1 + gamma) scale, so they are rounded in LDS from the float
+    rows; O and down read bf16 rows and gate with (1 + alpha)."""
+    base = synth.CONFIGS["bf16_d768_b32x512"].replace(adaln=True)
+    m = base.replace(batch=4, prompt_len=200, steps=6)
+    w = synth.make_weights(base)
+    prompts = synth.make_prompts(m)
+    sample = [0, 3]
+    g = parity.run_gpu(m, w, prompts, m.steps, max_pos=m.max_pos, keep_logits_rows=sample, prefill_act_bf16=True)
+    o = parity.run_oracle(m, w, prompts[sample], [t[sample] for t in g.step_tokens])
+    _check_bf16(m, w, prompts, g, o, sample, "bf16-adaln-one-part")
+
+
 @pytest.mark.parametrize("batch", [8, 1])
 def test_bf16_adaln_sampled_sequences(batch):
     base = synth.CONFIGS["bf16_d768_b32x512"].replace(adaln=True)
@@ -602,6 +620,58 @@ def test_bf16_adaln_sampled_sequences(batch):
     g = parity.run_gpu(m, w, prompts, m.steps, max_pos=m.max_pos, keep_logits_rows=sample)
     o = parity.run_oracle(m, w, prompts[sample], [t[sample] for t in g.step_tokens])
     _check_bf16(m, w, prompts, g, o, sample, f"bf16-adaln-B{batch}")
+
+
+# ---------------------------------------------------------------------------
+# Maximum sizes
+# ---------------------------------------------------------------------------
+
+def test_f32_max_batch():
+    """TLF_MAX_BATCH = 4096 sequences: the decode planner's four chunks of
+    sequences, the many-row LM head; every sequence's depths and cache index,
+    three sampled sequences against the oracle."""
+    from paper_2609_15160_amd import tlf
+    m = _f32_small(batch=tlf.MAX_BATCH, prompt_len=5, steps=3, vocab=300)
+    w = synth.make_weights(m)
+    prompts = synth.make_prompts(m)
+    sample = [0, 2047, tlf.MAX_BATCH - 1]
+    g = parity.run_gpu(m, w, prompts, m.steps, keep_logits_rows=sample)
+    o = parity.run_oracle(m, w, prompts[sample], [t[sample] for t in g.step_tokens])
+    assert np.array_equal(g.prefill_depths[sample], o.prefill_depths)
+    for s in range(m.steps):
+        assert np.array_equal(g.step_depths[s][sample], o.step_depths[s]), s
+        assert np.array_equal(g.step_next[s][sample], np.argmax(g.step_logits[s], axis=-1))
+    _check_index_matches_depths(g, m.max_loops)
+    err = max([_max_err(g.prefill_logits, o.prefill_logits)] +
+              [_max_err(g.step_logits[s], o.step_logits[s]) for s in range(m.steps)])
+    _report("f32-max-batch", max_abs_logit_err=f"{err:.3g}")
+    assert err <= F32_TOL
+
+
+def test_f32_max_cache_length_properties():
+    """max_pos = 65536, the longest cache whose page list the decode
+    attention stages (4096 pages): a 65528-token prompt and 8 decode steps of
+    the tiny model.  The oracle cannot replay a prefill this long, so the
+    checks are properties that hold at any size: every depth equals the
+    oracle router's (fp32: bit-exact), every cache index equals
+    {t : m_t >= i}, logits are finite and the greedy id is their first
+    argmax."""
+    m = synth.CONFIGS["f32_tiny_b1x32"].replace(prompt_len=65528, steps=8)
+    w = synth.make_weights(m)
+    prompts = synth.make_prompts(m)
+    g = parity.run_gpu(m, w, prompts, m.steps, max_pos=65536)
+    pos = np.arange(m.prompt_len)
+    od, _ = parity.router_decisions(m, w, prompts[0], pos)
+    assert np.array_equal(g.prefill_depths[0], od)
+    for s in range(m.steps):
+        sd, _ = parity.router_decisions(m, w, g.step_tokens[s], np.array([m.prompt_len + s]))
+        assert np.array_equal(g.step_depths[s], sd), s
+        assert np.all(np.isfinite(g.step_logits[s]))
+        assert np.array_equal(g.step_next[s], np.argmax(g.step_logits[s], axis=-1))
+    _check_index_matches_depths(g, m.max_loops)
+    assert np.all(np.isfinite(g.prefill_logits))
+    assert g.stats["seq_len"] == 65536
+    _report("f32-max-cache", depth_hist=g.stats["depth_hist"])
 
 
 # ---------------------------------------------------------------------------

@@ -67,6 +67,26 @@ def test_noalloc_plan_equals_workspace_plan(order):
         print(f"[noalloc] batch={batch} seq_len={seq_len} loop={loop} active={b[0]}", flush=True)
 
 
+def test_noalloc_plan_at_its_row_limit():
+    """TLF_GS_PLAN_NOALLOC_MAX_ROWS rows (4096 chunks, the whole fixed
+    scratch), then a small call: both against tlf_gs_plan_ws and the oracle."""
+    from paper_2609_15160_amd import tlf
+    lib = tlf.load()
+    for batch, seq_len, loop in [(2048, tlf.GS_PLAN_NOALLOC_MAX_ROWS // 2048, 2), (1, 3000, 1)]:
+        rows = batch * seq_len
+        m = synth.make_train_depths(rows, 8, seed=11 + loop)
+        depth = torch.from_numpy(m).cuda()
+        ws = torch.empty(tlf.gs_plan_ws_bytes(rows), dtype=torch.uint8, device="cuda")
+        a = _run(lib, "ws", depth, batch, seq_len, loop, ws)
+        b = _run(lib, "noalloc", depth, batch, seq_len, loop)
+        assert a[0] == b[0] == O.active_rows(m, loop).shape[0]
+        for x, y in zip(a[1:], b[1:]):
+            assert np.array_equal(x, y)
+        assert np.array_equal(b[1], O.active_rows(m, loop))
+        assert np.array_equal(b[3], O.sequence_offsets(m, seq_len, loop))
+        print(f"[noalloc] rows={rows} loop={loop} active={b[0]}", flush=True)
+
+
 def test_noalloc_plan_empty_and_size_limit():
     from paper_2609_15160_amd import tlf
     lib = tlf.load()
