@@ -625,6 +625,65 @@ def counter_summary(fetch_csv, write_csv, first, count, bench_json, window):
                            f"{wcopy:.1f} KiB WRITE_SIZE"}
 
 
+def mfma_summary(counter_csv):
+    """MFMA activity of the prefill from a rocprofv3 --pmc run of
+    `bench.py --prefill-only` that collected MfmaUtil and MfmaFlopsBF16.
+
+    The run holds two sessions of four prefills each (one warm-up, three
+    timed): activations as one bf16 part, then as hi + lo parts.  A prefill
+    is its embedding kernel with the fill kernels just before it, through its
+    last-position LM head (the last GEMM before the next prefill; the second
+    session's set-up kernels fall outside).  Per session, over its timed prefills and
+    per kernel: the MFMA busy fraction (SQ_VALU_MFMA_BUSY_CYCLES over
+    GRBM_GUI_ACTIVE x SIMDs, averaged with each dispatch's duration as the
+    weight), the bf16 MFMA work executed (MOPS x 512) and its rate over the
+    dispatch durations.  Dispatches run one at a time under counter
+    collection, so durations are those of isolated kernels."""
+    import csv
+    import collections
+    disp = {}
+    for r in csv.DictReader(open(counter_csv)):
+        d = disp.setdefault(int(r["Dispatch_Id"]), {"name": r["Kernel_Name"],
+                                                    "us": (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3})
+        d[r["Counter_Name"]] = float(r["Counter_Value"])
+    rows = [disp[k] for k in sorted(disp)]
+    starts = [i for i, r in enumerate(rows) if "k_embed_route" in r["name"]]
+    if len(starts) != 8:
+        raise SystemExit(f"{counter_csv}: {len(starts)} prefills, expected 8 (two sessions of four)")
+    bounds = starts + [len(rows)]
+
+    def prefill_rows(p):
+        a = bounds[p]
+        while a > 0 and "k_fill" in rows[a - 1]["name"]:
+            a -= 1
+        gemms = [i for i in range(bounds[p], bounds[p + 1]) if "k_gemm" in rows[i]["name"]]
+        return rows[a:gemms[-1] + 1]
+    out = {}
+    for label, first in (("one_part", 1), ("hi_lo_parts", 5)):
+        agg = collections.defaultdict(lambda: {"calls": 0, "us": 0.0, "util_us": 0.0, "flop": 0.0})
+        for p in range(first, first + 3):
+            for r in prefill_rows(p):
+                a = agg[r["name"]]
+                a["calls"] += 1
+                a["us"] += r["us"]
+                a["util_us"] += r.get("MfmaUtil", 0.0) * r["us"]
+                a["flop"] += r.get("MfmaFlopsBF16", 0.0)
+        tot_us = sum(a["us"] for a in agg.values())
+        tot_flop = sum(a["flop"] for a in agg.values())
+        kernels = sorted(agg.items(), key=lambda kv: -kv[1]["us"])
+        out[label] = {
+            "prefills": 3, "ms_per_prefill": tot_us / 3e3,
+            "mfma_busy_pct": sum(a["util_us"] for a in agg.values()) / tot_us,
+            "executed_tflop_per_prefill": tot_flop / 3e12,
+            "executed_tflops": tot_flop / (tot_us * 1e6),
+            "kernels": [{"name": n, "calls": a["calls"] // 3, "ms_per_prefill": a["us"] / 3e3,
+                         "mfma_busy_pct": a["util_us"] / a["us"] if a["us"] else 0.0,
+                         "executed_tflop_per_prefill": a["flop"] / 3e12,
+                         "executed_tflops": a["flop"] / (a["us"] * 1e6) if a["us"] else 0.0}
+                        for n, a in kernels[:10]]}
+    return out
+
+
 def trace_summary(trace_csv, routed_launches, last_dispatches, loops, layers, first_step, last_step):
     """Per-kernel durations from a rocprofv3 kernel trace of this benchmark,
     the decode attention's average over the routed run's event-timed region
@@ -708,9 +767,14 @@ def main():
                     help="summarize rocprofv3 FETCH_SIZE / WRITE_SIZE runs of this benchmark (run with the same "
                          "--warmup/--steps/--profiled-steps; BENCH_JSON is that run's output) and exit")
     ap.add_argument("--no-tiny", action="store_true", help="skip the tiny fp32 model's per-step latency")
+    ap.add_argument("--mfma-summary", metavar="COUNTER_CSV",
+                    help="summarize a rocprofv3 --pmc MfmaUtil MfmaFlopsBF16 run of --prefill-only and exit")
     ap.add_argument("--trace-summary", metavar="TRACE_CSV",
                     help="summarize a rocprofv3 kernel trace of this benchmark's default run and exit")
     args = ap.parse_args()
+    if args.mfma_summary:
+        print(json.dumps(mfma_summary(args.mfma_summary)))
+        return
     if args.trace_summary:
         import synth
         m = synth.CONFIGS[args.config]
