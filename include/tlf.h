@@ -104,8 +104,11 @@ typedef struct tlf_config {
   float route_threshold; /* CUMPROB threshold in (0, 1); the paper uses 0.5 */
   int32_t fixed_depth;   /* FIXED depth in [1, R] */
   float rms_eps;         /* RMSNorm epsilon (> 0) */
-  int32_t decode_graph;  /* 1: each decode step replays a captured HIP graph (captured on the first
-                            step and again whenever the batch or an output pointer changes);
+  int32_t decode_graph;  /* 1: each decode step replays a captured HIP graph; a graph belongs to
+                            the batch and the step's token and output pointers, the graphs of
+                            the last 4 distinct ones are kept (a step whose tokens are the
+                            previous step's next_tokens alternates between two) and a new one
+                            is captured in place of the least recently used;
                             0: kernels are launched one by one */
   int32_t router_hidden; /* 0: linear router z = W_r h0 + b_r; Hr > 0 (<= 4096, multiple of 64): the
                             two-layer MLP router z = W_r silu(W_1 h0 + b_1) + b_r (Section 3.2) */

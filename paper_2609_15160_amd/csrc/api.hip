@@ -181,9 +181,12 @@ struct tlf_ctx {
   int64_t attn_launches = 0;
   double attn_ms = 0.0, block_ms = 0.0;
 
-  // decode-step graph: captured on cap_stream, replayed on stream
+  // decode-step graphs: captured on cap_stream, replayed on stream.  A graph
+  // holds the batch and the step's buffer pointers; the last kGraphs distinct
+  // ones are kept (greedy decode alternates two token buffers, the output of
+  // one step being the input of the next), the least recently used replaced.
+  static constexpr int kGraphs = 4;
   hipStream_t cap_stream = nullptr;
-  hipGraphExec_t graph_exec = nullptr;
   struct GraphKey {
     int batch = -1;
     const void *tokens = nullptr, *logits = nullptr, *next = nullptr, *depths = nullptr, *margin = nullptr;
@@ -191,12 +194,19 @@ struct tlf_ctx {
       return batch == o.batch && tokens == o.tokens && logits == o.logits && next == o.next &&
              depths == o.depths && margin == o.margin;
     }
-  } graph_key;
+  };
+  struct CachedGraph {
+    GraphKey key;
+    hipGraphExec_t exec = nullptr;
+    uint64_t used = 0;  // last use (graph_clock)
+  } graphs[kGraphs];
+  uint64_t graph_clock = 0;
 
   ~tlf_ctx() {
     recycle_events();
     for (hipEvent_t e : event_pool) (void)hipEventDestroy(e);
-    if (graph_exec) (void)hipGraphExecDestroy(graph_exec);
+    for (CachedGraph& g : graphs)
+      if (g.exec) (void)hipGraphExecDestroy(g.exec);
     if (cap_stream) (void)hipStreamDestroy(cap_stream);
   }
   void recycle_events() {
@@ -713,10 +723,17 @@ int tlf_decode_step(tlf_ctx* ctx, const int32_t* d_tokens, float* d_logits, int3
   };
   if (ctx->cfg.decode_graph && !ctx->profiling) {
     const tlf_ctx::GraphKey key{ctx->batch, d_tokens, d_logits, d_next, d_depths, d_margin};
-    if (!ctx->graph_exec || !(key == ctx->graph_key)) {
-      if (ctx->graph_exec) {
-        (void)hipGraphExecDestroy(ctx->graph_exec);
-        ctx->graph_exec = nullptr;
+    tlf_ctx::CachedGraph* g = nullptr;
+    for (tlf_ctx::CachedGraph& c : ctx->graphs)
+      if (c.exec && c.key == key) g = &c;
+    if (!g) {
+      // the free or least recently used entry takes the new graph
+      g = &ctx->graphs[0];
+      for (tlf_ctx::CachedGraph& c : ctx->graphs)
+        if (!c.exec || (g->exec && c.used < g->used)) g = &c;
+      if (g->exec) {
+        (void)hipGraphExecDestroy(g->exec);
+        g->exec = nullptr;
       }
       // nothing runs while capturing; the graph is replayed on the context's stream
       if (hipStreamBeginCapture(ctx->cap_stream, hipStreamCaptureModeThreadLocal) != hipSuccess) {
@@ -731,16 +748,17 @@ int tlf_decode_step(tlf_ctx* ctx, const int32_t* d_tokens, float* d_logits, int3
         ctx->poisoned = true;
         return st != TLF_OK ? st : TLF_E_HIP;
       }
-      const hipError_t ei = hipGraphInstantiate(&ctx->graph_exec, graph, nullptr, nullptr, 0);
+      const hipError_t ei = hipGraphInstantiate(&g->exec, graph, nullptr, nullptr, 0);
       (void)hipGraphDestroy(graph);
       if (ei != hipSuccess) {
-        ctx->graph_exec = nullptr;
+        g->exec = nullptr;
         ctx->poisoned = true;
         return TLF_E_HIP;
       }
-      ctx->graph_key = key;
+      g->key = key;
     }
-    if (hipGraphLaunch(ctx->graph_exec, ctx->stream) != hipSuccess) {
+    g->used = ++ctx->graph_clock;
+    if (hipGraphLaunch(g->exec, ctx->stream) != hipSuccess) {
       ctx->poisoned = true;
       return TLF_E_HIP;
     }

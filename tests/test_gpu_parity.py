@@ -285,6 +285,41 @@ def test_graph_replays_match_eager_launches(name):
             assert np.array_equal(g.stats["index"][b][i], e.stats["index"][b][i])
 
 
+def test_graph_cache_replays_and_evicts():
+    """Greedy decode into two alternating token buffers replays two cached
+    graphs; then five distinct logits buffers in turn make every step replace
+    the least recently used of the four cached graphs, and a return to an
+    earlier buffer set replays it.  Every step equals kernel-by-kernel launches."""
+    import torch
+    from paper_2609_15160_amd import tlf
+    m = _f32_small(steps=24)
+    w = synth.make_weights(m)
+    prompts = synth.make_prompts(m)
+    B, V, steps = prompts.shape[0], m.vocab, 24
+    # buffer set of each step: ping-pong tokens, then logits buffers 0..4 in turn, then set 1 again
+    logit_ids = [0] * 8 + [k % 5 for k in range(12)] + [1, 2, 1, 2]
+
+    def run(graph):
+        sess = tlf.Session(m, w, max_batch=B, max_pos=prompts.shape[1] + steps, decode_graph=graph)
+        try:
+            lg, _ = sess.prefill(torch.from_numpy(prompts.astype(np.int32)).cuda())
+            tok = [torch.argmax(lg, -1).to(torch.int32).contiguous(), torch.empty(B, dtype=torch.int32, device="cuda")]
+            outs = [torch.empty((B, V), dtype=torch.float32, device="cuda") for _ in range(5)]
+            got = []
+            for k in range(steps):
+                out = outs[logit_ids[k]]
+                sess.decode_into(tok[k % 2], out, next_tok=tok[(k + 1) % 2])
+                got.append(out.cpu().numpy().copy())  # a host read between replays
+            assert sess.stats()["status"] == 0
+            return got
+        finally:
+            sess.close()
+
+    g, e = run(True), run(False)
+    for k in range(steps):
+        assert np.array_equal(g[k], e[k]), k
+
+
 def _check_bf16(m, w, prompts, g, o, sample, tag, route_rule="argmax", fixed_depth=None, threshold=0.5):
     """bf16 bar.  Every token's depth (all sequences, prompt and decode steps)
     against the oracle router: decisions with margin > 1e-2 match.  Every
