@@ -47,8 +47,15 @@ constexpr int kPreQW = 16;
 
 __device__ __forceinline__ float4 scale4(float4 v, float s) { return make_float4(v.x * s, v.y * s, v.z * s, v.w * s); }
 
+// 2^x for x <= 0 straight from the transcendental unit (v_exp_f32).  Results
+// below the smallest normal float flush to zero; exp2f would rescale around
+// the instruction to keep them, five instructions instead of one, for
+// softmax weights that are then rounded to bf16 or summed beside a maximum
+// weight of 1, where they make no difference.
+__device__ __forceinline__ float exp2_weight(float x) { return __builtin_amdgcn_exp2f(x); }
+
 __device__ __forceinline__ float merge_scale(float m, float mn) {
-  return m == kNegInf ? 0.f : exp2f(m - mn);
+  return m == kNegInf ? 0.f : exp2_weight(m - mn);
 }
 
 // Sum over aligned groups of G lanes (G = 2, 4, 8, 16, 32) with DPP moves
@@ -166,7 +173,7 @@ __global__ __launch_bounds__(W * 64) void k_attn_decode(AttnDecodeArgs a) {
       for (int p = 0; p < PPI; ++p)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          pr[p][r] = exp2f(sc[p][r] - mx);  // 0 for masked slots
+          pr[p][r] = exp2_weight(sc[p][r] - mx);  // 0 for masked slots
           lsum += pr[p][r];
         }
       // P.V: MFMA mm takes k-slots (page, r) = mm * EPL .. mm * EPL + EPL - 1 of
@@ -437,7 +444,7 @@ __global__ __launch_bounds__(256, 4) void k_attn_prefill(AttnPrefillArgs a) {
         for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
-            const float p = mx == kNegInf ? 0.f : exp2f(s[nt][qn][r] - mx);
+            const float p = mx == kNegInf ? 0.f : exp2_weight(s[nt][qn][r] - mx);
             s[nt][qn][r] = p;
             ps += p;
           }
