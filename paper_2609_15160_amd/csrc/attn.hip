@@ -164,10 +164,15 @@ __global__ __launch_bounds__(W * 64) void k_attn_decode(AttnDecodeArgs a) {
       mx = fmaxf(mx, shfl_xor(mx, 16));
       mx = fmaxf(mx, shfl_xor(mx, 32));
       if (mx == kNegInf) return;  // wave-uniform: nothing valid yet
-      const float alpha = merge_scale(m, mx);
-      lsum *= alpha;
+      if (mx != m) {
+        // wave-uniform (every lane holds the same query's scores): an
+        // unchanged maximum would scale by exactly 1, so the rescale, which
+        // moves the accumulators through VGPRs, runs only when it changes
+        const float alpha = merge_scale(m, mx);
+        lsum *= alpha;
 #pragma unroll
-      for (int dt = 0; dt < DT; ++dt) o[dt] *= alpha;
+        for (int dt = 0; dt < DT; ++dt) o[dt] *= alpha;
+      }
       float pr[PPI][4];
 #pragma unroll
       for (int p = 0; p < PPI; ++p)
