@@ -54,6 +54,20 @@ __device__ __forceinline__ float4 scale4(float4 v, float s) { return make_float4
 // weight of 1, where they make no difference.
 __device__ __forceinline__ float exp2_weight(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// In the decode attention the 16 lanes of a lane row (one quad) hold the
+// scores of the same tokens (q fills all 16 columns of the product): the
+// four rows' values, read as scalars, give a wave-uniform result without a
+// trip through the LDS crossbar.
+__device__ __forceinline__ float lane_read(float v, int l) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
+}
+__device__ __forceinline__ float rows_max(float v) {
+  return fmaxf(fmaxf(lane_read(v, 0), lane_read(v, 16)), fmaxf(lane_read(v, 32), lane_read(v, 48)));
+}
+__device__ __forceinline__ float rows_sum(float v) {  // (row 0 + row 1) + (row 2 + row 3)
+  return (lane_read(v, 0) + lane_read(v, 16)) + (lane_read(v, 32) + lane_read(v, 48));
+}
+
 __device__ __forceinline__ float merge_scale(float m, float mn) {
   return m == kNegInf ? 0.f : exp2_weight(m - mn);
 }
@@ -161,8 +175,7 @@ __global__ __launch_bounds__(W * 64) void k_attn_decode(AttnDecodeArgs a) {
           mx = fmaxf(mx, sc[p][r]);
         }
       }
-      mx = fmaxf(mx, shfl_xor(mx, 16));
-      mx = fmaxf(mx, shfl_xor(mx, 32));
+      mx = rows_max(mx);
       if (mx == kNegInf) return;  // wave-uniform: nothing valid yet
       if (mx != m) {
         // wave-uniform (every lane holds the same query's scores): an
@@ -240,8 +253,7 @@ __global__ __launch_bounds__(W * 64) void k_attn_decode(AttnDecodeArgs a) {
       }
     }
     // the four lane quads hold different tokens: add their softmax sums
-    lsum += shfl_xor(lsum, 16);
-    lsum += shfl_xor(lsum, 32);
+    lsum = rows_sum(lsum);
     if (quad == 0) {
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) s_red[w][2 + dt * 16 + c16] = o[dt][0];
