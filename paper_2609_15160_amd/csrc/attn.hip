@@ -160,6 +160,9 @@ __global__ __launch_bounds__(W * 64) void k_attn_decode(AttnDecodeArgs a) {
       // scores of this lane's tokens: page p, slot 4 * quad + r
       float sc[PPI][4];
       float mx = m;
+      // only a batch that reaches past the wave's pages or the cache's last
+      // token is masked (wave-uniform)
+      const bool edge = pg + PPI > p1 || (pg + PPI) * kPage > L;
 #pragma unroll
       for (int p = 0; p < PPI; ++p) {
         f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -169,9 +172,11 @@ __global__ __launch_bounds__(W * 64) void k_attn_decode(AttnDecodeArgs a) {
           for (int qa = 0; qa < NQ; ++qa) acc = M::mma(bk[p][ks], qf[qa][ks], acc);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const int t = (pg + p) * kPage + 4 * quad + r;
-          const bool ok = (pg + p) < p1 && t < L;
-          sc[p][r] = ok ? acc[r] * a.scale_log2 : kNegInf;
+          sc[p][r] = acc[r] * a.scale_log2;
+          if (edge) {
+            const int t = (pg + p) * kPage + 4 * quad + r;
+            if ((pg + p) >= p1 || t >= L) sc[p][r] = kNegInf;
+          }
           mx = fmaxf(mx, sc[p][r]);
         }
       }
