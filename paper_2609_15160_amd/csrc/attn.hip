@@ -68,6 +68,27 @@ __device__ __forceinline__ float rows_sum(float v) {  // (row 0 + row 1) + (row 
   return (lane_read(v, 0) + lane_read(v, 16)) + (lane_read(v, 32) + lane_read(v, 48));
 }
 
+// Exchanges between lane rows in the VALU instead of the LDS crossbar:
+// v_permlane16_swap / v_permlane32_swap of a value with itself hand every
+// lane its own and its xor-16 (xor-32) partner's value, the lower row's
+// first, so both partners combine the pair in the same order.
+__device__ __forceinline__ float max_xor16(float v) {
+  const auto p = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(p[0]), __uint_as_float(p[1]));
+}
+__device__ __forceinline__ float max_xor32(float v) {
+  const auto p = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(p[0]), __uint_as_float(p[1]));
+}
+__device__ __forceinline__ float sum_xor16(float v) {
+  const auto p = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(p[0]) + __uint_as_float(p[1]);
+}
+__device__ __forceinline__ float sum_xor32(float v) {
+  const auto p = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(p[0]) + __uint_as_float(p[1]);
+}
+
 __device__ __forceinline__ float merge_scale(float m, float mn) {
   return m == kNegInf ? 0.f : exp2_weight(m - mn);
 }
@@ -458,8 +479,7 @@ __global__ __launch_bounds__(256, 4) void k_attn_prefill(AttnPrefillArgs a) {
         for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
           for (int r = 0; r < 4; ++r) mx = fmaxf(mx, s[nt][qn][r]);
-        mx = fmaxf(mx, shfl_xor(mx, 16));
-        mx = fmaxf(mx, shfl_xor(mx, 32));
+        mx = max_xor32(max_xor16(mx));
         const float alpha = merge_scale(mq[qn], mx);
         float ps = 0.f;
 #pragma unroll
@@ -520,8 +540,7 @@ __global__ __launch_bounds__(256, 4) void k_attn_prefill(AttnPrefillArgs a) {
 #pragma unroll
   for (int qn = 0; qn < QN; ++qn) {
     float lt = lq[qn];
-    lt += shfl_xor(lt, 16);
-    lt += shfl_xor(lt, 32);
+    lt = sum_xor32(sum_xor16(lt));
     const int row = q0 + w * QW + qn * 16 + c16;
     if (row >= nq) continue;
     const int64_t oo = ((int64_t)g * a.T + row) * a.d + h * D + 4 * quad;
