@@ -481,12 +481,14 @@ __global__ __launch_bounds__(256, 4) void k_attn_prefill(AttnPrefillArgs a) {
           for (int r = 0; r < 4; ++r) mx = fmaxf(mx, s[nt][qn][r]);
         mx = max_xor32(max_xor16(mx));
         const float alpha = merge_scale(mq[qn], mx);
+        // a column with no key yet (every score -inf) subtracts 0 and gets weights exp2(-inf) = 0
+        const float mxs = mx == kNegInf ? 0.f : mx;
         float ps = 0.f;
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
-            const float p = mx == kNegInf ? 0.f : exp2_weight(s[nt][qn][r] - mx);
+            const float p = exp2_weight(s[nt][qn][r] - mxs);
             s[nt][qn][r] = p;
             ps += p;
           }

@@ -126,18 +126,25 @@ __device__ __forceinline__ unsigned int pack2(bf16 a, bf16 b) {
          ((unsigned int)__builtin_bit_cast(unsigned short, b) << 16);
 }
 
-// Two floats rounded to bf16 (nearest even) in one 32-bit word, lo first.
-__device__ __forceinline__ unsigned int pack_bf16x2(float lo, float hi) { return pack2((bf16)lo, (bf16)hi); }
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
-// Four float32 values as the packed hi and lo bf16 parts (2 words each).
+// Two floats rounded to bf16 (nearest even) in one 32-bit word, lo first:
+// one two-input conversion instruction (converting the halves one by one
+// takes two conversions, a shift and an or).
+__device__ __forceinline__ unsigned int pack_bf16x2(float lo, float hi) {
+  return __builtin_bit_cast(unsigned int, __builtin_convertvector((f32x2){lo, hi}, bf16x2));
+}
+
+// Four float32 values as the packed hi and lo bf16 parts (2 words each):
+// hi = bf16(v), lo = bf16(v - hi), each half of a packed word read back as
+// the float it is the upper 16 bits of.
 __device__ __forceinline__ void split4(float4 v, uint2& hi, uint2& lo) {
-  bf16 h0, l0, h1, l1, h2, l2, h3, l3;
-  split_bf16(v.x, h0, l0);
-  split_bf16(v.y, h1, l1);
-  split_bf16(v.z, h2, l2);
-  split_bf16(v.w, h3, l3);
-  hi = make_uint2(pack2(h0, h1), pack2(h2, h3));
-  lo = make_uint2(pack2(l0, l1), pack2(l2, l3));
+  const unsigned int h01 = pack_bf16x2(v.x, v.y), h23 = pack_bf16x2(v.z, v.w);
+  const float hx = __uint_as_float(h01 << 16), hy = __uint_as_float(h01 & 0xFFFF0000u);
+  const float hz = __uint_as_float(h23 << 16), hw = __uint_as_float(h23 & 0xFFFF0000u);
+  hi = make_uint2(h01, h23);
+  lo = make_uint2(pack_bf16x2(v.x - hx, v.y - hy), pack_bf16x2(v.z - hz, v.w - hw));
 }
 
 // Eight consecutive float32 values as the hi and lo fragments of a bf16 MFMA operand.
