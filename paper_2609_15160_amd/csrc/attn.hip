@@ -326,15 +326,26 @@ __global__ __launch_bounds__(256, 4) void k_attn_prefill(AttnPrefillArgs a) {
   constexpr int KBLK = kPage * D;                 // elements of one page's K (or V) block
   constexpr int EPC = 16 / (int)sizeof(T);        // elements per 16-byte chunk
   constexpr int VLD = kPage + (sizeof(T) == 2 ? 4 : 2);  // padded LDS row of one dimension of a V block
+  // bf16: one row per dimension holding the tile's 64 slots with the pages
+  // paired at 4-slot granularity (slots 4g..4g+3 of page 2m, then those of
+  // page 2m + 1), so that a lane's P.V fragment (its four slots of two
+  // pages) is one 16-byte read; 144-byte rows keep the 8 or 16 lanes of one
+  // LDS pass on distinct banks.  float32: [page][dim] rows of VLD slots.
+  constexpr int VDS = 4 * kPage + 8;
+  constexpr int VTILE = sizeof(T) == 2 ? D * VDS : 4 * D * VLD;
+  auto vidx = [](int p, int d, int slot) {  // element of (page p, dimension d, slot)
+    return sizeof(T) == 2 ? d * VDS + (p >> 1) * 32 + (slot >> 2) * 8 + (p & 1) * 4 + (slot & 3)
+                          : (p * D + d) * VLD + slot;
+  };
   constexpr int CH = 2 * 4 * KBLK / EPC;          // 16-byte chunks of one K + V tile
   static_assert(CH % 256 == 0, "tile chunks per thread");
   constexpr int CPT = CH / 256;
   static_assert(EPC % 4 == 0 && (4 * D) % EPC == 0, "V chunk: whole 4-slot groups of one slot group");
   // K tile: four pages' K blocks verbatim (fragment order: lane (key, quad) of a
   // K step reads EPL contiguous elements, 64 lanes one contiguous run);
-  // V tile: four pages' V blocks rearranged to [dim][slot] rows, padded against bank conflicts
+  // V tile: four pages' V blocks rearranged to rows of one dimension (layout at vidx)
   __shared__ __align__(16) T Ks[2][4 * KBLK];
-  __shared__ __align__(16) T Vs[2][4 * D * VLD];
+  __shared__ __align__(16) T Vs[2][VTILE];
 
   const CacheView& c = a.c;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -415,10 +426,10 @@ __global__ __launch_bounds__(256, 4) void k_attn_prefill(AttnPrefillArgs a) {
         // the chunk holds slots 4 g4 .. 4 g4 + 3 of EPC / 4 consecutive dimensions
         const int g4 = off / (4 * D), d0 = (off % (4 * D)) / 4;
         if constexpr (sizeof(T) == 2) {
-          *reinterpret_cast<uint2*>(&Vs[buf][(p * D + d0) * VLD + 4 * g4]) = make_uint2(pre[u].x, pre[u].y);
-          *reinterpret_cast<uint2*>(&Vs[buf][(p * D + d0 + 1) * VLD + 4 * g4]) = make_uint2(pre[u].z, pre[u].w);
+          *reinterpret_cast<uint2*>(&Vs[buf][vidx(p, d0, 4 * g4)]) = make_uint2(pre[u].x, pre[u].y);
+          *reinterpret_cast<uint2*>(&Vs[buf][vidx(p, d0 + 1, 4 * g4)]) = make_uint2(pre[u].z, pre[u].w);
         } else {
-          T* dst = &Vs[buf][(p * D + d0) * VLD + 4 * g4];
+          T* dst = &Vs[buf][vidx(p, d0, 4 * g4)];
           *reinterpret_cast<uint2*>(dst) = make_uint2(pre[u].x, pre[u].y);
           *reinterpret_cast<uint2*>(dst + 2) = make_uint2(pre[u].z, pre[u].w);
         }
@@ -514,9 +525,7 @@ __global__ __launch_bounds__(256, 4) void k_attn_prefill(AttnPrefillArgs a) {
 #pragma unroll
           for (int dt = 0; dt < DT; ++dt) {
             const int dim = dt * 16 + c16;
-            const uint2 v0 = *reinterpret_cast<const uint2*>(vb + (np * D + dim) * VLD + 4 * quad);
-            const uint2 v1 = *reinterpret_cast<const uint2*>(vb + ((np + 1) * D + dim) * VLD + 4 * quad);
-            const Frag vf = __builtin_bit_cast(Frag, make_uint4(v0.x, v0.y, v1.x, v1.y));
+            const Frag vf = *reinterpret_cast<const Frag*>(vb + vidx(np, dim, 4 * quad));  // pages np, np + 1
 #pragma unroll
             for (int qn = 0; qn < QN; ++qn) o[dt][qn] = M::mma(vf, pf[qn], o[dt][qn]);
           }
@@ -528,7 +537,7 @@ __global__ __launch_bounds__(256, 4) void k_attn_prefill(AttnPrefillArgs a) {
           for (int r = 0; r < 4; ++r)  // one key (nt, 4 quad + r) per lane per MFMA
 #pragma unroll
             for (int dt = 0; dt < DT; ++dt) {
-              const Frag vf = vb[(nt * D + dt * 16 + c16) * VLD + 4 * quad + r];
+              const Frag vf = vb[vidx(nt, dt * 16 + c16, 4 * quad + r)];
 #pragma unroll
               for (int qn = 0; qn < QN; ++qn) o[dt][qn] = M::mma(vf, s[nt][qn][r], o[dt][qn]);
             }
