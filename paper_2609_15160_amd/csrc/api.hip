@@ -338,6 +338,10 @@ int run_prefill(tlf_ctx* ctx, int B, int T_, int pos0, const int32_t* tokens, fl
     // GEMMs): RMSNorm(x), o and act are handed on as bf16 rows; the LM head
     // keeps reading the float32 RMSNorm(x)
     const bool one = c.prefill_act_bf16 && c.dtype == TLF_DTYPE_BF16 && !few;
+    // with the normed rows handed on as bf16 and no AdaLN scale to apply to
+    // the float rows, RMSNorm(x) in float32 feeds only the LM head: it is
+    // written once, for the head's rows, after the last loop
+    const bool y32 = !one || c.adaln;
     bf16* y16 = one ? ctx->buf<bf16>(B_Y16_PRE) : nullptr;
     bf16* o16 = one ? ctx->buf<bf16>(B_O_PRE) : nullptr;
     bf16* act16 = one ? ctx->buf<bf16>(B_ACT_PRE) : nullptr;
@@ -345,7 +349,7 @@ int run_prefill(tlf_ctx* ctx, int B, int T_, int pos0, const int32_t* tokens, fl
     ea.tok_emb = ctx->w.tok_emb; ea.pos_emb = ctx->w.pos_emb; ea.Wr = ctx->w.router_w; ea.br = ctx->w.router_b;
     ea.tokens = tokens + (int64_t)b0 * T_;
     ea.rows = rows; ea.V = c.vocab; ea.d = d; ea.R = R; ea.prefill_T = T_; ea.pos0 = pos0;
-    ea.x = x; ea.y = few ? nullptr : y; ea.y16 = y16; ea.eps = c.rms_eps; ea.depth = ctx->buf<int32_t>(B_DEPTH_PRE);
+    ea.x = x; ea.y = few || !y32 ? nullptr : y; ea.y16 = y16; ea.eps = c.rms_eps; ea.depth = ctx->buf<int32_t>(B_DEPTH_PRE);
     ea.out_depth = depths ? depths + (int64_t)b0 * T_ : nullptr;
     ea.rule = c.route_rule; ea.threshold = c.route_threshold; ea.fixed = c.fixed_depth;
     ea.err = ctx->cv.err;
@@ -372,7 +376,7 @@ int run_prefill(tlf_ctx* ctx, int B, int T_, int pos0, const int32_t* tokens, fl
       rm.seg = T_; rm.seg_cnt_stride = R; rm.rows = rows;
       if (few) rm.nact = rm.seg_cnt;  // one segment: rows [0, n) active
       ResidNormArgs rn;
-      rn.rm = rm; rn.x = x; rn.y = y; rn.y16 = y16; rn.d = d; rn.eps = c.rms_eps;
+      rn.rm = rm; rn.x = x; rn.y = y32 ? y : nullptr; rn.y16 = y16; rn.d = d; rn.eps = c.rms_eps;
       for (int j = 0; j < c.n_layers; ++j) {
         const tlf_layer_weights& lw = ctx->layers[j];
         GemmArgs q;
@@ -434,6 +438,11 @@ int run_prefill(tlf_ctx* ctx, int B, int T_, int pos0, const int32_t* tokens, fl
     } else {
       hd.rm.rows = Gc; hd.rm.src_stride = T_; hd.rm.src_off = T_ - 1;
       hd.out_row_off = b0;
+    }
+    if (!y32) {
+      ResidNormArgs hn;
+      hn.rm = hd.rm; hn.x = x; hn.y = y; hn.d = d; hn.eps = c.rms_eps;
+      TLF_HIP(launch_resid_norm<T>(hn, s));
     }
     if (few) TLF_HIP(launch_dgemm<T>(hd, A_SRC, E_LOGITS, true, ctx->cus, s));
     else TLF_HIP(launch_gemm<T>(hd, A_SRC, E_LOGITS, false, s));

@@ -199,7 +199,7 @@ hipError_t launch_route_rows(const RouteArgs& a, hipStream_t s);
 struct ResidNormArgs {
   RowMap rm;
   const float* x = nullptr;
-  float* y = nullptr;
+  float* y = nullptr;       // or nullptr
   bf16* y16 = nullptr;      // also RMSNorm(x) rounded to bf16, or nullptr
   int d = 0;
   float eps = 1e-5f;

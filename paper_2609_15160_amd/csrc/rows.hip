@@ -247,11 +247,13 @@ __global__ __launch_bounds__(256) void k_resid_norm(ResidNormArgs a) {
   __syncthreads();
   ss = (s_part[0] + s_part[1]) + (s_part[2] + s_part[3]);
   const float inv = rsqrtf(ss / (float)a.d + a.eps);
-  float* y = a.y + (int64_t)src * a.d;
+  if (a.y) {
+    float* y = a.y + (int64_t)src * a.d;
 #pragma unroll
-  for (int c = 0; c < NC; ++c) {
-    const int k = 4 * tid + 1024 * c;
-    if (k < a.d) V4<float>::store(y + k, scale4(h[c], inv));
+    for (int c = 0; c < NC; ++c) {
+      const int k = 4 * tid + 1024 * c;
+      if (k < a.d) V4<float>::store(y + k, scale4(h[c], inv));
+    }
   }
   if (a.y16) {
     bf16* y16 = a.y16 + (int64_t)src * a.d;
