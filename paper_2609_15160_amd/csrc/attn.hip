@@ -400,38 +400,48 @@ __global__ __launch_bounds__(256, 4) void k_attn_prefill(AttnPrefillArgs a) {
   }
 
   // one K + V tile: chunk ci < CH/2 is K chunk ci, else V chunk ci - CH/2;
-  // pages past the cache read as zeros (their scores are masked)
+  // pages past the cache are stored as zeros (their scores are masked).  A
+  // page block holds a multiple of 64 chunks, so the 64 chunks of one wave
+  // in round u lie in one block: its page and K/V choice are wave-uniform.
+  // The tile's table entries are read first (scalar loads), then every data
+  // load is issued, from the last page where the tile runs past the cache,
+  // so that none waits on another.
+  static_assert((KBLK / EPC) % kWave == 0, "a wave's chunks within one page block");
+  const int wu = __builtin_amdgcn_readfirstlane(w);
+  auto round_page = [&](int u) { return ((wu * kWave + u * 256) % (CH / 2)) / (KBLK / EPC); };
   uint4 pre[CPT];
   auto load_tile = [&](int kt) __attribute__((always_inline)) {
+    int pg[CPT];
+#pragma unroll
+    for (int u = 0; u < CPT; ++u) pg[u] = pt[min(kt * 4 + round_page(u), npages - 1)];
 #pragma unroll
     for (int u = 0; u < CPT; ++u) {
-      const int ci = tid + u * 256;
-      const int kv = ci / (CH / 2), cc = ci % (CH / 2);
-      const int p = cc / (KBLK / EPC), off = (cc % (KBLK / EPC)) * EPC;
-      const int pa = kt * 4 + p;
-      pre[u] = make_uint4(0, 0, 0, 0);
-      if (pa < npages)
-        pre[u] = *reinterpret_cast<const uint4*>(pool + (int64_t)pt[pa] * c.page_elems + (kv ? voff : koff) + off);
+      const int ci0 = wu * kWave + u * 256;  // the wave's first chunk of round u
+      const int kv = ci0 / (CH / 2);
+      const int off = ((ci0 % (CH / 2)) % (KBLK / EPC) + lane) * EPC;
+      pre[u] = *reinterpret_cast<const uint4*>(pool + (int64_t)pg[u] * c.page_elems + (kv ? voff : koff) + off);
     }
   };
-  auto store_tile = [&](int buf) __attribute__((always_inline)) {
+  auto store_tile = [&](int kt, int buf) __attribute__((always_inline)) {
 #pragma unroll
     for (int u = 0; u < CPT; ++u) {
       const int ci = tid + u * 256;
       const int kv = ci / (CH / 2), cc = ci % (CH / 2);
       const int p = cc / (KBLK / EPC), off = (cc % (KBLK / EPC)) * EPC;
+      uint4 v = pre[u];
+      if (kt * 4 + round_page(u) >= npages) v = make_uint4(0, 0, 0, 0);
       if (kv == 0) {
-        *reinterpret_cast<uint4*>(&Ks[buf][p * KBLK + off]) = pre[u];
+        *reinterpret_cast<uint4*>(&Ks[buf][p * KBLK + off]) = v;
       } else {
         // the chunk holds slots 4 g4 .. 4 g4 + 3 of EPC / 4 consecutive dimensions
         const int g4 = off / (4 * D), d0 = (off % (4 * D)) / 4;
         if constexpr (sizeof(T) == 2) {
-          *reinterpret_cast<uint2*>(&Vs[buf][vidx(p, d0, 4 * g4)]) = make_uint2(pre[u].x, pre[u].y);
-          *reinterpret_cast<uint2*>(&Vs[buf][vidx(p, d0 + 1, 4 * g4)]) = make_uint2(pre[u].z, pre[u].w);
+          *reinterpret_cast<uint2*>(&Vs[buf][vidx(p, d0, 4 * g4)]) = make_uint2(v.x, v.y);
+          *reinterpret_cast<uint2*>(&Vs[buf][vidx(p, d0 + 1, 4 * g4)]) = make_uint2(v.z, v.w);
         } else {
           T* dst = &Vs[buf][vidx(p, d0, 4 * g4)];
-          *reinterpret_cast<uint2*>(dst) = make_uint2(pre[u].x, pre[u].y);
-          *reinterpret_cast<uint2*>(dst + 2) = make_uint2(pre[u].z, pre[u].w);
+          *reinterpret_cast<uint2*>(dst) = make_uint2(v.x, v.y);
+          *reinterpret_cast<uint2*>(dst + 2) = make_uint2(v.z, v.w);
         }
       }
     }
@@ -447,7 +457,7 @@ __global__ __launch_bounds__(256, 4) void k_attn_prefill(AttnPrefillArgs a) {
   for (int qn = 0; qn < QN; ++qn) { mq[qn] = kNegInf; lq[qn] = 0.f; }
 
   load_tile(0);
-  store_tile(0);
+  store_tile(0, 0);
   __syncthreads();
   for (int kt = 0; kt < nkt; ++kt) {
     const int buf = kt & 1;
@@ -543,7 +553,7 @@ __global__ __launch_bounds__(256, 4) void k_attn_prefill(AttnPrefillArgs a) {
             }
       }
     }
-    if (kt + 1 < nkt) store_tile(buf ^ 1);
+    if (kt + 1 < nkt) store_tile(kt + 1, buf ^ 1);
     __syncthreads();
   }
   // the four lane quads hold different keys: add their softmax sums, then
