@@ -452,9 +452,17 @@ __global__ __launch_bounds__(256, 4) void k_attn_prefill(AttnPrefillArgs a) {
   for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
     for (int qn = 0; qn < QN; ++qn) o[dt][qn] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float mq[QN], lq[QN];  // running max (per query, replicated over quads) and this lane's sum
+  // Online softmax with a lazily moved base per query (column): the score
+  // products start from -base, so they come out relative to it, and a
+  // tile's weights are exp2 of them directly.  The base is set by the first
+  // key tile (key 0 is visible to every query) and moves up, rescaling the
+  // running sums, only when a lane's weights in a tile add up to more than
+  // kSumMax; weights therefore stay below kSumMax, far inside the range of
+  // float32 sums and bf16 operands, and o / l is unchanged by the choice.
+  constexpr float kSumMax = 65536.f;
+  float nb[QN], lq[QN];  // -base (per query, replicated over quads) and this lane's weight sum
 #pragma unroll
-  for (int qn = 0; qn < QN; ++qn) { mq[qn] = kNegInf; lq[qn] = 0.f; }
+  for (int qn = 0; qn < QN; ++qn) { nb[qn] = 0.f; lq[qn] = 0.f; }
 
   load_tile(0);
   store_tile(0, 0);
@@ -465,59 +473,91 @@ __global__ __launch_bounds__(256, 4) void k_attn_prefill(AttnPrefillArgs a) {
     // the wave's queries see keys <= their compact index: skip tiles past its last query
     if (kt * BKEY <= wq0 + QW - 1) {
       const T* kb = Ks[buf];
-      // S^T tile (nt, qn): lane holds keys nt * 16 + 4 quad + r of query c16
-      f32x4 s[NT][QN];
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-#pragma unroll
-        for (int qn = 0; qn < QN; ++qn) s[nt][qn] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int ks = 0; ks < KSTEPS; ++ks) {
-          const Frag kf = M::load(kb + nt * KBLK + ((ks * 4 + quad) * kPage + c16) * EPL);
-#pragma unroll
-          for (int qn = 0; qn < QN; ++qn)
-#pragma unroll
-            for (int qa = 0; qa < NQ; ++qa) s[nt][qn] = M::mma(kf, qf[qn][qa][ks], s[nt][qn]);
-        }
-      }
-      // online softmax per query (column): mask (only a tile that reaches
-      // past the wave's first query or the cache end), max, rescale
+      // mask only a tile that reaches past the wave's first query or the cache end
       const bool edge = kt * BKEY + BKEY - 1 > wq0 || kt * BKEY + BKEY > n;
+      // S^T tile (nt, qn) less the base: lane holds keys nt * 16 + 4 quad + r of query c16
+      f32x4 s[NT][QN];
+      auto scores = [&]() __attribute__((always_inline)) {
 #pragma unroll
-      for (int qn = 0; qn < QN; ++qn) {
-        const int qidx = wq0 + qn * 16 + c16;
+        for (int nt = 0; nt < NT; ++nt) {
+#pragma unroll
+          for (int qn = 0; qn < QN; ++qn) s[nt][qn] = f32x4{nb[qn], nb[qn], nb[qn], nb[qn]};
+#pragma unroll
+          for (int ks = 0; ks < KSTEPS; ++ks) {
+            const Frag kf = M::load(kb + nt * KBLK + ((ks * 4 + quad) * kPage + c16) * EPL);
+#pragma unroll
+            for (int qn = 0; qn < QN; ++qn)
+#pragma unroll
+              for (int qa = 0; qa < NQ; ++qa) s[nt][qn] = M::mma(kf, qf[qn][qa][ks], s[nt][qn]);
+          }
+        }
         if (edge) {
+#pragma unroll
+          for (int qn = 0; qn < QN; ++qn) {
+            const int qidx = wq0 + qn * 16 + c16;
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+              for (int r = 0; r < 4; ++r) {
+                const int kidx = kt * BKEY + nt * 16 + 4 * quad + r;
+                if (kidx > qidx || kidx >= n) s[nt][qn][r] = kNegInf;
+              }
+          }
+        }
+      };
+      scores();
+      float ps[QN];
+      bool move = kt == 0;
+      if (!move) {
+        bool over = false;
+#pragma unroll
+        for (int qn = 0; qn < QN; ++qn) {
+          ps[qn] = 0.f;
 #pragma unroll
           for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
-              const int kidx = kt * BKEY + nt * 16 + 4 * quad + r;
-              if (kidx > qidx || kidx >= n) s[nt][qn][r] = kNegInf;
+              const float p = exp2_weight(s[nt][qn][r]);
+              s[nt][qn][r] = p;
+              ps[qn] += p;
+            }
+          over |= !(ps[qn] <= kSumMax);
+        }
+        move = __builtin_amdgcn_ballot_w64(over) != 0;
+        if (move) scores();  // rare: the K tile is still in LDS
+      }
+      if (move) {
+        // new base: the column maximum (first tile), else the old base or
+        // the column maximum, whichever is larger
+#pragma unroll
+        for (int qn = 0; qn < QN; ++qn) {
+          float mx = kNegInf;
+#pragma unroll
+          for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) mx = fmaxf(mx, s[nt][qn][r]);
+          mx = max_xor32(max_xor16(mx));
+          const float dlt = kt == 0 ? mx : fmaxf(mx, 0.f);
+          if (kt > 0) {
+            const float alpha = exp2_weight(-dlt);
+            lq[qn] *= alpha;
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt) o[dt][qn] *= alpha;
+          }
+          nb[qn] -= dlt;
+          ps[qn] = 0.f;
+#pragma unroll
+          for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const float p = exp2_weight(s[nt][qn][r] - dlt);
+              s[nt][qn][r] = p;
+              ps[qn] += p;
             }
         }
-        float mx = mq[qn];
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) mx = fmaxf(mx, s[nt][qn][r]);
-        mx = max_xor32(max_xor16(mx));
-        const float alpha = merge_scale(mq[qn], mx);
-        // a column with no key yet (every score -inf) subtracts 0 and gets weights exp2(-inf) = 0
-        const float mxs = mx == kNegInf ? 0.f : mx;
-        float ps = 0.f;
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const float p = exp2_weight(s[nt][qn][r] - mxs);
-            s[nt][qn][r] = p;
-            ps += p;
-          }
-        lq[qn] = lq[qn] * alpha + ps;
-        mq[qn] = mx;
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt) o[dt][qn] *= alpha;
       }
+#pragma unroll
+      for (int qn = 0; qn < QN; ++qn) lq[qn] += ps[qn];
       // O^T += V^T P^T: the k-slots of one MFMA are keys this lane holds
       // scores for, in the same order on both operands
       const T* vb = Vs[buf];
