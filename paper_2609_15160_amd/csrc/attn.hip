@@ -47,11 +47,13 @@ constexpr int kPreQW = 16;
 
 __device__ __forceinline__ float4 scale4(float4 v, float s) { return make_float4(v.x * s, v.y * s, v.z * s, v.w * s); }
 
-// 2^x for x <= 0 straight from the transcendental unit (v_exp_f32).  Results
-// below the smallest normal float flush to zero; exp2f would rescale around
-// the instruction to keep them, five instructions instead of one, for
-// softmax weights that are then rounded to bf16 or summed beside a maximum
-// weight of 1, where they make no difference.
+// 2^x straight from the transcendental unit (v_exp_f32), for softmax
+// weights: x is a score less the running maximum (decode) or less a base
+// that the tile's weights exceed by at most 2^16 (prefill).  Results below
+// the smallest normal float flush to zero; exp2f would rescale around the
+// instruction to keep them, five instructions instead of one, for weights
+// that are then rounded to bf16 or summed beside a weight of at least 1,
+// where they make no difference.
 __device__ __forceinline__ float exp2_weight(float x) { return __builtin_amdgcn_exp2f(x); }
 
 // In the decode attention the 16 lanes of a lane row (one quad) hold the
