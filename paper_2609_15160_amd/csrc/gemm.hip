@@ -61,21 +61,47 @@ template <typename T> __device__ __forceinline__ int swz(int row, int c) {
   else return c ^ (row & 7);
 }
 
+// LDS byte address of a shared-memory pointer
+__device__ __forceinline__ unsigned lds_addr(void* p) {
+  return (unsigned)(uintptr_t)(__attribute__((address_space(3))) void*)p;
+}
+
+// 16 bytes from global memory straight into LDS: the wave's 64 lanes fill 64
+// consecutive 16-byte chunks from byte `lds` (wave-uniform, passed in M0).
+// Written as assembly so that the compiler's wait-count pass, which would
+// otherwise wait for every such load before any later LDS read, leaves the
+// ordering to wait_loads_barrier; it counts toward vmcnt like any load.
+__device__ __forceinline__ void load_lds16(const void* g, unsigned lds) {
+  asm volatile("global_load_lds_dwordx4 %0, off" ::"v"(g), "{m0}"(lds) : "memory");
+}
+
+// Waits until at most N vector-memory loads of this wave are outstanding,
+// then joins the workgroup barrier.  The memory clobber keeps the compiler
+// from moving LDS accesses across it.
+template <int N> __device__ __forceinline__ void wait_loads_barrier() {
+  asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(N) : "memory");
+}
+
 // MOD: the A rows are scaled by (1 + gamma) of their AdaLN modulation rows.
 // NORM: A holds residual rows x and the product is taken with RMSNorm(x): the
 // sum of squares of each row is accumulated from the A chunks as they pass
 // and the output row is scaled by 1 / rms, since (x / rms) W^T = (x W^T) / rms.
 // AMODE (bf16 weights): 0: float A enters the MFMA as hi + lo parts; 1: as
 // one bf16 part (round to nearest even), half the products and LDS traffic;
-// 2: A is read as bf16 rows (g.A16), half the A bytes as well.  Float32
-// weights take float A (AMODE 0).
+// 2: A is read as bf16 rows (g.A16), half the A bytes as well; 3: as 2, with
+// A and W copied into LDS by the loads themselves (global_load_lds: no
+// registers, no LDS stores), through three LDS stages so that two K tiles
+// are in flight while one is multiplied.  Float32 weights take float A
+// (AMODE 0).
 // MT x NT: each wave's 16 x 16 MFMA tiles; BK: K elements per LDS stage.
 template <typename T, int MT, int NT, int BK, int AK, int EK, bool MOD, bool NORM, int AMODE>
 __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs g) {
   constexpr int BM = 2 * MT * 16, BN = 2 * NT * 16;
   constexpr bool kBf16 = sizeof(T) == 2;             // bf16 weights: A converted to bf16 in LDS
   constexpr bool kSplit = kBf16 && AMODE == 0;       // ... as hi + lo parts
-  constexpr bool kA16 = kBf16 && AMODE == 2;         // A already bf16 in memory
+  constexpr bool kA16 = kBf16 && AMODE >= 2;         // A already bf16 in memory
+  constexpr bool kDirect = kBf16 && AMODE == 3;      // ... and copied to LDS by its loads
+  constexpr int NST = kDirect ? 3 : 2;               // LDS stages
   static_assert(!kA16 || (!MOD && !NORM), "bf16 A rows carry no modulation or norm");
   constexpr int NA = kSplit ? 2 : 1;
   constexpr int CE = 16 / (int)sizeof(T);            // storage elements per 16-byte chunk
@@ -89,8 +115,8 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs g) {
   static_assert(BCH >= 1 && BN * WCR % 256 == 0, "B tile split");
   static_assert(BK % KS == 0 && (KS * (int)sizeof(T)) % 16 == 0 || EPL == 1, "K tile");
 
-  __shared__ __align__(16) T As[2][NA][BM * BK];
-  __shared__ __align__(16) T Bs[2][BN * BK];
+  __shared__ __align__(16) T As[NST][NA][BM * BK];
+  __shared__ __align__(16) T Bs[NST][BN * BK];
   __shared__ int row_src_s[BM];
   __shared__ int row_mod_s[BM];  // modulation row offset (AdaLN), 0 without
   __shared__ float row_inv_s[NORM ? BM : 1];  // 1 / rms of each row
@@ -114,9 +140,9 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs g) {
   };
 
   float4 ra[kA16 ? 1 : ACH];
-  V16<T> ra16[kA16 ? ACH : 1];
+  V16<T> ra16[kA16 && !kDirect ? ACH : 1];
   float4 rg[MOD ? ACH : 1];  // gamma of the A chunks in flight
-  V16<T> rb[BCH];
+  V16<T> rb[kDirect ? 1 : BCH];
   const float* A = reinterpret_cast<const float*>(g.A);
   const T* A16 = reinterpret_cast<const T*>(g.A16);
   const T* W = reinterpret_cast<const T*>(g.W);
@@ -125,16 +151,19 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs g) {
   // chunk u of thread t: A row (t + 256 u) / ACR, floats 4 ((t + 256 u) % ACR)
   // .. + 3; W row (t + 256 u) / WCR, chunk (t + 256 u) % WCR
   auto load_b = [&](int kt) {
+    if constexpr (kDirect) return;
     const int kk = kt * BK;
 #pragma unroll
-    for (int c = 0; c < BCH; ++c) {
+    for (int c = 0; c < (kDirect ? 0 : BCH); ++c) {
       const int ch = tid + c * 256, row = ch / WCR, col = (ch % WCR) * CE;
       rb[c] = ld16(W + (int64_t)w_row(n0 + row) * g.K + kk + col);
     }
   };
   auto load_a = [&](int kt) {
     const int kk = kt * BK;
-    if constexpr (kA16) {
+    if constexpr (kDirect) {
+      return;
+    } else if constexpr (kA16) {
 #pragma unroll
       for (int c = 0; c < ACH; ++c) {
         const int ch = tid + c * 256, row = ch / ACR, col = (ch % ACR) * CE;
@@ -189,7 +218,7 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs g) {
         *reinterpret_cast<float4*>(dst) = av;
       }
     }
-    if constexpr (kA16) {
+    if constexpr (kA16 && !kDirect) {
 #pragma unroll
       for (int c = 0; c < ACH; ++c) {
         const int ch = tid + c * 256, row = ch / ACR, cc = ch % ACR;
@@ -197,7 +226,7 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs g) {
       }
     }
 #pragma unroll
-    for (int c = 0; c < BCH; ++c) {
+    for (int c = 0; c < (kDirect ? 0 : BCH); ++c) {
       const int ch = tid + c * 256, row = ch / WCR, cc = ch % WCR;
       st16(&Bs[st][row * BK + swz<T>(row, cc) * CE], rb[c]);
     }
@@ -228,17 +257,43 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs g) {
 #pragma unroll
     for (int j = 0; j < NT; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // double-buffered LDS: tile kt + 1 loads into registers while tile kt is
-  // multiplied, then goes to the other stage; one barrier per tile
-  store_tiles(0);
-  __syncthreads();
-  const int frow = lane & 15, quad = lane >> 4;
-  for (int kt = 0; kt < KT; ++kt) {
-    const int st = kt & 1;
-    if (kt + 1 < KT) {
-      load_b(kt + 1);
-      load_a(kt + 1);
+  // AMODE 3: one load instruction of a wave fills 64 consecutive 16-byte
+  // chunks of an LDS stage, lane l chunk l; so lane l fetches the chunk whose
+  // swizzled place that is (the swizzle is an XOR, its own inverse).  A
+  // thread's rows and chunks are the same in every K tile: their sources are
+  // resolved once (no LDS read between the loads, which would have to wait
+  // for them).  Rows without an active token read row 0 (never stored).
+  const T* a_src[kDirect ? ACH : 1];
+  const T* b_src[kDirect ? BCH : 1];
+  const int wbase = __builtin_amdgcn_readfirstlane(tid & ~(kWave - 1));
+  if constexpr (kDirect) {
+#pragma unroll
+    for (int c = 0; c < BCH; ++c) {
+      const int q = tid + c * 256, row = q / WCR;
+      b_src[c] = W + (int64_t)w_row(n0 + row) * g.K + swz<T>(row, q % WCR) * CE;
     }
+#pragma unroll
+    for (int c = 0; c < ACH; ++c) {
+      const int q = tid + c * 256, row = q / ACR;
+      const int sr = row_src_s[row];
+      const int64_t ar = sr < 0 ? 0 : (AK == A_SRC) ? (int64_t)sr : (int64_t)(r0 + row);
+      a_src[c] = A16 + ar * g.lda + swz<T>(row, q % ACR) * CE;
+    }
+  }
+  auto issue_tile = [&](int kt, int st) __attribute__((always_inline)) {
+    if constexpr (kDirect) {
+      const int kk = kt * BK;
+#pragma unroll
+      for (int c = 0; c < BCH; ++c)
+        load_lds16(b_src[c] + kk, lds_addr(&Bs[st][(c * 256 + wbase) * CE]));
+#pragma unroll
+      for (int c = 0; c < ACH; ++c)
+        load_lds16(a_src[c] + kk, lds_addr(&As[st][0][(c * 256 + wbase) * CE]));
+    }
+  };
+
+  const int frow = lane & 15, quad = lane >> 4;
+  auto multiply = [&](int st) __attribute__((always_inline)) {
 #pragma unroll
     for (int ks = 0; ks < BK / KS; ++ks) {
       const int k0 = ks * KS + quad * EPL;  // the lane's first element of this K step
@@ -262,8 +317,41 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs g) {
 #pragma unroll
           for (int j = 0; j < NT; ++j) acc[i][j] = M::mma(af[a][i], bfr[j], acc[i][j]);
     }
-    if (kt + 1 < KT) store_tiles(st ^ 1);
+  };
+  if constexpr (kDirect) {
+    // three stages: tile kt + 2 is fetched into the stage tile kt - 1 used
+    // while tile kt is multiplied.  Before the barrier a thread waits for its
+    // own loads of tile kt (tile kt + 1's, the last LPT issued, may stay in
+    // flight); after it every thread's tile kt is in LDS and every wave is
+    // done reading tile kt - 1.
+    constexpr int LPT = ACH + BCH;  // loads per thread and tile
+    static_assert(LPT < 16, "vmcnt field");
+    issue_tile(0, 0);
+    if (KT > 1) issue_tile(1, 1);
+    int st = 0;
+    for (int kt = 0; kt < KT; ++kt) {
+      if (kt + 1 < KT) wait_loads_barrier<LPT>();
+      else wait_loads_barrier<0>();
+      if (kt + 2 < KT) issue_tile(kt + 2, st == 0 ? 2 : st - 1);
+      multiply(st);
+      st = st == 2 ? 0 : st + 1;
+    }
     __syncthreads();
+  } else {
+    // double-buffered LDS: tile kt + 1 loads into registers while tile kt is
+    // multiplied, then goes to the other stage; one barrier per tile
+    store_tiles(0);
+    __syncthreads();
+    for (int kt = 0; kt < KT; ++kt) {
+      const int st = kt & 1;
+      if (kt + 1 < KT) {
+        load_b(kt + 1);
+        load_a(kt + 1);
+      }
+      multiply(st);
+      if (kt + 1 < KT) store_tiles(st ^ 1);
+      __syncthreads();
+    }
   }
   if constexpr (EK == E_QKV) {
     if (tid < BM) kv_base[tid] = my_kv;
@@ -460,8 +548,9 @@ hipError_t launch_tiles(const GemmArgs& a, AKind ak, EKind ek, bool norm, hipStr
   if (grid.x == 0 || grid.y == 0) return hipSuccess;
   const bool mod = a.mod_g != nullptr;
   // operand mode: hi + lo parts, one bf16 part of float A, or bf16 A rows
-  const int amode = sizeof(T) != 2 ? 0 : a.A16 ? 2 : a.a_single ? 1 : 0;
-  if (amode == 2 && (mod || norm)) return hipErrorInvalidValue;
+  // (copied into LDS by their loads)
+  const int amode = sizeof(T) != 2 ? 0 : a.A16 ? 3 : a.a_single ? 1 : 0;
+  if (amode == 3 && (mod || norm)) return hipErrorInvalidValue;
 #define TLF_GEMM_LAUNCH(AKV, EKV, MODV, NORMV, AM) \
   hipLaunchKernelGGL((k_gemm<T, MT, NT, kGemmBK, AKV, EKV, MODV, NORMV, AM>), grid, dim3(256), 0, s, a)
   {
@@ -469,7 +558,7 @@ hipError_t launch_tiles(const GemmArgs& a, AKind ak, EKind ek, bool norm, hipStr
   if (ak == AKV && ek == EKV && mod == MODV && norm == NORMV) {               \
     if (amode == 0) TLF_GEMM_LAUNCH(AKV, EKV, MODV, NORMV, 0);                \
     else if (amode == 1) TLF_GEMM_LAUNCH(AKV, EKV, MODV, NORMV, 1);           \
-    else if constexpr (!MODV && !NORMV) TLF_GEMM_LAUNCH(AKV, EKV, false, false, 2); \
+    else if constexpr (!MODV && !NORMV) TLF_GEMM_LAUNCH(AKV, EKV, false, false, 3); \
     return hipGetLastError();                                                 \
   }
   TLF_GEMM_CASE(A_SRC, E_QKV, false, false)
