@@ -94,14 +94,16 @@ template <int N> __device__ __forceinline__ void wait_loads_barrier() {
 // are in flight while one is multiplied.  Float32 weights take float A
 // (AMODE 0).
 // MT x NT: each wave's 16 x 16 MFMA tiles; BK: K elements per LDS stage.
-template <typename T, int MT, int NT, int BK, int AK, int EK, bool MOD, bool NORM, int AMODE>
-__global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs g) {
-  constexpr int BM = 2 * MT * 16, BN = 2 * NT * 16;
+template <typename T, int MT, int NT, int BK, int AK, int EK, bool MOD, bool NORM, int AMODE, int WM = 2,
+          int NSTD = 3>
+__global__ __launch_bounds__(WM * 128, WM == 2 ? 2 : 1) void k_gemm(GemmArgs g) {
+  constexpr int NTH = WM * 128;                      // threads: WM x 2 waves
+  constexpr int BM = WM * MT * 16, BN = 2 * NT * 16;
   constexpr bool kBf16 = sizeof(T) == 2;             // bf16 weights: A converted to bf16 in LDS
   constexpr bool kSplit = kBf16 && AMODE == 0;       // ... as hi + lo parts
   constexpr bool kA16 = kBf16 && AMODE >= 2;         // A already bf16 in memory
   constexpr bool kDirect = kBf16 && AMODE == 3;      // ... and copied to LDS by its loads
-  constexpr int NST = kDirect ? 3 : 2;               // LDS stages
+  constexpr int NST = kDirect ? NSTD : 2;            // LDS stages
   static_assert(!kA16 || (!MOD && !NORM), "bf16 A rows carry no modulation or norm");
   constexpr int NA = kSplit ? 2 : 1;
   constexpr int CE = 16 / (int)sizeof(T);            // storage elements per 16-byte chunk
@@ -109,10 +111,10 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs g) {
   constexpr int ACR = kA16 ? BK / CE : BK / 4;       // A chunks (8 bf16 or 4 floats) per row per K tile
   using M = Mfma<T>;
   constexpr int KS = M::KS, EPL = M::EPL;
-  constexpr int ACH = BM * ACR / 256;                // A chunks per thread
-  constexpr int BCH = BN * WCR / 256;                // B chunks per thread
-  static_assert(ACH >= 1 && BM * ACR % 256 == 0, "A tile split");
-  static_assert(BCH >= 1 && BN * WCR % 256 == 0, "B tile split");
+  constexpr int ACH = BM * ACR / NTH;                // A chunks per thread
+  constexpr int BCH = BN * WCR / NTH;                // B chunks per thread
+  static_assert(ACH >= 1 && BM * ACR % NTH == 0, "A tile split");
+  static_assert(BCH >= 1 && BN * WCR % NTH == 0, "B tile split");
   static_assert(BK % KS == 0 && (KS * (int)sizeof(T)) % 16 == 0 || EPL == 1, "K tile");
 
   __shared__ __align__(16) T As[NST][NA][BM * BK];
@@ -148,14 +150,14 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs g) {
   const T* W = reinterpret_cast<const T*>(g.W);
   const int KT = g.K / BK;
 
-  // chunk u of thread t: A row (t + 256 u) / ACR, floats 4 ((t + 256 u) % ACR)
-  // .. + 3; W row (t + 256 u) / WCR, chunk (t + 256 u) % WCR
+  // chunk u of thread t: A row (t + NTH u) / ACR, floats 4 ((t + NTH u) % ACR)
+  // .. + 3; W row (t + NTH u) / WCR, chunk (t + NTH u) % WCR
   auto load_b = [&](int kt) {
     if constexpr (kDirect) return;
     const int kk = kt * BK;
 #pragma unroll
     for (int c = 0; c < (kDirect ? 0 : BCH); ++c) {
-      const int ch = tid + c * 256, row = ch / WCR, col = (ch % WCR) * CE;
+      const int ch = tid + c * NTH, row = ch / WCR, col = (ch % WCR) * CE;
       rb[c] = ld16(W + (int64_t)w_row(n0 + row) * g.K + kk + col);
     }
   };
@@ -166,7 +168,7 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs g) {
     } else if constexpr (kA16) {
 #pragma unroll
       for (int c = 0; c < ACH; ++c) {
-        const int ch = tid + c * 256, row = ch / ACR, col = (ch % ACR) * CE;
+        const int ch = tid + c * NTH, row = ch / ACR, col = (ch % ACR) * CE;
         const int s = row_src_s[row];
         ra16[c].u = make_uint4(0u, 0u, 0u, 0u);
         if (s >= 0) {
@@ -178,7 +180,7 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs g) {
     }
 #pragma unroll
     for (int c = 0; c < ACH; ++c) {
-      const int ch = tid + c * 256, row = ch / ACR, col = (ch % ACR) * 4;
+      const int ch = tid + c * NTH, row = ch / ACR, col = (ch % ACR) * 4;
       const int s = row_src_s[row];
       float4 v = make_float4(0.f, 0.f, 0.f, 0.f), gm = v;
       if (s >= 0) {
@@ -192,14 +194,14 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs g) {
       if constexpr (MOD) rg[c] = gm;
     }
   };
-  // NORM: this thread's rows are tid / ACR + c * (256 / ACR), c < ACH
+  // NORM: this thread's rows are tid / ACR + c * (NTH / ACR), c < ACH
   float ssq[NORM ? ACH : 1];
 #pragma unroll
   for (int c = 0; c < (NORM ? ACH : 1); ++c) ssq[c] = 0.f;
   auto store_tiles = [&](int st) {
 #pragma unroll
     for (int c = 0; c < (kA16 ? 0 : ACH); ++c) {
-      const int ch = tid + c * 256, row = ch / ACR, f = ch % ACR;  // floats 4f .. 4f + 3 of the row
+      const int ch = tid + c * NTH, row = ch / ACR, f = ch % ACR;  // floats 4f .. 4f + 3 of the row
       float4 av = ra[c];
       if constexpr (NORM) ssq[c] += av.x * av.x + av.y * av.y + av.z * av.z + av.w * av.w;
       if constexpr (MOD)
@@ -221,13 +223,13 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs g) {
     if constexpr (kA16 && !kDirect) {
 #pragma unroll
       for (int c = 0; c < ACH; ++c) {
-        const int ch = tid + c * 256, row = ch / ACR, cc = ch % ACR;
+        const int ch = tid + c * NTH, row = ch / ACR, cc = ch % ACR;
         st16(&As[st][0][row * BK + swz<T>(row, cc) * CE], ra16[c]);
       }
     }
 #pragma unroll
     for (int c = 0; c < (kDirect ? 0 : BCH); ++c) {
-      const int ch = tid + c * 256, row = ch / WCR, cc = ch % WCR;
+      const int ch = tid + c * NTH, row = ch / WCR, cc = ch % WCR;
       st16(&Bs[st][row * BK + swz<T>(row, cc) * CE], rb[c]);
     }
   };
@@ -269,12 +271,12 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs g) {
   if constexpr (kDirect) {
 #pragma unroll
     for (int c = 0; c < BCH; ++c) {
-      const int q = tid + c * 256, row = q / WCR;
+      const int q = tid + c * NTH, row = q / WCR;
       b_src[c] = W + (int64_t)w_row(n0 + row) * g.K + swz<T>(row, q % WCR) * CE;
     }
 #pragma unroll
     for (int c = 0; c < ACH; ++c) {
-      const int q = tid + c * 256, row = q / ACR;
+      const int q = tid + c * NTH, row = q / ACR;
       const int sr = row_src_s[row];
       const int64_t ar = sr < 0 ? 0 : (AK == A_SRC) ? (int64_t)sr : (int64_t)(r0 + row);
       a_src[c] = A16 + ar * g.lda + swz<T>(row, q % ACR) * CE;
@@ -285,10 +287,10 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs g) {
       const int kk = kt * BK;
 #pragma unroll
       for (int c = 0; c < BCH; ++c)
-        load_lds16(b_src[c] + kk, lds_addr(&Bs[st][(c * 256 + wbase) * CE]));
+        load_lds16(b_src[c] + kk, lds_addr(&Bs[st][(c * NTH + wbase) * CE]));
 #pragma unroll
       for (int c = 0; c < ACH; ++c)
-        load_lds16(a_src[c] + kk, lds_addr(&As[st][0][(c * 256 + wbase) * CE]));
+        load_lds16(a_src[c] + kk, lds_addr(&As[st][0][(c * NTH + wbase) * CE]));
     }
   };
 
@@ -319,22 +321,26 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs g) {
     }
   };
   if constexpr (kDirect) {
-    // three stages: tile kt + 2 is fetched into the stage tile kt - 1 used
-    // while tile kt is multiplied.  Before the barrier a thread waits for its
-    // own loads of tile kt (tile kt + 1's, the last LPT issued, may stay in
-    // flight); after it every thread's tile kt is in LDS and every wave is
-    // done reading tile kt - 1.
+    // NST stages: tile kt + NST - 1 is fetched into the stage tile kt - 1
+    // used while tile kt is multiplied.  Before the barrier a thread waits
+    // for its own loads of tile kt (those of the up to NST - 2 later tiles,
+    // the last LPT each, may stay in flight); after it every thread's tile kt
+    // is in LDS and every wave is done reading tile kt - 1.
     constexpr int LPT = ACH + BCH;  // loads per thread and tile
-    static_assert(LPT < 16, "vmcnt field");
-    issue_tile(0, 0);
-    if (KT > 1) issue_tile(1, 1);
+    static_assert(NST == 3 || NST == 4, "stages");
+    static_assert(LPT * (NST - 2) < 16, "vmcnt field");
+#pragma unroll
+    for (int t = 0; t < NST - 1; ++t)
+      if (t < KT) issue_tile(t, t);
     int st = 0;
     for (int kt = 0; kt < KT; ++kt) {
-      if (kt + 1 < KT) wait_loads_barrier<LPT>();
+      const int later = min(NST - 2, KT - 1 - kt);  // tiles after kt already issued
+      if (later >= 2) wait_loads_barrier<2 * LPT>();
+      else if (later == 1) wait_loads_barrier<LPT>();
       else wait_loads_barrier<0>();
-      if (kt + 2 < KT) issue_tile(kt + 2, st == 0 ? 2 : st - 1);
+      if (kt + NST - 1 < KT) issue_tile(kt + NST - 1, st == 0 ? NST - 1 : st - 1);
       multiply(st);
-      st = st == 2 ? 0 : st + 1;
+      st = st == NST - 1 ? 0 : st + 1;
     }
     __syncthreads();
   } else {
@@ -358,14 +364,14 @@ __global__ __launch_bounds__(256, 2) void k_gemm(GemmArgs g) {
     __syncthreads();
   }
   if constexpr (NORM) {
-    static_assert(256 % ACR == 0 && ACR <= kWave, "rows of the A chunks");
+    static_assert(NTH % ACR == 0 && ACR <= kWave, "rows of the A chunks");
     // the ACR threads of a row are consecutive lanes of one wave
 #pragma unroll
     for (int c = 0; c < ACH; ++c) {
       float t = ssq[c];
 #pragma unroll
       for (int o = 1; o < ACR; o <<= 1) t += shfl_xor(t, o);
-      if (tid % ACR == 0) row_inv_s[tid / ACR + c * (256 / ACR)] = rsqrtf(t / (float)g.K + g.eps);
+      if (tid % ACR == 0) row_inv_s[tid / ACR + c * (NTH / ACR)] = rsqrtf(t / (float)g.K + g.eps);
     }
     __syncthreads();
   }
@@ -577,6 +583,23 @@ hipError_t launch_tiles(const GemmArgs& a, AKind ak, EKind ek, bool norm, hipStr
   return hipErrorInvalidValue;
 }
 
+// The down projection of many rows (bf16 rows, K = F): 256 x 256 tiles of
+// 8 waves (each still 64 x 128), one workgroup per compute unit; at 32768
+// rows x 1024 x 2816 it took 204 us against 232 us with 128 x 256 tiles of 4
+// waves, while the gate/up, QKV and O projections (K = d) gained nothing.
+constexpr int kWideResidMinK = 2048, kWideResidMinRows = 16384;
+template <typename T>
+hipError_t launch_resid_wide(const GemmArgs& a, hipStream_t s) {
+  if constexpr (sizeof(T) == 2) {
+    constexpr int WM = 4, BM = WM * kGemmMT * 16, BN = 2 * 8 * 16;
+    const dim3 grid((a.N + BN - 1) / BN, (a.rm.rows + BM - 1) / BM);
+    hipLaunchKernelGGL((k_gemm<T, kGemmMT, 8, kGemmBK, A_CMP, E_RESID, false, false, 3, WM>), grid, dim3(WM * 128),
+                       0, s, a);
+    return hipGetLastError();
+  }
+  return hipErrorInvalidValue;
+}
+
 }  // namespace
 
 template <typename T>
@@ -590,6 +613,9 @@ hipError_t launch_gemm(const GemmArgs& a, AKind ak, EKind ek, bool norm, hipStre
   if ((ek == E_RESID && (a.N % 4 != 0 || a.ldo % 4 != 0 || (a.mod_a && a.mod_ld % 4 != 0))) ||
       (ek == E_SWIGLU && (a.F % 4 != 0 || a.ldo % 4 != 0)))
     return hipErrorInvalidValue;
+  if (sizeof(T) == 2 && ak == A_CMP && ek == E_RESID && !norm && a.A16 && !a.mod_g && a.K >= kWideResidMinK &&
+      a.rm.rows >= kWideResidMinRows)
+    return launch_resid_wide<T>(a, s);
   // a few row tiles (the decode LM head) take 128-column tiles so the grid
   // still holds about two workgroups per compute unit; prefill takes 256
   const int row_tiles = (a.rm.rows + 2 * kGemmMT * 16 - 1) / (2 * kGemmMT * 16);
