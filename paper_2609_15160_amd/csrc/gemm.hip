@@ -17,19 +17,23 @@
 //   E_HIDDEN:  silu(result + bias), the MLP router's hidden layer
 //
 // Tiling: 256 threads = 4 waves in a 2 x 2 grid, a 128 x 256 output tile
-// per workgroup (64 x 128 per wave; 128 x 128 when there are few row tiles).  K advances 32
-// elements per tile through two LDS stages: the next tile's global loads
-// are in flight while the current one is multiplied, then stored to the
-// other stage (one barrier per tile).  LDS rows are XOR-swizzled by 16-byte
-// chunk instead of padded, so two workgroups fit on a compute unit.
+// per workgroup (64 x 128 per wave; 128 x 128 when there are few row tiles;
+// the down projection of many rows: 8 waves in a 4 x 2 grid, 256 x 256).  K
+// advances 32 elements per tile.  Float A: through two LDS stages, the next
+// tile's global loads in flight while the current one is multiplied, then
+// converted and stored to the other stage (one barrier per tile).  bf16 A
+// rows: A and W copied into LDS by the loads themselves, three stages, two
+// tiles in flight (one wait and barrier per tile).  LDS rows are
+// XOR-swizzled by 16-byte chunk instead of padded, so two workgroups fit on
+// a compute unit.
 #include "kernels.h"
 
 namespace tlf {
 
 namespace {
 
-// Tiling: 256 threads = 4 waves in a 2 x 2 grid, each wave kGemmMT x NT
-// MFMA tiles of 16 x 16 (64 rows x 128 or 64 columns), K kGemmBK at a time.
+// Each wave kGemmMT x NT MFMA tiles of 16 x 16 (64 rows x 128 or 64
+// columns), K kGemmBK at a time.
 constexpr int kGemmMT = 4, kGemmBK = 32;
 
 __device__ __forceinline__ unsigned int ordered_bits(float v) {
@@ -88,11 +92,12 @@ template <int N> __device__ __forceinline__ void wait_loads_barrier() {
 // and the output row is scaled by 1 / rms, since (x / rms) W^T = (x W^T) / rms.
 // AMODE (bf16 weights): 0: float A enters the MFMA as hi + lo parts; 1: as
 // one bf16 part (round to nearest even), half the products and LDS traffic;
-// 2: A is read as bf16 rows (g.A16), half the A bytes as well; 3: as 2, with
-// A and W copied into LDS by the loads themselves (global_load_lds: no
-// registers, no LDS stores), through three LDS stages so that two K tiles
+// 2: A is read as bf16 rows (g.A16), half the A bytes as well, and A and W
+// are copied into LDS by the loads themselves (global_load_lds: no
+// registers, no LDS stores), through NSTD LDS stages so that NSTD - 1 K tiles
 // are in flight while one is multiplied.  Float32 weights take float A
 // (AMODE 0).
+// WM: waves along M (2 or 4; two along N), each wave MT x NT MFMA tiles.
 // MT x NT: each wave's 16 x 16 MFMA tiles; BK: K elements per LDS stage.
 template <typename T, int MT, int NT, int BK, int AK, int EK, bool MOD, bool NORM, int AMODE, int WM = 2,
           int NSTD = 3>
@@ -101,14 +106,13 @@ __global__ __launch_bounds__(WM * 128, WM == 2 ? 2 : 1) void k_gemm(GemmArgs g) 
   constexpr int BM = WM * MT * 16, BN = 2 * NT * 16;
   constexpr bool kBf16 = sizeof(T) == 2;             // bf16 weights: A converted to bf16 in LDS
   constexpr bool kSplit = kBf16 && AMODE == 0;       // ... as hi + lo parts
-  constexpr bool kA16 = kBf16 && AMODE >= 2;         // A already bf16 in memory
-  constexpr bool kDirect = kBf16 && AMODE == 3;      // ... and copied to LDS by its loads
+  constexpr bool kDirect = kBf16 && AMODE == 2;      // bf16 A rows; A and W copied to LDS by their loads
   constexpr int NST = kDirect ? NSTD : 2;            // LDS stages
-  static_assert(!kA16 || (!MOD && !NORM), "bf16 A rows carry no modulation or norm");
+  static_assert(!kDirect || (!MOD && !NORM), "bf16 A rows carry no modulation or norm");
   constexpr int NA = kSplit ? 2 : 1;
   constexpr int CE = 16 / (int)sizeof(T);            // storage elements per 16-byte chunk
   constexpr int WCR = BK / CE;                       // weight chunks per row per K tile
-  constexpr int ACR = kA16 ? BK / CE : BK / 4;       // A chunks (8 bf16 or 4 floats) per row per K tile
+  constexpr int ACR = kDirect ? BK / CE : BK / 4;   // A chunks (8 bf16 or 4 floats) per row per K tile
   using M = Mfma<T>;
   constexpr int KS = M::KS, EPL = M::EPL;
   constexpr int ACH = BM * ACR / NTH;                // A chunks per thread
@@ -141,8 +145,7 @@ __global__ __launch_bounds__(WM * 128, WM == 2 ? 2 : 1) void k_gemm(GemmArgs g) 
     return wr < g.w_rows ? wr : g.w_rows - 1;
   };
 
-  float4 ra[kA16 ? 1 : ACH];
-  V16<T> ra16[kA16 && !kDirect ? ACH : 1];
+  float4 ra[kDirect ? 1 : ACH];
   float4 rg[MOD ? ACH : 1];  // gamma of the A chunks in flight
   V16<T> rb[kDirect ? 1 : BCH];
   const float* A = reinterpret_cast<const float*>(g.A);
@@ -163,21 +166,7 @@ __global__ __launch_bounds__(WM * 128, WM == 2 ? 2 : 1) void k_gemm(GemmArgs g) 
   };
   auto load_a = [&](int kt) {
     const int kk = kt * BK;
-    if constexpr (kDirect) {
-      return;
-    } else if constexpr (kA16) {
-#pragma unroll
-      for (int c = 0; c < ACH; ++c) {
-        const int ch = tid + c * NTH, row = ch / ACR, col = (ch % ACR) * CE;
-        const int s = row_src_s[row];
-        ra16[c].u = make_uint4(0u, 0u, 0u, 0u);
-        if (s >= 0) {
-          const int64_t ar = (AK == A_SRC) ? (int64_t)s : (int64_t)(r0 + row);
-          ra16[c] = ld16(A16 + ar * g.lda + kk + col);
-        }
-      }
-      return;
-    }
+    if constexpr (kDirect) return;
 #pragma unroll
     for (int c = 0; c < ACH; ++c) {
       const int ch = tid + c * NTH, row = ch / ACR, col = (ch % ACR) * 4;
@@ -200,7 +189,7 @@ __global__ __launch_bounds__(WM * 128, WM == 2 ? 2 : 1) void k_gemm(GemmArgs g) 
   for (int c = 0; c < (NORM ? ACH : 1); ++c) ssq[c] = 0.f;
   auto store_tiles = [&](int st) {
 #pragma unroll
-    for (int c = 0; c < (kA16 ? 0 : ACH); ++c) {
+    for (int c = 0; c < (kDirect ? 0 : ACH); ++c) {
       const int ch = tid + c * NTH, row = ch / ACR, f = ch % ACR;  // floats 4f .. 4f + 3 of the row
       float4 av = ra[c];
       if constexpr (NORM) ssq[c] += av.x * av.x + av.y * av.y + av.z * av.z + av.w * av.w;
@@ -218,13 +207,6 @@ __global__ __launch_bounds__(WM * 128, WM == 2 ? 2 : 1) void k_gemm(GemmArgs g) 
         *reinterpret_cast<uint2*>(dst) = make_uint2(pack_bf16x2(av.x, av.y), pack_bf16x2(av.z, av.w));
       } else {
         *reinterpret_cast<float4*>(dst) = av;
-      }
-    }
-    if constexpr (kA16 && !kDirect) {
-#pragma unroll
-      for (int c = 0; c < ACH; ++c) {
-        const int ch = tid + c * NTH, row = ch / ACR, cc = ch % ACR;
-        st16(&As[st][0][row * BK + swz<T>(row, cc) * CE], ra16[c]);
       }
     }
 #pragma unroll
@@ -259,7 +241,7 @@ __global__ __launch_bounds__(WM * 128, WM == 2 ? 2 : 1) void k_gemm(GemmArgs g) 
 #pragma unroll
     for (int j = 0; j < NT; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // AMODE 3: one load instruction of a wave fills 64 consecutive 16-byte
+  // AMODE 2: one load instruction of a wave fills 64 consecutive 16-byte
   // chunks of an LDS stage, lane l chunk l; so lane l fetches the chunk whose
   // swizzled place that is (the swizzle is an XOR, its own inverse).  A
   // thread's rows and chunks are the same in every K tile: their sources are
@@ -555,8 +537,8 @@ hipError_t launch_tiles(const GemmArgs& a, AKind ak, EKind ek, bool norm, hipStr
   const bool mod = a.mod_g != nullptr;
   // operand mode: hi + lo parts, one bf16 part of float A, or bf16 A rows
   // (copied into LDS by their loads)
-  const int amode = sizeof(T) != 2 ? 0 : a.A16 ? 3 : a.a_single ? 1 : 0;
-  if (amode == 3 && (mod || norm)) return hipErrorInvalidValue;
+  const int amode = sizeof(T) != 2 ? 0 : a.A16 ? 2 : a.a_single ? 1 : 0;
+  if (amode == 2 && (mod || norm)) return hipErrorInvalidValue;
 #define TLF_GEMM_LAUNCH(AKV, EKV, MODV, NORMV, AM) \
   hipLaunchKernelGGL((k_gemm<T, MT, NT, kGemmBK, AKV, EKV, MODV, NORMV, AM>), grid, dim3(256), 0, s, a)
   {
@@ -564,7 +546,7 @@ hipError_t launch_tiles(const GemmArgs& a, AKind ak, EKind ek, bool norm, hipStr
   if (ak == AKV && ek == EKV && mod == MODV && norm == NORMV) {               \
     if (amode == 0) TLF_GEMM_LAUNCH(AKV, EKV, MODV, NORMV, 0);                \
     else if (amode == 1) TLF_GEMM_LAUNCH(AKV, EKV, MODV, NORMV, 1);           \
-    else if constexpr (!MODV && !NORMV) TLF_GEMM_LAUNCH(AKV, EKV, false, false, 3); \
+    else if constexpr (!MODV && !NORMV) TLF_GEMM_LAUNCH(AKV, EKV, false, false, 2); \
     return hipGetLastError();                                                 \
   }
   TLF_GEMM_CASE(A_SRC, E_QKV, false, false)
@@ -593,7 +575,7 @@ hipError_t launch_resid_wide(const GemmArgs& a, hipStream_t s) {
   if constexpr (sizeof(T) == 2) {
     constexpr int WM = 4, BM = WM * kGemmMT * 16, BN = 2 * 8 * 16;
     const dim3 grid((a.N + BN - 1) / BN, (a.rm.rows + BM - 1) / BM);
-    hipLaunchKernelGGL((k_gemm<T, kGemmMT, 8, kGemmBK, A_CMP, E_RESID, false, false, 3, WM>), grid, dim3(WM * 128),
+    hipLaunchKernelGGL((k_gemm<T, kGemmMT, 8, kGemmBK, A_CMP, E_RESID, false, false, 2, WM>), grid, dim3(WM * 128),
                        0, s, a);
     return hipGetLastError();
   }
