@@ -324,6 +324,52 @@ __device__ __forceinline__ void dgemm_tile(const GemmArgs& g, int nact, int act_
   };
   const int row_end = min(g.rm.rows, nact);  // rows [r0, row_end) are active
 
+  if constexpr (EK == E_QKV) {
+    // Eight consecutive columns per thread: they lie in one of q, k and v and
+    // in one head (d and D are multiples of 16), so the part and head are
+    // resolved once per group; q goes out as two 16-byte stores, a bf16 k run
+    // as one (eight consecutive dimensions of a slot are adjacent in fragment
+    // order), v as eight elements four apart ([slot / 4][D][slot % 4]).
+    static_assert(BN % 8 == 0, "column groups");
+    T* pool = reinterpret_cast<T*>(g.kv.c.pool);
+    for (int e8 = tid; e8 < BM * BN / 8; e8 += NT) {
+      const int row = e8 / (BN / 8), col = (e8 % (BN / 8)) * 8, n = n0 + col;
+      if (r0 + row >= row_end || n >= g.N) continue;
+      float v[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) v[j] = tile_sum(row, col + j);
+      if (n < g.d) {
+        float* q = g.out + (int64_t)(r0 + row) * g.ldo + n;
+        *reinterpret_cast<float4*>(q) = make_float4(v[0], v[1], v[2], v[3]);
+        *reinterpret_cast<float4*>(q + 4) = make_float4(v[4], v[5], v[6], v[7]);
+        continue;
+      }
+      const int64_t base = sh.kv[row];
+      if (base < 0) continue;
+      const int slot = (int)(base & (kPage - 1));
+      const int64_t page = base - slot;
+      const bool is_v = n - g.d >= g.d;
+      const int within = n - g.d - (is_v ? g.d : 0);
+      const int h = within / g.kv.c.D, el = within - h * g.kv.c.D;
+      if (!is_v) {
+        if constexpr (sizeof(T) == 2) {
+          *reinterpret_cast<uint4*>(pool + page + k_block(g.kv.c, g.kv.layer, h) + k_frag_off<T>(slot, el)) =
+              make_uint4(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]), pack_bf16x2(v[4], v[5]),
+                         pack_bf16x2(v[6], v[7]));
+        } else {
+#pragma unroll
+          for (int j = 0; j < 8; ++j)
+            pool[page + k_block(g.kv.c, g.kv.layer, h) + k_frag_off<T>(slot, el + j)] = from_f<T>(v[j]);
+        }
+      } else {
+        T* dst = pool + page + v_block(g.kv.c, g.kv.layer, h) + v_frag_off(slot, el, g.kv.c.D);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) dst[4 * j] = from_f<T>(v[j]);
+      }
+    }
+    return;
+  }
+
 #pragma unroll
   for (int k = 0; k < EPT; ++k) {
     const int e = tid + k * NT;
@@ -370,22 +416,6 @@ __device__ __forceinline__ void dgemm_tile(const GemmArgs& g, int nact, int act_
       } else if constexpr (EK == E_HIDDEN) {
         const float u = v + g.bias[n];
         g.out[(int64_t)(r0 + row) * g.ldo + n] = u / (1.f + __expf(-u));
-      } else {  // E_QKV
-        if (n < g.d) {
-          g.out[(int64_t)(r0 + row) * g.ldo + n] = v;
-        } else {
-          const int64_t base = sh.kv[row];
-          if (base < 0) continue;
-          const int slot = (int)(base & (kPage - 1));
-          const int64_t page = base - slot;
-          const int nn = n - g.d, kvsel = nn / g.d, within = nn % g.d;
-          const int h = within / g.kv.c.D, el = within % g.kv.c.D;
-          T* pool = reinterpret_cast<T*>(g.kv.c.pool);
-          if (kvsel == 0)
-            pool[page + k_block(g.kv.c, g.kv.layer, h) + k_frag_off<T>(slot, el)] = from_f<T>(v);
-          else
-            pool[page + v_block(g.kv.c, g.kv.layer, h) + v_frag_off(slot, el, g.kv.c.D)] = from_f<T>(v);
-        }
       }
     }
   }
