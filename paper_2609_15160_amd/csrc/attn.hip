@@ -42,8 +42,8 @@ template <typename F, typename P> __device__ __forceinline__ F ld_stream(const P
   }
 }
 
-// Queries per wave of the prefill attention (four waves per workgroup).
-constexpr int kPreQW = 16;
+// Queries per wave and waves per workgroup of the prefill attention.
+constexpr int kPreQW = 16, kPreWaves = 8;
 
 __device__ __forceinline__ float4 scale4(float4 v, float s) { return make_float4(v.x * s, v.y * s, v.z * s, v.w * s); }
 
@@ -313,13 +313,14 @@ __global__ __launch_bounds__(W * 64) void k_attn_decode(AttnDecodeArgs a) {
 }
 
 template <typename T, int D, bool SPLITQ>
-__global__ __launch_bounds__(256, 4) void k_attn_prefill(AttnPrefillArgs a) {
+__global__ __launch_bounds__(kPreWaves * 64, 16 / kPreWaves) void k_attn_prefill(AttnPrefillArgs a) {
   using M = Mfma<T>;
   typedef typename M::frag Frag;
   constexpr int KS = M::KS, EPL = M::EPL;
   constexpr int QW = kPreQW;                      // queries per wave
   constexpr int QN = QW / 16;                     // query column tiles per wave
-  constexpr int BQ = 4 * QW;                      // queries per workgroup
+  constexpr int NTH = kPreWaves * kWave;          // threads
+  constexpr int BQ = kPreWaves * QW;              // queries per workgroup
   constexpr int BKEY = 4 * kPage;                 // keys per tile: four pages
   constexpr int NT = BKEY / 16;                   // 16-key subtiles
   constexpr int KSTEPS = D / KS;
@@ -340,8 +341,8 @@ __global__ __launch_bounds__(256, 4) void k_attn_prefill(AttnPrefillArgs a) {
                           : (p * D + d) * VLD + slot;
   };
   constexpr int CH = 2 * 4 * KBLK / EPC;          // 16-byte chunks of one K + V tile
-  static_assert(CH % 256 == 0, "tile chunks per thread");
-  constexpr int CPT = CH / 256;
+  static_assert(CH % NTH == 0, "tile chunks per thread");
+  constexpr int CPT = CH / NTH;
   static_assert(EPC % 4 == 0 && (4 * D) % EPC == 0, "V chunk: whole 4-slot groups of one slot group");
   // K tile: four pages' K blocks verbatim (fragment order: lane (key, quad) of a
   // K step reads EPL contiguous elements, 64 lanes one contiguous run);
@@ -410,7 +411,7 @@ __global__ __launch_bounds__(256, 4) void k_attn_prefill(AttnPrefillArgs a) {
   // so that none waits on another.
   static_assert((KBLK / EPC) % kWave == 0, "a wave's chunks within one page block");
   const int wu = __builtin_amdgcn_readfirstlane(w);
-  auto round_page = [&](int u) { return ((wu * kWave + u * 256) % (CH / 2)) / (KBLK / EPC); };
+  auto round_page = [&](int u) { return ((wu * kWave + u * NTH) % (CH / 2)) / (KBLK / EPC); };
   uint4 pre[CPT];
   auto load_tile = [&](int kt) __attribute__((always_inline)) {
     int pg[CPT];
@@ -418,7 +419,7 @@ __global__ __launch_bounds__(256, 4) void k_attn_prefill(AttnPrefillArgs a) {
     for (int u = 0; u < CPT; ++u) pg[u] = pt[min(kt * 4 + round_page(u), npages - 1)];
 #pragma unroll
     for (int u = 0; u < CPT; ++u) {
-      const int ci0 = wu * kWave + u * 256;  // the wave's first chunk of round u
+      const int ci0 = wu * kWave + u * NTH;  // the wave's first chunk of round u
       const int kv = ci0 / (CH / 2);
       const int off = ((ci0 % (CH / 2)) % (KBLK / EPC) + lane) * EPC;
       pre[u] = *reinterpret_cast<const uint4*>(pool + (int64_t)pg[u] * c.page_elems + (kv ? voff : koff) + off);
@@ -427,7 +428,7 @@ __global__ __launch_bounds__(256, 4) void k_attn_prefill(AttnPrefillArgs a) {
   auto store_tile = [&](int kt, int buf) __attribute__((always_inline)) {
 #pragma unroll
     for (int u = 0; u < CPT; ++u) {
-      const int ci = tid + u * 256;
+      const int ci = tid + u * NTH;
       const int kv = ci / (CH / 2), cc = ci % (CH / 2);
       const int p = cc / (KBLK / EPC), off = (cc % (KBLK / EPC)) * EPC;
       uint4 v = pre[u];
@@ -671,9 +672,9 @@ hipError_t attn_decode_blocks_per_cu(int D, int waves, int* blocks) {
 
 template <typename T>
 hipError_t launch_attn_prefill(const AttnPrefillArgs& a, hipStream_t s) {
-  const int BQ = 4 * kPreQW;
+  const int BQ = kPreWaves * kPreQW;
   const int QT = (a.T + BQ - 1) / BQ;
-  const dim3 grid(a.G * QT * a.c.H), block(256);
+  const dim3 grid(a.G * QT * a.c.H), block(kPreWaves * kWave);
   if (a.G <= 0) return hipSuccess;
   switch (a.c.D) {
     case 16:
