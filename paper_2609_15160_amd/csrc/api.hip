@@ -386,14 +386,19 @@ int run_prefill(tlf_ctx* ctx, int B, int T_, int pos0, const int32_t* tokens, fl
         set_mod(ctx, &q, i, j, 2, pre_depth, 1);
         q.a_single = one;
         if (one && !q.mod_g) q.A16 = y16;  // the AdaLN scale needs the float rows
+        const float scale_log2 = 1.4426950408889634f / std::sqrt((float)c.head_dim);
+        // one part: q handed on as bf16(q * scale_log2), as the attention rounds it
+        bf16* q16 = one ? reinterpret_cast<bf16*>(ctx->buf<float>(B_Q_PRE)) : nullptr;
+        q.q16 = q16; q.q_scale = scale_log2;
         if (few) TLF_HIP(launch_dgemm<T>(q, A_SRC, E_QKV, true, ctx->cus, s));
         else TLF_HIP(launch_gemm<T>(q, A_SRC, E_QKV, false, s));
 
         AttnPrefillArgs at;
         at.c = ctx->cv; at.loop = i; at.layer = j; at.d = d; at.b0 = b0; at.G = Gc; at.T = T_;
         at.q = ctx->buf<float>(B_Q_PRE); at.o = ctx->buf<float>(B_O_PRE);
-        at.scale_log2 = 1.4426950408889634f / std::sqrt((float)c.head_dim);
+        at.scale_log2 = scale_log2;
         at.q_single = one;
+        at.q16 = q16;
         at.o16 = o16;
         TLF_HIP(launch_attn_prefill<T>(at, s));
 

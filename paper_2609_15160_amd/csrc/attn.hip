@@ -392,10 +392,14 @@ __global__ __launch_bounds__(kPreWaves * 64, 16 / kPreWaves) void k_attn_prefill
         qf[qn][0][ks] = __builtin_bit_cast(Frag, make_uint4(h0.x, h0.y, h1.x, h1.y));
         qf[qn][1][ks] = __builtin_bit_cast(Frag, make_uint4(l0.x, l0.y, l1.x, l1.y));
       } else if constexpr (EPL == 8) {
-        const float4 v0 = scale4(*reinterpret_cast<const float4*>(qp + ks * KS), a.scale_log2);
-        const float4 v1 = scale4(*reinterpret_cast<const float4*>(qp + ks * KS + 4), a.scale_log2);
-        qf[qn][0][ks] = __builtin_bit_cast(Frag, make_uint4(pack_bf16x2(v0.x, v0.y), pack_bf16x2(v0.z, v0.w),
-                                                            pack_bf16x2(v1.x, v1.y), pack_bf16x2(v1.z, v1.w)));
+        if (a.q16) {  // written scaled and rounded by the QKV projection
+          qf[qn][0][ks] = *reinterpret_cast<const Frag*>(a.q16 + (qp - a.q) + ks * KS);
+        } else {
+          const float4 v0 = scale4(*reinterpret_cast<const float4*>(qp + ks * KS), a.scale_log2);
+          const float4 v1 = scale4(*reinterpret_cast<const float4*>(qp + ks * KS + 4), a.scale_log2);
+          qf[qn][0][ks] = __builtin_bit_cast(Frag, make_uint4(pack_bf16x2(v0.x, v0.y), pack_bf16x2(v0.z, v0.w),
+                                                              pack_bf16x2(v1.x, v1.y), pack_bf16x2(v1.z, v1.w)));
+        }
       } else {
         qf[qn][0][ks] = qp[ks * KS] * a.scale_log2;
       }

@@ -383,9 +383,16 @@ __global__ __launch_bounds__(WM * 128, WM == 2 ? 2 : 1) void k_gemm(GemmArgs g) 
           transpose4(v0, v1, v2, v3, t);
           const int rl = rl0 + t, cb = nt + (col16 & ~3);
           if (nt < g.d) {
-            if (row_src_s[rl] >= 0)
-              *reinterpret_cast<float4*>(reinterpret_cast<float*>(g.out) + (int64_t)(r0 + rl) * g.ldo + cb) =
-                  make_float4(v0, v1, v2, v3);
+            if (row_src_s[rl] >= 0) {
+              if (g.q16) {  // scaled and rounded to bf16 as the attention would on loading q
+                const float sc = g.q_scale;
+                *reinterpret_cast<uint2*>(g.q16 + (int64_t)(r0 + rl) * g.ldo + cb) =
+                    make_uint2(pack_bf16x2(v0 * sc, v1 * sc), pack_bf16x2(v2 * sc, v3 * sc));
+              } else {
+                *reinterpret_cast<float4*>(reinterpret_cast<float*>(g.out) + (int64_t)(r0 + rl) * g.ldo + cb) =
+                    make_float4(v0, v1, v2, v3);
+              }
+            }
           } else {
             const int64_t base = kv_base[rl];
             if (base >= 0) {

@@ -115,6 +115,8 @@ struct GemmArgs {
   const bf16* A16 = nullptr;  // launch_gemm with bf16 weights: A given as bf16 rows (same lda) in place of
                               // A (no norm, no operand modulation)
   bf16* out16 = nullptr;      // launch_gemm E_SWIGLU: act rows written as bf16 instead of float
+  bf16* q16 = nullptr;        // launch_gemm E_QKV: q rows written as bf16(q * q_scale) instead of to out
+  float q_scale = 1.f;
 };
 
 // Offset of element (R, k) of a [rows][K] operand stored in MFMA fragment order.
@@ -265,6 +267,7 @@ struct AttnPrefillArgs {
   float scale_log2 = 0.f;
   int q_single = 0;         // bf16 keys: the scaled q enters the score product as one bf16 part (not hi + lo)
   bf16* o16 = nullptr;      // [G*T][d]: o written as bf16 instead of to o
+  const bf16* q16 = nullptr;  // with q_single: [G*T][d] q already scaled and rounded (bf16(q * scale_log2)), read in place of q
 };
 template <typename T> hipError_t launch_attn_prefill(const AttnPrefillArgs& a, hipStream_t s);
 
