@@ -134,6 +134,12 @@ __global__ __launch_bounds__(WM * 128, WM == 2 ? 2 : 1) void k_gemm(GemmArgs g) 
 
   // decode: a tile whose first row has exited is empty (rows are depth-sorted)
   if (g.rm.nact && r0 >= *g.rm.nact) return;
+  // prefill: segments of seg slots with active prefixes; a tile inside one
+  // segment that starts past its active count is empty (most tiles of the
+  // later loops): leave before resolving rows
+  if (g.rm.seg_cnt && r0 % g.rm.seg + BM <= g.rm.seg &&
+      r0 % g.rm.seg >= g.rm.seg_cnt[(r0 / g.rm.seg) * g.rm.seg_cnt_stride])
+    return;
 
   // W row of output column n (clamped; columns >= N are never stored)
   auto w_row = [&](int n) -> int {
