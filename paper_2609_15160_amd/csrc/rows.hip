@@ -223,46 +223,56 @@ __global__ __launch_bounds__(256) void k_route_rows(RouteArgs a) {
 
 // ---------------------------------------------------------------------------
 // y[src(r)] = RMSNorm(x[src(r)]) for the active rows of a row map (prefill,
-// after each residual projection).  One workgroup per row: thread t holds
-// elements 4t + 1024c, c < NC.
+// after each residual projection).  One wave per row, four rows per
+// workgroup (most rows of the later loops are inactive, and a row's wave
+// leaves at once).  Lane l holds elements 4 (l + 64 v) + 1024 c, v < 4,
+// c < NC: those of threads l + 64 v of a 256-thread row.  Its sum of squares
+// is taken as such a row would take it: per thread over c, over the 64
+// lanes for each v, then the four partials in pairs.
 // ---------------------------------------------------------------------------
 template <int NC>
 __global__ __launch_bounds__(256) void k_resid_norm(ResidNormArgs a) {
-  __shared__ float s_part[4];
-  const int r = blockIdx.x;
+  const int lane = lane_id();
+  const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (!row_active(a.rm, r)) return;
-  const int tid = threadIdx.x, lane = lane_id(), w = tid >> 6;
   const int src = row_src(a.rm, r);
   const float* x = a.x + (int64_t)src * a.d;
-  float4 h[NC];
-  float ss = 0.f;
+  float4 h[4][NC];
+  float ps[4];
 #pragma unroll
-  for (int c = 0; c < NC; ++c) {
-    const int k = 4 * tid + 1024 * c;
-    h[c] = scale4(V4<float>::load(x + clamp_k(k, a.d)), k < a.d ? 1.f : 0.f);
-    ss = sumsq(h[c], ss);
+  for (int v = 0; v < 4; ++v) {
+    ps[v] = 0.f;
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      const int k = 4 * (lane + 64 * v) + 1024 * c;
+      h[v][c] = scale4(V4<float>::load(x + clamp_k(k, a.d)), k < a.d ? 1.f : 0.f);
+      ps[v] = sumsq(h[v][c], ps[v]);
+    }
   }
-  ss = wave_sum(ss);
-  if (lane == 0) s_part[w] = ss;
-  __syncthreads();
-  ss = (s_part[0] + s_part[1]) + (s_part[2] + s_part[3]);
+#pragma unroll
+  for (int v = 0; v < 4; ++v) ps[v] = wave_sum(ps[v]);
+  const float ss = (ps[0] + ps[1]) + (ps[2] + ps[3]);
   const float inv = rsqrtf(ss / (float)a.d + a.eps);
   if (a.y) {
     float* y = a.y + (int64_t)src * a.d;
 #pragma unroll
-    for (int c = 0; c < NC; ++c) {
-      const int k = 4 * tid + 1024 * c;
-      if (k < a.d) V4<float>::store(y + k, scale4(h[c], inv));
-    }
+    for (int v = 0; v < 4; ++v)
+#pragma unroll
+      for (int c = 0; c < NC; ++c) {
+        const int k = 4 * (lane + 64 * v) + 1024 * c;
+        if (k < a.d) V4<float>::store(y + k, scale4(h[v][c], inv));
+      }
   }
   if (a.y16) {
     bf16* y16 = a.y16 + (int64_t)src * a.d;
 #pragma unroll
-    for (int c = 0; c < NC; ++c) {
-      const int k = 4 * tid + 1024 * c;
-      const float4 v = scale4(h[c], inv);
-      if (k < a.d) *reinterpret_cast<uint2*>(y16 + k) = make_uint2(pack_bf16x2(v.x, v.y), pack_bf16x2(v.z, v.w));
-    }
+    for (int v = 0; v < 4; ++v)
+#pragma unroll
+      for (int c = 0; c < NC; ++c) {
+        const int k = 4 * (lane + 64 * v) + 1024 * c;
+        const float4 hv = scale4(h[v][c], inv);
+        if (k < a.d) *reinterpret_cast<uint2*>(y16 + k) = make_uint2(pack_bf16x2(hv.x, hv.y), pack_bf16x2(hv.z, hv.w));
+      }
   }
 }
 
@@ -294,7 +304,7 @@ template hipError_t launch_embed_route<bf16>(const EmbedArgs&, hipStream_t);
 template <typename T> hipError_t launch_resid_norm(const ResidNormArgs& a, hipStream_t s) {
   if (a.rm.rows <= 0) return hipSuccess;
   if (a.d <= 0 || a.d % 4 != 0 || a.d > 1024 * kNormChunks) return hipErrorInvalidValue;
-#define TLF_NORM(NC) hipLaunchKernelGGL((k_resid_norm<NC>), dim3(a.rm.rows), dim3(256), 0, s, a)
+#define TLF_NORM(NC) hipLaunchKernelGGL((k_resid_norm<NC>), dim3((a.rm.rows + 3) / 4), dim3(256), 0, s, a)
   switch ((a.d + 1023) / 1024) {
     case 1: TLF_NORM(1); break;
     case 2: TLF_NORM(2); break;
