@@ -125,11 +125,15 @@ __global__ __launch_bounds__(W * 64) void k_attn_decode(AttnDecodeArgs a) {
   for (int u = blockIdx.x; u < nunits; u += gridDim.x) {
     const int k = u / H, h = u % H;
     const int b = a.perm[k];
+    // the row's first W x 64 page-table entries are read together with the
+    // cache length (they do not depend on it), the rest once it is known
+    const int32_t* pt = c.page_table + ((int64_t)b * R + i) * c.pages_per_seq;
+    const int p_first = threadIdx.x < c.pages_per_seq ? pt[threadIdx.x] : 0;
     const int L = c.cache_len[b * R + i];
     const int np = (L + kPage - 1) / kPage;
-    const int32_t* pt = c.page_table + ((int64_t)b * R + i) * c.pages_per_seq;
     __syncthreads();  // the previous unit is done with s_pages and s_red
-    for (int p = threadIdx.x; p < np; p += W * kWave) s_pages[p] = pt[p];
+    if ((int)threadIdx.x < np) s_pages[threadIdx.x] = p_first;
+    for (int p = threadIdx.x + W * kWave; p < np; p += W * kWave) s_pages[p] = pt[p];
     __syncthreads();
 
     // this wave's pages [p0, p1), a multiple of PPI pages each
