@@ -65,7 +65,7 @@ __device__ __forceinline__ int mod_row_depth(const GemmArgs& g, int r) {
 }
 
 template <typename T, int RM, int CN, int W, int KB, int AK, int EK, bool NORM, bool MOD>
-__device__ __forceinline__ void dgemm_tile(const GemmArgs& g, int nact, int act_rows, const DgemmShared& sh) {
+__device__ __forceinline__ void dgemm_tile(const GemmArgs& g, int act_rows, const DgemmShared& sh) {
   using M = Mfma<T>;
   typedef typename M::frag Frag;
   constexpr int KS = M::KS, EPL = M::EPL;
@@ -96,12 +96,15 @@ __device__ __forceinline__ void dgemm_tile(const GemmArgs& g, int nact, int act_
   const int tn = t / RT, tm = t % RT;
   const int r0 = tm * BM, n0 = tn * BN;
 
-  // Loads are issued in dependency order: the weight fragments, the
-  // epilogue's bookkeeping and residual values, then the activation
-  // fragments (after the row permutation for A_SRC).  With g.spec (every
-  // row active, e.g. the first loop) the tiles and loads do not wait for
-  // the active-row count; otherwise the count decides the tiles first, and
-  // activation rows past it are not loaded.
+  // Loads go out before any loaded value is used: the epilogue's bookkeeping
+  // and residual values and the weight fragments of the first K batch (they
+  // depend on the tile only), then the activation fragments (after the row
+  // permutation for A_SRC).  The bookkeeping is kept in registers and written
+  // to LDS after the products, so that no use of it makes a wave wait before
+  // the weights are in flight.  With g.spec (every row active, e.g. the
+  // first loop) the tiles and loads do not wait for the active-row count;
+  // otherwise the count decides the tiles first, and activation rows past it
+  // are not loaded.
   const int a_rows = act_rows;  // activation rows worth loading
   // 32-bit element offsets from uniform bases (the weight and activation
   // matrices hold fewer than 2^31 elements)
@@ -127,29 +130,61 @@ __device__ __forceinline__ void dgemm_tile(const GemmArgs& g, int nact, int act_
       wo[c] = wr * g.K + quad * EPL;
     }
   }
-  if (w == 0 && quad == 0) {
+  // the wave's K steps of batch jb (past the wave's last step the last step
+  // is reread; its product is skipped)
+  Frag bw[KB][CN];
+  auto load_weights = [&](int jb) {
 #pragma unroll
-    for (int i = 0; i < RM; ++i) {
-      const int rl = i * 16 + c16, r = min(r0 + rl, g.rm.rows - 1);
-      if constexpr (EK == E_QKV) sh.kv[rl] = g.kv.prefill ? prefill_kv_slot(g.kv, r) : g.kv.slot_base[r];
-      if constexpr (EK == E_RESID) {
-        sh.keep[rl] = !g.keep_depth || g.keep_depth[r] > g.keep_loop;
-        sh.moff[rl] = g.mod_a && r0 + rl < a_rows ? (mod_row_depth(g, r) - 1) * g.mod_ld : 0;
-      }
-      if constexpr (EK == E_LOGITS) sh.orow[rl] = g.rm.src ? g.rm.src[r] : g.out_row_off + r;
+    for (int j = 0; j < KB; ++j) {
+      const int st = min(w + W * (jb + j), S - 1);
+#pragma unroll
+      for (int c = 0; c < CN; ++c) bw[j][c] = M::load(Wb + (wo[c] + st * wstep));
     }
-  }
+  };
+  // bookkeeping of the tile's rows (lanes of quad 0 in wave 0, one row per
+  // lane and row fragment; rows past the batch read its last row) and the
+  // residual value of each output
+  const bool bk_lane = w == 0 && quad == 0;
+  int64_t bk_kv[EK == E_QKV ? RM : 1];       // cache slot offset (-1: no cache entry)
+  int bk_keep[EK == E_RESID ? RM : 1];       // depth the row is kept below (keep_depth)
+  int bk_depth[EK == E_RESID ? RM : 1];      // modulation depth
+  int bk_orow[EK == E_LOGITS ? RM : 1];      // logits row
   float xr[EK == E_RESID ? EPT : 1];
   int xrow[EK == E_RESID ? EPT : 1];  // residual row of each output (scatter: src(r))
-  if constexpr (EK == E_RESID) {
+  auto load_epilogue_values = [&]() {
+    if (bk_lane) {
 #pragma unroll
-    for (int k = 0; k < EPT; ++k) {
-      const int e = tid + k * NT, row = e / BN, n = n0 + e % BN;
-      const bool ok = e < EOUT && r0 + row < a_rows && n < g.N;
-      xrow[k] = ok && g.scatter ? row_src(g.rm, r0 + row) : r0 + row;
-      xr[k] = ok ? g.out[g.out_frag ? frag_index<T>(xrow[k], n, g.N) : (int64_t)xrow[k] * g.ldo + n] : 0.f;
+      for (int i = 0; i < RM; ++i) {
+        const int rl = i * 16 + c16, r = min(r0 + rl, g.rm.rows - 1);
+        if constexpr (EK == E_QKV) bk_kv[i] = g.kv.prefill ? prefill_kv_slot(g.kv, r) : g.kv.slot_base[r];
+        if constexpr (EK == E_RESID) {
+          bk_keep[i] = g.keep_depth ? g.keep_depth[r] : INT_MAX;
+          bk_depth[i] = g.mod_a && r0 + rl < a_rows ? mod_row_depth(g, r) : 1;
+        }
+        if constexpr (EK == E_LOGITS) bk_orow[i] = g.rm.src ? g.rm.src[r] : g.out_row_off + r;
+      }
     }
-  }
+    if constexpr (EK == E_RESID) {
+      // every output's residual value is loaded (rows past those worth
+      // loading and columns past the matrix read its last such row or
+      // column; the epilogue stores active outputs only), so no load waits on
+      // a lane's condition
+#pragma unroll
+      for (int k = 0; k < EPT; ++k) {
+        const int e = tid + k * NT, row = min(r0 + e / BN, a_rows - 1), n = min(n0 + e % BN, g.N - 1);
+        xrow[k] = g.scatter ? row_src(g.rm, row) : row;
+        xr[k] = g.out[g.out_frag ? frag_index<T>(xrow[k], n, g.N) : (int64_t)xrow[k] * g.ldo + n];
+      }
+    }
+  };
+  int nact = g.rm.rows;  // active rows, read with the first K batch
+  // the residual projections load these before their weights, the others
+  // with their first K batch (measured: each order is the faster one for
+  // its projections)
+  constexpr bool kEpilogueFirst = EK == E_RESID;
+  if constexpr (kEpilogueFirst) load_epilogue_values();
+  load_weights(0);
+
   const float* Ab = g.A;
   int ao[RM];
 #pragma unroll
@@ -168,6 +203,7 @@ __device__ __forceinline__ void dgemm_tile(const GemmArgs& g, int nact, int act_
     }
   }
 
+
   const int NJ = (S - w + W - 1) / W;  // steps of this wave (w, w + W, ...)
   f32x4 acc[RM][CN];
 #pragma unroll
@@ -181,14 +217,7 @@ __device__ __forceinline__ void dgemm_tile(const GemmArgs& g, int nact, int act_
   for (int jb = 0; jb < (S + W - 1) / W; jb += KB) {
     float av[KB][RM][EPL];
     float gv[MOD ? KB : 1][RM][EPL];
-    Frag bw[KB][CN];
-    // past this wave's last step the last step is reread (its product is skipped)
-#pragma unroll
-    for (int j = 0; j < KB; ++j) {
-      const int st = min(w + W * (jb + j), S - 1);
-#pragma unroll
-      for (int c = 0; c < CN; ++c) bw[j][c] = M::load(Wb + (wo[c] + st * wstep));
-    }
+    if (jb > 0) load_weights(jb);
 #pragma unroll
     for (int j = 0; j < KB; ++j) {
       const int stj = min(w + W * (jb + j), S - 1);
@@ -221,7 +250,11 @@ __device__ __forceinline__ void dgemm_tile(const GemmArgs& g, int nact, int act_
         }
       }
     }
-    if (jb == 0 && r0 >= nact) return;  // uniform: the tile's rows have all exited
+    if (jb == 0) {
+      if constexpr (!kEpilogueFirst) load_epilogue_values();
+      if (g.rm.nact) nact = *g.rm.nact;
+      if (r0 >= nact) return;  // uniform: the tile's rows have all exited
+    }
 #pragma unroll
     for (int j = 0; j < KB; ++j) {
       if (jb + j >= NJ) break;  // wave-uniform
@@ -266,6 +299,18 @@ __device__ __forceinline__ void dgemm_tile(const GemmArgs& g, int nact, int act_
     }
   }
 
+  if (bk_lane) {
+#pragma unroll
+    for (int i = 0; i < RM; ++i) {
+      const int rl = i * 16 + c16;
+      if constexpr (EK == E_QKV) sh.kv[rl] = bk_kv[i];
+      if constexpr (EK == E_RESID) {
+        sh.keep[rl] = bk_keep[i] > g.keep_loop;
+        sh.moff[rl] = (bk_depth[i] - 1) * g.mod_ld;
+      }
+      if constexpr (EK == E_LOGITS) sh.orow[rl] = bk_orow[i];
+    }
+  }
   // partial tiles into LDS (lane: rows 4 * quad + r of column c16); with 16
   // waves, wave w + 8 first hands its tile to wave w
   if constexpr (W > SLOTS) {
@@ -442,15 +487,14 @@ __global__ __launch_bounds__(W * 64) void k_dgemm(GemmArgs g, int wide_above) {
   __shared__ int s_keep[EK == E_RESID ? BMX : 1];
   __shared__ int s_moff[EK == E_RESID ? BMX : 1];
   const DgemmShared sh{red, s_ss, s_inv, s_orow, s_kv, s_keep, s_moff};
-  const int nact = g.rm.nact ? *g.rm.nact : g.rm.rows;
-  const int act_rows = g.spec ? g.rm.rows : min(nact, g.rm.rows);
+  const int act_rows = g.spec ? g.rm.rows : min(g.rm.nact ? *g.rm.nact : g.rm.rows, g.rm.rows);
   if constexpr (RMn != RMw || CNn != CNw) {
     if (act_rows > wide_above) {
-      dgemm_tile<T, RMw, CNw, W, KB, AK, EK, NORM, MOD>(g, nact, act_rows, sh);
+      dgemm_tile<T, RMw, CNw, W, KB, AK, EK, NORM, MOD>(g, act_rows, sh);
       return;
     }
   }
-  dgemm_tile<T, RMn, CNn, W, KB, AK, EK, NORM, MOD>(g, nact, act_rows, sh);
+  dgemm_tile<T, RMn, CNn, W, KB, AK, EK, NORM, MOD>(g, act_rows, sh);
 }
 
 template <typename T, int RMn, int CNn, int RMw, int CNw, int W, int KB, int AK, int EK, bool NORM, bool MOD>
@@ -498,7 +542,7 @@ hipError_t launch_w(const GemmArgs& a, int cus, hipStream_t s) {
 //   router hidden layer: 32 x 32 (8 waves)
 template <typename T>
 hipError_t launch_dgemm(const GemmArgs& a, AKind ak, EKind ek, bool norm, int cus, hipStream_t s) {
-  if (a.K % Mfma<T>::KS != 0 || a.rm.rows <= 0 || cus <= 0) return hipErrorInvalidValue;
+  if (a.K <= 0 || a.K % Mfma<T>::KS != 0 || a.rm.rows <= 0 || cus <= 0) return hipErrorInvalidValue;
   if (a.a_frag && (ak != A_CMP || a.a_copy)) return hipErrorInvalidValue;
   if (a.copy_frag && !a.a_copy) return hipErrorInvalidValue;
   if (a.out_frag && !((ek == E_SWIGLU && a.F % Mfma<T>::KS == 0) || (ek == E_RESID && !a.scatter)))
