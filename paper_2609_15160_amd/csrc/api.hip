@@ -20,7 +20,7 @@ int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 enum Buf {
   B_POOL, B_POS, B_PAGE_TABLE, B_CACHE_LEN, B_CHUNK_LEN, B_SEQ_LEN, B_SCALARS, B_DEPTH_HIST, B_STEP_STATS,
   B_X_DEC, B_XC_DEC, B_KVSLOT, B_DEPTH_DEC, B_PERM, B_NACT, B_Q_DEC, B_O_DEC, B_ACT_DEC, B_KEYS,
-  B_X_PRE, B_Y_PRE, B_Y16_PRE, B_DEPTH_PRE, B_TOK_IDX, B_Q_PRE, B_O_PRE, B_ACT_PRE, B_HID,
+  B_X_PRE, B_Y_PRE, B_Y16_PRE, B_DEPTH_PRE, B_TOK_IDX, B_KVSLOT_PRE, B_Q_PRE, B_O_PRE, B_ACT_PRE, B_HID,
   B_ROW_DEPTH, B_MOD, B_COND_TMP, B_WFRAG,
   B_COUNT
 };
@@ -68,6 +68,7 @@ bool make_layout(const tlf_config& c, Layout* L) {
   sz[B_Y16_PRE] = c.prefill_act_bf16 && c.dtype == TLF_DTYPE_BF16 ? P * d * 2 : 0;
   sz[B_DEPTH_PRE] = P * 4;
   sz[B_TOK_IDX] = R * P * 4;
+  sz[B_KVSLOT_PRE] = R * P * 8;
   sz[B_Q_PRE] = P * d * 4;
   sz[B_O_PRE] = P * d * 4;
   sz[B_ACT_PRE] = P * F * 4;
@@ -364,6 +365,7 @@ int run_prefill(tlf_ctx* ctx, int B, int T_, int pos0, const int32_t* tokens, fl
     pa.c = ctx->cv; pa.b0 = b0; pa.G = Gc; pa.T = T_; pa.append = append; pa.pos0 = pos0;
     pa.depth = ctx->buf<int32_t>(B_DEPTH_PRE);
     pa.tok_idx = ctx->buf<int32_t>(B_TOK_IDX);
+    pa.kv_slot = ctx->buf<int64_t>(B_KVSLOT_PRE);
     TLF_HIP(launch_plan_prefill(pa, s));
 
     for (int i = 0; i < R; ++i) {
@@ -382,7 +384,7 @@ int run_prefill(tlf_ctx* ctx, int B, int T_, int pos0, const int32_t* tokens, fl
         GemmArgs q;
         q.A = few ? x : y; q.lda = d; q.W = lw.w_qkv; q.Wf = ctx->wfrag(j, 0); q.N = 3 * d; q.K = d; q.w_rows = 3 * d; q.rm = rm;
         q.out = ctx->buf<float>(B_Q_PRE); q.ldo = d; q.d = d; q.eps = c.rms_eps; q.spec = i == 0;
-        q.kv.c = ctx->cv; q.kv.loop = i; q.kv.layer = j; q.kv.prefill = 1; q.kv.b0 = b0; q.kv.seg = T_;
+        q.kv.c = ctx->cv; q.kv.loop = i; q.kv.layer = j; q.kv.slot_base = ctx->buf<int64_t>(B_KVSLOT_PRE) + (int64_t)i * rows;
         set_mod(ctx, &q, i, j, 2, pre_depth, 1);
         q.a_single = one;
         if (one && !q.mod_g) q.A16 = y16;  // the AdaLN scale needs the float rows
@@ -517,7 +519,7 @@ int run_decode(tlf_ctx* ctx, hipStream_t s, const int32_t* tokens, float* logits
       q.A = first ? x : xc; q.lda = d; q.a_copy = first ? xc : nullptr; q.W = lw.w_qkv; q.Wf = ctx->wfrag(j, 0); q.N = 3 * d; q.K = d; q.w_rows = 3 * d; q.rm = rm;
       q.copy_frag = first && xfrag; q.a_frag = !first && xfrag;
       q.out = ctx->buf<float>(B_Q_DEC); q.ldo = d; q.d = d; q.eps = c.rms_eps;
-      q.kv.c = ctx->cv; q.kv.loop = i; q.kv.layer = j; q.kv.prefill = 0; q.kv.slot_base = kv_slot + (int64_t)i * B;
+      q.kv.c = ctx->cv; q.kv.loop = i; q.kv.layer = j; q.kv.slot_base = kv_slot + (int64_t)i * B;
       q.spec = i == 0;
       set_mod(ctx, &q, i, j, 2, pa.row_depth, 0);
       TLF_HIP(launch_dgemm<T>(q, first ? A_SRC : A_CMP, E_QKV, true, ctx->cus, s));

@@ -156,7 +156,7 @@ __device__ __forceinline__ void dgemm_tile(const GemmArgs& g, int act_rows, cons
 #pragma unroll
       for (int i = 0; i < RM; ++i) {
         const int rl = i * 16 + c16, r = min(r0 + rl, g.rm.rows - 1);
-        if constexpr (EK == E_QKV) bk_kv[i] = g.kv.prefill ? prefill_kv_slot(g.kv, r) : g.kv.slot_base[r];
+        if constexpr (EK == E_QKV) bk_kv[i] = g.kv.slot_base[r];
         if constexpr (EK == E_RESID) {
           bk_keep[i] = g.keep_depth ? g.keep_depth[r] : INT_MAX;
           bk_depth[i] = g.mod_a && r0 + rl < a_rows ? mod_row_depth(g, r) : 1;

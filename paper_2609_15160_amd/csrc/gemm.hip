@@ -222,31 +222,6 @@ __global__ __launch_bounds__(WM * 128, WM == 2 ? 2 : 1) void k_gemm(GemmArgs g) 
     }
   };
 
-  // the weight tile does not depend on which rows are active: start it first
-  load_b(0);
-
-  // thread t < BM resolves row r0 + t; the cache slot of a QKV row is looked
-  // up here and only consumed by the epilogue, so its latency hides behind K
-  int my_src = -1;
-  int64_t my_kv = -1;
-  if (tid < BM) {
-    const int r = r0 + tid;
-    if (row_active(g.rm, r)) my_src = row_src(g.rm, r);
-    row_src_s[tid] = my_src;
-    row_mod_s[tid] = (g.mod_depth && my_src >= 0)
-                         ? (g.mod_depth[g.mod_by_src ? my_src : r] - 1) * g.mod_ld : 0;
-    if constexpr (EK == E_QKV)
-      if (my_src >= 0) my_kv = prefill_kv_slot(g.kv, r);
-  }
-  if (!__syncthreads_or(my_src >= 0)) return;
-  load_a(0);
-
-  f32x4 acc[MT][NT];
-#pragma unroll
-  for (int i = 0; i < MT; ++i)
-#pragma unroll
-    for (int j = 0; j < NT; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-
   // AMODE 2: one load instruction of a wave fills 64 consecutive 16-byte
   // chunks of an LDS stage, lane l chunk l; so lane l fetches the chunk whose
   // swizzled place that is (the swizzle is an XOR, its own inverse).  A
@@ -256,12 +231,72 @@ __global__ __launch_bounds__(WM * 128, WM == 2 ? 2 : 1) void k_gemm(GemmArgs g) 
   const T* a_src[kDirect ? ACH : 1];
   const T* b_src[kDirect ? BCH : 1];
   const int wbase = __builtin_amdgcn_readfirstlane(tid & ~(kWave - 1));
+  auto issue_b = [&](int kt, int st) __attribute__((always_inline)) {
+    if constexpr (kDirect) {
+#pragma unroll
+      for (int c = 0; c < BCH; ++c)
+        load_lds16(b_src[c] + kt * BK, lds_addr(&Bs[st][(c * NTH + wbase) * CE]));
+    }
+  };
+  auto issue_a = [&](int kt, int st) __attribute__((always_inline)) {
+    if constexpr (kDirect) {
+#pragma unroll
+      for (int c = 0; c < ACH; ++c)
+        load_lds16(a_src[c] + kt * BK, lds_addr(&As[st][0][(c * NTH + wbase) * CE]));
+    }
+  };
+
+  // the weight tiles do not depend on which rows are active: they go out
+  // first (AMODE 2: those of the first NST - 1 K tiles, straight into their
+  // stages)
+  load_b(0);
   if constexpr (kDirect) {
 #pragma unroll
     for (int c = 0; c < BCH; ++c) {
       const int q = tid + c * NTH, row = q / WCR;
       b_src[c] = W + (int64_t)w_row(n0 + row) * g.K + swz<T>(row, q % WCR) * CE;
     }
+#pragma unroll
+    for (int t = 0; t < NST - 1; ++t)
+      if (t < KT) issue_b(t, t);
+  }
+
+  // thread t < BM resolves row r0 + t.  Its source row (and for QKV its
+  // cache slot, consumed by the epilogue) is loaded together with the
+  // activity test: both are in bounds for every row of the grid and are used
+  // only for active rows.
+  // The activity test of a tile that lies in one segment takes the
+  // segment's count read for the empty-tile test above (uniform, no wait).
+  int my_src = -1;
+  int64_t my_kv = -1;
+  if (tid < BM) {
+    const int r = r0 + tid, rc = min(r, g.rm.rows - 1);
+    const int src = row_src(g.rm, rc);
+    if constexpr (EK == E_QKV) my_kv = g.kv.slot_base[rc];
+    bool act;
+    if (g.rm.seg_cnt && !g.rm.nact && r0 % g.rm.seg + BM <= g.rm.seg)
+      act = r < g.rm.rows && r % g.rm.seg < g.rm.seg_cnt[(r0 / g.rm.seg) * g.rm.seg_cnt_stride];
+    else
+      act = row_active(g.rm, r);
+    my_src = act ? src : -1;
+    row_src_s[tid] = my_src;
+    row_mod_s[tid] = (g.mod_depth && my_src >= 0)
+                         ? (g.mod_depth[g.mod_by_src ? my_src : r] - 1) * g.mod_ld : 0;
+  }
+  if (!__syncthreads_or(my_src >= 0)) {
+    // the weight loads into LDS complete before the workgroup gives up its LDS
+    if constexpr (kDirect) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    return;
+  }
+  load_a(0);
+
+  f32x4 acc[MT][NT];
+#pragma unroll
+  for (int i = 0; i < MT; ++i)
+#pragma unroll
+    for (int j = 0; j < NT; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  if constexpr (kDirect) {
 #pragma unroll
     for (int c = 0; c < ACH; ++c) {
       const int q = tid + c * NTH, row = q / ACR;
@@ -270,17 +305,6 @@ __global__ __launch_bounds__(WM * 128, WM == 2 ? 2 : 1) void k_gemm(GemmArgs g) 
       a_src[c] = A16 + ar * g.lda + swz<T>(row, q % ACR) * CE;
     }
   }
-  auto issue_tile = [&](int kt, int st) __attribute__((always_inline)) {
-    if constexpr (kDirect) {
-      const int kk = kt * BK;
-#pragma unroll
-      for (int c = 0; c < BCH; ++c)
-        load_lds16(b_src[c] + kk, lds_addr(&Bs[st][(c * NTH + wbase) * CE]));
-#pragma unroll
-      for (int c = 0; c < ACH; ++c)
-        load_lds16(a_src[c] + kk, lds_addr(&As[st][0][(c * NTH + wbase) * CE]));
-    }
-  };
 
   const int frow = lane & 15, quad = lane >> 4;
   auto multiply = [&](int st) __attribute__((always_inline)) {
@@ -314,19 +338,26 @@ __global__ __launch_bounds__(WM * 128, WM == 2 ? 2 : 1) void k_gemm(GemmArgs g) 
     // for its own loads of tile kt (those of the up to NST - 2 later tiles,
     // the last LPT each, may stay in flight); after it every thread's tile kt
     // is in LDS and every wave is done reading tile kt - 1.
+    // The weight tiles of K tiles 0 and 1 went out before the rows were
+    // resolved, so the loads of tile 0 are complete once at most tile 1's A
+    // loads are outstanding; from tile 1 on, a tile is complete once at most
+    // the next tile's loads are.
     constexpr int LPT = ACH + BCH;  // loads per thread and tile
-    static_assert(NST == 3 || NST == 4, "stages");
-    static_assert(LPT * (NST - 2) < 16, "vmcnt field");
+    static_assert(NST == 3, "stages: the weight tiles of the first two go out ahead");
+    static_assert(LPT < 16, "vmcnt field");
 #pragma unroll
     for (int t = 0; t < NST - 1; ++t)
-      if (t < KT) issue_tile(t, t);
+      if (t < KT) issue_a(t, t);
     int st = 0;
     for (int kt = 0; kt < KT; ++kt) {
-      const int later = min(NST - 2, KT - 1 - kt);  // tiles after kt already issued
-      if (later >= 2) wait_loads_barrier<2 * LPT>();
-      else if (later == 1) wait_loads_barrier<LPT>();
-      else wait_loads_barrier<0>();
-      if (kt + NST - 1 < KT) issue_tile(kt + NST - 1, st == 0 ? NST - 1 : st - 1);
+      if (kt + 1 >= KT) wait_loads_barrier<0>();
+      else if (kt == 0) wait_loads_barrier<ACH>();
+      else wait_loads_barrier<LPT>();
+      if (kt + NST - 1 < KT) {
+        const int sn = st == 0 ? NST - 1 : st - 1;
+        issue_b(kt + NST - 1, sn);
+        issue_a(kt + NST - 1, sn);
+      }
       multiply(st);
       st = st == NST - 1 ? 0 : st + 1;
     }
@@ -348,7 +379,7 @@ __global__ __launch_bounds__(WM * 128, WM == 2 ? 2 : 1) void k_gemm(GemmArgs g) 
     }
   }
   if constexpr (EK == E_QKV) {
-    if (tid < BM) kv_base[tid] = my_kv;
+    if (tid < BM) kv_base[tid] = my_src >= 0 ? my_kv : -1;
     __syncthreads();
   }
   if constexpr (NORM) {

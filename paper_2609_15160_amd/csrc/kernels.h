@@ -37,26 +37,13 @@ __device__ __forceinline__ int row_src(const RowMap& m, int r) {
 struct KvDst {
   CacheView c;
   int loop = 0, layer = 0;
-  int prefill = 0;  // 0: decode, the slot comes from slot_base;
-                    // 1: prefill, b = b0 + r / seg,
-                    //    slot = cache_len[b][i] - chunk_len[b][i] + r % seg
-  int b0 = 0, seg = 0;
-  const int64_t* slot_base = nullptr;  // decode projections: the planner's slot offset of
-                                       // compact row r at this loop (kv_slot + loop * B)
+  // element offset of the cache slot that compact row r of this loop writes:
+  // its page's offset (a multiple of kPage elements) plus the slot in the
+  // low 4 bits, or -1 when the row has no cache entry.  Written by the
+  // planners (decode: kv_slot + loop * B; prefill: the loop's gathered
+  // entries), so that the projection resolves it with one independent load.
+  const int64_t* slot_base = nullptr;
 };
-
-// Element offset of the cache slot that prefill row r writes: its page's
-// offset (a multiple of kPage elements) plus the slot in the low 4 bits, or
-// -1 when the page is missing.
-__device__ __forceinline__ int64_t prefill_kv_slot(const KvDst& kv, int r) {
-  const CacheView& c = kv.c;
-  const int b = kv.b0 + r / kv.seg;
-  const int bi = b * c.R + kv.loop;
-  const int slot = c.cache_len[bi] - c.chunk_len[bi] + r % kv.seg;
-  const int page = c.page_table[(int64_t)bi * c.pages_per_seq + slot / kPage];
-  if (page < 0 || page >= c.max_pages) return -1;
-  return (int64_t)page * c.page_elems + (slot % kPage);
-}
 
 // A operand: A_SRC reads rows src(r) of a position-ordered buffer (the
 // normalised residual y, or the residual x itself when the GEMM fuses the
@@ -236,6 +223,7 @@ struct PrefillPlanArgs {
   int pos0 = 0;    // position of the first token of the call
   const int32_t* depth = nullptr;  // [G][T]
   int32_t* tok_idx = nullptr;      // [R][G*T]
+  int64_t* kv_slot = nullptr;      // [R][G*T]: cache slot offset of each gathered entry (KvDst)
 };
 hipError_t launch_plan_prefill(const PrefillPlanArgs& a, hipStream_t s);
 

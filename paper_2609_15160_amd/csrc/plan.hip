@@ -305,6 +305,15 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan_prefill(PrefillPlanArgs a
         c.pos[(int64_t)base * kPage + s] = e < n ? a.pos0 + idx[e] - g * T : -1;
       }
     }
+    // the cache slot offset of every gathered entry, for the QKV epilogue:
+    // entry e goes to slot old + e, on the partly filled last page or on new
+    // page base + (page index - p_old)
+    int64_t* ks = a.kv_slot + (int64_t)i * GT + (int64_t)g * T;
+    for (int e = tid; e < n; e += kPlanThreads) {
+      const int s = old + e, pi = s / kPage;
+      const int page = base < 0 ? -1 : pi < p_old ? pt[pi] : base + (pi - p_old);
+      ks[e] = page < 0 || page >= c.max_pages ? -1 : (int64_t)page * c.page_elems + s % kPage;
+    }
     if (tid == 0) {
       c.cache_len[bi] = old + nn;
       c.chunk_len[bi] = nn;
