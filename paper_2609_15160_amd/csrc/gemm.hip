@@ -479,27 +479,48 @@ __global__ __launch_bounds__(WM * 128, WM == 2 ? 2 : 1) void k_gemm(GemmArgs g) 
     // group's four columns (SwiGLU: four consecutive hidden units) as one
     // 16-byte access (the launcher checks that the widths allow it)
     const int t = col16 & 3;
+    if constexpr (EK == E_RESID) {
+      // The residual values of one row fragment (NT float4 per lane) are
+      // loaded together, so the epilogue waits once per fragment instead of
+      // once per 16 x 16 tile.  Inactive rows and columns past N read row 0
+      // or the last four columns (in bounds) and store nothing.  With the
+      // AdaLN gate (1 + alpha) per column, its values are loaded with them.
+      float* out = reinterpret_cast<float*>(g.out);
+      auto residual = [&](auto gate_c) __attribute__((always_inline)) {
+        constexpr bool kGate = decltype(gate_c)::value;
+#pragma unroll
+        for (int i = 0; i < MT; ++i) {
+          const int rl = wm * MT * 16 + i * 16 + quad * 4 + t;
+          const int src = row_src_s[rl];
+          const int64_t xo = (int64_t)(src < 0 ? 0 : src) * g.ldo;
+          float4 xv[NT], gv[kGate ? NT : 1];
+#pragma unroll
+          for (int j = 0; j < NT; ++j) {
+            const int nb = min(n0 + wn * NT * 16 + j * 16 + (col16 & ~3), g.N - 4);
+            xv[j] = *reinterpret_cast<const float4*>(out + xo + nb);
+            if constexpr (kGate) gv[j] = *reinterpret_cast<const float4*>(g.mod_a + row_mod_s[rl] + nb);
+          }
+#pragma unroll
+          for (int j = 0; j < NT; ++j) {
+            float v0 = acc[i][j][0], v1 = acc[i][j][1], v2 = acc[i][j][2], v3 = acc[i][j][3];
+            transpose4(v0, v1, v2, v3, t);
+            if constexpr (kGate) { v0 *= 1.f + gv[j].x; v1 *= 1.f + gv[j].y; v2 *= 1.f + gv[j].z; v3 *= 1.f + gv[j].w; }
+            const int nb = n0 + wn * NT * 16 + j * 16 + (col16 & ~3);
+            if (src >= 0 && nb < g.N)
+              *reinterpret_cast<float4*>(out + xo + nb) =
+                  make_float4(xv[j].x + v0, xv[j].y + v1, xv[j].z + v2, xv[j].w + v3);
+          }
+        }
+      };
+      if (g.mod_a) residual(std::true_type{});
+      else residual(std::false_type{});
+      return;
+    }
 #pragma unroll
     for (int i = 0; i < MT; ++i) {
       const int rl = wm * MT * 16 + i * 16 + quad * 4 + t;
       const int src = row_src_s[rl];
-      if constexpr (EK == E_RESID) {
-#pragma unroll
-        for (int j = 0; j < NT; ++j) {
-          float v0 = acc[i][j][0], v1 = acc[i][j][1], v2 = acc[i][j][2], v3 = acc[i][j][3];
-          transpose4(v0, v1, v2, v3, t);
-          const int nb = n0 + wn * NT * 16 + j * 16 + (col16 & ~3);
-          if (src < 0 || nb >= g.N) continue;
-          if (g.mod_a) {  // AdaLN gate (1 + alpha) per column
-            const float4 ga = *reinterpret_cast<const float4*>(g.mod_a + row_mod_s[rl] + nb);
-            v0 *= 1.f + ga.x; v1 *= 1.f + ga.y; v2 *= 1.f + ga.z; v3 *= 1.f + ga.w;
-          }
-          float4* px = reinterpret_cast<float4*>(reinterpret_cast<float*>(g.out) + (int64_t)src * g.ldo + nb);
-          float4 x = *px;
-          x.x += v0; x.y += v1; x.z += v2; x.w += v3;
-          *px = x;
-        }
-      } else {
+      if constexpr (EK == E_SWIGLU) {
 #pragma unroll
         for (int j = 0; j < NT; j += 2) {
           // gate columns j, up columns j + 1 of the same 16 hidden units
