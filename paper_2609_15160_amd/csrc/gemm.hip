@@ -405,51 +405,54 @@ __global__ __launch_bounds__(WM * 128, WM == 2 ? 2 : 1) void k_gemm(GemmArgs g) 
     // fragment order).  A v tile keeps the lane's column: when its four rows
     // are consecutive slots of one page from a multiple of 4 (a fresh
     // prefill), their values of that dimension are one aligned run in the V
-    // block and go out as one store; otherwise element by element.
+    // block and go out as one store; otherwise element by element.  The
+    // tile's part, head and first dimension are resolved once per tile.
     T* pool = reinterpret_cast<T*>(g.kv.c.pool);
     const int t = col16 & 3;
 #pragma unroll
-    for (int i = 0; i < MT; ++i) {
-      const int rl0 = wm * MT * 16 + i * 16 + quad * 4;
+    for (int j = 0; j < NT; ++j) {
+      // the 16-column tile's first column (wave-uniform), its part (0: q,
+      // 1: k, 2: v), head and first dimension: one division per tile
+      const int nt = n0 + wn * NT * 16 + j * 16;
+      if (nt >= g.N) continue;
+      const int part = nt < g.d ? 0 : nt < 2 * g.d ? 1 : 2;
+      const int w0 = nt - part * g.d, h = w0 / g.kv.c.D, e0 = w0 - h * g.kv.c.D;
+      const int64_t kvb = part == 2 ? v_block(g.kv.c, g.kv.layer, h) : k_block(g.kv.c, g.kv.layer, h);
 #pragma unroll
-      for (int j = 0; j < NT; ++j) {
-        const int nt = n0 + wn * NT * 16 + j * 16;  // the tile's first column (wave-uniform)
-        if (nt >= g.N) continue;
-        if (nt < g.d || (sizeof(T) == 2 && nt < 2 * g.d)) {
+      for (int i = 0; i < MT; ++i) {
+        const int rl0 = wm * MT * 16 + i * 16 + quad * 4;
+        if (part == 0 || (sizeof(T) == 2 && part == 1)) {
           float v0 = acc[i][j][0], v1 = acc[i][j][1], v2 = acc[i][j][2], v3 = acc[i][j][3];
           transpose4(v0, v1, v2, v3, t);
-          const int rl = rl0 + t, cb = nt + (col16 & ~3);
-          if (nt < g.d) {
+          const int rl = rl0 + t, cw = col16 & ~3;  // the lane's first column in the tile
+          if (part == 0) {
             if (row_src_s[rl] >= 0) {
               if (g.q16) {  // scaled and rounded to bf16 as the attention would on loading q
                 const float sc = g.q_scale;
-                *reinterpret_cast<uint2*>(g.q16 + (int64_t)(r0 + rl) * g.ldo + cb) =
+                *reinterpret_cast<uint2*>(g.q16 + (int64_t)(r0 + rl) * g.ldo + nt + cw) =
                     make_uint2(pack_bf16x2(v0 * sc, v1 * sc), pack_bf16x2(v2 * sc, v3 * sc));
               } else {
-                *reinterpret_cast<float4*>(reinterpret_cast<float*>(g.out) + (int64_t)(r0 + rl) * g.ldo + cb) =
+                *reinterpret_cast<float4*>(reinterpret_cast<float*>(g.out) + (int64_t)(r0 + rl) * g.ldo + nt + cw) =
                     make_float4(v0, v1, v2, v3);
               }
             }
           } else {
             const int64_t base = kv_base[rl];
             if (base >= 0) {
-              const int slot = (int)(base & (kPage - 1)), within = cb - g.d;
-              T* dst = pool + (base - slot) + k_block(g.kv.c, g.kv.layer, within / g.kv.c.D) +
-                       k_frag_off<T>(slot, within % g.kv.c.D);
+              const int slot = (int)(base & (kPage - 1));
+              T* dst = pool + (base - slot) + kvb + k_frag_off<T>(slot, e0 + cw);
               *reinterpret_cast<uint2*>(dst) = make_uint2(pack_bf16x2(v0, v1), pack_bf16x2(v2, v3));
             }
           }
           continue;
         }
-        const int n = nt + col16;
-        const int nn = n - g.d, kvsel = nn / g.d, within = nn % g.d;
-        const int h = within / g.kv.c.D, e = within % g.kv.c.D;
+        const int e = e0 + col16;
         const int64_t b0 = kv_base[rl0];
-        const bool run4 = kvsel == 1 && b0 >= 0 && (b0 & 3) == 0 && kv_base[rl0 + 1] == b0 + 1 &&
+        const bool run4 = part == 2 && b0 >= 0 && (b0 & 3) == 0 && kv_base[rl0 + 1] == b0 + 1 &&
                           kv_base[rl0 + 2] == b0 + 2 && kv_base[rl0 + 3] == b0 + 3;
         if (run4) {
           const int slot = (int)(b0 & (kPage - 1));
-          T* dst = pool + (b0 - slot) + v_block(g.kv.c, g.kv.layer, h) + v_frag_off(slot, e, g.kv.c.D);
+          T* dst = pool + (b0 - slot) + kvb + v_frag_off(slot, e, g.kv.c.D);
           if constexpr (sizeof(T) == 2) {
             *reinterpret_cast<uint2*>(dst) = make_uint2(pack_bf16x2(acc[i][j][0], acc[i][j][1]),
                                                         pack_bf16x2(acc[i][j][2], acc[i][j][3]));
@@ -465,10 +468,10 @@ __global__ __launch_bounds__(WM * 128, WM == 2 ? 2 : 1) void k_gemm(GemmArgs g) 
           const int slot = (int)(base & (kPage - 1));
           const int64_t page = base - slot;
           const float v = acc[i][j][r];
-          if (kvsel == 0)
-            pool[page + k_block(g.kv.c, g.kv.layer, h) + k_frag_off<T>(slot, e)] = from_f<T>(v);
+          if (part == 1)
+            pool[page + kvb + k_frag_off<T>(slot, e)] = from_f<T>(v);
           else
-            pool[page + v_block(g.kv.c, g.kv.layer, h) + v_frag_off(slot, e, g.kv.c.D)] = from_f<T>(v);
+            pool[page + kvb + v_frag_off(slot, e, g.kv.c.D)] = from_f<T>(v);
         }
       }
     }
