@@ -21,7 +21,7 @@ enum Buf {
   B_POOL, B_POS, B_PAGE_TABLE, B_CACHE_LEN, B_CHUNK_LEN, B_SEQ_LEN, B_SCALARS, B_DEPTH_HIST, B_STEP_STATS,
   B_X_DEC, B_XC_DEC, B_KVSLOT, B_DEPTH_DEC, B_PERM, B_NACT, B_Q_DEC, B_O_DEC, B_ACT_DEC, B_KEYS,
   B_X_PRE, B_Y_PRE, B_Y16_PRE, B_DEPTH_PRE, B_TOK_IDX, B_KVSLOT_PRE, B_Q_PRE, B_O_PRE, B_ACT_PRE, B_HID,
-  B_ROW_DEPTH, B_MOD, B_COND_TMP, B_WFRAG,
+  B_ROW_DEPTH, B_MOD, B_COND_TMP, B_WFRAG, B_TILES,
   B_COUNT
 };
 
@@ -79,6 +79,8 @@ bool make_layout(const tlf_config& c, Layout* L) {
   sz[B_COND_TMP] = c.adaln ? (int64_t)cond_scratch_floats((int)R, (int)d) * 4 : 0;
   // every layer's block weights in MFMA fragment order (the decode projections' copy)
   sz[B_WFRAG] = (int64_t)c.n_layers * (4 * d * d + 3 * d * F) * s;
+  // each prefill loop's active row-tile counts and lists (one-part bf16 activations)
+  sz[B_TILES] = c.prefill_act_bf16 && c.dtype == TLF_DTYPE_BF16 ? R * (3 + P / 64 + P / 128) * 4 : 0;
   size_t off = 0;
   for (int i = 0; i < B_COUNT; ++i) {
     if (sz[i] < 0) return false;
@@ -366,6 +368,16 @@ int run_prefill(tlf_ctx* ctx, int B, int T_, int pos0, const int32_t* tokens, fl
     pa.depth = ctx->buf<int32_t>(B_DEPTH_PRE);
     pa.tok_idx = ctx->buf<int32_t>(B_TOK_IDX);
     pa.kv_slot = ctx->buf<int64_t>(B_KVSLOT_PRE);
+    // the later loops' projections take smaller tiles from each loop's list
+    // of active row tiles (whole tiles per sequence: T a multiple of 256)
+    const bool tiles = one && T_ % 256 == 0 && ctx->L.size[B_TILES] > 0;
+    int32_t* tile_cnt = ctx->buf<int32_t>(B_TILES);
+    int32_t* tile_list64 = tile_cnt + 3 * R;
+    int32_t* tile_list128 = tile_list64 + (int64_t)R * (ctx->L.pre_rows / 64);
+    if (tiles) {
+      TLF_HIP(launch_fill_i32(tile_cnt, 0, 3 * R, s));
+      pa.tile_cnt = tile_cnt; pa.tile_list64 = tile_list64; pa.tile_list128 = tile_list128;
+    }
     TLF_HIP(launch_plan_prefill(pa, s));
 
     for (int i = 0; i < R; ++i) {
@@ -377,6 +389,13 @@ int run_prefill(tlf_ctx* ctx, int B, int T_, int pos0, const int32_t* tokens, fl
       rm.seg_cnt = ctx->cv.chunk_len + (int64_t)b0 * R + i;
       rm.seg = T_; rm.seg_cnt_stride = R; rm.rows = rows;
       if (few) rm.nact = rm.seg_cnt;  // one segment: rows [0, n) active
+      TileList tl;
+      if (tiles) {
+        tl.cnt = tile_cnt + 3 * i;
+        tl.list64 = tile_list64 + (int64_t)i * (rows / 64);
+        tl.list128 = tile_list128 + (int64_t)i * (rows / 128);
+        tl.cus = ctx->cus;
+      }
       ResidNormArgs rn;
       rn.rm = rm; rn.x = x; rn.y = y32 ? y : nullptr; rn.y16 = y16; rn.d = d; rn.eps = c.rms_eps;
       for (int j = 0; j < c.n_layers; ++j) {
@@ -391,7 +410,7 @@ int run_prefill(tlf_ctx* ctx, int B, int T_, int pos0, const int32_t* tokens, fl
         const float scale_log2 = 1.4426950408889634f / std::sqrt((float)c.head_dim);
         // one part: q handed on as bf16(q * scale_log2), as the attention rounds it
         bf16* q16 = one ? reinterpret_cast<bf16*>(ctx->buf<float>(B_Q_PRE)) : nullptr;
-        q.q16 = q16; q.q_scale = scale_log2;
+        q.q16 = q16; q.q_scale = scale_log2; q.tl = tl;
         if (few) TLF_HIP(launch_dgemm<T>(q, A_SRC, E_QKV, true, ctx->cus, s));
         else TLF_HIP(launch_gemm<T>(q, A_SRC, E_QKV, false, s));
 
@@ -406,7 +425,7 @@ int run_prefill(tlf_ctx* ctx, int B, int T_, int pos0, const int32_t* tokens, fl
 
         GemmArgs o;
         o.A = ctx->buf<float>(B_O_PRE); o.lda = d; o.W = lw.w_o; o.Wf = ctx->wfrag(j, 1); o.N = d; o.K = d; o.w_rows = d; o.rm = rm;
-        o.out = x; o.ldo = d; o.scatter = 1; o.spec = i == 0; o.a_single = one; o.A16 = o16;
+        o.out = x; o.ldo = d; o.scatter = 1; o.spec = i == 0; o.a_single = one; o.A16 = o16; o.tl = tl;
         set_mod(ctx, &o, i, j, 0, pre_depth, 1);
         if (few) {
           TLF_HIP(launch_dgemm<T>(o, A_CMP, E_RESID, false, ctx->cus, s));
@@ -418,7 +437,7 @@ int run_prefill(tlf_ctx* ctx, int B, int T_, int pos0, const int32_t* tokens, fl
         GemmArgs gu;
         gu.A = few ? x : y; gu.lda = d; gu.W = lw.w_gate_up; gu.Wf = ctx->wfrag(j, 2); gu.N = 2 * F; gu.K = d; gu.w_rows = 2 * F; gu.rm = rm;
         gu.out = ctx->buf<float>(B_ACT_PRE); gu.ldo = F; gu.F = F; gu.eps = c.rms_eps; gu.spec = i == 0;
-        gu.a_single = one; gu.out16 = act16;
+        gu.a_single = one; gu.out16 = act16; gu.tl = tl;
         set_mod(ctx, &gu, i, j, 3, pre_depth, 1);
         if (one && !gu.mod_g) gu.A16 = y16;
         if (few) TLF_HIP(launch_dgemm<T>(gu, A_SRC, E_SWIGLU, true, ctx->cus, s));
@@ -427,6 +446,7 @@ int run_prefill(tlf_ctx* ctx, int B, int T_, int pos0, const int32_t* tokens, fl
         GemmArgs dn;
         dn.A = ctx->buf<float>(B_ACT_PRE); dn.lda = F; dn.W = lw.w_down; dn.Wf = ctx->wfrag(j, 3); dn.N = d; dn.K = F; dn.w_rows = d;
         dn.rm = rm; dn.out = x; dn.ldo = d; dn.scatter = 1; dn.spec = i == 0; dn.a_single = one; dn.A16 = act16;
+        dn.tl = tl;
         set_mod(ctx, &dn, i, j, 1, pre_depth, 1);
         if (few) {
           TLF_HIP(launch_dgemm<T>(dn, A_CMP, E_RESID, false, ctx->cus, s));

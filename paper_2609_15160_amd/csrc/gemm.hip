@@ -99,9 +99,9 @@ template <int N> __device__ __forceinline__ void wait_loads_barrier() {
 // (AMODE 0).
 // WM: waves along M (2 or 4; two along N), each wave MT x NT MFMA tiles.
 // MT x NT: each wave's 16 x 16 MFMA tiles; BK: K elements per LDS stage.
-template <typename T, int MT, int NT, int BK, int AK, int EK, bool MOD, bool NORM, int AMODE, int WM = 2,
-          int NSTD = 3>
-__global__ __launch_bounds__(WM * 128, WM == 2 ? 2 : 1) void k_gemm(GemmArgs g) {
+template <typename T, int MT, int NT, int BK, int AK, int EK, bool MOD, bool NORM, int AMODE, int WM, int NSTD>
+__device__ __forceinline__ void gemm_tile(const GemmArgs& g, const int r0, const int n0, void* as_lds, void* bs_lds,
+                                          int* row_src_s, int* row_mod_s, float* row_inv_s, int64_t* kv_base) {
   constexpr int NTH = WM * 128;                      // threads: WM x 2 waves
   constexpr int BM = WM * MT * 16, BN = 2 * NT * 16;
   constexpr bool kBf16 = sizeof(T) == 2;             // bf16 weights: A converted to bf16 in LDS
@@ -121,16 +121,13 @@ __global__ __launch_bounds__(WM * 128, WM == 2 ? 2 : 1) void k_gemm(GemmArgs g) 
   static_assert(BCH >= 1 && BN * WCR % NTH == 0, "B tile split");
   static_assert(BK % KS == 0 && (KS * (int)sizeof(T)) % 16 == 0 || EPL == 1, "K tile");
 
-  __shared__ __align__(16) T As[NST][NA][BM * BK];
-  __shared__ __align__(16) T Bs[NST][BN * BK];
-  __shared__ int row_src_s[BM];
-  __shared__ int row_mod_s[BM];  // modulation row offset (AdaLN), 0 without
-  __shared__ float row_inv_s[NORM ? BM : 1];  // 1 / rms of each row
-  __shared__ int64_t kv_base[EK == E_QKV ? BM : 1];
+  // the workgroup's LDS: operand stages, and per tile row its source row,
+  // modulation row offset (AdaLN, 0 without), 1 / rms and cache slot
+  auto& As = *reinterpret_cast<T (*)[NST][NA][BM * BK]>(as_lds);
+  auto& Bs = *reinterpret_cast<T (*)[NST][BN * BK]>(bs_lds);
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
-  const int r0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
 
   // decode: a tile whose first row has exited is empty (rows are depth-sorted)
   if (g.rm.nact && r0 >= *g.rm.nact) return;
@@ -600,6 +597,57 @@ __global__ __launch_bounds__(WM * 128, WM == 2 ? 2 : 1) void k_gemm(GemmArgs g) 
   }
 }
 
+// One output tile per workgroup: tile (blockIdx.y, blockIdx.x).
+template <typename T, int MT, int NT, int BK, int AK, int EK, bool MOD, bool NORM, int AMODE, int WM = 2,
+          int NSTD = 3>
+__global__ __launch_bounds__(WM * 128, WM == 2 ? 2 : 1) void k_gemm(GemmArgs g) {
+  constexpr bool kDirect = sizeof(T) == 2 && AMODE == 2;
+  constexpr int NST = kDirect ? NSTD : 2, NA = sizeof(T) == 2 && AMODE == 0 ? 2 : 1;
+  constexpr int BM = WM * MT * 16, BN = 2 * NT * 16;
+  __shared__ __align__(16) T As[NST][NA][BM * BK];
+  __shared__ __align__(16) T Bs[NST][BN * BK];
+  __shared__ int row_src_s[BM];
+  __shared__ int row_mod_s[BM];
+  __shared__ float row_inv_s[NORM ? BM : 1];
+  __shared__ int64_t kv_base[EK == E_QKV ? BM : 1];
+  gemm_tile<T, MT, NT, BK, AK, EK, MOD, NORM, AMODE, WM, NSTD>(g, blockIdx.y * BM, blockIdx.x * BN, As, Bs, row_src_s,
+                                                               row_mod_s, row_inv_s, kv_base);
+}
+
+// The same with two tile shapes (bf16 A rows): when a loop's active tiles of
+// the large shape fill at most half of the workgroup slots (the later
+// loops), the workgroups take tiles of the small shape (MT2 x NT2 MFMA tiles
+// per wave) from the planner's list instead, about four times as many
+// workgroups sharing the loop's K loops.  The small shape uses the large
+// one's LDS.
+template <typename T, int MT, int NT, int MT2, int NT2, int BK, int AK, int EK, int WM, int NSTD = 3>
+__global__ __launch_bounds__(WM * 128, WM == 2 ? 2 : 1) void k_gemm_dual(GemmArgs g) {
+  constexpr int BM = WM * MT * 16, BN = 2 * NT * 16, BM2 = WM * MT2 * 16, BN2 = 2 * NT2 * 16;
+  static_assert(BM2 < BM && BN2 <= BN && (BM2 == 64 || BM2 == 128), "small shape");
+  __shared__ __align__(16) T As[NSTD][1][BM * BK];
+  __shared__ __align__(16) T Bs[NSTD][BN * BK];
+  __shared__ int row_src_s[BM];
+  __shared__ int row_mod_s[BM];
+  __shared__ float row_inv_s[1];
+  __shared__ int64_t kv_base[EK == E_QKV ? BM : 1];
+  if (g.tl.cnt) {
+    const int large = g.tl.cnt[BM == 256 ? 2 : 1] * (int)gridDim.x;  // active tiles of the large shape
+    const int slots = g.tl.cus * (WM == 2 ? 2 : 1);
+    const int tiles_n2 = (g.N + BN2 - 1) / BN2;
+    const int small = g.tl.cnt[BM2 == 64 ? 0 : 1] * tiles_n2;
+    if (2 * large <= slots && small <= (int)(gridDim.x * gridDim.y)) {
+      const int L = (int)(blockIdx.y * gridDim.x + blockIdx.x);
+      if (L >= small) return;
+      const int32_t* list = BM2 == 64 ? g.tl.list64 : g.tl.list128;
+      gemm_tile<T, MT2, NT2, BK, AK, EK, false, false, 2, WM, NSTD>(g, list[L / tiles_n2], (L % tiles_n2) * BN2, As, Bs,
+                                                                     row_src_s, row_mod_s, row_inv_s, kv_base);
+      return;
+    }
+  }
+  gemm_tile<T, MT, NT, BK, AK, EK, false, false, 2, WM, NSTD>(g, blockIdx.y * BM, blockIdx.x * BN, As, Bs, row_src_s,
+                                                              row_mod_s, row_inv_s, kv_base);
+}
+
 template <typename T, int MT, int NT>
 hipError_t launch_tiles(const GemmArgs& a, AKind ak, EKind ek, bool norm, hipStream_t s) {
   constexpr int BM = 2 * MT * 16, BN = 2 * NT * 16;
@@ -617,7 +665,12 @@ hipError_t launch_tiles(const GemmArgs& a, AKind ak, EKind ek, bool norm, hipStr
   if (ak == AKV && ek == EKV && mod == MODV && norm == NORMV) {               \
     if (amode == 0) TLF_GEMM_LAUNCH(AKV, EKV, MODV, NORMV, 0);                \
     else if (amode == 1) TLF_GEMM_LAUNCH(AKV, EKV, MODV, NORMV, 1);           \
-    else if constexpr (!MODV && !NORMV) TLF_GEMM_LAUNCH(AKV, EKV, false, false, 2); \
+    else if constexpr (!MODV && !NORMV) {                                     \
+      if constexpr (sizeof(T) == 2 && NT == 8)                                \
+        hipLaunchKernelGGL((k_gemm_dual<T, MT, NT, 2, 4, kGemmBK, AKV, EKV, 2>), grid, dim3(256), 0, s, a); \
+      else                                                                    \
+        TLF_GEMM_LAUNCH(AKV, EKV, false, false, 2);                           \
+    }                                                                         \
     return hipGetLastError();                                                 \
   }
   TLF_GEMM_CASE(A_SRC, E_QKV, false, false)
@@ -646,8 +699,7 @@ hipError_t launch_resid_wide(const GemmArgs& a, hipStream_t s) {
   if constexpr (sizeof(T) == 2) {
     constexpr int WM = 4, BM = WM * kGemmMT * 16, BN = 2 * 8 * 16;
     const dim3 grid((a.N + BN - 1) / BN, (a.rm.rows + BM - 1) / BM);
-    hipLaunchKernelGGL((k_gemm<T, kGemmMT, 8, kGemmBK, A_CMP, E_RESID, false, false, 2, WM>), grid, dim3(WM * 128),
-                       0, s, a);
+    hipLaunchKernelGGL((k_gemm_dual<T, kGemmMT, 8, 2, 4, kGemmBK, A_CMP, E_RESID, WM>), grid, dim3(WM * 128), 0, s, a);
     return hipGetLastError();
   }
   return hipErrorInvalidValue;

@@ -56,6 +56,17 @@ enum AKind { A_SRC = 0, A_CMP = 1 };
 // (the MLP router's hidden layer).
 enum EKind { E_QKV = 0, E_RESID = 1, E_SWIGLU = 3, E_LOGITS = 4, E_HIDDEN = 5 };
 
+// Active row tiles of a prefill loop, listed by the planner (sequences of a
+// multiple of 256 tokens): with few of them the many-row GEMM takes smaller
+// tiles from the list, so that more workgroups share the K loops of the
+// later loops.
+struct TileList {
+  const int32_t* cnt = nullptr;      // this loop's active row tiles: [0] of 64 rows, [1] of 128, [2] of 256
+  const int32_t* list64 = nullptr;   // first rows of the active 64-row tiles (inside one segment)
+  const int32_t* list128 = nullptr;  // first rows of the active 128-row tiles
+  int cus = 0;                       // compute units
+};
+
 struct GemmArgs {
   const float* A = nullptr; // float32 rows
   int lda = 0;
@@ -104,6 +115,7 @@ struct GemmArgs {
   bf16* out16 = nullptr;      // launch_gemm E_SWIGLU: act rows written as bf16 instead of float
   bf16* q16 = nullptr;        // launch_gemm E_QKV: q rows written as bf16(q * q_scale) instead of to out
   float q_scale = 1.f;
+  TileList tl;                // launch_gemm with A16: the loop's active tiles (tl.cnt set) for the small shape
 };
 
 // Offset of element (R, k) of a [rows][K] operand stored in MFMA fragment order.
@@ -224,6 +236,11 @@ struct PrefillPlanArgs {
   const int32_t* depth = nullptr;  // [G][T]
   int32_t* tok_idx = nullptr;      // [R][G*T]
   int64_t* kv_slot = nullptr;      // [R][G*T]: cache slot offset of each gathered entry (KvDst)
+  // optional (T a multiple of 256): each loop's active row tiles (TileList),
+  // appended per sequence; the counts start at 0
+  int32_t* tile_cnt = nullptr;     // [R][3]: tiles of 64, 128 and 256 rows
+  int32_t* tile_list64 = nullptr;  // [R][G*T / 64]
+  int32_t* tile_list128 = nullptr; // [R][G*T / 128]
 };
 hipError_t launch_plan_prefill(const PrefillPlanArgs& a, hipStream_t s);
 
