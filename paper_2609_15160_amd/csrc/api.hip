@@ -80,7 +80,7 @@ bool make_layout(const tlf_config& c, Layout* L) {
   // every layer's block weights in MFMA fragment order (the decode projections' copy)
   sz[B_WFRAG] = (int64_t)c.n_layers * (4 * d * d + 3 * d * F) * s;
   // each prefill loop's active row-tile counts and lists (one-part bf16 activations)
-  sz[B_TILES] = c.prefill_act_bf16 && c.dtype == TLF_DTYPE_BF16 ? R * (3 + P / 64 + P / 128) * 4 : 0;
+  sz[B_TILES] = c.prefill_act_bf16 && c.dtype == TLF_DTYPE_BF16 ? R * (3 + P / 64 + P / 128 + P / 256) * 4 : 0;
   size_t off = 0;
   for (int i = 0; i < B_COUNT; ++i) {
     if (sz[i] < 0) return false;
@@ -374,9 +374,11 @@ int run_prefill(tlf_ctx* ctx, int B, int T_, int pos0, const int32_t* tokens, fl
     int32_t* tile_cnt = ctx->buf<int32_t>(B_TILES);
     int32_t* tile_list64 = tile_cnt + 3 * R;
     int32_t* tile_list128 = tile_list64 + (int64_t)R * (ctx->L.pre_rows / 64);
+    int32_t* tile_list256 = tile_list128 + (int64_t)R * (ctx->L.pre_rows / 128);
     if (tiles) {
       TLF_HIP(launch_fill_i32(tile_cnt, 0, 3 * R, s));
       pa.tile_cnt = tile_cnt; pa.tile_list64 = tile_list64; pa.tile_list128 = tile_list128;
+      pa.tile_list256 = tile_list256;
     }
     TLF_HIP(launch_plan_prefill(pa, s));
 
@@ -394,6 +396,7 @@ int run_prefill(tlf_ctx* ctx, int B, int T_, int pos0, const int32_t* tokens, fl
         tl.cnt = tile_cnt + 3 * i;
         tl.list64 = tile_list64 + (int64_t)i * (rows / 64);
         tl.list128 = tile_list128 + (int64_t)i * (rows / 128);
+        tl.list256 = tile_list256 + (int64_t)i * (rows / 256);
         tl.cus = ctx->cus;
       }
       ResidNormArgs rn;

@@ -643,6 +643,14 @@ __global__ __launch_bounds__(WM * 128, WM == 2 ? 2 : 1) void k_gemm_dual(GemmArg
                                                                      row_src_s, row_mod_s, row_inv_s, kv_base);
       return;
     }
+    // the large tiles from the list too: the active ones are the grid's first
+    // workgroups, in the order of a loop with every row active
+    const int L = (int)(blockIdx.y * gridDim.x + blockIdx.x);
+    if (L >= large) return;
+    const int32_t* list = BM == 256 ? g.tl.list256 : g.tl.list128;
+    gemm_tile<T, MT, NT, BK, AK, EK, false, false, 2, WM, NSTD>(g, list[L / (int)gridDim.x], (L % (int)gridDim.x) * BN,
+                                                                As, Bs, row_src_s, row_mod_s, row_inv_s, kv_base);
+    return;
   }
   gemm_tile<T, MT, NT, BK, AK, EK, false, false, 2, WM, NSTD>(g, blockIdx.y * BM, blockIdx.x * BN, As, Bs, row_src_s,
                                                               row_mod_s, row_inv_s, kv_base);

@@ -64,6 +64,7 @@ struct TileList {
   const int32_t* cnt = nullptr;      // this loop's active row tiles: [0] of 64 rows, [1] of 128, [2] of 256
   const int32_t* list64 = nullptr;   // first rows of the active 64-row tiles (inside one segment)
   const int32_t* list128 = nullptr;  // first rows of the active 128-row tiles
+  const int32_t* list256 = nullptr;  // first rows of the active 256-row tiles
   int cus = 0;                       // compute units
 };
 
@@ -241,6 +242,7 @@ struct PrefillPlanArgs {
   int32_t* tile_cnt = nullptr;     // [R][3]: tiles of 64, 128 and 256 rows
   int32_t* tile_list64 = nullptr;  // [R][G*T / 64]
   int32_t* tile_list128 = nullptr; // [R][G*T / 128]
+  int32_t* tile_list256 = nullptr; // [R][G*T / 256]
 };
 hipError_t launch_plan_prefill(const PrefillPlanArgs& a, hipStream_t s);
 

@@ -255,7 +255,7 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan_prefill(PrefillPlanArgs a
   const int b = a.b0 + g;
   const int64_t GT = (int64_t)a.G * T;
   __shared__ int scan_tmp[kPlanThreads / kWave + 1];
-  __shared__ int s_carry, s_base, s_tiles[2];
+  __shared__ int s_carry, s_base, s_tiles[3];
   __shared__ unsigned long long hist[kMaxLoops];
   if (tid < kMaxLoops) hist[tid] = 0ull;
   __syncthreads();
@@ -320,12 +320,14 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan_prefill(PrefillPlanArgs a
       if (tid == 0) {
         s_tiles[0] = atomicAdd(&a.tile_cnt[i * 3 + 0], t64);
         s_tiles[1] = atomicAdd(&a.tile_cnt[i * 3 + 1], t128);
-        atomicAdd(&a.tile_cnt[i * 3 + 2], t256);
+        s_tiles[2] = atomicAdd(&a.tile_cnt[i * 3 + 2], t256);
       }
       __syncthreads();
       for (int k = tid; k < t64; k += kPlanThreads) a.tile_list64[(int64_t)i * (GT / 64) + s_tiles[0] + k] = g * T + k * 64;
       for (int k = tid; k < t128; k += kPlanThreads)
         a.tile_list128[(int64_t)i * (GT / 128) + s_tiles[1] + k] = g * T + k * 128;
+      for (int k = tid; k < t256; k += kPlanThreads)
+        a.tile_list256[(int64_t)i * (GT / 256) + s_tiles[2] + k] = g * T + k * 256;
     }
     if (tid == 0) {
       c.cache_len[bi] = old + nn;
@@ -379,7 +381,8 @@ hipError_t launch_plan_decode(const DecodePlanArgs& a, hipStream_t s) {
 
 hipError_t launch_plan_prefill(const PrefillPlanArgs& a, hipStream_t s) {
   if (a.G <= 0) return hipSuccess;
-  if (a.tile_cnt && (a.T % 256 != 0 || !a.tile_list64 || !a.tile_list128)) return hipErrorInvalidValue;
+  if (a.tile_cnt && (a.T % 256 != 0 || !a.tile_list64 || !a.tile_list128 || !a.tile_list256))
+    return hipErrorInvalidValue;
   hipLaunchKernelGGL(k_plan_prefill, dim3(a.G), dim3(kPlanThreads), 0, s, a);
   return hipGetLastError();
 }
