@@ -646,8 +646,21 @@ __global__ __launch_bounds__(WM * 128, WM == 2 ? 2 : 1) void k_gemm_dual(GemmArg
     // the large tiles from the list too: the active ones are the grid's first
     // workgroups, in the order of a loop with every row active
     const int L = (int)(blockIdx.y * gridDim.x + blockIdx.x);
-    if (L >= large) return;
     const int32_t* list = BM == 256 ? g.tl.list256 : g.tl.list128;
+    // a last round at most half filled: each of its large tiles as four
+    // small ones (2 x 2, rows past a segment's count leave at once)
+    const int full = large / slots * slots, tail = large - full;
+    if constexpr (BM2 * 2 == BM && BN2 * 2 == BN) {
+      if (full > 0 && 2 * tail <= slots && full + 4 * tail <= (int)(gridDim.x * gridDim.y) && L >= full) {
+        if (L >= full + 4 * tail) return;
+        const int q = (L - full) & 3, t = full + ((L - full) >> 2);
+        gemm_tile<T, MT2, NT2, BK, AK, EK, false, false, 2, WM, NSTD>(
+            g, list[t / (int)gridDim.x] + (q >> 1) * BM2, (t % (int)gridDim.x) * BN + (q & 1) * BN2, As, Bs,
+            row_src_s, row_mod_s, row_inv_s, kv_base);
+        return;
+      }
+    }
+    if (L >= large) return;
     gemm_tile<T, MT, NT, BK, AK, EK, false, false, 2, WM, NSTD>(g, list[L / (int)gridDim.x], (L % (int)gridDim.x) * BN,
                                                                 As, Bs, row_src_s, row_mod_s, row_inv_s, kv_base);
     return;
