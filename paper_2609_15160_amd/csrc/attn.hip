@@ -420,8 +420,8 @@ __global__ __launch_bounds__(kPreWaves * 64, 16 / kPreWaves) void k_attn_prefill
   static_assert((KBLK / EPC) % kWave == 0, "a wave's chunks within one page block");
   const int wu = __builtin_amdgcn_readfirstlane(w);
   auto round_page = [&](int u) { return ((wu * kWave + u * NTH) % (CH / 2)) / (KBLK / EPC); };
-  uint4 pre[CPT];
-  auto load_tile = [&](int kt) __attribute__((always_inline)) {
+  uint4 pa[CPT], pb[CPT];  // tiles in flight in registers
+  auto load_tile = [&](int kt, uint4 (&pre)[CPT]) __attribute__((always_inline)) {
     int pg[CPT];
 #pragma unroll
     for (int u = 0; u < CPT; ++u) pg[u] = pt[min(kt * 4 + round_page(u), npages - 1)];
@@ -433,7 +433,7 @@ __global__ __launch_bounds__(kPreWaves * 64, 16 / kPreWaves) void k_attn_prefill
       pre[u] = *reinterpret_cast<const uint4*>(pool + (int64_t)pg[u] * c.page_elems + (kv ? voff : koff) + off);
     }
   };
-  auto store_tile = [&](int kt, int buf) __attribute__((always_inline)) {
+  auto store_tile = [&](int kt, int buf, const uint4 (&pre)[CPT]) __attribute__((always_inline)) {
 #pragma unroll
     for (int u = 0; u < CPT; ++u) {
       const int ci = tid + u * NTH;
@@ -475,12 +475,8 @@ __global__ __launch_bounds__(kPreWaves * 64, 16 / kPreWaves) void k_attn_prefill
 #pragma unroll
   for (int qn = 0; qn < QN; ++qn) { nb[qn] = 0.f; lq[qn] = 0.f; }
 
-  load_tile(0);
-  store_tile(0, 0);
-  __syncthreads();
-  for (int kt = 0; kt < nkt; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < nkt) load_tile(kt + 1);
+  // the products of key tile kt from LDS buffer buf
+  auto use_tile = [&](int kt, int buf) __attribute__((always_inline)) {
     // the wave's queries see keys <= their compact index: skip tiles past its last query
     if (kt * BKEY <= wq0 + QW - 1) {
       const T* kb = Ks[buf];
@@ -604,8 +600,39 @@ __global__ __launch_bounds__(kPreWaves * 64, 16 / kPreWaves) void k_attn_prefill
             }
       }
     }
-    if (kt + 1 < nkt) store_tile(kt + 1, buf ^ 1);
+  };
+  if constexpr (sizeof(T) == 2) {
+    // tile kt is used from LDS while tile kt + 1 waits in registers and tile
+    // kt + 2 is being loaded, so a load has two tiles of work to arrive.
+    // Loads past the last tile reread its pages (clamped) and are never
+    // skipped, so the wait before a store counts exactly the one tile issued
+    // after it.
+    load_tile(0, pa);
+    load_tile(1, pb);
+    store_tile(0, 0, pa);
     __syncthreads();
+    for (int kt = 0; kt < nkt; kt += 2) {
+      load_tile(kt + 2, pa);
+      use_tile(kt, 0);
+      if (kt + 1 < nkt) store_tile(kt + 1, 1, pb);
+      __syncthreads();
+      if (kt + 1 < nkt) {
+        load_tile(kt + 3, pb);
+        use_tile(kt + 1, 1);
+        if (kt + 2 < nkt) store_tile(kt + 2, 0, pa);
+        __syncthreads();
+      }
+    }
+  } else {  // float32: one tile ahead (two would spill at D = 128)
+    load_tile(0, pa);
+    store_tile(0, 0, pa);
+    __syncthreads();
+    for (int kt = 0; kt < nkt; ++kt) {
+      if (kt + 1 < nkt) load_tile(kt + 1, pa);
+      use_tile(kt, kt & 1);
+      if (kt + 1 < nkt) store_tile(kt + 1, (kt & 1) ^ 1, pa);
+      __syncthreads();
+    }
   }
   // the four lane quads hold different keys: add their softmax sums, then
   // write o[query][dims 4 quad .. 4 quad + 3] of every dimension tile
