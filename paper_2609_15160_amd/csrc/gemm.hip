@@ -650,8 +650,10 @@ __global__ __launch_bounds__(WM * 128, WM == 2 ? 2 : 1) void k_gemm_dual(GemmArg
     // a last round at most half filled: each of its large tiles as four
     // small ones (2 x 2, rows past a segment's count leave at once)
     const int full = large / slots * slots, tail = large - full;
+    bool split = false;
     if constexpr (BM2 * 2 == BM && BN2 * 2 == BN) {
-      if (full > 0 && 2 * tail <= slots && full + 4 * tail <= (int)(gridDim.x * gridDim.y) && L >= full) {
+      split = full > 0 && 2 * tail <= slots && full + 4 * tail <= (int)(gridDim.x * gridDim.y);
+      if (split && L >= full) {
         if (L >= full + 4 * tail) return;
         const int q = (L - full) & 3, t = full + ((L - full) >> 2);
         gemm_tile<T, MT2, NT2, BK, AK, EK, false, false, 2, WM, NSTD>(
@@ -660,8 +662,20 @@ __global__ __launch_bounds__(WM * 128, WM == 2 ? 2 : 1) void k_gemm_dual(GemmArg
         return;
       }
     }
-    if (L >= large) return;
-    gemm_tile<T, MT, NT, BK, AK, EK, false, false, 2, WM, NSTD>(g, list[L / (int)gridDim.x], (L % (int)gridDim.x) * BN,
+    // workgroup L runs on XCD L % 8 (dispatch is round-robin over the XCDs).
+    // With at most four column tiles (the O and down projections) the n large
+    // tiles go to the XCDs as contiguous runs, so that each XCD's L2 holds a
+    // few row tiles at a time rather than a slice of every one; with more
+    // columns the plain order, which gives each XCD a subset of the weight
+    // columns, measured faster.
+    const int n = split ? full : large;
+    if (L >= n) return;
+    int t = L;
+    if (gridDim.x <= 4) {
+      const int x = L & 7, per = n >> 3, rem = n & 7;
+      t = x * per + min(x, rem) + (L >> 3);
+    }
+    gemm_tile<T, MT, NT, BK, AK, EK, false, false, 2, WM, NSTD>(g, list[t / (int)gridDim.x], (t % (int)gridDim.x) * BN,
                                                                 As, Bs, row_src_s, row_mod_s, row_inv_s, kv_base);
     return;
   }
