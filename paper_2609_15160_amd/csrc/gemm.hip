@@ -584,7 +584,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, const int r0, const
               g.argmax_keys[(int64_t)orow * g.key_groups + (n0 + wn * NT * 16 + j0 * 16) / 64] = best;
           }
         }
-      } else {  // E_HIDDEN
+      } else if constexpr (EK == E_HIDDEN) {  // the other epilogues return above
 #pragma unroll
         for (int j = 0; j < NT; ++j) {
           const int n = n0 + wn * NT * 16 + j * 16 + col16;
