@@ -684,6 +684,42 @@ def mfma_summary(counter_csv):
     return out
 
 
+def prefill_trace_summary(trace_csv, loops, layers, first=1, count=3):
+    """Per-loop kernel durations of `--prefill-only` from a rocprofv3 kernel
+    trace: prefills [first, first + count) of the trace (the one-part
+    session's timed prefills; prefill k starts at the k-th prefill planner
+    dispatch; `first` >= 1), each (loop, layer) running QKV, attention, O,
+    gate/up and down in that order; us per call averaged over the prefills
+    and layers."""
+    import csv
+    import collections
+    rows = list(csv.DictReader(open(trace_csv)))
+    rows.sort(key=lambda r: int(r["Start_Timestamp"]))
+    dur = lambda r: (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+    plans = [k for k, r in enumerate(rows) if "k_plan_prefill" in r["Kernel_Name"]]
+    names = ("qkv", "attn", "o", "gate_up", "down")
+    per = collections.defaultdict(list)
+    spans = []
+    for pf in range(first, first + count):
+        a = plans[pf]
+        b = plans[pf + 1] if pf + 1 < len(plans) else len(rows)
+        blk = [r for r in rows[a + 1:b] if "k_gemm" in r["Kernel_Name"] or "k_attn_prefill" in r["Kernel_Name"]]
+        blk = blk[:loops * layers * 5]
+        for q, r in enumerate(blk):
+            i, rem = divmod(q, layers * 5)
+            per[(i, names[rem % 5])].append(dur(r))
+        # span: from the first kernel after the previous prefill's last GEMM
+        # (its LM head) to this prefill's LM head
+        prev = max(k for k in range(plans[pf - 1], a) if "k_gemm" in rows[k]["Kernel_Name"])
+        end = max(k for k in range(a, b) if "k_gemm" in rows[k]["Kernel_Name"])
+        spans.append((int(rows[end]["End_Timestamp"]) - int(rows[prev + 1]["Start_Timestamp"])) / 1e3)
+    table = [{"loop": i + 1, **{n: sum(per[(i, n)]) / len(per[(i, n)]) for n in names if per[(i, n)]}}
+             for i in range(loops)]
+    return {"prefills": [first, first + count], "span_us": sum(spans) / len(spans),
+            "per_prefill_us": {n: layers * sum(t.get(n, 0.0) for t in table) for n in names},
+            "per_loop_us": table}
+
+
 def trace_summary(trace_csv, routed_launches, last_dispatches, loops, layers, first_step, last_step):
     """Per-kernel durations from a rocprofv3 kernel trace of this benchmark,
     the decode attention's average over the routed run's event-timed region
@@ -769,11 +805,18 @@ def main():
     ap.add_argument("--no-tiny", action="store_true", help="skip the tiny fp32 model's per-step latency")
     ap.add_argument("--mfma-summary", metavar="COUNTER_CSV",
                     help="summarize a rocprofv3 --pmc MfmaUtil MfmaFlopsBF16 run of --prefill-only and exit")
+    ap.add_argument("--prefill-trace-summary", metavar="TRACE_CSV",
+                    help="print per-loop prefill kernel durations from a rocprofv3 kernel trace of --prefill-only")
     ap.add_argument("--trace-summary", metavar="TRACE_CSV",
                     help="summarize a rocprofv3 kernel trace of this benchmark's default run and exit")
     args = ap.parse_args()
     if args.mfma_summary:
         print(json.dumps(mfma_summary(args.mfma_summary)))
+        return
+    if args.prefill_trace_summary:
+        import synth
+        m = synth.CONFIGS["bf16_d1024_prefill_b8x4096"]
+        print(json.dumps(prefill_trace_summary(args.prefill_trace_summary, m.max_loops, m.n_layers)))
         return
     if args.trace_summary:
         import synth
